@@ -1,0 +1,213 @@
+"""Pins of the oracle's network arithmetic against things other than itself:
+an independent library-layer formulation with autograd, finite differences,
+node-permutation equivariance, partition consistency with exact halos,
+exact linearity of the backward pass, a dense incidence-matrix product for the
+receiver sum, and LayerNorm's closed-form row mean."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from synth import meshes
+import torch_ref
+from cases import local_case
+
+
+def _rel(a, b):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    den = np.abs(b).max() if b.size else 0.0
+    return float(np.abs(a - b).max() / den) if den > 0 else float(np.abs(a - b).max() if a.size else 0.0)
+
+
+def _segments(shapes):
+    off = 0
+    for name, _, shape in shapes:
+        n = int(np.prod(shape))
+        yield name, slice(off, off + n)
+        off += n
+
+
+CASES = [
+    ("hex4", lambda: meshes.hex_lattice(4), 0, 8, 2, 2),
+    ("hex5_D3", lambda: meshes.hex_lattice(5), 0, 8, 2, 3),
+    ("sector_p1_K3", lambda: meshes.sector(3, 8, 4, 4, seed=2), 1, 8, 3, 3),
+    ("sector_p0_K2", lambda: meshes.sector(3, 8, 4, 4, seed=2), 0, 16, 2, 2),
+    ("delaunay", lambda: meshes.delaunay_box(5, 4, 4, seed=6), 0, 16, 1, 2),
+]
+
+
+@pytest.mark.parametrize("name,mk,p,l,K,D", CASES, ids=[c[0] for c in CASES])
+def test_matches_torch_layers(name, mk, p, l, K, D):
+    c = local_case(mk(), p, l, K, D, seed=3)
+    g = c["g"]
+    r = oracle.step(c["cfg"], g, c["params"], c["nf"], c["ef"], c["halo"], c["d_out"])
+    out, dp, dh = torch_ref.run(l, K, D, c["shapes"], g, c["params"], c["nf"], c["ef"], c["halo"], c["d_out"])
+    assert _rel(r["out"], out) < 1e-12
+    for nm, sl in _segments(c["shapes"]):
+        assert _rel(r["d_params"][sl], dp[sl]) < 1e-11, nm
+    if g["n_halo"]:
+        assert _rel(r["d_halo"], dh) < 1e-11
+        assert np.abs(dh).max() > 0
+
+
+def test_edgeless_K0_is_encoder_then_decoder():
+    """K = 0 and no edges: the network is nn.Sequential(encoder, decoder)."""
+    l, D = 16, 3
+    shapes = synth.param_shapes(l, 0, D)
+    params = synth.init_params(shapes, 5).astype(np.float64)
+    rng = np.random.default_rng(1)
+    n = 37
+    nf = rng.standard_normal((n, 11))
+    g = dict(n_owned=n, n_halo=0, n_edges=0, row_ptr=np.zeros(n + 1, np.int32), send=np.zeros(0, np.int32))
+    d_out = rng.standard_normal((n, 5))
+    r = oracle.step(oracle.ModelCfg(l, 0, D), g, params, nf, np.zeros((0, 4)), None, d_out)
+    model = torch_ref.TorchMGN(l, 0, D)
+    model.load_flat(params, shapes)
+    seq = torch.nn.Sequential(model.enc_node, model.dec)
+    out = seq(torch.as_tensor(nf))
+    out.backward(torch.as_tensor(d_out))
+    assert _rel(r["out"], out.detach().numpy()) < 1e-13
+    dp = model.flat_grad().numpy()
+    assert _rel(r["d_params"], dp) < 1e-12
+    ee = [sl for nm, sl in _segments(shapes) if nm.startswith("enc_edge")]
+    assert all(np.all(r["d_params"][sl] == 0) for sl in ee)
+
+
+@pytest.mark.parametrize("D", [2, 3])
+def test_finite_differences(D):
+    """Central differences, h = 1e-6, over every parameter and halo entry of a
+    partitioned tiny sector (l = 8, K = 2)."""
+    c = local_case(meshes.sector(3, 8, 3, 4, seed=4), 1, 8, 2, D, seed=11)
+    g, cfg = c["g"], c["cfg"]
+    assert g["n_halo"] > 0
+    d_out = c["d_out"]
+    r = oracle.step(cfg, g, c["params"], c["nf"], c["ef"], c["halo"], d_out)
+
+    def L(params, halo):
+        o = oracle.step(cfg, g, params, c["nf"], c["ef"], halo)["out"]
+        return float((o * d_out).sum())
+
+    h = 1e-6
+    P = c["params"]
+    fd = np.empty_like(P)
+    for i in range(P.size):
+        a, b = P.copy(), P.copy()
+        a[i] += h
+        b[i] -= h
+        fd[i] = (L(a, c["halo"]) - L(b, c["halo"])) / (2 * h)
+    for nm, sl in _segments(c["shapes"]):
+        assert _rel(fd[sl], r["d_params"][sl]) < 1e-6, nm
+    H = c["halo"]
+    fdh = np.empty_like(H)
+    it = np.nditer(H, flags=["multi_index"])
+    for _ in it:
+        a, b = H.copy(), H.copy()
+        a[it.multi_index] += h
+        b[it.multi_index] -= h
+        fdh[it.multi_index] = (L(P, a) - L(P, b)) / (2 * h)
+    assert _rel(fdh, r["d_halo"]) < 1e-6
+
+
+def test_permutation_equivariance():
+    m = meshes.delaunay_box(5, 5, 4, seed=9)
+    c = local_case(m, 0, 16, 2, 2, seed=4)
+    r = oracle.step(c["cfg"], c["g"], c["params"], c["nf"], c["ef"], None, c["d_out"])
+    rng = np.random.default_rng(2)
+    pi = rng.permutation(m.n_nodes).astype(np.int32)        # new id of old node i
+    inv = np.argsort(pi)
+    part = np.zeros(m.n_nodes, np.int32)
+    g2 = oracle.graph_build(pi[m.send], pi[m.recv], part, m.n_nodes, 0)
+    # local ids of the relabelled graph are the new ids; inputs follow
+    nf_full = synth.node_features(m, 4).astype(np.float64)
+    ef_full = synth.edge_features(m).astype(np.float64)
+    nf2 = nf_full[inv]
+    ef2 = ef_full[g2["eperm"]]
+    d_out_full = np.empty_like(c["d_out"])
+    d_out_full[c["g"]["l2g"]] = c["d_out"]
+    r2 = oracle.step(c["cfg"], g2, c["params"], nf2, ef2, None, d_out_full[inv])
+    out_full = np.empty_like(r["out"])
+    out_full[c["g"]["l2g"]] = r["out"]
+    assert _rel(r2["out"], out_full[inv]) < 1e-12
+    assert _rel(r2["d_params"], r["d_params"]) < 1e-11
+
+
+def test_partition_consistency():
+    """Each partition fed the unpartitioned network's halo latents reproduces
+    the unpartitioned outputs and edge latents of everything it owns."""
+    m = meshes.sector(6, 16, 10, 4, seed=7)
+    K, l, D = 3, 8, 2
+    part = oracle.partition(m.key, 4)
+    full = local_case(m, 0, l, K, D, seed=5, part=np.zeros(m.n_nodes, np.int32))
+    gu = full["g"]
+    ru = oracle.step(full["cfg"], gu, full["params"], full["nf"], full["ef"], None, None, want_v=True, want_e=True)
+    # unpartitioned local ids are the global ids (one part, ascending)
+    assert np.array_equal(gu["l2g"], np.arange(m.n_nodes))
+    u_edge_of_global = np.empty(m.n_edges, np.int64)
+    u_edge_of_global[gu["eperm"]] = np.arange(gu["n_edges"])
+    for p in range(4):
+        c = local_case(m, p, l, K, D, seed=5, part=part)
+        g = c["g"]
+        halo_ids = g["l2g"][g["n_owned"]:]
+        H = np.stack([ru["v_all"][k][halo_ids] for k in range(K)])
+        rp = oracle.step(c["cfg"], g, c["params"], c["nf"], c["ef"], H, None, want_e=True)
+        assert _rel(rp["out"], ru["out"][g["l2g"][:g["n_owned"]]]) < 1e-12
+        ue = u_edge_of_global[g["eperm"]]
+        for k in range(K + 1):
+            assert _rel(rp["e_all"][k], ru["e_all"][k][ue]) < 1e-12
+
+
+def test_backward_is_linear_in_d_out():
+    c = local_case(meshes.sector(3, 8, 4, 4, seed=2), 1, 8, 2, 3, seed=8)
+    a = oracle.step(c["cfg"], c["g"], c["params"], c["nf"], c["ef"], c["halo"], c["d_out"])
+    b = oracle.step(c["cfg"], c["g"], c["params"], c["nf"], c["ef"], c["halo"], 2.0 * c["d_out"])
+    z = oracle.step(c["cfg"], c["g"], c["params"], c["nf"], c["ef"], c["halo"], 0.0 * c["d_out"])
+    assert np.array_equal(b["d_params"], 2.0 * a["d_params"])
+    assert np.array_equal(b["d_halo"], 2.0 * a["d_halo"])
+    assert np.all(z["d_params"] == 0) and np.all(z["d_halo"] == 0)
+    assert np.array_equal(a["out"], b["out"])
+
+
+def test_scatter_sum_is_incidence_product():
+    m = meshes.delaunay_box(4, 4, 4, seed=1)
+    g = oracle.graph_build(m.send, m.recv, np.zeros(m.n_nodes, np.int32), m.n_nodes, 0)
+    rng = np.random.default_rng(3)
+    msg = rng.integers(-3, 4, (g["n_edges"], 5)).astype(np.int64)
+    R = np.zeros((g["n_edges"], g["n_owned"]), np.int64)
+    R[np.arange(g["n_edges"]), np.repeat(np.arange(g["n_owned"]), np.diff(g["row_ptr"]))] = 1
+    assert np.array_equal(oracle.scatter_sum(g["row_ptr"], msg.astype(np.float64)), (R.T @ msg).astype(np.float64))
+    # with messages = sender rows, the sum is the adjacency-count product A V
+    V = rng.integers(-3, 4, (g["n_owned"], 3)).astype(np.int64)
+    A = np.zeros((g["n_owned"], g["n_owned"]), np.int64)
+    np.add.at(A, (np.repeat(np.arange(g["n_owned"]), np.diff(g["row_ptr"])), g["send"]), 1)
+    assert np.array_equal(oracle.scatter_sum(g["row_ptr"], V[g["send"]].astype(np.float64)), (A @ V).astype(np.float64))
+
+
+def test_layernorm_row_mean_is_mean_beta():
+    """With gamma = 1 the encoder's LayerNorm rows average to mean(beta)."""
+    c = local_case(meshes.hex_lattice(4), 0, 16, 1, 2, seed=2)
+    P = c["params"].copy()
+    for nm, sl in _segments(c["shapes"]):
+        if nm == "enc_node.ln.gamma":
+            P[sl] = 1.0
+        if nm == "enc_node.ln.beta":
+            beta = P[sl]
+    r = oracle.step(c["cfg"], c["g"], P, c["nf"], c["ef"], None, None, want_v=True)
+    v0 = r["v_all"][0]
+    np.testing.assert_allclose(v0.mean(1), beta.mean(), rtol=0, atol=1e-13)
+    assert np.all(((v0 - beta) ** 2).mean(1) <= 1.0)
+
+
+def test_mse_grad_matches_autograd():
+    rng = np.random.default_rng(4)
+    out, tgt = rng.standard_normal((50, 5)), rng.standard_normal((50, 5))
+    mask = rng.integers(0, 2, 50).astype(np.uint8)
+    L, d = oracle.mse_grad(out, tgt, mask)
+    o = torch.as_tensor(out).requires_grad_(True)
+    mt = torch.as_tensor(mask.astype(bool))
+    lt = ((o - torch.as_tensor(tgt))[mt] ** 2).mean()
+    lt.backward()
+    assert abs(L - lt.item()) < 1e-14
+    assert _rel(d, o.grad.numpy()) < 1e-14
+    L0, d0 = oracle.mse_grad(out, tgt, np.zeros(50, np.uint8))
+    assert L0 == 0 and np.all(d0 == 0)
