@@ -1,0 +1,195 @@
+/*
+ * libmgn -- one MeshGraphNets training step (forward and backward) on one
+ * GPU's mesh partition, for AMD MI355X (gfx950).
+ *
+ * The network is the encode-process-decode model of the paper (section
+ * "Model"; Algorithm 1 "Training of distributed MeshGraphNets"): EncNode and
+ * EncEdge map node and edge features to latent size l, K message-passing
+ * blocks update edge and node latents, DecNode maps node latents to outputs.
+ * Readings where the paper is silent:
+ *   - every MLP has `depth` Linear layers of width l with ReLU between them
+ *     and, except the decoder, ends in an affine LayerNorm (biased variance,
+ *     epsilon ln_eps);
+ *   - block k, edge e = (s -> r):  m_e = LN(MLP([e_e | v_s | v_r])),
+ *     e_e <- e_e + m_e;  agg_r = sum of m_e over the edges into r;
+ *     v_r <- v_r + LN(MLP([v_r | agg_r]));
+ *   - the partition holds the edges whose receiver it owns (section
+ *     "Methodology": halo of depth one); halo node latents at the input of
+ *     block k come in as halo[k] (the exchange between blocks of Algorithm 1
+ *     happens outside this library).
+ *
+ * Conventions
+ *   - Every function returns an mgn_status; MGN_OK is 0.  On error nothing is
+ *     enqueued and no state changes; mgn_last_error() explains.
+ *   - Device pointers are caller-owned device memory (any allocator).  Host
+ *     pointers are plain host memory.  The library owns only the parameters
+ *     (fp32 master copy plus packed copies for the kernels).
+ *   - Work is enqueued asynchronously on the given HIP stream (a hipStream_t
+ *     passed as void*; NULL is the default stream).  Only mgn_set_params,
+ *     mgn_get_params (host side) and mgn_graph_validate synchronise.
+ *   - Sums are taken in a fixed order without atomics: results are bitwise
+ *     reproducible for the same inputs.
+ *   - Indices are int32; element offsets are 64-bit internally.
+ */
+#ifndef LIBMGN_MGN_H
+#define LIBMGN_MGN_H
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MGN_OK = 0,
+  MGN_E_ARG = 1,          /* bad argument: null/misaligned pointer, bad size */
+  MGN_E_GRAPH = 2,        /* graph arrays fail validation */
+  MGN_E_STATE = 3,        /* call out of order (e.g. backward before forward) */
+  MGN_E_NOMEM = 4,        /* device allocation failed, or workspace too small */
+  MGN_E_HIP = 5,          /* a HIP runtime call or kernel launch failed */
+  MGN_E_UNSUPPORTED = 6   /* configuration outside what the kernels handle */
+} mgn_status;
+
+typedef enum {
+  MGN_FP32 = 0,  /* fp32 storage, fp32 MFMA (v_mfma_f32_16x16x4_f32) */
+  MGN_BF16 = 1   /* bf16 MFMA inputs and bf16 edge-latent stream; fp32
+                    accumulation, LayerNorm, residual of node latents and
+                    every receiver / sender sum (mixed precision, cf. the
+                    paper's section "Performance Study") */
+} mgn_precision;
+
+typedef struct {
+  int32_t latent;    /* l: 64, 128 or 256 */
+  int32_t n_blocks;  /* K >= 0 message-passing blocks */
+  int32_t depth;     /* Linear layers per MLP: 2 or 3 */
+  int32_t node_in;   /* node features: 1..32 (11 = 3 coords + 5 flow + 3 type) */
+  int32_t edge_in;   /* edge features: 1..32 (4 = displacement + norm) */
+  int32_t node_out;  /* outputs per node: 1..16 (5) */
+  int32_t precision; /* mgn_precision */
+  float ln_eps;      /* LayerNorm epsilon, > 0 (1e-5) */
+} mgn_config;
+
+typedef struct mgn_model mgn_model;
+typedef void* mgn_stream;
+
+/* Partition-local graph (device arrays, caller-owned, int32):
+ *   row_ptr [n_owned + 1]  receiver CSR: local edges of owned receiver r are
+ *                          row_ptr[r] .. row_ptr[r+1]-1;
+ *   send    [n_edges]      local id of each local edge's sender
+ *                          (0..n_owned-1 owned, n_owned.. halo);
+ *   trow_ptr[n_owned + n_halo + 1], tedge[n_edges]  transposed CSR: the local
+ *                          edges sent by node n, ascending.
+ * mgn_graph_build produces these arrays on the host. */
+typedef struct {
+  int64_t n_owned, n_halo, n_edges;
+  const int32_t* row_ptr;
+  const int32_t* send;
+  const int32_t* trow_ptr;
+  const int32_t* tedge;
+} mgn_graph;
+
+/* Creates a model for `cfg` (host state only; the parameters' device memory
+ * is allocated on the current HIP device by the first mgn_set_params).
+ * Errors: MGN_E_ARG (null), MGN_E_UNSUPPORTED (latent/depth/dims out of
+ * range). */
+mgn_status mgn_create(const mgn_config* cfg, mgn_model** out);
+/* Frees the model's device memory; NULL is allowed. */
+void mgn_destroy(mgn_model* m);
+/* Message for the last failed call on `m`, or for the last failed call of
+ * this thread without a model when m is NULL.  Never NULL. */
+const char* mgn_last_error(const mgn_model* m);
+
+/* Number of fp32 parameters.  Flat layout, in this order: EncNode, EncEdge,
+ * then for k = 0..K-1 the edge MLP and the node MLP of block k, then DecNode.
+ * Per MLP: for each Linear W[out][in] row-major then b[out]; then LayerNorm
+ * gamma[l], beta[l] (not for DecNode).  Edge Linear-1 input columns are
+ * [e | v_sender | v_receiver], node Linear-1 input columns are [v | agg]. */
+int64_t mgn_param_count(const mgn_model* m);
+
+/* Copies parameters in (src: host or device fp32 [param_count]) and refreshes
+ * the packed copies the kernels use.  Synchronises `stream`.  MGN_E_NOMEM if
+ * the first call cannot allocate the model's device memory. */
+mgn_status mgn_set_params(mgn_model* m, const float* src, int src_on_device, mgn_stream stream);
+/* Copies the fp32 parameters out (host or device).  Synchronises `stream`. */
+mgn_status mgn_get_params(const mgn_model* m, float* dst, int dst_on_device, mgn_stream stream);
+
+/* ---- host-side graph preprocessing (section "Methodology": partition plus
+ * depth-1 halo; Algorithm 1's send/receive masks, built once per mesh) ---- */
+
+/* Slab partition standing in for METIS: nodes ranked by (key, node id); the
+ * node of rank q goes to part floor(nparts * q / n).  Host arrays. */
+mgn_status mgn_partition_slabs(const int32_t* key, int64_t n, int32_t nparts, int32_t* part);
+/* Sizes of part p's local graph from the global directed edge list (host):
+ * sizes[0] owned nodes, sizes[1] halo nodes (senders of owned-receiver edges
+ * outside p), sizes[2] local edges (receiver in p). */
+mgn_status mgn_graph_sizes(const int32_t* send, const int32_t* recv, int64_t n_edges, const int32_t* part,
+                           int64_t n_nodes, int32_t p, int64_t* sizes);
+/* Builds part p's local graph into caller-allocated host arrays: local ids
+ * are the owned nodes by ascending global id, then the halo nodes by
+ * ascending global id; local edges sorted by (receiver, sender, global edge
+ * id).  row_ptr[n_owned+1], send_local[E], eperm[E] (global id of each local
+ * edge), trow_ptr[n_owned+n_halo+1], tedge[E], l2g[n_owned+n_halo]. */
+mgn_status mgn_graph_build(const int32_t* send, const int32_t* recv, int64_t n_edges, const int32_t* part,
+                           int64_t n_nodes, int32_t p, int32_t* row_ptr, int32_t* send_local, int32_t* eperm,
+                           int32_t* trow_ptr, int32_t* tedge, int32_t* l2g);
+/* Checks a device graph (copies it to the host; synchronises `stream`) and
+ * records it as the graph mgn_forward may run on.  MGN_E_GRAPH names the
+ * first violated property. */
+mgn_status mgn_graph_validate(mgn_model* m, const mgn_graph* g, mgn_stream stream);
+
+/* ---- the training step ---- */
+
+/* Device workspace mgn_forward/mgn_backward need for graph g (bytes): every
+ * block's inputs are kept for the backward pass. */
+mgn_status mgn_workspace_size(const mgn_model* m, const mgn_graph* g, size_t* bytes);
+
+/* Forward pass (device pointers):
+ *   node_feat [n_owned][node_in], edge_feat [n_edges][edge_in] in local edge
+ *   order, halo [K][n_halo][latent] (NULL iff n_halo == 0 or K == 0; 16-byte
+ *   aligned), out [n_owned][node_out], workspace (256-byte aligned).
+ * g must be the graph last passed to mgn_graph_validate.  The pointers and
+ * their contents must stay valid and unchanged until mgn_backward. */
+mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* node_feat, const float* edge_feat,
+                       const float* halo, float* out, void* workspace, size_t ws_bytes, mgn_stream stream);
+
+/* Backward pass of the last forward: d_out [n_owned][node_out] = dL/dout.
+ * d_params [param_count] receives dL/dtheta (overwritten, or added to when
+ * accumulate != 0: gradient accumulation of Algorithm 1).  d_halo
+ * [K][n_halo][latent] (NULL allowed; 16-byte aligned) receives dL/dhalo,
+ * overwritten: the gradients the halo owners would receive (section
+ * "Methodology": backward gradient exchange). */
+mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_params, int accumulate, float* d_halo,
+                        mgn_stream stream);
+
+/* Masked mean squared error (Algorithm 1: local squared error, mean over the
+ * loss-masked nodes and outputs) and its gradient, device pointers:
+ * out, target [n][d]; mask [n] (NULL = all rows); loss [2]: loss[0] = loss,
+ * loss[1] = 2/(rows*d) (scratch); d_out [n][d]. */
+mgn_status mgn_mse_grad(const float* out, const float* target, const uint8_t* mask, int64_t n, int32_t d,
+                        float* loss, float* d_out, mgn_stream stream);
+
+/* ---- kernel timing (measurement; the paper's section "Performance Study"
+ * times its step with host-synchronised streams, this records HIP events on
+ * the stream around each launch instead) ---- */
+typedef enum {
+  MGN_T_ENCODE = 0,        /* EncNode, EncEdge forward */
+  MGN_T_EDGE_FWD = 1,      /* fused edge half of a block, forward */
+  MGN_T_NODE_FWD = 2,      /* fused node half of a block, forward */
+  MGN_T_DECODE = 3,        /* DecNode forward */
+  MGN_T_EDGE_BWD = 4,      /* fused edge half, backward with recompute */
+  MGN_T_NODE_BWD = 5,      /* node half, decoder and encoders, backward */
+  MGN_T_SENDER_GATHER = 6, /* transposed-CSR gradient gather */
+  MGN_T_WEIGHT_GRAD = 7,   /* weight-gradient GEMMs and fixed-order reductions */
+  MGN_T_OTHER = 8,         /* planning, loss */
+  MGN_T_COUNT = 9
+} mgn_timer;
+/* Starts (enable != 0) or stops recording; starting clears earlier records. */
+mgn_status mgn_timing_enable(mgn_model* m, int enable);
+/* Sum of the recorded launch durations of one timer class (milliseconds) and
+ * the number of launches.  Waits for the recorded events. */
+mgn_status mgn_timing_read(mgn_model* m, int timer, double* ms_total, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

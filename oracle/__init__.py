@@ -20,7 +20,7 @@ _lib = None
 class orc_cfg(C.Structure):
     _fields_ = [("latent", C.c_int32), ("n_blocks", C.c_int32), ("depth", C.c_int32),
                 ("node_in", C.c_int32), ("edge_in", C.c_int32), ("node_out", C.c_int32),
-                ("ln_eps", C.c_double)]
+                ("ln_eps", C.c_double), ("bf16", C.c_int32)]
 
 
 @dataclass
@@ -32,10 +32,11 @@ class ModelCfg:
     edge_in: int = 4
     node_out: int = 5
     ln_eps: float = 1e-5
+    bf16: bool = False   # mixed-precision reading: bfloat16 operands of every matrix product
 
     def c(self) -> orc_cfg:
         return orc_cfg(self.latent, self.n_blocks, self.depth, self.node_in, self.edge_in,
-                       self.node_out, self.ln_eps)
+                       self.node_out, self.ln_eps, int(self.bf16))
 
 
 def lib():

@@ -85,6 +85,30 @@ Model make_model(const orc_cfg& c) {
   return m;
 }
 
+// bfloat16 rounding as a single-precision kernel performs it: x is first a
+// binary32 value, then rounded to the nearest value with 8 significant bits
+// (ties to even): add half an ulp of the bfloat16 (minus one when the kept
+// last bit is even) to the binary32 pattern and clear the low 16 bits.
+double round_bf16(double x) {
+  const float f = (float)x;
+  if (!std::isfinite(f)) return x;
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  u &= 0xffff0000u;
+  float r;
+  std::memcpy(&r, &u, 4);
+  return (double)r;
+}
+
+// Weights as the matrix products see them (rounded copies in bf16 mode).
+struct Params {
+  const double* P;   // exact: biases, LayerNorm parameters
+  const double* W;   // weights used in products
+  bool bf16;
+  double r(double x) const { return bf16 ? round_bf16(x) : x; }
+};
+
 // ------------------------------------------------------------- one MLP row ---
 // Everything the backward pass needs from the forward pass of one row.
 struct Trace {
@@ -95,23 +119,25 @@ struct Trace {
 };
 
 // y = LN(W_D ReLU(... ReLU(W_1 x + b_1) ...) + b_D), LN only if m.ln.
-void mlp_forward(const Mlp& m, const double* P, double eps, const double* x, double* y, Trace& t) {
+void mlp_forward(const Mlp& m, const Params& Q, double eps, const double* x, double* y, Trace& t) {
+  const double* P = Q.P;
   const int D = (int)m.lin.size();
   t.a.resize(D);
   t.z.resize(D);
-  t.a[0].assign(x, x + m.in);
+  t.a[0].resize(m.in);
+  for (int i = 0; i < m.in; ++i) t.a[0][i] = Q.r(x[i]);
   for (int j = 0; j < D; ++j) {
     const Linear& L = m.lin[j];
     t.z[j].assign(L.out, 0.0);
     for (int o = 0; o < L.out; ++o) {
       double s = P[L.b + o];
-      const double* w = P + L.w + (int64_t)o * L.in;
+      const double* w = Q.W + L.w + (int64_t)o * L.in;
       for (int i = 0; i < L.in; ++i) s += w[i] * t.a[j][i];
       t.z[j][o] = s;
     }
     if (j + 1 < D) {
       t.a[j + 1].resize(L.out);
-      for (int o = 0; o < L.out; ++o) t.a[j + 1][o] = t.z[j][o] > 0 ? t.z[j][o] : 0.0;
+      for (int o = 0; o < L.out; ++o) t.a[j + 1][o] = Q.r(t.z[j][o] > 0 ? t.z[j][o] : 0.0);
     }
   }
   const std::vector<double>& last = t.z[D - 1];
@@ -137,8 +163,9 @@ void mlp_forward(const Mlp& m, const double* P, double eps, const double* x, dou
 // Reverse mode through the row traced in t: given dy = dL/dy, add the
 // parameter gradients into g (indexed like the flat vector, relative to
 // m.begin) and write dx = dL/dx.
-void mlp_backward(const Mlp& m, const double* P, const Trace& t, const double* dy, double* dx,
+void mlp_backward(const Mlp& m, const Params& Q, const Trace& t, const double* dy, double* dx,
                   double* g) {
+  const double* P = Q.P;
   const int D = (int)m.lin.size();
   const int n = m.out;
   std::vector<double> dz(dy, dy + n);
@@ -162,10 +189,10 @@ void mlp_backward(const Mlp& m, const double* P, const Trace& t, const double* d
     const Linear& L = m.lin[j];
     std::vector<double> da(L.in, 0.0);
     for (int o = 0; o < L.out; ++o) {
-      const double d = dz[o];
-      g[L.b - m.begin + o] += d;
+      g[L.b - m.begin + o] += dz[o];
+      const double d = Q.r(dz[o]);
       double* gw = g + (L.w - m.begin) + (int64_t)o * L.in;
-      const double* w = P + L.w + (int64_t)o * L.in;
+      const double* w = Q.W + L.w + (int64_t)o * L.in;
       for (int i = 0; i < L.in; ++i) {
         gw[i] += d * t.a[j][i];
         da[i] += w[i] * d;
@@ -214,7 +241,7 @@ struct Graph {
 
 // One message-passing block's edge half: m[e] and e_next[e] (section "Model":
 // each block is its own MLP applied to the previous block's output).
-void edge_messages(const Model& M, const Mlp& em, const double* P, const Graph& G, const double* v,
+void edge_messages(const Model& M, const Mlp& em, const Params& Q, const Graph& G, const double* v,
                    const double* e, double* msg, double* e_next) {
   const int l = M.c.latent;
 #pragma omp parallel for schedule(static)
@@ -227,9 +254,9 @@ void edge_messages(const Model& M, const Mlp& em, const double* P, const Graph& 
       x[l + i] = v[s * l + i];
       x[2 * l + i] = v[r * l + i];
     }
-    mlp_forward(em, P, M.c.ln_eps, x.data(), msg + ed * l, t);
+    mlp_forward(em, Q, M.c.ln_eps, x.data(), msg + ed * l, t);
     if (e_next)
-      for (int i = 0; i < l; ++i) e_next[ed * l + i] = e[ed * l + i] + msg[ed * l + i];
+      for (int i = 0; i < l; ++i) e_next[ed * l + i] = Q.r(e[ed * l + i] + msg[ed * l + i]);
   }
 }
 
@@ -237,7 +264,7 @@ void aggregate(const Graph& G, const double* msg, int l, double* agg) {
   orc_scatter_sum(G.n_owned, G.row_ptr, msg, l, agg);
 }
 
-void node_update(const Model& M, const Mlp& nm, const double* P, const Graph& G, const double* v,
+void node_update(const Model& M, const Mlp& nm, const Params& Q, const Graph& G, const double* v,
                  const double* agg, double* v_next) {
   const int l = M.c.latent;
 #pragma omp parallel for schedule(static)
@@ -248,7 +275,7 @@ void node_update(const Model& M, const Mlp& nm, const double* P, const Graph& G,
       x[i] = v[r * l + i];
       x[l + i] = agg[r * l + i];
     }
-    mlp_forward(nm, P, M.c.ln_eps, x.data(), y.data(), t);
+    mlp_forward(nm, Q, M.c.ln_eps, x.data(), y.data(), t);
     for (int i = 0; i < l; ++i) v_next[r * l + i] = v[r * l + i] + y[i];
   }
 }
@@ -386,6 +413,14 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
   for (int64_t e = 0; e < n_edges; ++e)
     if (send[e] < 0 || send[e] >= nl) return -1;
 
+  // weights as the products see them
+  std::vector<double> Wr;
+  if (c->bf16) {
+    Wr.resize(M.total);
+    for (int64_t i = 0; i < M.total; ++i) Wr[i] = round_bf16(P[i]);
+  }
+  const Params Q{P, c->bf16 ? Wr.data() : P, c->bf16 != 0};
+
   // stash of every block's inputs: v[k] (owned + halo rows), e[k]
   std::vector<std::vector<double>> V(K + 1, std::vector<double>(nl * l, 0.0));
   std::vector<std::vector<double>> E(K + 1, std::vector<double>(n_edges * l, 0.0));
@@ -394,12 +429,13 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
 #pragma omp parallel for schedule(static)
   for (int64_t r = 0; r < n_owned; ++r) {
     Trace t;
-    mlp_forward(M.enc_node, P, c->ln_eps, node_feat + r * c->node_in, V[0].data() + r * l, t);
+    mlp_forward(M.enc_node, Q, c->ln_eps, node_feat + r * c->node_in, V[0].data() + r * l, t);
   }
 #pragma omp parallel for schedule(static)
   for (int64_t e = 0; e < n_edges; ++e) {
     Trace t;
-    mlp_forward(M.enc_edge, P, c->ln_eps, edge_feat + e * c->edge_in, E[0].data() + e * l, t);
+    mlp_forward(M.enc_edge, Q, c->ln_eps, edge_feat + e * c->edge_in, E[0].data() + e * l, t);
+    for (int i = 0; i < l; ++i) E[0][e * l + i] = Q.r(E[0][e * l + i]);
   }
 
   // processor: K blocks, halo rows of each block's input from halo[k]
@@ -407,16 +443,16 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
   for (int k = 0; k < K; ++k) {
     for (int64_t h = 0; h < n_halo; ++h)
       for (int i = 0; i < l; ++i) V[k][(n_owned + h) * l + i] = halo[((int64_t)k * n_halo + h) * l + i];
-    edge_messages(M, M.edge[k], P, G, V[k].data(), E[k].data(), msg.data(), E[k + 1].data());
+    edge_messages(M, M.edge[k], Q, G, V[k].data(), E[k].data(), msg.data(), E[k + 1].data());
     aggregate(G, msg.data(), l, agg.data());
-    node_update(M, M.node[k], P, G, V[k].data(), agg.data(), V[k + 1].data());
+    node_update(M, M.node[k], Q, G, V[k].data(), agg.data(), V[k + 1].data());
   }
 
   // decoder
 #pragma omp parallel for schedule(static)
   for (int64_t r = 0; r < n_owned; ++r) {
     Trace t;
-    mlp_forward(M.dec, P, c->ln_eps, V[K].data() + r * l, out + r * c->node_out, t);
+    mlp_forward(M.dec, Q, c->ln_eps, V[K].data() + r * l, out + r * c->node_out, t);
   }
   if (v_all)
     for (int k = 0; k <= K; ++k) std::memcpy(v_all + (int64_t)k * nl * l, V[k].data(), nl * l * 8);
@@ -432,12 +468,12 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
       de_next(n_edges * l), dagg(n_owned * l), dxs(n_edges * l), dxr(n_edges * l);
   rows_with_grad(n_owned, M.dec, d_params, [&](int64_t r, Trace& t, double* g) {
     std::vector<double> y(c->node_out);
-    mlp_forward(M.dec, P, c->ln_eps, V[K].data() + r * l, y.data(), t);
-    mlp_backward(M.dec, P, t, d_out + r * c->node_out, dv.data() + r * l, g);
+    mlp_forward(M.dec, Q, c->ln_eps, V[K].data() + r * l, y.data(), t);
+    mlp_backward(M.dec, Q, t, d_out + r * c->node_out, dv.data() + r * l, g);
   });
   for (int k = K - 1; k >= 0; --k) {
     // the block's messages and aggregates again, from its stashed inputs
-    edge_messages(M, M.edge[k], P, G, V[k].data(), E[k].data(), msg.data(), nullptr);
+    edge_messages(M, M.edge[k], Q, G, V[k].data(), E[k].data(), msg.data(), nullptr);
     aggregate(G, msg.data(), l, agg.data());
     // node half: v_next = v + LN(MLP([v | agg]))
     rows_with_grad(n_owned, M.node[k], d_params, [&](int64_t r, Trace& t, double* g) {
@@ -446,8 +482,8 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
         x[i] = V[k][r * l + i];
         x[l + i] = agg[r * l + i];
       }
-      mlp_forward(M.node[k], P, c->ln_eps, x.data(), y.data(), t);
-      mlp_backward(M.node[k], P, t, dv.data() + r * l, dx.data(), g);
+      mlp_forward(M.node[k], Q, c->ln_eps, x.data(), y.data(), t);
+      mlp_backward(M.node[k], Q, t, dv.data() + r * l, dx.data(), g);
       for (int i = 0; i < l; ++i) {
         dv_next[r * l + i] = dv[r * l + i] + dx[i];
         dagg[r * l + i] = dx[l + i];
@@ -463,8 +499,8 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
         x[2 * l + i] = V[k][r * l + i];
         dm[i] = de[ed * l + i] + dagg[r * l + i];
       }
-      mlp_forward(M.edge[k], P, c->ln_eps, x.data(), y.data(), t);
-      mlp_backward(M.edge[k], P, t, dm.data(), dx.data(), g);
+      mlp_forward(M.edge[k], Q, c->ln_eps, x.data(), y.data(), t);
+      mlp_backward(M.edge[k], Q, t, dm.data(), dx.data(), g);
       for (int i = 0; i < l; ++i) {
         de_next[ed * l + i] = de[ed * l + i] + dx[i];
         dxs[ed * l + i] = dx[l + i];
@@ -488,13 +524,13 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
   // encoders
   rows_with_grad(n_owned, M.enc_node, d_params, [&](int64_t r, Trace& t, double* g) {
     std::vector<double> y(l), dx(c->node_in);
-    mlp_forward(M.enc_node, P, c->ln_eps, node_feat + r * c->node_in, y.data(), t);
-    mlp_backward(M.enc_node, P, t, dv.data() + r * l, dx.data(), g);
+    mlp_forward(M.enc_node, Q, c->ln_eps, node_feat + r * c->node_in, y.data(), t);
+    mlp_backward(M.enc_node, Q, t, dv.data() + r * l, dx.data(), g);
   });
   rows_with_grad(n_edges, M.enc_edge, d_params, [&](int64_t ed, Trace& t, double* g) {
     std::vector<double> y(l), dx(c->edge_in);
-    mlp_forward(M.enc_edge, P, c->ln_eps, edge_feat + ed * c->edge_in, y.data(), t);
-    mlp_backward(M.enc_edge, P, t, de.data() + ed * l, dx.data(), g);
+    mlp_forward(M.enc_edge, Q, c->ln_eps, edge_feat + ed * c->edge_in, y.data(), t);
+    mlp_backward(M.enc_edge, Q, t, de.data() + ed * l, dx.data(), g);
   });
   return 0;
 }

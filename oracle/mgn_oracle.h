@@ -28,9 +28,18 @@
 extern "C" {
 #endif
 
+/* bf16 != 0 selects the mixed-precision reading of the paper's automatic
+ * mixed precision (section "Performance Study"): every Linear's input
+ * activations and weights, and every backward gradient that feeds a matrix
+ * product, are rounded to bfloat16 (as binary32 values, then to nearest
+ * with 8 significant bits, ties to even) before the
+ * product; the edge-latent stream is stored rounded; biases, LayerNorm, the
+ * node-latent stream, every sum and every bias / LayerNorm gradient stay in
+ * full precision.  bf16 == 0: float64 throughout. */
 typedef struct {
   int32_t latent, n_blocks, depth, node_in, edge_in, node_out;
   double ln_eps;
+  int32_t bf16;
 } orc_cfg;
 
 /* Number of parameters in the flat layout: EncNode, EncEdge, per block

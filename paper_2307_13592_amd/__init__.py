@@ -1,0 +1,231 @@
+"""Python binding of libmgn (include/mgn.h): one MeshGraphNets training step
+on one MI355X mesh partition.
+
+The functions here carry the C ABI's names and only marshal arguments
+(torch device tensors -> device pointers, numpy arrays -> host pointers,
+status codes -> exceptions).  Every step of the computation runs in the HIP
+kernels of libmgn.so; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+from . import build as _build
+
+MGN_OK, MGN_E_ARG, MGN_E_GRAPH, MGN_E_STATE, MGN_E_NOMEM, MGN_E_HIP, MGN_E_UNSUPPORTED = range(7)
+MGN_FP32, MGN_BF16 = 0, 1
+STATUS_NAMES = ["MGN_OK", "MGN_E_ARG", "MGN_E_GRAPH", "MGN_E_STATE", "MGN_E_NOMEM", "MGN_E_HIP", "MGN_E_UNSUPPORTED"]
+
+# every symbol include/mgn.h declares
+EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mgn_set_params", "mgn_get_params",
+           "mgn_partition_slabs", "mgn_graph_sizes", "mgn_graph_build", "mgn_graph_validate", "mgn_workspace_size",
+           "mgn_forward", "mgn_backward", "mgn_mse_grad", "mgn_timing_enable", "mgn_timing_read"]
+TIMERS = ["encode", "edge_fwd", "node_fwd", "decode", "edge_bwd", "node_bwd", "sender_gather", "weight_grad",
+          "other"]
+
+
+class MgnError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        self.status = status
+        name = STATUS_NAMES[status] if 0 <= status < len(STATUS_NAMES) else str(status)
+        super().__init__(f"{name}: {msg}")
+
+
+class mgn_config(C.Structure):
+    _fields_ = [("latent", C.c_int32), ("n_blocks", C.c_int32), ("depth", C.c_int32), ("node_in", C.c_int32),
+                ("edge_in", C.c_int32), ("node_out", C.c_int32), ("precision", C.c_int32), ("ln_eps", C.c_float)]
+
+
+class mgn_graph(C.Structure):
+    _fields_ = [("n_owned", C.c_int64), ("n_halo", C.c_int64), ("n_edges", C.c_int64), ("row_ptr", C.c_void_p),
+                ("send", C.c_void_p), ("trow_ptr", C.c_void_p), ("tedge", C.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Loads libmgn.so, building it first only if no build exists."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        L = C.CDLL(_build.LIB)
+        for name in EXPORTS:
+            getattr(L, name)
+        vp, i64, i32 = C.c_void_p, C.c_int64, C.c_int32
+        sig = {
+            "mgn_create": (C.c_int, [vp, vp]),
+            "mgn_destroy": (None, [vp]),
+            "mgn_last_error": (C.c_char_p, [vp]),
+            "mgn_param_count": (i64, [vp]),
+            "mgn_set_params": (C.c_int, [vp, vp, C.c_int, vp]),
+            "mgn_get_params": (C.c_int, [vp, vp, C.c_int, vp]),
+            "mgn_partition_slabs": (C.c_int, [vp, i64, i32, vp]),
+            "mgn_graph_sizes": (C.c_int, [vp, vp, i64, vp, i64, i32, vp]),
+            "mgn_graph_build": (C.c_int, [vp, vp, i64, vp, i64, i32, vp, vp, vp, vp, vp, vp]),
+            "mgn_graph_validate": (C.c_int, [vp, vp, vp]),
+            "mgn_workspace_size": (C.c_int, [vp, vp, vp]),
+            "mgn_forward": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]),
+            "mgn_backward": (C.c_int, [vp, vp, vp, C.c_int, vp, vp]),
+            "mgn_mse_grad": (C.c_int, [vp, vp, vp, i64, i32, vp, vp, vp]),
+            "mgn_timing_enable": (C.c_int, [vp, C.c_int]),
+            "mgn_timing_read": (C.c_int, [vp, C.c_int, vp, vp]),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+# ------------------------------------------------------------ marshalling ---
+def _dev(t):
+    """Device pointer of a torch tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return C.c_void_p(t.data_ptr())
+
+
+def _host(a, dtype):
+    if a is None:
+        return None, None
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(C.c_void_p)
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    return C.c_void_p(int(stream))
+
+
+def _check(st: int, model=None):
+    if st != MGN_OK:
+        msg = lib().mgn_last_error(model).decode()
+        raise MgnError(st, msg)
+
+
+# ------------------------------------------------------------------- ABI ---
+def mgn_create(latent: int, n_blocks: int, depth: int, precision: int = MGN_FP32, node_in: int = 11,
+               edge_in: int = 4, node_out: int = 5, ln_eps: float = 1e-5) -> C.c_void_p:
+    cfg = mgn_config(latent, n_blocks, depth, node_in, edge_in, node_out, precision, ln_eps)
+    h = C.c_void_p()
+    _check(lib().mgn_create(C.byref(cfg), C.byref(h)))
+    return h
+
+
+def mgn_destroy(model) -> None:
+    lib().mgn_destroy(model)
+
+
+def mgn_last_error(model=None) -> str:
+    return lib().mgn_last_error(model).decode()
+
+
+def mgn_param_count(model) -> int:
+    return int(lib().mgn_param_count(model))
+
+
+def mgn_set_params(model, params, stream=None) -> None:
+    """params: float32 device tensor or host array of mgn_param_count entries."""
+    if hasattr(params, "is_cuda") and params.is_cuda:
+        _check(lib().mgn_set_params(model, _dev(params), 1, _stream(stream)), model)
+    else:
+        a, p = _host(params, np.float32)
+        if a.size != mgn_param_count(model):
+            raise ValueError("parameter vector has the wrong length")
+        _check(lib().mgn_set_params(model, p, 0, _stream(stream)), model)
+
+
+def mgn_get_params(model, stream=None) -> np.ndarray:
+    out = np.empty(mgn_param_count(model), np.float32)
+    _check(lib().mgn_get_params(model, out.ctypes.data_as(C.c_void_p), 0, _stream(stream)), model)
+    return out
+
+
+def mgn_partition_slabs(key, nparts: int) -> np.ndarray:
+    k, kp = _host(key, np.int32)
+    part = np.empty(k.shape[0], np.int32)
+    _check(lib().mgn_partition_slabs(kp, k.shape[0], nparts, part.ctypes.data_as(C.c_void_p)))
+    return part
+
+
+def mgn_graph_sizes(send, recv, part, n_nodes: int, p: int):
+    s, sp = _host(send, np.int32)
+    r, rp = _host(recv, np.int32)
+    pa, pp = _host(part, np.int32)
+    sz = np.zeros(3, np.int64)
+    _check(lib().mgn_graph_sizes(sp, rp, s.shape[0], pp, n_nodes, p, sz.ctypes.data_as(C.c_void_p)))
+    return tuple(int(x) for x in sz)
+
+
+def mgn_graph_build(send, recv, part, n_nodes: int, p: int) -> dict:
+    """Host-side build of part p's local graph; returns numpy arrays."""
+    no, nh, ne = mgn_graph_sizes(send, recv, part, n_nodes, p)
+    s, sp = _host(send, np.int32)
+    r, rp = _host(recv, np.int32)
+    pa, pp = _host(part, np.int32)
+    g = dict(n_owned=no, n_halo=nh, n_edges=ne, row_ptr=np.empty(no + 1, np.int32), send=np.empty(ne, np.int32),
+             eperm=np.empty(ne, np.int32), trow_ptr=np.empty(no + nh + 1, np.int32), tedge=np.empty(ne, np.int32),
+             l2g=np.empty(no + nh, np.int32))
+    ptr = lambda k: g[k].ctypes.data_as(C.c_void_p)
+    _check(lib().mgn_graph_build(sp, rp, s.shape[0], pp, n_nodes, p, ptr("row_ptr"), ptr("send"), ptr("eperm"),
+                                 ptr("trow_ptr"), ptr("tedge"), ptr("l2g")))
+    return g
+
+
+def graph_struct(dg: dict) -> mgn_graph:
+    """mgn_graph from a dict of sizes and int32 device tensors."""
+    return mgn_graph(dg["n_owned"], dg["n_halo"], dg["n_edges"], _dev(dg["row_ptr"]), _dev(dg["send"]),
+                     _dev(dg["trow_ptr"]), _dev(dg["tedge"]))
+
+
+def mgn_graph_validate(model, graph: mgn_graph, stream=None) -> None:
+    _check(lib().mgn_graph_validate(model, C.byref(graph), _stream(stream)), model)
+
+
+def mgn_workspace_size(model, graph: mgn_graph) -> int:
+    n = C.c_size_t()
+    _check(lib().mgn_workspace_size(model, C.byref(graph), C.byref(n)), model)
+    return int(n.value)
+
+
+def mgn_forward(model, graph: mgn_graph, node_feat, edge_feat, halo, out, workspace, stream=None) -> None:
+    _check(lib().mgn_forward(model, C.byref(graph), _dev(node_feat), _dev(edge_feat), _dev(halo), _dev(out),
+                             _dev(workspace), workspace.numel() * workspace.element_size(), _stream(stream)),
+           model)
+
+
+def mgn_backward(model, d_out, d_params, accumulate: bool = False, d_halo=None, stream=None) -> None:
+    _check(lib().mgn_backward(model, _dev(d_out), _dev(d_params), int(bool(accumulate)), _dev(d_halo),
+                              _stream(stream)), model)
+
+
+def mgn_mse_grad(out, target, mask, loss, d_out, stream=None) -> None:
+    n, d = out.shape
+    _check(lib().mgn_mse_grad(_dev(out), _dev(target), _dev(mask), n, d, _dev(loss), _dev(d_out),
+                              _stream(stream)))
+
+
+def mgn_timing_enable(model, enable: bool = True) -> None:
+    _check(lib().mgn_timing_enable(model, int(bool(enable))), model)
+
+
+def mgn_timing_read(model) -> dict:
+    """{timer name: (total ms, launches)} for every timer class."""
+    res = {}
+    for i, name in enumerate(TIMERS):
+        ms, n = C.c_double(), C.c_int64()
+        _check(lib().mgn_timing_read(model, i, C.byref(ms), C.byref(n)), model)
+        res[name] = (ms.value, n.value)
+    return res

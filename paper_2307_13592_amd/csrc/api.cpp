@@ -1,0 +1,806 @@
+// libmgn C ABI (include/mgn.h): model state, parameter layout and packing,
+// argument / state checks, workspace plan and the launch sequence of one
+// training step.  Device work is enqueued on the caller's stream; the only
+// synchronising calls are the parameter copies and graph validation.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "mgn_internal.h"
+
+using namespace mgn;
+
+namespace {
+
+thread_local std::string g_err;  // last error of calls without a model
+
+constexpr int BWD_GRID = 1024;   // fixed persistent grid of the backward kernels (multiple of 8)
+constexpr int FWD_EDGE_GRID = 2048;
+
+struct LinL {
+  int64_t w = 0, b = 0;  // parameter offsets
+  int in = 0, out = 0;
+  size_t pf = 0, pb = 0;  // packed offsets (uint4 units)
+  int nkgf = 0, nkgb = 0;
+};
+
+struct MlpL {
+  LinL lin[3];
+  int64_t gamma = -1, beta = -1;
+  int depth = 0;
+  int nvec = 0;  // bias + LayerNorm gradient entries: (depth-1)*l + out + (LN ? 2l : 0)
+};
+
+struct WsPlan {
+  size_t erecv, chunk, unit_r, nunits, V, AGG, ES, DV[2], DAGG, DE[2], G, DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
+      PART, VPART, total;
+  int64_t max_units;
+};
+
+}  // namespace
+
+struct mgn_model {
+  mgn_config cfg{};
+  int prec = 0, L = 0, K = 0, D = 0;
+  int kg = 16;  // k-group of the precision
+  std::vector<MlpL> mlp;  // enc_node, enc_edge, {edge_k, node_k}..., dec
+  int64_t P = 0;
+  float* params = nullptr;
+  uint4* packed = nullptr;
+  size_t packed_n = 0;
+  bool params_set = false;
+  // graph accepted by mgn_graph_validate
+  bool graph_ok = false;
+  mgn_graph vg{};
+  // what the last forward used (kept for the backward)
+  bool fwd_done = false;
+  mgn_graph g{};
+  const float *nf = nullptr, *ef = nullptr, *halo = nullptr;
+  char* ws = nullptr;
+  WsPlan plan{};
+  std::string err;
+  // launch timing
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  std::vector<std::pair<int, size_t>> ev_rec;  // (timer, index of the start event)
+
+  MlpL& enc_node() { return mlp[0]; }
+  MlpL& enc_edge() { return mlp[1]; }
+  MlpL& edge(int k) { return mlp[2 + 2 * k]; }
+  MlpL& node(int k) { return mlp[3 + 2 * k]; }
+  MlpL& dec() { return mlp.back(); }
+};
+
+namespace {
+
+mgn_status fail(mgn_model* m, mgn_status s, const std::string& msg) {
+  if (m)
+    m->err = msg;
+  else
+    g_err = msg;
+  return s;
+}
+
+mgn_status hip_fail(mgn_model* m, hipError_t e, const char* what) {
+  return fail(m, MGN_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t tsize(const mgn_model* m) { return m->prec == BF16 ? 2 : 4; }
+
+// Records a pair of events around the launches in its scope when timing is on.
+struct Timed {
+  mgn_model* m;
+  hipStream_t st;
+  size_t i0 = 0;
+  bool on;
+  hipEvent_t next() {
+    if (m->ev_used == m->ev_pool.size()) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      m->ev_pool.push_back(e);
+    }
+    return m->ev_pool[m->ev_used++];
+  }
+  Timed(mgn_model* m_, int timer, hipStream_t s) : m(m_), st(s), on(m_->timing) {
+    if (!on) return;
+    i0 = m->ev_used;
+    hipEvent_t a = next(), b = next();
+    if (!a || !b) {
+      on = false;
+      return;
+    }
+    (void)hipEventRecord(a, st);
+    m->ev_rec.push_back({timer, i0});
+  }
+  ~Timed() {
+    if (on) (void)hipEventRecord(m->ev_pool[i0 + 1], st);
+  }
+};
+
+MlpL make_mlp(mgn_model* m, int fin, int fout, bool ln, int64_t& off, size_t& poff) {
+  MlpL r;
+  r.depth = m->D;
+  int prev = fin;
+  for (int j = 0; j < m->D; ++j) {
+    LinL& L = r.lin[j];
+    L.in = prev;
+    L.out = (j == m->D - 1) ? fout : m->L;
+    L.w = off;
+    L.b = off + (int64_t)L.out * L.in;
+    off += (int64_t)L.out * L.in + L.out;
+    L.nkgf = (L.in + m->kg - 1) / m->kg;
+    L.nkgb = (L.out + m->kg - 1) / m->kg;
+    L.pf = poff;
+    poff += (size_t)((L.out + 15) / 16) * L.nkgf * 64;
+    L.pb = poff;
+    poff += (size_t)((L.in + 15) / 16) * L.nkgb * 64;
+    prev = L.out;
+  }
+  if (ln) {
+    r.gamma = off;
+    r.beta = off + fout;
+    off += 2 * (int64_t)fout;
+  }
+  r.nvec = (m->D - 1) * m->L + fout + (ln ? 2 * fout : 0);
+  return r;
+}
+
+Mlp dev_mlp(const mgn_model* m, const MlpL& l) {
+  Mlp d{};
+  d.depth = l.depth;
+  for (int j = 0; j < l.depth; ++j) {
+    const LinL& L = l.lin[j];
+    d.lin[j] = Lin{m->packed + L.pf, m->packed + L.pb, m->params + L.b, L.in, L.out, L.nkgf, L.nkgb};
+  }
+  d.gamma = l.gamma >= 0 ? m->params + l.gamma : nullptr;
+  d.beta = l.beta >= 0 ? m->params + l.beta : nullptr;
+  return d;
+}
+
+size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
+
+WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
+  WsPlan p{};
+  const int64_t no = g->n_owned, ne = g->n_edges, L = m->L, K = m->K;
+  const size_t ts = tsize(m);
+  const int te = edge_tile_rows(m->prec, m->L, m->D);
+  p.max_units = plan_max_units(no, ne, 4 * te, 4 * te);
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t r = o;
+    o += al(bytes);
+    return r;
+  };
+  p.erecv = take(4 * (size_t)ne);
+  p.chunk = take(4 * (size_t)plan_chunks(no));
+  p.unit_r = take(4 * (size_t)(p.max_units + 1));
+  p.nunits = take(4);
+  p.V = take(4 * (size_t)(K + 1) * no * L);
+  p.AGG = take(4 * (size_t)K * no * L);
+  p.ES = take(ts * (size_t)std::max<int64_t>(K, 1) * ne * L);
+  p.DV[0] = take(4 * (size_t)no * L);
+  p.DV[1] = take(4 * (size_t)no * L);
+  p.DAGG = take(4 * (size_t)no * L);
+  p.DE[0] = take(4 * (size_t)ne * L);
+  p.DE[1] = take(4 * (size_t)ne * L);
+  p.G = take(4 * (size_t)ne * L);
+  for (int j = 0; j < 3; ++j) p.DEL_E[j] = j < m->D ? take(ts * (size_t)ne * L) : 0;
+  for (int j = 0; j < 2; ++j) p.HID_E[j] = j < m->D - 1 ? take(ts * (size_t)ne * L) : 0;
+  for (int j = 0; j < 3; ++j) p.DEL_N[j] = j < m->D ? take(ts * (size_t)no * std::max<int64_t>(L, 16)) : 0;
+  for (int j = 0; j < 2; ++j) p.HID_N[j] = j < m->D - 1 ? take(ts * (size_t)no * L) : 0;
+  // split-K partials: the largest S*O*I over all weight matrices
+  size_t part = 0;
+  const size_t nm = m->mlp.size();
+  for (size_t i = 0; i < nm; ++i) {
+    const MlpL& ml = m->mlp[i];
+    // EncEdge (index 1) and the edge MLPs (even indices 2 .. nm-2) run over edges
+    const bool edge_rows = i == 1 || (i >= 2 && i + 1 < nm && i % 2 == 0);
+    const int64_t R = edge_rows ? ne : no;
+    for (int j = 0; j < ml.depth; ++j) {
+      const LinL& Ln = ml.lin[j];
+      part = std::max(part, (size_t)dw_splits(R, Ln.out, Ln.in) * Ln.out * Ln.in);
+    }
+  }
+  p.PART = take(4 * part);
+  int nvec = 0;
+  for (const MlpL& ml : m->mlp) nvec = std::max(nvec, ml.nvec);
+  p.VPART = take(4 * (size_t)BWD_GRID * nvec);
+  p.total = o;
+  return p;
+}
+
+bool same_graph(const mgn_graph& a, const mgn_graph& b) {
+  return a.n_owned == b.n_owned && a.n_halo == b.n_halo && a.n_edges == b.n_edges && a.row_ptr == b.row_ptr &&
+         a.send == b.send && a.trow_ptr == b.trow_ptr && a.tedge == b.tedge;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+mgn_status check_graph_args(mgn_model* m, const mgn_graph* g) {
+  if (!g) return fail(m, MGN_E_ARG, "graph is NULL");
+  if (g->n_owned < 0 || g->n_halo < 0 || g->n_edges < 0)
+    return fail(m, MGN_E_ARG, "graph sizes must be non-negative");
+  if (g->n_owned + g->n_halo > INT32_MAX || g->n_edges > INT32_MAX)
+    return fail(m, MGN_E_UNSUPPORTED, "graph larger than int32 indexing");
+  if (!g->row_ptr || !g->trow_ptr || (g->n_edges > 0 && (!g->send || !g->tedge)))
+    return fail(m, MGN_E_ARG, "graph array is NULL");
+  if (!aligned(g->row_ptr, 4) || !aligned(g->send, 4) || !aligned(g->trow_ptr, 4) || !aligned(g->tedge, 4))
+    return fail(m, MGN_E_ARG, "graph arrays must be 4-byte aligned");
+  return MGN_OK;
+}
+
+}  // namespace
+
+// ================================================================== ABI ===
+extern "C" {
+
+const char* mgn_last_error(const mgn_model* m) { return m ? m->err.c_str() : g_err.c_str(); }
+
+mgn_status mgn_create(const mgn_config* cfg, mgn_model** out) {
+  if (!cfg || !out) return fail(nullptr, MGN_E_ARG, "mgn_create: NULL argument");
+  *out = nullptr;
+  const mgn_config& c = *cfg;
+  if (c.latent != 64 && c.latent != 128 && c.latent != 256)
+    return fail(nullptr, MGN_E_UNSUPPORTED, "latent must be 64, 128 or 256");
+  if (c.depth != 2 && c.depth != 3) return fail(nullptr, MGN_E_UNSUPPORTED, "depth must be 2 or 3");
+  if (c.n_blocks < 0 || c.n_blocks > 1024) return fail(nullptr, MGN_E_UNSUPPORTED, "n_blocks must be 0..1024");
+  if (c.node_in < 1 || c.node_in > 32 || c.edge_in < 1 || c.edge_in > 32)
+    return fail(nullptr, MGN_E_UNSUPPORTED, "node_in and edge_in must be 1..32");
+  if (c.node_out < 1 || c.node_out > 16) return fail(nullptr, MGN_E_UNSUPPORTED, "node_out must be 1..16");
+  if (c.precision != MGN_FP32 && c.precision != MGN_BF16)
+    return fail(nullptr, MGN_E_UNSUPPORTED, "precision must be MGN_FP32 or MGN_BF16");
+  if (!(c.ln_eps > 0.f)) return fail(nullptr, MGN_E_ARG, "ln_eps must be positive");
+  mgn_model* m = new mgn_model();
+  m->cfg = c;
+  m->prec = c.precision == MGN_BF16 ? BF16 : F32;
+  m->L = c.latent;
+  m->K = c.n_blocks;
+  m->D = c.depth;
+  m->kg = m->prec == BF16 ? PBF16::KG : PF32::KG;
+  int64_t off = 0;
+  size_t poff = 0;
+  m->mlp.push_back(make_mlp(m, c.node_in, m->L, true, off, poff));
+  m->mlp.push_back(make_mlp(m, c.edge_in, m->L, true, off, poff));
+  for (int k = 0; k < m->K; ++k) {
+    m->mlp.push_back(make_mlp(m, 3 * m->L, m->L, true, off, poff));
+    m->mlp.push_back(make_mlp(m, 2 * m->L, m->L, true, off, poff));
+  }
+  m->mlp.push_back(make_mlp(m, m->L, c.node_out, false, off, poff));
+  m->P = off;
+  m->packed_n = poff;
+  *out = m;  // device memory is allocated by the first mgn_set_params
+  return MGN_OK;
+}
+
+void mgn_destroy(mgn_model* m) {
+  if (!m) return;
+  for (hipEvent_t e : m->ev_pool) (void)hipEventDestroy(e);
+  if (m->params) (void)hipFree(m->params);
+  if (m->packed) (void)hipFree(m->packed);
+  delete m;
+}
+
+int64_t mgn_param_count(const mgn_model* m) { return m ? m->P : -1; }
+
+mgn_status mgn_set_params(mgn_model* m, const float* src, int src_on_device, mgn_stream stream) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_set_params: model is NULL");
+  if (!src) return fail(m, MGN_E_ARG, "mgn_set_params: src is NULL");
+  hipStream_t st = (hipStream_t)stream;
+  if (!m->params) {
+    hipError_t a = hipMalloc(&m->params, sizeof(float) * m->P);
+    if (a == hipSuccess) a = hipMalloc(&m->packed, sizeof(uint4) * m->packed_n);
+    if (a != hipSuccess) {
+      if (m->params) (void)hipFree(m->params);
+      m->params = nullptr;
+      m->packed = nullptr;
+      return fail(m, MGN_E_NOMEM, std::string("mgn_set_params: ") + hipGetErrorString(a));
+    }
+  }
+  hipError_t e = hipMemcpyAsync(m->params, src, sizeof(float) * m->P,
+                                src_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_set_params copy");
+  for (const MlpL& ml : m->mlp)
+    for (int j = 0; j < ml.depth; ++j) {
+      const LinL& L = ml.lin[j];
+      e = launch_pack(m->prec, m->params + L.w, L.out, L.in, 0, m->packed + L.pf, L.nkgf, st);
+      if (e == hipSuccess) e = launch_pack(m->prec, m->params + L.w, L.out, L.in, 1, m->packed + L.pb, L.nkgb, st);
+      if (e != hipSuccess) return hip_fail(m, e, "mgn_set_params pack");
+    }
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_set_params sync");
+  m->params_set = true;
+  m->fwd_done = false;
+  return MGN_OK;
+}
+
+mgn_status mgn_get_params(const mgn_model* cm, float* dst, int dst_on_device, mgn_stream stream) {
+  mgn_model* m = const_cast<mgn_model*>(cm);
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_get_params: model is NULL");
+  if (!dst) return fail(m, MGN_E_ARG, "mgn_get_params: dst is NULL");
+  if (!m->params_set) return fail(m, MGN_E_STATE, "mgn_get_params: parameters were never set");
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipMemcpyAsync(dst, m->params, sizeof(float) * m->P,
+                                dst_on_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_get_params");
+  return MGN_OK;
+}
+
+mgn_status mgn_partition_slabs(const int32_t* key, int64_t n, int32_t nparts, int32_t* part) {
+  return partition_slabs(key, n, nparts, part, g_err);
+}
+
+mgn_status mgn_graph_sizes(const int32_t* send, const int32_t* recv, int64_t n_edges, const int32_t* part,
+                           int64_t n_nodes, int32_t p, int64_t* sizes) {
+  return graph_sizes(send, recv, n_edges, part, n_nodes, p, sizes, g_err);
+}
+
+mgn_status mgn_graph_build(const int32_t* send, const int32_t* recv, int64_t n_edges, const int32_t* part,
+                           int64_t n_nodes, int32_t p, int32_t* row_ptr, int32_t* send_local, int32_t* eperm,
+                           int32_t* trow_ptr, int32_t* tedge, int32_t* l2g) {
+  return graph_build(send, recv, n_edges, part, n_nodes, p, row_ptr, send_local, eperm, trow_ptr, tedge, l2g, g_err);
+}
+
+mgn_status mgn_graph_validate(mgn_model* m, const mgn_graph* g, mgn_stream stream) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_graph_validate: model is NULL");
+  mgn_status s = check_graph_args(m, g);
+  if (s) return s;
+  const int64_t no = g->n_owned, nh = g->n_halo, ne = g->n_edges, nl = no + nh;
+  std::vector<int32_t> rp(no + 1), snd(ne), tr(nl + 1), te(ne);
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = hipMemcpy(rp.data(), g->row_ptr, 4 * (no + 1), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && ne) e = hipMemcpy(snd.data(), g->send, 4 * ne, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(tr.data(), g->trow_ptr, 4 * (nl + 1), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && ne) e = hipMemcpy(te.data(), g->tedge, 4 * ne, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_graph_validate copy");
+  std::string err;
+  s = graph_check(no, nh, ne, rp.data(), snd.data(), tr.data(), te.data(), err);
+  if (s) return fail(m, s, err);
+  m->vg = *g;
+  m->graph_ok = true;
+  return MGN_OK;
+}
+
+mgn_status mgn_workspace_size(const mgn_model* cm, const mgn_graph* g, size_t* bytes) {
+  mgn_model* m = const_cast<mgn_model*>(cm);
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_workspace_size: model is NULL");
+  if (!bytes) return fail(m, MGN_E_ARG, "mgn_workspace_size: bytes is NULL");
+  mgn_status s = check_graph_args(m, g);
+  if (s) return s;
+  *bytes = make_plan(m, g).total;
+  return MGN_OK;
+}
+
+mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const float* ef, const float* halo,
+                       float* out, void* workspace, size_t ws_bytes, mgn_stream stream) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_forward: model is NULL");
+  mgn_status s = check_graph_args(m, g);
+  if (s) return s;
+  if (!m->params_set) return fail(m, MGN_E_STATE, "mgn_forward: parameters were never set");
+  if (!m->graph_ok || !same_graph(*g, m->vg))
+    return fail(m, MGN_E_STATE, "mgn_forward: graph was not validated with mgn_graph_validate");
+  const int64_t no = g->n_owned, nh = g->n_halo, ne = g->n_edges;
+  if ((no > 0 && (!nf || !out)) || (ne > 0 && !ef)) return fail(m, MGN_E_ARG, "mgn_forward: input is NULL");
+  if (nh > 0 && m->K > 0 && !halo) return fail(m, MGN_E_ARG, "mgn_forward: halo is NULL but n_halo > 0");
+  if (!aligned(nf, 4) || !aligned(ef, 4) || !aligned(out, 4) || !aligned(halo, 16))
+    return fail(m, MGN_E_ARG, "mgn_forward: misaligned pointer (features 4 bytes, halo 16 bytes)");
+  if (!workspace || !aligned(workspace, 256)) return fail(m, MGN_E_ARG, "mgn_forward: workspace NULL or not 256-byte aligned");
+  const WsPlan p = make_plan(m, g);
+  if (ws_bytes < p.total)
+    return fail(m, MGN_E_NOMEM, "mgn_forward: workspace too small (need " + std::to_string(p.total) + " bytes)");
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  const int L = m->L, K = m->K, D = m->D;
+  const size_t ts = tsize(m);
+  const int te = edge_tile_rows(m->prec, L, D);
+  auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)k * no * L; };
+  auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)k * no * L; };
+  auto ES = [&](int k) { return (void*)(ws + p.ES + ts * (size_t)k * ne * L); };
+  int32_t* erecv = (int32_t*)(ws + p.erecv);
+  int32_t* unit_r = (int32_t*)(ws + p.unit_r);
+  int32_t* n_units = (int32_t*)(ws + p.nunits);
+  hipError_t e;
+  {
+    Timed t_(m, MGN_T_OTHER, st);
+    e = launch_erecv(g->row_ptr, no, erecv, st);
+    if (e == hipSuccess)
+      e = launch_plan(g->row_ptr, no, 4 * te, 4 * te, (int32_t*)(ws + p.chunk), unit_r, n_units, st);
+  }
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_forward plan");
+
+  RowsFwdArgs ra{};
+  ra.eps = m->cfg.ln_eps;
+  // EncNode: v^0 for owned nodes
+  ra.mlp = dev_mlp(m, m->enc_node());
+  ra.rows = no;
+  ra.fin = m->cfg.node_in;
+  ra.in0 = nf;
+  ra.out = V(0);
+  {
+    Timed t_(m, MGN_T_ENCODE, st);
+    e = launch_rows_fwd(m->prec, L, D, ENC_NODE, ra, st);
+  }
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_forward EncNode");
+  if (K > 0) {
+    ra.mlp = dev_mlp(m, m->enc_edge());
+    ra.rows = ne;
+    ra.fin = m->cfg.edge_in;
+    ra.in0 = ef;
+    ra.out = ES(0);
+    {
+      Timed t_(m, MGN_T_ENCODE, st);
+      e = launch_rows_fwd(m->prec, L, D, ENC_EDGE, ra, st);
+    }
+    if (e != hipSuccess) return hip_fail(m, e, "mgn_forward EncEdge");
+  }
+  for (int k = 0; k < K; ++k) {
+    EdgeFwdArgs ea{};
+    ea.mlp = dev_mlp(m, m->edge(k));
+    ea.row_ptr = g->row_ptr;
+    ea.send = g->send;
+    ea.erecv = erecv;
+    ea.unit_r = unit_r;
+    ea.n_units = n_units;
+    ea.V = V(k);
+    ea.H = nh > 0 ? halo + (size_t)k * nh * L : nullptr;
+    ea.n_owned = no;
+    ea.Ein = ES(k);
+    ea.Eout = k + 1 < K ? ES(k + 1) : nullptr;
+    ea.agg = AGG(k);
+    ea.eps = m->cfg.ln_eps;
+    if (no > 0) {
+      Timed t_(m, MGN_T_EDGE_FWD, st);
+      e = launch_edge_fwd(m->prec, L, D, ea, FWD_EDGE_GRID, st);
+      if (e != hipSuccess) return hip_fail(m, e, "mgn_forward edge block");
+    }
+    RowsFwdArgs na{};
+    na.mlp = dev_mlp(m, m->node(k));
+    na.rows = no;
+    na.in0 = V(k);
+    na.in1 = AGG(k);
+    na.out = V(k + 1);
+    na.eps = m->cfg.ln_eps;
+    {
+      Timed t_(m, MGN_T_NODE_FWD, st);
+      e = launch_rows_fwd(m->prec, L, D, NODE_BLOCK, na, st);
+    }
+    if (e != hipSuccess) return hip_fail(m, e, "mgn_forward node block");
+  }
+  RowsFwdArgs da{};
+  da.mlp = dev_mlp(m, m->dec());
+  da.rows = no;
+  da.in0 = V(K);
+  da.out = out;
+  da.fout = m->cfg.node_out;
+  da.eps = m->cfg.ln_eps;
+  {
+    Timed t_(m, MGN_T_DECODE, st);
+    e = launch_rows_fwd(m->prec, L, D, DECODER, da, st);
+  }
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_forward DecNode");
+  m->fwd_done = true;
+  m->g = *g;
+  m->nf = nf;
+  m->ef = ef;
+  m->halo = halo;
+  m->ws = ws;
+  m->plan = p;
+  return MGN_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Weight gradient of Linear j of an MLP: split-K GEMM into the partial
+// buffer, then the fixed-order reduction into d_params.
+hipError_t run_dw(mgn_model* m, const LinL& L, DwArgs a, float* d_params, int accumulate, hipStream_t st) {
+  a.O = L.out;
+  a.I = L.in;
+  a.S = dw_splits(a.R, a.O, a.I);
+  a.part = (float*)(m->ws + m->plan.PART);
+  a.L = m->L;
+  if (a.R == 0) {
+    // no rows: the gradient is zero
+    if (!accumulate) return launch_zero(d_params + L.w, (int64_t)L.out * L.in, st);
+    return hipSuccess;
+  }
+  Timed t_(m, MGN_T_WEIGHT_GRAD, st);
+  hipError_t e = launch_dw(m->prec, a, st);
+  if (e == hipSuccess) e = launch_dw_reduce(a.part, a.S, a.O, a.I, d_params + L.w, accumulate, st);
+  return e;
+}
+
+hipError_t run_vec(mgn_model* m, const MlpL& ml, float* d_params, int accumulate, hipStream_t st) {
+  VecSeg segs[4];
+  int n = 0, off = 0;
+  for (int j = 0; j < ml.depth; ++j) {
+    segs[n++] = VecSeg{off, ml.lin[j].b, ml.lin[j].out};
+    off += (j + 1 < ml.depth) ? m->L : ml.lin[j].out;
+  }
+  if (ml.gamma >= 0) segs[n++] = VecSeg{off, ml.gamma, 2 * ml.lin[ml.depth - 1].out};
+  Timed t_(m, MGN_T_WEIGHT_GRAD, st);
+  return launch_vec_reduce((float*)(m->ws + m->plan.VPART), BWD_GRID, ml.nvec, segs, n, d_params, accumulate, st);
+}
+
+}  // namespace
+
+extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_params, int accumulate, float* d_halo,
+                                   mgn_stream stream) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_backward: model is NULL");
+  if (!m->fwd_done) return fail(m, MGN_E_STATE, "mgn_backward: no forward pass to differentiate");
+  if (!m->graph_ok || !same_graph(m->g, m->vg))
+    return fail(m, MGN_E_STATE, "mgn_backward: the graph changed since the forward pass");
+  if (!d_params || (m->g.n_owned > 0 && !d_out)) return fail(m, MGN_E_ARG, "mgn_backward: NULL argument");
+  if (!aligned(d_out, 4) || !aligned(d_params, 4) || !aligned(d_halo, 16))
+    return fail(m, MGN_E_ARG, "mgn_backward: misaligned pointer (d_halo 16 bytes)");
+  hipStream_t st = (hipStream_t)stream;
+  const WsPlan& p = m->plan;
+  char* ws = m->ws;
+  const mgn_graph* g = &m->g;
+  const int64_t no = g->n_owned, nh = g->n_halo, ne = g->n_edges;
+  const int L = m->L, K = m->K, D = m->D;
+  const size_t ts = tsize(m);
+  auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)k * no * L; };
+  auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)k * no * L; };
+  auto ES = [&](int k) { return (void*)(ws + p.ES + ts * (size_t)k * ne * L); };
+  float* DV[2] = {(float*)(ws + p.DV[0]), (float*)(ws + p.DV[1])};
+  float* DE[2] = {(float*)(ws + p.DE[0]), (float*)(ws + p.DE[1])};
+  float* DAGG = (float*)(ws + p.DAGG);
+  float* G = (float*)(ws + p.G);
+  float* VP = (float*)(ws + p.VPART);
+  int32_t* erecv = (int32_t*)(ws + p.erecv);
+  hipError_t e = hipSuccess;
+#define CHK(what) \
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_backward " what);
+
+  auto rows_args = [&](const MlpL& ml, int64_t rows, void* const* del, void* const* hid) {
+    RowsBwdArgs a{};
+    a.mlp = dev_mlp(m, ml);
+    a.rows = rows;
+    a.vpart = VP;
+    a.nvec = ml.nvec;
+    a.eps = m->cfg.ln_eps;
+    for (int j = 0; j < 3; ++j) a.delta[j] = del[j];
+    for (int j = 0; j < 2; ++j) a.hid[j] = hid[j];
+    return a;
+  };
+  void* DEL_N[3] = {ws + p.DEL_N[0], ws + p.DEL_N[1], ws + p.DEL_N[2]};
+  void* HID_N[2] = {ws + p.HID_N[0], ws + p.HID_N[1]};
+  void* DEL_E[3] = {ws + p.DEL_E[0], ws + p.DEL_E[1], ws + p.DEL_E[2]};
+  void* HID_E[2] = {ws + p.HID_E[0], ws + p.HID_E[1]};
+
+  // weight gradients of the hidden / last Linears from the stored activations
+  auto dw_hidden = [&](const MlpL& ml, int64_t R, void* const* del, void* const* hid, int ld_last) -> hipError_t {
+    for (int j = 1; j < D; ++j) {
+      DwArgs a{};
+      a.delta = del[j];
+      a.ldd = (j == D - 1) ? ld_last : L;
+      a.a_kind = 0;
+      a.a0 = hid[j - 1];
+      a.lda0 = L;
+      a.R = R;
+      hipError_t r = run_dw(m, ml.lin[j], a, d_params, accumulate, st);
+      if (r != hipSuccess) return r;
+    }
+    return hipSuccess;
+  };
+
+  // ---- decoder
+  int a_ = 0;  // DV[a_] holds dL/dv^{k+1}
+  {
+    const MlpL& ml = m->dec();
+    RowsBwdArgs a = rows_args(ml, no, DEL_N, HID_N);
+    a.in0 = V(K);
+    a.dm = d_out;
+    a.dx0 = DV[a_];
+    a.fout = m->cfg.node_out;
+    {
+      Timed t_(m, MGN_T_NODE_BWD, st);
+      e = launch_rows_bwd(m->prec, L, D, DECODER, a, BWD_GRID, st);
+    }
+    CHK("decoder");
+    e = run_vec(m, ml, d_params, accumulate, st);
+    CHK("decoder vec");
+    DwArgs w{};
+    w.delta = DEL_N[0];
+    w.ldd = L;
+    w.a_kind = 1;
+    w.a0 = V(K);
+    w.lda0 = L;
+    w.R = no;
+    e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
+    CHK("decoder dW");
+    e = dw_hidden(ml, no, DEL_N, HID_N, 16);
+    CHK("decoder dW");
+  }
+  // ---- processor, last block first
+  for (int k = K - 1; k >= 0; --k) {
+    const int b_ = 1 - a_;
+    const float* Hk = nh > 0 ? m->halo + (size_t)k * nh * L : nullptr;
+    {
+      const MlpL& ml = m->node(k);
+      RowsBwdArgs a = rows_args(ml, no, DEL_N, HID_N);
+      a.in0 = V(k);
+      a.in1 = AGG(k);
+      a.dm = DV[a_];
+      a.dx0 = DV[b_];
+      a.dx1 = DAGG;
+      {
+        Timed t_(m, MGN_T_NODE_BWD, st);
+        e = launch_rows_bwd(m->prec, L, D, NODE_BLOCK, a, BWD_GRID, st);
+      }
+      CHK("node block");
+      e = run_vec(m, ml, d_params, accumulate, st);
+      CHK("node vec");
+      DwArgs w{};
+      w.delta = DEL_N[0];
+      w.ldd = L;
+      w.a_kind = 3;
+      w.a0 = V(k);
+      w.a1 = AGG(k);
+      w.R = no;
+      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
+      CHK("node dW");
+      e = dw_hidden(ml, no, DEL_N, HID_N, L);
+      CHK("node dW");
+    }
+    {
+      const MlpL& ml = m->edge(k);
+      EdgeBwdArgs a{};
+      a.mlp = dev_mlp(m, ml);
+      a.row_ptr = g->row_ptr;
+      a.send = g->send;
+      a.erecv = erecv;
+      a.unit_r = (int32_t*)(ws + p.unit_r);
+      a.n_units = (int32_t*)(ws + p.nunits);
+      a.V = V(k);
+      a.H = Hk;
+      a.n_owned = no;
+      a.Ein = ES(k);
+      a.de_next = (k == K - 1) ? nullptr : DE[a_];
+      a.dagg = DAGG;
+      a.de_out = DE[b_];
+      a.g = G;
+      a.dv = DV[b_];
+      for (int j = 0; j < 3; ++j) a.delta[j] = DEL_E[j];
+      for (int j = 0; j < 2; ++j) a.hid[j] = HID_E[j];
+      a.vpart = VP;
+      a.nvec = ml.nvec;
+      a.eps = m->cfg.ln_eps;
+      {
+        Timed t_(m, MGN_T_EDGE_BWD, st);
+        e = launch_edge_bwd(m->prec, L, D, a, BWD_GRID, st);
+      }
+      CHK("edge block");
+      e = run_vec(m, ml, d_params, accumulate, st);
+      CHK("edge vec");
+      DwArgs w{};
+      w.delta = DEL_E[0];
+      w.ldd = L;
+      w.a_kind = 2;
+      w.a0 = ES(k);
+      w.a1 = V(k);
+      w.a2 = Hk;
+      w.send = g->send;
+      w.erecv = erecv;
+      w.n_owned = no;
+      w.R = ne;
+      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
+      CHK("edge dW");
+      e = dw_hidden(ml, ne, DEL_E, HID_E, L);
+      CHK("edge dW");
+      Timed t_(m, MGN_T_SENDER_GATHER, st);
+      e = launch_sender_gather(no + nh, no, g->trow_ptr, g->tedge, G, DV[b_],
+                               d_halo ? d_halo + (size_t)k * nh * L : nullptr, L, st);
+      CHK("sender gather");
+    }
+    a_ = b_;
+  }
+  // ---- encoders
+  {
+    const MlpL& ml = m->enc_node();
+    RowsBwdArgs a = rows_args(ml, no, DEL_N, HID_N);
+    a.in0 = m->nf;
+    a.fin = m->cfg.node_in;
+    a.dm = DV[a_];
+    {
+      Timed t_(m, MGN_T_NODE_BWD, st);
+      e = launch_rows_bwd(m->prec, L, D, ENC_NODE, a, BWD_GRID, st);
+    }
+    CHK("EncNode");
+    e = run_vec(m, ml, d_params, accumulate, st);
+    CHK("EncNode vec");
+    DwArgs w{};
+    w.delta = DEL_N[0];
+    w.ldd = L;
+    w.a_kind = 1;
+    w.a0 = m->nf;
+    w.lda0 = m->cfg.node_in;
+    w.R = no;
+    e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
+    CHK("EncNode dW");
+    e = dw_hidden(ml, no, DEL_N, HID_N, L);
+    CHK("EncNode dW");
+  }
+  {
+    const MlpL& ml = m->enc_edge();
+    if (K > 0 && ne > 0) {
+      RowsBwdArgs a = rows_args(ml, ne, DEL_E, HID_E);
+      a.in0 = m->ef;
+      a.fin = m->cfg.edge_in;
+      a.dm = DE[a_];  // block 0 wrote dL/de^0 into DE[b_], and b_ became a_
+      {
+        Timed t_(m, MGN_T_NODE_BWD, st);
+        e = launch_rows_bwd(m->prec, L, D, ENC_EDGE, a, BWD_GRID, st);
+      }
+      CHK("EncEdge");
+      e = run_vec(m, ml, d_params, accumulate, st);
+      CHK("EncEdge vec");
+      DwArgs w{};
+      w.delta = DEL_E[0];
+      w.ldd = L;
+      w.a_kind = 1;
+      w.a0 = m->ef;
+      w.lda0 = m->cfg.edge_in;
+      w.R = ne;
+      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
+      CHK("EncEdge dW");
+      e = dw_hidden(ml, ne, DEL_E, HID_E, L);
+      CHK("EncEdge dW");
+    } else if (!accumulate) {
+      // no edges reach the output: the edge encoder's gradient is zero
+      const int64_t b = ml.lin[0].w;
+      const int64_t end = ml.beta + ml.lin[D - 1].out;
+      e = launch_zero(d_params + b, end - b, st);
+      CHK("EncEdge zero");
+    }
+  }
+#undef CHK
+  return MGN_OK;
+}
+
+extern "C" mgn_status mgn_mse_grad(const float* out, const float* target, const uint8_t* mask, int64_t n, int32_t d,
+                                   float* loss, float* d_out, mgn_stream stream) {
+  if (n < 0 || d < 1) return fail(nullptr, MGN_E_ARG, "mgn_mse_grad: bad sizes");
+  if (!loss || (n > 0 && (!out || !target || !d_out))) return fail(nullptr, MGN_E_ARG, "mgn_mse_grad: NULL argument");
+  hipError_t e = launch_mse(out, target, mask, n, d, loss, d_out, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(nullptr, e, "mgn_mse_grad");
+  return MGN_OK;
+}
+
+extern "C" mgn_status mgn_timing_enable(mgn_model* m, int enable) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_timing_enable: model is NULL");
+  m->timing = enable != 0;
+  if (m->timing) {
+    m->ev_used = 0;
+    m->ev_rec.clear();
+  }
+  return MGN_OK;
+}
+
+extern "C" mgn_status mgn_timing_read(mgn_model* m, int timer, double* ms_total, int64_t* launches) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_timing_read: model is NULL");
+  if (timer < 0 || timer >= MGN_T_COUNT || !ms_total || !launches)
+    return fail(m, MGN_E_ARG, "mgn_timing_read: bad argument");
+  double t = 0;
+  int64_t n = 0;
+  for (const auto& r : m->ev_rec) {
+    if (r.first != timer) continue;
+    hipError_t e = hipEventSynchronize(m->ev_pool[r.second + 1]);
+    float ms = 0;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, m->ev_pool[r.second], m->ev_pool[r.second + 1]);
+    if (e != hipSuccess) return hip_fail(m, e, "mgn_timing_read");
+    t += ms;
+    ++n;
+  }
+  *ms_total = t;
+  *launches = n;
+  return MGN_OK;
+}

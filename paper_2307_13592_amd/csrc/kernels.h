@@ -1,0 +1,131 @@
+// Host-visible launch interface of the libmgn kernels (internal; the public
+// C ABI is include/mgn.h).  Every launcher enqueues asynchronously on the
+// given stream and returns the hipError_t of the launch.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "device_common.h"
+
+namespace mgn {
+
+enum Prec { F32 = 0, BF16 = 1 };
+enum RowKind { ENC_NODE = 0, ENC_EDGE = 1, NODE_BLOCK = 2, DECODER = 3 };
+
+// ---------------------------------------------------------------- args ---
+struct RowsFwdArgs {
+  Mlp mlp;
+  int64_t rows;
+  int fin, fout;
+  const float* in0;  // ENC: features [rows][fin]; NODE/DEC: v [rows][L]
+  const float* in1;  // NODE: aggregated messages [rows][L]
+  void* out;         // ENC_NODE, NODE, DEC: fp32; ENC_EDGE: storage type
+  float eps;
+};
+
+struct EdgeFwdArgs {
+  Mlp mlp;
+  const int32_t* row_ptr;
+  const int32_t* send;
+  const int32_t* erecv;
+  const int32_t* unit_r;
+  const int32_t* n_units;
+  const float* V;  // block input, owned rows [n_owned][L]
+  const float* H;  // block input, halo rows [n_halo][L]
+  int64_t n_owned;
+  const void* Ein;  // edge latents in [E][L] (storage type)
+  void* Eout;       // edge latents out, or null (last block)
+  float* agg;       // [n_owned][L]
+  float eps;
+};
+
+struct RowsBwdArgs {
+  Mlp mlp;
+  int64_t rows;
+  int fin, fout;
+  const float* in0;
+  const float* in1;
+  const float* dm;   // gradient w.r.t. the MLP output (LN output; dOut for the decoder)
+  float* dx0;        // NODE: dv^k owned part (= dm + dX_v); DEC: dv^K
+  float* dx1;        // NODE: d agg
+  void* delta[3];    // storage type [rows][L]: gradient at each Linear's output
+  void* hid[2];      // storage type [rows][L]: inputs of Linear 1 .. D-1
+  float* vpart;      // [grid][nvec] per-workgroup bias / LayerNorm gradients
+  int nvec;
+  float eps;
+};
+
+struct EdgeBwdArgs {
+  Mlp mlp;
+  const int32_t* row_ptr;
+  const int32_t* send;
+  const int32_t* erecv;
+  const int32_t* unit_r;
+  const int32_t* n_units;
+  const float* V;
+  const float* H;
+  int64_t n_owned;
+  const void* Ein;      // e^k (storage type)
+  const float* de_next; // dL/de^{k+1} [E][L] or null (last block)
+  const float* dagg;    // [n_owned][L]
+  float* de_out;        // dL/de^k [E][L]
+  float* g;             // sender-side input gradients [E][L]
+  float* dv;            // [n_owned][L], receiver-side input gradients are added
+  void* delta[3];
+  void* hid[2];
+  float* vpart;
+  int nvec;
+  float eps;
+};
+
+struct DwArgs {
+  const void* delta;  // storage type [R][ldd]
+  int ldd;
+  int O, I;
+  int a_kind;         // 0 dense storage type, 1 dense fp32, 2 edge concat, 3 node concat
+  const void* a0;     // dense source / e^k / v
+  int lda0;
+  const float* a1;    // node concat: agg; edge concat: V (owned)
+  const float* a2;    // edge concat: H (halo)
+  const int32_t* send;
+  const int32_t* erecv;
+  int64_t n_owned;
+  int L;
+  int64_t R;
+  int S;
+  float* part;        // [S][O][I]
+};
+
+struct VecSeg {
+  int vec_off;
+  int64_t param_off;
+  int len;
+};
+
+// ------------------------------------------------------------ launchers ---
+hipError_t launch_zero(float* p, int64_t n, hipStream_t st);
+hipError_t launch_pack(int prec, const float* W, int out, int in, int bwd, uint4* dst, int nkg, hipStream_t st);
+hipError_t launch_erecv(const int32_t* row_ptr, int64_t n_owned, int32_t* erecv, hipStream_t st);
+hipError_t launch_plan(const int32_t* row_ptr, int64_t n_owned, int te_target, int r_max, int32_t* chunk_cnt,
+                       int32_t* unit_r, int32_t* n_units, hipStream_t st);
+int64_t plan_max_units(int64_t n_owned, int64_t n_edges, int te_target, int r_max);
+int64_t plan_chunks(int64_t n_owned);
+
+hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st);
+hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int grid, hipStream_t st);
+hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st);
+hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int grid, hipStream_t st);
+hipError_t launch_sender_gather(int64_t n_local, int64_t n_owned, const int32_t* trow, const int32_t* tedge,
+                                const float* g, float* dv, float* dh, int L, hipStream_t st);
+hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st);
+hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int accumulate, hipStream_t st);
+hipError_t launch_vec_reduce(const float* vpart, int nwg, int nvec, const VecSeg* segs, int nseg, float* dparams,
+                             int accumulate, hipStream_t st);
+hipError_t launch_mse(const float* out, const float* target, const uint8_t* mask, int64_t n, int d, float* loss,
+                      float* d_out, hipStream_t st);
+
+// tile sizes the host needs to know (rows per edge sub-tile, per prec/L/D)
+int edge_tile_rows(int prec, int L, int D);
+int dw_splits(int64_t R, int O, int I);
+
+}  // namespace mgn

@@ -1,0 +1,1430 @@
+// libmgn kernels for CDNA4 (gfx950): one training step (forward and backward)
+// of the MeshGraphNets encode-process-decode network on one partition.
+//
+// Kernel map (paper: section "Model", Algorithm 1; the paper's own code is
+// PyTorch layers, these are fused replacements):
+//   pack_kernel        parameter re-layout into MFMA fragment order
+//   erecv / plan       per-edge receiver ids; receiver-aligned edge work units
+//   rows_fwd           EncNode, EncEdge, node half of a block, DecNode
+//   edge_fwd           edge half of a block: gather [e | v_s | v_r] into LDS,
+//                      MLP on MFMA, LayerNorm, residual, ordered receiver sum
+//   rows_bwd/edge_bwd  the same with the forward recomputed in-tile
+//   sender_gather      ordered sum of sender-side gradients (transposed CSR)
+//   dw / dw_reduce     weight gradients as split-K MFMA GEMMs, fixed order
+//   vec_reduce         bias and LayerNorm gradients, fixed order
+//   mse                masked mean-squared-error loss and its gradient
+// No float atomics anywhere: every sum has a fixed order, so results are
+// bitwise reproducible run to run.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace mgn {
+
+constexpr int NT = 256;          // threads per workgroup
+constexpr int NW = NT / 64;      // waves per workgroup
+constexpr int LDS_MAX = 160 * 1024;
+
+template <int P>
+struct PrecOf;
+template <>
+struct PrecOf<F32> {
+  using type = PF32;
+};
+template <>
+struct PrecOf<BF16> {
+  using type = PBF16;
+};
+
+__host__ __device__ constexpr int rup(int x, int m) { return (x + m - 1) / m * m; }
+
+// ------------------------------------------------------------ staging ---
+// Loads 4 consecutive fp32 values and stores them to LDS in storage type.
+template <class P>
+__device__ __forceinline__ void st4(typename P::T* dst, float4 v) {
+  if constexpr (sizeof(typename P::T) == 4) {
+    *reinterpret_cast<float4*>(dst) = v;
+  } else {
+    uint2 w;
+    w.x = (uint32_t)P::cvt(v.x) | ((uint32_t)P::cvt(v.y) << 16);
+    w.y = (uint32_t)P::cvt(v.z) | ((uint32_t)P::cvt(v.w) << 16);
+    *reinterpret_cast<uint2*>(dst) = w;
+  }
+}
+
+// Copies `width` storage-type elements (a multiple of 16 bytes) from global
+// row src into LDS row dst, one 16-byte chunk per thread of the group.
+template <class P>
+__device__ __forceinline__ void copy_row16(typename P::T* dst, const typename P::T* src, int width, int lane,
+                                           int nlanes) {
+  constexpr int E16 = 16 / sizeof(typename P::T);
+  for (int c = lane * E16; c < width; c += nlanes * E16)
+    *reinterpret_cast<uint4*>(dst + c) = *reinterpret_cast<const uint4*>(src + c);
+}
+
+// Stores an accumulator tile (MB x NBW blocks of 16x16) plus bias and
+// optional ReLU into an LDS matrix of type OutT (row stride ld).
+template <class P, int MB, int NBW, bool RELU, class OutT>
+__device__ __forceinline__ void store_acc(const floatx4 (&acc)[MB][NBW], int nb0, const float* __restrict__ bias,
+                                          int nvalid, OutT* dst, int ld) {
+#pragma unroll
+  for (int n = 0; n < NBW; ++n) {
+    const int col = (nb0 + n) * 16 + acc_col();
+    const float bv = (bias && col < nvalid) ? bias[col] : 0.f;
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float v = acc[m][n][r] + bv;
+        if (RELU) v = v > 0.f ? v : 0.f;
+        const int row = m * 16 + acc_row(r);
+        if constexpr (__is_same(OutT, float)) {
+          dst[row * ld + col] = v;
+        } else {
+          dst[row * ld + col] = P::cvt(v);
+        }
+      }
+  }
+}
+
+// LayerNorm statistics of TM rows of width L (fp32 in LDS, row stride ld):
+// replaces y by xhat = (y - mean) * rstd and stores rstd per row.  TPR
+// consecutive threads share a row.
+template <int TM, int L>
+__device__ __forceinline__ void ln_normalise(float* Y, int ld, float eps, float* rstd_out) {
+  constexpr int TPR = NT / TM;
+  const int row = threadIdx.x / TPR, q = threadIdx.x % TPR;
+  float* y = Y + row * ld;
+  float s = 0.f;
+  for (int c = q; c < L; c += TPR) s += y[c];
+#pragma unroll
+  for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o, 64);
+  const float mu = s / L;
+  float v = 0.f;
+  for (int c = q; c < L; c += TPR) {
+    const float d = y[c] - mu;
+    v += d * d;
+  }
+#pragma unroll
+  for (int o = 1; o < TPR; o <<= 1) v += __shfl_xor(v, o, 64);
+  const float rs = 1.0f / sqrtf(v / L + eps);
+  for (int c = q; c < L; c += TPR) y[c] = (y[c] - mu) * rs;
+  if (q == 0 && rstd_out) rstd_out[row] = rs;
+}
+
+template <int TM, int L>
+__device__ __forceinline__ void ln_affine(float* Y, int ld, const float* __restrict__ gamma,
+                                          const float* __restrict__ beta) {
+  constexpr int TPR = NT / TM;
+  const int row = threadIdx.x / TPR, q = threadIdx.x % TPR;
+  float* y = Y + row * ld;
+  for (int c = q; c < L; c += TPR) y[c] = gamma[c] * y[c] + beta[c];
+}
+
+// LayerNorm backward for TM rows: DM holds dL/d(LN output); XH holds xhat.
+// Overwrites DM with dL/dy (y = LN input) and writes it in storage type to DY.
+template <class P, int TM, int L>
+__device__ __forceinline__ void ln_backward(float* DM, int ldm, const float* XH, int ldx, const float* rstd,
+                                            const float* __restrict__ gamma, typename P::T* DY, int ldy) {
+  constexpr int TPR = NT / TM;
+  const int row = threadIdx.x / TPR, q = threadIdx.x % TPR;
+  float* dm = DM + row * ldm;
+  const float* xh = XH + row * ldx;
+  float s1 = 0.f, s2 = 0.f;
+  for (int c = q; c < L; c += TPR) {
+    const float d = dm[c] * gamma[c];
+    s1 += d;
+    s2 += d * xh[c];
+  }
+#pragma unroll
+  for (int o = 1; o < TPR; o <<= 1) {
+    s1 += __shfl_xor(s1, o, 64);
+    s2 += __shfl_xor(s2, o, 64);
+  }
+  const float m1 = s1 / L, m2 = s2 / L, rs = rstd[row];
+  for (int c = q; c < L; c += TPR) {
+    const float dy = rs * (dm[c] * gamma[c] - m1 - xh[c] * m2);
+    dm[c] = dy;
+    DY[row * ldy + c] = P::cvt(dy);
+  }
+}
+
+// Column sums over TM rows with a fixed (ascending) row order.
+__device__ __forceinline__ float col_sum(const float* A, int ld, int rows, int c) {
+  float s = 0.f;
+  for (int r = 0; r < rows; ++r) s += A[r * ld + c];
+  return s;
+}
+
+// Sum of acc over the tile's rows for each of the wave's columns (all lanes
+// of a 16-lane column group end with the same value).
+template <int MB, int NBW>
+__device__ __forceinline__ void acc_colsum(const floatx4 (&acc)[MB][NBW], float (&out)[NBW]) {
+#pragma unroll
+  for (int n = 0; n < NBW; ++n) {
+    float s = 0.f;
+#pragma unroll
+    for (int m = 0; m < MB; ++m) s += (acc[m][n][0] + acc[m][n][1]) + (acc[m][n][2] + acc[m][n][3]);
+    s += __shfl_xor(s, 16, 64);
+    s += __shfl_xor(s, 32, 64);
+    out[n] = s;
+  }
+}
+
+// ----------------------------------------------------------------- pack ---
+template <class P>
+__global__ void pack_kernel(const float* __restrict__ W, int out, int in, int bwd, uint4* __restrict__ dst,
+                            int nkg, int64_t total) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int lane = (int)(idx & 63);
+  const int kg = (int)((idx >> 6) % nkg);
+  const int nb = (int)((idx >> 6) / nkg);
+  const int j = nb * 16 + (lane & 15);
+  const int k0 = kg * P::KG + (lane >> 4) * P::EL;
+  typename P::T v[P::EL];
+#pragma unroll
+  for (int e = 0; e < P::EL; ++e) {
+    const int k = k0 + e;
+    float x = 0.f;
+    if (!bwd) {
+      if (j < out && k < in) x = W[(int64_t)j * in + k];
+    } else {
+      if (j < in && k < out) x = W[(int64_t)k * in + j];
+    }
+    v[e] = P::cvt(x);
+  }
+  dst[idx] = *reinterpret_cast<const uint4*>(v);
+}
+
+// ------------------------------------------------------------- fills ---
+// Plain fill kernels (used instead of memset nodes, which some callers
+// capture into graphs).
+__global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+__global__ void fill_f32_kernel(float* p, int64_t n, float v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+hipError_t launch_zero(float* p, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int64_t g = (n + NT - 1) / NT;
+  hipLaunchKernelGGL(fill_f32_kernel, dim3((unsigned)(g < 4096 ? g : 4096)), dim3(NT), 0, st, p, n, 0.f);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------- planning ---
+__global__ void erecv_kernel(const int32_t* __restrict__ row_ptr, int64_t n_owned, int32_t* __restrict__ erecv) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= n_owned) return;
+  for (int32_t e = row_ptr[r]; e < row_ptr[r + 1]; ++e) erecv[e] = (int32_t)r;
+}
+
+constexpr int PLAN_CHUNK = 128;  // receivers per planning thread
+
+// Greedy packing of consecutive receivers into work units of at most
+// te_target edges and r_max receivers (a receiver with more edges than
+// te_target gets a unit of its own); chunk boundaries close a unit.
+__device__ int plan_chunk(const int32_t* row_ptr, int64_t r0, int64_t r1, int te_target, int r_max,
+                          int32_t* out) {
+  int count = 0, edges = 0, recv = 0;
+  for (int64_t r = r0; r < r1; ++r) {
+    const int d = row_ptr[r + 1] - row_ptr[r];
+    if (recv > 0 && (edges + d > te_target || recv + 1 > r_max)) {
+      edges = 0;
+      recv = 0;
+    }
+    if (recv == 0) {
+      if (out) out[count] = (int32_t)r;
+      ++count;
+    }
+    edges += d;
+    recv += 1;
+  }
+  return count;
+}
+
+__global__ void plan_count_kernel(const int32_t* __restrict__ row_ptr, int64_t n_owned, int te_target, int r_max,
+                                  int32_t* __restrict__ cnt, int64_t nch) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= nch) return;
+  const int64_t r0 = c * PLAN_CHUNK, r1 = r0 + PLAN_CHUNK < n_owned ? r0 + PLAN_CHUNK : n_owned;
+  cnt[c] = plan_chunk(row_ptr, r0, r1, te_target, r_max, nullptr);
+}
+
+// Exclusive scan of the chunk counts in one workgroup (fixed order).
+__global__ void plan_scan_kernel(int32_t* __restrict__ cnt, int64_t nch, int32_t* __restrict__ n_units) {
+  __shared__ int32_t part[NT];
+  const int t = threadIdx.x;
+  const int64_t per = (nch + NT - 1) / NT;
+  const int64_t b = t * per, e = b + per < nch ? b + per : nch;
+  int32_t s = 0;
+  for (int64_t i = b; i < e; ++i) s += cnt[i];
+  part[t] = s;
+  __syncthreads();
+  if (t == 0) {
+    int32_t acc = 0;
+    for (int i = 0; i < NT; ++i) {
+      const int32_t v = part[i];
+      part[i] = acc;
+      acc += v;
+    }
+    *n_units = acc;
+  }
+  __syncthreads();
+  int32_t acc = part[t];
+  for (int64_t i = b; i < e; ++i) {
+    const int32_t v = cnt[i];
+    cnt[i] = acc;
+    acc += v;
+  }
+}
+
+__global__ void plan_write_kernel(const int32_t* __restrict__ row_ptr, int64_t n_owned, int te_target, int r_max,
+                                  const int32_t* __restrict__ off, int64_t nch, const int32_t* __restrict__ n_units,
+                                  int32_t* __restrict__ unit_r) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= nch) return;
+  const int64_t r0 = c * PLAN_CHUNK, r1 = r0 + PLAN_CHUNK < n_owned ? r0 + PLAN_CHUNK : n_owned;
+  plan_chunk(row_ptr, r0, r1, te_target, r_max, unit_r + off[c]);
+  if (c == nch - 1) unit_r[*n_units] = (int32_t)n_owned;
+}
+
+// ---------------------------------------------------------- row kernels ---
+template <int KIND, int L>
+struct RowShape {
+  static constexpr int KIN = (KIND == ENC_NODE || KIND == ENC_EDGE) ? 32 : (KIND == NODE_BLOCK ? 2 * L : L);
+  static constexpr int NOUT = (KIND == DECODER) ? 16 : L;
+  static constexpr bool LN = KIND != DECODER;
+};
+
+// LDS layout of a row kernel with TM rows (bytes).  X: inputs; HB, HC: hidden
+// activations; Y: last-layer output / xhat (aliased onto X when it fits);
+// DY: gradient in storage type; DM: fp32 gradient / output staging.
+template <class P, int KIND, int L, int D, int TM>
+struct RowLds {
+  using S = RowShape<KIND, L>;
+  static constexpr int LDX = S::KIN + P::PAD;
+  static constexpr int LDH = L + P::PAD;
+  static constexpr int LDY = S::NOUT + 4;
+  static constexpr int LDM = (S::NOUT > L ? S::NOUT : L) + 4;
+  static constexpr int XB = TM * LDX * (int)sizeof(typename P::T);
+  static constexpr int HB = TM * LDH * (int)sizeof(typename P::T);
+  static constexpr int YB = TM * LDY * 4;
+  static constexpr int MB = TM * LDM * 4;
+  static constexpr bool Y_IN_X = XB >= YB;
+  static constexpr int OFF_H = rup(XB, 16);
+  static constexpr int OFF_H2 = OFF_H + HB;
+  static constexpr int OFF_Y = Y_IN_X ? 0 : OFF_H2 + (D == 3 ? HB : 0);
+  static constexpr int END_F = Y_IN_X ? OFF_H2 + (D == 3 ? HB : 0) : OFF_Y + YB;  // forward kernels
+  static constexpr int OFF_DY = rup(END_F, 16);
+  static constexpr int OFF_DM = OFF_DY + HB;
+  static constexpr int OFF_RS = OFF_DM + MB;
+  static constexpr int END_B = OFF_RS + TM * 4;  // backward kernels
+};
+
+template <class P, int KIND, int L, int D>
+struct RowTM {
+  static constexpr int value = RowLds<P, KIND, L, D, 64>::END_B <= LDS_MAX   ? 64
+                               : RowLds<P, KIND, L, D, 32>::END_B <= LDS_MAX ? 32
+                                                                             : 16;
+};
+
+// Stages the first Linear's input rows into LDS X (zero rows past `n`).
+template <class P, int KIND, int L, int TM, int LDX>
+__device__ __forceinline__ void stage_rows(typename P::T* X, const float* __restrict__ in0,
+                                           const float* __restrict__ in1, int fin, int64_t row0, int n) {
+  using S = RowShape<KIND, L>;
+  if constexpr (KIND == ENC_NODE || KIND == ENC_EDGE) {
+    for (int i = threadIdx.x; i < TM * S::KIN; i += NT) {
+      const int r = i / S::KIN, c = i % S::KIN;
+      const float v = (r < n && c < fin) ? in0[(row0 + r) * fin + c] : 0.f;
+      X[r * LDX + c] = P::cvt(v);
+    }
+  } else {
+    constexpr int Q = L / 4;  // float4 per source row
+    constexpr int NSRC = KIND == NODE_BLOCK ? 2 : 1;
+    for (int i = threadIdx.x; i < TM * Q * NSRC; i += NT) {
+      const int r = i / (Q * NSRC), rem = i % (Q * NSRC), s = rem / Q, c4 = rem % Q;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (r < n) {
+        const float* src = (s == 0 ? in0 : in1) + (row0 + r) * L;
+        v = reinterpret_cast<const float4*>(src)[c4];
+      }
+      st4<P>(X + r * LDX + s * L + c4 * 4, v);
+    }
+  }
+}
+
+// Forward of the MLP on a staged tile: X -> ... -> Y (fp32, last layer + bias,
+// before LayerNorm).  Hidden activations stay in HB (and HC for depth 3).
+template <class P, int KIND, int L, int D, int TM>
+__device__ __forceinline__ void mlp_tile_forward(const Mlp& mlp, typename P::T* X, typename P::T* HB,
+                                                 typename P::T* HC, float* Y, int ldx, int ldh, int ldy) {
+  using S = RowShape<KIND, L>;
+  constexpr int MB = TM / 16;
+  constexpr int NBW = L / 16 / NW > 0 ? L / 16 / NW : 1;
+  const int wave = threadIdx.x >> 6;
+  {
+    floatx4 acc[MB][NBW];
+    if (wave * NBW * 16 < L) {
+      wave_gemm<P, MB, NBW>(X, ldx, mlp.lin[0].wf, mlp.lin[0].nkgf, wave * NBW, acc);
+      store_acc<P, MB, NBW, true>(acc, wave * NBW, mlp.lin[0].b, L, HB, ldh);
+    }
+  }
+  __syncthreads();
+  typename P::T* hin = HB;
+  if constexpr (D == 3) {
+    floatx4 acc[MB][NBW];
+    if (wave * NBW * 16 < L) {
+      wave_gemm<P, MB, NBW>(HB, ldh, mlp.lin[1].wf, mlp.lin[1].nkgf, wave * NBW, acc);
+      store_acc<P, MB, NBW, true>(acc, wave * NBW, mlp.lin[1].b, L, HC, ldh);
+    }
+    __syncthreads();
+    hin = HC;
+  }
+  {
+    constexpr int NB_OUT = S::NOUT / 16;
+    constexpr int NBO = NB_OUT / NW > 0 ? NB_OUT / NW : 1;
+    floatx4 acc[MB][NBO];
+    if (wave * NBO < NB_OUT) {
+      wave_gemm<P, MB, NBO>(hin, ldh, mlp.lin[D - 1].wf, mlp.lin[D - 1].nkgf, wave * NBO, acc);
+      store_acc<P, MB, NBO, false>(acc, wave * NBO, mlp.lin[D - 1].b, mlp.lin[D - 1].out, Y, ldy);
+    }
+  }
+  __syncthreads();
+}
+
+template <int P_, int L, int D, int KIND>
+__global__ __launch_bounds__(NT) void rows_fwd_kernel(RowsFwdArgs a) {
+  using P = typename PrecOf<P_>::type;
+  using T = typename P::T;
+  constexpr int TM = RowTM<P, KIND, L, D>::value;
+  using Lay = RowLds<P, KIND, L, D, TM>;
+  extern __shared__ __align__(16) unsigned char lds[];
+  T* X = reinterpret_cast<T*>(lds);
+  T* HB = reinterpret_cast<T*>(lds + Lay::OFF_H);
+  T* HC = reinterpret_cast<T*>(lds + Lay::OFF_H2);
+  float* Y = reinterpret_cast<float*>(lds + Lay::OFF_Y);
+  const int64_t ntiles = (a.rows + TM - 1) / TM;
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t row0 = tile * TM;
+    const int n = (int)(a.rows - row0 < TM ? a.rows - row0 : TM);
+    stage_rows<P, KIND, L, TM, Lay::LDX>(X, a.in0, a.in1, a.fin, row0, n);
+    __syncthreads();
+    mlp_tile_forward<P, KIND, L, D, TM>(a.mlp, X, HB, HC, Y, Lay::LDX, Lay::LDH, Lay::LDY);
+    if constexpr (RowShape<KIND, L>::LN) {
+      ln_normalise<TM, L>(Y, Lay::LDY, a.eps, nullptr);
+      ln_affine<TM, L>(Y, Lay::LDY, a.mlp.gamma, a.mlp.beta);
+      __syncthreads();
+    }
+    if constexpr (KIND == DECODER) {
+      float* out = reinterpret_cast<float*>(a.out);
+      for (int i = threadIdx.x; i < n * a.fout; i += NT) {
+        const int r = i / a.fout, c = i % a.fout;
+        out[(row0 + r) * a.fout + c] = Y[r * Lay::LDY + c];
+      }
+    } else if constexpr (KIND == ENC_EDGE) {
+      T* out = reinterpret_cast<T*>(a.out);
+      for (int i = threadIdx.x; i < n * L; i += NT) {
+        const int r = i / L, c = i % L;
+        out[(row0 + r) * L + c] = P::cvt(Y[r * Lay::LDY + c]);
+      }
+    } else {
+      float* out = reinterpret_cast<float*>(a.out);
+      constexpr int Q = L / 4;
+      for (int i = threadIdx.x; i < n * Q; i += NT) {
+        const int r = i / Q, c4 = i % Q;
+        float4 y = *reinterpret_cast<const float4*>(Y + r * Lay::LDY + c4 * 4);
+        if constexpr (KIND == NODE_BLOCK) {
+          const float4 v = reinterpret_cast<const float4*>(a.in0 + (row0 + r) * L)[c4];
+          y.x += v.x;
+          y.y += v.y;
+          y.z += v.z;
+          y.w += v.w;
+        }
+        reinterpret_cast<float4*>(out + (row0 + r) * L)[c4] = y;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Backward of a row MLP with the forward recomputed in-tile.
+template <int P_, int L, int D, int KIND>
+__global__ __launch_bounds__(NT) void rows_bwd_kernel(RowsBwdArgs a) {
+  using P = typename PrecOf<P_>::type;
+  using T = typename P::T;
+  using S = RowShape<KIND, L>;
+  constexpr int TM = RowTM<P, KIND, L, D>::value;
+  using Lay = RowLds<P, KIND, L, D, TM>;
+  constexpr int MB = TM / 16;
+  constexpr int NBW = L / 16 / NW > 0 ? L / 16 / NW : 1;
+  extern __shared__ __align__(16) unsigned char lds[];
+  T* X = reinterpret_cast<T*>(lds);
+  T* HB = reinterpret_cast<T*>(lds + Lay::OFF_H);
+  T* HC = reinterpret_cast<T*>(lds + Lay::OFF_H2);
+  float* Y = reinterpret_cast<float*>(lds + Lay::OFF_Y);
+  T* DY = reinterpret_cast<T*>(lds + Lay::OFF_DY);
+  float* DM = reinterpret_cast<float*>(lds + Lay::OFF_DM);
+  float* RS = reinterpret_cast<float*>(lds + Lay::OFF_RS);
+  const int wave = threadIdx.x >> 6;
+  const bool wave_has_cols = wave * NBW * 16 < L;
+  const int tid = threadIdx.x;
+  const int nout_last = a.mlp.lin[D - 1].out;
+
+  // per-workgroup vector gradient accumulators
+  float g_gamma = 0.f, g_beta = 0.f, g_blast = 0.f;  // column tid
+  float g_bh[2][NBW];                                  // hidden-layer biases, columns of this wave
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int n = 0; n < NBW; ++n) g_bh[j][n] = 0.f;
+
+  const int64_t ntiles = (a.rows + TM - 1) / TM;
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t row0 = tile * TM;
+    const int n = (int)(a.rows - row0 < TM ? a.rows - row0 : TM);
+    stage_rows<P, KIND, L, TM, Lay::LDX>(X, a.in0, a.in1, a.fin, row0, n);
+    // incoming gradient (zero rows past n; decoder: dOut padded to 16 columns)
+    for (int i = tid; i < TM * S::NOUT; i += NT) {
+      const int r = i / S::NOUT, c = i % S::NOUT;
+      float v = 0.f;
+      if (r < n) {
+        if constexpr (KIND == DECODER) {
+          if (c < a.fout) v = a.dm[(row0 + r) * a.fout + c];
+        } else {
+          v = a.dm[(row0 + r) * L + c];
+        }
+      }
+      DM[r * Lay::LDM + c] = v;
+    }
+    __syncthreads();
+    if constexpr (S::LN) {
+      mlp_tile_forward<P, KIND, L, D, TM>(a.mlp, X, HB, HC, Y, Lay::LDX, Lay::LDH, Lay::LDY);
+      ln_normalise<TM, L>(Y, Lay::LDY, a.eps, RS);
+      __syncthreads();
+      if (tid < L) {
+        for (int r = 0; r < n; ++r) {
+          const float d = DM[r * Lay::LDM + tid];
+          g_gamma += d * Y[r * Lay::LDY + tid];
+          g_beta += d;
+        }
+      }
+      __syncthreads();
+      ln_backward<P, TM, L>(DM, Lay::LDM, Y, Lay::LDY, RS, a.mlp.gamma, DY, Lay::LDH);
+      __syncthreads();
+      if (tid < L) g_blast += col_sum(DM, Lay::LDM, n, tid);
+    } else {
+      // decoder: only the hidden activations are needed
+      {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols) {
+          wave_gemm<P, MB, NBW>(X, Lay::LDX, a.mlp.lin[0].wf, a.mlp.lin[0].nkgf, wave * NBW, acc);
+          store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[0].b, L, HB, Lay::LDH);
+        }
+      }
+      __syncthreads();
+      if constexpr (D == 3) {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols) {
+          wave_gemm<P, MB, NBW>(HB, Lay::LDH, a.mlp.lin[1].wf, a.mlp.lin[1].nkgf, wave * NBW, acc);
+          store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[1].b, L, HC, Lay::LDH);
+        }
+        __syncthreads();
+      }
+      // gradient at the decoder output, zero past the 16 padded columns up to
+      // one full k-group of the backward GEMM
+      for (int i = tid; i < TM * 32; i += NT) {
+        const int r = i / 32, c = i % 32;
+        DY[r * Lay::LDH + c] = P::cvt(c < 16 ? DM[r * Lay::LDM + c] : 0.f);
+      }
+      if (tid < nout_last) g_blast += col_sum(DM, Lay::LDM, n, tid);
+      __syncthreads();
+    }
+    // gradient at the last Linear's output and the hidden activations, for the
+    // weight-gradient GEMMs
+    {
+      const int w_last = S::NOUT;
+      T* dl = reinterpret_cast<T*>(a.delta[D - 1]);
+      for (int i = tid; i < n * w_last; i += NT) {
+        const int r = i / w_last, c = i % w_last;
+        dl[(row0 + r) * w_last + c] = DY[r * Lay::LDH + c];
+      }
+      T* h0 = reinterpret_cast<T*>(a.hid[0]);
+      for (int i = tid; i < n * L; i += NT) {
+        const int r = i / L, c = i % L;
+        h0[(row0 + r) * L + c] = HB[r * Lay::LDH + c];
+        if constexpr (D == 3) reinterpret_cast<T*>(a.hid[1])[(row0 + r) * L + c] = HC[r * Lay::LDH + c];
+      }
+    }
+    // back through the hidden layers: dz_{j-1} = (dz_j W_j) * [h_{j-1} > 0]
+#pragma unroll
+    for (int j = D - 1; j >= 1; --j) {
+      const T* hprev = (j == 2) ? HC : HB;
+      floatx4 acc[MB][NBW];
+      if (wave_has_cols) wave_gemm<P, MB, NBW>(DY, Lay::LDH, a.mlp.lin[j].wb, a.mlp.lin[j].nkgb, wave * NBW, acc);
+      __syncthreads();
+      if (wave_has_cols) {
+#pragma unroll
+        for (int nn = 0; nn < NBW; ++nn)
+#pragma unroll
+          for (int m = 0; m < MB; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int row = m * 16 + acc_row(r), col = (wave * NBW + nn) * 16 + acc_col();
+              const float h = P::tof(hprev[row * Lay::LDH + col]);
+              acc[m][nn][r] = h > 0.f ? acc[m][nn][r] : 0.f;
+              DY[row * Lay::LDH + col] = P::cvt(acc[m][nn][r]);
+            }
+        float cs[NBW];
+        acc_colsum<MB, NBW>(acc, cs);
+#pragma unroll
+        for (int nn = 0; nn < NBW; ++nn) g_bh[j - 1][nn] += cs[nn];
+      }
+      __syncthreads();
+      T* dj = reinterpret_cast<T*>(a.delta[j - 1]);
+      for (int i = tid; i < n * L; i += NT) {
+        const int r = i / L, c = i % L;
+        dj[(row0 + r) * L + c] = DY[r * Lay::LDH + c];
+      }
+    }
+    // input gradients
+    if constexpr (KIND == NODE_BLOCK || KIND == DECODER) {
+      constexpr int NPASS = KIND == NODE_BLOCK ? 2 : 1;
+#pragma unroll
+      for (int pass = 0; pass < NPASS; ++pass) {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols)
+          wave_gemm<P, MB, NBW>(DY, Lay::LDH, a.mlp.lin[0].wb, a.mlp.lin[0].nkgb, pass * (L / 16) + wave * NBW,
+                                acc);
+        __syncthreads();  // DM (gradient staging) may still be read above
+        if (wave_has_cols) store_acc<P, MB, NBW, false>(acc, wave * NBW, nullptr, L, DM, Lay::LDM);
+        __syncthreads();
+        float* dst = pass == 0 ? a.dx0 : a.dx1;
+        constexpr int Q = L / 4;
+        for (int i = tid; i < n * Q; i += NT) {
+          const int r = i / Q, c4 = i % Q;
+          float4 v = *reinterpret_cast<const float4*>(DM + r * Lay::LDM + c4 * 4);
+          if (KIND == NODE_BLOCK && pass == 0) {
+            const float4 d = reinterpret_cast<const float4*>(a.dm + (row0 + r) * L)[c4];
+            v.x += d.x;
+            v.y += d.y;
+            v.z += d.z;
+            v.w += d.w;
+          }
+          reinterpret_cast<float4*>(dst + (row0 + r) * L)[c4] = v;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // per-workgroup vector partials: [db_0 .. db_{D-1}, gamma, beta]
+  float* vp = a.vpart + (int64_t)blockIdx.x * a.nvec;
+  if (wave_has_cols && (threadIdx.x & 63) < 16) {
+#pragma unroll
+    for (int j = 0; j < D - 1; ++j)
+#pragma unroll
+      for (int nn = 0; nn < NBW; ++nn) vp[j * L + (wave * NBW + nn) * 16 + (threadIdx.x & 15)] = g_bh[j][nn];
+  }
+  const int off_last = (D - 1) * L;
+  if (tid < nout_last) vp[off_last + tid] = g_blast;
+  if constexpr (S::LN) {
+    if (tid < L) {
+      vp[off_last + L + tid] = g_gamma;
+      vp[off_last + 2 * L + tid] = g_beta;
+    }
+  }
+}
+
+// ---------------------------------------------------------- edge kernels ---
+// LDS of the edge kernels for TE rows: A holds [e | v_s | v_r] (storage type);
+// in the backward pass the same bytes then hold xhat (fp32, 4L bytes per row)
+// followed by the gradient in storage type.  B, C: hidden activations.  D:
+// fp32 gradient / output staging.
+template <class P, int L, int D, int TE>
+struct EdgeLds {
+  using T = typename P::T;
+  static constexpr int LDA = 3 * L + P::PAD;                    // storage-type elements
+  static constexpr int ROWB = LDA * (int)sizeof(T);             // bytes per A row
+  static constexpr int LDY = ROWB / 4;                          // fp32 stride over A rows
+  static constexpr int Y_OFF_F = L * (int)sizeof(T) / 4;        // forward: Y after e (fp32 index)
+  static constexpr int DY_OFF = 4 * L / (int)sizeof(T);         // backward: DY after xhat (T index)
+  static constexpr int LDH = L + P::PAD;
+  static constexpr int LDM = L + 4;
+  static constexpr int AB = TE * ROWB;
+  static constexpr int HB = TE * LDH * (int)sizeof(T);
+  static constexpr int OFF_B = rup(AB, 16);
+  static constexpr int OFF_C = OFF_B + HB;
+  static constexpr int OFF_D = OFF_C + (D == 3 ? HB : 0);
+  static constexpr int OFF_META = OFF_D + TE * LDM * 4;
+  static constexpr int END = OFF_META + TE * 12;
+  static constexpr int END_F = OFF_D + TE * 8;  // forward: meta right after B/C
+};
+
+template <class P, int L, int D>
+struct EdgeTE {
+  static constexpr int value = EdgeLds<P, L, D, 64>::END <= LDS_MAX   ? 64
+                               : EdgeLds<P, L, D, 32>::END <= LDS_MAX ? 32
+                                                                      : 16;
+};
+
+// Gathers one sub-tile [e | v_s | v_r] into LDS and the per-row receiver and
+// end-of-segment flags.
+template <class P, int L, int TE, int LDA>
+__device__ __forceinline__ void stage_edges(typename P::T* A, int32_t* rr, int32_t* last, const int32_t* erecv,
+                                            const int32_t* send, const typename P::T* Ein, const float* V,
+                                            const float* H, int64_t n_owned, int64_t sb, int n, int64_t e1) {
+  using T = typename P::T;
+  const int tid = threadIdx.x;
+  if (tid < TE) {
+    int32_t r = -1, l = 0;
+    if (tid < n) {
+      const int64_t e = sb + tid;
+      r = erecv[e];
+      l = (e + 1 == e1) || erecv[e + 1] != r;
+    }
+    rr[tid] = r;
+    last[tid] = l;
+  }
+  // e rows: 16-byte chunks
+  constexpr int E16 = 16 / sizeof(T);
+  constexpr int CPR = L / E16;
+  for (int i = tid; i < TE * CPR; i += NT) {
+    const int r = i / CPR, c = (i % CPR) * E16;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (r < n) v = *reinterpret_cast<const uint4*>(Ein + (sb + r) * L + c);
+    *reinterpret_cast<uint4*>(A + r * LDA + c) = v;
+  }
+  // sender and receiver node rows (fp32 -> storage type)
+  constexpr int Q = L / 4;
+  for (int i = tid; i < TE * 2 * Q; i += NT) {
+    const int r = i / (2 * Q), rem = i % (2 * Q), s = rem / Q, c4 = rem % Q;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < n) {
+      const int64_t e = sb + r;
+      const float* src;
+      if (s == 0) {
+        const int64_t snd = send[e];
+        src = snd < n_owned ? V + snd * L : H + (snd - n_owned) * L;
+      } else {
+        src = V + (int64_t)erecv[e] * L;
+      }
+      v = reinterpret_cast<const float4*>(src)[c4];
+    }
+    st4<P>(A + r * LDA + (1 + s) * L + c4 * 4, v);
+  }
+}
+
+// Zeroes `width` fp32 columns of the rows of receivers in [r0, r1) that have no
+// edges (their ordered sums are empty).
+__device__ __forceinline__ void zero_empty_receivers(const int32_t* row_ptr, int64_t r0, int64_t r1, float* dst,
+                                                     int L) {
+  for (int64_t r = r0; r < r1; ++r)
+    if (row_ptr[r] == row_ptr[r + 1])
+      for (int c = threadIdx.x; c < L; c += NT) dst[r * L + c] = 0.f;
+}
+
+template <int P_, int L, int D>
+__global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
+  using P = typename PrecOf<P_>::type;
+  using T = typename P::T;
+  constexpr int TE = EdgeTE<P, L, D>::value;
+  using Lay = EdgeLds<P, L, D, TE>;
+  constexpr int MB = TE / 16;
+  constexpr int NBW = L / 16 / NW > 0 ? L / 16 / NW : 1;
+  extern __shared__ __align__(16) unsigned char lds[];
+  T* A = reinterpret_cast<T*>(lds);
+  T* HB = reinterpret_cast<T*>(lds + Lay::OFF_B);
+  T* HC = reinterpret_cast<T*>(lds + Lay::OFF_C);
+  float* Y = reinterpret_cast<float*>(lds) + Lay::Y_OFF_F;
+  int32_t* rr = reinterpret_cast<int32_t*>(lds + Lay::OFF_D);
+  int32_t* last = rr + TE;
+  const int wave = threadIdx.x >> 6, tid = threadIdx.x;
+  const bool wave_has_cols = wave * NBW * 16 < L;
+  const T* Ein = reinterpret_cast<const T*>(a.Ein);
+  T* Eout = reinterpret_cast<T*>(a.Eout);
+
+  for (TileIter it(*a.n_units); it.valid(); it.next()) {
+    const int64_t r0 = a.unit_r[it.t], r1 = a.unit_r[it.t + 1];
+    const int64_t e0 = a.row_ptr[r0], e1 = a.row_ptr[r1];
+    zero_empty_receivers(a.row_ptr, r0, r1, a.agg, L);
+    float run = 0.f;  // running receiver sum of column tid
+    for (int64_t sb = e0; sb < e1; sb += TE) {
+      const int n = (int)(e1 - sb < TE ? e1 - sb : TE);
+      stage_edges<P, L, TE, Lay::LDA>(A, rr, last, a.erecv, a.send, Ein, a.V, a.H, a.n_owned, sb, n, e1);
+      __syncthreads();
+      {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols) {
+          wave_gemm<P, MB, NBW>(A, Lay::LDA, a.mlp.lin[0].wf, a.mlp.lin[0].nkgf, wave * NBW, acc);
+          store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[0].b, L, HB, Lay::LDH);
+        }
+      }
+      __syncthreads();
+      const T* hin = HB;
+      if constexpr (D == 3) {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols) {
+          wave_gemm<P, MB, NBW>(HB, Lay::LDH, a.mlp.lin[1].wf, a.mlp.lin[1].nkgf, wave * NBW, acc);
+          store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[1].b, L, HC, Lay::LDH);
+        }
+        __syncthreads();
+        hin = HC;
+      }
+      {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols) {
+          wave_gemm<P, MB, NBW>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, a.mlp.lin[D - 1].nkgf, wave * NBW, acc);
+          store_acc<P, MB, NBW, false>(acc, wave * NBW, a.mlp.lin[D - 1].b, L, Y, Lay::LDY);
+        }
+      }
+      __syncthreads();
+      ln_normalise<TE, L>(Y, Lay::LDY, a.eps, nullptr);
+      ln_affine<TE, L>(Y, Lay::LDY, a.mlp.gamma, a.mlp.beta);
+      __syncthreads();
+      if (Eout) {
+        for (int i = tid; i < n * L; i += NT) {
+          const int r = i / L, c = i % L;
+          Eout[(sb + r) * L + c] = P::cvt(P::tof(A[r * Lay::LDA + c]) + Y[r * Lay::LDY + c]);
+        }
+      }
+      for (int c = tid; c < L; c += NT) {
+        for (int r = 0; r < n; ++r) {
+          run += Y[r * Lay::LDY + c];
+          if (last[r]) {
+            a.agg[(int64_t)rr[r] * L + c] = run;
+            run = 0.f;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+template <int P_, int L, int D>
+__global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
+  using P = typename PrecOf<P_>::type;
+  using T = typename P::T;
+  constexpr int TE = EdgeTE<P, L, D>::value;
+  using Lay = EdgeLds<P, L, D, TE>;
+  constexpr int MB = TE / 16;
+  constexpr int NBW = L / 16 / NW > 0 ? L / 16 / NW : 1;
+  extern __shared__ __align__(16) unsigned char lds[];
+  T* A = reinterpret_cast<T*>(lds);
+  float* XH = reinterpret_cast<float*>(lds);     // xhat after the recompute (fp32, stride LDY)
+  T* DY = A + Lay::DY_OFF;                        // storage-type gradient (stride LDA)
+  float* Yf = reinterpret_cast<float*>(lds);     // last-layer output before LN (same place as xhat)
+  T* HB = reinterpret_cast<T*>(lds + Lay::OFF_B);
+  T* HC = reinterpret_cast<T*>(lds + Lay::OFF_C);
+  float* DM = reinterpret_cast<float*>(lds + Lay::OFF_D);
+  int32_t* rr = reinterpret_cast<int32_t*>(lds + Lay::OFF_META);
+  int32_t* last = rr + TE;
+  float* RS = reinterpret_cast<float*>(last + TE);
+  const int wave = threadIdx.x >> 6, tid = threadIdx.x;
+  const bool wave_has_cols = wave * NBW * 16 < L;
+  const T* Ein = reinterpret_cast<const T*>(a.Ein);
+
+  float g_gamma = 0.f, g_beta = 0.f, g_blast = 0.f;
+  float g_bh[2][NBW];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int n = 0; n < NBW; ++n) g_bh[j][n] = 0.f;
+
+  for (TileIter it(*a.n_units); it.valid(); it.next()) {
+    const int64_t r0 = a.unit_r[it.t], r1 = a.unit_r[it.t + 1];
+    const int64_t e0 = a.row_ptr[r0], e1 = a.row_ptr[r1];
+    float run = 0.f;  // running receiver sum (receiver-side input gradient), column tid
+    for (int64_t sb = e0; sb < e1; sb += TE) {
+      const int n = (int)(e1 - sb < TE ? e1 - sb : TE);
+      stage_edges<P, L, TE, Lay::LDA>(A, rr, last, a.erecv, a.send, Ein, a.V, a.H, a.n_owned, sb, n, e1);
+      // dm = de^{k+1} + dagg[receiver]
+      constexpr int Q = L / 4;
+      for (int i = tid; i < TE * Q; i += NT) {
+        const int r = i / Q, c4 = i % Q;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (r < n) {
+          const int64_t e = sb + r;
+          v = reinterpret_cast<const float4*>(a.dagg + (int64_t)a.erecv[e] * L)[c4];
+          if (a.de_next) {
+            const float4 d = reinterpret_cast<const float4*>(a.de_next + e * L)[c4];
+            v.x += d.x;
+            v.y += d.y;
+            v.z += d.z;
+            v.w += d.w;
+          }
+        }
+        *reinterpret_cast<float4*>(DM + r * Lay::LDM + c4 * 4) = v;
+      }
+      __syncthreads();
+      // recompute the forward: hidden activations and the LN input
+      {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols) {
+          wave_gemm<P, MB, NBW>(A, Lay::LDA, a.mlp.lin[0].wf, a.mlp.lin[0].nkgf, wave * NBW, acc);
+          store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[0].b, L, HB, Lay::LDH);
+        }
+      }
+      __syncthreads();
+      const T* hin = HB;
+      if constexpr (D == 3) {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols) {
+          wave_gemm<P, MB, NBW>(HB, Lay::LDH, a.mlp.lin[1].wf, a.mlp.lin[1].nkgf, wave * NBW, acc);
+          store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[1].b, L, HC, Lay::LDH);
+        }
+        __syncthreads();
+        hin = HC;
+      }
+      {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols)
+          wave_gemm<P, MB, NBW>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, a.mlp.lin[D - 1].nkgf, wave * NBW, acc);
+        __syncthreads();  // A (the gathered inputs) is overwritten below
+        if (wave_has_cols) store_acc<P, MB, NBW, false>(acc, wave * NBW, a.mlp.lin[D - 1].b, L, Yf, Lay::LDY);
+      }
+      __syncthreads();
+      ln_normalise<TE, L>(XH, Lay::LDY, a.eps, RS);
+      __syncthreads();
+      if (tid < L) {
+        for (int r = 0; r < n; ++r) {
+          const float d = DM[r * Lay::LDM + tid];
+          g_gamma += d * XH[r * Lay::LDY + tid];
+          g_beta += d;
+        }
+      }
+      __syncthreads();
+      ln_backward<P, TE, L>(DM, Lay::LDM, XH, Lay::LDY, RS, a.mlp.gamma, DY, Lay::LDA);
+      __syncthreads();
+      if (tid < L) g_blast += col_sum(DM, Lay::LDM, n, tid);
+      {
+        T* dl = reinterpret_cast<T*>(a.delta[D - 1]);
+        T* h0 = reinterpret_cast<T*>(a.hid[0]);
+        for (int i = tid; i < n * L; i += NT) {
+          const int r = i / L, c = i % L;
+          dl[(sb + r) * L + c] = DY[r * Lay::LDA + c];
+          h0[(sb + r) * L + c] = HB[r * Lay::LDH + c];
+          if constexpr (D == 3) reinterpret_cast<T*>(a.hid[1])[(sb + r) * L + c] = HC[r * Lay::LDH + c];
+        }
+      }
+#pragma unroll
+      for (int j = D - 1; j >= 1; --j) {
+        const T* hprev = (j == 2) ? HC : HB;
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols)
+          wave_gemm<P, MB, NBW>(DY, Lay::LDA, a.mlp.lin[j].wb, a.mlp.lin[j].nkgb, wave * NBW, acc);
+        __syncthreads();
+        if (wave_has_cols) {
+#pragma unroll
+          for (int nn = 0; nn < NBW; ++nn)
+#pragma unroll
+            for (int m = 0; m < MB; ++m)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int row = m * 16 + acc_row(r), col = (wave * NBW + nn) * 16 + acc_col();
+                const float h = P::tof(hprev[row * Lay::LDH + col]);
+                acc[m][nn][r] = h > 0.f ? acc[m][nn][r] : 0.f;
+                DY[row * Lay::LDA + col] = P::cvt(acc[m][nn][r]);
+              }
+          float cs[NBW];
+          acc_colsum<MB, NBW>(acc, cs);
+#pragma unroll
+          for (int nn = 0; nn < NBW; ++nn) g_bh[j - 1][nn] += cs[nn];
+        }
+        __syncthreads();
+        T* dj = reinterpret_cast<T*>(a.delta[j - 1]);
+        for (int i = tid; i < n * L; i += NT) {
+          const int r = i / L, c = i % L;
+          dj[(sb + r) * L + c] = DY[r * Lay::LDA + c];
+        }
+      }
+      // input gradient [d e | d v_s | d v_r] = dz_1 W_1, one L-wide pass each
+#pragma unroll
+      for (int pass = 0; pass < 3; ++pass) {
+        floatx4 acc[MB][NBW];
+        if (wave_has_cols)
+          wave_gemm<P, MB, NBW>(DY, Lay::LDA, a.mlp.lin[0].wb, a.mlp.lin[0].nkgb, pass * (L / 16) + wave * NBW,
+                                acc);
+        __syncthreads();
+        if (wave_has_cols) store_acc<P, MB, NBW, false>(acc, wave * NBW, nullptr, L, DM, Lay::LDM);
+        __syncthreads();
+        if (pass < 2) {
+          float* dst = pass == 0 ? a.de_out : a.g;
+          for (int i = tid; i < n * Q; i += NT) {
+            const int r = i / Q, c4 = i % Q;
+            float4 v = *reinterpret_cast<const float4*>(DM + r * Lay::LDM + c4 * 4);
+            if (pass == 0 && a.de_next) {
+              const float4 d = reinterpret_cast<const float4*>(a.de_next + (sb + r) * L)[c4];
+              v.x += d.x;
+              v.y += d.y;
+              v.z += d.z;
+              v.w += d.w;
+            }
+            reinterpret_cast<float4*>(dst + (sb + r) * L)[c4] = v;
+          }
+        } else {
+          for (int c = tid; c < L; c += NT) {
+            for (int r = 0; r < n; ++r) {
+              run += DM[r * Lay::LDM + c];
+              if (last[r]) {
+                a.dv[(int64_t)rr[r] * L + c] += run;
+                run = 0.f;
+              }
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
+  }
+  float* vp = a.vpart + (int64_t)blockIdx.x * a.nvec;
+  if (wave_has_cols && (threadIdx.x & 63) < 16) {
+#pragma unroll
+    for (int j = 0; j < D - 1; ++j)
+#pragma unroll
+      for (int nn = 0; nn < NBW; ++nn) vp[j * L + (wave * NBW + nn) * 16 + (threadIdx.x & 15)] = g_bh[j][nn];
+  }
+  const int off_last = (D - 1) * L;
+  if (tid < L) {
+    vp[off_last + tid] = g_blast;
+    vp[off_last + L + tid] = g_gamma;
+    vp[off_last + 2 * L + tid] = g_beta;
+  }
+}
+
+// ------------------------------------------------------- sender gather ---
+// dv[n] += sum of g[e] over the local edges sent by n, ascending e (owned n);
+// dh[n - n_owned] = the same sum (halo n).  L/4 threads per node.
+__global__ __launch_bounds__(NT) void sender_gather_kernel(int64_t n_local, int64_t n_owned,
+                                                           const int32_t* __restrict__ trow,
+                                                           const int32_t* __restrict__ tedge,
+                                                           const float* __restrict__ g, float* __restrict__ dv,
+                                                           float* __restrict__ dh, int L) {
+  const int Q = L / 4;
+  const int per = NT / Q;
+  const int64_t node = (int64_t)blockIdx.x * per + threadIdx.x / Q;
+  const int c4 = threadIdx.x % Q;
+  if (threadIdx.x / Q >= per || node >= n_local) return;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int32_t i = trow[node]; i < trow[node + 1]; ++i) {
+    const float4 v = reinterpret_cast<const float4*>(g + (int64_t)tedge[i] * L)[c4];
+    s.x += v.x;
+    s.y += v.y;
+    s.z += v.z;
+    s.w += v.w;
+  }
+  if (node < n_owned) {
+    float4* d = reinterpret_cast<float4*>(dv + node * L) + c4;
+    float4 v = *d;
+    v.x += s.x;
+    v.y += s.y;
+    v.z += s.z;
+    v.w += s.w;
+    *d = v;
+  } else if (dh) {
+    reinterpret_cast<float4*>(dh + (node - n_owned) * L)[c4] = s;
+  }
+}
+
+// -------------------------------------------------- weight gradients ---
+// part[s][o][i] = sum over rows of split s of delta[row][o] * A[row][i], as an
+// MFMA GEMM with both operands staged transposed in LDS (rows contiguous).
+constexpr int DW_TO = 128, DW_TI = 128, DW_RC = 64;
+
+template <class P>
+__device__ __forceinline__ void dw_load_a(const DwArgs& a, int64_t row, int col, float* v /*EL values*/) {
+  using T = typename P::T;
+  if (a.a_kind == 0) {
+    const T* src = reinterpret_cast<const T*>(a.a0) + row * a.lda0 + col;
+#pragma unroll
+    for (int e = 0; e < P::EL; ++e) v[e] = P::tof(src[e]);
+  } else if (a.a_kind == 1) {
+    const float* src = reinterpret_cast<const float*>(a.a0) + row * a.lda0 + col;
+#pragma unroll
+    for (int e = 0; e < P::EL; ++e) v[e] = (col + e < a.lda0) ? src[e] : 0.f;
+  } else if (a.a_kind == 2) {
+    const int L = a.L;
+    const float* src;
+    if (col < L) {
+      const T* s = reinterpret_cast<const T*>(a.a0) + row * L + col;
+#pragma unroll
+      for (int e = 0; e < P::EL; ++e) v[e] = P::tof(s[e]);
+      return;
+    } else if (col < 2 * L) {
+      const int64_t snd = a.send[row];
+      src = snd < a.n_owned ? a.a1 + snd * L : a.a2 + (snd - a.n_owned) * L;
+      src += col - L;
+    } else {
+      src = a.a1 + (int64_t)a.erecv[row] * L + (col - 2 * L);
+    }
+#pragma unroll
+    for (int e = 0; e < P::EL; ++e) v[e] = P::tof(P::cvt(src[e]));
+  } else {
+    const int L = a.L;
+    const float* src = (col < L ? reinterpret_cast<const float*>(a.a0) + row * L + col : a.a1 + row * L + (col - L));
+#pragma unroll
+    for (int e = 0; e < P::EL; ++e) v[e] = P::tof(P::cvt(src[e]));
+  }
+}
+
+template <int P_>
+__global__ __launch_bounds__(NT) void dw_kernel(DwArgs a) {
+  using P = typename PrecOf<P_>::type;
+  using T = typename P::T;
+  constexpr int LDT = DW_RC + P::PAD;
+  __shared__ __align__(16) T Dt[DW_TO * LDT];
+  __shared__ __align__(16) T At[DW_TI * LDT];
+  const int ot = blockIdx.x, itl = blockIdx.y, s = blockIdx.z;
+  const int o0 = ot * DW_TO, i0 = itl * DW_TI;
+  const int64_t per = (a.R + a.S - 1) / a.S;
+  const int64_t rb = (int64_t)s * per, re = rb + per < a.R ? rb + per : a.R;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wo = (wave >> 1) * 64, wi = (wave & 1) * 64;  // this wave's 64x64 quadrant
+  floatx4 acc[4][4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int n = 0; n < 4; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const T* dl = reinterpret_cast<const T*>(a.delta);
+  for (int64_t c0 = rb; c0 < re; c0 += DW_RC) {
+    // stage transposed: Dt[o][r] = delta[c0 + r][o0 + o], At[i][r] = A[c0 + r][i0 + i]
+    constexpr int GPR = DW_TO / P::EL;  // EL-wide groups per row
+    for (int idx = threadIdx.x; idx < DW_RC * GPR; idx += NT) {
+      const int r = idx / GPR, g = (idx % GPR) * P::EL;
+      const int64_t row = c0 + r;
+      const bool ok = row < re;
+#pragma unroll
+      for (int e = 0; e < P::EL; ++e) {
+        const int o = o0 + g + e;
+        Dt[(g + e) * LDT + r] = (ok && o < a.O) ? dl[row * a.ldd + o] : P::cvt(0.f);
+      }
+      float v[P::EL];
+      const int i = i0 + g;
+      if (ok && i < a.I) {
+        dw_load_a<P>(a, row, i, v);
+      } else {
+#pragma unroll
+        for (int e = 0; e < P::EL; ++e) v[e] = 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < P::EL; ++e) At[(g + e) * LDT + r] = P::cvt((i + e < a.I) ? v[e] : 0.f);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kg = 0; kg < DW_RC / P::KG; ++kg) {
+      uint4 af[4], bf[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+        af[m] = *reinterpret_cast<const uint4*>(Dt + (wo + m * 16 + (lane & 15)) * LDT + kg * P::KG +
+                                                (lane >> 4) * P::EL);
+#pragma unroll
+      for (int n = 0; n < 4; ++n)
+        bf[n] = *reinterpret_cast<const uint4*>(At + (wi + n * 16 + (lane & 15)) * LDT + kg * P::KG +
+                                                (lane >> 4) * P::EL);
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 4; ++n) P::mma(acc[m][n], af[m], bf[n]);
+    }
+    __syncthreads();
+  }
+  float* dst = a.part + (int64_t)s * a.O * a.I;
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int o = o0 + wo + m * 16 + acc_row(r), i = i0 + wi + n * 16 + acc_col();
+        if (o < a.O && i < a.I) dst[(int64_t)o * a.I + i] = acc[m][n][r];
+      }
+}
+
+__global__ void dw_reduce_kernel(const float* __restrict__ part, int S, int64_t n, float* __restrict__ dst,
+                                 int accumulate) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = accumulate ? dst[i] : 0.f;
+  float t = 0.f;
+  for (int k = 0; k < S; ++k) t += part[(int64_t)k * n + i];
+  dst[i] = s + t;
+}
+
+struct VecSegs {
+  VecSeg s[4];
+  int n;
+};
+
+__global__ void vec_reduce_kernel(const float* __restrict__ vpart, int nwg, int nvec, VecSegs segs,
+                                  float* __restrict__ dparams, int accumulate) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= nvec) return;
+  float t = 0.f;
+  for (int w = 0; w < nwg; ++w) t += vpart[(int64_t)w * nvec + i];
+  for (int k = 0; k < segs.n; ++k) {
+    const VecSeg& sg = segs.s[k];
+    if (i >= sg.vec_off && i < sg.vec_off + sg.len) {
+      float* d = dparams + sg.param_off + (i - sg.vec_off);
+      *d = (accumulate ? *d : 0.f) + t;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ loss ---
+// Masked mean squared error: one workgroup sums count and squared error in a
+// fixed order (double), then every element's gradient is written.
+__global__ __launch_bounds__(NT) void mse_loss_kernel(const float* __restrict__ out, const float* __restrict__ tgt,
+                                                      const uint8_t* __restrict__ mask, int64_t n, int d,
+                                                      float* __restrict__ loss, float* __restrict__ scale) {
+  __shared__ double ss[NT];
+  __shared__ int64_t sc[NT];
+  double s = 0.0;
+  int64_t cnt = 0;
+  for (int64_t i = threadIdx.x; i < n; i += NT) {
+    if (mask && !mask[i]) continue;
+    ++cnt;
+    for (int j = 0; j < d; ++j) {
+      const double df = (double)out[i * d + j] - (double)tgt[i * d + j];
+      s += df * df;
+    }
+  }
+  ss[threadIdx.x] = s;
+  sc[threadIdx.x] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    int64_t c = 0;
+    for (int i = 0; i < NT; ++i) {
+      t += ss[i];
+      c += sc[i];
+    }
+    const double den = (double)c * d;
+    *loss = c > 0 ? (float)(t / den) : 0.f;
+    *scale = c > 0 ? (float)(2.0 / den) : 0.f;
+  }
+}
+
+__global__ void mse_grad_kernel(const float* __restrict__ out, const float* __restrict__ tgt,
+                                const uint8_t* __restrict__ mask, int64_t n, int d, const float* __restrict__ scale,
+                                float* __restrict__ d_out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n * d) return;
+  const int64_t row = i / d;
+  const bool on = mask ? mask[row] != 0 : true;
+  d_out[i] = on ? (out[i] - tgt[i]) * *scale : 0.f;
+}
+
+// ============================================================ launchers ===
+int edge_tile_rows(int prec, int L, int D) {
+#define ETR(PP, LL, DD) \
+  if (prec == PP && L == LL && D == DD) return EdgeTE<typename PrecOf<PP>::type, LL, DD>::value;
+  ETR(F32, 64, 2) ETR(F32, 64, 3) ETR(F32, 128, 2) ETR(F32, 128, 3) ETR(F32, 256, 2) ETR(F32, 256, 3)
+  ETR(BF16, 64, 2) ETR(BF16, 64, 3) ETR(BF16, 128, 2) ETR(BF16, 128, 3) ETR(BF16, 256, 2) ETR(BF16, 256, 3)
+#undef ETR
+  return 0;
+}
+
+hipError_t launch_pack(int prec, const float* W, int out, int in, int bwd, uint4* dst, int nkg, hipStream_t st) {
+  const int nblk = ((bwd ? in : out) + 15) / 16;
+  const int64_t total = (int64_t)nblk * nkg * 64;
+  const int grid = (int)((total + NT - 1) / NT);
+  if (prec == F32)
+    hipLaunchKernelGGL(pack_kernel<PF32>, dim3(grid), dim3(NT), 0, st, W, out, in, bwd, dst, nkg, total);
+  else
+    hipLaunchKernelGGL(pack_kernel<PBF16>, dim3(grid), dim3(NT), 0, st, W, out, in, bwd, dst, nkg, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_erecv(const int32_t* row_ptr, int64_t n_owned, int32_t* erecv, hipStream_t st) {
+  if (n_owned == 0) return hipSuccess;
+  hipLaunchKernelGGL(erecv_kernel, dim3((unsigned)((n_owned + NT - 1) / NT)), dim3(NT), 0, st, row_ptr, n_owned,
+                     erecv);
+  return hipGetLastError();
+}
+
+int64_t plan_chunks(int64_t n_owned) { return (n_owned + PLAN_CHUNK - 1) / PLAN_CHUNK; }
+
+int64_t plan_max_units(int64_t n_owned, int64_t n_edges, int te_target, int r_max) {
+  // a closed unit plus the receiver that closed it exceeds te_target edges or
+  // r_max receivers, so two consecutive units hold more than min(te_target,
+  // r_max) of edges+receivers; each chunk adds at most one partial unit.
+  const int64_t lim = te_target < r_max ? te_target : r_max;
+  return 2 * (n_owned + n_edges) / lim + 2 * plan_chunks(n_owned) + 2;
+}
+
+hipError_t launch_plan(const int32_t* row_ptr, int64_t n_owned, int te_target, int r_max, int32_t* chunk_cnt,
+                       int32_t* unit_r, int32_t* n_units, hipStream_t st) {
+  const int64_t nch = plan_chunks(n_owned);
+  if (nch == 0) {
+    // no receivers: zero units, unit_r[0] = 0
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, st, n_units, (int64_t)1, 0);
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, st, unit_r, (int64_t)1, 0);
+    return hipGetLastError();
+  }
+  const unsigned g = (unsigned)((nch + NT - 1) / NT);
+  hipLaunchKernelGGL(plan_count_kernel, dim3(g), dim3(NT), 0, st, row_ptr, n_owned, te_target, r_max, chunk_cnt,
+                     nch);
+  hipLaunchKernelGGL(plan_scan_kernel, dim3(1), dim3(NT), 0, st, chunk_cnt, nch, n_units);
+  hipLaunchKernelGGL(plan_write_kernel, dim3(g), dim3(NT), 0, st, row_ptr, n_owned, te_target, r_max, chunk_cnt,
+                     nch, n_units, unit_r);
+  return hipGetLastError();
+}
+
+// Dynamic LDS above 64 KiB must be allowed explicitly per kernel.
+template <class F>
+static void allow_lds(F* fn, int bytes) {
+  if (bytes > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+}
+
+template <int P_, int L, int D, int KIND>
+static hipError_t rows_fwd_t(const RowsFwdArgs& a, hipStream_t st) {
+  using P = typename PrecOf<P_>::type;
+  constexpr int TM = RowTM<P, KIND, L, D>::value;
+  using Lay = RowLds<P, KIND, L, D, TM>;
+  const int64_t ntiles = (a.rows + TM - 1) / TM;
+  if (ntiles == 0) return hipSuccess;
+  const int grid = (int)(ntiles < 4096 ? ntiles : 4096);
+  allow_lds(rows_fwd_kernel<P_, L, D, KIND>, Lay::END_F);
+  hipLaunchKernelGGL((rows_fwd_kernel<P_, L, D, KIND>), dim3(grid), dim3(NT), Lay::END_F, st, a);
+  return hipGetLastError();
+}
+
+template <int P_, int L, int D, int KIND>
+static hipError_t rows_bwd_t(const RowsBwdArgs& a, int grid, hipStream_t st) {
+  using P = typename PrecOf<P_>::type;
+  constexpr int TM = RowTM<P, KIND, L, D>::value;
+  using Lay = RowLds<P, KIND, L, D, TM>;
+  allow_lds(rows_bwd_kernel<P_, L, D, KIND>, Lay::END_B);
+  hipLaunchKernelGGL((rows_bwd_kernel<P_, L, D, KIND>), dim3(grid), dim3(NT), Lay::END_B, st, a);
+  return hipGetLastError();
+}
+
+template <int P_, int L, int D>
+static hipError_t edge_fwd_t(const EdgeFwdArgs& a, int grid, hipStream_t st) {
+  using P = typename PrecOf<P_>::type;
+  using Lay = EdgeLds<P, L, D, EdgeTE<P, L, D>::value>;
+  allow_lds(edge_fwd_kernel<P_, L, D>, Lay::END_F);
+  hipLaunchKernelGGL((edge_fwd_kernel<P_, L, D>), dim3(grid), dim3(NT), Lay::END_F, st, a);
+  return hipGetLastError();
+}
+
+template <int P_, int L, int D>
+static hipError_t edge_bwd_t(const EdgeBwdArgs& a, int grid, hipStream_t st) {
+  using P = typename PrecOf<P_>::type;
+  using Lay = EdgeLds<P, L, D, EdgeTE<P, L, D>::value>;
+  allow_lds(edge_bwd_kernel<P_, L, D>, Lay::END);
+  hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D>), dim3(grid), dim3(NT), Lay::END, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st) {
+#define RF(PP, LL, DD)                                                                      \
+  if (prec == PP && L == LL && D == DD) {                                                   \
+    switch (kind) {                                                                         \
+      case ENC_NODE: return rows_fwd_t<PP, LL, DD, ENC_NODE>(a, st);                        \
+      case ENC_EDGE: return rows_fwd_t<PP, LL, DD, ENC_EDGE>(a, st);                        \
+      case NODE_BLOCK: return rows_fwd_t<PP, LL, DD, NODE_BLOCK>(a, st);                    \
+      default: return rows_fwd_t<PP, LL, DD, DECODER>(a, st);                               \
+    }                                                                                       \
+  }
+  RF(F32, 64, 2) RF(F32, 64, 3) RF(F32, 128, 2) RF(F32, 128, 3) RF(F32, 256, 2) RF(F32, 256, 3)
+  RF(BF16, 64, 2) RF(BF16, 64, 3) RF(BF16, 128, 2) RF(BF16, 128, 3) RF(BF16, 256, 2) RF(BF16, 256, 3)
+#undef RF
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st) {
+#define RB(PP, LL, DD)                                                                      \
+  if (prec == PP && L == LL && D == DD) {                                                   \
+    switch (kind) {                                                                         \
+      case ENC_NODE: return rows_bwd_t<PP, LL, DD, ENC_NODE>(a, grid, st);                  \
+      case ENC_EDGE: return rows_bwd_t<PP, LL, DD, ENC_EDGE>(a, grid, st);                  \
+      case NODE_BLOCK: return rows_bwd_t<PP, LL, DD, NODE_BLOCK>(a, grid, st);              \
+      default: return rows_bwd_t<PP, LL, DD, DECODER>(a, grid, st);                         \
+    }                                                                                       \
+  }
+  RB(F32, 64, 2) RB(F32, 64, 3) RB(F32, 128, 2) RB(F32, 128, 3) RB(F32, 256, 2) RB(F32, 256, 3)
+  RB(BF16, 64, 2) RB(BF16, 64, 3) RB(BF16, 128, 2) RB(BF16, 128, 3) RB(BF16, 256, 2) RB(BF16, 256, 3)
+#undef RB
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int grid, hipStream_t st) {
+#define EF(PP, LL, DD) \
+  if (prec == PP && L == LL && D == DD) return edge_fwd_t<PP, LL, DD>(a, grid, st);
+  EF(F32, 64, 2) EF(F32, 64, 3) EF(F32, 128, 2) EF(F32, 128, 3) EF(F32, 256, 2) EF(F32, 256, 3)
+  EF(BF16, 64, 2) EF(BF16, 64, 3) EF(BF16, 128, 2) EF(BF16, 128, 3) EF(BF16, 256, 2) EF(BF16, 256, 3)
+#undef EF
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int grid, hipStream_t st) {
+#define EB(PP, LL, DD) \
+  if (prec == PP && L == LL && D == DD) return edge_bwd_t<PP, LL, DD>(a, grid, st);
+  EB(F32, 64, 2) EB(F32, 64, 3) EB(F32, 128, 2) EB(F32, 128, 3) EB(F32, 256, 2) EB(F32, 256, 3)
+  EB(BF16, 64, 2) EB(BF16, 64, 3) EB(BF16, 128, 2) EB(BF16, 128, 3) EB(BF16, 256, 2) EB(BF16, 256, 3)
+#undef EB
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_sender_gather(int64_t n_local, int64_t n_owned, const int32_t* trow, const int32_t* tedge,
+                                const float* g, float* dv, float* dh, int L, hipStream_t st) {
+  if (n_local == 0) return hipSuccess;
+  const int per = NT / (L / 4);
+  const unsigned grid = (unsigned)((n_local + per - 1) / per);
+  hipLaunchKernelGGL(sender_gather_kernel, dim3(grid), dim3(NT), 0, st, n_local, n_owned, trow, tedge, g, dv, dh, L);
+  return hipGetLastError();
+}
+
+int dw_splits(int64_t R, int O, int I) {
+  const int64_t tiles = (int64_t)((O + DW_TO - 1) / DW_TO) * ((I + DW_TI - 1) / DW_TI);
+  int64_t s = 2048 / tiles;
+  const int64_t by_rows = (R + 4 * DW_RC - 1) / (4 * DW_RC);  // at least 4 chunks per split
+  if (s > by_rows) s = by_rows;
+  if (s < 1) s = 1;
+  return (int)s;
+}
+
+hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st) {
+  dim3 grid((a.O + DW_TO - 1) / DW_TO, (a.I + DW_TI - 1) / DW_TI, a.S);
+  if (prec == F32)
+    hipLaunchKernelGGL(dw_kernel<F32>, grid, dim3(NT), 0, st, a);
+  else
+    hipLaunchKernelGGL(dw_kernel<BF16>, grid, dim3(NT), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int accumulate, hipStream_t st) {
+  const int64_t n = (int64_t)O * I;
+  hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)((n + NT - 1) / NT)), dim3(NT), 0, st, part, S, n, dst,
+                     accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_vec_reduce(const float* vpart, int nwg, int nvec, const VecSeg* segs, int nseg, float* dparams,
+                             int accumulate, hipStream_t st) {
+  VecSegs s;
+  s.n = nseg;
+  for (int i = 0; i < nseg && i < 4; ++i) s.s[i] = segs[i];
+  hipLaunchKernelGGL(vec_reduce_kernel, dim3((nvec + NT - 1) / NT), dim3(NT), 0, st, vpart, nwg, nvec, s, dparams,
+                     accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_mse(const float* out, const float* target, const uint8_t* mask, int64_t n, int d, float* loss,
+                      float* d_out, hipStream_t st) {
+  // loss[1] doubles as scratch for the gradient scale: scale is written to loss+1
+  hipLaunchKernelGGL(mse_loss_kernel, dim3(1), dim3(NT), 0, st, out, target, mask, n, d, loss, loss + 1);
+  if (n > 0)
+    hipLaunchKernelGGL(mse_grad_kernel, dim3((unsigned)((n * d + NT - 1) / NT)), dim3(NT), 0, st, out, target, mask,
+                       n, d, loss + 1, d_out);
+  return hipGetLastError();
+}
+
+}  // namespace mgn

@@ -1,0 +1,71 @@
+"""Device-side session for one partition: uploads a host-built local graph and
+its inputs to HBM once, then runs the training step through the C ABI.
+Argument marshalling only; the step itself runs in libmgn's kernels."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import (MGN_BF16, MGN_FP32, graph_struct, mgn_backward, mgn_create, mgn_destroy, mgn_forward,
+               mgn_graph_validate, mgn_mse_grad, mgn_param_count, mgn_set_params, mgn_workspace_size)
+
+
+class Session:
+    def __init__(self, latent: int, K: int, depth: int, precision: str, graph: dict, node_feat, edge_feat, halo,
+                 params, device: str = "cuda", node_in: int = 11, edge_in: int = 4, node_out: int = 5):
+        if not torch.cuda.is_available():
+            raise RuntimeError("libmgn needs a HIP device")
+        self.device = torch.device(device)
+        self.K, self.latent = K, latent
+        prec = MGN_BF16 if precision == "bf16" else MGN_FP32
+        self.model = mgn_create(latent, K, depth, prec, node_in, edge_in, node_out)
+        dev = lambda a, dt: torch.as_tensor(np.ascontiguousarray(a, dtype=dt)).to(self.device)
+        self.g = dict(n_owned=int(graph["n_owned"]), n_halo=int(graph["n_halo"]), n_edges=int(graph["n_edges"]),
+                      row_ptr=dev(graph["row_ptr"], np.int32), send=dev(graph["send"], np.int32),
+                      trow_ptr=dev(graph["trow_ptr"], np.int32), tedge=dev(graph["tedge"], np.int32))
+        self.gs = graph_struct(self.g)
+        no, nh, ne = self.g["n_owned"], self.g["n_halo"], self.g["n_edges"]
+        self.node_feat = dev(np.asarray(node_feat).reshape(no, node_in), np.float32)
+        self.edge_feat = dev(np.asarray(edge_feat).reshape(ne, edge_in), np.float32)
+        self.halo = dev(halo, np.float32) if (nh > 0 and K > 0) else None
+        self.n_params = mgn_param_count(self.model)
+        self.set_params(params)
+        mgn_graph_validate(self.model, self.gs)
+        self.ws_bytes = mgn_workspace_size(self.model, self.gs)
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=self.device)
+        self.out = torch.empty((no, node_out), dtype=torch.float32, device=self.device)
+        self.d_params = torch.empty(self.n_params, dtype=torch.float32, device=self.device)
+        self.d_halo = torch.empty((K, nh, latent), dtype=torch.float32, device=self.device) if (nh and K) else None
+
+    def set_params(self, params):
+        if isinstance(params, torch.Tensor):
+            mgn_set_params(self.model, params.to(self.device, torch.float32).contiguous())
+        else:
+            mgn_set_params(self.model, np.asarray(params, np.float32))
+
+    def forward(self, stream=None):
+        mgn_forward(self.model, self.gs, self.node_feat, self.edge_feat, self.halo, self.out, self.workspace, stream)
+        return self.out
+
+    def backward(self, d_out, accumulate: bool = False, stream=None):
+        if not isinstance(d_out, torch.Tensor):
+            d_out = torch.as_tensor(np.ascontiguousarray(d_out, np.float32)).to(self.device)
+        mgn_backward(self.model, d_out.contiguous(), self.d_params, accumulate, self.d_halo, stream)
+        return self.d_params, self.d_halo
+
+    def mse(self, target, mask=None, stream=None):
+        loss = torch.empty(2, dtype=torch.float32, device=self.device)
+        d_out = torch.empty_like(self.out)
+        mgn_mse_grad(self.out, target, mask, loss, d_out, stream)
+        return loss, d_out
+
+    def close(self):
+        if self.model:
+            mgn_destroy(self.model)
+            self.model = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,145 @@
+"""GPU parity at sizes the oracle runs in seconds: every output, every
+parameter-gradient tensor and the halo gradient of libmgn's fwd+bwd against
+the oracle on the same seeded inputs (max relative error per tensor <= 1e-4
+fp32 against the float64 oracle, <= 2e-2 bf16 against the oracle's
+mixed-precision mode, which rounds to bfloat16 where the kernels do), plus the edge cases: K = 0, no edges, receivers
+without edges, receivers with more edges than one tile, ragged tails, halos
+on one or two sides; bitwise determinism and exact linearity of the backward."""
+import numpy as np
+import pytest
+
+import synth
+from synth import meshes
+import paper_2307_13592_amd as mgn
+from parity import TOL, compare, local_inputs, rel_err, run_gpu, run_oracle, say
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(name, mesh, p, l, K, D, prec, seed=3, part=None):
+    say(f"[parity] {name} l={l} K={K} D={D} {prec}")
+    c = local_inputs(mesh, p, l, K, D, seed, part)
+    gpu = run_gpu(c, l, K, D, prec)
+    ref = run_oracle(c, l, K, D, bf16=prec == "bf16")
+    bad = compare(name, prec, c["shapes"], gpu, ref)
+    assert not bad, bad
+    if prec == "bf16":
+        # the outputs also stay within the bf16 tolerance of the float64 network
+        ref64 = run_oracle(c, l, K, D)
+        e = rel_err(gpu[0], ref64["out"])
+        say(f"  outputs vs float64 network: {e:.2e}")
+        assert e <= TOL["bf16"]
+
+
+def test_c1_full():
+    cfg = synth.CONFIGS["C1"]
+    _case("C1 hex16", cfg.build_mesh(False), 0, cfg.latent, cfg.K, cfg.depth, cfg.precision, seed=cfg.seed)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+@pytest.mark.parametrize("l,D", [(64, 2), (128, 2), (128, 3), (256, 2), (256, 3), (64, 3)])
+def test_sector_partition(prec, l, D):
+    """Interior slab (halo on both sides), several tiles and a ragged tail."""
+    _case("sector 6x16x10 p1", meshes.sector(6, 16, 10, 4, seed=7), 1, l, 3, D, prec)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_sector_edge_slab(prec):
+    """First slab: halo on one side only."""
+    _case("sector 5x12x9 p0", meshes.sector(5, 12, 9, 4, seed=2), 0, 128, 2, 2, prec)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_delaunay(prec):
+    """Unstructured tets: irregular in-degrees up to ~40."""
+    _case("delaunay 12x11x10", meshes.delaunay_box(12, 11, 10, seed=4), 0, 128, 2, 2, prec)
+
+
+def _with_edges(mesh, keep):
+    m = meshes.Mesh(**{**mesh.__dict__})
+    m.send, m.recv = mesh.send[keep], mesh.recv[keep]
+    return m
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_receivers_without_edges(prec):
+    m = meshes.hex_lattice(7)
+    keep = (m.recv % 5) != 0          # every 5th node receives nothing
+    _case("hex7 isolated receivers", _with_edges(m, keep), 0, 64, 2, 2, prec)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_large_in_degree(prec):
+    """Hub receivers with 300 in-edges: one receiver spans several sub-tiles."""
+    m = meshes.hex_lattice(8)
+    rng = np.random.default_rng(3)
+    extra_s, extra_r = [], []
+    for hub in (17, 200, 511):
+        src = rng.choice(np.setdiff1d(np.arange(m.n_nodes), [hub]), 300, replace=False)
+        extra_s.append(src)
+        extra_r.append(np.full(300, hub))
+    s = np.concatenate([m.send] + extra_s).astype(np.int32)
+    r = np.concatenate([m.recv] + extra_r).astype(np.int32)
+    key = s.astype(np.int64) * m.n_nodes + r
+    _, first = np.unique(key, return_index=True)
+    first = np.sort(first)
+    mm = meshes.Mesh(**{**m.__dict__})
+    mm.send, mm.recv = s[first], r[first]
+    _case("hex8 + 3 hubs", mm, 0, 128, 2, 2, prec)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_no_edges(prec):
+    m = meshes.hex_lattice(4)
+    _case("hex4 no edges", _with_edges(m, np.zeros(m.n_edges, bool)), 0, 64, 2, 2, prec)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_zero_blocks(prec):
+    _case("hex5 K=0", meshes.hex_lattice(5), 0, 64, 0, 3, prec)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_determinism_and_linearity(prec):
+    say(f"[parity] determinism/linearity {prec}")
+    c = local_inputs(meshes.sector(6, 16, 10, 4, seed=7), 1, 128, 3, 2, 5)
+    a = run_gpu(c, 128, 3, 2, prec)
+    b = run_gpu(c, 128, 3, 2, prec)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y), "two runs differ"
+    two = run_gpu(c, 128, 3, 2, prec, d_out=2.0 * c["d_out"])
+    assert np.array_equal(two[1], 2.0 * a[1]) and np.array_equal(two[2], 2.0 * a[2])
+    zero = run_gpu(c, 128, 3, 2, prec, d_out=0.0 * c["d_out"])
+    assert not np.any(zero[1]) and not np.any(zero[2])
+
+
+def test_accumulate_and_param_roundtrip():
+    say("[parity] accumulate")
+    from paper_2307_13592_amd.runner import Session
+    c = local_inputs(meshes.sector(5, 12, 9, 4, seed=2), 1, 64, 2, 2, 6)
+    s = Session(64, 2, 2, "fp32", c["g"], c["nf"], c["ef"], c["halo"], c["params"])
+    try:
+        assert np.array_equal(mgn.mgn_get_params(s.model), c["params"])
+        s.forward()
+        g1 = s.backward(c["d_out"])[0].cpu().numpy().copy()
+        g2 = s.backward(c["d_out"], accumulate=True)[0].cpu().numpy().copy()
+        assert np.array_equal(g2, 2.0 * g1)
+    finally:
+        s.close()
+
+
+def test_mse_grad():
+    import torch
+    say("[parity] mse")
+    rng = np.random.default_rng(4)
+    out = rng.standard_normal((1000, 5)).astype(np.float32)
+    tgt = rng.standard_normal((1000, 5)).astype(np.float32)
+    mask = (rng.random(1000) < 0.7).astype(np.uint8)
+    L, d = oracle.mse_grad(out.astype(np.float64), tgt.astype(np.float64), mask)
+    dev = lambda a: torch.as_tensor(a).cuda()
+    loss = torch.empty(2, device="cuda")
+    dout = torch.empty((1000, 5), device="cuda")
+    mgn.mgn_mse_grad(dev(out), dev(tgt), dev(mask), loss, dout)
+    assert abs(loss[0].item() - L) / L < 1e-6
+    assert rel_err(dout.cpu().numpy(), d) < 1e-6

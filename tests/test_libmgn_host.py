@@ -1,0 +1,130 @@
+"""libmgn without a GPU: the shared library loads and exports every entry
+point include/mgn.h declares; its host-side graph preprocessing agrees bit
+for bit with the oracle's; parameter layout sizes agree; argument and state
+errors are reported before anything is launched."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth import meshes
+import paper_2307_13592_amd as mgn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_exports_every_declared_symbol():
+    hdr = open(os.path.join(ROOT, "include", "mgn.h")).read()
+    declared = set(re.findall(r"^\S[^;(]*?\b(mgn_\w+)\s*\(", hdr, re.M))
+    assert declared == set(mgn.EXPORTS)
+    L = mgn.lib()
+    for name in declared:
+        assert getattr(L, name) is not None
+
+
+@pytest.mark.parametrize("mesh,P", [
+    (meshes.hex_lattice(6), 1),
+    (meshes.sector(4, 12, 5, 4, seed=1), 4),
+    (meshes.sector(6, 16, 10, 4, seed=7), 4),
+    (meshes.delaunay_box(8, 7, 6, seed=3), 1),
+])
+def test_graph_build_matches_oracle(mesh, P):
+    part_o = oracle.partition(mesh.key, P)
+    part_m = mgn.mgn_partition_slabs(mesh.key, P)
+    assert np.array_equal(part_o, part_m)
+    for p in range(P):
+        go = oracle.graph_build(mesh.send, mesh.recv, part_o, mesh.n_nodes, p)
+        gm = mgn.mgn_graph_build(mesh.send, mesh.recv, part_m, mesh.n_nodes, p)
+        for k in go:
+            assert np.array_equal(np.asarray(go[k]), np.asarray(gm[k])), k
+
+
+def test_graph_build_random_partition_matches_oracle():
+    m = meshes.delaunay_box(9, 8, 7, seed=5)
+    part = np.random.default_rng(1).integers(0, 5, m.n_nodes).astype(np.int32)
+    for p in range(5):
+        go = oracle.graph_build(m.send, m.recv, part, m.n_nodes, p)
+        gm = mgn.mgn_graph_build(m.send, m.recv, part, m.n_nodes, p)
+        for k in go:
+            assert np.array_equal(np.asarray(go[k]), np.asarray(gm[k])), k
+
+
+def test_partition_matches_oracle_wide_keys():
+    rng = np.random.default_rng(2)
+    for n, P, hi in ((1000, 7, 5), (5000, 3, 10 ** 9), (17, 4, 2)):
+        key = rng.integers(-hi, hi, n).astype(np.int32)
+        assert np.array_equal(oracle.partition(key, P), mgn.mgn_partition_slabs(key, P))
+
+
+def test_c3_graph_build_matches_oracle():
+    """The 1M-owned-node slab at full size, bit-exact."""
+    cfg = synth.CONFIGS["C3"]
+    m = cfg.build_mesh(True)
+    go = oracle.graph_build(m.send, m.recv, m.part, m.n_nodes, cfg.part)
+    gm = mgn.mgn_graph_build(m.send, m.recv, m.part, m.n_nodes, cfg.part)
+    for k in go:
+        assert np.array_equal(np.asarray(go[k]), np.asarray(gm[k])), k
+
+
+def test_param_count_matches_oracle_and_layout():
+    for l, K, D in ((64, 2, 2), (128, 15, 2), (256, 15, 3), (64, 0, 3)):
+        h = mgn.mgn_create(l, K, D)
+        try:
+            n = mgn.mgn_param_count(h)
+        finally:
+            mgn.mgn_destroy(h)
+        assert n == oracle.param_count(oracle.ModelCfg(l, K, D))
+        assert n == sum(int(np.prod(s)) for _, _, s in synth.param_shapes(l, K, D))
+
+
+def test_create_rejects_unsupported():
+    for kw in (dict(latent=96), dict(depth=4), dict(node_out=17), dict(node_in=0), dict(precision=7),
+               dict(n_blocks=-1)):
+        args = dict(latent=64, n_blocks=2, depth=2)
+        args.update(kw)
+        with pytest.raises(mgn.MgnError) as e:
+            mgn.mgn_create(**args)
+        assert e.value.status == mgn.MGN_E_UNSUPPORTED
+    with pytest.raises(mgn.MgnError) as e:
+        mgn.mgn_create(64, 2, 2, ln_eps=0.0)
+    assert e.value.status == mgn.MGN_E_ARG
+
+
+def test_graph_errors():
+    m = meshes.hex_lattice(3)
+    part = np.zeros(m.n_nodes, np.int32)
+    bad = m.send.copy()
+    bad[5] = m.n_nodes + 3
+    with pytest.raises(mgn.MgnError) as e:
+        mgn.mgn_graph_sizes(bad, m.recv, part, m.n_nodes, 0)
+    assert e.value.status == mgn.MGN_E_GRAPH
+    with pytest.raises(mgn.MgnError) as e:
+        mgn.mgn_partition_slabs(np.zeros(4, np.int32), 0)
+    assert e.value.status == mgn.MGN_E_ARG
+
+
+def test_state_errors_before_any_launch():
+    """Forward before set_params / validation, backward before forward: the
+    status comes back without touching the device."""
+    import ctypes as C
+    h = mgn.mgn_create(64, 1, 2)
+    try:
+        g = mgn.mgn_graph(4, 0, 0, C.c_void_p(256), C.c_void_p(512), C.c_void_p(768), C.c_void_p(1024))
+        L = mgn.lib()
+        st = L.mgn_forward(h, C.byref(g), None, None, None, None, None, 0, None)
+        assert st == mgn.MGN_E_STATE and "never set" in mgn.mgn_last_error(h)
+        st = L.mgn_backward(h, None, C.c_void_p(256), 0, None, None)
+        assert st == mgn.MGN_E_STATE and "no forward" in mgn.mgn_last_error(h)
+        n = C.c_size_t()
+        assert L.mgn_workspace_size(h, C.byref(g), C.byref(n)) == mgn.MGN_OK and n.value > 0
+        g.n_owned = -1
+        assert L.mgn_workspace_size(h, C.byref(g), C.byref(n)) == mgn.MGN_E_ARG
+        g.n_owned = 4
+        g.row_ptr = C.c_void_p(258)     # misaligned
+        assert L.mgn_workspace_size(h, C.byref(g), C.byref(n)) == mgn.MGN_E_ARG
+    finally:
+        mgn.mgn_destroy(h)
+    assert mgn.lib().mgn_mse_grad(None, None, None, 3, 0, None, None, None) == mgn.MGN_E_ARG

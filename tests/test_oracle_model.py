@@ -51,6 +51,25 @@ def test_matches_torch_layers(name, mk, p, l, K, D):
         assert np.abs(dh).max() > 0
 
 
+@pytest.mark.parametrize("name,mk,p,l,K,D", CASES[:3], ids=[c[0] for c in CASES[:3]])
+def test_bf16_mode_matches_torch_bfloat16(name, mk, p, l, K, D):
+    """The oracle's mixed-precision mode against torch's own bfloat16
+    rounding at the same points (independent formulation)."""
+    c = local_case(mk(), p, l, K, D, seed=3)
+    cfg = oracle.ModelCfg(l, K, D, bf16=True)
+    r = oracle.step(cfg, c["g"], c["params"], c["nf"], c["ef"], c["halo"], c["d_out"])
+    out, dp, dh = torch_ref.run(l, K, D, c["shapes"], c["g"], c["params"], c["nf"], c["ef"], c["halo"],
+                                c["d_out"], bf16=True)
+    assert _rel(r["out"], out) < 1e-12
+    for nm, sl in _segments(c["shapes"]):
+        assert _rel(r["d_params"][sl], dp[sl]) < 1e-10, nm
+    if c["g"]["n_halo"]:
+        assert _rel(r["d_halo"], dh) < 1e-10
+    # and it is a different function from the float64 one
+    r64 = oracle.step(c["cfg"], c["g"], c["params"], c["nf"], c["ef"], c["halo"], c["d_out"])
+    assert _rel(r["out"], r64["out"]) > 1e-5
+
+
 def test_edgeless_K0_is_encoder_then_decoder():
     """K = 0 and no edges: the network is nn.Sequential(encoder, decoder)."""
     l, D = 16, 3

@@ -19,14 +19,14 @@ from cases import local_case
 SRC = os.path.join(os.path.dirname(obuild.LIB), "mgn_oracle.cpp")
 
 MUTATIONS = {
-    "edge_residual_dropped": ("e_next[ed * l + i] = e[ed * l + i] + msg[ed * l + i];",
-                              "e_next[ed * l + i] = msg[ed * l + i];"),
+    "edge_residual_dropped": ("e_next[ed * l + i] = Q.r(e[ed * l + i] + msg[ed * l + i]);",
+                              "e_next[ed * l + i] = Q.r(msg[ed * l + i]);"),
     "sender_receiver_swapped": ("x[l + i] = v[s * l + i];\n      x[2 * l + i] = v[r * l + i];",
                                 "x[l + i] = v[r * l + i];\n      x[2 * l + i] = v[s * l + i];"),
     "unbiased_variance": ("  var /= n;", "  var /= (n - 1);"),
     "node_residual_dropped": ("v_next[r * l + i] = v[r * l + i] + y[i];", "v_next[r * l + i] = y[i];"),
-    "weight_transposed": ("const double* w = P + L.w + (int64_t)o * L.in;\n      for (int i = 0; i < L.in; ++i) s += w[i] * t.a[j][i];",
-                          "for (int i = 0; i < L.in; ++i) s += P[L.w + (int64_t)i * L.out + (o % L.in)] * t.a[j][i];"),
+    "weight_transposed": ("const double* w = Q.W + L.w + (int64_t)o * L.in;\n      for (int i = 0; i < L.in; ++i) s += w[i] * t.a[j][i];",
+                          "for (int i = 0; i < L.in; ++i) s += Q.W[L.w + (int64_t)i * L.out + (o % L.in)] * t.a[j][i];"),
     "halo_block_off_by_one": ("halo[((int64_t)k * n_halo + h) * l + i]",
                               "halo[((int64_t)(k + 1 < K ? k + 1 : k) * n_halo + h) * l + i]"),
     "dagg_dropped": ("dm[i] = de[ed * l + i] + dagg[r * l + i];", "dm[i] = de[ed * l + i];"),

@@ -13,6 +13,51 @@ import torch
 from torch import nn
 
 
+def _bf16(x):
+    return x.to(torch.bfloat16).to(torch.float64)
+
+
+class _LinearBf16(torch.autograd.Function):
+    """Linear with bfloat16 operands (mixed-precision reading): inputs and
+    weights rounded for the product, the incoming gradient rounded before the
+    two gradient products; bias and its gradient exact."""
+
+    @staticmethod
+    def forward(ctx, x, W, b):
+        xr, Wr = _bf16(x), _bf16(W)
+        ctx.save_for_backward(xr, Wr)
+        return xr @ Wr.T + b
+
+    @staticmethod
+    def backward(ctx, dy):
+        xr, Wr = ctx.saved_tensors
+        dyr = _bf16(dy)
+        return dyr @ Wr, dyr.T @ xr, dy.sum(0)
+
+
+class _RoundBf16(torch.autograd.Function):
+    """Storage rounding of the edge-latent stream (gradient passes through)."""
+
+    @staticmethod
+    def forward(ctx, x):
+        return _bf16(x)
+
+    @staticmethod
+    def backward(ctx, g):
+        return g
+
+
+def _apply(seq, x, bf16):
+    if not bf16:
+        return seq(x)
+    for layer in seq:
+        if isinstance(layer, nn.Linear):
+            x = _LinearBf16.apply(x, layer.weight, layer.bias)
+        else:
+            x = layer(x)
+    return x
+
+
 def _mlp(fin, fout, latent, depth, ln):
     dims = [fin] + [latent] * (depth - 1) + [fout]
     layers = []
@@ -62,25 +107,26 @@ class TorchMGN(nn.Module):
         return torch.cat([t.grad.reshape(-1) if t.grad is not None else torch.zeros(t.numel(), dtype=torch.float64)
                           for t in self.ordered_tensors()])
 
-    def forward(self, g, node_feat, edge_feat, halo):
+    def forward(self, g, node_feat, edge_feat, halo, bf16=False):
         """g: partition-local graph (row_ptr, send, n_owned, n_halo).  halo:
         tensor [K, n_halo, l] (requires_grad for d_halo)."""
+        R = (lambda x: _RoundBf16.apply(x)) if bf16 else (lambda x: x)
         no, nh = g["n_owned"], g["n_halo"]
         row_ptr = np.asarray(g["row_ptr"], np.int64)
         recv = torch.as_tensor(np.repeat(np.arange(no), np.diff(row_ptr)), dtype=torch.long)
         send = torch.as_tensor(np.asarray(g["send"], np.int64))
-        v = self.enc_node(node_feat)
-        e = self.enc_edge(edge_feat)
+        v = _apply(self.enc_node, node_feat, bf16)
+        e = R(_apply(self.enc_edge, edge_feat, bf16))
         for k in range(self.K):
             vk = torch.cat([v, halo[k]], 0) if nh > 0 else v
-            m = self.edge[k](torch.cat([e, vk.index_select(0, send), vk.index_select(0, recv)], 1))
-            e = e + m
+            m = _apply(self.edge[k], torch.cat([e, vk.index_select(0, send), vk.index_select(0, recv)], 1), bf16)
+            e = R(e + m)
             agg = torch.zeros(no, self.l, dtype=torch.float64).index_add(0, recv, m)
-            v = v + self.node[k](torch.cat([v, agg], 1))
-        return self.dec(v)
+            v = v + _apply(self.node[k], torch.cat([v, agg], 1), bf16)
+        return _apply(self.dec, v, bf16)
 
 
-def run(latent, K, depth, shapes, g, params, node_feat, edge_feat, halo, d_out):
+def run(latent, K, depth, shapes, g, params, node_feat, edge_feat, halo, d_out, bf16=False):
     """Returns out, flat d_params, d_halo (numpy float64)."""
     torch.manual_seed(0)
     model = TorchMGN(latent, K, depth)
@@ -89,7 +135,7 @@ def run(latent, K, depth, shapes, g, params, node_feat, edge_feat, halo, d_out):
     ef = torch.as_tensor(np.asarray(edge_feat, np.float64))
     nh = g["n_halo"]
     H = torch.as_tensor(np.asarray(halo, np.float64) if nh > 0 else np.zeros((K, 0, latent))).clone().requires_grad_(True)
-    out = model(g, nf, ef, H)
+    out = model(g, nf, ef, H, bf16=bf16)
     out.backward(torch.as_tensor(np.asarray(d_out, np.float64)))
     dh = H.grad.numpy() if H.grad is not None else np.zeros((K, nh, latent))
     return out.detach().numpy(), model.flat_grad().numpy(), dh
