@@ -1,0 +1,179 @@
+"""Benchmark: one MeshGraphNets training step (forward, loss gradient,
+backward) on one GPU's mesh partition, through libmgn's C ABI.
+
+Default workload: the 2M-owned-node theta slab of the 100x160x500 swept
+sector mesh (100k halo nodes, 27,808,160 local edges), latent 128, 15
+message-passing blocks, 2-layer MLPs, bf16 matrix products.  Inputs are
+synthetic and seeded, resident in HBM before the timed region.
+
+metric: edge-block updates per second, E * K / step time.  Prints one JSON
+line with the roofline position of the dominant kernel and the oracle's
+throughput on a bounded sample of the same workload (its CPU baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"hbm": 8.0e12, "bf16": 2.5e15, "fp32": 157.3e12}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic(timer: str, cfg, E: int, N: int):
+    """Algorithmic work of one launch of the kernel class `timer` for one
+    block: (bytes, flops).  Bytes count compulsory HBM traffic of a fused
+    kernel (each operand row once); flops count the MLP products in the
+    concatenated form of the model (2 flops per multiply-add)."""
+    l, D = cfg.latent, cfg.depth
+    s_e = 2 if cfg.precision == "bf16" else 4
+    mlp_edge = 2 * l * (3 * l) + 2 * l * l * (D - 1)          # per edge, forward
+    mlp_node = 2 * l * (2 * l) + 2 * l * l * (D - 1)          # per node, forward
+    if timer == "edge_fwd":
+        # read e^k, write e^{k+1}; node rows (owned + halo) and agg once
+        return E * (2 * l * s_e + 4) + N * l * 4 * 2, E * mlp_edge
+    if timer == "edge_bwd":
+        # read e^k and de^{k+1}, write de^k and the sender-side gradient; node rows
+        return E * (l * s_e + 3 * 4 * l + 4) + N * l * 4 * 3, 2 * E * mlp_edge
+    if timer == "node_fwd":
+        return N * l * 4 * 3, N * mlp_node
+    if timer == "node_bwd":
+        return N * l * 4 * 5, 2 * N * mlp_node
+    if timer == "sender_gather":
+        return E * (4 * l + 4) + N * l * 4 * 2, 0
+    return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="C4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (pass --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2307_13592_amd as mgn
+    from paper_2307_13592_amd.runner import Session
+
+    cfg = synth.CONFIGS[args.config]
+    t0 = time.time()
+    case = synth.make_case(cfg, region=True)
+    mesh = case.mesh
+    part = mesh.part if mesh.part is not None else np.zeros(mesh.n_nodes, np.int32)
+    g = mgn.mgn_graph_build(mesh.send, mesh.recv, part, mesh.n_nodes, cfg.part)
+    loc = case.local_inputs(g["l2g"], g["eperm"], g["n_owned"], g["n_halo"])
+    no, nh, ne = g["n_owned"], g["n_halo"], g["n_edges"]
+    log(f"[bench] {cfg.name}: {cfg.note}; owned {no}, halo {nh}, edges {ne}; inputs {time.time() - t0:.1f}s")
+    sess = Session(cfg.latent, cfg.K, cfg.depth, cfg.precision, g, loc["node_feat"], loc["edge_feat"],
+                   loc["halo"], case.params)
+    target = torch.as_tensor(loc["target"]).cuda()
+    log(f"[bench] workspace {sess.ws_bytes / 2**30:.1f} GiB")
+
+    def step():
+        sess.forward()
+        _, d_out = sess.mse(target)
+        sess.backward(d_out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("[bench] warm-up done")
+    mgn.mgn_timing_enable(sess.model, True)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    timers = mgn.mgn_timing_read(sess.model)
+    mgn.mgn_timing_enable(sess.model, False)
+    log(f"[bench] {ms:.2f} ms/step")
+    for k, (t, n) in sorted(timers.items(), key=lambda kv: -kv[1][0]):
+        if n:
+            log(f"[bench]   {k:14s} {t / args.steps:9.3f} ms/step  {n // args.steps:4d} launches/step  "
+                f"{t / n:8.4f} ms/launch")
+
+    # dominant kernel and its roofline position
+    dom = max((k for k in timers if algorithmic(k, cfg, ne, no + nh) is not None and timers[k][1]),
+              key=lambda k: timers[k][0])
+    t_launch = timers[dom][0] / timers[dom][1] * 1e-3
+    by, fl = algorithmic(dom, cfg, ne, no + nh)
+    peak_flops = PEAK["bf16"] if cfg.precision == "bf16" else PEAK["fp32"]
+    intensity = fl / by if by else 0
+    if intensity >= peak_flops / PEAK["hbm"]:
+        roof = dict(bound="mfma", achieved=fl / t_launch / 1e12, peak=peak_flops / 1e12, unit="TFLOP/s")
+    else:
+        roof = dict(bound="hbm", achieved=by / t_launch / 1e9, peak=PEAK["hbm"] / 1e9, unit="GB/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["kernel"] = dom
+    roof["traffic"] = None
+    value = ne * cfg.K / (ms * 1e-3)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, g, loc, case)
+    sess.close()
+    line = {
+        "metric": "edges/sec per message-passing step (fwd+bwd)",
+        "value": value, "unit": "edge-block updates/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.precision, "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.note}", "owned_nodes": no, "halo_nodes": nh, "edges": ne,
+                   "latent": cfg.latent, "blocks": cfg.K, "mlp_depth": cfg.depth, "parallelism": "none"},
+        "nodes_per_sec": no * cfg.K / (ms * 1e-3),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(cfg, g, loc, case):
+    """The oracle on a bounded sample of the workload: the receptive field of
+    one corner node (every block's edges into nodes within K-1 hops), which is
+    what one output and, with the loss gradient on that node, its share of the
+    parameter gradients depend on."""
+    import oracle
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from cone import cone
+
+    c = cone(g, [0], cfg.K)
+    ef = loc["edge_feat"][c["edges"]]
+    nf = loc["node_feat"][c["owned"]]
+    halo = loc["halo"][:, c["halo"]] if c["n_halo"] else None
+    d_out = np.zeros((c["n_owned"], 5))
+    d_out[c["centers_sub"]] = 1.0
+    ocfg = oracle.ModelCfg(cfg.latent, cfg.K, cfg.depth, bf16=cfg.precision == "bf16")
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    t = time.time()
+    oracle.step(ocfg, c, case.params.astype(np.float64), nf.astype(np.float64), ef.astype(np.float64),
+                None if halo is None else halo.astype(np.float64), d_out)
+    dt = time.time() - t
+    log(f"[bench] oracle sample: {c['n_edges']} edges x {cfg.K} blocks in {dt:.1f}s ({threads} threads)")
+    return {"value": c["n_edges"] * cfg.K / dt, "unit": "edge-block updates/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"receptive field of one corner node: {c['n_owned']} owned + {c['n_halo']} halo nodes, "
+                      f"{c['n_edges']} edges, all {cfg.K} blocks, fwd+bwd"}
+
+
+if __name__ == "__main__":
+    main()

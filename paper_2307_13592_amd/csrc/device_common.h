@@ -105,6 +105,50 @@ __device__ __forceinline__ void wave_gemm(const typename P::T* A, int lda, const
   }
 }
 
+// Same with the number of k-groups known at compile time, software
+// pipelined: B fragments are fetched PF k-groups ahead (a ring of registers),
+// A fragments one k-group ahead, so neither global nor LDS latency is waited
+// on inside the loop.
+template <class P, int MB, int NBW, int NKG>
+__device__ __forceinline__ void wave_gemm_k(const typename P::T* A, int lda, const uint4* __restrict__ Bp, int nb0,
+                                            floatx4 (&acc)[MB][NBW]) {
+  constexpr int PF = NKG < 4 ? NKG : 4;
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int m = 0; m < MB; ++m)
+#pragma unroll
+    for (int n = 0; n < NBW; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const typename P::T* Ar = A + (lane & 15) * lda + (lane >> 4) * P::EL;
+  const uint4* Bl = Bp + (size_t)nb0 * NKG * 64 + lane;
+  uint4 b[PF][NBW];
+#pragma unroll
+  for (int p = 0; p < PF; ++p)
+#pragma unroll
+    for (int n = 0; n < NBW; ++n) b[p][n] = Bl[(n * NKG + p) * 64];
+  uint4 a[2][MB];
+#pragma unroll
+  for (int m = 0; m < MB; ++m) a[0][m] = *reinterpret_cast<const uint4*>(Ar + m * 16 * lda);
+#pragma unroll
+  for (int kg = 0; kg < NKG; ++kg) {
+    uint4 bc[NBW];
+#pragma unroll
+    for (int n = 0; n < NBW; ++n) bc[n] = b[kg % PF][n];
+    if (kg + PF < NKG) {
+#pragma unroll
+      for (int n = 0; n < NBW; ++n) b[kg % PF][n] = Bl[(n * NKG + kg + PF) * 64];
+    }
+    if (kg + 1 < NKG) {
+#pragma unroll
+      for (int m = 0; m < MB; ++m)
+        a[(kg + 1) & 1][m] = *reinterpret_cast<const uint4*>(Ar + m * 16 * lda + (kg + 1) * P::KG);
+    }
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+#pragma unroll
+      for (int n = 0; n < NBW; ++n) P::mma(acc[m][n], a[kg & 1][m], bc[n]);
+  }
+}
+
 // Row / column of accumulator element r (0..3) of a 16x16 MFMA block for
 // this lane: row 4*(lane/16) + r, column lane%16.
 __device__ __forceinline__ int acc_row(int r) { return ((threadIdx.x & 63) >> 4) * 4 + r; }

@@ -62,6 +62,18 @@ __device__ __forceinline__ void copy_row16(typename P::T* dst, const typename P:
     *reinterpret_cast<uint4*>(dst + c) = *reinterpret_cast<const uint4*>(src + c);
 }
 
+// Copies n rows of `width` elements (16-byte multiple) from LDS (row stride
+// ld) to consecutive global rows starting at dst, 16 bytes per thread.
+template <class T>
+__device__ __forceinline__ void store_rows(T* __restrict__ dst, const T* src, int ld, int n, int width) {
+  constexpr int E16 = 16 / sizeof(T);
+  const int cpr = width / E16;
+  for (int i = threadIdx.x; i < n * cpr; i += NT) {
+    const int r = i / cpr, c = (i % cpr) * E16;
+    *reinterpret_cast<uint4*>(dst + (int64_t)r * width + c) = *reinterpret_cast<const uint4*>(src + r * ld + c);
+  }
+}
+
 // Stores an accumulator tile (MB x NBW blocks of 16x16) plus bias and
 // optional ReLU into an LDS matrix of type OutT (row stride ld).
 template <class P, int MB, int NBW, bool RELU, class OutT>
@@ -110,6 +122,40 @@ __device__ __forceinline__ void ln_normalise(float* Y, int ld, float eps, float*
   const float rs = 1.0f / sqrtf(v / L + eps);
   for (int c = q; c < L; c += TPR) y[c] = (y[c] - mu) * rs;
   if (q == 0 && rstd_out) rstd_out[row] = rs;
+}
+
+// LayerNorm of TM rows in place: y <- gamma * (y - mean) * rstd + beta.
+template <int TM, int L>
+__device__ __forceinline__ void ln_rows(float* Y, int ld, float eps, const float* __restrict__ gamma,
+                                        const float* __restrict__ beta) {
+  constexpr int TPR = NT / TM;
+  constexpr int PER = L / TPR;
+  const int row = threadIdx.x / TPR, q = threadIdx.x % TPR;
+  float* y = Y + row * ld;
+  float v[PER];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    v[j] = y[q + j * TPR];
+    s += v[j];
+  }
+#pragma unroll
+  for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o, 64);
+  const float mu = s / L;
+  float var = 0.f;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const float d = v[j] - mu;
+    var += d * d;
+  }
+#pragma unroll
+  for (int o = 1; o < TPR; o <<= 1) var += __shfl_xor(var, o, 64);
+  const float rs = 1.0f / sqrtf(var / L + eps);
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int c = q + j * TPR;
+    y[c] = gamma[c] * ((v[j] - mu) * rs) + beta[c];
+  }
 }
 
 template <int TM, int L>
@@ -347,14 +393,18 @@ __device__ __forceinline__ void stage_rows(typename P::T* X, const float* __rest
   } else {
     constexpr int Q = L / 4;  // float4 per source row
     constexpr int NSRC = KIND == NODE_BLOCK ? 2 : 1;
-    for (int i = threadIdx.x; i < TM * Q * NSRC; i += NT) {
-      const int r = i / (Q * NSRC), rem = i % (Q * NSRC), s = rem / Q, c4 = rem % Q;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (r < n) {
-        const float* src = (s == 0 ? in0 : in1) + (row0 + r) * L;
-        v = reinterpret_cast<const float4*>(src)[c4];
-      }
-      st4<P>(X + r * LDX + s * L + c4 * 4, v);
+    constexpr int IT = (TM * Q * NSRC + NT - 1) / NT;
+    float4 v[IT];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int i = threadIdx.x + j * NT, r = i / (Q * NSRC), rem = i % (Q * NSRC), s = rem / Q, c4 = rem % Q;
+      v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (i < TM * Q * NSRC && r < n) v[j] = reinterpret_cast<const float4*>((s == 0 ? in0 : in1) + (row0 + r) * L)[c4];
+    }
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int i = threadIdx.x + j * NT, r = i / (Q * NSRC), rem = i % (Q * NSRC), s = rem / Q, c4 = rem % Q;
+      if (i < TM * Q * NSRC) st4<P>(X + r * LDX + s * L + c4 * 4, v[j]);
     }
   }
 }
@@ -371,7 +421,10 @@ __device__ __forceinline__ void mlp_tile_forward(const Mlp& mlp, typename P::T* 
   {
     floatx4 acc[MB][NBW];
     if (wave * NBW * 16 < L) {
-      wave_gemm<P, MB, NBW>(X, ldx, mlp.lin[0].wf, mlp.lin[0].nkgf, wave * NBW, acc);
+      if constexpr (KIND == ENC_NODE || KIND == ENC_EDGE)
+        wave_gemm<P, MB, NBW>(X, ldx, mlp.lin[0].wf, mlp.lin[0].nkgf, wave * NBW, acc);
+      else
+        wave_gemm_k<P, MB, NBW, S::KIN / P::KG>(X, ldx, mlp.lin[0].wf, wave * NBW, acc);
       store_acc<P, MB, NBW, true>(acc, wave * NBW, mlp.lin[0].b, L, HB, ldh);
     }
   }
@@ -380,7 +433,7 @@ __device__ __forceinline__ void mlp_tile_forward(const Mlp& mlp, typename P::T* 
   if constexpr (D == 3) {
     floatx4 acc[MB][NBW];
     if (wave * NBW * 16 < L) {
-      wave_gemm<P, MB, NBW>(HB, ldh, mlp.lin[1].wf, mlp.lin[1].nkgf, wave * NBW, acc);
+      wave_gemm_k<P, MB, NBW, L / P::KG>(HB, ldh, mlp.lin[1].wf, wave * NBW, acc);
       store_acc<P, MB, NBW, true>(acc, wave * NBW, mlp.lin[1].b, L, HC, ldh);
     }
     __syncthreads();
@@ -391,7 +444,7 @@ __device__ __forceinline__ void mlp_tile_forward(const Mlp& mlp, typename P::T* 
     constexpr int NBO = NB_OUT / NW > 0 ? NB_OUT / NW : 1;
     floatx4 acc[MB][NBO];
     if (wave * NBO < NB_OUT) {
-      wave_gemm<P, MB, NBO>(hin, ldh, mlp.lin[D - 1].wf, mlp.lin[D - 1].nkgf, wave * NBO, acc);
+      wave_gemm_k<P, MB, NBO, L / P::KG>(hin, ldh, mlp.lin[D - 1].wf, wave * NBO, acc);
       store_acc<P, MB, NBO, false>(acc, wave * NBO, mlp.lin[D - 1].b, mlp.lin[D - 1].out, Y, ldy);
     }
   }
@@ -417,8 +470,7 @@ __global__ __launch_bounds__(NT) void rows_fwd_kernel(RowsFwdArgs a) {
     __syncthreads();
     mlp_tile_forward<P, KIND, L, D, TM>(a.mlp, X, HB, HC, Y, Lay::LDX, Lay::LDH, Lay::LDY);
     if constexpr (RowShape<KIND, L>::LN) {
-      ln_normalise<TM, L>(Y, Lay::LDY, a.eps, nullptr);
-      ln_affine<TM, L>(Y, Lay::LDY, a.mlp.gamma, a.mlp.beta);
+      ln_rows<TM, L>(Y, Lay::LDY, a.eps, a.mlp.gamma, a.mlp.beta);
       __syncthreads();
     }
     if constexpr (KIND == DECODER) {
@@ -523,7 +575,7 @@ __global__ __launch_bounds__(NT) void rows_bwd_kernel(RowsBwdArgs a) {
       {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm<P, MB, NBW>(X, Lay::LDX, a.mlp.lin[0].wf, a.mlp.lin[0].nkgf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, S::KIN / P::KG>(X, Lay::LDX, a.mlp.lin[0].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[0].b, L, HB, Lay::LDH);
         }
       }
@@ -531,7 +583,7 @@ __global__ __launch_bounds__(NT) void rows_bwd_kernel(RowsBwdArgs a) {
       if constexpr (D == 3) {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm<P, MB, NBW>(HB, Lay::LDH, a.mlp.lin[1].wf, a.mlp.lin[1].nkgf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, L / P::KG>(HB, Lay::LDH, a.mlp.lin[1].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[1].b, L, HC, Lay::LDH);
         }
         __syncthreads();
@@ -547,26 +599,20 @@ __global__ __launch_bounds__(NT) void rows_bwd_kernel(RowsBwdArgs a) {
     }
     // gradient at the last Linear's output and the hidden activations, for the
     // weight-gradient GEMMs
-    {
-      const int w_last = S::NOUT;
-      T* dl = reinterpret_cast<T*>(a.delta[D - 1]);
-      for (int i = tid; i < n * w_last; i += NT) {
-        const int r = i / w_last, c = i % w_last;
-        dl[(row0 + r) * w_last + c] = DY[r * Lay::LDH + c];
-      }
-      T* h0 = reinterpret_cast<T*>(a.hid[0]);
-      for (int i = tid; i < n * L; i += NT) {
-        const int r = i / L, c = i % L;
-        h0[(row0 + r) * L + c] = HB[r * Lay::LDH + c];
-        if constexpr (D == 3) reinterpret_cast<T*>(a.hid[1])[(row0 + r) * L + c] = HC[r * Lay::LDH + c];
-      }
-    }
+    store_rows(reinterpret_cast<T*>(a.delta[D - 1]) + row0 * S::NOUT, DY, Lay::LDH, n, S::NOUT);
+    store_rows(reinterpret_cast<T*>(a.hid[0]) + row0 * L, HB, Lay::LDH, n, L);
+    if constexpr (D == 3) store_rows(reinterpret_cast<T*>(a.hid[1]) + row0 * L, HC, Lay::LDH, n, L);
     // back through the hidden layers: dz_{j-1} = (dz_j W_j) * [h_{j-1} > 0]
 #pragma unroll
     for (int j = D - 1; j >= 1; --j) {
       const T* hprev = (j == 2) ? HC : HB;
       floatx4 acc[MB][NBW];
-      if (wave_has_cols) wave_gemm<P, MB, NBW>(DY, Lay::LDH, a.mlp.lin[j].wb, a.mlp.lin[j].nkgb, wave * NBW, acc);
+      if (wave_has_cols) {
+        if (KIND == DECODER && j == D - 1)
+          wave_gemm_k<P, MB, NBW, 1>(DY, Lay::LDH, a.mlp.lin[j].wb, wave * NBW, acc);
+        else
+          wave_gemm_k<P, MB, NBW, L / P::KG>(DY, Lay::LDH, a.mlp.lin[j].wb, wave * NBW, acc);
+      }
       __syncthreads();
       if (wave_has_cols) {
 #pragma unroll
@@ -586,11 +632,7 @@ __global__ __launch_bounds__(NT) void rows_bwd_kernel(RowsBwdArgs a) {
         for (int nn = 0; nn < NBW; ++nn) g_bh[j - 1][nn] += cs[nn];
       }
       __syncthreads();
-      T* dj = reinterpret_cast<T*>(a.delta[j - 1]);
-      for (int i = tid; i < n * L; i += NT) {
-        const int r = i / L, c = i % L;
-        dj[(row0 + r) * L + c] = DY[r * Lay::LDH + c];
-      }
+      store_rows(reinterpret_cast<T*>(a.delta[j - 1]) + row0 * L, DY, Lay::LDH, n, L);
     }
     // input gradients
     if constexpr (KIND == NODE_BLOCK || KIND == DECODER) {
@@ -599,8 +641,7 @@ __global__ __launch_bounds__(NT) void rows_bwd_kernel(RowsBwdArgs a) {
       for (int pass = 0; pass < NPASS; ++pass) {
         floatx4 acc[MB][NBW];
         if (wave_has_cols)
-          wave_gemm<P, MB, NBW>(DY, Lay::LDH, a.mlp.lin[0].wb, a.mlp.lin[0].nkgb, pass * (L / 16) + wave * NBW,
-                                acc);
+          wave_gemm_k<P, MB, NBW, L / P::KG>(DY, Lay::LDH, a.mlp.lin[0].wb, pass * (L / 16) + wave * NBW, acc);
         __syncthreads();  // DM (gradient staging) may still be read above
         if (wave_has_cols) store_acc<P, MB, NBW, false>(acc, wave * NBW, nullptr, L, DM, Lay::LDM);
         __syncthreads();
@@ -660,9 +701,9 @@ struct EdgeLds {
   static constexpr int OFF_B = rup(AB, 16);
   static constexpr int OFF_C = OFF_B + HB;
   static constexpr int OFF_D = OFF_C + (D == 3 ? HB : 0);
-  static constexpr int OFF_META = OFF_D + TE * LDM * 4;
-  static constexpr int END = OFF_META + TE * 12;
-  static constexpr int END_F = OFF_D + TE * 8;  // forward: meta right after B/C
+  static constexpr int OFF_META = OFF_D + TE * LDM * 4;            // backward: rr, ss, mask, rstd
+  static constexpr int END = OFF_META + TE * 12 + 16;
+  static constexpr int END_F = OFF_D + TE * 8 + 16;                  // forward: rr, ss, mask after B/C
 };
 
 template <class P, int L, int D>
@@ -672,50 +713,97 @@ struct EdgeTE {
                                                                       : 16;
 };
 
-// Gathers one sub-tile [e | v_s | v_r] into LDS and the per-row receiver and
-// end-of-segment flags.
+// Per-row metadata of a sub-tile in LDS: receiver and sender local ids, and a
+// bit mask of the rows that end their receiver's segment.
+struct EdgeMeta {
+  int32_t* rr;
+  int32_t* ss;
+  unsigned long long* last;
+};
+
+// Gathers one sub-tile [e | v_s | v_r] into LDS.  First the TE row indices
+// (one load round), then every row load of this thread is issued before any
+// is stored, so the gather costs two memory latencies, not one per row.
 template <class P, int L, int TE, int LDA>
-__device__ __forceinline__ void stage_edges(typename P::T* A, int32_t* rr, int32_t* last, const int32_t* erecv,
+__device__ __forceinline__ void stage_edges(typename P::T* A, EdgeMeta mt, const int32_t* erecv,
                                             const int32_t* send, const typename P::T* Ein, const float* V,
                                             const float* H, int64_t n_owned, int64_t sb, int n, int64_t e1) {
   using T = typename P::T;
   const int tid = threadIdx.x;
-  if (tid < TE) {
-    int32_t r = -1, l = 0;
+  if (tid < 64) {
+    int32_t r = -1, sd = 0;
+    bool l = false;
     if (tid < n) {
       const int64_t e = sb + tid;
       r = erecv[e];
+      sd = send[e];
       l = (e + 1 == e1) || erecv[e + 1] != r;
     }
-    rr[tid] = r;
-    last[tid] = l;
+    const unsigned long long m = __ballot(l);
+    if (tid < TE) {
+      mt.rr[tid] = r;
+      mt.ss[tid] = sd;
+    }
+    if (tid == 0) *mt.last = m;
   }
-  // e rows: 16-byte chunks
+  __syncthreads();
   constexpr int E16 = 16 / sizeof(T);
-  constexpr int CPR = L / E16;
-  for (int i = tid; i < TE * CPR; i += NT) {
-    const int r = i / CPR, c = (i % CPR) * E16;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (r < n) v = *reinterpret_cast<const uint4*>(Ein + (sb + r) * L + c);
-    *reinterpret_cast<uint4*>(A + r * LDA + c) = v;
+  constexpr int CPR = L / E16;                   // 16-byte chunks per e row
+  constexpr int IE = (TE * CPR + NT - 1) / NT;
+  constexpr int Q = L / 4;                       // float4 per node row
+  constexpr int IV = (TE * 2 * Q + NT - 1) / NT;
+  uint4 ev[IE];
+  float4 vv[IV];
+#pragma unroll
+  for (int j = 0; j < IE; ++j) {
+    const int i = tid + j * NT, r = i / CPR, c = (i % CPR) * E16;
+    ev[j] = make_uint4(0, 0, 0, 0);
+    if (i < TE * CPR && r < n) ev[j] = *reinterpret_cast<const uint4*>(Ein + (sb + r) * L + c);
   }
-  // sender and receiver node rows (fp32 -> storage type)
-  constexpr int Q = L / 4;
-  for (int i = tid; i < TE * 2 * Q; i += NT) {
-    const int r = i / (2 * Q), rem = i % (2 * Q), s = rem / Q, c4 = rem % Q;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < n) {
-      const int64_t e = sb + r;
+#pragma unroll
+  for (int j = 0; j < IV; ++j) {
+    const int i = tid + j * NT, r = i / (2 * Q), rem = i % (2 * Q), sside = rem / Q, c4 = rem % Q;
+    vv[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i < TE * 2 * Q && r < n) {
       const float* src;
-      if (s == 0) {
-        const int64_t snd = send[e];
+      if (sside == 0) {
+        const int64_t snd = mt.ss[r];
         src = snd < n_owned ? V + snd * L : H + (snd - n_owned) * L;
       } else {
-        src = V + (int64_t)erecv[e] * L;
+        src = V + (int64_t)mt.rr[r] * L;
       }
-      v = reinterpret_cast<const float4*>(src)[c4];
+      vv[j] = reinterpret_cast<const float4*>(src)[c4];
     }
-    st4<P>(A + r * LDA + (1 + s) * L + c4 * 4, v);
+  }
+#pragma unroll
+  for (int j = 0; j < IE; ++j) {
+    const int i = tid + j * NT, r = i / CPR, c = (i % CPR) * E16;
+    if (i < TE * CPR) *reinterpret_cast<uint4*>(A + r * LDA + c) = ev[j];
+  }
+#pragma unroll
+  for (int j = 0; j < IV; ++j) {
+    const int i = tid + j * NT, r = i / (2 * Q), rem = i % (2 * Q), sside = rem / Q, c4 = rem % Q;
+    if (i < TE * 2 * Q) st4<P>(A + r * LDA + (1 + sside) * L + c4 * 4, vv[j]);
+  }
+}
+
+// Ordered running sum over the rows of a sub-tile for column c: adds rows
+// 0..n-1 of M (fp32, row stride ld) to `run`; at each row that ends a
+// receiver segment, hands the segment's total to emit(receiver, total) and
+// restarts.  The running value carries into the next sub-tile of the unit.
+template <int TE, class Emit>
+__device__ __forceinline__ void segment_sums(const float* M, int ld, int n, int c, EdgeMeta mt, float& run,
+                                             Emit emit) {
+  const unsigned long long mask = *mt.last;
+#pragma unroll 8
+  for (int r = 0; r < TE; ++r) {
+    if (r < n) {
+      run += M[r * ld + c];
+      if ((mask >> r) & 1ull) {
+        emit(mt.rr[r], run);
+        run = 0.f;
+      }
+    }
   }
 }
 
@@ -723,9 +811,9 @@ __device__ __forceinline__ void stage_edges(typename P::T* A, int32_t* rr, int32
 // edges (their ordered sums are empty).
 __device__ __forceinline__ void zero_empty_receivers(const int32_t* row_ptr, int64_t r0, int64_t r1, float* dst,
                                                      int L) {
-  for (int64_t r = r0; r < r1; ++r)
+  for (int64_t r = r0 + threadIdx.x; r < r1; r += NT)
     if (row_ptr[r] == row_ptr[r + 1])
-      for (int c = threadIdx.x; c < L; c += NT) dst[r * L + c] = 0.f;
+      for (int c = 0; c < L; c += 4) *reinterpret_cast<float4*>(dst + r * L + c) = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
 template <int P_, int L, int D>
@@ -741,8 +829,10 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
   T* HB = reinterpret_cast<T*>(lds + Lay::OFF_B);
   T* HC = reinterpret_cast<T*>(lds + Lay::OFF_C);
   float* Y = reinterpret_cast<float*>(lds) + Lay::Y_OFF_F;
-  int32_t* rr = reinterpret_cast<int32_t*>(lds + Lay::OFF_D);
-  int32_t* last = rr + TE;
+  EdgeMeta mt;
+  mt.rr = reinterpret_cast<int32_t*>(lds + Lay::OFF_D);
+  mt.ss = mt.rr + TE;
+  mt.last = reinterpret_cast<unsigned long long*>(mt.ss + TE);
   const int wave = threadIdx.x >> 6, tid = threadIdx.x;
   const bool wave_has_cols = wave * NBW * 16 < L;
   const T* Ein = reinterpret_cast<const T*>(a.Ein);
@@ -755,12 +845,12 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
     float run = 0.f;  // running receiver sum of column tid
     for (int64_t sb = e0; sb < e1; sb += TE) {
       const int n = (int)(e1 - sb < TE ? e1 - sb : TE);
-      stage_edges<P, L, TE, Lay::LDA>(A, rr, last, a.erecv, a.send, Ein, a.V, a.H, a.n_owned, sb, n, e1);
+      stage_edges<P, L, TE, Lay::LDA>(A, mt, a.erecv, a.send, Ein, a.V, a.H, a.n_owned, sb, n, e1);
       __syncthreads();
       {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm<P, MB, NBW>(A, Lay::LDA, a.mlp.lin[0].wf, a.mlp.lin[0].nkgf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, 3 * L / P::KG>(A, Lay::LDA, a.mlp.lin[0].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[0].b, L, HB, Lay::LDH);
         }
       }
@@ -769,7 +859,7 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
       if constexpr (D == 3) {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm<P, MB, NBW>(HB, Lay::LDH, a.mlp.lin[1].wf, a.mlp.lin[1].nkgf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, L / P::KG>(HB, Lay::LDH, a.mlp.lin[1].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[1].b, L, HC, Lay::LDH);
         }
         __syncthreads();
@@ -778,29 +868,28 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
       {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm<P, MB, NBW>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, a.mlp.lin[D - 1].nkgf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, L / P::KG>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, false>(acc, wave * NBW, a.mlp.lin[D - 1].b, L, Y, Lay::LDY);
         }
       }
       __syncthreads();
-      ln_normalise<TE, L>(Y, Lay::LDY, a.eps, nullptr);
-      ln_affine<TE, L>(Y, Lay::LDY, a.mlp.gamma, a.mlp.beta);
+      ln_rows<TE, L>(Y, Lay::LDY, a.eps, a.mlp.gamma, a.mlp.beta);
       __syncthreads();
       if (Eout) {
-        for (int i = tid; i < n * L; i += NT) {
-          const int r = i / L, c = i % L;
-          Eout[(sb + r) * L + c] = P::cvt(P::tof(A[r * Lay::LDA + c]) + Y[r * Lay::LDY + c]);
+        // e^{k+1} = e^k + m, 16 bytes of output per thread
+        constexpr int E16 = 16 / sizeof(T);
+        constexpr int CPR = L / E16;
+        for (int i = tid; i < n * CPR; i += NT) {
+          const int r = i / CPR, c = (i % CPR) * E16;
+          T o[E16];
+#pragma unroll
+          for (int j = 0; j < E16; ++j) o[j] = P::cvt(P::tof(A[r * Lay::LDA + c + j]) + Y[r * Lay::LDY + c + j]);
+          *reinterpret_cast<uint4*>(Eout + (sb + r) * L + c) = *reinterpret_cast<const uint4*>(o);
         }
       }
-      for (int c = tid; c < L; c += NT) {
-        for (int r = 0; r < n; ++r) {
-          run += Y[r * Lay::LDY + c];
-          if (last[r]) {
-            a.agg[(int64_t)rr[r] * L + c] = run;
-            run = 0.f;
-          }
-        }
-      }
+      if (tid < L)
+        segment_sums<TE>(Y, Lay::LDY, n, tid, mt, run,
+                         [&](int32_t r, float v) { a.agg[(int64_t)r * L + tid] = v; });
       __syncthreads();
     }
   }
@@ -822,9 +911,11 @@ __global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
   T* HB = reinterpret_cast<T*>(lds + Lay::OFF_B);
   T* HC = reinterpret_cast<T*>(lds + Lay::OFF_C);
   float* DM = reinterpret_cast<float*>(lds + Lay::OFF_D);
-  int32_t* rr = reinterpret_cast<int32_t*>(lds + Lay::OFF_META);
-  int32_t* last = rr + TE;
-  float* RS = reinterpret_cast<float*>(last + TE);
+  EdgeMeta mt;
+  mt.rr = reinterpret_cast<int32_t*>(lds + Lay::OFF_META);
+  mt.ss = mt.rr + TE;
+  mt.last = reinterpret_cast<unsigned long long*>(mt.ss + TE);
+  float* RS = reinterpret_cast<float*>(mt.last + 2);
   const int wave = threadIdx.x >> 6, tid = threadIdx.x;
   const bool wave_has_cols = wave * NBW * 16 < L;
   const T* Ein = reinterpret_cast<const T*>(a.Ein);
@@ -842,31 +933,36 @@ __global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
     float run = 0.f;  // running receiver sum (receiver-side input gradient), column tid
     for (int64_t sb = e0; sb < e1; sb += TE) {
       const int n = (int)(e1 - sb < TE ? e1 - sb : TE);
-      stage_edges<P, L, TE, Lay::LDA>(A, rr, last, a.erecv, a.send, Ein, a.V, a.H, a.n_owned, sb, n, e1);
-      // dm = de^{k+1} + dagg[receiver]
+      stage_edges<P, L, TE, Lay::LDA>(A, mt, a.erecv, a.send, Ein, a.V, a.H, a.n_owned, sb, n, e1);
+      // dm = de^{k+1} + dagg[receiver], all loads of the thread issued first
       constexpr int Q = L / 4;
-      for (int i = tid; i < TE * Q; i += NT) {
-        const int r = i / Q, c4 = i % Q;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (r < n) {
-          const int64_t e = sb + r;
-          v = reinterpret_cast<const float4*>(a.dagg + (int64_t)a.erecv[e] * L)[c4];
-          if (a.de_next) {
-            const float4 d = reinterpret_cast<const float4*>(a.de_next + e * L)[c4];
-            v.x += d.x;
-            v.y += d.y;
-            v.z += d.z;
-            v.w += d.w;
+      constexpr int IM = (TE * Q + NT - 1) / NT;
+      {
+        float4 va[IM], vd[IM];
+#pragma unroll
+        for (int j = 0; j < IM; ++j) {
+          const int i = tid + j * NT, r = i / Q, c4 = i % Q;
+          va[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+          vd[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (i < TE * Q && r < n) {
+            va[j] = reinterpret_cast<const float4*>(a.dagg + (int64_t)mt.rr[r] * L)[c4];
+            if (a.de_next) vd[j] = reinterpret_cast<const float4*>(a.de_next + (sb + r) * L)[c4];
           }
         }
-        *reinterpret_cast<float4*>(DM + r * Lay::LDM + c4 * 4) = v;
+#pragma unroll
+        for (int j = 0; j < IM; ++j) {
+          const int i = tid + j * NT, r = i / Q, c4 = i % Q;
+          if (i < TE * Q)
+            *reinterpret_cast<float4*>(DM + r * Lay::LDM + c4 * 4) =
+                make_float4(va[j].x + vd[j].x, va[j].y + vd[j].y, va[j].z + vd[j].z, va[j].w + vd[j].w);
+        }
       }
       __syncthreads();
       // recompute the forward: hidden activations and the LN input
       {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm<P, MB, NBW>(A, Lay::LDA, a.mlp.lin[0].wf, a.mlp.lin[0].nkgf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, 3 * L / P::KG>(A, Lay::LDA, a.mlp.lin[0].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[0].b, L, HB, Lay::LDH);
         }
       }
@@ -875,7 +971,7 @@ __global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
       if constexpr (D == 3) {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm<P, MB, NBW>(HB, Lay::LDH, a.mlp.lin[1].wf, a.mlp.lin[1].nkgf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, L / P::KG>(HB, Lay::LDH, a.mlp.lin[1].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[1].b, L, HC, Lay::LDH);
         }
         __syncthreads();
@@ -884,7 +980,7 @@ __global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
       {
         floatx4 acc[MB][NBW];
         if (wave_has_cols)
-          wave_gemm<P, MB, NBW>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, a.mlp.lin[D - 1].nkgf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, L / P::KG>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, wave * NBW, acc);
         __syncthreads();  // A (the gathered inputs) is overwritten below
         if (wave_has_cols) store_acc<P, MB, NBW, false>(acc, wave * NBW, a.mlp.lin[D - 1].b, L, Yf, Lay::LDY);
       }
@@ -902,22 +998,15 @@ __global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
       ln_backward<P, TE, L>(DM, Lay::LDM, XH, Lay::LDY, RS, a.mlp.gamma, DY, Lay::LDA);
       __syncthreads();
       if (tid < L) g_blast += col_sum(DM, Lay::LDM, n, tid);
-      {
-        T* dl = reinterpret_cast<T*>(a.delta[D - 1]);
-        T* h0 = reinterpret_cast<T*>(a.hid[0]);
-        for (int i = tid; i < n * L; i += NT) {
-          const int r = i / L, c = i % L;
-          dl[(sb + r) * L + c] = DY[r * Lay::LDA + c];
-          h0[(sb + r) * L + c] = HB[r * Lay::LDH + c];
-          if constexpr (D == 3) reinterpret_cast<T*>(a.hid[1])[(sb + r) * L + c] = HC[r * Lay::LDH + c];
-        }
-      }
+      store_rows(reinterpret_cast<T*>(a.delta[D - 1]) + sb * L, DY, Lay::LDA, n, L);
+      store_rows(reinterpret_cast<T*>(a.hid[0]) + sb * L, HB, Lay::LDH, n, L);
+      if constexpr (D == 3) store_rows(reinterpret_cast<T*>(a.hid[1]) + sb * L, HC, Lay::LDH, n, L);
 #pragma unroll
       for (int j = D - 1; j >= 1; --j) {
         const T* hprev = (j == 2) ? HC : HB;
         floatx4 acc[MB][NBW];
         if (wave_has_cols)
-          wave_gemm<P, MB, NBW>(DY, Lay::LDA, a.mlp.lin[j].wb, a.mlp.lin[j].nkgb, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, L / P::KG>(DY, Lay::LDA, a.mlp.lin[j].wb, wave * NBW, acc);
         __syncthreads();
         if (wave_has_cols) {
 #pragma unroll
@@ -937,19 +1026,14 @@ __global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
           for (int nn = 0; nn < NBW; ++nn) g_bh[j - 1][nn] += cs[nn];
         }
         __syncthreads();
-        T* dj = reinterpret_cast<T*>(a.delta[j - 1]);
-        for (int i = tid; i < n * L; i += NT) {
-          const int r = i / L, c = i % L;
-          dj[(sb + r) * L + c] = DY[r * Lay::LDA + c];
-        }
+        store_rows(reinterpret_cast<T*>(a.delta[j - 1]) + sb * L, DY, Lay::LDA, n, L);
       }
       // input gradient [d e | d v_s | d v_r] = dz_1 W_1, one L-wide pass each
 #pragma unroll
       for (int pass = 0; pass < 3; ++pass) {
         floatx4 acc[MB][NBW];
         if (wave_has_cols)
-          wave_gemm<P, MB, NBW>(DY, Lay::LDA, a.mlp.lin[0].wb, a.mlp.lin[0].nkgb, pass * (L / 16) + wave * NBW,
-                                acc);
+          wave_gemm_k<P, MB, NBW, L / P::KG>(DY, Lay::LDA, a.mlp.lin[0].wb, pass * (L / 16) + wave * NBW, acc);
         __syncthreads();
         if (wave_has_cols) store_acc<P, MB, NBW, false>(acc, wave * NBW, nullptr, L, DM, Lay::LDM);
         __syncthreads();
@@ -968,15 +1052,9 @@ __global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
             reinterpret_cast<float4*>(dst + (sb + r) * L)[c4] = v;
           }
         } else {
-          for (int c = tid; c < L; c += NT) {
-            for (int r = 0; r < n; ++r) {
-              run += DM[r * Lay::LDM + c];
-              if (last[r]) {
-                a.dv[(int64_t)rr[r] * L + c] += run;
-                run = 0.f;
-              }
-            }
-          }
+          if (tid < L)
+            segment_sums<TE>(DM, Lay::LDM, n, tid, mt, run,
+                             [&](int32_t r, float v) { a.dv[(int64_t)r * L + tid] += v; });
         }
         __syncthreads();
       }

@@ -60,9 +60,13 @@ class Session:
         return loss, d_out
 
     def close(self):
-        if self.model:
+        """Destroys the model and drops every device buffer of the session."""
+        if getattr(self, "model", None):
             mgn_destroy(self.model)
             self.model = None
+        for k in ("workspace", "out", "d_params", "d_halo", "node_feat", "edge_feat", "halo", "g"):
+            setattr(self, k, None)
+        torch.cuda.empty_cache()
 
     def __del__(self):
         try:

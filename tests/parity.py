@@ -77,26 +77,65 @@ def run_oracle(c, latent, K, depth, d_out=None, g=None, nf=None, ef=None, halo=N
     return r
 
 
-def compare(name, prec, shapes, gpu, ref, halo_sel=None):
-    """Per-tensor max relative error; returns the list of failures."""
+def calibrate(c, latent, K, depth, prec, g=None, nf=None, ef=None, halo=None, d_out=None, runs=6,
+              rel=2.0 ** -20):
+    """An independent single-precision implementation (PyTorch float32
+    layers, bfloat16 operands when prec is bf16) on the same inputs, run
+    `runs` times: once as given and then with the node features, edge
+    features and halo latents perturbed by a relative `rel` (a few float32
+    roundings, the size of float32 accumulation error).  Whether a pre-activation within rounding distance of zero
+    (or of a bfloat16 rounding boundary) flips is a coin toss for any single
+    precision implementation; the largest distance from the oracle over the
+    runs is what correct single-precision arithmetic can cost on this input.
+    Returns the per-run results."""
+    import torch
+    import torch_ref
+    g = c["g"] if g is None else g
+    nf = c["nf"] if nf is None else nf
+    ef = c["ef"] if ef is None else ef
+    halo = c["halo"] if halo is None else halo
+    d_out = c["d_out"] if d_out is None else d_out
+    res = []
+    for i in range(runs):
+        if i == 0:
+            x = (nf, ef, halo)
+        else:
+            rng = np.random.default_rng([1234, i])
+            x = tuple(np.asarray(a, np.float64) * (1 + rel * rng.choice([-1.0, 1.0], np.shape(a)))
+                      for a in (nf, ef, halo))
+        res.append(torch_ref.run(latent, K, depth, c["shapes"], g, c["params"], x[0], x[1], x[2], d_out,
+                                 bf16=prec == "bf16", dtype=torch.float32))
+    return res
+
+
+def compare(name, prec, shapes, gpu, ref, calib=None, halo_sel=None, calib_factor=2.0):
+    """Per-tensor max relative error of the GPU against the oracle.  Outputs
+    must meet the tolerance of the precision.  A gradient tensor must meet
+    max(tolerance, calib_factor * the error of the independent float32
+    implementation's runs `calib` on the same tensor): gradients of a ReLU network
+    jump where a pre-activation sits within rounding distance of zero, and
+    in bf16 every rounded operand is such a place.  Returns the failures."""
     out, dp, dh = gpu
     tol = TOL[prec]
     bad = []
     e = rel_err(out, ref["out"])
-    worst = ("out", e)
+    worst = ("out", e, tol)
     if e > tol:
-        bad.append(("out", e))
+        bad.append(("out", e, tol))
+
+    def check(nm, got, want, cal):
+        nonlocal worst
+        e = rel_err(got, want)
+        t = tol if cal is None else max(tol, calib_factor * max(rel_err(x, want) for x in cal))
+        if e / t > worst[1] / worst[2]:
+            worst = (nm, e, t)
+        if e > t:
+            bad.append((nm, e, t))
+
     for nm, sl in segments(shapes):
-        e = rel_err(dp[sl], ref["d_params"][sl])
-        if e > worst[1]:
-            worst = (nm, e)
-        if e > tol:
-            bad.append((nm, e))
+        check(nm, dp[sl], ref["d_params"][sl], None if calib is None else [cr[1][sl] for cr in calib])
     if ref["d_halo"].size:
-        e = rel_err(dh if halo_sel is None else dh[:, halo_sel], ref["d_halo"])
-        if e > worst[1]:
-            worst = ("d_halo", e)
-        if e > tol:
-            bad.append(("d_halo", e))
-    say(f"  {name}: worst {worst[0]} {worst[1]:.2e} (tol {tol:g})")
+        check("d_halo", dh if halo_sel is None else dh[:, halo_sel], ref["d_halo"],
+              None if calib is None else [cr[2] for cr in calib])
+    say(f"  {name}: out {rel_err(out, ref['out']):.2e}; tightest {worst[0]} {worst[1]:.2e} (bound {worst[2]:.2e})")
     return bad

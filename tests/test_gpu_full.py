@@ -1,0 +1,115 @@
+"""GPU parity at the benchmark sizes, in the launch configuration bench.py
+times (the whole partition in one step).
+
+Sampled outputs: an owned node's output after K blocks depends only on its
+receptive field (tests/cone.py), so the oracle computes it on that
+sub-graph.  With the loss gradient non-zero only on the sampled nodes, every
+parameter gradient and every halo gradient of the full partition equals the
+sub-graph's, which the oracle also computes.  Sampled nodes: local id 0 (the
+slab's first theta layer at the hub and the inflow face, next to the halo)
+and an interior node of the same layer (mid radius, mid span).
+
+Properties at full size: two runs agree bitwise; the backward pass is exactly
+linear in the loss gradient; halo gradients outside the receptive field are
+exactly zero.
+"""
+import gc
+
+import numpy as np
+import pytest
+
+import synth
+import paper_2307_13592_amd as mgn
+from paper_2307_13592_amd.runner import Session
+from cone import cone
+from parity import TOL, calibrate, compare, rel_err, run_oracle, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(cfg):
+    say(f"[full] {cfg.name}: building {cfg.note}")
+    case = synth.make_case(cfg, region=True)
+    m = case.mesh
+    part = m.part if m.part is not None else np.zeros(m.n_nodes, np.int32)
+    g = mgn.mgn_graph_build(m.send, m.recv, part, m.n_nodes, cfg.part)
+    loc = case.local_inputs(g["l2g"], g["eperm"], g["n_owned"], g["n_halo"])
+    say(f"[full] {cfg.name}: owned {g['n_owned']}, halo {g['n_halo']}, edges {g['n_edges']}")
+    return case, g, loc
+
+
+def _free(s):
+    import torch
+    s.close()
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["C3", "C4"])
+def test_sampled_outputs_and_gradients(name):
+    cfg = synth.CONFIGS[name]
+    case, g, loc = _inputs(cfg)
+    no, l, K, D = g["n_owned"], cfg.latent, cfg.K, cfg.depth
+    r_mid, z_mid = (100 if name == "C4" else 50) // 2, 250
+    centers = np.array([0, r_mid * 500 + z_mid])
+    d_out = np.zeros((no, 5), np.float32)
+    d_out[centers] = np.random.default_rng([cfg.seed, 5]).standard_normal((centers.size, 5)).astype(np.float32)
+    s = Session(l, K, D, cfg.precision, g, loc["node_feat"], loc["edge_feat"], loc["halo"], case.params)
+    try:
+        say(f"[full] {name}: GPU step")
+        out = s.forward().cpu().numpy()
+        dp, dh = s.backward(d_out)
+        dp, dh = dp.cpu().numpy().copy(), dh.cpu().numpy().copy()
+    finally:
+        _free(s)
+    c = cone(g, centers, K)
+    say(f"[full] {name}: receptive field {c['n_owned']} owned + {c['n_halo']} halo nodes, {c['n_edges']} edges")
+    sub = dict(g=c, shapes=case.shapes, params=case.params, nf=loc["node_feat"][c["owned"]],
+               ef=loc["edge_feat"][c["edges"]], halo=loc["halo"][:, c["halo"]],
+               d_out=d_out[c["owned"]])
+    ref = run_oracle(sub, l, K, D, bf16=cfg.precision == "bf16")
+    say(f"[full] {name}: oracle done")
+    cal = calibrate(sub, l, K, D, cfg.precision)
+    say(f"[full] {name}: calibration done")
+    # outputs at the sampled nodes only
+    e_out = rel_err(out[centers], ref["out"][c["centers_sub"]])
+    ref_c = dict(ref)
+    ref_c["out"] = ref["out"][c["centers_sub"]]
+    bad = compare(f"{name} sampled", cfg.precision, case.shapes, (out[centers], dp, dh), ref_c, cal,
+                  halo_sel=c["halo"])
+    assert e_out <= TOL[cfg.precision]
+    assert not bad, bad
+    outside = np.setdiff1d(np.arange(g["n_halo"]), c["halo"])
+    assert not np.any(dh[:, outside]), "halo gradient outside the receptive field must be zero"
+
+
+@pytest.mark.parametrize("name", ["C2", "C3", "C4"])
+def test_full_size_determinism_and_linearity(name):
+    cfg = synth.CONFIGS[name]
+    case, g, loc = _inputs(cfg)
+    d_out = np.random.default_rng([cfg.seed, 6]).standard_normal((g["n_owned"], 5)).astype(np.float32)
+    s = Session(cfg.latent, cfg.K, cfg.depth, cfg.precision, g, loc["node_feat"], loc["edge_feat"], loc["halo"],
+                case.params)
+    try:
+        say(f"[full] {name}: run 1")
+        o1 = s.forward().cpu().numpy().copy()
+        p1, h1 = (x.cpu().numpy().copy() if x is not None else None for x in s.backward(d_out))
+        say(f"[full] {name}: run 2")
+        o2 = s.forward().cpu().numpy().copy()
+        p2, h2 = (x.cpu().numpy().copy() if x is not None else None for x in s.backward(d_out))
+        assert np.array_equal(o1, o2) and np.array_equal(p1, p2)
+        if h1 is not None:
+            assert np.array_equal(h1, h2)
+        say(f"[full] {name}: doubled loss gradient")
+        p3, h3 = (x.cpu().numpy().copy() if x is not None else None for x in s.backward(2.0 * d_out))
+        assert np.array_equal(p3, 2.0 * p1)
+        if h1 is not None:
+            assert np.array_equal(h3, 2.0 * h1)
+        assert np.all(np.isfinite(o1)) and np.all(np.isfinite(p1))
+    finally:
+        _free(s)
+
+
+def test_c5_needs_checkpointing():
+    pytest.skip("C5 (4M owned nodes, l=256, D=3) needs the checkpointed edge stream, not built yet: "
+                "keeping every block's edge latents would take ~430 GB")

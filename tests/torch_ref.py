@@ -14,7 +14,7 @@ from torch import nn
 
 
 def _bf16(x):
-    return x.to(torch.bfloat16).to(torch.float64)
+    return x.to(torch.bfloat16).to(x.dtype)
 
 
 class _LinearBf16(torch.autograd.Function):
@@ -67,18 +67,20 @@ def _mlp(fin, fout, latent, depth, ln):
             layers.append(nn.ReLU())
     if ln:
         layers.append(nn.LayerNorm(fout, eps=1e-5))
-    return nn.Sequential(*layers).double()
+    return nn.Sequential(*layers)
 
 
 class TorchMGN(nn.Module):
-    def __init__(self, latent, K, depth, node_in=11, edge_in=4, node_out=5):
+    def __init__(self, latent, K, depth, node_in=11, edge_in=4, node_out=5, dtype=torch.float64):
         super().__init__()
+        self.dtype = dtype
         self.l, self.K = latent, K
         self.enc_node = _mlp(node_in, latent, latent, depth, True)
         self.enc_edge = _mlp(edge_in, latent, latent, depth, True)
         self.edge = nn.ModuleList([_mlp(3 * latent, latent, latent, depth, True) for _ in range(K)])
         self.node = nn.ModuleList([_mlp(2 * latent, latent, latent, depth, True) for _ in range(K)])
         self.dec = _mlp(latent, node_out, latent, depth, False)
+        self.to(dtype)
 
     def ordered_tensors(self):
         """Parameter tensors in the flat layout order."""
@@ -99,13 +101,13 @@ class TorchMGN(nn.Module):
             for t, (_, _, shape) in zip(ts, shapes):
                 n = int(np.prod(shape))
                 assert tuple(t.shape) == tuple(shape)
-                t.copy_(torch.as_tensor(np.asarray(flat[off:off + n], np.float64).reshape(shape)))
+                t.copy_(torch.as_tensor(np.asarray(flat[off:off + n], np.float64).reshape(shape)).to(t.dtype))
                 off += n
         assert off == len(flat)
 
     def flat_grad(self):
-        return torch.cat([t.grad.reshape(-1) if t.grad is not None else torch.zeros(t.numel(), dtype=torch.float64)
-                          for t in self.ordered_tensors()])
+        return torch.cat([t.grad.reshape(-1).double() if t.grad is not None
+                          else torch.zeros(t.numel(), dtype=torch.float64) for t in self.ordered_tensors()])
 
     def forward(self, g, node_feat, edge_feat, halo, bf16=False):
         """g: partition-local graph (row_ptr, send, n_owned, n_halo).  halo:
@@ -121,21 +123,25 @@ class TorchMGN(nn.Module):
             vk = torch.cat([v, halo[k]], 0) if nh > 0 else v
             m = _apply(self.edge[k], torch.cat([e, vk.index_select(0, send), vk.index_select(0, recv)], 1), bf16)
             e = R(e + m)
-            agg = torch.zeros(no, self.l, dtype=torch.float64).index_add(0, recv, m)
+            agg = torch.zeros(no, self.l, dtype=self.dtype).index_add(0, recv, m)
             v = v + _apply(self.node[k], torch.cat([v, agg], 1), bf16)
         return _apply(self.dec, v, bf16)
 
 
-def run(latent, K, depth, shapes, g, params, node_feat, edge_feat, halo, d_out, bf16=False):
-    """Returns out, flat d_params, d_halo (numpy float64)."""
+def run(latent, K, depth, shapes, g, params, node_feat, edge_feat, halo, d_out, bf16=False,
+        dtype=torch.float64):
+    """Returns out, flat d_params, d_halo (numpy float64).  dtype float32 gives
+    an independent single-precision implementation (used to measure how far
+    a correct single-precision computation sits from the float64 oracle)."""
     torch.manual_seed(0)
-    model = TorchMGN(latent, K, depth)
+    model = TorchMGN(latent, K, depth, dtype=dtype)
     model.load_flat(params, shapes)
-    nf = torch.as_tensor(np.asarray(node_feat, np.float64))
-    ef = torch.as_tensor(np.asarray(edge_feat, np.float64))
+    nf = torch.as_tensor(np.asarray(node_feat, np.float64)).to(dtype)
+    ef = torch.as_tensor(np.asarray(edge_feat, np.float64)).to(dtype)
     nh = g["n_halo"]
-    H = torch.as_tensor(np.asarray(halo, np.float64) if nh > 0 else np.zeros((K, 0, latent))).clone().requires_grad_(True)
+    H = torch.as_tensor(np.asarray(halo, np.float64) if nh > 0 else np.zeros((K, 0, latent))).to(dtype)
+    H = H.clone().requires_grad_(True)
     out = model(g, nf, ef, H, bf16=bf16)
-    out.backward(torch.as_tensor(np.asarray(d_out, np.float64)))
-    dh = H.grad.numpy() if H.grad is not None else np.zeros((K, nh, latent))
-    return out.detach().numpy(), model.flat_grad().numpy(), dh
+    out.backward(torch.as_tensor(np.asarray(d_out, np.float64)).to(dtype))
+    dh = H.grad.double().numpy() if H.grad is not None else np.zeros((K, nh, latent))
+    return out.detach().double().numpy(), model.flat_grad().numpy(), dh
