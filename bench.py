@@ -61,6 +61,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="C4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed region, copy 1 GiB once (a plain copy kernel of known size, "
+                         "for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (pass --gpus 1)", file=sys.stderr)
@@ -125,7 +128,13 @@ def main():
         roof = dict(bound="hbm", achieved=by / t_launch / 1e9, peak=PEAK["hbm"] / 1e9, unit="GB/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["kernel"] = dom
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(dom, cfg.name)
+    if args.copy_calibration:
+        src = torch.ones(2 ** 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     value = ne * cfg.K / (ms * 1e-3)
 
     cpu = None
@@ -145,6 +154,29 @@ def main():
         "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},
     }
     print(json.dumps(line), flush=True)
+
+
+def measured_traffic(kernel: str, config: str):
+    """HBM bytes per launch of `kernel` from a committed counter summary
+    (profiles/<kernel>_<config>_traffic.txt: FETCH_SIZE and WRITE_SIZE per
+    launch, scaled by the counters of a plain copy of known size), used only
+    while the kernels are the ones the counters were taken on."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{config}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    src = open(os.path.join(ROOT, "paper_2307_13592_amd", "csrc", "kernels.hip"), "rb").read()
+    if vals.get("kernels_sha256") != hashlib.sha256(src).hexdigest():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(cfg, g, loc, case):

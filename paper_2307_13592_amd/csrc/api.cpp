@@ -36,7 +36,7 @@ struct MlpL {
 };
 
 struct WsPlan {
-  size_t erecv, chunk, unit_r, nunits, V, AGG, ES, DV[2], DAGG, DE[2], G, DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
+  size_t erecv, chunk, unit_r, nunits, V, V16, AGG, ES, DV[2], DAGG, DE[2], G, DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
       PART, VPART, total;
   int64_t max_units;
 };
@@ -181,6 +181,8 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.unit_r = take(4 * (size_t)(p.max_units + 1));
   p.nunits = take(4);
   p.V = take(4 * (size_t)(K + 1) * no * L);
+  // bf16 mode: bf16 copy of every block's node input, owned then halo rows
+  p.V16 = m->prec == BF16 ? take(2 * (size_t)(K + 1) * (no + g->n_halo) * L) : 0;
   p.AGG = take(4 * (size_t)K * no * L);
   p.ES = take(ts * (size_t)std::max<int64_t>(K, 1) * ne * L);
   p.DV[0] = take(4 * (size_t)no * L);
@@ -402,6 +404,10 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
   auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)k * no * L; };
   auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)k * no * L; };
   auto ES = [&](int k) { return (void*)(ws + p.ES + ts * (size_t)k * ne * L); };
+  const int64_t v16_stride = (no + nh) * L;  // elements per block of the bf16 node copy
+  auto V16 = [&](int k) -> void* {
+    return m->prec == BF16 ? (void*)((uint16_t*)(ws + p.V16) + (size_t)k * v16_stride) : nullptr;
+  };
   int32_t* erecv = (int32_t*)(ws + p.erecv);
   int32_t* unit_r = (int32_t*)(ws + p.unit_r);
   int32_t* n_units = (int32_t*)(ws + p.nunits);
@@ -413,6 +419,11 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
       e = launch_plan(g->row_ptr, no, 4 * te, 4 * te, (int32_t*)(ws + p.chunk), unit_r, n_units, st);
   }
   if (e != hipSuccess) return hip_fail(m, e, "mgn_forward plan");
+  if (m->prec == BF16 && K > 0 && nh > 0) {
+    Timed t_(m, MGN_T_OTHER, st);
+    e = launch_halo_bf16(halo, K, nh, no, L, V16(0), v16_stride, st);
+    if (e != hipSuccess) return hip_fail(m, e, "mgn_forward halo copy");
+  }
 
   RowsFwdArgs ra{};
   ra.eps = m->cfg.ln_eps;
@@ -422,6 +433,7 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
   ra.fin = m->cfg.node_in;
   ra.in0 = nf;
   ra.out = V(0);
+  ra.out16 = V16(0);
   {
     Timed t_(m, MGN_T_ENCODE, st);
     e = launch_rows_fwd(m->prec, L, D, ENC_NODE, ra, st);
@@ -433,6 +445,7 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
     ra.fin = m->cfg.edge_in;
     ra.in0 = ef;
     ra.out = ES(0);
+    ra.out16 = nullptr;
     {
       Timed t_(m, MGN_T_ENCODE, st);
       e = launch_rows_fwd(m->prec, L, D, ENC_EDGE, ra, st);
@@ -449,6 +462,7 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
     ea.n_units = n_units;
     ea.V = V(k);
     ea.H = nh > 0 ? halo + (size_t)k * nh * L : nullptr;
+    ea.V16 = V16(k);
     ea.n_owned = no;
     ea.Ein = ES(k);
     ea.Eout = k + 1 < K ? ES(k + 1) : nullptr;
@@ -465,6 +479,7 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
     na.in0 = V(k);
     na.in1 = AGG(k);
     na.out = V(k + 1);
+    na.out16 = V16(k + 1);
     na.eps = m->cfg.ln_eps;
     {
       Timed t_(m, MGN_T_NODE_FWD, st);
@@ -550,6 +565,9 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
   auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)k * no * L; };
   auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)k * no * L; };
   auto ES = [&](int k) { return (void*)(ws + p.ES + ts * (size_t)k * ne * L); };
+  auto V16 = [&](int k) -> void* {
+    return m->prec == BF16 ? (void*)((uint16_t*)(ws + p.V16) + (size_t)k * (no + nh) * L) : nullptr;
+  };
   float* DV[2] = {(float*)(ws + p.DV[0]), (float*)(ws + p.DV[1])};
   float* DE[2] = {(float*)(ws + p.DE[0]), (float*)(ws + p.DE[1])};
   float* DAGG = (float*)(ws + p.DAGG);
@@ -662,6 +680,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.n_units = (int32_t*)(ws + p.nunits);
       a.V = V(k);
       a.H = Hk;
+      a.V16 = V16(k);
       a.n_owned = no;
       a.Ein = ES(k);
       a.de_next = (k == K - 1) ? nullptr : DE[a_];

@@ -20,6 +20,7 @@ struct RowsFwdArgs {
   const float* in0;  // ENC: features [rows][fin]; NODE/DEC: v [rows][L]
   const float* in1;  // NODE: aggregated messages [rows][L]
   void* out;         // ENC_NODE, NODE, DEC: fp32; ENC_EDGE: storage type
+  void* out16;       // ENC_NODE, NODE in bf16 mode: bf16 copy of the output rows (or null)
   float eps;
 };
 
@@ -32,6 +33,7 @@ struct EdgeFwdArgs {
   const int32_t* n_units;
   const float* V;  // block input, owned rows [n_owned][L]
   const float* H;  // block input, halo rows [n_halo][L]
+  const void* V16;  // bf16 mode: bf16 copy of the block input, owned then halo rows [n_owned+n_halo][L]
   int64_t n_owned;
   const void* Ein;  // edge latents in [E][L] (storage type)
   void* Eout;       // edge latents out, or null (last block)
@@ -64,6 +66,7 @@ struct EdgeBwdArgs {
   const int32_t* n_units;
   const float* V;
   const float* H;
+  const void* V16;
   int64_t n_owned;
   const void* Ein;      // e^k (storage type)
   const float* de_next; // dL/de^{k+1} [E][L] or null (last block)
@@ -104,6 +107,8 @@ struct VecSeg {
 
 // ------------------------------------------------------------ launchers ---
 hipError_t launch_zero(float* p, int64_t n, hipStream_t st);
+hipError_t launch_halo_bf16(const float* H, int K, int64_t n_halo, int64_t n_owned, int L, void* V16,
+                            int64_t v16_block_stride, hipStream_t st);
 hipError_t launch_pack(int prec, const float* W, int out, int in, int bwd, uint4* dst, int nkg, hipStream_t st);
 hipError_t launch_erecv(const int32_t* row_ptr, int64_t n_owned, int32_t* erecv, hipStream_t st);
 hipError_t launch_plan(const int32_t* row_ptr, int64_t n_owned, int te_target, int r_max, int32_t* chunk_cnt,

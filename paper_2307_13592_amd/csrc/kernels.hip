@@ -262,6 +262,31 @@ hipError_t launch_zero(float* p, int64_t n, hipStream_t st) {
   return hipGetLastError();
 }
 
+// bf16 copy of the halo latents of every block: V16[k][n_owned + h] = H[k][h].
+__global__ void halo_bf16_kernel(const float* __restrict__ H, int K, int64_t n_halo, int64_t n_owned, int L,
+                                 uint16_t* __restrict__ V16, int64_t stride) {
+  const int64_t per = n_halo * L / 4;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < (int64_t)K * per;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t k = i / per, j = i % per;
+    const float4 v = reinterpret_cast<const float4*>(H + k * n_halo * L)[j];
+    uint2 w;
+    w.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+    w.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+    reinterpret_cast<uint2*>(V16 + k * stride + n_owned * L)[j] = w;
+  }
+}
+
+hipError_t launch_halo_bf16(const float* H, int K, int64_t n_halo, int64_t n_owned, int L, void* V16,
+                            int64_t v16_block_stride, hipStream_t st) {
+  const int64_t n = (int64_t)K * n_halo * L / 4;
+  if (n == 0) return hipSuccess;
+  const int64_t g = (n + NT - 1) / NT;
+  hipLaunchKernelGGL(halo_bf16_kernel, dim3((unsigned)(g < 8192 ? g : 8192)), dim3(NT), 0, st, H, K, n_halo, n_owned,
+                     L, reinterpret_cast<uint16_t*>(V16), v16_block_stride);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------- planning ---
 __global__ void erecv_kernel(const int32_t* __restrict__ row_ptr, int64_t n_owned, int32_t* __restrict__ erecv) {
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -487,6 +512,7 @@ __global__ __launch_bounds__(NT) void rows_fwd_kernel(RowsFwdArgs a) {
       }
     } else {
       float* out = reinterpret_cast<float*>(a.out);
+      uint16_t* out16 = reinterpret_cast<uint16_t*>(a.out16);
       constexpr int Q = L / 4;
       for (int i = threadIdx.x; i < n * Q; i += NT) {
         const int r = i / Q, c4 = i % Q;
@@ -499,6 +525,12 @@ __global__ __launch_bounds__(NT) void rows_fwd_kernel(RowsFwdArgs a) {
           y.w += v.w;
         }
         reinterpret_cast<float4*>(out + (row0 + r) * L)[c4] = y;
+        if (out16) {
+          uint2 w;
+          w.x = (uint32_t)f2bf(y.x) | ((uint32_t)f2bf(y.y) << 16);
+          w.y = (uint32_t)f2bf(y.z) | ((uint32_t)f2bf(y.w) << 16);
+          reinterpret_cast<uint2*>(out16 + (row0 + r) * L)[c4] = w;
+        }
       }
     }
     __syncthreads();
@@ -727,7 +759,8 @@ struct EdgeMeta {
 template <class P, int L, int TE, int LDA>
 __device__ __forceinline__ void stage_edges(typename P::T* A, EdgeMeta mt, const int32_t* erecv,
                                             const int32_t* send, const typename P::T* Ein, const float* V,
-                                            const float* H, int64_t n_owned, int64_t sb, int n, int64_t e1) {
+                                            const float* H, const void* V16, int64_t n_owned, int64_t sb, int n,
+                                            int64_t e1) {
   using T = typename P::T;
   const int tid = threadIdx.x;
   if (tid < 64) {
@@ -749,6 +782,29 @@ __device__ __forceinline__ void stage_edges(typename P::T* A, EdgeMeta mt, const
   __syncthreads();
   constexpr int E16 = 16 / sizeof(T);
   constexpr int CPR = L / E16;                   // 16-byte chunks per e row
+  if constexpr (sizeof(T) == 2) {
+    // bf16: e^k rows and the bf16 copy of the node rows, 16-byte chunks
+    const T* V16t = reinterpret_cast<const T*>(V16);
+    constexpr int IT = (TE * 3 * CPR + NT - 1) / NT;
+    uint4 buf[IT];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int i = tid + j * NT, r = i / (3 * CPR), rem = i % (3 * CPR), part = rem / CPR;
+      const int c = (rem % CPR) * E16;
+      buf[j] = make_uint4(0, 0, 0, 0);
+      if (i < TE * 3 * CPR && r < n) {
+        const T* src = part == 0 ? Ein + (sb + r) * L : V16t + (int64_t)(part == 1 ? mt.ss[r] : mt.rr[r]) * L;
+        buf[j] = *reinterpret_cast<const uint4*>(src + c);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int i = tid + j * NT, r = i / (3 * CPR), rem = i % (3 * CPR), part = rem / CPR;
+      const int c = (rem % CPR) * E16;
+      if (i < TE * 3 * CPR) *reinterpret_cast<uint4*>(A + r * LDA + part * L + c) = buf[j];
+    }
+    return;
+  }
   constexpr int IE = (TE * CPR + NT - 1) / NT;
   constexpr int Q = L / 4;                       // float4 per node row
   constexpr int IV = (TE * 2 * Q + NT - 1) / NT;
@@ -837,6 +893,17 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
   const bool wave_has_cols = wave * NBW * 16 < L;
   const T* Ein = reinterpret_cast<const T*>(a.Ein);
   T* Eout = reinterpret_cast<T*>(a.Eout);
+  // weight-stationary when the wave's weight slices fit in registers
+  constexpr int NK1 = 3 * L / P::KG, NKH = L / P::KG;
+  constexpr bool WS = (NK1 + (D - 1) * NKH) * NBW * 4 <= 160;
+  uint4 w1[WS ? NK1 : 1][NBW], wh[WS && D == 3 ? NKH : 1][NBW], wl[WS ? NKH : 1][NBW];
+  if constexpr (WS) {
+    if (wave_has_cols) {
+      load_weights(a.mlp.lin[0].wf, wave * NBW, w1);
+      if constexpr (D == 3) load_weights(a.mlp.lin[1].wf, wave * NBW, wh);
+      load_weights(a.mlp.lin[D - 1].wf, wave * NBW, wl);
+    }
+  }
 
   for (TileIter it(*a.n_units); it.valid(); it.next()) {
     const int64_t r0 = a.unit_r[it.t], r1 = a.unit_r[it.t + 1];
@@ -845,12 +912,15 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
     float run = 0.f;  // running receiver sum of column tid
     for (int64_t sb = e0; sb < e1; sb += TE) {
       const int n = (int)(e1 - sb < TE ? e1 - sb : TE);
-      stage_edges<P, L, TE, Lay::LDA>(A, mt, a.erecv, a.send, Ein, a.V, a.H, a.n_owned, sb, n, e1);
+      stage_edges<P, L, TE, Lay::LDA>(A, mt, a.erecv, a.send, Ein, a.V, a.H, a.V16, a.n_owned, sb, n, e1);
       __syncthreads();
       {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm_k<P, MB, NBW, 3 * L / P::KG>(A, Lay::LDA, a.mlp.lin[0].wf, wave * NBW, acc);
+          if constexpr (WS)
+            wave_gemm_reg<P, MB, NBW, NK1>(A, Lay::LDA, w1, acc);
+          else
+            wave_gemm_k<P, MB, NBW, NK1>(A, Lay::LDA, a.mlp.lin[0].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[0].b, L, HB, Lay::LDH);
         }
       }
@@ -859,7 +929,10 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
       if constexpr (D == 3) {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm_k<P, MB, NBW, L / P::KG>(HB, Lay::LDH, a.mlp.lin[1].wf, wave * NBW, acc);
+          if constexpr (WS)
+            wave_gemm_reg<P, MB, NBW, NKH>(HB, Lay::LDH, wh, acc);
+          else
+            wave_gemm_k<P, MB, NBW, NKH>(HB, Lay::LDH, a.mlp.lin[1].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[1].b, L, HC, Lay::LDH);
         }
         __syncthreads();
@@ -868,7 +941,10 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
       {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          wave_gemm_k<P, MB, NBW, L / P::KG>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, wave * NBW, acc);
+          if constexpr (WS)
+            wave_gemm_reg<P, MB, NBW, NKH>(hin, Lay::LDH, wl, acc);
+          else
+            wave_gemm_k<P, MB, NBW, NKH>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, false>(acc, wave * NBW, a.mlp.lin[D - 1].b, L, Y, Lay::LDY);
         }
       }
@@ -933,7 +1009,7 @@ __global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
     float run = 0.f;  // running receiver sum (receiver-side input gradient), column tid
     for (int64_t sb = e0; sb < e1; sb += TE) {
       const int n = (int)(e1 - sb < TE ? e1 - sb : TE);
-      stage_edges<P, L, TE, Lay::LDA>(A, mt, a.erecv, a.send, Ein, a.V, a.H, a.n_owned, sb, n, e1);
+      stage_edges<P, L, TE, Lay::LDA>(A, mt, a.erecv, a.send, Ein, a.V, a.H, a.V16, a.n_owned, sb, n, e1);
       // dm = de^{k+1} + dagg[receiver], all loads of the thread issued first
       constexpr int Q = L / 4;
       constexpr int IM = (TE * Q + NT - 1) / NT;
