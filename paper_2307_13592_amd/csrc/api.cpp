@@ -707,6 +707,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       w.a0 = ES(k);
       w.a1 = V(k);
       w.a2 = Hk;
+      w.a3 = V16(k);
       w.send = g->send;
       w.erecv = erecv;
       w.n_owned = no;

@@ -150,45 +150,6 @@ __device__ __forceinline__ void wave_gemm_k(const typename P::T* A, int lda, con
   }
 }
 
-// Weight-stationary variant: the wave's B fragments of the whole layer are
-// already in registers (loaded once per kernel); only A comes from LDS,
-// double-buffered.
-template <class P, int MB, int NBW, int NKG>
-__device__ __forceinline__ void wave_gemm_reg(const typename P::T* A, int lda, const uint4 (&w)[NKG][NBW],
-                                              floatx4 (&acc)[MB][NBW]) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int m = 0; m < MB; ++m)
-#pragma unroll
-    for (int n = 0; n < NBW; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const typename P::T* Ar = A + (lane & 15) * lda + (lane >> 4) * P::EL;
-  uint4 a[2][MB];
-#pragma unroll
-  for (int m = 0; m < MB; ++m) a[0][m] = *reinterpret_cast<const uint4*>(Ar + m * 16 * lda);
-#pragma unroll
-  for (int kg = 0; kg < NKG; ++kg) {
-    if (kg + 1 < NKG) {
-#pragma unroll
-      for (int m = 0; m < MB; ++m)
-        a[(kg + 1) & 1][m] = *reinterpret_cast<const uint4*>(Ar + m * 16 * lda + (kg + 1) * P::KG);
-    }
-#pragma unroll
-    for (int m = 0; m < MB; ++m)
-#pragma unroll
-      for (int n = 0; n < NBW; ++n) P::mma(acc[m][n], a[kg & 1][m], w[kg][n]);
-  }
-}
-
-// Loads the wave's B fragments (n-blocks nb0.., all k-groups) of a layer.
-template <int NKG, int NBW>
-__device__ __forceinline__ void load_weights(const uint4* __restrict__ Bp, int nb0, uint4 (&w)[NKG][NBW]) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int kg = 0; kg < NKG; ++kg)
-#pragma unroll
-    for (int n = 0; n < NBW; ++n) w[kg][n] = Bp[((size_t)(nb0 + n) * NKG + kg) * 64 + lane];
-}
-
 // Row / column of accumulator element r (0..3) of a 16x16 MFMA block for
 // this lane: row 4*(lane/16) + r, column lane%16.
 __device__ __forceinline__ int acc_row(int r) { return ((threadIdx.x & 63) >> 4) * 4 + r; }

@@ -90,6 +90,7 @@ struct DwArgs {
   int lda0;
   const float* a1;    // node concat: agg; edge concat: V (owned)
   const float* a2;    // edge concat: H (halo)
+  const void* a3;     // edge concat, bf16 mode: bf16 copy of the node rows (owned then halo), or null
   const int32_t* send;
   const int32_t* erecv;
   int64_t n_owned;

@@ -745,6 +745,14 @@ struct EdgeTE {
                                                                       : 16;
 };
 
+// Backward sub-tiles are capped at 32 rows: the smaller LDS footprint lets
+// two workgroups share a CU, which hides more gather latency than the larger
+// tile saves in weight-fragment reloads.
+template <class P, int L, int D>
+struct EdgeTEB {
+  static constexpr int value = EdgeTE<P, L, D>::value > 32 ? 32 : EdgeTE<P, L, D>::value;
+};
+
 // Per-row metadata of a sub-tile in LDS: receiver and sender local ids, and a
 // bit mask of the rows that end their receiver's segment.
 struct EdgeMeta {
@@ -873,7 +881,10 @@ __device__ __forceinline__ void zero_empty_receivers(const int32_t* row_ptr, int
 }
 
 template <int P_, int L, int D>
-__global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
+// Two waves per SIMD: the register budget is capped so that two workgroups
+// can be resident, which the edge gather's latency needs more than the
+// products need registers.
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void edge_fwd_kernel(EdgeFwdArgs a) {
   using P = typename PrecOf<P_>::type;
   using T = typename P::T;
   constexpr int TE = EdgeTE<P, L, D>::value;
@@ -893,17 +904,7 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
   const bool wave_has_cols = wave * NBW * 16 < L;
   const T* Ein = reinterpret_cast<const T*>(a.Ein);
   T* Eout = reinterpret_cast<T*>(a.Eout);
-  // weight-stationary when the wave's weight slices fit in registers
   constexpr int NK1 = 3 * L / P::KG, NKH = L / P::KG;
-  constexpr bool WS = (NK1 + (D - 1) * NKH) * NBW * 4 <= 160;
-  uint4 w1[WS ? NK1 : 1][NBW], wh[WS && D == 3 ? NKH : 1][NBW], wl[WS ? NKH : 1][NBW];
-  if constexpr (WS) {
-    if (wave_has_cols) {
-      load_weights(a.mlp.lin[0].wf, wave * NBW, w1);
-      if constexpr (D == 3) load_weights(a.mlp.lin[1].wf, wave * NBW, wh);
-      load_weights(a.mlp.lin[D - 1].wf, wave * NBW, wl);
-    }
-  }
 
   for (TileIter it(*a.n_units); it.valid(); it.next()) {
     const int64_t r0 = a.unit_r[it.t], r1 = a.unit_r[it.t + 1];
@@ -917,10 +918,7 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
       {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          if constexpr (WS)
-            wave_gemm_reg<P, MB, NBW, NK1>(A, Lay::LDA, w1, acc);
-          else
-            wave_gemm_k<P, MB, NBW, NK1>(A, Lay::LDA, a.mlp.lin[0].wf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, NK1>(A, Lay::LDA, a.mlp.lin[0].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[0].b, L, HB, Lay::LDH);
         }
       }
@@ -929,10 +927,7 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
       if constexpr (D == 3) {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          if constexpr (WS)
-            wave_gemm_reg<P, MB, NBW, NKH>(HB, Lay::LDH, wh, acc);
-          else
-            wave_gemm_k<P, MB, NBW, NKH>(HB, Lay::LDH, a.mlp.lin[1].wf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, NKH>(HB, Lay::LDH, a.mlp.lin[1].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[1].b, L, HC, Lay::LDH);
         }
         __syncthreads();
@@ -941,10 +936,7 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
       {
         floatx4 acc[MB][NBW];
         if (wave_has_cols) {
-          if constexpr (WS)
-            wave_gemm_reg<P, MB, NBW, NKH>(hin, Lay::LDH, wl, acc);
-          else
-            wave_gemm_k<P, MB, NBW, NKH>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, wave * NBW, acc);
+          wave_gemm_k<P, MB, NBW, NKH>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, wave * NBW, acc);
           store_acc<P, MB, NBW, false>(acc, wave * NBW, a.mlp.lin[D - 1].b, L, Y, Lay::LDY);
         }
       }
@@ -972,10 +964,10 @@ __global__ __launch_bounds__(NT) void edge_fwd_kernel(EdgeFwdArgs a) {
 }
 
 template <int P_, int L, int D>
-__global__ __launch_bounds__(NT) void edge_bwd_kernel(EdgeBwdArgs a) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void edge_bwd_kernel(EdgeBwdArgs a) {
   using P = typename PrecOf<P_>::type;
   using T = typename P::T;
-  constexpr int TE = EdgeTE<P, L, D>::value;
+  constexpr int TE = EdgeTEB<P, L, D>::value;
   using Lay = EdgeLds<P, L, D, TE>;
   constexpr int MB = TE / 16;
   constexpr int NBW = L / 16 / NW > 0 ? L / 16 / NW : 1;
@@ -1190,47 +1182,57 @@ __global__ __launch_bounds__(NT) void sender_gather_kernel(int64_t n_local, int6
 // MFMA GEMM with both operands staged transposed in LDS (rows contiguous).
 constexpr int DW_TO = 128, DW_TI = 128, DW_RC = 64;
 
+// EL consecutive elements (16 bytes of storage type) of row `row` of the
+// weight-gradient input operand, starting at column col, as storage type.
 template <class P>
-__device__ __forceinline__ void dw_load_a(const DwArgs& a, int64_t row, int col, float* v /*EL values*/) {
+__device__ __forceinline__ uint4 dw_load_a(const DwArgs& a, int64_t row, int col) {
   using T = typename P::T;
+  T v[P::EL];
   if (a.a_kind == 0) {
-    const T* src = reinterpret_cast<const T*>(a.a0) + row * a.lda0 + col;
-#pragma unroll
-    for (int e = 0; e < P::EL; ++e) v[e] = P::tof(src[e]);
+    return *reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.a0) + row * a.lda0 + col);
   } else if (a.a_kind == 1) {
     const float* src = reinterpret_cast<const float*>(a.a0) + row * a.lda0 + col;
 #pragma unroll
-    for (int e = 0; e < P::EL; ++e) v[e] = (col + e < a.lda0) ? src[e] : 0.f;
+    for (int e = 0; e < P::EL; ++e) v[e] = P::cvt((col + e < a.lda0) ? src[e] : 0.f);
   } else if (a.a_kind == 2) {
     const int L = a.L;
-    const float* src;
-    if (col < L) {
-      const T* s = reinterpret_cast<const T*>(a.a0) + row * L + col;
-#pragma unroll
-      for (int e = 0; e < P::EL; ++e) v[e] = P::tof(s[e]);
-      return;
-    } else if (col < 2 * L) {
-      const int64_t snd = a.send[row];
-      src = snd < a.n_owned ? a.a1 + snd * L : a.a2 + (snd - a.n_owned) * L;
-      src += col - L;
-    } else {
-      src = a.a1 + (int64_t)a.erecv[row] * L + (col - 2 * L);
+    if (col < L) return *reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.a0) + row * L + col);
+    const int64_t node = col < 2 * L ? (int64_t)a.send[row] : (int64_t)a.erecv[row];
+    const int c = col < 2 * L ? col - L : col - 2 * L;
+    if (a.a3) {  // bf16 copy of the node rows, owned then halo
+      return *reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.a3) + node * L + c);
     }
+    const float* src = node < a.n_owned ? a.a1 + node * L + c : a.a2 + (node - a.n_owned) * L + c;
 #pragma unroll
-    for (int e = 0; e < P::EL; ++e) v[e] = P::tof(P::cvt(src[e]));
+    for (int e = 0; e < P::EL; ++e) v[e] = P::cvt(src[e]);
   } else {
     const int L = a.L;
     const float* src = (col < L ? reinterpret_cast<const float*>(a.a0) + row * L + col : a.a1 + row * L + (col - L));
 #pragma unroll
-    for (int e = 0; e < P::EL; ++e) v[e] = P::tof(P::cvt(src[e]));
+    for (int e = 0; e < P::EL; ++e) v[e] = P::cvt(src[e]);
   }
+  return *reinterpret_cast<const uint4*>(v);
+}
+
+// Transposed LDS tiles [column][row] of DW_RC rows.  A wave stores 16 rows
+// of four column groups (EL columns each) at once.  In fp32 the row padding
+// alone spreads them over the banks; in bf16 the four groups' columns are
+// 8 apart, which the padding maps onto the same banks, so the row index is
+// XORed with 16 * ((column / 8) % 4).  Aligned 16-element runs stay
+// contiguous, so MFMA fragments (EL consecutive rows) remain 16-byte reads.
+template <class P>
+__device__ __forceinline__ int dw_swz(int col, int r) {
+  if constexpr (P::EL == 4) return r;
+  else return r ^ (16 * ((col >> 3) & 3));
 }
 
 template <int P_>
-__global__ __launch_bounds__(NT) void dw_kernel(DwArgs a) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void dw_kernel(DwArgs a) {
   using P = typename PrecOf<P_>::type;
   using T = typename P::T;
   constexpr int LDT = DW_RC + P::PAD;
+  constexpr int GPR = DW_TO / P::EL;              // 16-byte groups per operand row
+  constexpr int IT = DW_RC * GPR / NT;            // loads per thread per operand per chunk
   __shared__ __align__(16) T Dt[DW_TO * LDT];
   __shared__ __align__(16) T At[DW_TI * LDT];
   const int ot = blockIdx.x, itl = blockIdx.y, s = blockIdx.z;
@@ -1245,41 +1247,66 @@ __global__ __launch_bounds__(NT) void dw_kernel(DwArgs a) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
   const T* dl = reinterpret_cast<const T*>(a.delta);
-  for (int64_t c0 = rb; c0 < re; c0 += DW_RC) {
-    // stage transposed: Dt[o][r] = delta[c0 + r][o0 + o], At[i][r] = A[c0 + r][i0 + i]
-    constexpr int GPR = DW_TO / P::EL;  // EL-wide groups per row
-    for (int idx = threadIdx.x; idx < DW_RC * GPR; idx += NT) {
-      const int r = idx / GPR, g = (idx % GPR) * P::EL;
+  // thread -> (row, column group): 16 consecutive rows per 16 lanes, four
+  // column groups per wave (64 contiguous bytes of each row per wave)
+  auto rowof = [&](int j) { const int idx = threadIdx.x + j * NT; return (idx & 15) + 16 * (idx / (16 * GPR)); };
+  auto grpof = [&](int j) { const int idx = threadIdx.x + j * NT; return ((idx >> 4) % GPR) * P::EL; };
+  uint4 rd[IT], ra[IT];
+  auto load = [&](int64_t c0) {
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int r = rowof(j), g = grpof(j);
       const int64_t row = c0 + r;
-      const bool ok = row < re;
+      rd[j] = make_uint4(0, 0, 0, 0);
+      ra[j] = make_uint4(0, 0, 0, 0);
+      if (row < re) {
+        if (o0 + g < a.O) {
+          if (o0 + g + P::EL <= a.ldd && (a.ldd % P::EL) == 0) {
+            rd[j] = *reinterpret_cast<const uint4*>(dl + row * a.ldd + o0 + g);
+          } else {
+            T v[P::EL];
+#pragma unroll
+            for (int e = 0; e < P::EL; ++e) v[e] = (o0 + g + e < a.O) ? dl[row * a.ldd + o0 + g + e] : P::cvt(0.f);
+            rd[j] = *reinterpret_cast<const uint4*>(v);
+          }
+        }
+        if (i0 + g < a.I) ra[j] = dw_load_a<P>(a, row, i0 + g);
+      }
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int r = rowof(j), g = grpof(j);
+      const T* vd = reinterpret_cast<const T*>(&rd[j]);
+      const T* va = reinterpret_cast<const T*>(&ra[j]);
 #pragma unroll
       for (int e = 0; e < P::EL; ++e) {
-        const int o = o0 + g + e;
-        Dt[(g + e) * LDT + r] = (ok && o < a.O) ? dl[row * a.ldd + o] : P::cvt(0.f);
+        const int c = g + e;
+        Dt[c * LDT + dw_swz<P>(c, r)] = (o0 + c < a.O) ? vd[e] : P::cvt(0.f);
+        At[c * LDT + dw_swz<P>(c, r)] = (i0 + c < a.I) ? va[e] : P::cvt(0.f);
       }
-      float v[P::EL];
-      const int i = i0 + g;
-      if (ok && i < a.I) {
-        dw_load_a<P>(a, row, i, v);
-      } else {
-#pragma unroll
-        for (int e = 0; e < P::EL; ++e) v[e] = 0.f;
-      }
-#pragma unroll
-      for (int e = 0; e < P::EL; ++e) At[(g + e) * LDT + r] = P::cvt((i + e < a.I) ? v[e] : 0.f);
     }
+  };
+  if (rb < re) load(rb);
+  for (int64_t c0 = rb; c0 < re; c0 += DW_RC) {
+    store();
     __syncthreads();
+    if (c0 + DW_RC < re) load(c0 + DW_RC);  // next chunk in flight during the products
 #pragma unroll
     for (int kg = 0; kg < DW_RC / P::KG; ++kg) {
       uint4 af[4], bf[4];
+      const int kk = kg * P::KG + (lane >> 4) * P::EL;
 #pragma unroll
-      for (int m = 0; m < 4; ++m)
-        af[m] = *reinterpret_cast<const uint4*>(Dt + (wo + m * 16 + (lane & 15)) * LDT + kg * P::KG +
-                                                (lane >> 4) * P::EL);
+      for (int m = 0; m < 4; ++m) {
+        const int c = wo + m * 16 + (lane & 15);
+        af[m] = *reinterpret_cast<const uint4*>(Dt + c * LDT + dw_swz<P>(c, kk));
+      }
 #pragma unroll
-      for (int n = 0; n < 4; ++n)
-        bf[n] = *reinterpret_cast<const uint4*>(At + (wi + n * 16 + (lane & 15)) * LDT + kg * P::KG +
-                                                (lane >> 4) * P::EL);
+      for (int n = 0; n < 4; ++n) {
+        const int c = wi + n * 16 + (lane & 15);
+        bf[n] = *reinterpret_cast<const uint4*>(At + c * LDT + dw_swz<P>(c, kk));
+      }
 #pragma unroll
       for (int m = 0; m < 4; ++m)
 #pragma unroll
@@ -1471,7 +1498,7 @@ static hipError_t edge_fwd_t(const EdgeFwdArgs& a, int grid, hipStream_t st) {
 template <int P_, int L, int D>
 static hipError_t edge_bwd_t(const EdgeBwdArgs& a, int grid, hipStream_t st) {
   using P = typename PrecOf<P_>::type;
-  using Lay = EdgeLds<P, L, D, EdgeTE<P, L, D>::value>;
+  using Lay = EdgeLds<P, L, D, EdgeTEB<P, L, D>::value>;
   allow_lds(edge_bwd_kernel<P_, L, D>, Lay::END);
   hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D>), dim3(grid), dim3(NT), Lay::END, st, a);
   return hipGetLastError();
