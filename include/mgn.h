@@ -178,7 +178,7 @@ typedef enum {
   MGN_T_DECODE = 3,        /* DecNode forward */
   MGN_T_EDGE_BWD = 4,      /* fused edge half, backward with recompute */
   MGN_T_NODE_BWD = 5,      /* node half, decoder and encoders, backward */
-  MGN_T_SENDER_GATHER = 6, /* transposed-CSR gradient gather */
+  MGN_T_INPUT_GRAD = 6,    /* node gradients through the edge MLP's first Linear */
   MGN_T_WEIGHT_GRAD = 7,   /* weight-gradient GEMMs and fixed-order reductions */
   MGN_T_OTHER = 8,         /* planning, loss */
   MGN_T_COUNT = 9

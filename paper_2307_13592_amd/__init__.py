@@ -23,7 +23,7 @@ STATUS_NAMES = ["MGN_OK", "MGN_E_ARG", "MGN_E_GRAPH", "MGN_E_STATE", "MGN_E_NOME
 EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mgn_set_params", "mgn_get_params",
            "mgn_partition_slabs", "mgn_graph_sizes", "mgn_graph_build", "mgn_graph_validate", "mgn_workspace_size",
            "mgn_forward", "mgn_backward", "mgn_mse_grad", "mgn_timing_enable", "mgn_timing_read"]
-TIMERS = ["encode", "edge_fwd", "node_fwd", "decode", "edge_bwd", "node_bwd", "sender_gather", "weight_grad",
+TIMERS = ["encode", "edge_fwd", "node_fwd", "decode", "edge_bwd", "node_bwd", "input_grad", "weight_grad",
           "other"]
 
 

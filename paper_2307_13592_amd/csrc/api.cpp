@@ -36,7 +36,7 @@ struct MlpL {
 };
 
 struct WsPlan {
-  size_t erecv, chunk, unit_r, nunits, V, V16, AGG, ES, DV[2], DAGG, DE[2], G, DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
+  size_t erecv, chunk, unit_r, nunits, V, V16, AGG, ES, DV[2], DAGG, DZS, DE[2], DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
       PART, VPART, total;
   int64_t max_units;
 };
@@ -188,9 +188,9 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.DV[0] = take(4 * (size_t)no * L);
   p.DV[1] = take(4 * (size_t)no * L);
   p.DAGG = take(4 * (size_t)no * L);
+  p.DZS = take(4 * (size_t)(no + g->n_halo) * L);
   p.DE[0] = take(4 * (size_t)ne * L);
   p.DE[1] = take(4 * (size_t)ne * L);
-  p.G = take(4 * (size_t)ne * L);
   for (int j = 0; j < 3; ++j) p.DEL_E[j] = j < m->D ? take(ts * (size_t)ne * L) : 0;
   for (int j = 0; j < 2; ++j) p.HID_E[j] = j < m->D - 1 ? take(ts * (size_t)ne * L) : 0;
   for (int j = 0; j < 3; ++j) p.DEL_N[j] = j < m->D ? take(ts * (size_t)no * std::max<int64_t>(L, 16)) : 0;
@@ -515,24 +515,34 @@ namespace {
 
 // Weight gradient of Linear j of an MLP: split-K GEMM into the partial
 // buffer, then the fixed-order reduction into d_params.
-hipError_t run_dw(mgn_model* m, const LinL& L, DwArgs a, float* d_params, int accumulate, hipStream_t st) {
+// Gradient of Linear L's weight, or of its input columns [col0, col0 + ncols)
+// when ncols >= 0 (the operand a then covers just those columns).
+hipError_t run_dw(mgn_model* m, const LinL& L, DwArgs a, float* d_params, int accumulate, hipStream_t st,
+                  int col0 = 0, int ncols = -1) {
   a.O = L.out;
-  a.I = L.in;
+  a.I = ncols < 0 ? L.in : ncols;
   a.S = dw_splits(a.R, a.O, a.I);
   a.part = (float*)(m->ws + m->plan.PART);
   a.L = m->L;
+  float* dst = d_params + L.w + col0;
   if (a.R == 0) {
     // no rows: the gradient is zero
-    if (!accumulate) return launch_zero(d_params + L.w, (int64_t)L.out * L.in, st);
+    if (accumulate) return hipSuccess;
+    if (ncols < 0) return launch_zero(dst, (int64_t)L.out * L.in, st);
+    for (int o = 0; o < L.out; ++o) {
+      hipError_t e = launch_zero(dst + (size_t)o * L.in, a.I, st);
+      if (e != hipSuccess) return e;
+    }
     return hipSuccess;
   }
   Timed t_(m, MGN_T_WEIGHT_GRAD, st);
   hipError_t e = launch_dw(m->prec, a, st);
-  if (e == hipSuccess) e = launch_dw_reduce(a.part, a.S, a.O, a.I, d_params + L.w, accumulate, st);
+  if (e == hipSuccess) e = launch_dw_reduce(a.part, a.S, a.O, a.I, dst, L.in, accumulate, st);
   return e;
 }
 
-hipError_t run_vec(mgn_model* m, const MlpL& ml, float* d_params, int accumulate, hipStream_t st) {
+hipError_t run_vec(mgn_model* m, const MlpL& ml, float* d_params, int accumulate, hipStream_t st,
+                   int slots = BWD_GRID) {
   VecSeg segs[4];
   int n = 0, off = 0;
   for (int j = 0; j < ml.depth; ++j) {
@@ -541,7 +551,7 @@ hipError_t run_vec(mgn_model* m, const MlpL& ml, float* d_params, int accumulate
   }
   if (ml.gamma >= 0) segs[n++] = VecSeg{off, ml.gamma, 2 * ml.lin[ml.depth - 1].out};
   Timed t_(m, MGN_T_WEIGHT_GRAD, st);
-  return launch_vec_reduce((float*)(m->ws + m->plan.VPART), BWD_GRID, ml.nvec, segs, n, d_params, accumulate, st);
+  return launch_vec_reduce((float*)(m->ws + m->plan.VPART), slots, ml.nvec, segs, n, d_params, accumulate, st);
 }
 
 }  // namespace
@@ -571,7 +581,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
   float* DV[2] = {(float*)(ws + p.DV[0]), (float*)(ws + p.DV[1])};
   float* DE[2] = {(float*)(ws + p.DE[0]), (float*)(ws + p.DE[1])};
   float* DAGG = (float*)(ws + p.DAGG);
-  float* G = (float*)(ws + p.G);
+  float* DZS = (float*)(ws + p.DZS);
   float* VP = (float*)(ws + p.VPART);
   int32_t* erecv = (int32_t*)(ws + p.erecv);
   hipError_t e = hipSuccess;
@@ -686,8 +696,6 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.de_next = (k == K - 1) ? nullptr : DE[a_];
       a.dagg = DAGG;
       a.de_out = DE[b_];
-      a.g = G;
-      a.dv = DV[b_];
       for (int j = 0; j < 3; ++j) a.delta[j] = DEL_E[j];
       for (int j = 0; j < 2; ++j) a.hid[j] = HID_E[j];
       a.vpart = VP;
@@ -698,28 +706,57 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
         e = launch_edge_bwd(m->prec, L, D, a, BWD_GRID, st);
       }
       CHK("edge block");
-      e = run_vec(m, ml, d_params, accumulate, st);
+      e = run_vec(m, ml, d_params, accumulate, st, edge_bwd_grid(m->prec, L, D, BWD_GRID));
       CHK("edge vec");
+      e = dw_hidden(ml, ne, DEL_E, HID_E, L);
+      CHK("edge dW");
+      InGradArgs ig{};
+      ig.w1 = a.mlp.lin[0];
+      ig.trow = g->trow_ptr;
+      ig.tedge = g->tedge;
+      ig.dz = DEL_E[0];
+      ig.dzr = DAGG;
+      ig.dv = DV[b_];
+      ig.dh = d_halo ? d_halo + (size_t)k * nh * L : nullptr;
+      ig.dzs = DZS;
+      ig.n_local = no + nh;
+      ig.n_owned = no;
+      {
+        Timed t_(m, MGN_T_INPUT_GRAD, st);
+        e = launch_input_grad(m->prec, L, ig, st);
+      }
+      CHK("node input gradient");
+      // first Linear's weight gradient by input block: e rows per edge; the
+      // sender / receiver blocks as sums over nodes of (per-node sum of dz_0)
+      // times the node's v (the same sums, reassociated)
       DwArgs w{};
       w.delta = DEL_E[0];
       w.ldd = L;
-      w.a_kind = 2;
+      w.a_kind = 0;
       w.a0 = ES(k);
-      w.a1 = V(k);
-      w.a2 = Hk;
-      w.a3 = V16(k);
-      w.send = g->send;
-      w.erecv = erecv;
-      w.n_owned = no;
+      w.lda0 = L;
       w.R = ne;
-      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
-      CHK("edge dW");
-      e = dw_hidden(ml, ne, DEL_E, HID_E, L);
-      CHK("edge dW");
-      Timed t_(m, MGN_T_SENDER_GATHER, st);
-      e = launch_sender_gather(no + nh, no, g->trow_ptr, g->tedge, G, DV[b_],
-                               d_halo ? d_halo + (size_t)k * nh * L : nullptr, L, st);
-      CHK("sender gather");
+      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st, 0, L);
+      CHK("edge dW (e block)");
+      for (int side = 0; side < 2; ++side) {  // sender block, then receiver block
+        DwArgs wn{};
+        wn.delta = side == 0 ? (const void*)DZS : (const void*)DAGG;
+        wn.d_kind = 1;
+        wn.ldd = L;
+        wn.lda0 = L;
+        wn.R = side == 0 ? no + nh : no;
+        if (m->prec == BF16) {
+          wn.a_kind = 0;
+          wn.a0 = V16(k);
+        } else {
+          wn.a_kind = 4;
+          wn.a0 = V(k);
+          wn.a2 = Hk;
+          wn.n_owned = no;
+        }
+        e = run_dw(m, ml.lin[0], wn, d_params, accumulate, st, (1 + side) * L, L);
+        CHK("edge dW (node blocks)");
+      }
     }
     a_ = b_;
   }

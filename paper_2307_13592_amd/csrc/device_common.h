@@ -108,17 +108,19 @@ __device__ __forceinline__ void wave_gemm(const typename P::T* A, int lda, const
 // Same with the number of k-groups known at compile time, software
 // pipelined: B fragments are fetched PF k-groups ahead (a ring of registers),
 // A fragments one k-group ahead, so neither global nor LDS latency is waited
-// on inside the loop.
-template <class P, int MB, int NBW, int NKG>
+// on inside the loop.  ZERO = false accumulates onto acc.
+template <class P, int MB, int NBW, int NKG, bool ZERO = true>
 __device__ __forceinline__ void wave_gemm_k(const typename P::T* A, int lda, const uint4* __restrict__ Bp, int nb0,
                                             floatx4 (&acc)[MB][NBW]) {
   constexpr int PFW = NBW >= 4 ? 2 : (NBW == 2 ? 4 : 6);  // at most ~8 fragments in flight
   constexpr int PF = NKG < PFW ? NKG : PFW;
   const int lane = threadIdx.x & 63;
+  if constexpr (ZERO) {
 #pragma unroll
-  for (int m = 0; m < MB; ++m)
+    for (int m = 0; m < MB; ++m)
 #pragma unroll
-    for (int n = 0; n < NBW; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int n = 0; n < NBW; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
   const typename P::T* Ar = A + (lane & 15) * lda + (lane >> 4) * P::EL;
   const uint4* Bl = Bp + (size_t)nb0 * NKG * 64 + lane;
   uint4 b[PF][NBW];
@@ -148,6 +150,38 @@ __device__ __forceinline__ void wave_gemm_k(const typename P::T* A, int lda, con
 #pragma unroll
       for (int n = 0; n < NBW; ++n) P::mma(acc[m][n], a[kg & 1][m], bc[n]);
   }
+}
+
+// One 16-column block with the layer's B fragments held in registers (all
+// NKG k-groups, loaded once per kernel); A comes from LDS, one k-group ahead.
+template <class P, int MB, int NKG>
+__device__ __forceinline__ void wave_gemm_w(const typename P::T* A, int lda, const uint4 (&w)[NKG],
+                                            floatx4 (&acc)[MB]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int m = 0; m < MB; ++m) acc[m] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const typename P::T* Ar = A + (lane & 15) * lda + (lane >> 4) * P::EL;
+  uint4 a[2][MB];
+#pragma unroll
+  for (int m = 0; m < MB; ++m) a[0][m] = *reinterpret_cast<const uint4*>(Ar + m * 16 * lda);
+#pragma unroll
+  for (int kg = 0; kg < NKG; ++kg) {
+    if (kg + 1 < NKG) {
+#pragma unroll
+      for (int m = 0; m < MB; ++m)
+        a[(kg + 1) & 1][m] = *reinterpret_cast<const uint4*>(Ar + m * 16 * lda + (kg + 1) * P::KG);
+    }
+#pragma unroll
+    for (int m = 0; m < MB; ++m) P::mma(acc[m], a[kg & 1][m], w[kg]);
+  }
+}
+
+// Loads the B fragments of 16-column block nb (all NKG k-groups) of a packed layer.
+template <int NKG>
+__device__ __forceinline__ void load_block(const uint4* __restrict__ Bp, int nb, uint4 (&w)[NKG]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int kg = 0; kg < NKG; ++kg) w[kg] = Bp[((size_t)nb * NKG + kg) * 64 + lane];
 }
 
 // Row / column of accumulator element r (0..3) of a 16x16 MFMA block for

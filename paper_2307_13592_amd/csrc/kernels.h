@@ -70,10 +70,8 @@ struct EdgeBwdArgs {
   int64_t n_owned;
   const void* Ein;      // e^k (storage type)
   const float* de_next; // dL/de^{k+1} [E][L] or null (last block)
-  const float* dagg;    // [n_owned][L]
+  float* dagg;          // [n_owned][L]: dL/dagg in; each receiver's sum of dz_0 out
   float* de_out;        // dL/de^k [E][L]
-  float* g;             // sender-side input gradients [E][L]
-  float* dv;            // [n_owned][L], receiver-side input gradients are added
   void* delta[3];
   void* hid[2];
   float* vpart;
@@ -81,11 +79,25 @@ struct EdgeBwdArgs {
   float eps;
 };
 
+struct InGradArgs {
+  Lin w1;               // first Linear of the edge MLP (backward packing)
+  const int32_t* trow;  // transposed CSR over local senders
+  const int32_t* tedge;
+  const void* dz;       // dz_0 per edge, storage type [E][L]
+  const float* dzr;     // per-receiver sums of dz_0 [n_owned][L]
+  float* dv;            // [n_owned][L], accumulated into
+  float* dh;            // [n_halo][L] or null
+  float* dzs;           // out: per-sender sums of dz_0 [n_local][L]
+  int64_t n_local, n_owned;
+};
+
 struct DwArgs {
-  const void* delta;  // storage type [R][ldd]
+  const void* delta;  // d_kind 0: storage type [R][ldd]; 1: fp32 [R][ldd]
+  int d_kind;
   int ldd;
   int O, I;
-  int a_kind;         // 0 dense storage type, 1 dense fp32, 2 edge concat, 3 node concat
+  int a_kind;         // 0 dense storage type, 1 dense fp32, 2 edge concat, 3 node concat,
+                      // 4 node rows fp32 (owned rows a0, halo rows a2; row stride lda0)
   const void* a0;     // dense source / e^k / v
   int lda0;
   const float* a1;    // node concat: agg; edge concat: V (owned)
@@ -121,10 +133,12 @@ hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& 
 hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int grid, hipStream_t st);
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st);
 hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int grid, hipStream_t st);
-hipError_t launch_sender_gather(int64_t n_local, int64_t n_owned, const int32_t* trow, const int32_t* tedge,
-                                const float* g, float* dv, float* dh, int L, hipStream_t st);
+// Workgroups (= vector-partial slots) the edge backward uses when asked for `grid`.
+int edge_bwd_grid(int prec, int L, int D, int grid);
+hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t st);
 hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st);
-hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int accumulate, hipStream_t st);
+hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int ldw, int accumulate,
+                            hipStream_t st);
 hipError_t launch_vec_reduce(const float* vpart, int nwg, int nvec, const VecSeg* segs, int nseg, float* dparams,
                              int accumulate, hipStream_t st);
 hipError_t launch_mse(const float* out, const float* target, const uint8_t* mask, int64_t n, int d, float* loss,

@@ -8,8 +8,12 @@
 //   rows_fwd           EncNode, EncEdge, node half of a block, DecNode
 //   edge_fwd           edge half of a block: gather [e | v_s | v_r] into LDS,
 //                      MLP on MFMA, LayerNorm, residual, ordered receiver sum
-//   rows_bwd/edge_bwd  the same with the forward recomputed in-tile
-//   sender_gather      ordered sum of sender-side gradients (transposed CSR)
+//   rows_bwd/edge_bwd  the same with the forward recomputed in-tile; the edge
+//                      half ends at the first Linear's output gradient dz_0
+//                      (edge-stream part applied, receiver sums formed)
+//   input_grad         node gradients through that Linear's sender/receiver
+//                      blocks: ordered per-node sums of dz_0 (transposed CSR
+//                      for senders), then one node-level product
 //   dw / dw_reduce     weight gradients as split-K MFMA GEMMs, fixed order
 //   vec_reduce         bias and LayerNorm gradients, fixed order
 //   mse                masked mean-squared-error loss and its gradient
@@ -64,11 +68,11 @@ __device__ __forceinline__ void copy_row16(typename P::T* dst, const typename P:
 
 // Copies n rows of `width` elements (16-byte multiple) from LDS (row stride
 // ld) to consecutive global rows starting at dst, 16 bytes per thread.
-template <class T>
+template <class T, int NTH = NT>
 __device__ __forceinline__ void store_rows(T* __restrict__ dst, const T* src, int ld, int n, int width) {
   constexpr int E16 = 16 / sizeof(T);
   const int cpr = width / E16;
-  for (int i = threadIdx.x; i < n * cpr; i += NT) {
+  for (int i = threadIdx.x; i < n * cpr; i += NTH) {
     const int r = i / cpr, c = (i % cpr) * E16;
     *reinterpret_cast<uint4*>(dst + (int64_t)r * width + c) = *reinterpret_cast<const uint4*>(src + r * ld + c);
   }
@@ -216,6 +220,95 @@ __device__ __forceinline__ void acc_colsum(const floatx4 (&acc)[MB][NBW], float 
     out[n] = s;
   }
 }
+
+// Row totals over all L columns of a wave-column-split tile (MB row blocks of
+// 16; wave w holds the 16-column blocks w*NBW ..).  v[q][m][r] enters as this
+// lane's partial of row m*16 + acc_row(r) and leaves as the row's total, with
+// the same bits in every lane that holds the row: the 16 lanes of a row group
+// combine by a butterfly (commutative pairs), the waves through LDS slots
+// red[NW][Q][MB*16] in ascending wave order.
+template <int Q, int MB, int NWAVES = NW>
+__device__ __forceinline__ void row_totals(float (&v)[Q][MB][4], float* red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float x = v[q][m][r];
+        x += __shfl_xor(x, 1, 64);
+        x += __shfl_xor(x, 2, 64);
+        x += __shfl_xor(x, 4, 64);
+        x += __shfl_xor(x, 8, 64);
+        v[q][m][r] = x;
+      }
+  if ((lane & 15) == 0) {
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+#pragma unroll
+      for (int m = 0; m < MB; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[((wave * Q + q) * MB + m) * 16 + acc_row(r)] = v[q][m][r];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float x = 0.f;
+#pragma unroll
+        for (int w = 0; w < NWAVES; ++w) x += red[((w * Q + q) * MB + m) * 16 + acc_row(r)];
+        v[q][m][r] = x;
+      }
+}
+
+// LayerNorm statistics on an accumulator tile (bias already added): y
+// becomes xhat = (y - mean) * rstd, with the two-pass variance; rstd of the
+// lane's rows is returned.  Uses two disjoint slot sets red0, red1.
+template <int MB, int NBW, int L, int NWAVES = NW>
+__device__ __forceinline__ void ln_tile(floatx4 (&y)[MB][NBW], float eps, float* red0, float* red1,
+                                        float (&rs)[MB][4]) {
+  float s[1][MB][4], v[1][MB][4];
+#pragma unroll
+  for (int m = 0; m < MB; ++m)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float x = 0.f;
+#pragma unroll
+      for (int n = 0; n < NBW; ++n) x += y[m][n][r];
+      s[0][m][r] = x;
+    }
+  row_totals<1, MB, NWAVES>(s, red0);
+#pragma unroll
+  for (int m = 0; m < MB; ++m)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float mu = s[0][m][r] / L;
+      float x = 0.f;
+#pragma unroll
+      for (int n = 0; n < NBW; ++n) {
+        const float d = y[m][n][r] - mu;
+        x += d * d;
+      }
+      s[0][m][r] = mu;
+      v[0][m][r] = x;
+    }
+  row_totals<1, MB, NWAVES>(v, red1);
+#pragma unroll
+  for (int m = 0; m < MB; ++m)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      rs[m][r] = 1.0f / sqrtf(v[0][m][r] / L + eps);
+#pragma unroll
+      for (int n = 0; n < NBW; ++n) y[m][n][r] = (y[m][n][r] - s[0][m][r]) * rs[m][r];
+    }
+}
+
+__device__ __forceinline__ float to_f(float x) { return x; }
+__device__ __forceinline__ float to_f(uint16_t x) { return bf2f(x); }
 
 // ----------------------------------------------------------------- pack ---
 template <class P>
@@ -761,15 +854,11 @@ struct EdgeMeta {
   unsigned long long* last;
 };
 
-// Gathers one sub-tile [e | v_s | v_r] into LDS.  First the TE row indices
-// (one load round), then every row load of this thread is issued before any
-// is stored, so the gather costs two memory latencies, not one per row.
-template <class P, int L, int TE, int LDA>
-__device__ __forceinline__ void stage_edges(typename P::T* A, EdgeMeta mt, const int32_t* erecv,
-                                            const int32_t* send, const typename P::T* Ein, const float* V,
-                                            const float* H, const void* V16, int64_t n_owned, int64_t sb, int n,
-                                            int64_t e1) {
-  using T = typename P::T;
+// Loads a sub-tile's metadata into LDS (receiver and sender ids of its TE
+// rows, and which rows end a receiver segment), then synchronises.
+template <int TE>
+__device__ __forceinline__ void stage_meta(EdgeMeta mt, const int32_t* erecv, const int32_t* send, int64_t sb,
+                                           int n, int64_t e1) {
   const int tid = threadIdx.x;
   if (tid < 64) {
     int32_t r = -1, sd = 0;
@@ -788,6 +877,16 @@ __device__ __forceinline__ void stage_edges(typename P::T* A, EdgeMeta mt, const
     if (tid == 0) *mt.last = m;
   }
   __syncthreads();
+}
+
+// Gathers the rows [e | v_s | v_r] of a sub-tile whose metadata is in LDS.
+// Every row load of this thread is issued before any is stored, so the
+// gather costs one memory latency, not one per row.  No barrier at the end.
+template <class P, int L, int TE, int LDA>
+__device__ __forceinline__ void gather_rows(typename P::T* A, EdgeMeta mt, const typename P::T* Ein, const float* V,
+                                            const float* H, const void* V16, int64_t n_owned, int64_t sb, int n) {
+  using T = typename P::T;
+  const int tid = threadIdx.x;
   constexpr int E16 = 16 / sizeof(T);
   constexpr int CPR = L / E16;                   // 16-byte chunks per e row
   if constexpr (sizeof(T) == 2) {
@@ -851,18 +950,29 @@ __device__ __forceinline__ void stage_edges(typename P::T* A, EdgeMeta mt, const
   }
 }
 
+// Metadata, then rows: the whole staging of a sub-tile (no barrier at the end).
+template <class P, int L, int TE, int LDA>
+__device__ __forceinline__ void stage_edges(typename P::T* A, EdgeMeta mt, const int32_t* erecv,
+                                            const int32_t* send, const typename P::T* Ein, const float* V,
+                                            const float* H, const void* V16, int64_t n_owned, int64_t sb, int n,
+                                            int64_t e1) {
+  stage_meta<TE>(mt, erecv, send, sb, n, e1);
+  gather_rows<P, L, TE, LDA>(A, mt, Ein, V, H, V16, n_owned, sb, n);
+}
+
 // Ordered running sum over the rows of a sub-tile for column c: adds rows
-// 0..n-1 of M (fp32, row stride ld) to `run`; at each row that ends a
-// receiver segment, hands the segment's total to emit(receiver, total) and
-// restarts.  The running value carries into the next sub-tile of the unit.
-template <int TE, class Emit>
-__device__ __forceinline__ void segment_sums(const float* M, int ld, int n, int c, EdgeMeta mt, float& run,
+// 0..n-1 of M (fp32 or storage type, row stride ld) to `run`; at each row
+// that ends a receiver segment, hands the segment's total to emit(receiver,
+// total) and restarts.  The running value carries into the next sub-tile of
+// the unit.
+template <int TE, class MT, class Emit>
+__device__ __forceinline__ void segment_sums(const MT* M, int ld, int n, int c, EdgeMeta mt, float& run,
                                              Emit emit) {
   const unsigned long long mask = *mt.last;
 #pragma unroll 8
   for (int r = 0; r < TE; ++r) {
     if (r < n) {
-      run += M[r * ld + c];
+      run += to_f(M[r * ld + c]);
       if ((mask >> r) & 1ull) {
         emit(mt.rr[r], run);
         run = 0.f;
@@ -963,218 +1073,351 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void ed
   }
 }
 
+// LDS of the edge backward kernel for TE rows: A holds [e | v_s | v_r]
+// (storage type) for the recompute and then the gradients: dy at columns
+// 0..L, dz of the hidden layers at L.. and 2L..; B, C: hidden activations;
+// the sub-tile metadata; slots for cross-wave row reductions.
+template <class P, int L, int D, int TE>
+struct EdgeBwdLds {
+  using T = typename P::T;
+  static constexpr int LDA = 3 * L + P::PAD;
+  static constexpr int LDH = L + P::PAD;
+  static constexpr int HB = TE * LDH * (int)sizeof(T);
+  static constexpr int OFF_B = rup(TE * LDA * (int)sizeof(T), 16);
+  static constexpr int OFF_C = OFF_B + HB;
+  static constexpr int OFF_META = OFF_C + (D == 3 ? HB : 0);
+  static constexpr int OFF_RED = OFF_META + rup(TE * 8 + 8, 16);
+  static constexpr int END = OFF_RED + 4 * NW * TE * 4;
+};
+
+// Backward of one block's edge half with the forward recomputed in the tile.
+// Per edge: dm = de^{k+1} + dagg[receiver]; LayerNorm backward; the MLP's
+// backward down to dz_0, the gradient at the first Linear's output; then
+// de^k = de^{k+1} + dz_0 W_1[:, e-block].  The sender and receiver blocks of
+// W_1 are the same for every edge, so their products are taken per node
+// later (input_grad_kernel): here each receiver's sum of dz_0 (in the
+// precision that feeds the products) overwrites its dagg row once the last of
+// its edges is done, and receivers without edges get a zero row.  dz_0, the
+// LN-backward output and the hidden activations go to HBM for the weight
+// gradients; bias / gamma / beta gradients are per-lane column partials over
+// the workgroup's rows, written once at the end.
 template <int P_, int L, int D>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void edge_bwd_kernel(EdgeBwdArgs a) {
   using P = typename PrecOf<P_>::type;
   using T = typename P::T;
   constexpr int TE = EdgeTEB<P, L, D>::value;
-  using Lay = EdgeLds<P, L, D, TE>;
+  using Lay = EdgeBwdLds<P, L, D, TE>;
   constexpr int MB = TE / 16;
-  constexpr int NBW = L / 16 / NW > 0 ? L / 16 / NW : 1;
+  constexpr int NBW = L / 16 / NW;
+  static_assert(NBW >= 1 && L % (16 * NW) == 0, "latent width must be a multiple of 64");
+  constexpr int NK1 = 3 * L / P::KG, NKH = L / P::KG;
   extern __shared__ __align__(16) unsigned char lds[];
   T* A = reinterpret_cast<T*>(lds);
-  float* XH = reinterpret_cast<float*>(lds);     // xhat after the recompute (fp32, stride LDY)
-  T* DY = A + Lay::DY_OFF;                        // storage-type gradient (stride LDA)
-  float* Yf = reinterpret_cast<float*>(lds);     // last-layer output before LN (same place as xhat)
   T* HB = reinterpret_cast<T*>(lds + Lay::OFF_B);
   T* HC = reinterpret_cast<T*>(lds + Lay::OFF_C);
-  float* DM = reinterpret_cast<float*>(lds + Lay::OFF_D);
   EdgeMeta mt;
   mt.rr = reinterpret_cast<int32_t*>(lds + Lay::OFF_META);
   mt.ss = mt.rr + TE;
   mt.last = reinterpret_cast<unsigned long long*>(mt.ss + TE);
-  float* RS = reinterpret_cast<float*>(mt.last + 2);
-  const int wave = threadIdx.x >> 6, tid = threadIdx.x;
-  const bool wave_has_cols = wave * NBW * 16 < L;
+  float* red = reinterpret_cast<float*>(lds + Lay::OFF_RED);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, tid = threadIdx.x;
+  const int nb0 = wave * NBW;
   const T* Ein = reinterpret_cast<const T*>(a.Ein);
 
-  float g_gamma = 0.f, g_beta = 0.f, g_blast = 0.f;
-  float g_bh[2][NBW];
+  float gam[NBW], blast[NBW];
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+  for (int n = 0; n < NBW; ++n) {
+    const int col = (nb0 + n) * 16 + acc_col();
+    gam[n] = a.mlp.gamma[col];
+    blast[n] = a.mlp.lin[D - 1].b[col];
+  }
+  // column partials over this lane's rows: gamma, beta, last bias, hidden biases
+  float pg[NBW], pb[NBW], pl[NBW], ph[2][NBW];
 #pragma unroll
-    for (int n = 0; n < NBW; ++n) g_bh[j][n] = 0.f;
+  for (int n = 0; n < NBW; ++n) pg[n] = pb[n] = pl[n] = ph[0][n] = ph[1][n] = 0.f;
 
   for (TileIter it(*a.n_units); it.valid(); it.next()) {
     const int64_t r0 = a.unit_r[it.t], r1 = a.unit_r[it.t + 1];
     const int64_t e0 = a.row_ptr[r0], e1 = a.row_ptr[r1];
-    float run = 0.f;  // running receiver sum (receiver-side input gradient), column tid
+    zero_empty_receivers(a.row_ptr, r0, r1, a.dagg, L);
+    float run = 0.f;  // running receiver sum of dz_0, column tid
     for (int64_t sb = e0; sb < e1; sb += TE) {
       const int n = (int)(e1 - sb < TE ? e1 - sb : TE);
-      stage_edges<P, L, TE, Lay::LDA>(A, mt, a.erecv, a.send, Ein, a.V, a.H, a.V16, a.n_owned, sb, n, e1);
-      // dm = de^{k+1} + dagg[receiver], all loads of the thread issued first
-      constexpr int Q = L / 4;
-      constexpr int IM = (TE * Q + NT - 1) / NT;
-      {
-        float4 va[IM], vd[IM];
+      stage_meta<TE>(mt, a.erecv, a.send, sb, n, e1);
+      // dm = de^{k+1} + dagg[receiver] in accumulator layout, issued before
+      // the row gather so that both latencies overlap
+      float de[MB][NBW][4], da[MB][NBW][4];
 #pragma unroll
-        for (int j = 0; j < IM; ++j) {
-          const int i = tid + j * NT, r = i / Q, c4 = i % Q;
-          va[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-          vd[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (i < TE * Q && r < n) {
-            va[j] = reinterpret_cast<const float4*>(a.dagg + (int64_t)mt.rr[r] * L)[c4];
-            if (a.de_next) vd[j] = reinterpret_cast<const float4*>(a.de_next + (sb + r) * L)[c4];
+      for (int m = 0; m < MB; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = m * 16 + acc_row(r);
+          const bool ok = row < n;
+          const int64_t rv = ok ? (int64_t)mt.rr[row] : 0;
+#pragma unroll
+          for (int nn = 0; nn < NBW; ++nn) {
+            const int col = (nb0 + nn) * 16 + acc_col();
+            de[m][nn][r] = (ok && a.de_next) ? a.de_next[(sb + row) * L + col] : 0.f;
+            da[m][nn][r] = ok ? a.dagg[rv * L + col] : 0.f;
           }
         }
-#pragma unroll
-        for (int j = 0; j < IM; ++j) {
-          const int i = tid + j * NT, r = i / Q, c4 = i % Q;
-          if (i < TE * Q)
-            *reinterpret_cast<float4*>(DM + r * Lay::LDM + c4 * 4) =
-                make_float4(va[j].x + vd[j].x, va[j].y + vd[j].y, va[j].z + vd[j].z, va[j].w + vd[j].w);
-        }
-      }
+      gather_rows<P, L, TE, Lay::LDA>(A, mt, Ein, a.V, a.H, a.V16, a.n_owned, sb, n);
       __syncthreads();
-      // recompute the forward: hidden activations and the LN input
+      // recompute the forward: hidden activations, then the LN input
       {
         floatx4 acc[MB][NBW];
-        if (wave_has_cols) {
-          wave_gemm_k<P, MB, NBW, 3 * L / P::KG>(A, Lay::LDA, a.mlp.lin[0].wf, wave * NBW, acc);
-          store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[0].b, L, HB, Lay::LDH);
-        }
+        wave_gemm_k<P, MB, NBW, NK1>(A, Lay::LDA, a.mlp.lin[0].wf, nb0, acc);
+        store_acc<P, MB, NBW, true>(acc, nb0, a.mlp.lin[0].b, L, HB, Lay::LDH);
       }
       __syncthreads();
       const T* hin = HB;
       if constexpr (D == 3) {
         floatx4 acc[MB][NBW];
-        if (wave_has_cols) {
-          wave_gemm_k<P, MB, NBW, L / P::KG>(HB, Lay::LDH, a.mlp.lin[1].wf, wave * NBW, acc);
-          store_acc<P, MB, NBW, true>(acc, wave * NBW, a.mlp.lin[1].b, L, HC, Lay::LDH);
-        }
+        wave_gemm_k<P, MB, NBW, NKH>(HB, Lay::LDH, a.mlp.lin[1].wf, nb0, acc);
+        store_acc<P, MB, NBW, true>(acc, nb0, a.mlp.lin[1].b, L, HC, Lay::LDH);
         __syncthreads();
         hin = HC;
       }
-      {
-        floatx4 acc[MB][NBW];
-        if (wave_has_cols)
-          wave_gemm_k<P, MB, NBW, L / P::KG>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, wave * NBW, acc);
-        __syncthreads();  // A (the gathered inputs) is overwritten below
-        if (wave_has_cols) store_acc<P, MB, NBW, false>(acc, wave * NBW, a.mlp.lin[D - 1].b, L, Yf, Lay::LDY);
-      }
-      __syncthreads();
-      ln_normalise<TE, L>(XH, Lay::LDY, a.eps, RS);
-      __syncthreads();
-      if (tid < L) {
-        for (int r = 0; r < n; ++r) {
-          const float d = DM[r * Lay::LDM + tid];
-          g_gamma += d * XH[r * Lay::LDY + tid];
-          g_beta += d;
+      floatx4 y[MB][NBW];
+      wave_gemm_k<P, MB, NBW, NKH>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, nb0, y);
+#pragma unroll
+      for (int m = 0; m < MB; ++m)
+#pragma unroll
+        for (int nn = 0; nn < NBW; ++nn)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) y[m][nn][r] += blast[nn];
+      float rs[MB][4];
+      ln_tile<MB, NBW, L>(y, a.eps, red, red + NW * TE, rs);  // y now holds xhat
+      // LayerNorm backward: dy = rstd (dm g - mean(dm g) - xhat mean(dm g xhat))
+      float s2[2][MB][4];
+#pragma unroll
+      for (int m = 0; m < MB; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float s1 = 0.f, sx = 0.f;
+#pragma unroll
+          for (int nn = 0; nn < NBW; ++nn) {
+            const float dm = da[m][nn][r] + de[m][nn][r];
+            const float d = dm * gam[nn];
+            s1 += d;
+            sx += d * y[m][nn][r];
+            pg[nn] += dm * y[m][nn][r];
+            pb[nn] += dm;
+          }
+          s2[0][m][r] = s1;
+          s2[1][m][r] = sx;
         }
-      }
+      row_totals<2, MB>(s2, red + 2 * NW * TE);
+#pragma unroll
+      for (int m = 0; m < MB; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = m * 16 + acc_row(r);
+          const float m1 = s2[0][m][r] / L, m2 = s2[1][m][r] / L;
+#pragma unroll
+          for (int nn = 0; nn < NBW; ++nn) {
+            const int col = (nb0 + nn) * 16 + acc_col();
+            const float dm = da[m][nn][r] + de[m][nn][r];
+            const float dy = rs[m][r] * (dm * gam[nn] - m1 - y[m][nn][r] * m2);
+            pl[nn] += dy;
+            A[row * Lay::LDA + col] = P::cvt(dy);
+          }
+        }
       __syncthreads();
-      ln_backward<P, TE, L>(DM, Lay::LDM, XH, Lay::LDY, RS, a.mlp.gamma, DY, Lay::LDA);
-      __syncthreads();
-      if (tid < L) g_blast += col_sum(DM, Lay::LDM, n, tid);
-      store_rows(reinterpret_cast<T*>(a.delta[D - 1]) + sb * L, DY, Lay::LDA, n, L);
+      store_rows(reinterpret_cast<T*>(a.delta[D - 1]) + sb * L, A, Lay::LDA, n, L);
       store_rows(reinterpret_cast<T*>(a.hid[0]) + sb * L, HB, Lay::LDH, n, L);
       if constexpr (D == 3) store_rows(reinterpret_cast<T*>(a.hid[1]) + sb * L, HC, Lay::LDH, n, L);
+      // hidden layers: dz_{j-1} = (dz_j W_j) * [h_{j-1} > 0], into A column block D-j
 #pragma unroll
       for (int j = D - 1; j >= 1; --j) {
+        const T* din = A + (D - 1 - j) * L;
+        T* dout = A + (D - j) * L;
         const T* hprev = (j == 2) ? HC : HB;
         floatx4 acc[MB][NBW];
-        if (wave_has_cols)
-          wave_gemm_k<P, MB, NBW, L / P::KG>(DY, Lay::LDA, a.mlp.lin[j].wb, wave * NBW, acc);
-        __syncthreads();
-        if (wave_has_cols) {
+        wave_gemm_k<P, MB, NBW, NKH>(din, Lay::LDA, a.mlp.lin[j].wb, nb0, acc);
 #pragma unroll
-          for (int nn = 0; nn < NBW; ++nn)
+        for (int nn = 0; nn < NBW; ++nn)
 #pragma unroll
-            for (int m = 0; m < MB; ++m)
+          for (int m = 0; m < MB; ++m)
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const int row = m * 16 + acc_row(r), col = (wave * NBW + nn) * 16 + acc_col();
-                const float h = P::tof(hprev[row * Lay::LDH + col]);
-                acc[m][nn][r] = h > 0.f ? acc[m][nn][r] : 0.f;
-                DY[row * Lay::LDA + col] = P::cvt(acc[m][nn][r]);
-              }
-          float cs[NBW];
-          acc_colsum<MB, NBW>(acc, cs);
-#pragma unroll
-          for (int nn = 0; nn < NBW; ++nn) g_bh[j - 1][nn] += cs[nn];
-        }
-        __syncthreads();
-        store_rows(reinterpret_cast<T*>(a.delta[j - 1]) + sb * L, DY, Lay::LDA, n, L);
-      }
-      // input gradient [d e | d v_s | d v_r] = dz_1 W_1, one L-wide pass each
-#pragma unroll
-      for (int pass = 0; pass < 3; ++pass) {
-        floatx4 acc[MB][NBW];
-        if (wave_has_cols)
-          wave_gemm_k<P, MB, NBW, L / P::KG>(DY, Lay::LDA, a.mlp.lin[0].wb, pass * (L / 16) + wave * NBW, acc);
-        __syncthreads();
-        if (wave_has_cols) store_acc<P, MB, NBW, false>(acc, wave * NBW, nullptr, L, DM, Lay::LDM);
-        __syncthreads();
-        if (pass < 2) {
-          float* dst = pass == 0 ? a.de_out : a.g;
-          for (int i = tid; i < n * Q; i += NT) {
-            const int r = i / Q, c4 = i % Q;
-            float4 v = *reinterpret_cast<const float4*>(DM + r * Lay::LDM + c4 * 4);
-            if (pass == 0 && a.de_next) {
-              const float4 d = reinterpret_cast<const float4*>(a.de_next + (sb + r) * L)[c4];
-              v.x += d.x;
-              v.y += d.y;
-              v.z += d.z;
-              v.w += d.w;
+            for (int r = 0; r < 4; ++r) {
+              const int row = m * 16 + acc_row(r), col = (nb0 + nn) * 16 + acc_col();
+              const float v = P::tof(hprev[row * Lay::LDH + col]) > 0.f ? acc[m][nn][r] : 0.f;
+              ph[j - 1][nn] += v;
+              dout[row * Lay::LDA + col] = P::cvt(v);
             }
-            reinterpret_cast<float4*>(dst + (sb + r) * L)[c4] = v;
-          }
-        } else {
-          if (tid < L)
-            segment_sums<TE>(DM, Lay::LDM, n, tid, mt, run,
-                             [&](int32_t r, float v) { a.dv[(int64_t)r * L + tid] += v; });
-        }
         __syncthreads();
+        store_rows(reinterpret_cast<T*>(a.delta[j - 1]) + sb * L, dout, Lay::LDA, n, L);
       }
+      // edge-stream gradient: de^k = de^{k+1} + dz_0 W_1[:, e-block]
+      const T* dz0 = A + (D - 1) * L;
+      {
+        floatx4 acc[MB][NBW];
+        wave_gemm_k<P, MB, NBW, NKH>(dz0, Lay::LDA, a.mlp.lin[0].wb, nb0, acc);
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int row = m * 16 + acc_row(r);
+            if (row < n) {
+#pragma unroll
+              for (int nn = 0; nn < NBW; ++nn)
+                a.de_out[(sb + row) * L + (nb0 + nn) * 16 + acc_col()] = acc[m][nn][r] + de[m][nn][r];
+            }
+          }
+      }
+      // receiver sums of dz_0, ascending edge order
+      if (tid < L)
+        segment_sums<TE>(dz0, Lay::LDA, n, tid, mt, run,
+                         [&](int32_t r, float v) { a.dagg[(int64_t)r * L + tid] = v; });
+      __syncthreads();
+    }
+  }
+  // column partials: the four 16-lane groups of a column, then one writer lane
+#pragma unroll
+  for (int nn = 0; nn < NBW; ++nn) {
+    float* v[5] = {&pg[nn], &pb[nn], &pl[nn], &ph[0][nn], &ph[1][nn]};
+#pragma unroll
+    for (int q = 0; q < 5; ++q) {
+      float x = *v[q];
+      x += __shfl_xor(x, 16, 64);
+      x += __shfl_xor(x, 32, 64);
+      *v[q] = x;
     }
   }
   float* vp = a.vpart + (int64_t)blockIdx.x * a.nvec;
-  if (wave_has_cols && (threadIdx.x & 63) < 16) {
+  if (lane < 16) {
+    const int off_last = (D - 1) * L;
 #pragma unroll
-    for (int j = 0; j < D - 1; ++j)
+    for (int nn = 0; nn < NBW; ++nn) {
+      const int col = (nb0 + nn) * 16 + lane;
 #pragma unroll
-      for (int nn = 0; nn < NBW; ++nn) vp[j * L + (wave * NBW + nn) * 16 + (threadIdx.x & 15)] = g_bh[j][nn];
-  }
-  const int off_last = (D - 1) * L;
-  if (tid < L) {
-    vp[off_last + tid] = g_blast;
-    vp[off_last + L + tid] = g_gamma;
-    vp[off_last + 2 * L + tid] = g_beta;
+      for (int j = 0; j < D - 1; ++j) vp[j * L + col] = ph[j][nn];
+      vp[off_last + col] = pl[nn];
+      vp[off_last + L + col] = pg[nn];
+      vp[off_last + 2 * L + col] = pb[nn];
+    }
   }
 }
 
-// ------------------------------------------------------- sender gather ---
-// dv[n] += sum of g[e] over the local edges sent by n, ascending e (owned n);
-// dh[n - n_owned] = the same sum (halo n).  L/4 threads per node.
-__global__ __launch_bounds__(NT) void sender_gather_kernel(int64_t n_local, int64_t n_owned,
-                                                           const int32_t* __restrict__ trow,
-                                                           const int32_t* __restrict__ tedge,
-                                                           const float* __restrict__ g, float* __restrict__ dv,
-                                                           float* __restrict__ dh, int L) {
-  const int Q = L / 4;
-  const int per = NT / Q;
-  const int64_t node = (int64_t)blockIdx.x * per + threadIdx.x / Q;
-  const int c4 = threadIdx.x % Q;
-  if (threadIdx.x / Q >= per || node >= n_local) return;
-  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int32_t i = trow[node]; i < trow[node + 1]; ++i) {
-    const float4 v = reinterpret_cast<const float4*>(g + (int64_t)tedge[i] * L)[c4];
-    s.x += v.x;
-    s.y += v.y;
-    s.z += v.z;
-    s.w += v.w;
+// --------------------------------------------------- node input gradient ---
+// Gradient reaching the nodes through the first Linear of a block's edge MLP.
+// Its sender and receiver column blocks W_s, W_r are shared by all edges, so
+//   dv[n] += dzr[n] W_r + dzs[n] W_s   (owned n)
+//   dh[n - n_owned] = dzs[n] W_s       (halo n)
+// with dzr[n] the sum of dz_0 over the edges n receives (from the edge
+// backward kernel) and dzs[n] the sum over the edges n sends, gathered here in
+// ascending local edge id through the transposed CSR.  Sums are fp32; in
+// bf16 mode each fp32 operand enters the bf16 products as hi + lo, two bf16
+// values whose sum is within 2^-17 of it (relative).
+template <class P, int L>
+struct InGradTile {
+  static constexpr int TM = L <= 128 ? 64 : 32;                       // nodes per workgroup
+  static constexpr int LDT = L + P::PAD;
+  static constexpr int NOP = sizeof(typename P::T) == 2 ? 4 : 2;     // operand tiles: (hi, lo) x (r, s)
+  static constexpr int END = NOP * TM * LDT * (int)sizeof(typename P::T);
+};
+
+template <class P>
+__device__ __forceinline__ void put_operand(typename P::T* hi, typename P::T* lo, float x) {
+  if constexpr (sizeof(typename P::T) == 2) {
+    const uint16_t h = f2bf(x);
+    *hi = h;
+    *lo = f2bf(x - bf2f(h));
+  } else {
+    *hi = x;
   }
-  if (node < n_owned) {
-    float4* d = reinterpret_cast<float4*>(dv + node * L) + c4;
-    float4 v = *d;
-    v.x += s.x;
-    v.y += s.y;
-    v.z += s.z;
-    v.w += s.w;
-    *d = v;
-  } else if (dh) {
-    reinterpret_cast<float4*>(dh + (node - n_owned) * L)[c4] = s;
+}
+
+template <int P_, int L>
+__global__ __launch_bounds__(NT) void input_grad_kernel(InGradArgs a) {
+  using P = typename PrecOf<P_>::type;
+  using T = typename P::T;
+  using G = InGradTile<P, L>;
+  constexpr int TM = G::TM, LDT = G::LDT, MB = TM / 16;
+  constexpr int NBW = L / 16 / NW;
+  constexpr int NKH = L / P::KG;
+  constexpr bool SPLIT = sizeof(T) == 2;
+  extern __shared__ __align__(16) unsigned char lds[];
+  T* Rh = reinterpret_cast<T*>(lds);
+  T* Sh = Rh + TM * LDT;
+  T* Rl = SPLIT ? Sh + TM * LDT : Rh;
+  T* Sl = SPLIT ? Rl + TM * LDT : Sh;
+  const int64_t n0 = (int64_t)blockIdx.x * TM;
+  const int tid = threadIdx.x, wave = tid >> 6;
+  const T* dz = reinterpret_cast<const T*>(a.dz);
+  // sender sums: (node, 16-byte chunk) items, ascending edges, 4 loads in flight
+  constexpr int E16 = 16 / sizeof(T);
+  constexpr int CPR = L / E16;
+  for (int it = tid; it < TM * CPR; it += NT) {
+    const int row = it / CPR, c = (it % CPR) * E16;
+    const int64_t node = n0 + row;
+    float s[E16];
+#pragma unroll
+    for (int j = 0; j < E16; ++j) s[j] = 0.f;
+    if (node < a.n_local) {
+      int32_t i = a.trow[node];
+      const int32_t end = a.trow[node + 1];
+      for (; i + 4 <= end; i += 4) {
+        uint4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const uint4*>(dz + (int64_t)a.tedge[i + u] * L + c);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const T* t = reinterpret_cast<const T*>(&v[u]);
+#pragma unroll
+          for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
+        }
+      }
+      for (; i < end; ++i) {
+        const uint4 v = *reinterpret_cast<const uint4*>(dz + (int64_t)a.tedge[i] * L + c);
+        const T* t = reinterpret_cast<const T*>(&v);
+#pragma unroll
+        for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < E16; ++j) put_operand<P>(Sh + row * LDT + c + j, Sl + row * LDT + c + j, s[j]);
+    if (node < a.n_local) {
+#pragma unroll
+      for (int j = 0; j < E16; j += 4)
+        *reinterpret_cast<float4*>(a.dzs + node * L + c + j) = make_float4(s[j], s[j + 1], s[j + 2], s[j + 3]);
+    }
   }
+  // receiver sums (owned rows; zero for halo rows and past the end)
+  for (int it = tid; it < TM * (L / 4); it += NT) {
+    const int row = it / (L / 4), c = (it % (L / 4)) * 4;
+    const int64_t node = n0 + row;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (node < a.n_owned) v = *reinterpret_cast<const float4*>(a.dzr + node * L + c);
+    put_operand<P>(Rh + row * LDT + c, Rl + row * LDT + c, v.x);
+    put_operand<P>(Rh + row * LDT + c + 1, Rl + row * LDT + c + 1, v.y);
+    put_operand<P>(Rh + row * LDT + c + 2, Rl + row * LDT + c + 2, v.z);
+    put_operand<P>(Rh + row * LDT + c + 3, Rl + row * LDT + c + 3, v.w);
+  }
+  __syncthreads();
+  const int nb = wave * NBW;
+  floatx4 acc[MB][NBW];
+  wave_gemm_k<P, MB, NBW, NKH, true>(Rh, LDT, a.w1.wb, 2 * (L / 16) + nb, acc);
+  if constexpr (SPLIT) wave_gemm_k<P, MB, NBW, NKH, false>(Rl, LDT, a.w1.wb, 2 * (L / 16) + nb, acc);
+  wave_gemm_k<P, MB, NBW, NKH, false>(Sh, LDT, a.w1.wb, (L / 16) + nb, acc);
+  if constexpr (SPLIT) wave_gemm_k<P, MB, NBW, NKH, false>(Sl, LDT, a.w1.wb, (L / 16) + nb, acc);
+#pragma unroll
+  for (int m = 0; m < MB; ++m)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t node = n0 + m * 16 + acc_row(r);
+#pragma unroll
+      for (int nn = 0; nn < NBW; ++nn) {
+        const int col = (nb + nn) * 16 + acc_col();
+        if (node < a.n_owned) {
+          float* d = a.dv + node * L + col;
+          *d = *d + acc[m][nn][r];
+        } else if (node < a.n_local && a.dh) {
+          a.dh[(node - a.n_owned) * L + col] = acc[m][nn][r];
+        }
+      }
+    }
 }
 
 // -------------------------------------------------- weight gradients ---
@@ -1205,9 +1448,15 @@ __device__ __forceinline__ uint4 dw_load_a(const DwArgs& a, int64_t row, int col
     const float* src = node < a.n_owned ? a.a1 + node * L + c : a.a2 + (node - a.n_owned) * L + c;
 #pragma unroll
     for (int e = 0; e < P::EL; ++e) v[e] = P::cvt(src[e]);
-  } else {
+  } else if (a.a_kind == 3) {
     const int L = a.L;
     const float* src = (col < L ? reinterpret_cast<const float*>(a.a0) + row * L + col : a.a1 + row * L + (col - L));
+#pragma unroll
+    for (int e = 0; e < P::EL; ++e) v[e] = P::cvt(src[e]);
+  } else {
+    // node rows, fp32: owned rows from a0, halo rows from a2
+    const float* src = row < a.n_owned ? reinterpret_cast<const float*>(a.a0) + row * a.lda0 + col
+                                       : a.a2 + (row - a.n_owned) * a.lda0 + col;
 #pragma unroll
     for (int e = 0; e < P::EL; ++e) v[e] = P::cvt(src[e]);
   }
@@ -1226,14 +1475,18 @@ __device__ __forceinline__ int dw_swz(int col, int r) {
   else return r ^ (16 * ((col >> 3) & 3));
 }
 
-template <int P_>
+// SPLIT (bf16 only): delta is fp32 and enters the products as hi + lo, two
+// bf16 operands whose sum is within 2^-17 of it (relative).
+template <int P_, bool SPLIT>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void dw_kernel(DwArgs a) {
   using P = typename PrecOf<P_>::type;
   using T = typename P::T;
+  static_assert(!SPLIT || sizeof(T) == 2, "split operands are a bf16-mode form");
   constexpr int LDT = DW_RC + P::PAD;
   constexpr int GPR = DW_TO / P::EL;              // 16-byte groups per operand row
   constexpr int IT = DW_RC * GPR / NT;            // loads per thread per operand per chunk
   __shared__ __align__(16) T Dt[DW_TO * LDT];
+  __shared__ __align__(16) T Dl[SPLIT ? DW_TO * LDT : 16];
   __shared__ __align__(16) T At[DW_TI * LDT];
   const int ot = blockIdx.x, itl = blockIdx.y, s = blockIdx.z;
   const int o0 = ot * DW_TO, i0 = itl * DW_TI;
@@ -1251,7 +1504,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void dw
   // column groups per wave (64 contiguous bytes of each row per wave)
   auto rowof = [&](int j) { const int idx = threadIdx.x + j * NT; return (idx & 15) + 16 * (idx / (16 * GPR)); };
   auto grpof = [&](int j) { const int idx = threadIdx.x + j * NT; return ((idx >> 4) % GPR) * P::EL; };
-  uint4 rd[IT], ra[IT];
+  uint4 rd[IT], ra[IT], rl[SPLIT ? IT : 1];
   auto load = [&](int64_t c0) {
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
@@ -1259,8 +1512,24 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void dw
       const int64_t row = c0 + r;
       rd[j] = make_uint4(0, 0, 0, 0);
       ra[j] = make_uint4(0, 0, 0, 0);
+      if constexpr (SPLIT) rl[j] = make_uint4(0, 0, 0, 0);
       if (row < re) {
-        if (o0 + g < a.O) {
+        if constexpr (SPLIT) {
+          // fp32 delta (a.O and a.ldd multiples of 8): 8 values, hi and lo halves
+          if (o0 + g < a.O) {
+            const float* src = reinterpret_cast<const float*>(a.delta) + row * a.ldd + o0 + g;
+            const float4 x0 = reinterpret_cast<const float4*>(src)[0], x1 = reinterpret_cast<const float4*>(src)[1];
+            const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+            uint16_t h[8], l[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              h[e] = f2bf(x[e]);
+              l[e] = f2bf(x[e] - bf2f(h[e]));
+            }
+            rd[j] = *reinterpret_cast<const uint4*>(h);
+            rl[j] = *reinterpret_cast<const uint4*>(l);
+          }
+        } else if (o0 + g < a.O) {
           if (o0 + g + P::EL <= a.ldd && (a.ldd % P::EL) == 0) {
             rd[j] = *reinterpret_cast<const uint4*>(dl + row * a.ldd + o0 + g);
           } else {
@@ -1285,6 +1554,14 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void dw
         const int c = g + e;
         Dt[c * LDT + dw_swz<P>(c, r)] = (o0 + c < a.O) ? vd[e] : P::cvt(0.f);
         At[c * LDT + dw_swz<P>(c, r)] = (i0 + c < a.I) ? va[e] : P::cvt(0.f);
+      }
+      if constexpr (SPLIT) {
+        const T* vl = reinterpret_cast<const T*>(&rl[j]);
+#pragma unroll
+        for (int e = 0; e < P::EL; ++e) {
+          const int c = g + e;
+          Dl[c * LDT + dw_swz<P>(c, r)] = (o0 + c < a.O) ? vl[e] : P::cvt(0.f);
+        }
       }
     }
   };
@@ -1311,6 +1588,17 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void dw
       for (int m = 0; m < 4; ++m)
 #pragma unroll
         for (int n = 0; n < 4; ++n) P::mma(acc[m][n], af[m], bf[n]);
+      if constexpr (SPLIT) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const int c = wo + m * 16 + (lane & 15);
+          af[m] = *reinterpret_cast<const uint4*>(Dl + c * LDT + dw_swz<P>(c, kk));
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+          for (int n = 0; n < 4; ++n) P::mma(acc[m][n], af[m], bf[n]);
+      }
     }
     __syncthreads();
   }
@@ -1326,14 +1614,18 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void dw
       }
 }
 
-__global__ void dw_reduce_kernel(const float* __restrict__ part, int S, int64_t n, float* __restrict__ dst,
-                                 int accumulate) {
+// dst[o * ldw + i] (+)= sum over the S split partials of part[.][o][i], in
+// split order.
+__global__ void dw_reduce_kernel(const float* __restrict__ part, int S, int O, int I, float* __restrict__ dst,
+                                 int ldw, int accumulate) {
+  const int64_t n = (int64_t)O * I;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
-  float s = accumulate ? dst[i] : 0.f;
+  float* d = dst + (i / I) * ldw + (i % I);
+  float s = accumulate ? *d : 0.f;
   float t = 0.f;
   for (int k = 0; k < S; ++k) t += part[(int64_t)k * n + i];
-  dst[i] = s + t;
+  *d = s + t;
 }
 
 struct VecSegs {
@@ -1359,6 +1651,61 @@ __global__ void vec_reduce_kernel(const float* __restrict__ vpart, int nwg, int 
 // ------------------------------------------------------------------ loss ---
 // Masked mean squared error: one workgroup sums count and squared error in a
 // fixed order (double), then every element's gradient is written.
+// Partial sums of the masked squared error, one per workgroup: (sum as fp64
+// bits, selected row count) in 4 words at scratch + 4 * blockIdx.x.
+constexpr int MSE_G = 256;
+__global__ __launch_bounds__(NT) void mse_partial_kernel(const float* __restrict__ out, const float* __restrict__ tgt,
+                                                         const uint8_t* __restrict__ mask, int64_t n, int d,
+                                                         uint32_t* __restrict__ scratch) {
+  __shared__ double ss[NT];
+  __shared__ int64_t sc[NT];
+  double s = 0.0;
+  int64_t cnt = 0;
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < n; i += (int64_t)gridDim.x * NT) {
+    if (mask && !mask[i]) continue;
+    ++cnt;
+    for (int j = 0; j < d; ++j) {
+      const double df = (double)out[i * d + j] - (double)tgt[i * d + j];
+      s += df * df;
+    }
+  }
+  ss[threadIdx.x] = s;
+  sc[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int w = NT / 2; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      ss[threadIdx.x] += ss[threadIdx.x + w];
+      sc[threadIdx.x] += sc[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const uint64_t b = __double_as_longlong(ss[0]);
+    const uint64_t c = (uint64_t)sc[0];
+    scratch[4 * blockIdx.x + 0] = (uint32_t)b;
+    scratch[4 * blockIdx.x + 1] = (uint32_t)(b >> 32);
+    scratch[4 * blockIdx.x + 2] = (uint32_t)c;
+    scratch[4 * blockIdx.x + 3] = (uint32_t)(c >> 32);
+  }
+}
+
+// Combines the MSE_G partials in workgroup order; writes the loss and the
+// gradient scale 2 / (rows * d).
+__global__ void mse_final_kernel(const uint32_t* __restrict__ scratch, int d, float* __restrict__ loss,
+                                 float* __restrict__ scale) {
+  if (threadIdx.x != 0) return;
+  double t = 0.0;
+  int64_t c = 0;
+  for (int b = 0; b < MSE_G; ++b) {
+    const uint64_t bits = (uint64_t)scratch[4 * b] | ((uint64_t)scratch[4 * b + 1] << 32);
+    t += __longlong_as_double((long long)bits);
+    c += (int64_t)((uint64_t)scratch[4 * b + 2] | ((uint64_t)scratch[4 * b + 3] << 32));
+  }
+  const double den = (double)c * d;
+  *loss = c > 0 ? (float)(t / den) : 0.f;
+  *scale = c > 0 ? (float)(2.0 / den) : 0.f;
+}
+
 __global__ __launch_bounds__(NT) void mse_loss_kernel(const float* __restrict__ out, const float* __restrict__ tgt,
                                                       const uint8_t* __restrict__ mask, int64_t n, int d,
                                                       float* __restrict__ loss, float* __restrict__ scale) {
@@ -1498,7 +1845,7 @@ static hipError_t edge_fwd_t(const EdgeFwdArgs& a, int grid, hipStream_t st) {
 template <int P_, int L, int D>
 static hipError_t edge_bwd_t(const EdgeBwdArgs& a, int grid, hipStream_t st) {
   using P = typename PrecOf<P_>::type;
-  using Lay = EdgeLds<P, L, D, EdgeTEB<P, L, D>::value>;
+  using Lay = EdgeBwdLds<P, L, D, EdgeTEB<P, L, D>::value>;
   allow_lds(edge_bwd_kernel<P_, L, D>, Lay::END);
   hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D>), dim3(grid), dim3(NT), Lay::END, st, a);
   return hipGetLastError();
@@ -1545,6 +1892,8 @@ hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int gri
   return hipErrorInvalidValue;
 }
 
+int edge_bwd_grid(int prec, int L, int D, int grid) { return grid; }
+
 hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int grid, hipStream_t st) {
 #define EB(PP, LL, DD) \
   if (prec == PP && L == LL && D == DD) return edge_bwd_t<PP, LL, DD>(a, grid, st);
@@ -1554,13 +1903,23 @@ hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int gri
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_sender_gather(int64_t n_local, int64_t n_owned, const int32_t* trow, const int32_t* tedge,
-                                const float* g, float* dv, float* dh, int L, hipStream_t st) {
-  if (n_local == 0) return hipSuccess;
-  const int per = NT / (L / 4);
-  const unsigned grid = (unsigned)((n_local + per - 1) / per);
-  hipLaunchKernelGGL(sender_gather_kernel, dim3(grid), dim3(NT), 0, st, n_local, n_owned, trow, tedge, g, dv, dh, L);
+template <int P_, int L>
+static hipError_t input_grad_t(const InGradArgs& a, hipStream_t st) {
+  using P = typename PrecOf<P_>::type;
+  using G = InGradTile<P, L>;
+  allow_lds(input_grad_kernel<P_, L>, G::END);
+  const unsigned grid = (unsigned)((a.n_local + G::TM - 1) / G::TM);
+  hipLaunchKernelGGL((input_grad_kernel<P_, L>), dim3(grid), dim3(NT), G::END, st, a);
   return hipGetLastError();
+}
+
+hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t st) {
+  if (a.n_local == 0) return hipSuccess;
+#define IG(PP, LL) \
+  if (prec == PP && L == LL) return input_grad_t<PP, LL>(a, st);
+  IG(F32, 64) IG(F32, 128) IG(F32, 256) IG(BF16, 64) IG(BF16, 128) IG(BF16, 256)
+#undef IG
+  return hipErrorInvalidValue;
 }
 
 int dw_splits(int64_t R, int O, int I) {
@@ -1574,16 +1933,20 @@ int dw_splits(int64_t R, int O, int I) {
 
 hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st) {
   dim3 grid((a.O + DW_TO - 1) / DW_TO, (a.I + DW_TI - 1) / DW_TI, a.S);
+  if (a.d_kind == 1 && (a.O % 8 != 0 || a.ldd % 8 != 0)) return hipErrorInvalidValue;
   if (prec == F32)
-    hipLaunchKernelGGL(dw_kernel<F32>, grid, dim3(NT), 0, st, a);
+    hipLaunchKernelGGL((dw_kernel<F32, false>), grid, dim3(NT), 0, st, a);
+  else if (a.d_kind == 1)
+    hipLaunchKernelGGL((dw_kernel<BF16, true>), grid, dim3(NT), 0, st, a);
   else
-    hipLaunchKernelGGL(dw_kernel<BF16>, grid, dim3(NT), 0, st, a);
+    hipLaunchKernelGGL((dw_kernel<BF16, false>), grid, dim3(NT), 0, st, a);
   return hipGetLastError();
 }
 
-hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int accumulate, hipStream_t st) {
+hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int ldw, int accumulate,
+                            hipStream_t st) {
   const int64_t n = (int64_t)O * I;
-  hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)((n + NT - 1) / NT)), dim3(NT), 0, st, part, S, n, dst,
+  hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)((n + NT - 1) / NT)), dim3(NT), 0, st, part, S, O, I, dst, ldw,
                      accumulate);
   return hipGetLastError();
 }
@@ -1600,8 +1963,16 @@ hipError_t launch_vec_reduce(const float* vpart, int nwg, int nvec, const VecSeg
 
 hipError_t launch_mse(const float* out, const float* target, const uint8_t* mask, int64_t n, int d, float* loss,
                       float* d_out, hipStream_t st) {
-  // loss[1] doubles as scratch for the gradient scale: scale is written to loss+1
-  hipLaunchKernelGGL(mse_loss_kernel, dim3(1), dim3(NT), 0, st, out, target, mask, n, d, loss, loss + 1);
+  // loss[1] doubles as scratch for the gradient scale: scale is written to loss+1.
+  // Large inputs: per-workgroup partials first, parked in d_out (overwritten
+  // by the gradient afterwards).
+  if (n * d >= 4 * MSE_G) {
+    uint32_t* scratch = reinterpret_cast<uint32_t*>(d_out);
+    hipLaunchKernelGGL(mse_partial_kernel, dim3(MSE_G), dim3(NT), 0, st, out, target, mask, n, d, scratch);
+    hipLaunchKernelGGL(mse_final_kernel, dim3(1), dim3(64), 0, st, scratch, d, loss, loss + 1);
+  } else {
+    hipLaunchKernelGGL(mse_loss_kernel, dim3(1), dim3(NT), 0, st, out, target, mask, n, d, loss, loss + 1);
+  }
   if (n > 0)
     hipLaunchKernelGGL(mse_grad_kernel, dim3((unsigned)((n * d + NT - 1) / NT)), dim3(NT), 0, st, out, target, mask,
                        n, d, loss + 1, d_out);
