@@ -181,7 +181,8 @@ typedef enum {
   MGN_T_INPUT_GRAD = 6,    /* node gradients through the edge MLP's first Linear */
   MGN_T_WEIGHT_GRAD = 7,   /* weight-gradient GEMMs and fixed-order reductions */
   MGN_T_OTHER = 8,         /* planning, loss */
-  MGN_T_COUNT = 9
+  MGN_T_NODE_PROJ = 9,     /* per-node products of the edge MLP's first Linear (row-split edge kernels) */
+  MGN_T_COUNT = 10
 } mgn_timer;
 /* Starts (enable != 0) or stops recording; starting clears earlier records. */
 mgn_status mgn_timing_enable(mgn_model* m, int enable);

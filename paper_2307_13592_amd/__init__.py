@@ -24,7 +24,7 @@ EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mg
            "mgn_partition_slabs", "mgn_graph_sizes", "mgn_graph_build", "mgn_graph_validate", "mgn_workspace_size",
            "mgn_forward", "mgn_backward", "mgn_mse_grad", "mgn_timing_enable", "mgn_timing_read"]
 TIMERS = ["encode", "edge_fwd", "node_fwd", "decode", "edge_bwd", "node_bwd", "input_grad", "weight_grad",
-          "other"]
+          "other", "node_proj"]
 
 
 class MgnError(RuntimeError):

@@ -36,7 +36,7 @@ struct MlpL {
 };
 
 struct WsPlan {
-  size_t erecv, chunk, unit_r, nunits, V, V16, AGG, ES, DV[2], DAGG, DZS, DE[2], DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
+  size_t erecv, chunk, unit_r, nunits, V, V16, PROJ, AGG, ES, DV[2], DAGG, DZS, DE[2], DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
       PART, VPART, total;
   int64_t max_units;
 };
@@ -183,6 +183,8 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.V = take(4 * (size_t)(K + 1) * no * L);
   // bf16 mode: bf16 copy of every block's node input, owned then halo rows
   p.V16 = m->prec == BF16 ? take(2 * (size_t)(K + 1) * (no + g->n_halo) * L) : 0;
+  // row-split edge kernels: node projections of the current block input
+  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(no + g->n_halo) * 2 * L) : 0;
   p.AGG = take(4 * (size_t)K * no * L);
   p.ES = take(ts * (size_t)std::max<int64_t>(K, 1) * ne * L);
   p.DV[0] = take(4 * (size_t)no * L);
@@ -468,7 +470,14 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
     ea.Eout = k + 1 < K ? ES(k + 1) : nullptr;
     ea.agg = AGG(k);
     ea.eps = m->cfg.ln_eps;
+    const bool rs = edge_rs(m->prec, L, D);
+    ea.proj = rs ? (const float*)(ws + p.PROJ) : nullptr;
     if (no > 0) {
+      if (rs) {
+        Timed t_(m, MGN_T_NODE_PROJ, st);
+        e = launch_node_proj(L, V16(k), no + nh, ea.mlp.lin[0], (float*)(ws + p.PROJ), st);
+        if (e != hipSuccess) return hip_fail(m, e, "mgn_forward node projections");
+      }
       Timed t_(m, MGN_T_EDGE_FWD, st);
       e = launch_edge_fwd(m->prec, L, D, ea, FWD_EDGE_GRID, st);
       if (e != hipSuccess) return hip_fail(m, e, "mgn_forward edge block");
@@ -696,6 +705,13 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.de_next = (k == K - 1) ? nullptr : DE[a_];
       a.dagg = DAGG;
       a.de_out = DE[b_];
+      const bool rs = edge_rs(m->prec, L, D);
+      a.proj = rs ? (const float*)(ws + p.PROJ) : nullptr;
+      if (rs && no > 0) {
+        Timed t_(m, MGN_T_NODE_PROJ, st);
+        e = launch_node_proj(L, V16(k), no + nh, a.mlp.lin[0], (float*)(ws + p.PROJ), st);
+        CHK("node projections");
+      }
       for (int j = 0; j < 3; ++j) a.delta[j] = DEL_E[j];
       for (int j = 0; j < 2; ++j) a.hid[j] = HID_E[j];
       a.vpart = VP;

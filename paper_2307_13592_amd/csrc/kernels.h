@@ -38,6 +38,7 @@ struct EdgeFwdArgs {
   const void* Ein;  // edge latents in [E][L] (storage type)
   void* Eout;       // edge latents out, or null (last block)
   float* agg;       // [n_owned][L]
+  const float* proj;  // node projections [n_local][2L] (row-split kernels), else unused
   float eps;
 };
 
@@ -72,6 +73,7 @@ struct EdgeBwdArgs {
   const float* de_next; // dL/de^{k+1} [E][L] or null (last block)
   float* dagg;          // [n_owned][L]: dL/dagg in; each receiver's sum of dz_0 out
   float* de_out;        // dL/de^k [E][L]
+  const float* proj;    // node projections [n_local][2L] (row-split kernels), else unused
   void* delta[3];
   void* hid[2];
   float* vpart;
@@ -135,6 +137,10 @@ hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& 
 hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int grid, hipStream_t st);
 // Workgroups (= vector-partial slots) the edge backward uses when asked for `grid`.
 int edge_bwd_grid(int prec, int L, int D, int grid);
+// Whether the edge kernels take the row-split form (it needs the node
+// projections of launch_node_proj for each block).
+bool edge_rs(int prec, int L, int D);
+hipError_t launch_node_proj(int L, const void* v16, int64_t n_local, const Lin& w1, float* proj, hipStream_t st);
 hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t st);
 hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st);
 hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int ldw, int accumulate,

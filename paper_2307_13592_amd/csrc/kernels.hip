@@ -1300,6 +1300,600 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void ed
   }
 }
 
+// ------------------------------------------------ row-split edge kernels ---
+// bf16, latent 64 or 128.  The first Linear of the edge MLP acts on
+// [e | v_s | v_r]; its sender and receiver blocks are applied per node once
+// per block (node_proj_kernel: P[n] = [W_s v_n | W_r v_n], fp32), so per edge
+// z_1 = W_e e + P_s[s] + P_r[r] + b_1 and the per-edge weights shrink to
+// L x L matrices.  Those sit in LDS, shared by the workgroup's waves, and
+// every wave works alone on 16-edge tiles of its own receiver-aligned edge
+// range: A operands come straight from HBM in MFMA fragment order, row-wise
+// quantities (LayerNorm statistics, segment sums) stay inside the wave, and
+// there is no barrier in the edge loop, so one wave's memory latency hides
+// behind the others' products.  A wave-private LDS scratch turns
+// accumulator tiles back into row order (operands of the next product,
+// coalesced row stores).
+
+constexpr int RS_NWV = 8;              // waves per workgroup
+constexpr int RS_NTH = 64 * RS_NWV;
+constexpr int RS_GRID = 256;           // one workgroup per compute unit; a multiple of 8
+
+// bf16 / fp32 element index of (row, col) in a 16-row scratch tile of width
+// L whose 16-byte chunks are XOR-swizzled by row (conflict-free both for
+// accumulator-order writes and for fragment / row-order reads).
+template <int L>
+__device__ __forceinline__ int rs_sw16(int row, int col) {
+  constexpr int M = (L / 8 < 16 ? L / 8 : 16) - 1;
+  return row * L + ((((col >> 3) ^ (row & M))) << 3) + (col & 7);
+}
+template <int L>
+__device__ __forceinline__ int rs_sw32(int row, int col) {
+  constexpr int M = (L / 4 < 16 ? L / 4 : 16) - 1;
+  return row * L + ((((col >> 2) ^ (row & M))) << 2) + (col & 3);
+}
+
+// acc[cb] = sum over k-groups of A[kg] x B[cb][kg]: one 16-row tile, every
+// 16-column block cb, B fragments in LDS ([cb][kg][lane], 16 bytes each).
+template <int NB, int NKG>
+__device__ __forceinline__ void rs_gemm(const uint4 (&A)[NKG], const uint4* Bl, floatx4 (&acc)[NB], int lane) {
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kg = 0; kg < NKG; ++kg)
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) PBF16::mma(acc[cb], A[kg], Bl[(cb * NKG + kg) * 64 + lane]);
+}
+
+// Copies nb 16-column blocks x nkg k-groups of packed fragments (source
+// block stride src_nkg k-groups, first k-group kg0) into LDS, all threads.
+__device__ __forceinline__ void rs_copy_frags(uint4* dst, const uint4* __restrict__ src, int nb, int nkg, int src_nkg,
+                                              int kg0) {
+  const int total = nb * nkg * 64;
+  for (int i = threadIdx.x; i < total; i += blockDim.x) {
+    const int cb = i / (nkg * 64), kg = (i / 64) % nkg, ln = i % 64;
+    dst[i] = src[((size_t)cb * src_nkg + kg0 + kg) * 64 + ln];
+  }
+}
+
+// Receiver range of wave w (of W waves in total): receiver-aligned, about
+// E / W edges each; the waves of one XCD (blockIdx % 8) get neighbouring ranges.
+__device__ __forceinline__ void rs_range(const int32_t* __restrict__ row_ptr, int64_t n_owned, int64_t& r0,
+                                         int64_t& r1) {
+  const int G = gridDim.x, b = blockIdx.x, nwv = blockDim.x >> 6, wave = threadIdx.x >> 6;
+  const int64_t W = (int64_t)G * nwv;
+  const int64_t q = ((int64_t)(b & 7) * (G >> 3) + (b >> 3)) * nwv + wave;
+  const int64_t E = row_ptr[n_owned];
+  auto find = [&](int64_t target) {  // first receiver r with row_ptr[r] >= target
+    int64_t lo = 0, hi = n_owned;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (row_ptr[mid] >= target) hi = mid;
+      else lo = mid + 1;
+    }
+    return lo;
+  };
+  r0 = q == 0 ? 0 : find(E * q / W);
+  r1 = q + 1 == W ? n_owned : find(E * (q + 1) / W);
+}
+
+// Zeroes the rows (width L) of the receivers in [r0, r1) without edges (one
+// wave, a lane per receiver).
+__device__ __forceinline__ void rs_zero_empty(const int32_t* __restrict__ row_ptr, int64_t r0, int64_t r1, float* dst,
+                                              int L) {
+  const int lane = threadIdx.x & 63;
+  for (int64_t r = r0 + lane; r < r1; r += 64)
+    if (row_ptr[r] == row_ptr[r + 1])
+      for (int c = 0; c < L; c += 4) *reinterpret_cast<float4*>(dst + r * L + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// One 16-edge tile's metadata: lane j < 16 holds edge sb + j's receiver,
+// sender and the next edge's receiver (-1 past the range end); the mask has
+// bit j set where row j ends a receiver segment.
+struct RsMeta {
+  int32_t r, s;
+  unsigned long long last;
+};
+__device__ __forceinline__ RsMeta rs_meta(const int32_t* __restrict__ erecv, const int32_t* __restrict__ send,
+                                          int64_t sb, int64_t e1) {
+  const int lane = threadIdx.x & 63;
+  RsMeta mt{-1, 0, 0};
+  int32_t rn = -1;
+  if (lane < 16 && sb + lane < e1) {
+    mt.r = erecv[sb + lane];
+    mt.s = send[sb + lane];
+    if (sb + lane + 1 < e1) rn = erecv[sb + lane + 1];
+  }
+  mt.last = __ballot(mt.r >= 0 && rn != mt.r);
+  return mt;
+}
+
+// z_1 of a tile in accumulator order: W_e e (MFMA) + P_s[s] + P_r[r] + b_1,
+// added in that order (the forward and the recompute in the backward share it).
+template <int L>
+__device__ __forceinline__ void rs_first_layer(const uint4 (&ef)[L / 32], const uint4* W1e, const RsMeta& mt, int n,
+                                               const float* __restrict__ proj, const float* __restrict__ b1,
+                                               floatx4 (&z)[L / 16], int lane) {
+  constexpr int NB = L / 16;
+  float ps[NB][4], pr[NB][4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int row = (lane >> 4) * 4 + r;
+    const int64_t s = __shfl(mt.s, row, 64), rv = __shfl(mt.r, row, 64);
+    const bool ok = row < n;
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const int col = cb * 16 + (lane & 15);
+      ps[cb][r] = ok ? proj[s * (2 * L) + col] : 0.f;
+      pr[cb][r] = ok ? proj[rv * (2 * L) + L + col] : 0.f;
+    }
+  }
+  rs_gemm<NB, L / 32>(ef, W1e, z, lane);
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) {
+    const float bv = b1[cb * 16 + (lane & 15)];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) z[cb][r] = ((z[cb][r] + ps[cb][r]) + pr[cb][r]) + bv;
+  }
+}
+
+// Accumulator tile -> bf16 scratch (row order, swizzled) -> A fragments.
+template <int L>
+__device__ __forceinline__ void rs_to_frags(const float (&v)[L / 16][4], uint16_t* scr, uint4 (&f)[L / 32], int lane) {
+  constexpr int NB = L / 16;
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) scr[rs_sw16<L>((lane >> 4) * 4 + r, cb * 16 + (lane & 15))] = f2bf(v[cb][r]);
+#pragma unroll
+  for (int kg = 0; kg < L / 32; ++kg)
+    f[kg] = *reinterpret_cast<const uint4*>(scr + rs_sw16<L>(lane & 15, kg * 32 + (lane >> 4) * 8));
+}
+
+// n rows of a bf16 scratch tile -> consecutive global rows at dst.
+template <int L>
+__device__ __forceinline__ void rs_store_rows(uint16_t* __restrict__ dst, const uint16_t* scr, int n, int lane) {
+  constexpr int CPR = L / 8;
+  for (int i = lane; i < 16 * CPR; i += 64) {
+    const int row = i / CPR, c = (i % CPR) * 8;
+    if (row < n) *reinterpret_cast<uint4*>(dst + (int64_t)row * L + c) = *reinterpret_cast<const uint4*>(scr + rs_sw16<L>(row, c));
+  }
+}
+
+// Row totals of an accumulator tile over all L columns (the 16 lanes of a
+// row group, butterfly): every lane gets its rows' totals.
+template <int NB>
+__device__ __forceinline__ void rs_row_totals(const float (&v)[NB][4], float (&t)[4]) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float x = 0.f;
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) x += v[cb][r];
+    x += __shfl_xor(x, 1, 64);
+    x += __shfl_xor(x, 2, 64);
+    x += __shfl_xor(x, 4, 64);
+    x += __shfl_xor(x, 8, 64);
+    t[r] = x;
+  }
+}
+
+template <int L, int D>
+struct RsFwdLay {
+  static constexpr int NKH = L / 32, NB = L / 16;
+  static constexpr int W = NB * NKH * 64 * 16;         // bytes of one L x L packed layer
+  static constexpr int SCR = 16 * L * 4;               // per-wave scratch (fp32 tile)
+  static constexpr int OFF_W1 = 0, OFF_WH = W, OFF_WL = (D - 1) * W, OFF_SCR = D * W;
+  static constexpr int END = OFF_SCR + RS_NWV * SCR;
+};
+
+// Forward of one block's edge half; P = node projections of the block input.
+template <int L, int D>
+__global__ __launch_bounds__(RS_NTH) void edge_fwd_rs_kernel(EdgeFwdArgs a) {
+  using Lay = RsFwdLay<L, D>;
+  constexpr int NKH = Lay::NKH, NB = Lay::NB;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* W1 = reinterpret_cast<uint4*>(lds + Lay::OFF_W1);
+  uint4* WH = reinterpret_cast<uint4*>(lds + Lay::OFF_WH);
+  uint4* WL = reinterpret_cast<uint4*>(lds + Lay::OFF_WL);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float* scr32 = reinterpret_cast<float*>(lds + Lay::OFF_SCR + wave * Lay::SCR);
+  uint16_t* scr16 = reinterpret_cast<uint16_t*>(scr32);
+  rs_copy_frags(W1, a.mlp.lin[0].wf, NB, NKH, 3 * NKH, 0);
+  if constexpr (D == 3) rs_copy_frags(WH, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
+  rs_copy_frags(WL, a.mlp.lin[D - 1].wf, NB, NKH, NKH, 0);
+  __syncthreads();
+  int64_t r0, r1;
+  rs_range(a.row_ptr, a.n_owned, r0, r1);
+  rs_zero_empty(a.row_ptr, r0, r1, a.agg, L);
+  const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
+  const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
+  uint16_t* Eout = reinterpret_cast<uint16_t*>(a.Eout);
+  float run[(L + 63) / 64] = {};  // running receiver sums, columns lane + 64 j
+  for (int64_t sb = E0; sb < E1; sb += 16) {
+    // an opaque copy of the lane index, so that the lane-dependent addresses
+    // are recomputed per tile instead of being hoisted into registers
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int arow = ln & 15, ach = ln >> 4;
+    const int n = (int)(E1 - sb < 16 ? E1 - sb : 16);
+    const RsMeta mt = rs_meta(a.erecv, a.send, sb, E1);
+    uint4 ef[NKH];
+#pragma unroll
+    for (int kg = 0; kg < NKH; ++kg)
+      ef[kg] = arow < n ? *reinterpret_cast<const uint4*>(Ein + (sb + arow) * L + kg * 32 + ach * 8)
+                        : make_uint4(0, 0, 0, 0);
+    floatx4 z[NB];
+    rs_first_layer<L>(ef, W1, mt, n, a.proj, a.mlp.lin[0].b, z, ln);
+    float h[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) h[cb][r] = z[cb][r] > 0.f ? z[cb][r] : 0.f;
+    uint4 hf[NKH];
+    rs_to_frags<L>(h, scr16, hf, ln);
+    if constexpr (D == 3) {
+      floatx4 acc[NB];
+      rs_gemm<NB, NKH>(hf, WH, acc, ln);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float bv = a.mlp.lin[1].b[cb * 16 + (ln & 15)];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float v = acc[cb][r] + bv;
+          h[cb][r] = v > 0.f ? v : 0.f;
+        }
+      }
+      rs_to_frags<L>(h, scr16, hf, ln);
+    }
+    floatx4 acc[NB];
+    rs_gemm<NB, NKH>(hf, WL, acc, ln);
+    float y[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float bv = a.mlp.lin[D - 1].b[cb * 16 + (ln & 15)];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[cb][r] = acc[cb][r] + bv;
+    }
+    // LayerNorm: two-pass statistics per row, then gamma * xhat + beta
+    float mu[4], var[4];
+    rs_row_totals<NB>(y, mu);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) mu[r] = mu[r] / L;
+    float dv[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float d = y[cb][r] - mu[r];
+        dv[cb][r] = d * d;
+      }
+    rs_row_totals<NB>(dv, var);
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const int col = cb * 16 + (ln & 15);
+      const float g = a.mlp.gamma[col], bt = a.mlp.beta[col];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float rs = 1.0f / sqrtf(var[r] / L + a.eps);
+        scr32[rs_sw32<L>(((ln >> 4) * 4 + r), col)] = g * ((y[cb][r] - mu[r]) * rs) + bt;
+      }
+    }
+    // e^{k+1} = e^k + m in fragment order (16 bytes per lane and k-group)
+    if (Eout && arow < n) {
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) {
+        const int c = kg * 32 + ach * 8;
+        const float4 m0 = *reinterpret_cast<const float4*>(scr32 + rs_sw32<L>(arow, c));
+        const float4 m1 = *reinterpret_cast<const float4*>(scr32 + rs_sw32<L>(arow, c + 4));
+        const uint16_t* e = reinterpret_cast<const uint16_t*>(&ef[kg]);
+        uint16_t o[8];
+        o[0] = f2bf(bf2f(e[0]) + m0.x);
+        o[1] = f2bf(bf2f(e[1]) + m0.y);
+        o[2] = f2bf(bf2f(e[2]) + m0.z);
+        o[3] = f2bf(bf2f(e[3]) + m0.w);
+        o[4] = f2bf(bf2f(e[4]) + m1.x);
+        o[5] = f2bf(bf2f(e[5]) + m1.y);
+        o[6] = f2bf(bf2f(e[6]) + m1.z);
+        o[7] = f2bf(bf2f(e[7]) + m1.w);
+        *reinterpret_cast<uint4*>(Eout + (sb + arow) * L + c) = *reinterpret_cast<const uint4*>(o);
+      }
+    }
+    // ordered receiver sums; a segment's total goes out at its last row
+#pragma unroll
+    for (int j = 0; j < (L + 63) / 64; ++j) {
+      const int c = ln + 64 * j;
+      if (c < L) {
+        for (int row = 0; row < n; ++row) {
+          run[j] += scr32[rs_sw32<L>(row, c)];
+          if ((mt.last >> row) & 1ull) {
+            a.agg[(int64_t)__shfl(mt.r, row, 64) * L + c] = run[j];
+            run[j] = 0.f;
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int L, int D>
+struct RsBwdLay {
+  static constexpr int NKH = L / 32, NB = L / 16;
+  static constexpr int W = NB * NKH * 64 * 16;
+  static constexpr int SCR = 16 * L * 2;               // per-wave scratch (bf16 tile)
+  // W_e (fwd), [W_h (fwd)], W_last (fwd), W_last (bwd), [W_h (bwd)], W_e (bwd)
+  static constexpr int NW = D == 3 ? 6 : 4;
+  static constexpr int OFF_SCR = NW * W;
+  static constexpr int END = OFF_SCR + RS_NWV * SCR;
+  static constexpr int NVEC = (D + 2) * L;             // bias / gamma / beta partials per wave
+  static_assert(RS_NWV * NVEC * 4 <= OFF_SCR, "partials reuse the weight area");
+};
+
+// Backward of one block's edge half with the tile's forward recomputed (same
+// quantities as edge_bwd_kernel: dz_0 receiver sums over the consumed dagg
+// rows, de^k, the stored gradients and activations, per-workgroup partials).
+template <int L, int D>
+__global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
+  using Lay = RsBwdLay<L, D>;
+  constexpr int NKH = Lay::NKH, NB = Lay::NB, W = Lay::W;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* W1f = reinterpret_cast<uint4*>(lds);
+  uint4* WHf = reinterpret_cast<uint4*>(lds + W);
+  uint4* WLf = reinterpret_cast<uint4*>(lds + (D - 1) * W);
+  uint4* WLb = reinterpret_cast<uint4*>(lds + D * W);
+  uint4* WHb = reinterpret_cast<uint4*>(lds + (D + 1) * W);
+  uint4* W1b = reinterpret_cast<uint4*>(lds + (Lay::NW - 1) * W);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  uint16_t* scr = reinterpret_cast<uint16_t*>(lds + Lay::OFF_SCR + wave * Lay::SCR);
+  rs_copy_frags(W1f, a.mlp.lin[0].wf, NB, NKH, 3 * NKH, 0);
+  if constexpr (D == 3) rs_copy_frags(WHf, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
+  rs_copy_frags(WLf, a.mlp.lin[D - 1].wf, NB, NKH, NKH, 0);
+  rs_copy_frags(WLb, a.mlp.lin[D - 1].wb, NB, NKH, NKH, 0);
+  if constexpr (D == 3) rs_copy_frags(WHb, a.mlp.lin[1].wb, NB, NKH, NKH, 0);
+  rs_copy_frags(W1b, a.mlp.lin[0].wb, NB, NKH, NKH, 0);  // e block: the first NB column blocks
+  __syncthreads();
+  int64_t r0, r1;
+  rs_range(a.row_ptr, a.n_owned, r0, r1);
+  rs_zero_empty(a.row_ptr, r0, r1, a.dagg, L);
+  const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
+  const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
+  float pg[NB], pb[NB], pl[NB], ph[2][NB];  // column partials over this lane's rows
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) pg[cb] = pb[cb] = pl[cb] = ph[0][cb] = ph[1][cb] = 0.f;
+  float run[(L + 63) / 64] = {};
+  for (int64_t sb = E0; sb < E1; sb += 16) {
+    // an opaque copy of the lane index, so that the lane-dependent addresses
+    // are recomputed per tile instead of being hoisted into registers
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int arow = ln & 15, ach = ln >> 4;
+    const int n = (int)(E1 - sb < 16 ? E1 - sb : 16);
+    const RsMeta mt = rs_meta(a.erecv, a.send, sb, E1);
+    uint4 ef[NKH];
+#pragma unroll
+    for (int kg = 0; kg < NKH; ++kg)
+      ef[kg] = arow < n ? *reinterpret_cast<const uint4*>(Ein + (sb + arow) * L + kg * 32 + ach * 8)
+                        : make_uint4(0, 0, 0, 0);
+    floatx4 z[NB];
+    rs_first_layer<L>(ef, W1f, mt, n, a.proj, a.mlp.lin[0].b, z, ln);
+    // dm = de^{k+1} + dagg[receiver], accumulator order
+    float de[NB][4], da[NB][4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = ((ln >> 4) * 4 + r);
+      const bool ok = row < n;
+      const int64_t rv = __shfl(mt.r, row, 64);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const int col = cb * 16 + (ln & 15);
+        de[cb][r] = (ok && a.de_next) ? a.de_next[(sb + row) * L + col] : 0.f;
+        da[cb][r] = ok ? a.dagg[rv * L + col] : 0.f;
+      }
+    }
+    uint32_t mask[2] = {0u, 0u};  // ReLU derivative of the hidden layers, bit cb * 4 + r
+    float h[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool on = z[cb][r] > 0.f;
+        mask[0] |= (on ? 1u : 0u) << (cb * 4 + r);
+        h[cb][r] = on ? z[cb][r] : 0.f;
+      }
+    uint4 hf[NKH];
+    rs_to_frags<L>(h, scr, hf, ln);
+    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.hid[0]) + sb * L, scr, n, ln);
+    if constexpr (D == 3) {
+      floatx4 acc[NB];
+      rs_gemm<NB, NKH>(hf, WHf, acc, ln);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float bv = a.mlp.lin[1].b[cb * 16 + (ln & 15)];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float v = acc[cb][r] + bv;
+          const bool on = v > 0.f;
+          mask[1] |= (on ? 1u : 0u) << (cb * 4 + r);
+          h[cb][r] = on ? v : 0.f;
+        }
+      }
+      rs_to_frags<L>(h, scr, hf, ln);
+      rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.hid[1]) + sb * L, scr, n, ln);
+    }
+    float y[NB][4];
+    {
+      floatx4 acc[NB];
+      rs_gemm<NB, NKH>(hf, WLf, acc, ln);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float bv = a.mlp.lin[D - 1].b[cb * 16 + (ln & 15)];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[cb][r] = acc[cb][r] + bv;
+      }
+    }
+    // LayerNorm (recomputed): y becomes xhat
+    float mu[4], rs[4], t1[4], t2[4];
+    rs_row_totals<NB>(y, mu);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) mu[r] = mu[r] / L;
+    {
+      float dv[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d = y[cb][r] - mu[r];
+          dv[cb][r] = d * d;
+        }
+      rs_row_totals<NB>(dv, rs);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) rs[r] = 1.0f / sqrtf(rs[r] / L + a.eps);
+    // LayerNorm backward: dy = rstd (dm g - mean(dm g) - xhat mean(dm g xhat))
+    float dg[NB][4], dgx[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        y[cb][r] = (y[cb][r] - mu[r]) * rs[r];
+        const float dm = da[cb][r] + de[cb][r];
+        dg[cb][r] = dm * g;
+        dgx[cb][r] = dg[cb][r] * y[cb][r];
+        pg[cb] += dm * y[cb][r];
+        pb[cb] += dm;
+      }
+    }
+    rs_row_totals<NB>(dg, t1);
+    rs_row_totals<NB>(dgx, t2);
+    float v[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[cb][r] = rs[r] * (dg[cb][r] - t1[r] / L - y[cb][r] * (t2[r] / L));
+        pl[cb] += v[cb][r];
+      }
+    uint4 gf[NKH];
+    rs_to_frags<L>(v, scr, gf, ln);
+    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + sb * L, scr, n, ln);
+    // hidden layers: dz_{j-1} = (dz_j W_j) * [z_{j-1} > 0]
+#pragma unroll
+    for (int j = D - 1; j >= 1; --j) {
+      floatx4 acc[NB];
+      if (j == D - 1) {
+        rs_gemm<NB, NKH>(gf, WLb, acc, ln);
+      } else {
+        if constexpr (D == 3) rs_gemm<NB, NKH>(gf, WHb, acc, ln);
+      }
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[cb][r] = ((mask[j - 1] >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
+          ph[j - 1][cb] += v[cb][r];
+        }
+      rs_to_frags<L>(v, scr, gf, ln);
+      rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + sb * L, scr, n, ln);
+    }
+    // edge-stream gradient: de^k = de^{k+1} + dz_0 W_1[:, e-block]
+    {
+      floatx4 acc[NB];
+      rs_gemm<NB, NKH>(gf, W1b, acc, ln);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = ((ln >> 4) * 4 + r);
+        if (row < n) {
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb) a.de_out[(sb + row) * L + cb * 16 + (ln & 15)] = acc[cb][r] + de[cb][r];
+        }
+      }
+    }
+    // receiver sums of dz_0 (bf16, as it fed the products), ascending edge order
+#pragma unroll
+    for (int j = 0; j < (L + 63) / 64; ++j) {
+      const int c = ln + 64 * j;
+      if (c < L) {
+        for (int row = 0; row < n; ++row) {
+          run[j] += bf2f(scr[rs_sw16<L>(row, c)]);
+          if ((mt.last >> row) & 1ull) {
+            a.dagg[(int64_t)__shfl(mt.r, row, 64) * L + c] = run[j];
+            run[j] = 0.f;
+          }
+        }
+      }
+    }
+  }
+  // column partials: the four 16-lane groups of each column, then the waves
+  // in order through LDS (the weight area is free now)
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(lds);
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) {
+    float q[5] = {ph[0][cb], ph[1][cb], pl[cb], pg[cb], pb[cb]};
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      q[k] += __shfl_xor(q[k], 16, 64);
+      q[k] += __shfl_xor(q[k], 32, 64);
+    }
+    if (lane < 16) {
+      const int col = cb * 16 + lane;
+      float* rw = red + wave * Lay::NVEC;
+#pragma unroll
+      for (int j = 0; j < D - 1; ++j) rw[j * L + col] = q[j];
+      rw[(D - 1) * L + col] = q[2];
+      rw[D * L + col] = q[3];
+      rw[(D + 1) * L + col] = q[4];
+    }
+  }
+  __syncthreads();
+  float* vp = a.vpart + (int64_t)blockIdx.x * a.nvec;
+  for (int i = threadIdx.x; i < Lay::NVEC; i += RS_NTH) {
+    float t = 0.f;
+    for (int w = 0; w < RS_NWV; ++w) t += red[w * Lay::NVEC + i];
+    vp[i] = t;
+  }
+}
+
+// P[n] = [W_s v_n | W_r v_n] for the local nodes: the sender and receiver
+// blocks of the edge MLP's first Linear on the bf16 block input (fp32 sums).
+template <int L>
+__global__ __launch_bounds__(RS_NTH) void node_proj_kernel(const uint16_t* __restrict__ V16, int64_t n_local, Lin w1,
+                                                           float* __restrict__ proj) {
+  constexpr int NKH = L / 32, NB = L / 16;
+  constexpr int W = NB * NKH * 64 * 16;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* WS = reinterpret_cast<uint4*>(lds);
+  uint4* WR = reinterpret_cast<uint4*>(lds + W);
+  rs_copy_frags(WS, w1.wf, NB, NKH, 3 * NKH, NKH);
+  rs_copy_frags(WR, w1.wf, NB, NKH, 3 * NKH, 2 * NKH);
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t ntiles = (n_local + 15) / 16;
+  for (int64_t t = (int64_t)blockIdx.x * RS_NWV + wave; t < ntiles; t += (int64_t)gridDim.x * RS_NWV) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int arow = ln & 15, ach = ln >> 4;
+    const int64_t n0 = t * 16;
+    uint4 vf[NKH];
+#pragma unroll
+    for (int kg = 0; kg < NKH; ++kg)
+      vf[kg] = n0 + arow < n_local ? *reinterpret_cast<const uint4*>(V16 + (n0 + arow) * L + kg * 32 + ach * 8)
+                                   : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int side = 0; side < 2; ++side) {
+      floatx4 acc[NB];
+      rs_gemm<NB, NKH>(vf, side == 0 ? WS : WR, acc, ln);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t node = n0 + (ln >> 4) * 4 + r;
+        if (node < n_local) {
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb) proj[node * (2 * L) + side * L + cb * 16 + (ln & 15)] = acc[cb][r];
+        }
+      }
+    }
+  }
+}
+
 // --------------------------------------------------- node input gradient ---
 // Gradient reaching the nodes through the first Linear of a block's edge MLP.
 // Its sender and receiver column blocks W_s, W_r are shared by all edges, so
@@ -1883,7 +2477,45 @@ hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& 
   return hipErrorInvalidValue;
 }
 
+bool edge_rs(int prec, int L, int D) { return prec == BF16 && (L == 64 || (L == 128 && D == 2)); }
+
+template <int L, int D>
+static hipError_t edge_fwd_rs_t(const EdgeFwdArgs& a, hipStream_t st) {
+  using Lay = RsFwdLay<L, D>;
+  allow_lds(edge_fwd_rs_kernel<L, D>, Lay::END);
+  hipLaunchKernelGGL((edge_fwd_rs_kernel<L, D>), dim3(RS_GRID), dim3(RS_NTH), Lay::END, st, a);
+  return hipGetLastError();
+}
+
+template <int L, int D>
+static hipError_t edge_bwd_rs_t(const EdgeBwdArgs& a, hipStream_t st) {
+  using Lay = RsBwdLay<L, D>;
+  allow_lds(edge_bwd_rs_kernel<L, D>, Lay::END);
+  hipLaunchKernelGGL((edge_bwd_rs_kernel<L, D>), dim3(RS_GRID), dim3(RS_NTH), Lay::END, st, a);
+  return hipGetLastError();
+}
+
+template <int L>
+static hipError_t node_proj_t(const void* v16, int64_t n_local, const Lin& w1, float* proj, hipStream_t st) {
+  constexpr int W = (L / 16) * (L / 32) * 64 * 16;
+  allow_lds(node_proj_kernel<L>, 2 * W);
+  hipLaunchKernelGGL((node_proj_kernel<L>), dim3(RS_GRID), dim3(RS_NTH), 2 * W, st,
+                     reinterpret_cast<const uint16_t*>(v16), n_local, w1, proj);
+  return hipGetLastError();
+}
+
+hipError_t launch_node_proj(int L, const void* v16, int64_t n_local, const Lin& w1, float* proj, hipStream_t st) {
+  if (n_local == 0) return hipSuccess;
+  if (L == 64) return node_proj_t<64>(v16, n_local, w1, proj, st);
+  if (L == 128) return node_proj_t<128>(v16, n_local, w1, proj, st);
+  return hipErrorInvalidValue;
+}
+
 hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int grid, hipStream_t st) {
+  if (edge_rs(prec, L, D)) {
+    if (L == 64) return D == 2 ? edge_fwd_rs_t<64, 2>(a, st) : edge_fwd_rs_t<64, 3>(a, st);
+    return edge_fwd_rs_t<128, 2>(a, st);
+  }
 #define EF(PP, LL, DD) \
   if (prec == PP && L == LL && D == DD) return edge_fwd_t<PP, LL, DD>(a, grid, st);
   EF(F32, 64, 2) EF(F32, 64, 3) EF(F32, 128, 2) EF(F32, 128, 3) EF(F32, 256, 2) EF(F32, 256, 3)
@@ -1892,9 +2524,13 @@ hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int gri
   return hipErrorInvalidValue;
 }
 
-int edge_bwd_grid(int prec, int L, int D, int grid) { return grid; }
+int edge_bwd_grid(int prec, int L, int D, int grid) { return edge_rs(prec, L, D) ? RS_GRID : grid; }
 
 hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int grid, hipStream_t st) {
+  if (edge_rs(prec, L, D)) {
+    if (L == 64) return D == 2 ? edge_bwd_rs_t<64, 2>(a, st) : edge_bwd_rs_t<64, 3>(a, st);
+    return edge_bwd_rs_t<128, 2>(a, st);
+  }
 #define EB(PP, LL, DD) \
   if (prec == PP && L == LL && D == DD) return edge_bwd_t<PP, LL, DD>(a, grid, st);
   EB(F32, 64, 2) EB(F32, 64, 3) EB(F32, 128, 2) EB(F32, 128, 3) EB(F32, 256, 2) EB(F32, 256, 3)
