@@ -1332,6 +1332,28 @@ __device__ __forceinline__ int rs_sw32(int row, int col) {
   return row * L + ((((col >> 2) ^ (row & M))) << 2) + (col & 3);
 }
 
+// Lane-major column order of fp32 rows the row-split kernels exchange in
+// accumulator order (node projections, edge-stream gradients): column
+// cb * 16 + c is stored at c * NB + cb, so the NB columns one lane holds of
+// a row are contiguous (NB / 4 16-byte accesses instead of NB 4-byte ones).
+template <int L>
+__device__ __forceinline__ void rs_load_row(const float* __restrict__ row, int c, float (&v)[L / 16]) {
+#pragma unroll
+  for (int q = 0; q < L / 64; ++q) {
+    const float4 x = reinterpret_cast<const float4*>(row + c * (L / 16))[q];
+    v[4 * q] = x.x;
+    v[4 * q + 1] = x.y;
+    v[4 * q + 2] = x.z;
+    v[4 * q + 3] = x.w;
+  }
+}
+template <int L>
+__device__ __forceinline__ void rs_store_row(float* __restrict__ row, int c, const float (&v)[L / 16]) {
+#pragma unroll
+  for (int q = 0; q < L / 64; ++q)
+    reinterpret_cast<float4*>(row + c * (L / 16))[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+}
+
 // acc[cb] = sum over k-groups of A[kg] x B[cb][kg]: one 16-row tile, every
 // 16-column block cb, B fragments in LDS ([cb][kg][lane], 16 bytes each).
 template <int NB, int NKG>
@@ -1389,21 +1411,29 @@ __device__ __forceinline__ void rs_zero_empty(const int32_t* __restrict__ row_pt
 // One 16-edge tile's metadata: lane j < 16 holds edge sb + j's receiver,
 // sender and the next edge's receiver (-1 past the range end); the mask has
 // bit j set where row j ends a receiver segment.
+// The loads are issued one tile ahead (rs_meta_load) and turned into the
+// mask when the tile starts (rs_meta_make), so no tile waits for them.
 struct RsMeta {
   int32_t r, s;
   unsigned long long last;
 };
-__device__ __forceinline__ RsMeta rs_meta(const int32_t* __restrict__ erecv, const int32_t* __restrict__ send,
-                                          int64_t sb, int64_t e1) {
+struct RsMetaRaw {
+  int32_t r, s, rn;
+};
+__device__ __forceinline__ RsMetaRaw rs_meta_load(const int32_t* __restrict__ erecv, const int32_t* __restrict__ send,
+                                                  int64_t sb, int64_t e1) {
   const int lane = threadIdx.x & 63;
-  RsMeta mt{-1, 0, 0};
-  int32_t rn = -1;
+  RsMetaRaw w{-1, 0, -1};
   if (lane < 16 && sb + lane < e1) {
-    mt.r = erecv[sb + lane];
-    mt.s = send[sb + lane];
-    if (sb + lane + 1 < e1) rn = erecv[sb + lane + 1];
+    w.r = erecv[sb + lane];
+    w.s = send[sb + lane];
+    if (sb + lane + 1 < e1) w.rn = erecv[sb + lane + 1];
   }
-  mt.last = __ballot(mt.r >= 0 && rn != mt.r);
+  return w;
+}
+__device__ __forceinline__ RsMeta rs_meta_make(const RsMetaRaw& w) {
+  RsMeta mt{w.r, w.s, 0};
+  mt.last = __ballot(w.r >= 0 && w.rn != w.r);
   return mt;
 }
 
@@ -1414,17 +1444,17 @@ __device__ __forceinline__ void rs_first_layer(const uint4 (&ef)[L / 32], const 
                                                const float* __restrict__ proj, const float* __restrict__ b1,
                                                floatx4 (&z)[L / 16], int lane) {
   constexpr int NB = L / 16;
-  float ps[NB][4], pr[NB][4];
+  float ps[4][NB], pr[4][NB];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int row = (lane >> 4) * 4 + r;
     const int64_t s = __shfl(mt.s, row, 64), rv = __shfl(mt.r, row, 64);
-    const bool ok = row < n;
+    if (row < n) {
+      rs_load_row<L>(proj + s * (2 * L), lane & 15, ps[r]);
+      rs_load_row<L>(proj + rv * (2 * L) + L, lane & 15, pr[r]);
+    } else {
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-      const int col = cb * 16 + (lane & 15);
-      ps[cb][r] = ok ? proj[s * (2 * L) + col] : 0.f;
-      pr[cb][r] = ok ? proj[rv * (2 * L) + L + col] : 0.f;
+      for (int cb = 0; cb < NB; ++cb) ps[r][cb] = pr[r][cb] = 0.f;
     }
   }
   rs_gemm<NB, L / 32>(ef, W1e, z, lane);
@@ -1432,7 +1462,7 @@ __device__ __forceinline__ void rs_first_layer(const uint4 (&ef)[L / 32], const 
   for (int cb = 0; cb < NB; ++cb) {
     const float bv = b1[cb * 16 + (lane & 15)];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) z[cb][r] = ((z[cb][r] + ps[cb][r]) + pr[cb][r]) + bv;
+    for (int r = 0; r < 4; ++r) z[cb][r] = ((z[cb][r] + ps[r][cb]) + pr[r][cb]) + bv;
   }
 }
 
@@ -1459,8 +1489,21 @@ __device__ __forceinline__ void rs_store_rows(uint16_t* __restrict__ dst, const 
   }
 }
 
-// Row totals of an accumulator tile over all L columns (the 16 lanes of a
-// row group, butterfly): every lane gets its rows' totals.
+// Per-lane partials of the lane's four rows -> row totals over the 16 lanes
+// of the row group (butterfly; every lane of the group gets the same bits).
+__device__ __forceinline__ void rs_butterfly(float (&t)[4]) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float x = t[r];
+    x += __shfl_xor(x, 1, 64);
+    x += __shfl_xor(x, 2, 64);
+    x += __shfl_xor(x, 4, 64);
+    x += __shfl_xor(x, 8, 64);
+    t[r] = x;
+  }
+}
+
+// Row totals of an accumulator tile over all L columns.
 template <int NB>
 __device__ __forceinline__ void rs_row_totals(const float (&v)[NB][4], float (&t)[4]) {
 #pragma unroll
@@ -1468,12 +1511,9 @@ __device__ __forceinline__ void rs_row_totals(const float (&v)[NB][4], float (&t
     float x = 0.f;
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb) x += v[cb][r];
-    x += __shfl_xor(x, 1, 64);
-    x += __shfl_xor(x, 2, 64);
-    x += __shfl_xor(x, 4, 64);
-    x += __shfl_xor(x, 8, 64);
     t[r] = x;
   }
+  rs_butterfly(t);
 }
 
 template <int L, int D>
@@ -1508,6 +1548,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_fwd_rs_kernel(EdgeFwdArgs a) {
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
   uint16_t* Eout = reinterpret_cast<uint16_t*>(a.Eout);
   float run[(L + 63) / 64] = {};  // running receiver sums, columns lane + 64 j
+  RsMetaRaw nxt = rs_meta_load(a.erecv, a.send, E0, E1);
   for (int64_t sb = E0; sb < E1; sb += 16) {
     // an opaque copy of the lane index, so that the lane-dependent addresses
     // are recomputed per tile instead of being hoisted into registers
@@ -1515,7 +1556,8 @@ __global__ __launch_bounds__(RS_NTH) void edge_fwd_rs_kernel(EdgeFwdArgs a) {
     asm volatile("" : "+v"(ln));
     const int arow = ln & 15, ach = ln >> 4;
     const int n = (int)(E1 - sb < 16 ? E1 - sb : 16);
-    const RsMeta mt = rs_meta(a.erecv, a.send, sb, E1);
+    const RsMeta mt = rs_meta_make(nxt);
+    nxt = rs_meta_load(a.erecv, a.send, sb + 16, E1);
     uint4 ef[NKH];
 #pragma unroll
     for (int kg = 0; kg < NKH; ++kg)
@@ -1601,11 +1643,15 @@ __global__ __launch_bounds__(RS_NTH) void edge_fwd_rs_kernel(EdgeFwdArgs a) {
 #pragma unroll
     for (int j = 0; j < (L + 63) / 64; ++j) {
       const int c = ln + 64 * j;
-      if (c < L) {
-        for (int row = 0; row < n; ++row) {
-          run[j] += scr32[rs_sw32<L>(row, c)];
+      float x[16];
+#pragma unroll
+      for (int row = 0; row < 16; ++row) x[row] = scr32[rs_sw32<L>(row, c)];
+#pragma unroll
+      for (int row = 0; row < 16; ++row) {
+        if (row < n) {
+          run[j] += x[row];
           if ((mt.last >> row) & 1ull) {
-            a.agg[(int64_t)__shfl(mt.r, row, 64) * L + c] = run[j];
+            a.agg[(int64_t)__builtin_amdgcn_readlane(mt.r, row) * L + c] = run[j];
             run[j] = 0.f;
           }
         }
@@ -1659,6 +1705,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
 #pragma unroll
   for (int cb = 0; cb < NB; ++cb) pg[cb] = pb[cb] = pl[cb] = ph[0][cb] = ph[1][cb] = 0.f;
   float run[(L + 63) / 64] = {};
+  RsMetaRaw nxt = rs_meta_load(a.erecv, a.send, E0, E1);
   for (int64_t sb = E0; sb < E1; sb += 16) {
     // an opaque copy of the lane index, so that the lane-dependent addresses
     // are recomputed per tile instead of being hoisted into registers
@@ -1666,7 +1713,8 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
     asm volatile("" : "+v"(ln));
     const int arow = ln & 15, ach = ln >> 4;
     const int n = (int)(E1 - sb < 16 ? E1 - sb : 16);
-    const RsMeta mt = rs_meta(a.erecv, a.send, sb, E1);
+    const RsMeta mt = rs_meta_make(nxt);
+    nxt = rs_meta_load(a.erecv, a.send, sb + 16, E1);
     uint4 ef[NKH];
 #pragma unroll
     for (int kg = 0; kg < NKH; ++kg)
@@ -1674,20 +1722,6 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
                         : make_uint4(0, 0, 0, 0);
     floatx4 z[NB];
     rs_first_layer<L>(ef, W1f, mt, n, a.proj, a.mlp.lin[0].b, z, ln);
-    // dm = de^{k+1} + dagg[receiver], accumulator order
-    float de[NB][4], da[NB][4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = ((ln >> 4) * 4 + r);
-      const bool ok = row < n;
-      const int64_t rv = __shfl(mt.r, row, 64);
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb) {
-        const int col = cb * 16 + (ln & 15);
-        de[cb][r] = (ok && a.de_next) ? a.de_next[(sb + row) * L + col] : 0.f;
-        da[cb][r] = ok ? a.dagg[rv * L + col] : 0.f;
-      }
-    }
     uint32_t mask[2] = {0u, 0u};  // ReLU derivative of the hidden layers, bit cb * 4 + r
     float h[NB][4];
 #pragma unroll
@@ -1729,49 +1763,69 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
         for (int r = 0; r < 4; ++r) y[cb][r] = acc[cb][r] + bv;
       }
     }
+    // dm = dagg[receiver] + de^{k+1}, accumulator order
+    float dm[NB][4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = ((ln >> 4) * 4 + r);
+      const bool ok = row < n;
+      const int64_t rv = __shfl(mt.r, row, 64);
+      float de[NB];
+      if (ok && a.de_next) {
+        rs_load_row<L>(a.de_next + (sb + row) * L, ln & 15, de);
+      } else {
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) de[cb] = 0.f;
+      }
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) dm[cb][r] = (ok ? a.dagg[rv * L + cb * 16 + (ln & 15)] : 0.f) + de[cb];
+    }
     // LayerNorm (recomputed): y becomes xhat
     float mu[4], rs[4], t1[4], t2[4];
     rs_row_totals<NB>(y, mu);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) mu[r] = mu[r] / L;
-    {
-      float dv[NB][4];
+    for (int r = 0; r < 4; ++r) {
+      mu[r] = mu[r] / L;
+      float x = 0.f;
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float d = y[cb][r] - mu[r];
-          dv[cb][r] = d * d;
-        }
-      rs_row_totals<NB>(dv, rs);
+      for (int cb = 0; cb < NB; ++cb) {
+        const float d = y[cb][r] - mu[r];
+        x += d * d;
+      }
+      rs[r] = x;
     }
+    rs_butterfly(rs);
 #pragma unroll
     for (int r = 0; r < 4; ++r) rs[r] = 1.0f / sqrtf(rs[r] / L + a.eps);
     // LayerNorm backward: dy = rstd (dm g - mean(dm g) - xhat mean(dm g xhat))
-    float dg[NB][4], dgx[NB][4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) t1[r] = t2[r] = 0.f;
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb) {
       const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         y[cb][r] = (y[cb][r] - mu[r]) * rs[r];
-        const float dm = da[cb][r] + de[cb][r];
-        dg[cb][r] = dm * g;
-        dgx[cb][r] = dg[cb][r] * y[cb][r];
-        pg[cb] += dm * y[cb][r];
-        pb[cb] += dm;
+        const float d = dm[cb][r] * g;
+        t1[r] += d;
+        t2[r] += d * y[cb][r];
+        pg[cb] += dm[cb][r] * y[cb][r];
+        pb[cb] += dm[cb][r];
       }
     }
-    rs_row_totals<NB>(dg, t1);
-    rs_row_totals<NB>(dgx, t2);
+    rs_butterfly(t1);
+    rs_butterfly(t2);
     float v[NB][4];
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb)
+    for (int cb = 0; cb < NB; ++cb) {
+      const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        v[cb][r] = rs[r] * (dg[cb][r] - t1[r] / L - y[cb][r] * (t2[r] / L));
+        const float d = dm[cb][r] * g;
+        v[cb][r] = rs[r] * (d - t1[r] / L - y[cb][r] * (t2[r] / L));
         pl[cb] += v[cb][r];
       }
+    }
     uint4 gf[NKH];
     rs_to_frags<L>(v, scr, gf, ln);
     rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + sb * L, scr, n, ln);
@@ -1802,8 +1856,21 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
       for (int r = 0; r < 4; ++r) {
         const int row = ((ln >> 4) * 4 + r);
         if (row < n) {
+          float v[NB], dn[NB];
+          if (a.de_next) {
+            rs_load_row<L>(a.de_next + (sb + row) * L, ln & 15, dn);
+          } else {
 #pragma unroll
-          for (int cb = 0; cb < NB; ++cb) a.de_out[(sb + row) * L + cb * 16 + (ln & 15)] = acc[cb][r] + de[cb][r];
+            for (int cb = 0; cb < NB; ++cb) dn[cb] = 0.f;
+          }
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb) v[cb] = acc[cb][r] + dn[cb];
+          if (a.de_std) {
+#pragma unroll
+            for (int cb = 0; cb < NB; ++cb) a.de_out[(sb + row) * L + cb * 16 + (ln & 15)] = v[cb];
+          } else {
+            rs_store_row<L>(a.de_out + (sb + row) * L, ln & 15, v);
+          }
         }
       }
     }
@@ -1811,11 +1878,15 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
 #pragma unroll
     for (int j = 0; j < (L + 63) / 64; ++j) {
       const int c = ln + 64 * j;
-      if (c < L) {
-        for (int row = 0; row < n; ++row) {
-          run[j] += bf2f(scr[rs_sw16<L>(row, c)]);
+      float x[16];
+#pragma unroll
+      for (int row = 0; row < 16; ++row) x[row] = bf2f(scr[rs_sw16<L>(row, c)]);
+#pragma unroll
+      for (int row = 0; row < 16; ++row) {
+        if (row < n) {
+          run[j] += x[row];
           if ((mt.last >> row) & 1ull) {
-            a.dagg[(int64_t)__shfl(mt.r, row, 64) * L + c] = run[j];
+            a.dagg[(int64_t)__builtin_amdgcn_readlane(mt.r, row) * L + c] = run[j];
             run[j] = 0.f;
           }
         }
@@ -1854,7 +1925,8 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
 }
 
 // P[n] = [W_s v_n | W_r v_n] for the local nodes: the sender and receiver
-// blocks of the edge MLP's first Linear on the bf16 block input (fp32 sums).
+// blocks of the edge MLP's first Linear on the bf16 block input (fp32 sums),
+// each half in lane-major column order.
 template <int L>
 __global__ __launch_bounds__(RS_NTH) void node_proj_kernel(const uint16_t* __restrict__ V16, int64_t n_local, Lin w1,
                                                            float* __restrict__ proj) {
@@ -1886,8 +1958,10 @@ __global__ __launch_bounds__(RS_NTH) void node_proj_kernel(const uint16_t* __res
       for (int r = 0; r < 4; ++r) {
         const int64_t node = n0 + (ln >> 4) * 4 + r;
         if (node < n_local) {
+          float v[NB];
 #pragma unroll
-          for (int cb = 0; cb < NB; ++cb) proj[node * (2 * L) + side * L + cb * 16 + (ln & 15)] = acc[cb][r];
+          for (int cb = 0; cb < NB; ++cb) v[cb] = acc[cb][r];
+          rs_store_row<L>(proj + node * (2 * L) + side * L, ln & 15, v);
         }
       }
     }
@@ -2208,18 +2282,28 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void dw
       }
 }
 
-// dst[o * ldw + i] (+)= sum over the S split partials of part[.][o][i], in
-// split order.
-__global__ void dw_reduce_kernel(const float* __restrict__ part, int S, int O, int I, float* __restrict__ dst,
-                                 int ldw, int accumulate) {
+// dst[o * ldw + i] (+)= sum over the S split partials of part[.][o][i]: 64
+// outputs per workgroup, four threads per output each summing the splits
+// k = q (mod 4) in increasing k, combined in q order.
+__global__ __launch_bounds__(NT) void dw_reduce_kernel(const float* __restrict__ part, int S, int O, int I,
+                                                       float* __restrict__ dst, int ldw, int accumulate) {
+  __shared__ float sh[NT];
+  const int j = threadIdx.x & 63, q = threadIdx.x >> 6;
   const int64_t n = (int64_t)O * I;
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  float* d = dst + (i / I) * ldw + (i % I);
-  float s = accumulate ? *d : 0.f;
+  const int64_t i = (int64_t)blockIdx.x * 64 + j;
   float t = 0.f;
-  for (int k = 0; k < S; ++k) t += part[(int64_t)k * n + i];
-  *d = s + t;
+  if (i < n) {
+#pragma unroll 8
+    for (int k = q; k < S; k += 4) t += part[(int64_t)k * n + i];
+  }
+  sh[threadIdx.x] = t;
+  __syncthreads();
+  if (q == 0 && i < n) {
+    const float t4 = ((sh[j] + sh[64 + j]) + sh[128 + j]) + sh[192 + j];
+    float* d = dst + (i / I) * ldw + (i % I);
+    const float s = accumulate ? *d : 0.f;
+    *d = s + t4;
+  }
 }
 
 struct VecSegs {
@@ -2227,12 +2311,21 @@ struct VecSegs {
   int n;
 };
 
-__global__ void vec_reduce_kernel(const float* __restrict__ vpart, int nwg, int nvec, VecSegs segs,
-                                  float* __restrict__ dparams, int accumulate) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= nvec) return;
+// The same four-way split of the slot sums as dw_reduce_kernel.
+__global__ __launch_bounds__(NT) void vec_reduce_kernel(const float* __restrict__ vpart, int nwg, int nvec,
+                                                        VecSegs segs, float* __restrict__ dparams, int accumulate) {
+  __shared__ float sh[NT];
+  const int j = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int i = blockIdx.x * 64 + j;
   float t = 0.f;
-  for (int w = 0; w < nwg; ++w) t += vpart[(int64_t)w * nvec + i];
+  if (i < nvec) {
+#pragma unroll 8
+    for (int w = q; w < nwg; w += 4) t += vpart[(int64_t)w * nvec + i];
+  }
+  sh[threadIdx.x] = t;
+  __syncthreads();
+  if (q != 0 || i >= nvec) return;
+  t = ((sh[j] + sh[64 + j]) + sh[128 + j]) + sh[192 + j];
   for (int k = 0; k < segs.n; ++k) {
     const VecSeg& sg = segs.s[k];
     if (i >= sg.vec_off && i < sg.vec_off + sg.len) {
@@ -2582,7 +2675,7 @@ hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st) {
 hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int ldw, int accumulate,
                             hipStream_t st) {
   const int64_t n = (int64_t)O * I;
-  hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)((n + NT - 1) / NT)), dim3(NT), 0, st, part, S, O, I, dst, ldw,
+  hipLaunchKernelGGL(dw_reduce_kernel, dim3((unsigned)((n + 63) / 64)), dim3(NT), 0, st, part, S, O, I, dst, ldw,
                      accumulate);
   return hipGetLastError();
 }
@@ -2592,7 +2685,7 @@ hipError_t launch_vec_reduce(const float* vpart, int nwg, int nvec, const VecSeg
   VecSegs s;
   s.n = nseg;
   for (int i = 0; i < nseg && i < 4; ++i) s.s[i] = segs[i];
-  hipLaunchKernelGGL(vec_reduce_kernel, dim3((nvec + NT - 1) / NT), dim3(NT), 0, st, vpart, nwg, nvec, s, dparams,
+  hipLaunchKernelGGL(vec_reduce_kernel, dim3((nvec + 63) / 64), dim3(NT), 0, st, vpart, nwg, nvec, s, dparams,
                      accumulate);
   return hipGetLastError();
 }
