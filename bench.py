@@ -30,27 +30,33 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic(timer: str, cfg, E: int, N: int):
-    """Algorithmic work of one launch of the kernel class `timer` for one
-    block: (bytes, flops).  Bytes count compulsory HBM traffic of a fused
-    kernel (each operand row once); flops count the MLP products in the
-    concatenated form of the model (2 flops per multiply-add)."""
+def algorithmic(timer: str, cfg, E: int, No: int, Nh: int):
+    """Compulsory work of one launch of the kernel class `timer` for one
+    block, as (HBM bytes, flops), for the bf16 row-split path the benchmark
+    workload takes (latent 64/128, depth 2): each operand row counted once,
+    gathered node rows once per node; flops are the MLP products (2 per
+    multiply-add).  E edges, No owned and Nh halo nodes."""
     l, D = cfg.latent, cfg.depth
-    s_e = 2 if cfg.precision == "bf16" else 4
-    mlp_edge = 2 * l * (3 * l) + 2 * l * l * (D - 1)          # per edge, forward
-    mlp_node = 2 * l * (2 * l) + 2 * l * l * (D - 1)          # per node, forward
-    if timer == "edge_fwd":
-        # read e^k, write e^{k+1}; node rows (owned + halo) and agg once
-        return E * (2 * l * s_e + 4) + N * l * 4 * 2, E * mlp_edge
+    if cfg.precision != "bf16" or D != 2 or l not in (64, 128):
+        return None
+    Nl = No + Nh
     if timer == "edge_bwd":
-        # read e^k and de^{k+1}, write de^k and the sender-side gradient; node rows
-        return E * (l * s_e + 3 * 4 * l + 4) + N * l * 4 * 3, 2 * E * mlp_edge
-    if timer == "node_fwd":
-        return N * l * 4 * 3, N * mlp_node
-    if timer == "node_bwd":
-        return N * l * 4 * 5, 2 * N * mlp_node
-    if timer == "sender_gather":
-        return E * (4 * l + 4) + N * l * 4 * 2, 0
+        # read e^k (bf16), de^{k+1} (fp32), receiver / sender ids, dagg rows,
+        # node projections; write de^k, dy, dz_0, h_1 (bf16) and the
+        # receiver sums of dz_0
+        by = E * (2 * l + 4 * l + 8 + 4 * l + 3 * 2 * l) + No * l * 4 * 2 + Nl * 2 * l * 4
+        return by, E * 4 * 2 * l * l
+    if timer == "edge_fwd":
+        # read e^k, ids, projections; write e^{k+1} and agg
+        by = E * (2 * l + 8 + 2 * l) + Nl * 2 * l * 4 + No * l * 4
+        return by, E * 2 * 2 * l * l
+    if timer == "node_proj":
+        return Nl * (2 * l + 2 * l * 4), Nl * 2 * l * 2 * l
+    if timer == "input_grad":
+        # dz_0 rows through the transposed CSR, receiver sums, dv (read and
+        # write), halo gradients, sender sums out
+        by = E * (2 * l + 4) + Nl * 4 + No * l * 4 * 3 + Nh * l * 4 + Nl * l * 4
+        return by, Nl * 2 * l * 2 * l
     return None
 
 
@@ -116,10 +122,12 @@ def main():
                 f"{t / n:8.4f} ms/launch")
 
     # dominant kernel and its roofline position
-    dom = max((k for k in timers if algorithmic(k, cfg, ne, no + nh) is not None and timers[k][1]),
-              key=lambda k: timers[k][0])
+    dom = max((k for k in timers if timers[k][1]), key=lambda k: timers[k][0])
     t_launch = timers[dom][0] / timers[dom][1] * 1e-3
-    by, fl = algorithmic(dom, cfg, ne, no + nh)
+    alg = algorithmic(dom, cfg, ne, no, nh)
+    if alg is None:
+        raise SystemExit(f"no algorithmic model for the dominant kernel class {dom}")
+    by, fl = alg
     peak_flops = PEAK["bf16"] if cfg.precision == "bf16" else PEAK["fp32"]
     intensity = fl / by if by else 0
     if intensity >= peak_flops / PEAK["hbm"]:

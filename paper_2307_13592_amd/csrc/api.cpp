@@ -674,7 +674,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
         e = launch_rows_bwd(m->prec, L, D, NODE_BLOCK, a, BWD_GRID, st);
       }
       CHK("node block");
-      e = run_vec(m, ml, d_params, accumulate, st);
+      e = run_vec(m, ml, d_params, accumulate, st, rows_bwd_grid(m->prec, L, D, NODE_BLOCK, BWD_GRID));
       CHK("node vec");
       DwArgs w{};
       w.delta = DEL_N[0];
@@ -815,7 +815,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
         e = launch_rows_bwd(m->prec, L, D, ENC_EDGE, a, BWD_GRID, st);
       }
       CHK("EncEdge");
-      e = run_vec(m, ml, d_params, accumulate, st);
+      e = run_vec(m, ml, d_params, accumulate, st, rows_bwd_grid(m->prec, L, D, ENC_EDGE, BWD_GRID));
       CHK("EncEdge vec");
       DwArgs w{};
       w.delta = DEL_E[0];

@@ -135,6 +135,8 @@ int64_t plan_chunks(int64_t n_owned);
 hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st);
 hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int grid, hipStream_t st);
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st);
+// Workgroups (= vector-partial slots) launch_rows_bwd uses when asked for `grid`.
+int rows_bwd_grid(int prec, int L, int D, int kind, int grid);
 hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int grid, hipStream_t st);
 // Workgroups (= vector-partial slots) the edge backward uses when asked for `grid`.
 int edge_bwd_grid(int prec, int L, int D, int grid);

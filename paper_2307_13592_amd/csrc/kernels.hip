@@ -1968,6 +1968,241 @@ __global__ __launch_bounds__(RS_NTH) void node_proj_kernel(const uint16_t* __res
   }
 }
 
+// acc[cb] = sum over k-groups of A[kg] x B[cb][kg] with the B fragments read
+// from the packed weights in memory (a layer too large to keep in LDS).
+template <int NB, int NKG>
+__device__ __forceinline__ void rs_gemm_g(const uint4 (&A)[NKG], const uint4* __restrict__ Bg, floatx4 (&acc)[NB],
+                                          int lane) {
+  // an opaque zero offset keeps the fragment loads inside the caller's loop
+  int z0 = 0;
+  asm volatile("" : "+v"(z0));
+  const uint4* B = Bg + z0;
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kg = 0; kg < NKG; ++kg) {
+    uint4 b[NB];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) b[cb] = B[(cb * NKG + kg) * 64 + lane];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) PBF16::mma(acc[cb], A[kg], b[cb]);
+  }
+}
+
+template <int L, int KIND>
+struct RsRowsLay {
+  static constexpr int NKH = L / 32, NB = L / 16;
+  static constexpr int W = NB * NKH * 64 * 16;               // one L x L packed layer
+  // W_last (fwd), W_last (bwd), then the first Linear: its backward packing
+  // for the node half (input 2L), its forward packing for the edge encoder
+  static constexpr int W1B = KIND == NODE_BLOCK ? 2 * W : NB * 64 * 16;
+  static constexpr int OFF_W1 = 2 * W;
+  static constexpr int OFF_SCR = OFF_W1 + W1B;
+  static constexpr int SCR = 16 * L * 2;
+  static constexpr int END = OFF_SCR + RS_NWV * SCR;
+  static constexpr int NVEC = 4 * L;
+  static_assert(RS_NWV * NVEC * 4 <= OFF_SCR, "partials reuse the weight area");
+};
+
+// Backward of the node half of a block (KIND NODE_BLOCK: input [v | agg],
+// residual v + LN(MLP)) or of the edge encoder (ENC_EDGE: input the edge
+// features), bf16, depth 2, with the forward recomputed per 16-row tile:
+// every wave works alone on its tiles as in the row-split edge kernels.
+// Same outputs as rows_bwd_kernel for these kinds.
+template <int L, int KIND>
+__global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
+  using Lay = RsRowsLay<L, KIND>;
+  constexpr int NKH = Lay::NKH, NB = Lay::NB, W = Lay::W;
+  constexpr int NK1 = KIND == NODE_BLOCK ? 2 * NKH : 1;  // k-groups of the first Linear
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* W2f = reinterpret_cast<uint4*>(lds);
+  uint4* W2b = reinterpret_cast<uint4*>(lds + W);
+  uint4* W1 = reinterpret_cast<uint4*>(lds + Lay::OFF_W1);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  uint16_t* scr = reinterpret_cast<uint16_t*>(lds + Lay::OFF_SCR + wave * Lay::SCR);
+  rs_copy_frags(W2f, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
+  rs_copy_frags(W2b, a.mlp.lin[1].wb, NB, NKH, NKH, 0);
+  if constexpr (KIND == NODE_BLOCK) rs_copy_frags(W1, a.mlp.lin[0].wb, 2 * NB, NKH, NKH, 0);
+  else rs_copy_frags(W1, a.mlp.lin[0].wf, NB, 1, 1, 0);
+  __syncthreads();
+  float pg[NB], pb[NB], pl[NB], ph[NB];  // column partials over this lane's rows
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) pg[cb] = pb[cb] = pl[cb] = ph[cb] = 0.f;
+  const int64_t ntiles = (a.rows + 15) / 16;
+  const int64_t nw = (int64_t)gridDim.x * RS_NWV;
+  for (int64_t t = (int64_t)blockIdx.x * RS_NWV + wave; t < ntiles; t += nw) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int arow = ln & 15, ach = ln >> 4;
+    const int64_t row0 = t * 16;
+    const int n = (int)(a.rows - row0 < 16 ? a.rows - row0 : 16);
+    // first-layer operands in fragment order (bf16 of the fp32 inputs)
+    uint4 xf[NK1];
+    if constexpr (KIND == NODE_BLOCK) {
+#pragma unroll
+      for (int kg = 0; kg < NK1; ++kg) {
+        const float* src = (kg < NKH ? a.in0 : a.in1) + (row0 + arow) * L + (kg % NKH) * 32 + ach * 8;
+        float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+        if (arow < n) {
+          x0 = reinterpret_cast<const float4*>(src)[0];
+          x1 = reinterpret_cast<const float4*>(src)[1];
+        }
+        uint16_t h[8] = {f2bf(x0.x), f2bf(x0.y), f2bf(x0.z), f2bf(x0.w), f2bf(x1.x), f2bf(x1.y), f2bf(x1.z), f2bf(x1.w)};
+        xf[kg] = *reinterpret_cast<const uint4*>(h);
+      }
+    } else {
+      uint16_t h[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = ach * 8 + j;
+        h[j] = f2bf((arow < n && k < a.fin) ? a.in0[(row0 + arow) * a.fin + k] : 0.f);
+      }
+      xf[0] = *reinterpret_cast<const uint4*>(h);
+    }
+    floatx4 z[NB];
+    if constexpr (KIND == NODE_BLOCK) rs_gemm_g<NB, NK1>(xf, a.mlp.lin[0].wf, z, ln);
+    else rs_gemm<NB, 1>(xf, W1, z, ln);
+    uint32_t mask = 0u;
+    float h[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float bv = a.mlp.lin[0].b[cb * 16 + (ln & 15)];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float v = z[cb][r] + bv;
+        const bool on = v > 0.f;
+        mask |= (on ? 1u : 0u) << (cb * 4 + r);
+        h[cb][r] = on ? v : 0.f;
+      }
+    }
+    uint4 hf[NKH];
+    rs_to_frags<L>(h, scr, hf, ln);
+    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.hid[0]) + row0 * L, scr, n, ln);
+    float y[NB][4];
+    {
+      floatx4 acc[NB];
+      rs_gemm<NB, NKH>(hf, W2f, acc, ln);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float bv = a.mlp.lin[1].b[cb * 16 + (ln & 15)];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[cb][r] = acc[cb][r] + bv;
+      }
+    }
+    float dm[NB][4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = (ln >> 4) * 4 + r;
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) dm[cb][r] = row < n ? a.dm[(row0 + row) * L + cb * 16 + (ln & 15)] : 0.f;
+    }
+    float mu[4], rs[4], t1[4], t2[4];
+    rs_row_totals<NB>(y, mu);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      mu[r] = mu[r] / L;
+      float x = 0.f;
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float d = y[cb][r] - mu[r];
+        x += d * d;
+      }
+      rs[r] = x;
+    }
+    rs_butterfly(rs);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      rs[r] = 1.0f / sqrtf(rs[r] / L + a.eps);
+      t1[r] = t2[r] = 0.f;
+    }
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        y[cb][r] = (y[cb][r] - mu[r]) * rs[r];
+        const float d = dm[cb][r] * g;
+        t1[r] += d;
+        t2[r] += d * y[cb][r];
+        pg[cb] += dm[cb][r] * y[cb][r];
+        pb[cb] += dm[cb][r];
+      }
+    }
+    rs_butterfly(t1);
+    rs_butterfly(t2);
+    float v[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[cb][r] = rs[r] * (dm[cb][r] * g - t1[r] / L - y[cb][r] * (t2[r] / L));
+        pl[cb] += v[cb][r];
+      }
+    }
+    uint4 gf[NKH];
+    rs_to_frags<L>(v, scr, gf, ln);
+    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[1]) + row0 * L, scr, n, ln);
+    {
+      floatx4 acc[NB];
+      rs_gemm<NB, NKH>(gf, W2b, acc, ln);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[cb][r] = ((mask >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
+          ph[cb] += v[cb][r];
+        }
+    }
+    rs_to_frags<L>(v, scr, gf, ln);
+    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[0]) + row0 * L, scr, n, ln);
+    if constexpr (KIND == NODE_BLOCK) {
+      // input gradients: dv = dm + dz W_1[:, v-block], dagg = dz W_1[:, agg-block]
+#pragma unroll
+      for (int pass = 0; pass < 2; ++pass) {
+        floatx4 acc[NB];
+        rs_gemm<NB, NKH>(gf, W1 + pass * NB * NKH * 64, acc, ln);
+        float* dst = pass == 0 ? a.dx0 : a.dx1;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = (ln >> 4) * 4 + r;
+          if (row < n) {
+#pragma unroll
+            for (int cb = 0; cb < NB; ++cb) {
+              const int64_t o = (row0 + row) * L + cb * 16 + (ln & 15);
+              dst[o] = pass == 0 ? acc[cb][r] + a.dm[o] : acc[cb][r];
+            }
+          }
+        }
+      }
+    }
+  }
+  // column partials: lane groups, then the waves in order through LDS
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(lds);
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) {
+    float q[4] = {ph[cb], pl[cb], pg[cb], pb[cb]};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      q[k] += __shfl_xor(q[k], 16, 64);
+      q[k] += __shfl_xor(q[k], 32, 64);
+    }
+    if (lane < 16) {
+      float* rw = red + wave * Lay::NVEC;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) rw[k * L + cb * 16 + lane] = q[k];
+    }
+  }
+  __syncthreads();
+  float* vp = a.vpart + (int64_t)blockIdx.x * a.nvec;
+  for (int i = threadIdx.x; i < Lay::NVEC; i += RS_NTH) {
+    float s = 0.f;
+    for (int w = 0; w < RS_NWV; ++w) s += red[w * Lay::NVEC + i];
+    vp[i] = s;
+  }
+}
+
 // --------------------------------------------------- node input gradient ---
 // Gradient reaching the nodes through the first Linear of a block's edge MLP.
 // Its sender and receiver column blocks W_s, W_r are shared by all edges, so
@@ -2554,7 +2789,25 @@ hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& 
   return hipErrorInvalidValue;
 }
 
+static bool rows_rs(int prec, int L, int D, int kind) {
+  return prec == BF16 && D == 2 && (L == 64 || L == 128) && (kind == NODE_BLOCK || kind == ENC_EDGE);
+}
+
+int rows_bwd_grid(int prec, int L, int D, int kind, int grid) { return rows_rs(prec, L, D, kind) ? RS_GRID : grid; }
+
+template <int L, int KIND>
+static hipError_t rows_bwd_rs_t(const RowsBwdArgs& a, hipStream_t st) {
+  using Lay = RsRowsLay<L, KIND>;
+  allow_lds(rows_bwd_rs_kernel<L, KIND>, Lay::END);
+  hipLaunchKernelGGL((rows_bwd_rs_kernel<L, KIND>), dim3(RS_GRID), dim3(RS_NTH), Lay::END, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st) {
+  if (rows_rs(prec, L, D, kind)) {
+    if (L == 64) return kind == NODE_BLOCK ? rows_bwd_rs_t<64, NODE_BLOCK>(a, st) : rows_bwd_rs_t<64, ENC_EDGE>(a, st);
+    return kind == NODE_BLOCK ? rows_bwd_rs_t<128, NODE_BLOCK>(a, st) : rows_bwd_rs_t<128, ENC_EDGE>(a, st);
+  }
 #define RB(PP, LL, DD)                                                                      \
   if (prec == PP && L == LL && D == DD) {                                                   \
     switch (kind) {                                                                         \
