@@ -139,8 +139,21 @@ mgn_status mgn_graph_validate(mgn_model* m, const mgn_graph* g, mgn_stream strea
 
 /* ---- the training step ---- */
 
-/* Device workspace mgn_forward/mgn_backward need for graph g (bytes): every
- * block's inputs are kept for the backward pass. */
+/* Edge-stream checkpointing (bf16 precision only).  interval 0 (the
+ * default) keeps every block's inputs for the backward pass.  interval s >= 1
+ * keeps the edge latents of blocks 0, s, 2s, ... only, and of the node stream
+ * only the bf16 copy: the backward pass recomputes each block's edge latents
+ * from the nearest checkpoint at or below it and the block's aggregate by
+ * one more edge forward, and runs the edge backward in receiver chunks of
+ * about chunk_edges edges (0: 8Mi).  Same computation (the weight-gradient
+ * sums over chunks add in another order); the workspace then holds
+ * ceil(K/s) + 1 edge-latent copies instead of K.  Takes effect for the next
+ * mgn_workspace_size / mgn_forward (a pending backward is dropped).
+ * MGN_E_UNSUPPORTED for fp32 models, MGN_E_ARG for negative arguments. */
+mgn_status mgn_set_recompute(mgn_model* m, int32_t interval, int64_t chunk_edges);
+
+/* Device workspace mgn_forward/mgn_backward need for graph g (bytes) under
+ * the model's checkpointing setting. */
 mgn_status mgn_workspace_size(const mgn_model* m, const mgn_graph* g, size_t* bytes);
 
 /* Forward pass (device pointers):
@@ -164,7 +177,8 @@ mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_params, int a
 /* Masked mean squared error (Algorithm 1: local squared error, mean over the
  * loss-masked nodes and outputs) and its gradient, device pointers:
  * out, target [n][d]; mask [n] (NULL = all rows); loss [2]: loss[0] = loss,
- * loss[1] = 2/(rows*d) (scratch); d_out [n][d]. */
+ * loss[1] = 2/(rows*d) (scratch); d_out [n][d] (also holds per-workgroup
+ * partial sums before the gradient overwrites it). */
 mgn_status mgn_mse_grad(const float* out, const float* target, const uint8_t* mask, int64_t n, int32_t d,
                         float* loss, float* d_out, mgn_stream stream);
 

@@ -21,7 +21,8 @@ STATUS_NAMES = ["MGN_OK", "MGN_E_ARG", "MGN_E_GRAPH", "MGN_E_STATE", "MGN_E_NOME
 
 # every symbol include/mgn.h declares
 EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mgn_set_params", "mgn_get_params",
-           "mgn_partition_slabs", "mgn_graph_sizes", "mgn_graph_build", "mgn_graph_validate", "mgn_workspace_size",
+           "mgn_partition_slabs", "mgn_graph_sizes", "mgn_graph_build", "mgn_graph_validate", "mgn_set_recompute",
+           "mgn_workspace_size",
            "mgn_forward", "mgn_backward", "mgn_mse_grad", "mgn_timing_enable", "mgn_timing_read"]
 TIMERS = ["encode", "edge_fwd", "node_fwd", "decode", "edge_bwd", "node_bwd", "input_grad", "weight_grad",
           "other", "node_proj"]
@@ -68,6 +69,7 @@ def lib() -> C.CDLL:
             "mgn_graph_sizes": (C.c_int, [vp, vp, i64, vp, i64, i32, vp]),
             "mgn_graph_build": (C.c_int, [vp, vp, i64, vp, i64, i32, vp, vp, vp, vp, vp, vp]),
             "mgn_graph_validate": (C.c_int, [vp, vp, vp]),
+            "mgn_set_recompute": (C.c_int, [vp, i32, i64]),
             "mgn_workspace_size": (C.c_int, [vp, vp, vp]),
             "mgn_forward": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]),
             "mgn_backward": (C.c_int, [vp, vp, vp, C.c_int, vp, vp]),
@@ -192,6 +194,10 @@ def graph_struct(dg: dict) -> mgn_graph:
 
 def mgn_graph_validate(model, graph: mgn_graph, stream=None) -> None:
     _check(lib().mgn_graph_validate(model, C.byref(graph), _stream(stream)), model)
+
+
+def mgn_set_recompute(model, interval: int, chunk_edges: int = 0) -> None:
+    _check(lib().mgn_set_recompute(model, int(interval), int(chunk_edges)), model)
 
 
 def mgn_workspace_size(model, graph: mgn_graph) -> int:

@@ -36,10 +36,17 @@ struct MlpL {
 };
 
 struct WsPlan {
-  size_t erecv, chunk, unit_r, nunits, V, V16, PROJ, AGG, ES, DV[2], DAGG, DZS, DE[2], DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
+  size_t erecv, chunk, unit_r, nunits, V, V16, PROJ, AGG, ES, DV[2], DAGG, DZS, DE, DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
       PART, VPART, total;
   int64_t max_units;
+  // edge-stream checkpointing: interval s (0: every block kept), checkpoints
+  bool lean = false;
+  int s = 0, nck = 0;
+  // receiver / edge boundaries of the backward's edge chunks
+  std::vector<int64_t> cr, ce;
 };
+
+constexpr int64_t LEAN_CHUNK_EDGES = 8 << 20;  // edges per backward chunk with checkpointing
 
 }  // namespace
 
@@ -53,9 +60,12 @@ struct mgn_model {
   uint4* packed = nullptr;
   size_t packed_n = 0;
   bool params_set = false;
-  // graph accepted by mgn_graph_validate
+  // graph accepted by mgn_graph_validate, and a host copy of its row_ptr
   bool graph_ok = false;
   mgn_graph vg{};
+  std::vector<int32_t> rp_host;
+  int ckpt = 0;                 // edge-stream checkpoint interval (0: keep every block)
+  int64_t chunk_edges = 0;      // edges per backward chunk with checkpointing (0: the default)
   // what the last forward used (kept for the backward)
   bool fwd_done = false;
   mgn_graph g{};
@@ -164,12 +174,37 @@ Mlp dev_mlp(const mgn_model* m, const MlpL& l) {
 
 size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 
+bool same_graph(const mgn_graph& a, const mgn_graph& b) {
+  return a.n_owned == b.n_owned && a.n_halo == b.n_halo && a.n_edges == b.n_edges && a.row_ptr == b.row_ptr &&
+         a.send == b.send && a.trow_ptr == b.trow_ptr && a.tedge == b.tedge;
+}
+
 WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   WsPlan p{};
-  const int64_t no = g->n_owned, ne = g->n_edges, L = m->L, K = m->K;
+  const int64_t no = g->n_owned, ne = g->n_edges, nl = no + g->n_halo, L = m->L, K = m->K;
   const size_t ts = tsize(m);
   const int te = edge_tile_rows(m->prec, m->L, m->D);
   p.max_units = plan_max_units(no, ne, 4 * te, 4 * te);
+  p.lean = m->ckpt > 0 && K > 0;
+  p.s = m->ckpt;
+  p.nck = p.lean ? (int)((K + p.s - 1) / p.s) : 0;
+  // backward edge chunks: one, or ~LEAN_CHUNK_EDGES edges each on planning-chunk receiver boundaries
+  p.cr = {0};
+  const int64_t che = m->chunk_edges > 0 ? m->chunk_edges : LEAN_CHUNK_EDGES;
+  const bool host_rp = (int64_t)m->rp_host.size() == no + 1 && same_graph(*g, m->vg);
+  if (p.lean && ne > che && host_rp) {
+    const int64_t nc = (ne + che - 1) / che, q = plan_chunk_receivers();
+    for (int64_t c = 1; c < nc; ++c) {
+      const int64_t target = ne * c / nc;
+      int64_t r = std::lower_bound(m->rp_host.begin(), m->rp_host.end(), (int32_t)target) - m->rp_host.begin();
+      r = r / q * q;
+      if (r > p.cr.back() && r < no) p.cr.push_back(r);
+    }
+  }
+  p.cr.push_back(no);
+  int64_t emax = 0;
+  for (int64_t r : p.cr) p.ce.push_back(r == no ? ne : (host_rp ? m->rp_host[r] : 0));
+  for (size_t c = 0; c + 1 < p.ce.size(); ++c) emax = std::max(emax, p.ce[c + 1] - p.ce[c]);
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t r = o;
@@ -180,21 +215,22 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.chunk = take(4 * (size_t)plan_chunks(no));
   p.unit_r = take(4 * (size_t)(p.max_units + 1));
   p.nunits = take(4);
-  p.V = take(4 * (size_t)(K + 1) * no * L);
+  // fp32 node stream: every block's input, or (checkpointing) two working rows
+  p.V = take(4 * (size_t)(p.lean ? 2 : K + 1) * no * L);
   // bf16 mode: bf16 copy of every block's node input, owned then halo rows
-  p.V16 = m->prec == BF16 ? take(2 * (size_t)(K + 1) * (no + g->n_halo) * L) : 0;
+  p.V16 = m->prec == BF16 ? take(2 * (size_t)(K + 1) * nl * L) : 0;
   // row-split edge kernels: node projections of the current block input
-  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(no + g->n_halo) * 2 * L) : 0;
-  p.AGG = take(4 * (size_t)K * no * L);
-  p.ES = take(ts * (size_t)std::max<int64_t>(K, 1) * ne * L);
+  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)nl * 2 * L) : 0;
+  p.AGG = take(4 * (size_t)(p.lean ? 1 : K) * no * L);
+  // edge stream: every block's input, or the checkpoints plus one working copy
+  p.ES = take(ts * (size_t)(p.lean ? p.nck + 1 : std::max<int64_t>(K, 1)) * ne * L);
   p.DV[0] = take(4 * (size_t)no * L);
   p.DV[1] = take(4 * (size_t)no * L);
   p.DAGG = take(4 * (size_t)no * L);
-  p.DZS = take(4 * (size_t)(no + g->n_halo) * L);
-  p.DE[0] = take(4 * (size_t)ne * L);
-  p.DE[1] = take(4 * (size_t)ne * L);
-  for (int j = 0; j < 3; ++j) p.DEL_E[j] = j < m->D ? take(ts * (size_t)ne * L) : 0;
-  for (int j = 0; j < 2; ++j) p.HID_E[j] = j < m->D - 1 ? take(ts * (size_t)ne * L) : 0;
+  p.DZS = take(4 * (size_t)nl * L);
+  p.DE = take(4 * (size_t)ne * L);  // dL/de, updated in place block by block
+  for (int j = 0; j < 3; ++j) p.DEL_E[j] = j < m->D ? take(ts * (size_t)emax * L) : 0;
+  for (int j = 0; j < 2; ++j) p.HID_E[j] = j < m->D - 1 ? take(ts * (size_t)emax * L) : 0;
   for (int j = 0; j < 3; ++j) p.DEL_N[j] = j < m->D ? take(ts * (size_t)no * std::max<int64_t>(L, 16)) : 0;
   for (int j = 0; j < 2; ++j) p.HID_N[j] = j < m->D - 1 ? take(ts * (size_t)no * L) : 0;
   // split-K partials: the largest S*O*I over all weight matrices
@@ -204,7 +240,7 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
     const MlpL& ml = m->mlp[i];
     // EncEdge (index 1) and the edge MLPs (even indices 2 .. nm-2) run over edges
     const bool edge_rows = i == 1 || (i >= 2 && i + 1 < nm && i % 2 == 0);
-    const int64_t R = edge_rows ? ne : no;
+    const int64_t R = edge_rows ? ne : nl;
     for (int j = 0; j < ml.depth; ++j) {
       const LinL& Ln = ml.lin[j];
       part = std::max(part, (size_t)dw_splits(R, Ln.out, Ln.in) * Ln.out * Ln.in);
@@ -218,10 +254,6 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   return p;
 }
 
-bool same_graph(const mgn_graph& a, const mgn_graph& b) {
-  return a.n_owned == b.n_owned && a.n_halo == b.n_halo && a.n_edges == b.n_edges && a.row_ptr == b.row_ptr &&
-         a.send == b.send && a.trow_ptr == b.trow_ptr && a.tedge == b.tedge;
-}
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
@@ -368,6 +400,18 @@ mgn_status mgn_graph_validate(mgn_model* m, const mgn_graph* g, mgn_stream strea
   if (s) return fail(m, s, err);
   m->vg = *g;
   m->graph_ok = true;
+  m->rp_host = std::move(rp);
+  return MGN_OK;
+}
+
+mgn_status mgn_set_recompute(mgn_model* m, int32_t interval, int64_t chunk_edges) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_set_recompute: model is NULL");
+  if (interval < 0 || chunk_edges < 0) return fail(m, MGN_E_ARG, "mgn_set_recompute: negative argument");
+  if (interval > 0 && m->prec != BF16)
+    return fail(m, MGN_E_UNSUPPORTED, "mgn_set_recompute: edge-stream checkpointing needs the bf16 precision");
+  m->ckpt = interval;
+  m->chunk_edges = chunk_edges;
+  m->fwd_done = false;  // the workspace plan changes
   return MGN_OK;
 }
 
@@ -380,6 +424,49 @@ mgn_status mgn_workspace_size(const mgn_model* cm, const mgn_graph* g, size_t* b
   *bytes = make_plan(m, g).total;
   return MGN_OK;
 }
+
+}  // extern "C"
+
+namespace {
+
+// The edge half of block k forward: node projections (row-split path), then
+// the fused edge kernel: e^{k+1} = e^k + m into eout (may equal ein, or be
+// null), ordered receiver sums into agg.
+hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p, char* ws, const float* halo, int k,
+                              float* v, void* v16, const void* ein, void* eout, float* agg, hipStream_t st) {
+  const int64_t no = g.n_owned, nh = g.n_halo;
+  const int L = m->L, D = m->D;
+  if (no == 0) return hipSuccess;
+  EdgeFwdArgs ea{};
+  ea.mlp = dev_mlp(m, m->edge(k));
+  ea.row_ptr = g.row_ptr;
+  ea.send = g.send;
+  ea.erecv = (int32_t*)(ws + p.erecv);
+  ea.unit_r = (int32_t*)(ws + p.unit_r);
+  ea.n_units = (int32_t*)(ws + p.nunits);
+  ea.V = v;
+  ea.H = nh > 0 ? halo + (size_t)k * nh * L : nullptr;
+  ea.V16 = v16;
+  ea.n_owned = no;
+  ea.Ein = ein;
+  ea.Eout = eout;
+  ea.agg = agg;
+  ea.eps = m->cfg.ln_eps;
+  const bool rs = edge_rs(m->prec, L, D);
+  ea.proj = rs ? (const float*)(ws + p.PROJ) : nullptr;
+  hipError_t e = hipSuccess;
+  if (rs) {
+    Timed t_(m, MGN_T_NODE_PROJ, st);
+    e = launch_node_proj(L, v16, no + nh, ea.mlp.lin[0], (float*)(ws + p.PROJ), st);
+    if (e != hipSuccess) return e;
+  }
+  Timed t_(m, MGN_T_EDGE_FWD, st);
+  return launch_edge_fwd(m->prec, L, D, ea, FWD_EDGE_GRID, st);
+}
+
+}  // namespace
+
+extern "C" {
 
 mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const float* ef, const float* halo,
                        float* out, void* workspace, size_t ws_bytes, mgn_stream stream) {
@@ -403,9 +490,12 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
   const int L = m->L, K = m->K, D = m->D;
   const size_t ts = tsize(m);
   const int te = edge_tile_rows(m->prec, L, D);
-  auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)k * no * L; };
-  auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)k * no * L; };
-  auto ES = [&](int k) { return (void*)(ws + p.ES + ts * (size_t)k * ne * L); };
+  auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)(p.lean ? (k & 1) : k) * no * L; };
+  auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)(p.lean ? 0 : k) * no * L; };
+  auto ES = [&](int k) -> void* {
+    const int slot = !p.lean ? k : (k % p.s == 0 ? k / p.s : p.nck);
+    return (void*)(ws + p.ES + ts * (size_t)slot * ne * L);
+  };
   const int64_t v16_stride = (no + nh) * L;  // elements per block of the bf16 node copy
   auto V16 = [&](int k) -> void* {
     return m->prec == BF16 ? (void*)((uint16_t*)(ws + p.V16) + (size_t)k * v16_stride) : nullptr;
@@ -455,33 +545,8 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
     if (e != hipSuccess) return hip_fail(m, e, "mgn_forward EncEdge");
   }
   for (int k = 0; k < K; ++k) {
-    EdgeFwdArgs ea{};
-    ea.mlp = dev_mlp(m, m->edge(k));
-    ea.row_ptr = g->row_ptr;
-    ea.send = g->send;
-    ea.erecv = erecv;
-    ea.unit_r = unit_r;
-    ea.n_units = n_units;
-    ea.V = V(k);
-    ea.H = nh > 0 ? halo + (size_t)k * nh * L : nullptr;
-    ea.V16 = V16(k);
-    ea.n_owned = no;
-    ea.Ein = ES(k);
-    ea.Eout = k + 1 < K ? ES(k + 1) : nullptr;
-    ea.agg = AGG(k);
-    ea.eps = m->cfg.ln_eps;
-    const bool rs = edge_rs(m->prec, L, D);
-    ea.proj = rs ? (const float*)(ws + p.PROJ) : nullptr;
-    if (no > 0) {
-      if (rs) {
-        Timed t_(m, MGN_T_NODE_PROJ, st);
-        e = launch_node_proj(L, V16(k), no + nh, ea.mlp.lin[0], (float*)(ws + p.PROJ), st);
-        if (e != hipSuccess) return hip_fail(m, e, "mgn_forward node projections");
-      }
-      Timed t_(m, MGN_T_EDGE_FWD, st);
-      e = launch_edge_fwd(m->prec, L, D, ea, FWD_EDGE_GRID, st);
-      if (e != hipSuccess) return hip_fail(m, e, "mgn_forward edge block");
-    }
+    e = edge_forward_block(m, *g, p, ws, halo, k, V(k), V16(k), ES(k), k + 1 < K ? ES(k + 1) : nullptr, AGG(k), st);
+    if (e != hipSuccess) return hip_fail(m, e, "mgn_forward edge block");
     RowsFwdArgs na{};
     na.mlp = dev_mlp(m, m->node(k));
     na.rows = no;
@@ -581,14 +646,17 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
   const int64_t no = g->n_owned, nh = g->n_halo, ne = g->n_edges;
   const int L = m->L, K = m->K, D = m->D;
   const size_t ts = tsize(m);
-  auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)k * no * L; };
-  auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)k * no * L; };
-  auto ES = [&](int k) { return (void*)(ws + p.ES + ts * (size_t)k * ne * L); };
+  auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)(p.lean ? (k & 1) : k) * no * L; };
+  auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)(p.lean ? 0 : k) * no * L; };
+  auto ES = [&](int k) -> void* {
+    const int slot = !p.lean ? k : (k % p.s == 0 ? k / p.s : p.nck);
+    return (void*)(ws + p.ES + ts * (size_t)slot * ne * L);
+  };
   auto V16 = [&](int k) -> void* {
     return m->prec == BF16 ? (void*)((uint16_t*)(ws + p.V16) + (size_t)k * (no + nh) * L) : nullptr;
   };
   float* DV[2] = {(float*)(ws + p.DV[0]), (float*)(ws + p.DV[1])};
-  float* DE[2] = {(float*)(ws + p.DE[0]), (float*)(ws + p.DE[1])};
+  float* DE = (float*)(ws + p.DE);
   float* DAGG = (float*)(ws + p.DAGG);
   float* DZS = (float*)(ws + p.DZS);
   float* VP = (float*)(ws + p.VPART);
@@ -614,7 +682,8 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
   void* HID_E[2] = {ws + p.HID_E[0], ws + p.HID_E[1]};
 
   // weight gradients of the hidden / last Linears from the stored activations
-  auto dw_hidden = [&](const MlpL& ml, int64_t R, void* const* del, void* const* hid, int ld_last) -> hipError_t {
+  auto dw_hidden = [&](const MlpL& ml, int64_t R, void* const* del, void* const* hid, int ld_last,
+                       int acc) -> hipError_t {
     for (int j = 1; j < D; ++j) {
       DwArgs a{};
       a.delta = del[j];
@@ -623,7 +692,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.a0 = hid[j - 1];
       a.lda0 = L;
       a.R = R;
-      hipError_t r = run_dw(m, ml.lin[j], a, d_params, accumulate, st);
+      hipError_t r = run_dw(m, ml.lin[j], a, d_params, acc, st);
       if (r != hipSuccess) return r;
     }
     return hipSuccess;
@@ -654,17 +723,30 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
     w.R = no;
     e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
     CHK("decoder dW");
-    e = dw_hidden(ml, no, DEL_N, HID_N, 16);
+    e = dw_hidden(ml, no, DEL_N, HID_N, 16, accumulate);
     CHK("decoder dW");
   }
   // ---- processor, last block first
+  const size_t nch = p.cr.size() - 1;  // edge chunks of the backward
   for (int k = K - 1; k >= 0; --k) {
     const int b_ = 1 - a_;
     const float* Hk = nh > 0 ? m->halo + (size_t)k * nh * L : nullptr;
+    if (p.lean) {
+      // e^k: the edge forwards of blocks b0 .. k-1 from the checkpoint e^{b0};
+      // then block k's forward once more for agg^k (and its projections)
+      const int b0 = k - k % p.s;
+      for (int j = b0; j < k; ++j) {
+        e = edge_forward_block(m, *g, p, ws, m->halo, j, V(j), V16(j), ES(j), ES(j + 1), AGG(0), st);
+        CHK("edge-stream recompute");
+      }
+      e = edge_forward_block(m, *g, p, ws, m->halo, k, V(k), V16(k), ES(k), nullptr, AGG(0), st);
+      CHK("aggregate recompute");
+    }
     {
       const MlpL& ml = m->node(k);
       RowsBwdArgs a = rows_args(ml, no, DEL_N, HID_N);
-      a.in0 = V(k);
+      a.in0 = p.lean ? nullptr : V(k);
+      a.in0_16 = p.lean ? V16(k) : nullptr;  // the bf16 copy is the product operand either way
       a.in1 = AGG(k);
       a.dm = DV[a_];
       a.dx0 = DV[b_];
@@ -679,13 +761,18 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       DwArgs w{};
       w.delta = DEL_N[0];
       w.ldd = L;
-      w.a_kind = 3;
-      w.a0 = V(k);
+      if (p.lean) {
+        w.a_kind = 5;
+        w.a3 = V16(k);
+      } else {
+        w.a_kind = 3;
+        w.a0 = V(k);
+      }
       w.a1 = AGG(k);
       w.R = no;
       e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
       CHK("node dW");
-      e = dw_hidden(ml, no, DEL_N, HID_N, L);
+      e = dw_hidden(ml, no, DEL_N, HID_N, L, accumulate);
       CHK("node dW");
     }
     {
@@ -702,13 +789,13 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.V16 = V16(k);
       a.n_owned = no;
       a.Ein = ES(k);
-      a.de_next = (k == K - 1) ? nullptr : DE[a_];
+      a.de_next = (k == K - 1) ? nullptr : DE;  // dL/de is updated in place
       a.dagg = DAGG;
-      a.de_out = DE[b_];
+      a.de_out = DE;
       a.de_std = k == 0;  // block 0's dL/de^0 feeds the edge encoder's backward
       const bool rs = edge_rs(m->prec, L, D);
       a.proj = rs ? (const float*)(ws + p.PROJ) : nullptr;
-      if (rs && no > 0) {
+      if (rs && no > 0 && !p.lean) {  // (the aggregate recompute made them already)
         Timed t_(m, MGN_T_NODE_PROJ, st);
         e = launch_node_proj(L, V16(k), no + nh, a.mlp.lin[0], (float*)(ws + p.PROJ), st);
         CHK("node projections");
@@ -718,15 +805,39 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.vpart = VP;
       a.nvec = ml.nvec;
       a.eps = m->cfg.ln_eps;
-      {
-        Timed t_(m, MGN_T_EDGE_BWD, st);
-        e = launch_edge_bwd(m->prec, L, D, a, BWD_GRID, st);
+      for (size_t c = 0; c < nch; ++c) {
+        // one receiver chunk: its per-edge gradients are stored from edge ce[c]
+        const int acc = accumulate || c > 0;
+        const int64_t e0 = p.ce[c], rows = p.ce[c + 1] - p.ce[c];
+        a.r_lo = p.cr[c];
+        a.r_hi = p.cr[c + 1];
+        a.e_base = e0;
+        {
+          Timed t_(m, MGN_T_EDGE_BWD, st);
+          e = launch_edge_bwd(m->prec, L, D, a, BWD_GRID, st);
+        }
+        CHK("edge block");
+        e = run_vec(m, ml, d_params, acc, st, edge_bwd_grid(m->prec, L, D, BWD_GRID));
+        CHK("edge vec");
+        e = dw_hidden(ml, rows, DEL_E, HID_E, L, acc);
+        CHK("edge dW");
+        // first Linear's weight gradient, e block: e rows of the chunk
+        DwArgs w{};
+        w.delta = DEL_E[0];
+        w.ldd = L;
+        w.a_kind = 0;
+        w.a0 = (const char*)ES(k) + ts * (size_t)e0 * L;
+        w.lda0 = L;
+        w.R = rows;
+        e = run_dw(m, ml.lin[0], w, d_params, acc, st, 0, L);
+        CHK("edge dW (e block)");
+        if (nch > 1) {
+          Timed t_(m, MGN_T_INPUT_GRAD, st);
+          e = launch_sender_sums(m->prec, L, g->trow_ptr, g->tedge, DEL_E[0], e0, e0 + rows, no + nh, DZS, c == 0,
+                                 st);
+          CHK("sender sums");
+        }
       }
-      CHK("edge block");
-      e = run_vec(m, ml, d_params, accumulate, st, edge_bwd_grid(m->prec, L, D, BWD_GRID));
-      CHK("edge vec");
-      e = dw_hidden(ml, ne, DEL_E, HID_E, L);
-      CHK("edge dW");
       InGradArgs ig{};
       ig.w1 = a.mlp.lin[0];
       ig.trow = g->trow_ptr;
@@ -736,6 +847,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       ig.dv = DV[b_];
       ig.dh = d_halo ? d_halo + (size_t)k * nh * L : nullptr;
       ig.dzs = DZS;
+      ig.dzs_ready = nch > 1;
       ig.n_local = no + nh;
       ig.n_owned = no;
       {
@@ -743,18 +855,9 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
         e = launch_input_grad(m->prec, L, ig, st);
       }
       CHK("node input gradient");
-      // first Linear's weight gradient by input block: e rows per edge; the
-      // sender / receiver blocks as sums over nodes of (per-node sum of dz_0)
-      // times the node's v (the same sums, reassociated)
-      DwArgs w{};
-      w.delta = DEL_E[0];
-      w.ldd = L;
-      w.a_kind = 0;
-      w.a0 = ES(k);
-      w.lda0 = L;
-      w.R = ne;
-      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st, 0, L);
-      CHK("edge dW (e block)");
+      // the first Linear's sender / receiver weight-gradient blocks as sums
+      // over nodes of (per-node sum of dz_0) times the node's v (the same
+      // sums as over edges, reassociated)
       for (int side = 0; side < 2; ++side) {  // sender block, then receiver block
         DwArgs wn{};
         wn.delta = side == 0 ? (const void*)DZS : (const void*)DAGG;
@@ -800,34 +903,39 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
     w.R = no;
     e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
     CHK("EncNode dW");
-    e = dw_hidden(ml, no, DEL_N, HID_N, L);
+    e = dw_hidden(ml, no, DEL_N, HID_N, L, accumulate);
     CHK("EncNode dW");
   }
   {
     const MlpL& ml = m->enc_edge();
     if (K > 0 && ne > 0) {
-      RowsBwdArgs a = rows_args(ml, ne, DEL_E, HID_E);
-      a.in0 = m->ef;
-      a.fin = m->cfg.edge_in;
-      a.dm = DE[a_];  // block 0 wrote dL/de^0 into DE[b_], and b_ became a_
-      {
-        Timed t_(m, MGN_T_NODE_BWD, st);
-        e = launch_rows_bwd(m->prec, L, D, ENC_EDGE, a, BWD_GRID, st);
+      // over the same edge chunks as the blocks (per-edge gradients stored per chunk)
+      for (size_t c = 0; c < nch; ++c) {
+        const int acc = accumulate || c > 0;
+        const int64_t e0 = p.ce[c], rows = p.ce[c + 1] - p.ce[c];
+        RowsBwdArgs a = rows_args(ml, rows, DEL_E, HID_E);
+        a.in0 = m->ef + (size_t)e0 * m->cfg.edge_in;
+        a.fin = m->cfg.edge_in;
+        a.dm = DE + (size_t)e0 * L;  // dL/de^0 (block 0 wrote it in plain column order)
+        {
+          Timed t_(m, MGN_T_NODE_BWD, st);
+          e = launch_rows_bwd(m->prec, L, D, ENC_EDGE, a, BWD_GRID, st);
+        }
+        CHK("EncEdge");
+        e = run_vec(m, ml, d_params, acc, st, rows_bwd_grid(m->prec, L, D, ENC_EDGE, BWD_GRID));
+        CHK("EncEdge vec");
+        DwArgs w{};
+        w.delta = DEL_E[0];
+        w.ldd = L;
+        w.a_kind = 1;
+        w.a0 = a.in0;
+        w.lda0 = m->cfg.edge_in;
+        w.R = rows;
+        e = run_dw(m, ml.lin[0], w, d_params, acc, st);
+        CHK("EncEdge dW");
+        e = dw_hidden(ml, rows, DEL_E, HID_E, L, acc);
+        CHK("EncEdge dW");
       }
-      CHK("EncEdge");
-      e = run_vec(m, ml, d_params, accumulate, st, rows_bwd_grid(m->prec, L, D, ENC_EDGE, BWD_GRID));
-      CHK("EncEdge vec");
-      DwArgs w{};
-      w.delta = DEL_E[0];
-      w.ldd = L;
-      w.a_kind = 1;
-      w.a0 = m->ef;
-      w.lda0 = m->cfg.edge_in;
-      w.R = ne;
-      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
-      CHK("EncEdge dW");
-      e = dw_hidden(ml, ne, DEL_E, HID_E, L);
-      CHK("EncEdge dW");
     } else if (!accumulate) {
       // no edges reach the output: the edge encoder's gradient is zero
       const int64_t b = ml.lin[0].w;

@@ -194,11 +194,11 @@ __device__ __forceinline__ int acc_col() { return threadIdx.x & 15; }
 // b%8-th contiguous eighth of the tiles and neighbouring tiles share an L2.
 struct TileIter {
   int t, end, stride;
-  __device__ TileIter(int ntiles) {
+  __device__ TileIter(int ntiles, int first = 0) {
     const int x = blockIdx.x & 7, q = blockIdx.x >> 3, nq = gridDim.x >> 3;
     const int lo = (int)(((int64_t)ntiles * x) >> 3), hi = (int)(((int64_t)ntiles * (x + 1)) >> 3);
-    t = lo + q;
-    end = hi;
+    t = first + lo + q;
+    end = first + hi;
     stride = nq;
   }
   __device__ bool valid() const { return t < end; }

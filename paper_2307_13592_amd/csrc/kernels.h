@@ -48,6 +48,7 @@ struct RowsBwdArgs {
   int fin, fout;
   const float* in0;
   const float* in1;
+  const void* in0_16;  // NODE / DEC: bf16 rows [rows][L] read instead of in0 when set
   const float* dm;   // gradient w.r.t. the MLP output (LN output; dOut for the decoder)
   float* dx0;        // NODE: dv^k owned part (= dm + dX_v); DEC: dv^K
   float* dx1;        // NODE: d agg
@@ -75,6 +76,8 @@ struct EdgeBwdArgs {
   float* dagg;          // [n_owned][L]: dL/dagg in; each receiver's sum of dz_0 out
   float* de_out;        // dL/de^k [E][L]
   const float* proj;    // node projections [n_local][2L] (row-split kernels), else unused
+  int64_t r_lo, r_hi;   // receiver range of this launch (a multiple of the planning chunk apart)
+  int64_t e_base;       // first edge of the range: delta / hid rows are stored from it
   void* delta[3];
   void* hid[2];
   float* vpart;
@@ -90,7 +93,8 @@ struct InGradArgs {
   const float* dzr;     // per-receiver sums of dz_0 [n_owned][L]
   float* dv;            // [n_owned][L], accumulated into
   float* dh;            // [n_halo][L] or null
-  float* dzs;           // out: per-sender sums of dz_0 [n_local][L]
+  float* dzs;           // per-sender sums of dz_0 [n_local][L]: written here, or read when dzs_ready
+  int dzs_ready;
   int64_t n_local, n_owned;
 };
 
@@ -100,7 +104,8 @@ struct DwArgs {
   int ldd;
   int O, I;
   int a_kind;         // 0 dense storage type, 1 dense fp32, 2 edge concat, 3 node concat,
-                      // 4 node rows fp32 (owned rows a0, halo rows a2; row stride lda0)
+                      // 4 node rows fp32 (owned rows a0, halo rows a2; row stride lda0),
+                      // 5 node concat with the v part in bf16 (a3) and agg fp32 (a1)
   const void* a0;     // dense source / e^k / v
   int lda0;
   const float* a1;    // node concat: agg; edge concat: V (owned)
@@ -131,6 +136,8 @@ hipError_t launch_plan(const int32_t* row_ptr, int64_t n_owned, int te_target, i
                        int32_t* unit_r, int32_t* n_units, hipStream_t st);
 int64_t plan_max_units(int64_t n_owned, int64_t n_edges, int te_target, int r_max);
 int64_t plan_chunks(int64_t n_owned);
+// Receivers per planning chunk: work units never cross a multiple of it.
+int plan_chunk_receivers();
 
 hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st);
 hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int grid, hipStream_t st);
@@ -145,6 +152,10 @@ int edge_bwd_grid(int prec, int L, int D, int grid);
 bool edge_rs(int prec, int L, int D);
 hipError_t launch_node_proj(int L, const void* v16, int64_t n_local, const Lin& w1, float* proj, hipStream_t st);
 hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t st);
+// Per-sender sums of dz_0 over the edges [e_lo, e_hi) (dz rows stored from e_lo),
+// assigned (first) or added into dzs.
+hipError_t launch_sender_sums(int prec, int L, const int32_t* trow, const int32_t* tedge, const void* dz, int64_t e_lo,
+                              int64_t e_hi, int64_t n_local, float* dzs, int first, hipStream_t st);
 hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st);
 hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int ldw, int accumulate,
                             hipStream_t st);

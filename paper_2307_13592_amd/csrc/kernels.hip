@@ -500,7 +500,8 @@ struct RowTM {
 // Stages the first Linear's input rows into LDS X (zero rows past `n`).
 template <class P, int KIND, int L, int TM, int LDX>
 __device__ __forceinline__ void stage_rows(typename P::T* X, const float* __restrict__ in0,
-                                           const float* __restrict__ in1, int fin, int64_t row0, int n) {
+                                           const float* __restrict__ in1, int fin, int64_t row0, int n,
+                                           const uint16_t* __restrict__ in0_16 = nullptr) {
   using S = RowShape<KIND, L>;
   if constexpr (KIND == ENC_NODE || KIND == ENC_EDGE) {
     for (int i = threadIdx.x; i < TM * S::KIN; i += NT) {
@@ -517,7 +518,15 @@ __device__ __forceinline__ void stage_rows(typename P::T* X, const float* __rest
     for (int j = 0; j < IT; ++j) {
       const int i = threadIdx.x + j * NT, r = i / (Q * NSRC), rem = i % (Q * NSRC), s = rem / Q, c4 = rem % Q;
       v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (i < TM * Q * NSRC && r < n) v[j] = reinterpret_cast<const float4*>((s == 0 ? in0 : in1) + (row0 + r) * L)[c4];
+      if (i < TM * Q * NSRC && r < n) {
+        if (s == 0 && in0_16) {  // bf16 copy of the node rows (exact in the bf16 operand type)
+          const uint2 w = reinterpret_cast<const uint2*>(in0_16 + (row0 + r) * L)[c4];
+          v[j] = make_float4(bf2f((uint16_t)w.x), bf2f((uint16_t)(w.x >> 16)), bf2f((uint16_t)w.y),
+                             bf2f((uint16_t)(w.y >> 16)));
+        } else {
+          v[j] = reinterpret_cast<const float4*>((s == 0 ? in0 : in1) + (row0 + r) * L)[c4];
+        }
+      }
     }
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
@@ -665,7 +674,8 @@ __global__ __launch_bounds__(NT) void rows_bwd_kernel(RowsBwdArgs a) {
   for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int64_t row0 = tile * TM;
     const int n = (int)(a.rows - row0 < TM ? a.rows - row0 : TM);
-    stage_rows<P, KIND, L, TM, Lay::LDX>(X, a.in0, a.in1, a.fin, row0, n);
+    stage_rows<P, KIND, L, TM, Lay::LDX>(X, a.in0, a.in1, a.fin, row0, n,
+                                         reinterpret_cast<const uint16_t*>(a.in0_16));
     // incoming gradient (zero rows past n; decoder: dOut padded to 16 columns)
     for (int i = tid; i < TM * S::NOUT; i += NT) {
       const int r = i / S::NOUT, c = i % S::NOUT;
@@ -1136,7 +1146,23 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void ed
 #pragma unroll
   for (int n = 0; n < NBW; ++n) pg[n] = pb[n] = pl[n] = ph[0][n] = ph[1][n] = 0.f;
 
-  for (TileIter it(*a.n_units); it.valid(); it.next()) {
+  // the work units of the receiver range [r_lo, r_hi) (unit boundaries fall on it)
+  int u_lo, u_hi;
+  {
+    const int nu = *a.n_units;
+    auto lower = [&](int64_t r) {
+      int lo = 0, hi = nu;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (a.unit_r[mid] < r) lo = mid + 1;
+        else hi = mid;
+      }
+      return lo;
+    };
+    u_lo = lower(a.r_lo);
+    u_hi = lower(a.r_hi);
+  }
+  for (TileIter it(u_hi - u_lo, u_lo); it.valid(); it.next()) {
     const int64_t r0 = a.unit_r[it.t], r1 = a.unit_r[it.t + 1];
     const int64_t e0 = a.row_ptr[r0], e1 = a.row_ptr[r1];
     zero_empty_receivers(a.row_ptr, r0, r1, a.dagg, L);
@@ -1224,9 +1250,9 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void ed
           }
         }
       __syncthreads();
-      store_rows(reinterpret_cast<T*>(a.delta[D - 1]) + sb * L, A, Lay::LDA, n, L);
-      store_rows(reinterpret_cast<T*>(a.hid[0]) + sb * L, HB, Lay::LDH, n, L);
-      if constexpr (D == 3) store_rows(reinterpret_cast<T*>(a.hid[1]) + sb * L, HC, Lay::LDH, n, L);
+      store_rows(reinterpret_cast<T*>(a.delta[D - 1]) + (sb - a.e_base) * L, A, Lay::LDA, n, L);
+      store_rows(reinterpret_cast<T*>(a.hid[0]) + (sb - a.e_base) * L, HB, Lay::LDH, n, L);
+      if constexpr (D == 3) store_rows(reinterpret_cast<T*>(a.hid[1]) + (sb - a.e_base) * L, HC, Lay::LDH, n, L);
       // hidden layers: dz_{j-1} = (dz_j W_j) * [h_{j-1} > 0], into A column block D-j
 #pragma unroll
       for (int j = D - 1; j >= 1; --j) {
@@ -1247,7 +1273,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void ed
               dout[row * Lay::LDA + col] = P::cvt(v);
             }
         __syncthreads();
-        store_rows(reinterpret_cast<T*>(a.delta[j - 1]) + sb * L, dout, Lay::LDA, n, L);
+        store_rows(reinterpret_cast<T*>(a.delta[j - 1]) + (sb - a.e_base) * L, dout, Lay::LDA, n, L);
       }
       // edge-stream gradient: de^k = de^{k+1} + dz_0 W_1[:, e-block]
       const T* dz0 = A + (D - 1) * L;
@@ -1377,16 +1403,17 @@ __device__ __forceinline__ void rs_copy_frags(uint4* dst, const uint4* __restric
   }
 }
 
-// Receiver range of wave w (of W waves in total): receiver-aligned, about
-// E / W edges each; the waves of one XCD (blockIdx % 8) get neighbouring ranges.
-__device__ __forceinline__ void rs_range(const int32_t* __restrict__ row_ptr, int64_t n_owned, int64_t& r0,
+// Receiver range of wave w (of W waves in total) within [lo_r, hi_r):
+// receiver-aligned, about E / W edges each; the waves of one XCD
+// (blockIdx % 8) get neighbouring ranges.
+__device__ __forceinline__ void rs_range(const int32_t* __restrict__ row_ptr, int64_t lo_r, int64_t hi_r, int64_t& r0,
                                          int64_t& r1) {
   const int G = gridDim.x, b = blockIdx.x, nwv = blockDim.x >> 6, wave = threadIdx.x >> 6;
   const int64_t W = (int64_t)G * nwv;
   const int64_t q = ((int64_t)(b & 7) * (G >> 3) + (b >> 3)) * nwv + wave;
-  const int64_t E = row_ptr[n_owned];
-  auto find = [&](int64_t target) {  // first receiver r with row_ptr[r] >= target
-    int64_t lo = 0, hi = n_owned;
+  const int64_t e0 = row_ptr[lo_r], E = row_ptr[hi_r] - e0;
+  auto find = [&](int64_t target) {  // first receiver r >= lo_r with row_ptr[r] >= target
+    int64_t lo = lo_r, hi = hi_r;
     while (lo < hi) {
       const int64_t mid = (lo + hi) >> 1;
       if (row_ptr[mid] >= target) hi = mid;
@@ -1394,8 +1421,8 @@ __device__ __forceinline__ void rs_range(const int32_t* __restrict__ row_ptr, in
     }
     return lo;
   };
-  r0 = q == 0 ? 0 : find(E * q / W);
-  r1 = q + 1 == W ? n_owned : find(E * (q + 1) / W);
+  r0 = q == 0 ? lo_r : find(e0 + E * q / W);
+  r1 = q + 1 == W ? hi_r : find(e0 + E * (q + 1) / W);
 }
 
 // Zeroes the rows (width L) of the receivers in [r0, r1) without edges (one
@@ -1542,7 +1569,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_fwd_rs_kernel(EdgeFwdArgs a) {
   rs_copy_frags(WL, a.mlp.lin[D - 1].wf, NB, NKH, NKH, 0);
   __syncthreads();
   int64_t r0, r1;
-  rs_range(a.row_ptr, a.n_owned, r0, r1);
+  rs_range(a.row_ptr, 0, a.n_owned, r0, r1);
   rs_zero_empty(a.row_ptr, r0, r1, a.agg, L);
   const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
@@ -1697,13 +1724,31 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
   rs_copy_frags(W1b, a.mlp.lin[0].wb, NB, NKH, NKH, 0);  // e block: the first NB column blocks
   __syncthreads();
   int64_t r0, r1;
-  rs_range(a.row_ptr, a.n_owned, r0, r1);
+  rs_range(a.row_ptr, a.r_lo, a.r_hi, r0, r1);
   rs_zero_empty(a.row_ptr, r0, r1, a.dagg, L);
   const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
-  float pg[NB], pb[NB], pl[NB], ph[2][NB];  // column partials over this lane's rows
+  // column sums of the bias / LayerNorm gradients: each tile's 16-row sums
+  // (butterfly over the four row groups) are added here; lane group g keeps
+  // the column blocks g * NB/4 ..
+  constexpr int NQ = 2 + D;  // gamma, beta, last bias, hidden biases
+  constexpr int NG = NB / 4;
+  float qacc[NQ][NG];
 #pragma unroll
-  for (int cb = 0; cb < NB; ++cb) pg[cb] = pb[cb] = pl[cb] = ph[0][cb] = ph[1][cb] = 0.f;
+  for (int q = 0; q < NQ; ++q)
+#pragma unroll
+    for (int j = 0; j < NG; ++j) qacc[q][j] = 0.f;
+  auto fold = [&](int q, float (&t)[NB], int grp) {
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      float x = t[cb];
+      x += __shfl_xor(x, 16, 64);
+      x += __shfl_xor(x, 32, 64);
+#pragma unroll
+      for (int j = 0; j < NG; ++j)
+        if (cb == grp * NG + j) qacc[q][j] += x;
+    }
+  };
   float run[(L + 63) / 64] = {};
   RsMetaRaw nxt = rs_meta_load(a.erecv, a.send, E0, E1);
   for (int64_t sb = E0; sb < E1; sb += 16) {
@@ -1734,7 +1779,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
       }
     uint4 hf[NKH];
     rs_to_frags<L>(h, scr, hf, ln);
-    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.hid[0]) + sb * L, scr, n, ln);
+    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.hid[0]) + (sb - a.e_base) * L, scr, n, ln);
     if constexpr (D == 3) {
       floatx4 acc[NB];
       rs_gemm<NB, NKH>(hf, WHf, acc, ln);
@@ -1750,7 +1795,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
         }
       }
       rs_to_frags<L>(h, scr, hf, ln);
-      rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.hid[1]) + sb * L, scr, n, ln);
+      rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.hid[1]) + (sb - a.e_base) * L, scr, n, ln);
     }
     float y[NB][4];
     {
@@ -1800,35 +1845,46 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
     // LayerNorm backward: dy = rstd (dm g - mean(dm g) - xhat mean(dm g xhat))
 #pragma unroll
     for (int r = 0; r < 4; ++r) t1[r] = t2[r] = 0.f;
+    {
+      float tg[NB], tb[NB];
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-      const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+      for (int cb = 0; cb < NB; ++cb) {
+        const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+        tg[cb] = tb[cb] = 0.f;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        y[cb][r] = (y[cb][r] - mu[r]) * rs[r];
-        const float d = dm[cb][r] * g;
-        t1[r] += d;
-        t2[r] += d * y[cb][r];
-        pg[cb] += dm[cb][r] * y[cb][r];
-        pb[cb] += dm[cb][r];
+        for (int r = 0; r < 4; ++r) {
+          y[cb][r] = (y[cb][r] - mu[r]) * rs[r];
+          const float d = dm[cb][r] * g;
+          t1[r] += d;
+          t2[r] += d * y[cb][r];
+          tg[cb] += dm[cb][r] * y[cb][r];
+          tb[cb] += dm[cb][r];
+        }
       }
+      fold(0, tg, ln >> 4);
+      fold(1, tb, ln >> 4);
     }
     rs_butterfly(t1);
     rs_butterfly(t2);
     float v[NB][4];
+    {
+      float tl[NB];
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-      const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+      for (int cb = 0; cb < NB; ++cb) {
+        const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+        tl[cb] = 0.f;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float d = dm[cb][r] * g;
-        v[cb][r] = rs[r] * (d - t1[r] / L - y[cb][r] * (t2[r] / L));
-        pl[cb] += v[cb][r];
+        for (int r = 0; r < 4; ++r) {
+          const float d = dm[cb][r] * g;
+          v[cb][r] = rs[r] * (d - t1[r] / L - y[cb][r] * (t2[r] / L));
+          tl[cb] += v[cb][r];
+        }
       }
+      fold(2, tl, ln >> 4);
     }
     uint4 gf[NKH];
     rs_to_frags<L>(v, scr, gf, ln);
-    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + sb * L, scr, n, ln);
+    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + (sb - a.e_base) * L, scr, n, ln);
     // hidden layers: dz_{j-1} = (dz_j W_j) * [z_{j-1} > 0]
 #pragma unroll
     for (int j = D - 1; j >= 1; --j) {
@@ -1838,15 +1894,21 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
       } else {
         if constexpr (D == 3) rs_gemm<NB, NKH>(gf, WHb, acc, ln);
       }
+      {
+        float th[NB];
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb)
+        for (int cb = 0; cb < NB; ++cb) {
+          th[cb] = 0.f;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          v[cb][r] = ((mask[j - 1] >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
-          ph[j - 1][cb] += v[cb][r];
+          for (int r = 0; r < 4; ++r) {
+            v[cb][r] = ((mask[j - 1] >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
+            th[cb] += v[cb][r];
+          }
         }
+        fold(3 + (j - 1), th, ln >> 4);
+      }
       rs_to_frags<L>(v, scr, gf, ln);
-      rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + sb * L, scr, n, ln);
+      rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + (sb - a.e_base) * L, scr, n, ln);
     }
     // edge-stream gradient: de^k = de^{k+1} + dz_0 W_1[:, e-block]
     {
@@ -1897,22 +1959,16 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
   // in order through LDS (the weight area is free now)
   __syncthreads();
   float* red = reinterpret_cast<float*>(lds);
+  {
+    float* rw = red + wave * Lay::NVEC;
 #pragma unroll
-  for (int cb = 0; cb < NB; ++cb) {
-    float q[5] = {ph[0][cb], ph[1][cb], pl[cb], pg[cb], pb[cb]};
+    for (int j = 0; j < NG; ++j) {
+      const int col = ((lane >> 4) * NG + j) * 16 + (lane & 15);
 #pragma unroll
-    for (int k = 0; k < 5; ++k) {
-      q[k] += __shfl_xor(q[k], 16, 64);
-      q[k] += __shfl_xor(q[k], 32, 64);
-    }
-    if (lane < 16) {
-      const int col = cb * 16 + lane;
-      float* rw = red + wave * Lay::NVEC;
-#pragma unroll
-      for (int j = 0; j < D - 1; ++j) rw[j * L + col] = q[j];
-      rw[(D - 1) * L + col] = q[2];
-      rw[D * L + col] = q[3];
-      rw[(D + 1) * L + col] = q[4];
+      for (int h = 0; h < D - 1; ++h) rw[h * L + col] = qacc[3 + h][j];
+      rw[(D - 1) * L + col] = qacc[2][j];
+      rw[D * L + col] = qacc[0][j];
+      rw[(D + 1) * L + col] = qacc[1][j];
     }
   }
   __syncthreads();
@@ -2025,9 +2081,25 @@ __global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
   if constexpr (KIND == NODE_BLOCK) rs_copy_frags(W1, a.mlp.lin[0].wb, 2 * NB, NKH, NKH, 0);
   else rs_copy_frags(W1, a.mlp.lin[0].wf, NB, 1, 1, 0);
   __syncthreads();
-  float pg[NB], pb[NB], pl[NB], ph[NB];  // column partials over this lane's rows
+  // column sums of the bias / LayerNorm gradients, folded per tile as in
+  // edge_bwd_rs_kernel: hidden bias, last bias, gamma, beta
+  constexpr int NG = NB / 4;
+  float qacc[4][NG];
 #pragma unroll
-  for (int cb = 0; cb < NB; ++cb) pg[cb] = pb[cb] = pl[cb] = ph[cb] = 0.f;
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int j = 0; j < NG; ++j) qacc[q][j] = 0.f;
+  auto fold = [&](int q, float (&t)[NB], int grp) {
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      float x = t[cb];
+      x += __shfl_xor(x, 16, 64);
+      x += __shfl_xor(x, 32, 64);
+#pragma unroll
+      for (int j = 0; j < NG; ++j)
+        if (cb == grp * NG + j) qacc[q][j] += x;
+    }
+  };
   const int64_t ntiles = (a.rows + 15) / 16;
   const int64_t nw = (int64_t)gridDim.x * RS_NWV;
   for (int64_t t = (int64_t)blockIdx.x * RS_NWV + wave; t < ntiles; t += nw) {
@@ -2041,6 +2113,12 @@ __global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
     if constexpr (KIND == NODE_BLOCK) {
 #pragma unroll
       for (int kg = 0; kg < NK1; ++kg) {
+        if (kg < NKH && a.in0_16) {  // bf16 copy of v
+          xf[kg] = arow < n ? *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a.in0_16) +
+                                                              (row0 + arow) * L + kg * 32 + ach * 8)
+                            : make_uint4(0, 0, 0, 0);
+          continue;
+        }
         const float* src = (kg < NKH ? a.in0 : a.in1) + (row0 + arow) * L + (kg % NKH) * 32 + ach * 8;
         float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
         if (arow < n) {
@@ -2115,30 +2193,41 @@ __global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
       rs[r] = 1.0f / sqrtf(rs[r] / L + a.eps);
       t1[r] = t2[r] = 0.f;
     }
+    {
+      float tg[NB], tb[NB];
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-      const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+      for (int cb = 0; cb < NB; ++cb) {
+        const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+        tg[cb] = tb[cb] = 0.f;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        y[cb][r] = (y[cb][r] - mu[r]) * rs[r];
-        const float d = dm[cb][r] * g;
-        t1[r] += d;
-        t2[r] += d * y[cb][r];
-        pg[cb] += dm[cb][r] * y[cb][r];
-        pb[cb] += dm[cb][r];
+        for (int r = 0; r < 4; ++r) {
+          y[cb][r] = (y[cb][r] - mu[r]) * rs[r];
+          const float d = dm[cb][r] * g;
+          t1[r] += d;
+          t2[r] += d * y[cb][r];
+          tg[cb] += dm[cb][r] * y[cb][r];
+          tb[cb] += dm[cb][r];
+        }
       }
+      fold(2, tg, ln >> 4);
+      fold(3, tb, ln >> 4);
     }
     rs_butterfly(t1);
     rs_butterfly(t2);
     float v[NB][4];
+    {
+      float tl[NB];
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-      const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+      for (int cb = 0; cb < NB; ++cb) {
+        const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
+        tl[cb] = 0.f;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        v[cb][r] = rs[r] * (dm[cb][r] * g - t1[r] / L - y[cb][r] * (t2[r] / L));
-        pl[cb] += v[cb][r];
+        for (int r = 0; r < 4; ++r) {
+          v[cb][r] = rs[r] * (dm[cb][r] * g - t1[r] / L - y[cb][r] * (t2[r] / L));
+          tl[cb] += v[cb][r];
+        }
       }
+      fold(1, tl, ln >> 4);
     }
     uint4 gf[NKH];
     rs_to_frags<L>(v, scr, gf, ln);
@@ -2146,13 +2235,17 @@ __global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
     {
       floatx4 acc[NB];
       rs_gemm<NB, NKH>(gf, W2b, acc, ln);
+      float th[NB];
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb)
+      for (int cb = 0; cb < NB; ++cb) {
+        th[cb] = 0.f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           v[cb][r] = ((mask >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
-          ph[cb] += v[cb][r];
+          th[cb] += v[cb][r];
         }
+      }
+      fold(0, th, ln >> 4);
     }
     rs_to_frags<L>(v, scr, gf, ln);
     rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[0]) + row0 * L, scr, n, ln);
@@ -2180,18 +2273,13 @@ __global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
   // column partials: lane groups, then the waves in order through LDS
   __syncthreads();
   float* red = reinterpret_cast<float*>(lds);
+  {
+    float* rw = red + wave * Lay::NVEC;
 #pragma unroll
-  for (int cb = 0; cb < NB; ++cb) {
-    float q[4] = {ph[cb], pl[cb], pg[cb], pb[cb]};
+    for (int j = 0; j < NG; ++j) {
+      const int col = ((lane >> 4) * NG + j) * 16 + (lane & 15);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      q[k] += __shfl_xor(q[k], 16, 64);
-      q[k] += __shfl_xor(q[k], 32, 64);
-    }
-    if (lane < 16) {
-      float* rw = red + wave * Lay::NVEC;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) rw[k * L + cb * 16 + lane] = q[k];
+      for (int q = 0; q < 4; ++q) rw[q * L + col] = qacc[q][j];
     }
   }
   __syncthreads();
@@ -2249,10 +2337,24 @@ __global__ __launch_bounds__(NT) void input_grad_kernel(InGradArgs a) {
   const int64_t n0 = (int64_t)blockIdx.x * TM;
   const int tid = threadIdx.x, wave = tid >> 6;
   const T* dz = reinterpret_cast<const T*>(a.dz);
-  // sender sums: (node, 16-byte chunk) items, ascending edges, 4 loads in flight
+  // sender sums: (node, 16-byte chunk) items, ascending edges, 4 loads in
+  // flight; or, when they were formed chunk by chunk (sender_sums_kernel),
+  // read back from dzs
   constexpr int E16 = 16 / sizeof(T);
   constexpr int CPR = L / E16;
-  for (int it = tid; it < TM * CPR; it += NT) {
+  if (a.dzs_ready) {
+    for (int it = tid; it < TM * (L / 4); it += NT) {
+      const int row = it / (L / 4), c = (it % (L / 4)) * 4;
+      const int64_t node = n0 + row;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (node < a.n_local) v = *reinterpret_cast<const float4*>(a.dzs + node * L + c);
+      put_operand<P>(Sh + row * LDT + c, Sl + row * LDT + c, v.x);
+      put_operand<P>(Sh + row * LDT + c + 1, Sl + row * LDT + c + 1, v.y);
+      put_operand<P>(Sh + row * LDT + c + 2, Sl + row * LDT + c + 2, v.z);
+      put_operand<P>(Sh + row * LDT + c + 3, Sl + row * LDT + c + 3, v.w);
+    }
+  }
+  for (int it = tid; !a.dzs_ready && it < TM * CPR; it += NT) {
     const int row = it / CPR, c = (it % CPR) * E16;
     const int64_t node = n0 + row;
     float s[E16];
@@ -2323,6 +2425,45 @@ __global__ __launch_bounds__(NT) void input_grad_kernel(InGradArgs a) {
     }
 }
 
+// Per-sender sums of dz_0 over the edges of one chunk [e_lo, e_hi) (dz rows
+// stored from e_lo): dzs[n] = (first chunk ? 0 : dzs[n]) + sum, each node's
+// edges of the chunk in ascending id (a contiguous run of its transposed-CSR
+// list).  Chunk by chunk this gives the sums input_grad_kernel forms in one
+// pass when the whole edge range is one chunk.
+template <int P_, int L>
+__global__ __launch_bounds__(NT) void sender_sums_kernel(const int32_t* __restrict__ trow,
+                                                         const int32_t* __restrict__ tedge, const void* dzv,
+                                                         int64_t e_lo, int64_t e_hi, int64_t n_local,
+                                                         float* __restrict__ dzs, int first) {
+  using P = typename PrecOf<P_>::type;
+  using T = typename P::T;
+  constexpr int E16 = 16 / sizeof(T);
+  constexpr int CPR = L / E16;
+  const T* dz = reinterpret_cast<const T*>(dzv);
+  const int64_t it = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (it >= n_local * CPR) return;
+  const int64_t node = it / CPR;
+  const int c = (int)(it % CPR) * E16;
+  int32_t lo = trow[node], hi = trow[node + 1];
+  while (lo < hi) {  // first of the node's edges at or after e_lo
+    const int32_t mid = (lo + hi) >> 1;
+    if (tedge[mid] < e_lo) lo = mid + 1;
+    else hi = mid;
+  }
+  float s[E16];
+#pragma unroll
+  for (int j = 0; j < E16; ++j) s[j] = 0.f;
+  for (int32_t i = lo; i < trow[node + 1] && tedge[i] < e_hi; ++i) {
+    const uint4 v = *reinterpret_cast<const uint4*>(dz + (int64_t)(tedge[i] - e_lo) * L + c);
+    const T* t = reinterpret_cast<const T*>(&v);
+#pragma unroll
+    for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
+  }
+  float* d = dzs + node * L + c;
+#pragma unroll
+  for (int j = 0; j < E16; ++j) d[j] = (first ? 0.f : d[j]) + s[j];
+}
+
 // -------------------------------------------------- weight gradients ---
 // part[s][o][i] = sum over rows of split s of delta[row][o] * A[row][i], as an
 // MFMA GEMM with both operands staged transposed in LDS (rows contiguous).
@@ -2354,6 +2495,13 @@ __device__ __forceinline__ uint4 dw_load_a(const DwArgs& a, int64_t row, int col
   } else if (a.a_kind == 3) {
     const int L = a.L;
     const float* src = (col < L ? reinterpret_cast<const float*>(a.a0) + row * L + col : a.a1 + row * L + (col - L));
+#pragma unroll
+    for (int e = 0; e < P::EL; ++e) v[e] = P::cvt(src[e]);
+  } else if (a.a_kind == 5) {
+    // node concat with v as bf16 rows (bf16 mode; EL = 8 columns never straddle v | agg)
+    const int L = a.L;
+    if (col < L) return *reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.a3) + row * L + col);
+    const float* src = a.a1 + row * L + (col - L);
 #pragma unroll
     for (int e = 0; e < P::EL; ++e) v[e] = P::cvt(src[e]);
   } else {
@@ -2698,6 +2846,7 @@ hipError_t launch_erecv(const int32_t* row_ptr, int64_t n_owned, int32_t* erecv,
 }
 
 int64_t plan_chunks(int64_t n_owned) { return (n_owned + PLAN_CHUNK - 1) / PLAN_CHUNK; }
+int plan_chunk_receivers() { return PLAN_CHUNK; }
 
 int64_t plan_max_units(int64_t n_owned, int64_t n_edges, int te_target, int r_max) {
   // a closed unit plus the receiver that closed it exceeds te_target edges or
@@ -2893,6 +3042,26 @@ static hipError_t input_grad_t(const InGradArgs& a, hipStream_t st) {
   const unsigned grid = (unsigned)((a.n_local + G::TM - 1) / G::TM);
   hipLaunchKernelGGL((input_grad_kernel<P_, L>), dim3(grid), dim3(NT), G::END, st, a);
   return hipGetLastError();
+}
+
+template <int P_, int L>
+static hipError_t sender_sums_t(const int32_t* trow, const int32_t* tedge, const void* dz, int64_t e_lo, int64_t e_hi,
+                                int64_t n_local, float* dzs, int first, hipStream_t st) {
+  constexpr int CPR = L / (16 / (P_ == BF16 ? 2 : 4));
+  const unsigned grid = (unsigned)((n_local * CPR + NT - 1) / NT);
+  hipLaunchKernelGGL((sender_sums_kernel<P_, L>), dim3(grid), dim3(NT), 0, st, trow, tedge, dz, e_lo, e_hi, n_local,
+                     dzs, first);
+  return hipGetLastError();
+}
+
+hipError_t launch_sender_sums(int prec, int L, const int32_t* trow, const int32_t* tedge, const void* dz, int64_t e_lo,
+                              int64_t e_hi, int64_t n_local, float* dzs, int first, hipStream_t st) {
+  if (n_local == 0) return hipSuccess;
+#define SS(PP, LL) \
+  if (prec == PP && L == LL) return sender_sums_t<PP, LL>(trow, tedge, dz, e_lo, e_hi, n_local, dzs, first, st);
+  SS(F32, 64) SS(F32, 128) SS(F32, 256) SS(BF16, 64) SS(BF16, 128) SS(BF16, 256)
+#undef SS
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t st) {

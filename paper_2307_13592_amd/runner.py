@@ -7,12 +7,14 @@ import numpy as np
 import torch
 
 from . import (MGN_BF16, MGN_FP32, graph_struct, mgn_backward, mgn_create, mgn_destroy, mgn_forward,
-               mgn_graph_validate, mgn_mse_grad, mgn_param_count, mgn_set_params, mgn_workspace_size)
+               mgn_graph_validate, mgn_mse_grad, mgn_param_count, mgn_set_params, mgn_set_recompute,
+               mgn_workspace_size)
 
 
 class Session:
     def __init__(self, latent: int, K: int, depth: int, precision: str, graph: dict, node_feat, edge_feat, halo,
-                 params, device: str = "cuda", node_in: int = 11, edge_in: int = 4, node_out: int = 5):
+                 params, device: str = "cuda", node_in: int = 11, edge_in: int = 4, node_out: int = 5,
+                 recompute: int = 0, chunk_edges: int = 0):
         if not torch.cuda.is_available():
             raise RuntimeError("libmgn needs a HIP device")
         self.device = torch.device(device)
@@ -31,6 +33,8 @@ class Session:
         self.n_params = mgn_param_count(self.model)
         self.set_params(params)
         mgn_graph_validate(self.model, self.gs)
+        if recompute:
+            mgn_set_recompute(self.model, recompute, chunk_edges)
         self.ws_bytes = mgn_workspace_size(self.model, self.gs)
         self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=self.device)
         self.out = torch.empty((no, node_out), dtype=torch.float32, device=self.device)

@@ -1,0 +1,50 @@
+"""Edge-stream checkpointing (mgn_set_recompute): the backward pass that
+recomputes each block's edge latents from the checkpoint below it, its
+aggregate by one more edge forward, reads the node stream's bf16 copy and
+runs the edge backward (and the edge encoder's) in receiver chunks.  Against
+the run that keeps every block's inputs, on the same inputs: outputs bitwise
+equal (the forward is the same computation, only stored elsewhere), every
+gradient tensor equal up to the order in which chunk sums are added; and
+against the oracle with the parity criterion of test_gpu_parity."""
+import numpy as np
+import pytest
+
+from synth import meshes
+from parity import calibrate, compare, local_inputs, rel_err, run_gpu, run_oracle, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _segments_err(shapes, a, b):
+    off, worst = 0, (0.0, "")
+    for name, _, shape in shapes:
+        n = int(np.prod(shape))
+        e = rel_err(a[off:off + n], b[off:off + n])
+        worst = max(worst, (e, name))
+        off += n
+    return worst
+
+
+@pytest.mark.parametrize("l,D", [(64, 3), (128, 2), (256, 3)])
+@pytest.mark.parametrize("interval,chunk", [(1, 0), (2, 600), (3, 250)])
+def test_checkpointed_equals_stash_all(l, D, interval, chunk):
+    K = 5
+    say(f"[lean] l={l} D={D} K={K} interval={interval} chunk_edges={chunk}")
+    c = local_inputs(meshes.sector(6, 16, 10, 4, seed=7), 1, l, K, D, 3)
+    base = run_gpu(c, l, K, D, "bf16")
+    lean = run_gpu(c, l, K, D, "bf16", recompute=interval, chunk_edges=chunk)
+    assert np.array_equal(base[0], lean[0]), "outputs differ"
+    e, name = _segments_err(c["shapes"], lean[1], base[1])
+    eh = rel_err(lean[2], base[2])
+    say(f"  parameter gradients: worst {e:.2e} ({name}); halo gradient {eh:.2e}")
+    assert e <= 1e-4 and eh <= 1e-4
+
+
+def test_checkpointed_against_oracle():
+    l, K, D = 128, 4, 2
+    say(f"[lean] oracle parity l={l} K={K} D={D}")
+    c = local_inputs(meshes.sector(6, 16, 10, 4, seed=11), 1, l, K, D, 5)
+    gpu = run_gpu(c, l, K, D, "bf16", recompute=3, chunk_edges=300)
+    ref = run_oracle(c, l, K, D, bf16=True)
+    bad = compare("checkpointed", "bf16", c["shapes"], gpu, ref, calibrate(c, l, K, D, "bf16"))
+    assert not bad, bad

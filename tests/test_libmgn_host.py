@@ -128,3 +128,29 @@ def test_state_errors_before_any_launch():
     finally:
         mgn.mgn_destroy(h)
     assert mgn.lib().mgn_mse_grad(None, None, None, 3, 0, None, None, None) == mgn.MGN_E_ARG
+
+
+def test_recompute_setting():
+    """Edge-stream checkpointing is a bf16-mode setting; it shrinks the
+    workspace of a graph with several blocks."""
+    import ctypes as C
+    L = mgn.lib()
+    h32 = mgn.mgn_create(64, 4, 2)
+    try:
+        assert L.mgn_set_recompute(h32, 2, 0) == mgn.MGN_E_UNSUPPORTED
+        assert L.mgn_set_recompute(h32, 0, 0) == mgn.MGN_OK
+    finally:
+        mgn.mgn_destroy(h32)
+    h = mgn.mgn_create(64, 8, 2, mgn.MGN_BF16)
+    try:
+        assert L.mgn_set_recompute(h, -1, 0) == mgn.MGN_E_ARG
+        assert L.mgn_set_recompute(h, 1, -5) == mgn.MGN_E_ARG
+        g = mgn.mgn_graph(1000, 0, 20000, C.c_void_p(256), C.c_void_p(512), C.c_void_p(768), C.c_void_p(1024))
+        n0, n4 = C.c_size_t(), C.c_size_t()
+        assert L.mgn_workspace_size(h, C.byref(g), C.byref(n0)) == mgn.MGN_OK
+        assert L.mgn_set_recompute(h, 4, 0) == mgn.MGN_OK
+        assert L.mgn_workspace_size(h, C.byref(g), C.byref(n4)) == mgn.MGN_OK
+        # 8 edge-latent copies down to 2 checkpoints + 1 working copy (bf16, 64 wide)
+        assert n0.value - n4.value >= 5 * 20000 * 64 * 2
+    finally:
+        mgn.mgn_destroy(h)
