@@ -792,7 +792,6 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.de_next = (k == K - 1) ? nullptr : DE;  // dL/de is updated in place
       a.dagg = DAGG;
       a.de_out = DE;
-      a.de_std = k == 0;  // block 0's dL/de^0 feeds the edge encoder's backward
       const bool rs = edge_rs(m->prec, L, D);
       a.proj = rs ? (const float*)(ws + p.PROJ) : nullptr;
       if (rs && no > 0 && !p.lean) {  // (the aggregate recompute made them already)

@@ -72,7 +72,6 @@ struct EdgeBwdArgs {
   int64_t n_owned;
   const void* Ein;      // e^k (storage type)
   const float* de_next; // dL/de^{k+1} [E][L] or null (last block)
-  int de_std;           // row-split kernels: de_out in plain column order (else lane-major, as de_next)
   float* dagg;          // [n_owned][L]: dL/dagg in; each receiver's sum of dz_0 out
   float* de_out;        // dL/de^k [E][L]
   const float* proj;    // node projections [n_local][2L] (row-split kernels), else unused

@@ -1358,28 +1358,6 @@ __device__ __forceinline__ int rs_sw32(int row, int col) {
   return row * L + ((((col >> 2) ^ (row & M))) << 2) + (col & 3);
 }
 
-// Lane-major column order of fp32 rows the row-split kernels exchange in
-// accumulator order (node projections, edge-stream gradients): column
-// cb * 16 + c is stored at c * NB + cb, so the NB columns one lane holds of
-// a row are contiguous (NB / 4 16-byte accesses instead of NB 4-byte ones).
-template <int L>
-__device__ __forceinline__ void rs_load_row(const float* __restrict__ row, int c, float (&v)[L / 16]) {
-#pragma unroll
-  for (int q = 0; q < L / 64; ++q) {
-    const float4 x = reinterpret_cast<const float4*>(row + c * (L / 16))[q];
-    v[4 * q] = x.x;
-    v[4 * q + 1] = x.y;
-    v[4 * q + 2] = x.z;
-    v[4 * q + 3] = x.w;
-  }
-}
-template <int L>
-__device__ __forceinline__ void rs_store_row(float* __restrict__ row, int c, const float (&v)[L / 16]) {
-#pragma unroll
-  for (int q = 0; q < L / 64; ++q)
-    reinterpret_cast<float4*>(row + c * (L / 16))[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
-}
-
 // acc[cb] = sum over k-groups of A[kg] x B[cb][kg]: one 16-row tile, every
 // 16-column block cb, B fragments in LDS ([cb][kg][lane], 16 bytes each).
 template <int NB, int NKG>
@@ -1403,12 +1381,15 @@ __device__ __forceinline__ void rs_copy_frags(uint4* dst, const uint4* __restric
   }
 }
 
+// The wave's index in its workgroup, as a wave-uniform (scalar) value.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
 // Receiver range of wave w (of W waves in total) within [lo_r, hi_r):
 // receiver-aligned, about E / W edges each; the waves of one XCD
 // (blockIdx % 8) get neighbouring ranges.
 __device__ __forceinline__ void rs_range(const int32_t* __restrict__ row_ptr, int64_t lo_r, int64_t hi_r, int64_t& r0,
                                          int64_t& r1) {
-  const int G = gridDim.x, b = blockIdx.x, nwv = blockDim.x >> 6, wave = threadIdx.x >> 6;
+  const int G = gridDim.x, b = blockIdx.x, nwv = blockDim.x >> 6, wave = wave_id();
   const int64_t W = (int64_t)G * nwv;
   const int64_t q = ((int64_t)(b & 7) * (G >> 3) + (b >> 3)) * nwv + wave;
   const int64_t e0 = row_ptr[lo_r], E = row_ptr[hi_r] - e0;
@@ -1435,11 +1416,27 @@ __device__ __forceinline__ void rs_zero_empty(const int32_t* __restrict__ row_pt
       for (int c = 0; c < L; c += 4) *reinterpret_cast<float4*>(dst + r * L + c) = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
-// One 16-edge tile's metadata: lane j < 16 holds edge sb + j's receiver,
-// sender and the next edge's receiver (-1 past the range end); the mask has
-// bit j set where row j ends a receiver segment.
-// The loads are issued one tile ahead (rs_meta_load) and turned into the
-// mask when the tile starts (rs_meta_make), so no tile waits for them.
+// ----------------------------------------------------------------- T form ---
+// The row-split edge kernels and node_proj_kernel compute every product
+// transposed, Y^T = W X^T: weight fragments are the MFMA A operand and a
+// 16-row tile of activations the B operand (lane (e, q) = (lane & 15,
+// lane >> 4) supplies row e, k-slots 8 q ..).  Lane (e, q) of the
+// accumulator tile then holds output columns 16 cb + 4 q + r (every 16-column
+// block cb, r = 0..3) of row e.  Three things follow.  Rounded to bf16, the
+// accumulators of one product are the B operand of the next as they stand:
+// for k-group kg lane (e, q) has columns 32 kg + 16 h + 4 q + r (h = 0, 1),
+// which the next weight matrix's fragments match once their k-slots are
+// permuted the same way (rt_copy_frags).  A row's LayerNorm statistics are a
+// per-lane sum plus a sum over the four 16-lane groups (two lane-swap
+// instructions).  Column sums over a tile's rows are a reduce-scatter across
+// the 16 lanes of a group (DPP).  Rows in memory keep the plain column order:
+// a lane reads or writes 4 consecutive columns per 16-column block.
+
+// One 16-edge tile's metadata, every lane for its row e = lane & 15: the
+// edge's receiver, sender and the next edge's receiver (-1 past the range
+// end); the mask has bit j (j < 16) set where row j ends a receiver segment.
+// The loads are issued one tile ahead (rt_meta_load) and turned into the
+// mask when the tile starts (rt_meta_make), so no tile waits for them.
 struct RsMeta {
   int32_t r, s;
   unsigned long long last;
@@ -1447,50 +1444,158 @@ struct RsMeta {
 struct RsMetaRaw {
   int32_t r, s, rn;
 };
-__device__ __forceinline__ RsMetaRaw rs_meta_load(const int32_t* __restrict__ erecv, const int32_t* __restrict__ send,
+__device__ __forceinline__ RsMetaRaw rt_meta_load(const int32_t* __restrict__ erecv, const int32_t* __restrict__ send,
                                                   int64_t sb, int64_t e1) {
-  const int lane = threadIdx.x & 63;
+  const int e = threadIdx.x & 15;
   RsMetaRaw w{-1, 0, -1};
-  if (lane < 16 && sb + lane < e1) {
-    w.r = erecv[sb + lane];
-    w.s = send[sb + lane];
-    if (sb + lane + 1 < e1) w.rn = erecv[sb + lane + 1];
+  if (sb + e < e1) {
+    w.r = erecv[sb + e];
+    w.s = send[sb + e];
+    if (sb + e + 1 < e1) w.rn = erecv[sb + e + 1];
   }
   return w;
 }
-__device__ __forceinline__ RsMeta rs_meta_make(const RsMetaRaw& w) {
+__device__ __forceinline__ RsMeta rt_meta_make(const RsMetaRaw& w) {
   RsMeta mt{w.r, w.s, 0};
   mt.last = __ballot(w.r >= 0 && w.rn != w.r);
   return mt;
 }
 
-// z_1 of a tile in accumulator order: W_e e (MFMA) + P_s[s] + P_r[r] + b_1,
-// added in that order (the forward and the recompute in the backward share it).
-template <int L>
-__device__ __forceinline__ void rs_first_layer(const uint4 (&ef)[L / 32], const uint4* W1e, const RsMeta& mt, int n,
-                                               const float* __restrict__ proj, const float* __restrict__ b1,
-                                               floatx4 (&z)[L / 16], int lane) {
-  constexpr int NB = L / 16;
-  float ps[4][NB], pr[4][NB];
+// Like rs_copy_frags, with the eight k-slots of every fragment reordered so
+// that slot j of lane group q pairs with k = 32 kg + 16 (j / 4) + 4 q + j % 4:
+// its low half comes from lane group q / 2, its high half from 2 + q / 2,
+// slots 4 (q % 2) .. of each.
+__device__ __forceinline__ void rt_copy_frags(uint4* dst, const uint4* __restrict__ src, int nb, int nkg, int src_nkg,
+                                              int kg0) {
+  const int total = nb * nkg * 64;
+  for (int i = threadIdx.x; i < total; i += blockDim.x) {
+    const int cb = i / (nkg * 64), kg = (i / 64) % nkg, ln = i % 64, q = ln >> 4, c = ln & 15;
+    const uint2* s = reinterpret_cast<const uint2*>(src + ((size_t)cb * src_nkg + kg0 + kg) * 64);
+    const uint2 lo = s[(c + 16 * (q >> 1)) * 2 + (q & 1)];
+    const uint2 hi = s[(c + 16 * (2 + (q >> 1))) * 2 + (q & 1)];
+    dst[i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  }
+}
+
+// acc[cb] = sum over k-groups of W[cb][kg] (LDS, [cb][kg][lane]) x X[kg].
+template <int NB, int NKG>
+__device__ __forceinline__ void rt_gemm(const uint4* Wl, const uint4 (&X)[NKG], floatx4 (&acc)[NB], int lane) {
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kg = 0; kg < NKG; ++kg)
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) PBF16::mma(acc[cb], Wl[(cb * NKG + kg) * 64 + lane], X[kg]);
+}
+
+// Two fp32 values -> two bf16 (round to nearest even, one conversion instruction).
+__device__ __forceinline__ uint32_t bf_pack(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  const f32x2_t f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
+
+// Accumulator-order values -> bf16 B operands of the next product.
+template <int NB>
+__device__ __forceinline__ void rt_frags(const float (&v)[NB][4], uint4 (&f)[NB / 2]) {
+#pragma unroll
+  for (int kg = 0; kg < NB / 2; ++kg)
+    f[kg] = make_uint4(bf_pack(v[2 * kg][0], v[2 * kg][1]), bf_pack(v[2 * kg][2], v[2 * kg][3]),
+                       bf_pack(v[2 * kg + 1][0], v[2 * kg + 1][1]), bf_pack(v[2 * kg + 1][2], v[2 * kg + 1][3]));
+}
+
+// The values of rt_frags -> one plain-order bf16 row (lane group q's columns).
+template <int NKH>
+__device__ __forceinline__ void rt_store_frags(uint16_t* __restrict__ row, int q, const uint4 (&f)[NKH]) {
+#pragma unroll
+  for (int kg = 0; kg < NKH; ++kg) {
+    *reinterpret_cast<uint2*>(row + kg * 32 + q * 4) = make_uint2(f[kg].x, f[kg].y);
+    *reinterpret_cast<uint2*>(row + kg * 32 + 16 + q * 4) = make_uint2(f[kg].z, f[kg].w);
+  }
+}
+
+// Sum over the four 16-lane groups; every lane gets the same bits.
+__device__ __forceinline__ float rt_sum4(float x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float s = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  const auto p2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+  return __uint_as_float(p2[0]) + __uint_as_float(p2[1]);
+}
+
+// Per-lane partial over an accumulator tile's values, four chains.
+template <int NB>
+__device__ __forceinline__ float rt_lane_sum(const float (&v)[NB][4]) {
+  float t[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int row = (lane >> 4) * 4 + r;
-    const int64_t s = __shfl(mt.s, row, 64), rv = __shfl(mt.r, row, 64);
-    if (row < n) {
-      rs_load_row<L>(proj + s * (2 * L), lane & 15, ps[r]);
-      rs_load_row<L>(proj + rv * (2 * L) + L, lane & 15, pr[r]);
-    } else {
+    t[r] = v[0][r];
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb) ps[r][cb] = pr[r][cb] = 0.f;
-    }
+    for (int cb = 1; cb < NB; ++cb) t[r] += v[cb][r];
   }
-  rs_gemm<NB, L / 32>(ef, W1e, z, lane);
+  return (t[0] + t[1]) + (t[2] + t[3]);
+}
+
+// One reduce-scatter step within a 16-lane group: v[0, N) -> v[0, N / 2);
+// the lane keeps the half that `hi` selects and adds the DPP partner's copy
+// of it (the partner keeps the other half).
+template <int N, int CTRL>
+__device__ __forceinline__ void rt_halve(float* v, bool hi) {
+#pragma unroll
+  for (int k = 0; k < N / 2; ++k) {
+    const float keep = hi ? v[k + N / 2] : v[k], send = hi ? v[k] : v[k + N / 2];
+    v[k] = keep + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(send), CTRL, 0xf, 0xf, false));
+  }
+}
+
+// Column totals over a tile's 16 rows.  In: v[NV] per lane (index 4 cb + r of
+// the accumulator order).  Out: lane e's v[t], t < NV / 16, is the total of
+// index e * NV / 16 + t.  Partners: row mirror (e ^ 15), half-row mirror
+// (e ^ 7), then e ^ 3 and e ^ 1 within quads.
+template <int NV>
+__device__ __forceinline__ void rt_col_totals(float (&v)[NV], int e) {
+  static_assert(NV >= 16, "at least one total per lane");
+  rt_halve<NV, 0x140>(v, e & 8);
+  rt_halve<NV / 2, 0x141>(v, e & 4);
+  rt_halve<NV / 4, 0x1B>(v, e & 2);
+  rt_halve<NV / 8, 0xB1>(v, e & 1);
+}
+
+// 4 consecutive floats of a plain-order row at column 16 cb + 4 q.
+__device__ __forceinline__ float4 rt_ld4(const float* __restrict__ p, int cb, int q) {
+  return *reinterpret_cast<const float4*>(p + cb * 16 + q * 4);
+}
+
+// z_1 of a tile in T order: W_e e (MFMA) + P_s[s] + P_r[r], added in that
+// order, with b_1 inside P_r (the forward and the recompute in the backward
+// share it).
+template <int L>
+__device__ __forceinline__ void rt_first_layer(const uint4 (&ef)[L / 32], const uint4* W1e, const RsMeta& mt, bool ok,
+                                               const float* __restrict__ proj, floatx4 (&z)[L / 16], int lane) {
+  constexpr int NB = L / 16;
+  const int q = lane >> 4;
+  // rows past the tile's end gather node 0 (their results are never used)
+  const float* sp = proj + (int64_t)(ok ? mt.s : 0) * (2 * L);
+  const float* rp = proj + (int64_t)(ok ? mt.r : 0) * (2 * L) + L;
+  float4 ps[NB], pr[NB];
 #pragma unroll
   for (int cb = 0; cb < NB; ++cb) {
-    const float bv = b1[cb * 16 + (lane & 15)];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) z[cb][r] = ((z[cb][r] + ps[r][cb]) + pr[r][cb]) + bv;
+    ps[cb] = rt_ld4(sp, cb, q);
+    pr[cb] = rt_ld4(rp, cb, q);
   }
+  rt_gemm<NB, L / 32>(W1e, ef, z, lane);
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) {
+    z[cb][0] = (z[cb][0] + ps[cb].x) + pr[cb].x;
+    z[cb][1] = (z[cb][1] + ps[cb].y) + pr[cb].y;
+    z[cb][2] = (z[cb][2] + ps[cb].z) + pr[cb].z;
+    z[cb][3] = (z[cb][3] + ps[cb].w) + pr[cb].w;
+  }
+}
+
+// Copies n floats into LDS (all threads of the workgroup).
+__device__ __forceinline__ void rt_copy_vec(float* dst, const float* __restrict__ src, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = src[i];
 }
 
 // Accumulator tile -> bf16 scratch (row order, swizzled) -> A fragments.
@@ -1547,26 +1652,41 @@ template <int L, int D>
 struct RsFwdLay {
   static constexpr int NKH = L / 32, NB = L / 16;
   static constexpr int W = NB * NKH * 64 * 16;         // bytes of one L x L packed layer
-  static constexpr int SCR = 16 * L * 4;               // per-wave scratch (fp32 tile)
-  static constexpr int OFF_W1 = 0, OFF_WH = W, OFF_WL = (D - 1) * W, OFF_SCR = D * W;
-  static constexpr int END = OFF_SCR + RS_NWV * SCR;
+  static constexpr int SCR = 16 * 64 * 4;              // per-wave scratch: 16 rows x 64 fp32 columns
+  // vectors: last bias, gamma, beta[, hidden bias]
+  static constexpr int OFF_W1 = 0, OFF_WH = W, OFF_WL = (D - 1) * W, OFF_VEC = D * W;
+  static constexpr int NVEC = (D == 3 ? 4 : 3) * L;
+  static constexpr int OFF_SCR = OFF_VEC + NVEC * 4;
+  // waves per workgroup: l = 64 fits 16 (at most 128 registers each), l = 128 12 (168)
+  static constexpr int NWV = L == 64 ? 16 : 12;
+  static constexpr int NTH = 64 * NWV;
+  static constexpr int END = OFF_SCR + NWV * SCR;
+  static_assert(END <= 160 * 1024, "LDS");
 };
 
-// Forward of one block's edge half; P = node projections of the block input.
+// Forward of one block's edge half (T form); P = node projections of the
+// block input.
 template <int L, int D>
-__global__ __launch_bounds__(RS_NTH) void edge_fwd_rs_kernel(EdgeFwdArgs a) {
+__global__ __launch_bounds__((RsFwdLay<L, D>::NTH)) void edge_fwd_rs_kernel(EdgeFwdArgs a) {
   using Lay = RsFwdLay<L, D>;
   constexpr int NKH = Lay::NKH, NB = Lay::NB;
   extern __shared__ __align__(16) unsigned char lds[];
   uint4* W1 = reinterpret_cast<uint4*>(lds + Lay::OFF_W1);
   uint4* WH = reinterpret_cast<uint4*>(lds + Lay::OFF_WH);
   uint4* WL = reinterpret_cast<uint4*>(lds + Lay::OFF_WL);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float* vbl = reinterpret_cast<float*>(lds + Lay::OFF_VEC);  // last bias
+  float* vg = vbl + L;                                          // gamma
+  float* vbt = vbl + 2 * L;                                     // beta
+  float* vbh = vbl + 3 * L;                                     // hidden bias (D = 3)
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   float* scr32 = reinterpret_cast<float*>(lds + Lay::OFF_SCR + wave * Lay::SCR);
-  uint16_t* scr16 = reinterpret_cast<uint16_t*>(scr32);
-  rs_copy_frags(W1, a.mlp.lin[0].wf, NB, NKH, 3 * NKH, 0);
-  if constexpr (D == 3) rs_copy_frags(WH, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
-  rs_copy_frags(WL, a.mlp.lin[D - 1].wf, NB, NKH, NKH, 0);
+  rs_copy_frags(W1, a.mlp.lin[0].wf, NB, NKH, 3 * NKH, 0);  // B operand read from memory rows
+  if constexpr (D == 3) rt_copy_frags(WH, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
+  rt_copy_frags(WL, a.mlp.lin[D - 1].wf, NB, NKH, NKH, 0);
+  rt_copy_vec(vbl, a.mlp.lin[D - 1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  rt_copy_vec(vbt, a.mlp.beta, L);
+  if constexpr (D == 3) rt_copy_vec(vbh, a.mlp.lin[1].b, L);
   __syncthreads();
   int64_t r0, r1;
   rs_range(a.row_ptr, 0, a.n_owned, r0, r1);
@@ -1575,104 +1695,105 @@ __global__ __launch_bounds__(RS_NTH) void edge_fwd_rs_kernel(EdgeFwdArgs a) {
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
   uint16_t* Eout = reinterpret_cast<uint16_t*>(a.Eout);
   float run[(L + 63) / 64] = {};  // running receiver sums, columns lane + 64 j
-  RsMetaRaw nxt = rs_meta_load(a.erecv, a.send, E0, E1);
+  RsMetaRaw nxt = rt_meta_load(a.erecv, a.send, E0, E1);
   for (int64_t sb = E0; sb < E1; sb += 16) {
     // an opaque copy of the lane index, so that the lane-dependent addresses
     // are recomputed per tile instead of being hoisted into registers
     int ln = lane;
     asm volatile("" : "+v"(ln));
-    const int arow = ln & 15, ach = ln >> 4;
+    const int e = ln & 15, q = ln >> 4;
     const int n = (int)(E1 - sb < 16 ? E1 - sb : 16);
-    const RsMeta mt = rs_meta_make(nxt);
-    nxt = rs_meta_load(a.erecv, a.send, sb + 16, E1);
+    const bool ok = e < n;
+    const RsMeta mt = rt_meta_make(nxt);
+    nxt = rt_meta_load(a.erecv, a.send, sb + 16, E1);
+    // rows past the tile's end repeat row 0 (their results are never stored)
+    const int64_t er = sb + (ok ? e : 0);
+    const uint16_t* erow = Ein + er * L;
     uint4 ef[NKH];
 #pragma unroll
-    for (int kg = 0; kg < NKH; ++kg)
-      ef[kg] = arow < n ? *reinterpret_cast<const uint4*>(Ein + (sb + arow) * L + kg * 32 + ach * 8)
-                        : make_uint4(0, 0, 0, 0);
+    for (int kg = 0; kg < NKH; ++kg) ef[kg] = *reinterpret_cast<const uint4*>(erow + kg * 32 + q * 8);
     floatx4 z[NB];
-    rs_first_layer<L>(ef, W1, mt, n, a.proj, a.mlp.lin[0].b, z, ln);
+    rt_first_layer<L>(ef, W1, mt, ok, a.proj, z, ln);
     float h[NB][4];
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) h[cb][r] = z[cb][r] > 0.f ? z[cb][r] : 0.f;
     uint4 hf[NKH];
-    rs_to_frags<L>(h, scr16, hf, ln);
+    rt_frags<NB>(h, hf);
     if constexpr (D == 3) {
       floatx4 acc[NB];
-      rs_gemm<NB, NKH>(hf, WH, acc, ln);
+      rt_gemm<NB, NKH>(WH, hf, acc, ln);
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
-        const float bv = a.mlp.lin[1].b[cb * 16 + (ln & 15)];
+        const float4 bv = rt_ld4(vbh, cb, q);
+        const float b4[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float v = acc[cb][r] + bv;
+          const float v = acc[cb][r] + b4[r];
           h[cb][r] = v > 0.f ? v : 0.f;
         }
       }
-      rs_to_frags<L>(h, scr16, hf, ln);
+      rt_frags<NB>(h, hf);
     }
     floatx4 acc[NB];
-    rs_gemm<NB, NKH>(hf, WL, acc, ln);
+    rt_gemm<NB, NKH>(WL, hf, acc, ln);
     float y[NB][4];
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb) {
-      const float bv = a.mlp.lin[D - 1].b[cb * 16 + (ln & 15)];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) y[cb][r] = acc[cb][r] + bv;
+      const float4 bv = rt_ld4(vbl, cb, q);
+      y[cb][0] = acc[cb][0] + bv.x;
+      y[cb][1] = acc[cb][1] + bv.y;
+      y[cb][2] = acc[cb][2] + bv.z;
+      y[cb][3] = acc[cb][3] + bv.w;
     }
-    // LayerNorm: two-pass statistics per row, then gamma * xhat + beta
-    float mu[4], var[4];
-    rs_row_totals<NB>(y, mu);
+    // e^k again in T order (4 columns per block) for the residual
+    uint2 ev[NB];
+    if (Eout) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) mu[r] = mu[r] / L;
+      for (int cb = 0; cb < NB; ++cb) ev[cb] = *reinterpret_cast<const uint2*>(erow + cb * 16 + q * 4);
+    }
+    // LayerNorm: two-pass statistics of row e, then gamma * xhat + beta
+    const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
     float dv[NB][4];
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float d = y[cb][r] - mu[r];
+        const float d = y[cb][r] - mu;
         dv[cb][r] = d * d;
       }
-    rs_row_totals<NB>(dv, var);
+    const float rs = 1.0f / sqrtf(rt_sum4(rt_lane_sum<NB>(dv)) / L + a.eps);
+    // y becomes m
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb) {
-      const int col = cb * 16 + (ln & 15);
-      const float g = a.mlp.gamma[col], bt = a.mlp.beta[col];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float rs = 1.0f / sqrtf(var[r] / L + a.eps);
-        scr32[rs_sw32<L>(((ln >> 4) * 4 + r), col)] = g * ((y[cb][r] - mu[r]) * rs) + bt;
-      }
+      const float4 g = rt_ld4(vg, cb, q), bt = rt_ld4(vbt, cb, q);
+      y[cb][0] = g.x * ((y[cb][0] - mu) * rs) + bt.x;
+      y[cb][1] = g.y * ((y[cb][1] - mu) * rs) + bt.y;
+      y[cb][2] = g.z * ((y[cb][2] - mu) * rs) + bt.z;
+      y[cb][3] = g.w * ((y[cb][3] - mu) * rs) + bt.w;
+      // e^{k+1} = e^k + m
+      const uint2 w = ev[cb];
+      ev[cb] = make_uint2(bf_pack(__uint_as_float(w.x << 16) + y[cb][0], __uint_as_float(w.x & 0xffff0000u) + y[cb][1]),
+                          bf_pack(__uint_as_float(w.y << 16) + y[cb][2], __uint_as_float(w.y & 0xffff0000u) + y[cb][3]));
     }
-    // e^{k+1} = e^k + m in fragment order (16 bytes per lane and k-group)
-    if (Eout && arow < n) {
+    if (Eout && ok) {
+      uint16_t* orow = Eout + (sb + e) * L;
 #pragma unroll
-      for (int kg = 0; kg < NKH; ++kg) {
-        const int c = kg * 32 + ach * 8;
-        const float4 m0 = *reinterpret_cast<const float4*>(scr32 + rs_sw32<L>(arow, c));
-        const float4 m1 = *reinterpret_cast<const float4*>(scr32 + rs_sw32<L>(arow, c + 4));
-        const uint16_t* e = reinterpret_cast<const uint16_t*>(&ef[kg]);
-        uint16_t o[8];
-        o[0] = f2bf(bf2f(e[0]) + m0.x);
-        o[1] = f2bf(bf2f(e[1]) + m0.y);
-        o[2] = f2bf(bf2f(e[2]) + m0.z);
-        o[3] = f2bf(bf2f(e[3]) + m0.w);
-        o[4] = f2bf(bf2f(e[4]) + m1.x);
-        o[5] = f2bf(bf2f(e[5]) + m1.y);
-        o[6] = f2bf(bf2f(e[6]) + m1.z);
-        o[7] = f2bf(bf2f(e[7]) + m1.w);
-        *reinterpret_cast<uint4*>(Eout + (sb + arow) * L + c) = *reinterpret_cast<const uint4*>(o);
-      }
+      for (int cb = 0; cb < NB; ++cb) *reinterpret_cast<uint2*>(orow + cb * 16 + q * 4) = ev[cb];
     }
-    // ordered receiver sums; a segment's total goes out at its last row
+    // ordered receiver sums, 64 columns at a time through the wave's scratch
+    // tile; a segment's total goes out at its last row
 #pragma unroll
     for (int j = 0; j < (L + 63) / 64; ++j) {
       const int c = ln + 64 * j;
+#pragma unroll
+      for (int cb = 4 * j; cb < 4 * j + 4 && cb < NB; ++cb)
+        *reinterpret_cast<float4*>(scr32 + rs_sw32<64>(e, (cb - 4 * j) * 16 + q * 4)) =
+            make_float4(y[cb][0], y[cb][1], y[cb][2], y[cb][3]);
       float x[16];
 #pragma unroll
-      for (int row = 0; row < 16; ++row) x[row] = scr32[rs_sw32<L>(row, c)];
+      for (int row = 0; row < 16; ++row) x[row] = scr32[rs_sw32<64>(row, ln)];
 #pragma unroll
       for (int row = 0; row < 16; ++row) {
         if (row < n) {
@@ -1691,22 +1812,25 @@ template <int L, int D>
 struct RsBwdLay {
   static constexpr int NKH = L / 32, NB = L / 16;
   static constexpr int W = NB * NKH * 64 * 16;
-  static constexpr int SCR = 16 * L * 2;               // per-wave scratch (bf16 tile)
+  static constexpr int SCR = 16 * 64 * 2;              // per-wave scratch: 16 rows x 64 bf16 columns
   // W_e (fwd), [W_h (fwd)], W_last (fwd), W_last (bwd), [W_h (bwd)], W_e (bwd)
   static constexpr int NW = D == 3 ? 6 : 4;
-  static constexpr int OFF_SCR = NW * W;
+  static constexpr int OFF_VEC = NW * W;               // last bias, gamma[, hidden bias]
+  static constexpr int OFF_SCR = OFF_VEC + (D == 3 ? 3 : 2) * L * 4;
   static constexpr int END = OFF_SCR + RS_NWV * SCR;
+  static_assert(END <= 160 * 1024, "LDS");
   static constexpr int NVEC = (D + 2) * L;             // bias / gamma / beta partials per wave
   static_assert(RS_NWV * NVEC * 4 <= OFF_SCR, "partials reuse the weight area");
 };
 
-// Backward of one block's edge half with the tile's forward recomputed (same
-// quantities as edge_bwd_kernel: dz_0 receiver sums over the consumed dagg
-// rows, de^k, the stored gradients and activations, per-workgroup partials).
+// Backward of one block's edge half (T form) with the tile's forward
+// recomputed: dz_0 receiver sums over the consumed dagg rows, de^k, the
+// stored gradients and activations, per-workgroup bias / LayerNorm partials.
 template <int L, int D>
 __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
   using Lay = RsBwdLay<L, D>;
   constexpr int NKH = Lay::NKH, NB = Lay::NB, W = Lay::W;
+  constexpr int NV = 4 * NB, NR = NV / 16;  // accumulator values per lane; column totals kept per lane
   extern __shared__ __align__(16) unsigned char lds[];
   uint4* W1f = reinterpret_cast<uint4*>(lds);
   uint4* WHf = reinterpret_cast<uint4*>(lds + W);
@@ -1714,59 +1838,54 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
   uint4* WLb = reinterpret_cast<uint4*>(lds + D * W);
   uint4* WHb = reinterpret_cast<uint4*>(lds + (D + 1) * W);
   uint4* W1b = reinterpret_cast<uint4*>(lds + (Lay::NW - 1) * W);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float* vbl = reinterpret_cast<float*>(lds + Lay::OFF_VEC);  // last bias
+  float* vg = vbl + L;                                          // gamma
+  float* vbh = vbl + 2 * L;                                     // hidden bias (D = 3)
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   uint16_t* scr = reinterpret_cast<uint16_t*>(lds + Lay::OFF_SCR + wave * Lay::SCR);
-  rs_copy_frags(W1f, a.mlp.lin[0].wf, NB, NKH, 3 * NKH, 0);
-  if constexpr (D == 3) rs_copy_frags(WHf, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
-  rs_copy_frags(WLf, a.mlp.lin[D - 1].wf, NB, NKH, NKH, 0);
-  rs_copy_frags(WLb, a.mlp.lin[D - 1].wb, NB, NKH, NKH, 0);
-  if constexpr (D == 3) rs_copy_frags(WHb, a.mlp.lin[1].wb, NB, NKH, NKH, 0);
-  rs_copy_frags(W1b, a.mlp.lin[0].wb, NB, NKH, NKH, 0);  // e block: the first NB column blocks
+  rt_copy_vec(vbl, a.mlp.lin[D - 1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  if constexpr (D == 3) rt_copy_vec(vbh, a.mlp.lin[1].b, L);
+  rs_copy_frags(W1f, a.mlp.lin[0].wf, NB, NKH, 3 * NKH, 0);  // B operand read from memory rows
+  if constexpr (D == 3) rt_copy_frags(WHf, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
+  rt_copy_frags(WLf, a.mlp.lin[D - 1].wf, NB, NKH, NKH, 0);
+  rt_copy_frags(WLb, a.mlp.lin[D - 1].wb, NB, NKH, NKH, 0);
+  if constexpr (D == 3) rt_copy_frags(WHb, a.mlp.lin[1].wb, NB, NKH, NKH, 0);
+  rt_copy_frags(W1b, a.mlp.lin[0].wb, NB, NKH, NKH, 0);  // e block: the first NB column blocks
   __syncthreads();
   int64_t r0, r1;
   rs_range(a.row_ptr, a.r_lo, a.r_hi, r0, r1);
   rs_zero_empty(a.row_ptr, r0, r1, a.dagg, L);
   const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
-  // column sums of the bias / LayerNorm gradients: each tile's 16-row sums
-  // (butterfly over the four row groups) are added here; lane group g keeps
-  // the column blocks g * NB/4 ..
-  constexpr int NQ = 2 + D;  // gamma, beta, last bias, hidden biases
-  constexpr int NG = NB / 4;
-  float qacc[NQ][NG];
+  // column totals of the bias / LayerNorm gradients (rt_col_totals' share of
+  // each lane): gamma, beta, last bias, hidden biases
+  constexpr int NQ = 2 + D;
+  float qacc[NQ][NR];
 #pragma unroll
-  for (int q = 0; q < NQ; ++q)
+  for (int k = 0; k < NQ; ++k)
 #pragma unroll
-    for (int j = 0; j < NG; ++j) qacc[q][j] = 0.f;
-  auto fold = [&](int q, float (&t)[NB], int grp) {
-#pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-      float x = t[cb];
-      x += __shfl_xor(x, 16, 64);
-      x += __shfl_xor(x, 32, 64);
-#pragma unroll
-      for (int j = 0; j < NG; ++j)
-        if (cb == grp * NG + j) qacc[q][j] += x;
-    }
-  };
+    for (int t = 0; t < NR; ++t) qacc[k][t] = 0.f;
   float run[(L + 63) / 64] = {};
-  RsMetaRaw nxt = rs_meta_load(a.erecv, a.send, E0, E1);
+  RsMetaRaw nxt = rt_meta_load(a.erecv, a.send, E0, E1);
   for (int64_t sb = E0; sb < E1; sb += 16) {
     // an opaque copy of the lane index, so that the lane-dependent addresses
     // are recomputed per tile instead of being hoisted into registers
     int ln = lane;
     asm volatile("" : "+v"(ln));
-    const int arow = ln & 15, ach = ln >> 4;
+    const int e = ln & 15, q = ln >> 4;
     const int n = (int)(E1 - sb < 16 ? E1 - sb : 16);
-    const RsMeta mt = rs_meta_make(nxt);
-    nxt = rs_meta_load(a.erecv, a.send, sb + 16, E1);
+    const bool ok = e < n;
+    const RsMeta mt = rt_meta_make(nxt);
+    nxt = rt_meta_load(a.erecv, a.send, sb + 16, E1);
+    const int64_t srow = (sb - a.e_base + e) * L;  // row of the stored gradients / activations
+    // rows past the tile's end repeat row 0 (dm = 0 there, so they add nothing)
+    const int64_t er = sb + (ok ? e : 0);
     uint4 ef[NKH];
 #pragma unroll
-    for (int kg = 0; kg < NKH; ++kg)
-      ef[kg] = arow < n ? *reinterpret_cast<const uint4*>(Ein + (sb + arow) * L + kg * 32 + ach * 8)
-                        : make_uint4(0, 0, 0, 0);
+    for (int kg = 0; kg < NKH; ++kg) ef[kg] = *reinterpret_cast<const uint4*>(Ein + er * L + kg * 32 + q * 8);
     floatx4 z[NB];
-    rs_first_layer<L>(ef, W1f, mt, n, a.proj, a.mlp.lin[0].b, z, ln);
+    rt_first_layer<L>(ef, W1f, mt, ok, a.proj, z, ln);
     uint32_t mask[2] = {0u, 0u};  // ReLU derivative of the hidden layers, bit cb * 4 + r
     float h[NB][4];
 #pragma unroll
@@ -1778,171 +1897,180 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
         h[cb][r] = on ? z[cb][r] : 0.f;
       }
     uint4 hf[NKH];
-    rs_to_frags<L>(h, scr, hf, ln);
-    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.hid[0]) + (sb - a.e_base) * L, scr, n, ln);
+    rt_frags<NB>(h, hf);
+    if (ok) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[0]) + srow, q, hf);
     if constexpr (D == 3) {
       floatx4 acc[NB];
-      rs_gemm<NB, NKH>(hf, WHf, acc, ln);
+      rt_gemm<NB, NKH>(WHf, hf, acc, ln);
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
-        const float bv = a.mlp.lin[1].b[cb * 16 + (ln & 15)];
+        const float4 bv = rt_ld4(vbh, cb, q);
+        const float b4[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float v = acc[cb][r] + bv;
+          const float v = acc[cb][r] + b4[r];
           const bool on = v > 0.f;
           mask[1] |= (on ? 1u : 0u) << (cb * 4 + r);
           h[cb][r] = on ? v : 0.f;
         }
       }
-      rs_to_frags<L>(h, scr, hf, ln);
-      rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.hid[1]) + (sb - a.e_base) * L, scr, n, ln);
+      rt_frags<NB>(h, hf);
+      if (ok) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[1]) + srow, q, hf);
     }
     float y[NB][4];
     {
       floatx4 acc[NB];
-      rs_gemm<NB, NKH>(hf, WLf, acc, ln);
+      rt_gemm<NB, NKH>(WLf, hf, acc, ln);
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
-        const float bv = a.mlp.lin[D - 1].b[cb * 16 + (ln & 15)];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) y[cb][r] = acc[cb][r] + bv;
+        const float4 bv = rt_ld4(vbl, cb, q);
+        y[cb][0] = acc[cb][0] + bv.x;
+        y[cb][1] = acc[cb][1] + bv.y;
+        y[cb][2] = acc[cb][2] + bv.z;
+        y[cb][3] = acc[cb][3] + bv.w;
       }
     }
-    // dm = dagg[receiver] + de^{k+1}, accumulator order
+    // dm = dagg[receiver] + de^{k+1}
     float dm[NB][4];
+    float4 d4[NB];  // de^{k+1}, kept for de^k
+    {
+      const float* gp = a.dagg + (int64_t)(ok ? mt.r : 0) * L;
+      float4 g4[NB];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = ((ln >> 4) * 4 + r);
-      const bool ok = row < n;
-      const int64_t rv = __shfl(mt.r, row, 64);
-      float de[NB];
-      if (ok && a.de_next) {
-        rs_load_row<L>(a.de_next + (sb + row) * L, ln & 15, de);
-      } else {
+      for (int cb = 0; cb < NB; ++cb) {
+        g4[cb] = rt_ld4(gp, cb, q);
+        d4[cb] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      if (a.de_next) {
 #pragma unroll
-        for (int cb = 0; cb < NB; ++cb) de[cb] = 0.f;
+        for (int cb = 0; cb < NB; ++cb) d4[cb] = rt_ld4(a.de_next + er * L, cb, q);
       }
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb) dm[cb][r] = (ok ? a.dagg[rv * L + cb * 16 + (ln & 15)] : 0.f) + de[cb];
+      for (int cb = 0; cb < NB; ++cb) {
+        dm[cb][0] = ok ? g4[cb].x + d4[cb].x : 0.f;
+        dm[cb][1] = ok ? g4[cb].y + d4[cb].y : 0.f;
+        dm[cb][2] = ok ? g4[cb].z + d4[cb].z : 0.f;
+        dm[cb][3] = ok ? g4[cb].w + d4[cb].w : 0.f;
+      }
     }
     // LayerNorm (recomputed): y becomes xhat
-    float mu[4], rs[4], t1[4], t2[4];
-    rs_row_totals<NB>(y, mu);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      mu[r] = mu[r] / L;
-      float x = 0.f;
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb) {
-        const float d = y[cb][r] - mu[r];
-        x += d * d;
-      }
-      rs[r] = x;
-    }
-    rs_butterfly(rs);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) rs[r] = 1.0f / sqrtf(rs[r] / L + a.eps);
-    // LayerNorm backward: dy = rstd (dm g - mean(dm g) - xhat mean(dm g xhat))
-#pragma unroll
-    for (int r = 0; r < 4; ++r) t1[r] = t2[r] = 0.f;
+    const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
+    float rs;
     {
-      float tg[NB], tb[NB];
+      float dv[NB][4];
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb) {
-        const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
-        tg[cb] = tb[cb] = 0.f;
+      for (int cb = 0; cb < NB; ++cb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          y[cb][r] = (y[cb][r] - mu[r]) * rs[r];
-          const float d = dm[cb][r] * g;
-          t1[r] += d;
-          t2[r] += d * y[cb][r];
-          tg[cb] += dm[cb][r] * y[cb][r];
-          tb[cb] += dm[cb][r];
+          const float d = y[cb][r] - mu;
+          dv[cb][r] = d * d;
+        }
+      rs = 1.0f / sqrtf(rt_sum4(rt_lane_sum<NB>(dv)) / L + a.eps);
+    }
+    // LayerNorm backward: dy = rstd (dm g - mean(dm g) - xhat mean(dm g xhat))
+    float t1, t2;
+    {
+      float d1[NB][4], d2[NB][4], tg[NV], tb[NV];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float4 g4 = rt_ld4(vg, cb, q);
+        const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          y[cb][r] = (y[cb][r] - mu) * rs;
+          const float d = dm[cb][r] * g[r];
+          d1[cb][r] = d;
+          d2[cb][r] = d * y[cb][r];
+          tg[cb * 4 + r] = dm[cb][r] * y[cb][r];
+          tb[cb * 4 + r] = dm[cb][r];
         }
       }
-      fold(0, tg, ln >> 4);
-      fold(1, tb, ln >> 4);
+      t1 = rt_sum4(rt_lane_sum<NB>(d1));
+      t2 = rt_sum4(rt_lane_sum<NB>(d2));
+      rt_col_totals<NV>(tg, e);
+      rt_col_totals<NV>(tb, e);
+#pragma unroll
+      for (int t = 0; t < NR; ++t) {
+        qacc[0][t] += tg[t];
+        qacc[1][t] += tb[t];
+      }
     }
-    rs_butterfly(t1);
-    rs_butterfly(t2);
     float v[NB][4];
     {
-      float tl[NB];
+      float tl[NV];
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
-        const float g = a.mlp.gamma[cb * 16 + (ln & 15)];
-        tl[cb] = 0.f;
+        const float4 g4 = rt_ld4(vg, cb, q);
+        const float g[4] = {g4.x, g4.y, g4.z, g4.w};
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float d = dm[cb][r] * g;
-          v[cb][r] = rs[r] * (d - t1[r] / L - y[cb][r] * (t2[r] / L));
-          tl[cb] += v[cb][r];
+          const float d = dm[cb][r] * g[r];
+          v[cb][r] = rs * (d - t1 / L - y[cb][r] * (t2 / L));
+          tl[cb * 4 + r] = v[cb][r];
         }
       }
-      fold(2, tl, ln >> 4);
+      rt_col_totals<NV>(tl, e);
+#pragma unroll
+      for (int t = 0; t < NR; ++t) qacc[2][t] += tl[t];
     }
     uint4 gf[NKH];
-    rs_to_frags<L>(v, scr, gf, ln);
-    rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + (sb - a.e_base) * L, scr, n, ln);
+    rt_frags<NB>(v, gf);
+    if (ok) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + srow, q, gf);
     // hidden layers: dz_{j-1} = (dz_j W_j) * [z_{j-1} > 0]
 #pragma unroll
     for (int j = D - 1; j >= 1; --j) {
       floatx4 acc[NB];
       if (j == D - 1) {
-        rs_gemm<NB, NKH>(gf, WLb, acc, ln);
+        rt_gemm<NB, NKH>(WLb, gf, acc, ln);
       } else {
-        if constexpr (D == 3) rs_gemm<NB, NKH>(gf, WHb, acc, ln);
+        if constexpr (D == 3) rt_gemm<NB, NKH>(WHb, gf, acc, ln);
       }
-      {
-        float th[NB];
+      float th[NV];
 #pragma unroll
-        for (int cb = 0; cb < NB; ++cb) {
-          th[cb] = 0.f;
+      for (int cb = 0; cb < NB; ++cb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            v[cb][r] = ((mask[j - 1] >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
-            th[cb] += v[cb][r];
-          }
+        for (int r = 0; r < 4; ++r) {
+          v[cb][r] = ((mask[j - 1] >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
+          th[cb * 4 + r] = v[cb][r];
         }
-        fold(3 + (j - 1), th, ln >> 4);
-      }
-      rs_to_frags<L>(v, scr, gf, ln);
-      rs_store_rows<L>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + (sb - a.e_base) * L, scr, n, ln);
+      rt_col_totals<NV>(th, e);
+#pragma unroll
+      for (int t = 0; t < NR; ++t) qacc[3 + (j - 1)][t] += th[t];
+      rt_frags<NB>(v, gf);
+      if (ok) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + srow, q, gf);
     }
     // edge-stream gradient: de^k = de^{k+1} + dz_0 W_1[:, e-block]
     {
       floatx4 acc[NB];
-      rs_gemm<NB, NKH>(gf, W1b, acc, ln);
+      rt_gemm<NB, NKH>(W1b, gf, acc, ln);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = ((ln >> 4) * 4 + r);
-        if (row < n) {
-          float v[NB], dn[NB];
-          if (a.de_next) {
-            rs_load_row<L>(a.de_next + (sb + row) * L, ln & 15, dn);
-          } else {
+      for (int cb = 0; cb < NB; ++cb) {
+        acc[cb][0] += d4[cb].x;
+        acc[cb][1] += d4[cb].y;
+        acc[cb][2] += d4[cb].z;
+        acc[cb][3] += d4[cb].w;
+      }
+      if (ok) {
+        float* op = a.de_out + (sb + e) * L;
 #pragma unroll
-            for (int cb = 0; cb < NB; ++cb) dn[cb] = 0.f;
-          }
-#pragma unroll
-          for (int cb = 0; cb < NB; ++cb) v[cb] = acc[cb][r] + dn[cb];
-          if (a.de_std) {
-#pragma unroll
-            for (int cb = 0; cb < NB; ++cb) a.de_out[(sb + row) * L + cb * 16 + (ln & 15)] = v[cb];
-          } else {
-            rs_store_row<L>(a.de_out + (sb + row) * L, ln & 15, v);
-          }
-        }
+        for (int cb = 0; cb < NB; ++cb)
+          *reinterpret_cast<float4*>(op + cb * 16 + q * 4) = make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
       }
     }
-    // receiver sums of dz_0 (bf16, as it fed the products), ascending edge order
+    // receiver sums of dz_0 (bf16, as it fed the products), ascending edge
+    // order, 64 columns at a time through the wave's scratch tile
 #pragma unroll
     for (int j = 0; j < (L + 63) / 64; ++j) {
       const int c = ln + 64 * j;
+#pragma unroll
+      for (int kg = 2 * j; kg < 2 * j + 2 && kg < NKH; ++kg) {
+        const int c0 = (kg - 2 * j) * 32 + q * 4;
+        *reinterpret_cast<uint2*>(scr + rs_sw16<64>(e, c0)) = make_uint2(gf[kg].x, gf[kg].y);
+        *reinterpret_cast<uint2*>(scr + rs_sw16<64>(e, c0 + 16)) = make_uint2(gf[kg].z, gf[kg].w);
+      }
       float x[16];
 #pragma unroll
-      for (int row = 0; row < 16; ++row) x[row] = bf2f(scr[rs_sw16<L>(row, c)]);
+      for (int row = 0; row < 16; ++row) x[row] = bf2f(scr[rs_sw16<64>(row, ln)]);
 #pragma unroll
       for (int row = 0; row < 16; ++row) {
         if (row < n) {
@@ -1955,20 +2083,22 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
       }
     }
   }
-  // column partials: the four 16-lane groups of each column, then the waves
-  // in order through LDS (the weight area is free now)
+  // column partials: lane (e, q)'s totals are columns 16 cb + 4 q + r for
+  // index e * NR + t = 4 cb + r; then the waves in order through LDS (the
+  // weight area is free now)
   __syncthreads();
   float* red = reinterpret_cast<float*>(lds);
   {
     float* rw = red + wave * Lay::NVEC;
 #pragma unroll
-    for (int j = 0; j < NG; ++j) {
-      const int col = ((lane >> 4) * NG + j) * 16 + (lane & 15);
+    for (int t = 0; t < NR; ++t) {
+      const int i = (lane & 15) * NR + t;
+      const int col = (i >> 2) * 16 + (lane >> 4) * 4 + (i & 3);
 #pragma unroll
-      for (int h = 0; h < D - 1; ++h) rw[h * L + col] = qacc[3 + h][j];
-      rw[(D - 1) * L + col] = qacc[2][j];
-      rw[D * L + col] = qacc[0][j];
-      rw[(D + 1) * L + col] = qacc[1][j];
+      for (int h = 0; h < D - 1; ++h) rw[h * L + col] = qacc[3 + h][t];
+      rw[(D - 1) * L + col] = qacc[2][t];
+      rw[D * L + col] = qacc[0][t];
+      rw[(D + 1) * L + col] = qacc[1][t];
     }
   }
   __syncthreads();
@@ -1980,9 +2110,9 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
   }
 }
 
-// P[n] = [W_s v_n | W_r v_n] for the local nodes: the sender and receiver
-// blocks of the edge MLP's first Linear on the bf16 block input (fp32 sums),
-// each half in lane-major column order.
+// P[n] = [W_s v_n | W_r v_n + b_1] for the local nodes (T form, plain
+// column order): the sender and receiver blocks of the edge MLP's first
+// Linear on the bf16 block input, fp32 sums.
 template <int L>
 __global__ __launch_bounds__(RS_NTH) void node_proj_kernel(const uint16_t* __restrict__ V16, int64_t n_local, Lin w1,
                                                            float* __restrict__ proj) {
@@ -1994,31 +2124,37 @@ __global__ __launch_bounds__(RS_NTH) void node_proj_kernel(const uint16_t* __res
   rs_copy_frags(WS, w1.wf, NB, NKH, 3 * NKH, NKH);
   rs_copy_frags(WR, w1.wf, NB, NKH, 3 * NKH, 2 * NKH);
   __syncthreads();
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   const int64_t ntiles = (n_local + 15) / 16;
   for (int64_t t = (int64_t)blockIdx.x * RS_NWV + wave; t < ntiles; t += (int64_t)gridDim.x * RS_NWV) {
     int ln = lane;
     asm volatile("" : "+v"(ln));
-    const int arow = ln & 15, ach = ln >> 4;
-    const int64_t n0 = t * 16;
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t node = t * 16 + e;
+    const bool ok = node < n_local;
+    const int64_t src = ok ? node : t * 16;  // rows past the end repeat the tile's first row (not stored)
     uint4 vf[NKH];
 #pragma unroll
-    for (int kg = 0; kg < NKH; ++kg)
-      vf[kg] = n0 + arow < n_local ? *reinterpret_cast<const uint4*>(V16 + (n0 + arow) * L + kg * 32 + ach * 8)
-                                   : make_uint4(0, 0, 0, 0);
+    for (int kg = 0; kg < NKH; ++kg) vf[kg] = *reinterpret_cast<const uint4*>(V16 + src * L + kg * 32 + q * 8);
 #pragma unroll
     for (int side = 0; side < 2; ++side) {
       floatx4 acc[NB];
-      rs_gemm<NB, NKH>(vf, side == 0 ? WS : WR, acc, ln);
+      rt_gemm<NB, NKH>(side == 0 ? WS : WR, vf, acc, ln);
+      if (side == 1) {  // the first Linear's bias rides with the receiver half
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t node = n0 + (ln >> 4) * 4 + r;
-        if (node < n_local) {
-          float v[NB];
-#pragma unroll
-          for (int cb = 0; cb < NB; ++cb) v[cb] = acc[cb][r];
-          rs_store_row<L>(proj + node * (2 * L) + side * L, ln & 15, v);
+        for (int cb = 0; cb < NB; ++cb) {
+          const float4 bv = rt_ld4(w1.b, cb, q);
+          acc[cb][0] += bv.x;
+          acc[cb][1] += bv.y;
+          acc[cb][2] += bv.z;
+          acc[cb][3] += bv.w;
         }
+      }
+      if (ok) {
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+          *reinterpret_cast<float4*>(proj + node * (2 * L) + side * L + cb * 16 + q * 4) =
+              make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
       }
     }
   }
@@ -2074,7 +2210,7 @@ __global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
   uint4* W2f = reinterpret_cast<uint4*>(lds);
   uint4* W2b = reinterpret_cast<uint4*>(lds + W);
   uint4* W1 = reinterpret_cast<uint4*>(lds + Lay::OFF_W1);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   uint16_t* scr = reinterpret_cast<uint16_t*>(lds + Lay::OFF_SCR + wave * Lay::SCR);
   rs_copy_frags(W2f, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
   rs_copy_frags(W2b, a.mlp.lin[1].wb, NB, NKH, NKH, 0);
@@ -2978,7 +3114,7 @@ template <int L, int D>
 static hipError_t edge_fwd_rs_t(const EdgeFwdArgs& a, hipStream_t st) {
   using Lay = RsFwdLay<L, D>;
   allow_lds(edge_fwd_rs_kernel<L, D>, Lay::END);
-  hipLaunchKernelGGL((edge_fwd_rs_kernel<L, D>), dim3(RS_GRID), dim3(RS_NTH), Lay::END, st, a);
+  hipLaunchKernelGGL((edge_fwd_rs_kernel<L, D>), dim3(RS_GRID), dim3(Lay::NTH), Lay::END, st, a);
   return hipGetLastError();
 }
 
