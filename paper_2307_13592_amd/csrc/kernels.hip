@@ -1505,13 +1505,36 @@ __device__ __forceinline__ void rt_frags(const float (&v)[NB][4], uint4 (&f)[NB 
                        bf_pack(v[2 * kg + 1][0], v[2 * kg + 1][1]), bf_pack(v[2 * kg + 1][2], v[2 * kg + 1][3]));
 }
 
-// The values of rt_frags -> one plain-order bf16 row (lane group q's columns).
+// T-order bf16 of one k-group -> plain order.  In: lane group q holds
+// columns 32 kg + 4 q .. +3 (x, y) and 32 kg + 16 + 4 q .. +3 (z, w).  Out:
+// columns 32 kg + 8 q .. +7, one 16-byte row chunk.  A lane swap between the
+// group pairs (0, 1) <-> (2, 3), then one between groups 0 <-> 1 and 2 <-> 3.
+__device__ __forceinline__ uint4 rt_to_plain(const uint4 f) {
+  const auto s0 = __builtin_amdgcn_permlane32_swap(f.x, f.z, false, false);
+  const auto s1 = __builtin_amdgcn_permlane32_swap(f.y, f.w, false, false);
+  const auto t0 = __builtin_amdgcn_permlane16_swap(s0[0], s0[1], false, false);
+  const auto t1 = __builtin_amdgcn_permlane16_swap(s1[0], s1[1], false, false);
+  return make_uint4(t0[0], t1[0], t0[1], t1[1]);
+}
+// Inverse of rt_to_plain (both swaps are involutions, applied in reverse).
+__device__ __forceinline__ uint4 rt_from_plain(const uint4 p) {
+  const auto t0 = __builtin_amdgcn_permlane16_swap(p.x, p.z, false, false);
+  const auto t1 = __builtin_amdgcn_permlane16_swap(p.y, p.w, false, false);
+  const auto s0 = __builtin_amdgcn_permlane32_swap(t0[0], t0[1], false, false);
+  const auto s1 = __builtin_amdgcn_permlane32_swap(t1[0], t1[1], false, false);
+  return make_uint4(s0[0], s1[0], s0[1], s1[1]);
+}
+
+// The values of rt_frags -> one plain-order bf16 row, 16 bytes per lane and
+// k-group.  All lanes take part in the swaps; only lanes with ok store.
 template <int NKH>
-__device__ __forceinline__ void rt_store_frags(uint16_t* __restrict__ row, int q, const uint4 (&f)[NKH]) {
+__device__ __forceinline__ void rt_store_frags(uint16_t* __restrict__ row, int q, const uint4 (&f)[NKH], bool ok) {
+  uint4 p[NKH];
 #pragma unroll
-  for (int kg = 0; kg < NKH; ++kg) {
-    *reinterpret_cast<uint2*>(row + kg * 32 + q * 4) = make_uint2(f[kg].x, f[kg].y);
-    *reinterpret_cast<uint2*>(row + kg * 32 + 16 + q * 4) = make_uint2(f[kg].z, f[kg].w);
+  for (int kg = 0; kg < NKH; ++kg) p[kg] = rt_to_plain(f[kg]);
+  if (ok) {
+#pragma unroll
+    for (int kg = 0; kg < NKH; ++kg) *reinterpret_cast<uint4*>(row + kg * 32 + q * 8) = p[kg];
   }
 }
 
@@ -1657,8 +1680,8 @@ struct RsFwdLay {
   static constexpr int OFF_W1 = 0, OFF_WH = W, OFF_WL = (D - 1) * W, OFF_VEC = D * W;
   static constexpr int NVEC = (D == 3 ? 4 : 3) * L;
   static constexpr int OFF_SCR = OFF_VEC + NVEC * 4;
-  // waves per workgroup: l = 64 fits 16 (at most 128 registers each), l = 128 12 (168)
-  static constexpr int NWV = L == 64 ? 16 : 12;
+  // 16 waves per workgroup (at most 128 registers each)
+  static constexpr int NWV = 16;
   static constexpr int NTH = 64 * NWV;
   static constexpr int END = OFF_SCR + NWV * SCR;
   static_assert(END <= 160 * 1024, "LDS");
@@ -1747,11 +1770,13 @@ __global__ __launch_bounds__((RsFwdLay<L, D>::NTH)) void edge_fwd_rs_kernel(Edge
       y[cb][2] = acc[cb][2] + bv.z;
       y[cb][3] = acc[cb][3] + bv.w;
     }
-    // e^k again in T order (4 columns per block) for the residual
+    // e^k in T order (4 columns per block) for the residual
     uint2 ev[NB];
-    if (Eout) {
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb) ev[cb] = *reinterpret_cast<const uint2*>(erow + cb * 16 + q * 4);
+    for (int kg = 0; kg < NKH; ++kg) {
+      const uint4 t = rt_from_plain(ef[kg]);
+      ev[2 * kg] = make_uint2(t.x, t.y);
+      ev[2 * kg + 1] = make_uint2(t.z, t.w);
     }
     // LayerNorm: two-pass statistics of row e, then gamma * xhat + beta
     const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
@@ -1777,10 +1802,16 @@ __global__ __launch_bounds__((RsFwdLay<L, D>::NTH)) void edge_fwd_rs_kernel(Edge
       ev[cb] = make_uint2(bf_pack(__uint_as_float(w.x << 16) + y[cb][0], __uint_as_float(w.x & 0xffff0000u) + y[cb][1]),
                           bf_pack(__uint_as_float(w.y << 16) + y[cb][2], __uint_as_float(w.y & 0xffff0000u) + y[cb][3]));
     }
-    if (Eout && ok) {
-      uint16_t* orow = Eout + (sb + e) * L;
+    if (Eout) {
+      uint4 o[NKH];
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb) *reinterpret_cast<uint2*>(orow + cb * 16 + q * 4) = ev[cb];
+      for (int kg = 0; kg < NKH; ++kg)
+        o[kg] = rt_to_plain(make_uint4(ev[2 * kg].x, ev[2 * kg].y, ev[2 * kg + 1].x, ev[2 * kg + 1].y));
+      if (ok) {
+        uint16_t* orow = Eout + (sb + e) * L;
+#pragma unroll
+        for (int kg = 0; kg < NKH; ++kg) *reinterpret_cast<uint4*>(orow + kg * 32 + q * 8) = o[kg];
+      }
     }
     // ordered receiver sums, 64 columns at a time through the wave's scratch
     // tile; a segment's total goes out at its last row
@@ -1898,7 +1929,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
       }
     uint4 hf[NKH];
     rt_frags<NB>(h, hf);
-    if (ok) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[0]) + srow, q, hf);
+    rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[0]) + srow, q, hf, ok);
     if constexpr (D == 3) {
       floatx4 acc[NB];
       rt_gemm<NB, NKH>(WHf, hf, acc, ln);
@@ -1915,7 +1946,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
         }
       }
       rt_frags<NB>(h, hf);
-      if (ok) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[1]) + srow, q, hf);
+      rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[1]) + srow, q, hf, ok);
     }
     float y[NB][4];
     {
@@ -2015,7 +2046,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
     }
     uint4 gf[NKH];
     rt_frags<NB>(v, gf);
-    if (ok) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + srow, q, gf);
+    rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + srow, q, gf, ok);
     // hidden layers: dz_{j-1} = (dz_j W_j) * [z_{j-1} > 0]
 #pragma unroll
     for (int j = D - 1; j >= 1; --j) {
@@ -2037,7 +2068,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
 #pragma unroll
       for (int t = 0; t < NR; ++t) qacc[3 + (j - 1)][t] += th[t];
       rt_frags<NB>(v, gf);
-      if (ok) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + srow, q, gf);
+      rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + srow, q, gf, ok);
     }
     // edge-stream gradient: de^k = de^{k+1} + dz_0 W_1[:, e-block]
     {
