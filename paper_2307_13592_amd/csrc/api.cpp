@@ -246,6 +246,7 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
       part = std::max(part, (size_t)dw_splits(R, Ln.out, Ln.in) * Ln.out * Ln.in);
     }
   }
+  part = std::max(part, (size_t)dw_stream_parts() * 16384);
   p.PART = take(4 * part);
   int nvec = 0;
   for (const MlpL& ml : m->mlp) nvec = std::max(nvec, ml.nvec);
@@ -610,6 +611,7 @@ hipError_t run_dw(mgn_model* m, const LinL& L, DwArgs a, float* d_params, int ac
     return hipSuccess;
   }
   Timed t_(m, MGN_T_WEIGHT_GRAD, st);
+  if (dw_stream_ok(m->prec, a)) return launch_dw_stream(a, dst, L.in, accumulate, st);
   hipError_t e = launch_dw(m->prec, a, st);
   if (e == hipSuccess) e = launch_dw_reduce(a.part, a.S, a.O, a.I, dst, L.in, accumulate, st);
   return e;

@@ -155,6 +155,12 @@ hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t s
 // assigned (first) or added into dzs.
 hipError_t launch_sender_sums(int prec, int L, const int32_t* trow, const int32_t* tedge, const void* dz, int64_t e_lo,
                               int64_t e_hi, int64_t n_local, float* dzs, int first, hipStream_t st);
+// Register-resident weight gradient for bf16 layers with 128 inputs and 128
+// outputs over many rows (dw_stream_ok); part needs dw_stream_parts() * 16384
+// floats; writes (or adds to) dst[o * ldw + i].
+int dw_stream_parts();
+bool dw_stream_ok(int prec, const DwArgs& a);
+hipError_t launch_dw_stream(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st);
 hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st);
 hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int ldw, int accumulate,
                             hipStream_t st);

@@ -2832,6 +2832,116 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void dw
       }
 }
 
+// ------------------------------------- weight gradients, register-resident ---
+// dW = D^T A for bf16 row-major D [R][ldd] and A [R][lda], 128 columns each
+// (the per-edge layers of the row-split path at l = 128), without LDS or
+// barriers.  One wave per SIMD; each wave reduces a contiguous range of rows
+// into a 128 x 128 fp32 tile held in the accumulator registers.  Per 32 rows,
+// lane (q, m) = (lane >> 4, lane & 15) loads rows 8 q .. 8 q + 7, columns
+// 8 m .. 8 m + 7 of both operands (16-byte loads: a wave instruction reads four
+// whole rows), transposes each 8 x 8 block in registers into eight
+// k-fragments (one column, eight consecutive rows) and issues 64 MFMAs:
+// fragment j of lane (q, m) is column 8 m + j, so accumulator block (j, j')
+// holds dW[8 m' + j][8 n + j'] at (row m', column n) of its 16 x 16 tile.
+constexpr int DWS_NT = 256;
+constexpr int DWS_GRID = 256;
+constexpr int DWS_WAVES = DWS_GRID * DWS_NT / 64;
+
+// v[r][k]: row r, columns 2k (low half) and 2k + 1 -> f[c][p]: column c, rows
+// 2p (low half) and 2p + 1.
+__device__ __forceinline__ void dws_transpose(const uint32_t (&v)[8][4], uint32_t (&f)[8][4]) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      f[2 * k][p] = __builtin_amdgcn_perm(v[2 * p + 1][k], v[2 * p][k], 0x05040100u);
+      f[2 * k + 1][p] = __builtin_amdgcn_perm(v[2 * p + 1][k], v[2 * p][k], 0x07060302u);
+    }
+}
+
+__device__ __forceinline__ void dws_load(const uint16_t* __restrict__ X, int ldx, int64_t row, int64_t R, int col,
+                                         uint32_t (&v)[8][4]) {
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    uint4 t = make_uint4(0, 0, 0, 0);
+    if (row + r < R) t = *reinterpret_cast<const uint4*>(X + (row + r) * ldx + col);
+    v[r][0] = t.x;
+    v[r][1] = t.y;
+    v[r][2] = t.z;
+    v[r][3] = t.w;
+  }
+}
+
+__device__ __forceinline__ void dws_mma(const uint32_t (&fd)[8][4], const uint32_t (&fa)[8][4], floatx4 (&acc)[8][8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj)
+      PBF16::mma(acc[j][jj], make_uint4(fd[j][0], fd[j][1], fd[j][2], fd[j][3]),
+                 make_uint4(fa[jj][0], fa[jj][1], fa[jj][2], fa[jj][3]));
+}
+
+// part[w] (16384 floats, accumulator order [j][j'][lane][4]) = wave w's sum.
+__global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void dw_stream_kernel(
+    const uint16_t* __restrict__ D, int ldd, const uint16_t* __restrict__ A, int lda, int64_t R,
+    float* __restrict__ part) {
+  const int lane = threadIdx.x & 63, q = lane >> 4, m = lane & 15;
+  const int64_t w = (int64_t)blockIdx.x * (DWS_NT / 64) + wave_id();
+  const int64_t nw = (int64_t)gridDim.x * (DWS_NT / 64);
+  const int64_t steps = (R + 31) / 32;
+  const int64_t s0 = steps * w / nw, s1 = steps * (w + 1) / nw;  // this wave's 32-row steps
+  floatx4 acc[8][8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) acc[j][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // the next step's loads reuse the source registers once they are
+  // transposed, so they are in flight during the current step's products
+  uint32_t dv[8][4], av[8][4], fd[8][4], fa[8][4];
+  const int64_t rq = 8 * q;
+  if (s0 < s1) {
+    dws_load(D, ldd, s0 * 32 + rq, R, 8 * m, dv);
+    dws_load(A, lda, s0 * 32 + rq, R, 8 * m, av);
+  }
+  for (int64_t st = s0; st < s1; ++st) {
+    dws_transpose(dv, fd);
+    dws_transpose(av, fa);
+    if (st + 1 < s1) {
+      dws_load(D, ldd, (st + 1) * 32 + rq, R, 8 * m, dv);
+      dws_load(A, lda, (st + 1) * 32 + rq, R, 8 * m, av);
+    }
+    dws_mma(fd, fa, acc);
+  }
+  float4* out = reinterpret_cast<float4*>(part + w * 16384);
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj)
+      out[(j * 8 + jj) * 64 + lane] = make_float4(acc[j][jj][0], acc[j][jj][1], acc[j][jj][2], acc[j][jj][3]);
+}
+
+// dst[o * ldw + i] (+)= sum over the S wave partials, in wave order within
+// each of four interleaved sets, combined in set order; entry x of a partial
+// is (j, j', lane, r) -> o = 8 (4 (lane >> 4) + r) + j, i = 8 (lane & 15) + j'.
+__global__ __launch_bounds__(NT) void dw_stream_reduce_kernel(const float* __restrict__ part, int S,
+                                                              float* __restrict__ dst, int ldw, int accumulate) {
+  __shared__ float sh[NT];
+  const int jx = threadIdx.x & 63, qq = threadIdx.x >> 6;
+  const int x = blockIdx.x * 64 + jx;
+  float t = 0.f;
+#pragma unroll 8
+  for (int k = qq; k < S; k += 4) t += part[(int64_t)k * 16384 + x];
+  sh[threadIdx.x] = t;
+  __syncthreads();
+  if (qq == 0) {
+    const float t4 = ((sh[jx] + sh[64 + jx]) + sh[128 + jx]) + sh[192 + jx];
+    const int blk = x >> 8, ln = (x >> 2) & 63, r = x & 3;
+    const int o = 8 * (4 * (ln >> 4) + r) + (blk >> 3), i = 8 * (ln & 15) + (blk & 7);
+    float* d = dst + (int64_t)o * ldw + i;
+    *d = (accumulate ? *d : 0.f) + t4;
+  }
+}
+
 // dst[o * ldw + i] (+)= sum over the S split partials of part[.][o][i]: 64
 // outputs per workgroup, four threads per output each summing the splits
 // k = q (mod 4) in increasing k, combined in q order.
@@ -3258,6 +3368,24 @@ hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((dw_kernel<BF16, true>), grid, dim3(NT), 0, st, a);
   else
     hipLaunchKernelGGL((dw_kernel<BF16, false>), grid, dim3(NT), 0, st, a);
+  return hipGetLastError();
+}
+
+int dw_stream_parts() { return DWS_WAVES; }
+
+bool dw_stream_ok(int prec, const DwArgs& a) {
+  return prec == BF16 && a.a_kind == 0 && a.d_kind == 0 && a.O == 128 && a.I == 128 && a.ldd % 8 == 0 &&
+         a.lda0 % 8 == 0 && a.R >= 8192;
+}
+
+hipError_t launch_dw_stream(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st) {
+  hipLaunchKernelGGL(dw_stream_kernel, dim3(DWS_GRID), dim3(DWS_NT), 0, st,
+                     reinterpret_cast<const uint16_t*>(a.delta), a.ldd, reinterpret_cast<const uint16_t*>(a.a0),
+                     a.lda0, a.R, a.part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(dw_stream_reduce_kernel, dim3(16384 / 64), dim3(NT), 0, st, a.part, DWS_WAVES, dst, ldw,
+                     accumulate);
   return hipGetLastError();
 }
 
