@@ -2470,7 +2470,7 @@ __global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
 // values whose sum is within 2^-17 of it (relative).
 template <class P, int L>
 struct InGradTile {
-  static constexpr int TM = L <= 128 ? 64 : 32;                       // nodes per workgroup
+  static constexpr int TM = 32;                                      // nodes per workgroup
   static constexpr int LDT = L + P::PAD;
   static constexpr int NOP = sizeof(typename P::T) == 2 ? 4 : 2;     // operand tiles: (hi, lo) x (r, s)
   static constexpr int END = NOP * TM * LDT * (int)sizeof(typename P::T);
@@ -2528,24 +2528,23 @@ __global__ __launch_bounds__(NT) void input_grad_kernel(InGradArgs a) {
 #pragma unroll
     for (int j = 0; j < E16; ++j) s[j] = 0.f;
     if (node < a.n_local) {
-      int32_t i = a.trow[node];
+      // up to IG_FLIGHT rows in flight per thread, summed in ascending edge order
+      constexpr int IG_FLIGHT = 16;
       const int32_t end = a.trow[node + 1];
-      for (; i + 4 <= end; i += 4) {
-        uint4 v[4];
+      for (int32_t i = a.trow[node]; i < end; i += IG_FLIGHT) {
+        uint4 v[IG_FLIGHT];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const uint4*>(dz + (int64_t)a.tedge[i + u] * L + c);
+        for (int u = 0; u < IG_FLIGHT; ++u)
+          v[u] = i + u < end ? *reinterpret_cast<const uint4*>(dz + (int64_t)a.tedge[i + u] * L + c)
+                             : make_uint4(0, 0, 0, 0);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const T* t = reinterpret_cast<const T*>(&v[u]);
+        for (int u = 0; u < IG_FLIGHT; ++u) {
+          if (i + u < end) {
+            const T* t = reinterpret_cast<const T*>(&v[u]);
 #pragma unroll
-          for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
+            for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
+          }
         }
-      }
-      for (; i < end; ++i) {
-        const uint4 v = *reinterpret_cast<const uint4*>(dz + (int64_t)a.tedge[i] * L + c);
-        const T* t = reinterpret_cast<const T*>(&v);
-#pragma unroll
-        for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
       }
     }
 #pragma unroll
@@ -2620,11 +2619,26 @@ __global__ __launch_bounds__(NT) void sender_sums_kernel(const int32_t* __restri
   float s[E16];
 #pragma unroll
   for (int j = 0; j < E16; ++j) s[j] = 0.f;
-  for (int32_t i = lo; i < trow[node + 1] && tedge[i] < e_hi; ++i) {
-    const uint4 v = *reinterpret_cast<const uint4*>(dz + (int64_t)(tedge[i] - e_lo) * L + c);
-    const T* t = reinterpret_cast<const T*>(&v);
+  // up to 16 rows in flight, summed in ascending edge order
+  const int32_t nend = trow[node + 1];
+  for (int32_t i = lo; i < nend; i += 16) {
+    int32_t ed[16];
 #pragma unroll
-    for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
+    for (int u = 0; u < 16; ++u) ed[u] = i + u < nend ? tedge[i + u] : INT32_MAX;
+    uint4 v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      v[u] = ed[u] < e_hi ? *reinterpret_cast<const uint4*>(dz + (int64_t)(ed[u] - e_lo) * L + c)
+                          : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      if (ed[u] < e_hi) {
+        const T* t = reinterpret_cast<const T*>(&v[u]);
+#pragma unroll
+        for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
+      }
+    }
+    if (ed[15] >= e_hi) break;
   }
   float* d = dzs + node * L + c;
 #pragma unroll
