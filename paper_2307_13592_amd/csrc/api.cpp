@@ -219,8 +219,9 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.V = take(4 * (size_t)(p.lean ? 2 : K + 1) * no * L);
   // bf16 mode: bf16 copy of every block's node input, owned then halo rows
   p.V16 = m->prec == BF16 ? take(2 * (size_t)(K + 1) * nl * L) : 0;
-  // row-split edge kernels: node projections of the current block input
-  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)nl * 2 * L) : 0;
+  // row-split edge kernels: node projections of every block's input (kept for
+  // the backward), or of the current block only (checkpointing)
+  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(p.lean ? 1 : K) * nl * 2 * L) : 0;
   p.AGG = take(4 * (size_t)(p.lean ? 1 : K) * no * L);
   // edge stream: every block's input, or the checkpoints plus one working copy
   p.ES = take(ts * (size_t)(p.lean ? p.nck + 1 : std::max<int64_t>(K, 1)) * ne * L);
@@ -433,6 +434,11 @@ namespace {
 // The edge half of block k forward: node projections (row-split path), then
 // the fused edge kernel: e^{k+1} = e^k + m into eout (may equal ein, or be
 // null), ordered receiver sums into agg.
+// Node projections of block k (one shared slot when checkpointing).
+float* proj_block(const WsPlan& p, char* ws, int k, int64_t nl, int L) {
+  return (float*)(ws + p.PROJ) + (p.lean ? 0 : (size_t)k * nl * 2 * L);
+}
+
 hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p, char* ws, const float* halo, int k,
                               float* v, void* v16, const void* ein, void* eout, float* agg, hipStream_t st) {
   const int64_t no = g.n_owned, nh = g.n_halo;
@@ -454,11 +460,12 @@ hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p,
   ea.agg = agg;
   ea.eps = m->cfg.ln_eps;
   const bool rs = edge_rs(m->prec, L, D);
-  ea.proj = rs ? (const float*)(ws + p.PROJ) : nullptr;
+  float* proj = rs ? proj_block(p, ws, k, no + nh, L) : nullptr;
+  ea.proj = proj;
   hipError_t e = hipSuccess;
   if (rs) {
     Timed t_(m, MGN_T_NODE_PROJ, st);
-    e = launch_node_proj(L, v16, no + nh, ea.mlp.lin[0], (float*)(ws + p.PROJ), st);
+    e = launch_node_proj(L, v16, no + nh, ea.mlp.lin[0], proj, st);
     if (e != hipSuccess) return e;
   }
   Timed t_(m, MGN_T_EDGE_FWD, st);
@@ -795,12 +802,8 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.dagg = DAGG;
       a.de_out = DE;
       const bool rs = edge_rs(m->prec, L, D);
-      a.proj = rs ? (const float*)(ws + p.PROJ) : nullptr;
-      if (rs && no > 0 && !p.lean) {  // (the aggregate recompute made them already)
-        Timed t_(m, MGN_T_NODE_PROJ, st);
-        e = launch_node_proj(L, V16(k), no + nh, a.mlp.lin[0], (float*)(ws + p.PROJ), st);
-        CHK("node projections");
-      }
+      // the forward's projections of block k (or those of the aggregate recompute)
+      a.proj = rs ? proj_block(p, ws, k, no + nh, L) : nullptr;
       for (int j = 0; j < 3; ++j) a.delta[j] = DEL_E[j];
       for (int j = 0; j < 2; ++j) a.hid[j] = HID_E[j];
       a.vpart = VP;
