@@ -2895,9 +2895,37 @@ __device__ __forceinline__ void dws_mma(const uint32_t (&fd)[8][4], const uint32
                  make_uint4(fa[jj][0], fa[jj][1], fa[jj][2], fa[jj][3]));
 }
 
+// fp32 delta rows: 8 rows x 8 columns -> the bf16 hi and lo parts (x = hi +
+// lo within 2^-17 relative), each as v[r][k] of dws_transpose.
+__device__ __forceinline__ void dws_load_f32(const float* __restrict__ X, int ldx, int64_t row, int64_t R, int col,
+                                             float4 (&v)[8][2]) {
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    v[r][0] = v[r][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (row + r < R) {
+      v[r][0] = *reinterpret_cast<const float4*>(X + (row + r) * ldx + col);
+      v[r][1] = *reinterpret_cast<const float4*>(X + (row + r) * ldx + col + 4);
+    }
+  }
+}
+__device__ __forceinline__ void dws_split(const float4 (&v)[8][2], uint32_t (&hi)[8][4], uint32_t (&lo)[8][4]) {
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const float x[8] = {v[r][0].x, v[r][0].y, v[r][0].z, v[r][0].w, v[r][1].x, v[r][1].y, v[r][1].z, v[r][1].w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint16_t h0 = f2bf(x[2 * k]), h1 = f2bf(x[2 * k + 1]);
+      hi[r][k] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+      lo[r][k] = (uint32_t)f2bf(x[2 * k] - bf2f(h0)) | ((uint32_t)f2bf(x[2 * k + 1] - bf2f(h1)) << 16);
+    }
+  }
+}
+
 // part[w] (16384 floats, accumulator order [j][j'][lane][4]) = wave w's sum.
+// SPLIT: D is fp32 and enters the products as hi + lo (two MFMAs each).
+template <bool SPLIT>
 __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void dw_stream_kernel(
-    const uint16_t* __restrict__ D, int ldd, const uint16_t* __restrict__ A, int lda, int64_t R,
+    const void* __restrict__ Dv, int ldd, const uint16_t* __restrict__ A, int lda, int64_t R,
     float* __restrict__ part) {
   const int lane = threadIdx.x & 63, q = lane >> 4, m = lane & 15;
   const int64_t w = (int64_t)blockIdx.x * (DWS_NT / 64) + wave_id();
@@ -2909,22 +2937,46 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
   for (int j = 0; j < 8; ++j)
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) acc[j][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int64_t rq = 8 * q;
   // the next step's loads reuse the source registers once they are
   // transposed, so they are in flight during the current step's products
-  uint32_t dv[8][4], av[8][4], fd[8][4], fa[8][4];
-  const int64_t rq = 8 * q;
-  if (s0 < s1) {
-    dws_load(D, ldd, s0 * 32 + rq, R, 8 * m, dv);
-    dws_load(A, lda, s0 * 32 + rq, R, 8 * m, av);
-  }
-  for (int64_t st = s0; st < s1; ++st) {
-    dws_transpose(dv, fd);
-    dws_transpose(av, fa);
-    if (st + 1 < s1) {
-      dws_load(D, ldd, (st + 1) * 32 + rq, R, 8 * m, dv);
-      dws_load(A, lda, (st + 1) * 32 + rq, R, 8 * m, av);
+  if constexpr (SPLIT) {
+    const float* D = reinterpret_cast<const float*>(Dv);
+    float4 dv[8][2];
+    uint32_t av[8][4], fa[8][4];
+    if (s0 < s1) {
+      dws_load_f32(D, ldd, s0 * 32 + rq, R, 8 * m, dv);
+      dws_load(A, lda, s0 * 32 + rq, R, 8 * m, av);
     }
-    dws_mma(fd, fa, acc);
+    for (int64_t st = s0; st < s1; ++st) {
+      uint32_t hi[8][4], lo[8][4], f[8][4];
+      dws_split(dv, hi, lo);
+      dws_transpose(av, fa);
+      if (st + 1 < s1) {
+        dws_load_f32(D, ldd, (st + 1) * 32 + rq, R, 8 * m, dv);
+        dws_load(A, lda, (st + 1) * 32 + rq, R, 8 * m, av);
+      }
+      dws_transpose(hi, f);
+      dws_mma(f, fa, acc);
+      dws_transpose(lo, f);
+      dws_mma(f, fa, acc);
+    }
+  } else {
+    const uint16_t* D = reinterpret_cast<const uint16_t*>(Dv);
+    uint32_t dv[8][4], av[8][4], fd[8][4], fa[8][4];
+    if (s0 < s1) {
+      dws_load(D, ldd, s0 * 32 + rq, R, 8 * m, dv);
+      dws_load(A, lda, s0 * 32 + rq, R, 8 * m, av);
+    }
+    for (int64_t st = s0; st < s1; ++st) {
+      dws_transpose(dv, fd);
+      dws_transpose(av, fa);
+      if (st + 1 < s1) {
+        dws_load(D, ldd, (st + 1) * 32 + rq, R, 8 * m, dv);
+        dws_load(A, lda, (st + 1) * 32 + rq, R, 8 * m, av);
+      }
+      dws_mma(fd, fa, acc);
+    }
   }
   float4* out = reinterpret_cast<float4*>(part + w * 16384);
 #pragma unroll
@@ -3388,14 +3440,17 @@ hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st) {
 int dw_stream_parts() { return DWS_WAVES; }
 
 bool dw_stream_ok(int prec, const DwArgs& a) {
-  return prec == BF16 && a.a_kind == 0 && a.d_kind == 0 && a.O == 128 && a.I == 128 && a.ldd % 8 == 0 &&
-         a.lda0 % 8 == 0 && a.R >= 8192;
+  return prec == BF16 && a.a_kind == 0 && (a.d_kind == 0 || a.d_kind == 1) && a.O == 128 && a.I == 128 &&
+         a.ldd % 8 == 0 && a.lda0 % 8 == 0 && a.R >= 8192;
 }
 
 hipError_t launch_dw_stream(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st) {
-  hipLaunchKernelGGL(dw_stream_kernel, dim3(DWS_GRID), dim3(DWS_NT), 0, st,
-                     reinterpret_cast<const uint16_t*>(a.delta), a.ldd, reinterpret_cast<const uint16_t*>(a.a0),
-                     a.lda0, a.R, a.part);
+  if (a.d_kind == 1)
+    hipLaunchKernelGGL(dw_stream_kernel<true>, dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd,
+                       reinterpret_cast<const uint16_t*>(a.a0), a.lda0, a.R, a.part);
+  else
+    hipLaunchKernelGGL(dw_stream_kernel<false>, dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd,
+                       reinterpret_cast<const uint16_t*>(a.a0), a.lda0, a.R, a.part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(dw_stream_reduce_kernel, dim3(16384 / 64), dim3(NT), 0, st, a.part, DWS_WAVES, dst, ldw,
