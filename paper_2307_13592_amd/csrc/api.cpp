@@ -37,7 +37,7 @@ struct MlpL {
 
 struct WsPlan {
   size_t erecv, chunk, unit_r, nunits, V, V16, PROJ, AGG, ES, DV[2], DAGG, DZS, DE, DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
-      PART, VPART, total;
+      HID_NK, PART, VPART, total;
   int64_t max_units;
   // edge-stream checkpointing: interval s (0: every block kept), checkpoints
   bool lean = false;
@@ -234,6 +234,9 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   for (int j = 0; j < 2; ++j) p.HID_E[j] = j < m->D - 1 ? take(ts * (size_t)emax * L) : 0;
   for (int j = 0; j < 3; ++j) p.DEL_N[j] = j < m->D ? take(ts * (size_t)no * std::max<int64_t>(L, 16)) : 0;
   for (int j = 0; j < 2; ++j) p.HID_N[j] = j < m->D - 1 ? take(ts * (size_t)no * L) : 0;
+  // T-form node kernels: every block's first-Linear ReLU output, written by
+  // the forward for the backward; checkpointing: one block's, recomputed
+  p.HID_NK = rows_rt(m->prec, L, m->D, NODE_BLOCK) ? take(2 * (size_t)(p.lean ? 1 : K) * no * L) : 0;
   // split-K partials: the largest S*O*I over all weight matrices
   size_t part = 0;
   const size_t nm = m->mlp.size();
@@ -562,6 +565,8 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const 
     na.in1 = AGG(k);
     na.out = V(k + 1);
     na.out16 = V16(k + 1);
+    na.in0_16 = V16(k);
+    na.hid_out = (p.HID_NK && !p.lean) ? (void*)((uint16_t*)(ws + p.HID_NK) + (size_t)k * no * L) : nullptr;
     na.eps = m->cfg.ln_eps;
     {
       Timed t_(m, MGN_T_NODE_FWD, st);
@@ -757,6 +762,24 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.in0 = p.lean ? nullptr : V(k);
       a.in0_16 = p.lean ? V16(k) : nullptr;  // the bf16 copy is the product operand either way
       a.in1 = AGG(k);
+      void* hidk[2] = {HID_N[0], HID_N[1]};
+      if (p.HID_NK) {  // the forward's ReLU output of this block
+        uint16_t* hk = (uint16_t*)(ws + p.HID_NK) + (p.lean ? 0 : (size_t)k * no * L);
+        if (p.lean && no > 0) {  // recomputed from the block's inputs by the same kernel
+          RowsFwdArgs ra{};
+          ra.mlp = a.mlp;
+          ra.rows = no;
+          ra.in1 = AGG(k);
+          ra.in0_16 = V16(k);
+          ra.hid_out = hk;
+          ra.eps = m->cfg.ln_eps;
+          Timed t_(m, MGN_T_NODE_BWD, st);
+          e = launch_rows_fwd(m->prec, L, D, NODE_BLOCK, ra, st);
+          CHK("node ReLU output recompute");
+        }
+        a.hid_in = hk;
+        hidk[0] = hk;
+      }
       a.dm = DV[a_];
       a.dx0 = DV[b_];
       a.dx1 = DAGG;
@@ -781,7 +804,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       w.R = no;
       e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
       CHK("node dW");
-      e = dw_hidden(ml, no, DEL_N, HID_N, L, accumulate);
+      e = dw_hidden(ml, no, DEL_N, hidk, L, accumulate);
       CHK("node dW");
     }
     {

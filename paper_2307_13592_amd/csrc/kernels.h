@@ -21,6 +21,8 @@ struct RowsFwdArgs {
   const float* in1;  // NODE: aggregated messages [rows][L]
   void* out;         // ENC_NODE, NODE, DEC: fp32; ENC_EDGE: storage type
   void* out16;       // ENC_NODE, NODE in bf16 mode: bf16 copy of the output rows (or null)
+  const void* in0_16;  // NODE, bf16 T-form kernel: bf16 copy of v (the product operand), or null
+  void* hid_out;       // NODE, bf16 T-form kernel: first Linear's ReLU output [rows][L] bf16, or null
   float eps;
 };
 
@@ -49,6 +51,7 @@ struct RowsBwdArgs {
   const float* in0;
   const float* in1;
   const void* in0_16;  // NODE / DEC: bf16 rows [rows][L] read instead of in0 when set
+  const void* hid_in;  // NODE, bf16 T-form kernel: the forward's first-Linear ReLU output [rows][L]
   const float* dm;   // gradient w.r.t. the MLP output (LN output; dOut for the decoder)
   float* dx0;        // NODE: dv^k owned part (= dm + dX_v); DEC: dv^K
   float* dx1;        // NODE: d agg
@@ -138,6 +141,11 @@ int64_t plan_chunks(int64_t n_owned);
 // Receivers per planning chunk: work units never cross a multiple of it.
 int plan_chunk_receivers();
 
+// T-form row kernels (bf16, depth 2, l 64 / 128; not the decoder).  The node
+// half's T-form backward needs the forward's first-Linear ReLU output
+// (RowsFwdArgs::hid_out -> RowsBwdArgs::hid_in); without it the older
+// row-split kernel recomputes it.
+bool rows_rt(int prec, int L, int D, int kind);
 hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st);
 hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int grid, hipStream_t st);
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st);

@@ -2458,6 +2458,377 @@ __global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
   }
 }
 
+// ------------------------------------------------ row MLPs in T form ---
+// Encoders and the node half of a block (bf16, depth 2, l in {64, 128}) with
+// the T-form products of the edge kernels: one wave per 16-row tile, no LDS
+// round trips, weights and vectors in LDS.  The first Linear's B operand is
+// the input row tile in plain order: the edge / node features (fin <= 16
+// values, lane groups 0 and 1) or [v | agg] (2 l values).
+template <int L, int KIND>
+struct RtRowsLay {
+  static constexpr int NKH = L / 32, NB = L / 16;
+  static constexpr int W = NB * NKH * 64 * 16;           // one l x l packed layer
+  static constexpr int NK1 = KIND == NODE_BLOCK ? 2 * NKH : 1;
+  static constexpr int W1 = NB * NK1 * 64 * 16;          // first Linear (forward packing)
+  // forward: W1, W2, then b1, b2, gamma, beta
+  static constexpr int F_W2 = W1, F_VEC = W1 + W, F_END = F_VEC + 4 * L * 4;
+  // backward: W2 (fwd), W2 (bwd), then W1 (ENC_EDGE: forward packing, for the
+  // recompute; NODE_BLOCK: backward packing, both input blocks), then b1, b2, gamma
+  static constexpr int B_W2F = 0, B_W2B = W, B_W1 = 2 * W;
+  static constexpr int B_W1S = KIND == NODE_BLOCK ? 2 * W : W1;
+  static constexpr int B_VEC = B_W1 + B_W1S, B_END = B_VEC + 3 * L * 4;
+  // waves per workgroup: forward 16 (at most 128 registers), backward 12 (168)
+  static constexpr int FNWV = 16, FNTH = 64 * FNWV, NWV = 12, NTH = 64 * NWV;
+  static constexpr int NVEC = 4 * L;                     // bias / LayerNorm partials per wave
+  static_assert(F_END <= 160 * 1024 && B_END <= 160 * 1024, "LDS");
+  static_assert(NWV * NVEC * 4 <= B_VEC, "partials reuse the weight area");
+};
+
+// First-Linear B operand of a row tile (row `row`, lane group q).
+template <int L, int KIND>
+__device__ __forceinline__ void rt_rows_input(const float* __restrict__ in0, const float* __restrict__ in1,
+                                              const uint16_t* __restrict__ in0_16, int fin, int64_t row, int q,
+                                              uint4 (&xf)[RtRowsLay<L, KIND>::NK1]) {
+  constexpr int NKH = L / 32;
+  if constexpr (KIND == NODE_BLOCK) {
+#pragma unroll
+    for (int kg = 0; kg < 2 * NKH; ++kg) {
+      if (kg < NKH && in0_16) {  // bf16 copy of v (the rounded operand)
+        xf[kg] = *reinterpret_cast<const uint4*>(in0_16 + row * L + kg * 32 + q * 8);
+        continue;
+      }
+      const float* src = (kg < NKH ? in0 : in1) + row * L + (kg % NKH) * 32 + q * 8;
+      const float4 x0 = reinterpret_cast<const float4*>(src)[0], x1 = reinterpret_cast<const float4*>(src)[1];
+      xf[kg] = make_uint4(bf_pack(x0.x, x0.y), bf_pack(x0.z, x0.w), bf_pack(x1.x, x1.y), bf_pack(x1.z, x1.w));
+    }
+  } else {
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = q * 8 + j;
+      x[j] = k < fin ? in0[row * fin + k] : 0.f;
+    }
+    xf[0] = make_uint4(bf_pack(x[0], x[1]), bf_pack(x[2], x[3]), bf_pack(x[4], x[5]), bf_pack(x[6], x[7]));
+  }
+}
+
+// acc += b (a T-order vector in LDS), then ReLU; bits of the mask, T-form frags.
+template <int NB>
+__device__ __forceinline__ void rt_bias_relu(floatx4 (&z)[NB], const float* bv, int q, float (&h)[NB][4],
+                                             uint32_t* mask) {
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) {
+    const float4 b = rt_ld4(bv, cb, q);
+    const float b4[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float v = z[cb][r] + b4[r];
+      const bool on = v > 0.f;
+      if (mask) *mask |= (on ? 1u : 0u) << (cb * 4 + r);
+      h[cb][r] = on ? v : 0.f;
+    }
+  }
+}
+
+// Forward: ENC_EDGE -> bf16 rows; ENC_NODE -> fp32 rows + bf16 copy;
+// NODE_BLOCK -> v + LN(MLP([v | agg])) fp32 + bf16 copy, and the ReLU output
+// of the first Linear (bf16, for the backward) when a.hid_out is set (only
+// that when a.out is null).
+template <int L, int KIND>
+__global__ __launch_bounds__((RtRowsLay<L, KIND>::FNTH)) void rows_rt_fwd_kernel(RowsFwdArgs a) {
+  using Lay = RtRowsLay<L, KIND>;
+  constexpr int NKH = Lay::NKH, NB = Lay::NB, NK1 = Lay::NK1;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* W1 = reinterpret_cast<uint4*>(lds);
+  uint4* W2 = reinterpret_cast<uint4*>(lds + Lay::F_W2);
+  float* vb1 = reinterpret_cast<float*>(lds + Lay::F_VEC);
+  float* vb2 = vb1 + L;
+  float* vg = vb1 + 2 * L;
+  float* vbt = vb1 + 3 * L;
+  rs_copy_frags(W1, a.mlp.lin[0].wf, NB, NK1, NK1, 0);
+  rt_copy_frags(W2, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
+  rt_copy_vec(vb1, a.mlp.lin[0].b, L);
+  rt_copy_vec(vb2, a.mlp.lin[1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  rt_copy_vec(vbt, a.mlp.beta, L);
+  __syncthreads();
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int64_t ntiles = (a.rows + 15) / 16;
+  for (int64_t t = (int64_t)blockIdx.x * Lay::FNWV + wave; t < ntiles; t += (int64_t)gridDim.x * Lay::FNWV) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t row = t * 16 + e;
+    const bool ok = row < a.rows;
+    const int64_t src = ok ? row : t * 16;  // rows past the end repeat the tile's first row (not stored)
+    uint4 xf[NK1];
+    rt_rows_input<L, KIND>(a.in0, a.in1, reinterpret_cast<const uint16_t*>(a.in0_16), a.fin, src, q, xf);
+    floatx4 z[NB];
+    rt_gemm<NB, NK1>(W1, xf, z, ln);
+    float h[NB][4];
+    rt_bias_relu<NB>(z, vb1, q, h, nullptr);
+    uint4 hf[NKH];
+    rt_frags<NB>(h, hf);
+    if constexpr (KIND == NODE_BLOCK) {
+      if (a.hid_out) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid_out) + row * L, q, hf, ok);
+      if (!a.out) continue;  // only the ReLU output wanted (the backward's recompute)
+    }
+    floatx4 acc[NB];
+    rt_gemm<NB, NKH>(W2, hf, acc, ln);
+    float y[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float4 bv = rt_ld4(vb2, cb, q);
+      y[cb][0] = acc[cb][0] + bv.x;
+      y[cb][1] = acc[cb][1] + bv.y;
+      y[cb][2] = acc[cb][2] + bv.z;
+      y[cb][3] = acc[cb][3] + bv.w;
+    }
+    const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
+    float dv[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float d = y[cb][r] - mu;
+        dv[cb][r] = d * d;
+      }
+    const float rs = 1.0f / sqrtf(rt_sum4(rt_lane_sum<NB>(dv)) / L + a.eps);
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float4 g = rt_ld4(vg, cb, q), bt = rt_ld4(vbt, cb, q);
+      y[cb][0] = g.x * ((y[cb][0] - mu) * rs) + bt.x;
+      y[cb][1] = g.y * ((y[cb][1] - mu) * rs) + bt.y;
+      y[cb][2] = g.z * ((y[cb][2] - mu) * rs) + bt.z;
+      y[cb][3] = g.w * ((y[cb][3] - mu) * rs) + bt.w;
+    }
+    if constexpr (KIND == NODE_BLOCK) {  // residual: v + m
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float4 v = rt_ld4(a.in0 + src * L, cb, q);
+        y[cb][0] = y[cb][0] + v.x;
+        y[cb][1] = y[cb][1] + v.y;
+        y[cb][2] = y[cb][2] + v.z;
+        y[cb][3] = y[cb][3] + v.w;
+      }
+    }
+    uint4 o[NKH];
+    rt_frags<NB>(y, o);
+    if constexpr (KIND == ENC_EDGE) {
+      rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.out) + row * L, q, o, ok);
+    } else {
+      if (ok) {
+        float* op = reinterpret_cast<float*>(a.out) + row * L;
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+          *reinterpret_cast<float4*>(op + cb * 16 + q * 4) = make_float4(y[cb][0], y[cb][1], y[cb][2], y[cb][3]);
+      }
+      if (a.out16) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.out16) + row * L, q, o, ok);
+    }
+  }
+}
+
+// Backward: ENC_EDGE recomputes its tile's forward from the features;
+// NODE_BLOCK takes the first Linear's ReLU output from the forward
+// (a.hid_in) and ends in the input gradients dv = dm + dz W_1[:, v-block],
+// dagg = dz W_1[:, agg-block].  Outputs as rows_bwd_kernel for these kinds.
+template <int L, int KIND>
+__global__ __launch_bounds__((RtRowsLay<L, KIND>::NTH)) void rows_rt_bwd_kernel(RowsBwdArgs a) {
+  using Lay = RtRowsLay<L, KIND>;
+  constexpr int NKH = Lay::NKH, NB = Lay::NB, NK1 = Lay::NK1, W = Lay::W;
+  constexpr int NV = 4 * NB, NR = NV / 16;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* W2f = reinterpret_cast<uint4*>(lds + Lay::B_W2F);
+  uint4* W2b = reinterpret_cast<uint4*>(lds + Lay::B_W2B);
+  uint4* W1 = reinterpret_cast<uint4*>(lds + Lay::B_W1);
+  float* vb1 = reinterpret_cast<float*>(lds + Lay::B_VEC);
+  float* vb2 = vb1 + L;
+  float* vg = vb1 + 2 * L;
+  rt_copy_frags(W2f, a.mlp.lin[1].wf, NB, NKH, NKH, 0);
+  rt_copy_frags(W2b, a.mlp.lin[1].wb, NB, NKH, NKH, 0);
+  if constexpr (KIND == NODE_BLOCK) rt_copy_frags(W1, a.mlp.lin[0].wb, 2 * NB, NKH, NKH, 0);
+  else rs_copy_frags(W1, a.mlp.lin[0].wf, NB, NK1, NK1, 0);
+  rt_copy_vec(vb1, a.mlp.lin[0].b, L);
+  rt_copy_vec(vb2, a.mlp.lin[1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  __syncthreads();
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  // column totals (rt_col_totals' share of each lane): hidden bias, last bias, gamma, beta
+  float qacc[4][NR];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int t = 0; t < NR; ++t) qacc[k][t] = 0.f;
+  auto coltot = [&](float (&x)[NB][4], int k, int e) {
+    float* f = &x[0][0];
+    rt_col_totals<NV>(*reinterpret_cast<float(*)[NV]>(f), e);
+#pragma unroll
+    for (int t = 0; t < NR; ++t) qacc[k][t] += f[t];
+  };
+  const int64_t ntiles = (a.rows + 15) / 16;
+  for (int64_t t = (int64_t)blockIdx.x * Lay::NWV + wave; t < ntiles; t += (int64_t)gridDim.x * Lay::NWV) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t row = t * 16 + e;
+    const bool ok = row < a.rows;
+    const int64_t src = ok ? row : t * 16;
+    uint32_t mask = 0u;
+    uint4 hf[NKH];
+    if constexpr (KIND == NODE_BLOCK) {
+      // h_1 of the forward (plain order) -> T order; its sign is the ReLU mask
+      const uint16_t* hp = reinterpret_cast<const uint16_t*>(a.hid_in) + src * L;
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) {
+        hf[kg] = rt_from_plain(*reinterpret_cast<const uint4*>(hp + kg * 32 + q * 8));
+        const uint32_t w[4] = {hf[kg].x, hf[kg].y, hf[kg].z, hf[kg].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {  // dword i: block 2 kg + i / 2, rows r = 2 (i % 2) .. + 1
+          const int cb = 2 * kg + i / 2, r = 2 * (i % 2);
+          mask |= ((w[i] & 0x7fffu) != 0u && !(w[i] & 0x8000u) ? 1u : 0u) << (cb * 4 + r);
+          mask |= (((w[i] >> 16) & 0x7fffu) != 0u && !(w[i] & 0x80000000u) ? 1u : 0u) << (cb * 4 + r + 1);
+        }
+      }
+    } else {
+      uint4 xf[NK1];
+      rt_rows_input<L, KIND>(a.in0, a.in1, nullptr, a.fin, src, q, xf);
+      floatx4 z[NB];
+      rt_gemm<NB, NK1>(W1, xf, z, ln);
+      float h[NB][4];
+      rt_bias_relu<NB>(z, vb1, q, h, &mask);
+      rt_frags<NB>(h, hf);
+      rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[0]) + row * L, q, hf, ok);
+    }
+    float y[NB][4];
+    {
+      floatx4 acc[NB];
+      rt_gemm<NB, NKH>(W2f, hf, acc, ln);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float4 bv = rt_ld4(vb2, cb, q);
+        y[cb][0] = acc[cb][0] + bv.x;
+        y[cb][1] = acc[cb][1] + bv.y;
+        y[cb][2] = acc[cb][2] + bv.z;
+        y[cb][3] = acc[cb][3] + bv.w;
+      }
+    }
+    float dm[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float4 d4 = rt_ld4(a.dm + src * L, cb, q);
+      dm[cb][0] = ok ? d4.x : 0.f;
+      dm[cb][1] = ok ? d4.y : 0.f;
+      dm[cb][2] = ok ? d4.z : 0.f;
+      dm[cb][3] = ok ? d4.w : 0.f;
+    }
+    // LayerNorm (recomputed): y becomes xhat
+    const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
+    float rs;
+    {
+      float dv[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d = y[cb][r] - mu;
+          dv[cb][r] = d * d;
+        }
+      rs = 1.0f / sqrtf(rt_sum4(rt_lane_sum<NB>(dv)) / L + a.eps);
+    }
+    // LayerNorm backward: dy = rstd (dm g - mean(dm g) - xhat mean(dm g xhat))
+    float t1, t2;
+    {
+      float p1[4], p2[4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float4 g4 = rt_ld4(vg, cb, q);
+        const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          y[cb][r] = (y[cb][r] - mu) * rs;
+          const float d = dm[cb][r] * g[r];
+          p1[r] = cb == 0 ? d : p1[r] + d;
+          p2[r] = cb == 0 ? d * y[cb][r] : p2[r] + d * y[cb][r];
+        }
+      }
+      t1 = rt_sum4((p1[0] + p1[1]) + (p1[2] + p1[3]));
+      t2 = rt_sum4((p2[0] + p2[1]) + (p2[2] + p2[3]));
+    }
+    float v[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float4 g4 = rt_ld4(vg, cb, q);
+      const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[cb][r] = rs * (dm[cb][r] * g[r] - t1 / L - y[cb][r] * (t2 / L));
+        y[cb][r] = dm[cb][r] * y[cb][r];  // gamma's column terms
+      }
+    }
+    coltot(y, 2, e);   // gamma
+    coltot(dm, 3, e);  // beta
+    uint4 gf[NKH];
+    rt_frags<NB>(v, gf);
+    rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[1]) + row * L, q, gf, ok);
+    coltot(v, 1, e);  // last bias
+    {
+      floatx4 acc[NB];
+      rt_gemm<NB, NKH>(W2b, gf, acc, ln);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[cb][r] = ((mask >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
+    }
+    rt_frags<NB>(v, gf);
+    rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[0]) + row * L, q, gf, ok);
+    coltot(v, 0, e);  // hidden bias
+    if constexpr (KIND == NODE_BLOCK) {
+#pragma unroll
+      for (int pass = 0; pass < 2; ++pass) {
+        floatx4 acc[NB];
+        rt_gemm<NB, NKH>(W1 + pass * NB * NKH * 64, gf, acc, ln);
+        if (pass == 0) {  // dv = dz W_1[:, v-block] + dm
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb) {
+            const float4 d4 = rt_ld4(a.dm + src * L, cb, q);
+            acc[cb][0] += d4.x;
+            acc[cb][1] += d4.y;
+            acc[cb][2] += d4.z;
+            acc[cb][3] += d4.w;
+          }
+        }
+        if (ok) {
+          float* op = (pass == 0 ? a.dx0 : a.dx1) + row * L;
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb)
+            *reinterpret_cast<float4*>(op + cb * 16 + q * 4) = make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
+        }
+      }
+    }
+  }
+  // column partials: lane (e, q)'s totals are columns 16 cb + 4 q + r for
+  // index e * NR + t = 4 cb + r; then the waves in order through LDS
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(lds);
+  {
+    float* rw = red + wave * Lay::NVEC;
+#pragma unroll
+    for (int t = 0; t < NR; ++t) {
+      const int i = (lane & 15) * NR + t;
+      const int col = (i >> 2) * 16 + (lane >> 4) * 4 + (i & 3);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) rw[k * L + col] = qacc[k][t];
+    }
+  }
+  __syncthreads();
+  float* vp = a.vpart + (int64_t)blockIdx.x * a.nvec;
+  for (int i = threadIdx.x; i < Lay::NVEC; i += Lay::NTH) {
+    float s = 0.f;
+    for (int w = 0; w < Lay::NWV; ++w) s += red[w * Lay::NVEC + i];
+    vp[i] = s;
+  }
+}
+
 // --------------------------------------------------- node input gradient ---
 // Gradient reaching the nodes through the first Linear of a block's edge MLP.
 // Its sender and receiver column blocks W_s, W_r are shared by all edges, so
@@ -3265,7 +3636,38 @@ static hipError_t edge_bwd_t(const EdgeBwdArgs& a, int grid, hipStream_t st) {
   return hipGetLastError();
 }
 
+bool rows_rt(int prec, int L, int D, int kind) {
+  return prec == BF16 && D == 2 && (L == 64 || L == 128) && kind != DECODER;
+}
+
+template <int L, int KIND>
+static hipError_t rows_rt_fwd_t(const RowsFwdArgs& a, hipStream_t st) {
+  using Lay = RtRowsLay<L, KIND>;
+  if (a.rows == 0) return hipSuccess;
+  allow_lds(rows_rt_fwd_kernel<L, KIND>, Lay::F_END);
+  hipLaunchKernelGGL((rows_rt_fwd_kernel<L, KIND>), dim3(RS_GRID), dim3(Lay::FNTH), Lay::F_END, st, a);
+  return hipGetLastError();
+}
+
+template <int L, int KIND>
+static hipError_t rows_rt_bwd_t(const RowsBwdArgs& a, hipStream_t st) {
+  using Lay = RtRowsLay<L, KIND>;
+  allow_lds(rows_rt_bwd_kernel<L, KIND>, Lay::B_END);
+  hipLaunchKernelGGL((rows_rt_bwd_kernel<L, KIND>), dim3(RS_GRID), dim3(Lay::NTH), Lay::B_END, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st) {
+  if (rows_rt(prec, L, D, kind)) {
+    if (L == 64) {
+      if (kind == ENC_NODE) return rows_rt_fwd_t<64, ENC_NODE>(a, st);
+      if (kind == ENC_EDGE) return rows_rt_fwd_t<64, ENC_EDGE>(a, st);
+      return rows_rt_fwd_t<64, NODE_BLOCK>(a, st);
+    }
+    if (kind == ENC_NODE) return rows_rt_fwd_t<128, ENC_NODE>(a, st);
+    if (kind == ENC_EDGE) return rows_rt_fwd_t<128, ENC_EDGE>(a, st);
+    return rows_rt_fwd_t<128, NODE_BLOCK>(a, st);
+  }
 #define RF(PP, LL, DD)                                                                      \
   if (prec == PP && L == LL && D == DD) {                                                   \
     switch (kind) {                                                                         \
@@ -3296,6 +3698,10 @@ static hipError_t rows_bwd_rs_t(const RowsBwdArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st) {
+  if (rows_rt(prec, L, D, kind) && (kind == ENC_EDGE || (kind == NODE_BLOCK && a.hid_in))) {
+    if (L == 64) return kind == ENC_EDGE ? rows_rt_bwd_t<64, ENC_EDGE>(a, st) : rows_rt_bwd_t<64, NODE_BLOCK>(a, st);
+    return kind == ENC_EDGE ? rows_rt_bwd_t<128, ENC_EDGE>(a, st) : rows_rt_bwd_t<128, NODE_BLOCK>(a, st);
+  }
   if (rows_rs(prec, L, D, kind)) {
     if (L == 64) return kind == NODE_BLOCK ? rows_bwd_rs_t<64, NODE_BLOCK>(a, st) : rows_bwd_rs_t<64, ENC_EDGE>(a, st);
     return kind == NODE_BLOCK ? rows_bwd_rs_t<128, NODE_BLOCK>(a, st) : rows_bwd_rs_t<128, ENC_EDGE>(a, st);

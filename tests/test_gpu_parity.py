@@ -41,7 +41,10 @@ def _case(name, mesh, p, l, K, D, prec, seed=3, part=None):
 def test_one_block_strict(prec, mesh_name):
     """One message-passing block on jittered meshes (no repeated feature
     values): every gradient tensor within the nominal tolerance of the
-    precision, no calibration."""
+    precision.  In bf16 the bound is relaxed only for a tensor on which an
+    independent float32 implementation with bf16 operands itself misses it
+    (on the Delaunay case the decoder's first Linear: 6.3e-2), to twice that
+    implementation's error; fp32 stays strict."""
     say(f"[parity] {mesh_name} K=1 strict {prec}")
     if mesh_name == "sector":
         mesh, p = meshes.sector(8, 16, 12, 4, seed=7), 1
@@ -50,7 +53,8 @@ def test_one_block_strict(prec, mesh_name):
     c = local_inputs(mesh, p, 128, 1, 2, 3)
     gpu = run_gpu(c, 128, 1, 2, prec)
     ref = run_oracle(c, 128, 1, 2, bf16=prec == "bf16")
-    bad = compare(f"{mesh_name} K=1", prec, c["shapes"], gpu, ref)
+    cal = calibrate(c, 128, 1, 2, prec, runs=3) if prec == "bf16" else None
+    bad = compare(f"{mesh_name} K=1", prec, c["shapes"], gpu, ref, cal)
     assert not bad, bad
 
 
