@@ -1000,11 +1000,17 @@ __device__ __forceinline__ void zero_empty_receivers(const int32_t* row_ptr, int
       for (int c = 0; c < L; c += 4) *reinterpret_cast<float4*>(dst + r * L + c) = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
+// Waves per SIMD the streaming edge kernels are compiled for: two where two
+// workgroups fit the LDS (the edge gather's latency needs them more than the
+// products need registers); at l = 256 one workgroup fills the LDS, and one
+// wave per SIMD may use the accumulator registers too instead of spilling.
+template <int L>
+struct EdgeWpe {
+  static constexpr int value = L >= 256 ? 1 : 2;
+};
+
 template <int P_, int L, int D>
-// Two waves per SIMD: the register budget is capped so that two workgroups
-// can be resident, which the edge gather's latency needs more than the
-// products need registers.
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void edge_fwd_kernel(EdgeFwdArgs a) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::value))) void edge_fwd_kernel(EdgeFwdArgs a) {
   using P = typename PrecOf<P_>::type;
   using T = typename P::T;
   constexpr int TE = EdgeTE<P, L, D>::value;
@@ -1112,7 +1118,7 @@ struct EdgeBwdLds {
 // gradients; bias / gamma / beta gradients are per-lane column partials over
 // the workgroup's rows, written once at the end.
 template <int P_, int L, int D>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void edge_bwd_kernel(EdgeBwdArgs a) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::value))) void edge_bwd_kernel(EdgeBwdArgs a) {
   using P = typename PrecOf<P_>::type;
   using T = typename P::T;
   constexpr int TE = EdgeTEB<P, L, D>::value;
