@@ -67,7 +67,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="C4")
     ap.add_argument("--recompute", type=int, default=None,
-                    help="edge-stream checkpoint interval (default: 8 for C5, whose stash-all workspace exceeds "
+                    help="edge-stream checkpoint interval (default: 5 for C5, whose stash-all workspace exceeds "
                          "the GPU's memory; 0 otherwise)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -92,7 +92,7 @@ def main():
     loc = case.local_inputs(g["l2g"], g["eperm"], g["n_owned"], g["n_halo"])
     no, nh, ne = g["n_owned"], g["n_halo"], g["n_edges"]
     log(f"[bench] {cfg.name}: {cfg.note}; owned {no}, halo {nh}, edges {ne}; inputs {time.time() - t0:.1f}s")
-    recompute = args.recompute if args.recompute is not None else (8 if cfg.name == "C5" else 0)
+    recompute = args.recompute if args.recompute is not None else (5 if cfg.name == "C5" else 0)
     sess = Session(cfg.latent, cfg.K, cfg.depth, cfg.precision, g, loc["node_feat"], loc["edge_feat"],
                    loc["halo"], case.params, recompute=recompute)
     target = torch.as_tensor(loc["target"]).cuda()
