@@ -15,8 +15,9 @@
  *     v_r <- v_r + LN(MLP([v_r | agg_r]));
  *   - the partition holds the edges whose receiver it owns (section
  *     "Methodology": halo of depth one); halo node latents at the input of
- *     block k come in as halo[k] (the exchange between blocks of Algorithm 1
- *     happens outside this library).
+ *     block k come in as halo[k]; the caller exchanges them between the
+ *     stages of a staged step (mgn_forward_block, mgn_copy_latents and
+ *     mgn_add_latent_grads below) or supplies them all up front.
  *
  * Conventions
  *   - Every function returns an mgn_status; MGN_OK is 0.  On error nothing is
@@ -174,6 +175,75 @@ mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* node_feat,
 mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_params, int accumulate, float* d_halo,
                         mgn_stream stream);
 
+/* ---- the step in stages, for several partitions stepped in lockstep ----
+ *
+ * Algorithm 1 exchanges the halo after every message-passing block: halo
+ * node latents forward (owners -> partitions holding them as halo), and in
+ * the backward the halo gradients back to the owners (section
+ * "Methodology": forward halo exchange and backward gradient exchange).
+ * mgn_forward is exactly
+ *     mgn_forward_begin; mgn_forward_block x K; mgn_forward_end
+ * and mgn_backward is
+ *     mgn_backward_begin; mgn_backward_block x K; mgn_backward_end,
+ * so a caller stepping P partitions of one mesh (one model each, same
+ * parameters) can exchange between the stages:
+ *   forward:  begin (all parts); for k = 0..K-1: for every (part p, owner q):
+ *             mgn_copy_latents(q -> p's halo[k]); mgn_forward_block (all parts);
+ *             end (all parts);
+ *   backward: begin (all); for k = K-1..0: mgn_backward_block (all); for every
+ *             (p, q): mgn_add_latent_grads(p's d_halo[k] -> q); end (all).
+ * With d_params shared and accumulate = 1 for every part but the first, the
+ * parts' gradients add up to the gradient of the unpartitioned network.
+ * Every stage enqueues on the given stream; a stage called out of order
+ * returns MGN_E_STATE and enqueues nothing.  Errors inside a stage leave the
+ * step unusable (start again with mgn_forward_begin). */
+
+/* Arguments, checks and ownership as mgn_forward; runs the encoders.  halo
+ * may be filled block by block: halo[k] is read when block k runs. */
+mgn_status mgn_forward_begin(mgn_model* m, const mgn_graph* g, const float* node_feat, const float* edge_feat,
+                             const float* halo, float* out, void* workspace, size_t ws_bytes, mgn_stream stream);
+/* Runs the next message-passing block (k = 0, 1, ..., K-1 in turn). */
+mgn_status mgn_forward_block(mgn_model* m, mgn_stream stream);
+/* Runs the decoder after the K blocks; the step is then ready for a backward. */
+mgn_status mgn_forward_end(mgn_model* m, mgn_stream stream);
+/* Arguments and checks as mgn_backward; runs the decoder's backward. */
+mgn_status mgn_backward_begin(mgn_model* m, const float* d_out, float* d_params, int accumulate, float* d_halo,
+                              mgn_stream stream);
+/* Runs the backward of the next block (k = K-1, ..., 0 in turn): writes
+ * d_halo[k] and leaves dL/dv^k (owned node latents at block k's input). */
+mgn_status mgn_backward_block(mgn_model* m, mgn_stream stream);
+/* Runs the encoders' backward after the K blocks. */
+mgn_status mgn_backward_end(mgn_model* m, mgn_stream stream);
+
+/* Exchange lists between part p and its neighbour q (host arrays; Algorithm
+ * 1's create_masks, built once per mesh): the halo nodes of p that q owns,
+ * in ascending halo index.  recv_idx[i] = halo index j of such a node in p
+ * (p's local id n_owned_p + j), send_rows[i] = its local id in q.  Inputs:
+ * l2g_p [n_owned_p + n_halo_p] and l2g_q [n_owned_q + ...] from
+ * mgn_graph_build, part [n_nodes].  recv_idx, send_rows: caller arrays of
+ * n_halo_p entries; *count receives the number written.  MGN_E_GRAPH if q's
+ * owned list is not ascending global ids of part q or misses a node. */
+mgn_status mgn_halo_masks(const int32_t* l2g_p, int64_t n_owned_p, int64_t n_halo_p, const int32_t* part,
+                          int64_t n_nodes, const int32_t* l2g_q, int64_t n_owned_q, int32_t q, int32_t* recv_idx,
+                          int32_t* send_rows, int64_t* count);
+/* Forward exchange (device arrays): halo_k[recv_idx[i]][:] = v[send_rows[i]][:]
+ * for i < n, where v are the owner's node latents at the input of its next
+ * block (after mgn_forward_begin: v^0; after block k-1: v^k; after the
+ * forward: v^K).  halo_k is a [n_halo][latent] fp32 block of the receiving
+ * part's halo buffer (16-byte aligned).  Pairs with an index outside
+ * [0, owner's n_owned) or [0, n_halo) are skipped.  Enqueued on `stream`. */
+mgn_status mgn_copy_latents(const mgn_model* owner, const int32_t* send_rows, const int32_t* recv_idx, int64_t n,
+                            float* halo_k, int64_t n_halo, mgn_stream stream);
+/* Backward exchange (device arrays): dv[send_rows[i]][:] += d_halo_k[recv_idx[i]][:]
+ * for i < n, where dv is the owner's dL/dv of its last backward stage
+ * (after mgn_backward_block for block k: dL/dv^k) and d_halo_k the
+ * [n_halo][latent] block k of the holding part's d_halo.  send_rows must be
+ * distinct within one call (lists from mgn_halo_masks are); calls adding
+ * into one owner run in stream order, so the sum has a fixed order.
+ * Out-of-range pairs are skipped, as above. */
+mgn_status mgn_add_latent_grads(mgn_model* owner, const float* d_halo_k, int64_t n_halo, const int32_t* recv_idx,
+                                const int32_t* send_rows, int64_t n, mgn_stream stream);
+
 /* Masked mean squared error (Algorithm 1: local squared error, mean over the
  * loss-masked nodes and outputs) and its gradient, device pointers:
  * out, target [n][d]; mask [n] (NULL = all rows); loss [2]: loss[0] = loss,
@@ -196,7 +266,9 @@ typedef enum {
   MGN_T_WEIGHT_GRAD = 7,   /* weight-gradient GEMMs and fixed-order reductions */
   MGN_T_OTHER = 8,         /* planning, loss */
   MGN_T_NODE_PROJ = 9,     /* per-node products of the edge MLP's first Linear (row-split edge kernels) */
-  MGN_T_COUNT = 10
+  MGN_T_EXCHANGE = 10,     /* halo exchange between partitions (mgn_copy_latents, mgn_add_latent_grads),
+                              timed on the owner's model */
+  MGN_T_COUNT = 11
 } mgn_timer;
 /* Starts (enable != 0) or stops recording; starting clears earlier records. */
 mgn_status mgn_timing_enable(mgn_model* m, int enable);

@@ -23,9 +23,11 @@ STATUS_NAMES = ["MGN_OK", "MGN_E_ARG", "MGN_E_GRAPH", "MGN_E_STATE", "MGN_E_NOME
 EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mgn_set_params", "mgn_get_params",
            "mgn_partition_slabs", "mgn_graph_sizes", "mgn_graph_build", "mgn_graph_validate", "mgn_set_recompute",
            "mgn_workspace_size",
-           "mgn_forward", "mgn_backward", "mgn_mse_grad", "mgn_timing_enable", "mgn_timing_read"]
+           "mgn_forward", "mgn_backward", "mgn_forward_begin", "mgn_forward_block", "mgn_forward_end",
+           "mgn_backward_begin", "mgn_backward_block", "mgn_backward_end", "mgn_halo_masks", "mgn_copy_latents",
+           "mgn_add_latent_grads", "mgn_mse_grad", "mgn_timing_enable", "mgn_timing_read"]
 TIMERS = ["encode", "edge_fwd", "node_fwd", "decode", "edge_bwd", "node_bwd", "input_grad", "weight_grad",
-          "other", "node_proj"]
+          "other", "node_proj", "exchange"]
 
 
 class MgnError(RuntimeError):
@@ -73,6 +75,15 @@ def lib() -> C.CDLL:
             "mgn_workspace_size": (C.c_int, [vp, vp, vp]),
             "mgn_forward": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]),
             "mgn_backward": (C.c_int, [vp, vp, vp, C.c_int, vp, vp]),
+            "mgn_forward_begin": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]),
+            "mgn_forward_block": (C.c_int, [vp, vp]),
+            "mgn_forward_end": (C.c_int, [vp, vp]),
+            "mgn_backward_begin": (C.c_int, [vp, vp, vp, C.c_int, vp, vp]),
+            "mgn_backward_block": (C.c_int, [vp, vp]),
+            "mgn_backward_end": (C.c_int, [vp, vp]),
+            "mgn_halo_masks": (C.c_int, [vp, i64, i64, vp, i64, vp, i64, i32, vp, vp, vp]),
+            "mgn_copy_latents": (C.c_int, [vp, vp, vp, i64, vp, i64, vp]),
+            "mgn_add_latent_grads": (C.c_int, [vp, vp, i64, vp, vp, i64, vp]),
             "mgn_mse_grad": (C.c_int, [vp, vp, vp, i64, i32, vp, vp, vp]),
             "mgn_timing_enable": (C.c_int, [vp, C.c_int]),
             "mgn_timing_read": (C.c_int, [vp, C.c_int, vp, vp]),
@@ -215,6 +226,60 @@ def mgn_forward(model, graph: mgn_graph, node_feat, edge_feat, halo, out, worksp
 def mgn_backward(model, d_out, d_params, accumulate: bool = False, d_halo=None, stream=None) -> None:
     _check(lib().mgn_backward(model, _dev(d_out), _dev(d_params), int(bool(accumulate)), _dev(d_halo),
                               _stream(stream)), model)
+
+
+def mgn_forward_begin(model, graph: mgn_graph, node_feat, edge_feat, halo, out, workspace, stream=None) -> None:
+    _check(lib().mgn_forward_begin(model, C.byref(graph), _dev(node_feat), _dev(edge_feat), _dev(halo), _dev(out),
+                                   _dev(workspace), workspace.numel() * workspace.element_size(), _stream(stream)),
+           model)
+
+
+def mgn_forward_block(model, stream=None) -> None:
+    _check(lib().mgn_forward_block(model, _stream(stream)), model)
+
+
+def mgn_forward_end(model, stream=None) -> None:
+    _check(lib().mgn_forward_end(model, _stream(stream)), model)
+
+
+def mgn_backward_begin(model, d_out, d_params, accumulate: bool = False, d_halo=None, stream=None) -> None:
+    _check(lib().mgn_backward_begin(model, _dev(d_out), _dev(d_params), int(bool(accumulate)), _dev(d_halo),
+                                    _stream(stream)), model)
+
+
+def mgn_backward_block(model, stream=None) -> None:
+    _check(lib().mgn_backward_block(model, _stream(stream)), model)
+
+
+def mgn_backward_end(model, stream=None) -> None:
+    _check(lib().mgn_backward_end(model, _stream(stream)), model)
+
+
+def mgn_halo_masks(l2g_p, n_owned_p: int, part, l2g_q, n_owned_q: int, q: int):
+    """Host exchange lists of part p's halo nodes owned by part q:
+    (recv_idx, send_rows) int32 arrays (halo index in p, local id in q)."""
+    lp, lpp = _host(l2g_p, np.int32)
+    pa, pp = _host(part, np.int32)
+    lq, lqp = _host(l2g_q, np.int32)
+    nh = lp.shape[0] - int(n_owned_p)
+    recv = np.empty(max(nh, 0), np.int32)
+    send = np.empty(max(nh, 0), np.int32)
+    cnt = C.c_int64()
+    _check(lib().mgn_halo_masks(lpp, int(n_owned_p), nh, pp, pa.shape[0], lqp, int(n_owned_q), int(q),
+                                recv.ctypes.data_as(C.c_void_p), send.ctypes.data_as(C.c_void_p), C.byref(cnt)))
+    return recv[:cnt.value].copy(), send[:cnt.value].copy()
+
+
+def mgn_copy_latents(owner, send_rows, recv_idx, halo_k, stream=None) -> None:
+    """halo_k[recv_idx[i]] = owner's current node latents[send_rows[i]] (device tensors)."""
+    _check(lib().mgn_copy_latents(owner, _dev(send_rows), _dev(recv_idx), int(send_rows.numel()), _dev(halo_k),
+                                  int(halo_k.shape[0]), _stream(stream)), owner)
+
+
+def mgn_add_latent_grads(owner, d_halo_k, recv_idx, send_rows, stream=None) -> None:
+    """owner's dL/dv[send_rows[i]] += d_halo_k[recv_idx[i]] (device tensors)."""
+    _check(lib().mgn_add_latent_grads(owner, _dev(d_halo_k), int(d_halo_k.shape[0]), _dev(recv_idx),
+                                      _dev(send_rows), int(send_rows.numel()), _stream(stream)), owner)
 
 
 def mgn_mse_grad(out, target, mask, loss, d_out, stream=None) -> None:

@@ -70,8 +70,19 @@ struct mgn_model {
   bool fwd_done = false;
   mgn_graph g{};
   const float *nf = nullptr, *ef = nullptr, *halo = nullptr;
+  float* out = nullptr;
   char* ws = nullptr;
   WsPlan plan{};
+  // staged step: the forward's next block (-1: no forward in progress); the
+  // backward in progress, its next block (-1: its blocks are done), the dL/dv
+  // buffer holding the gradient of the last stage's node latents, and the
+  // gradient outputs of the backward_begin call
+  int fwd_next = -1;
+  bool bwd_active = false;
+  int bwd_next = -1, bwd_a = 0;
+  float* d_params = nullptr;
+  float* d_halo = nullptr;
+  int accumulate = 0;
   std::string err;
   // launch timing
   bool timing = false;
@@ -355,7 +366,9 @@ mgn_status mgn_set_params(mgn_model* m, const float* src, int src_on_device, mgn
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_fail(m, e, "mgn_set_params sync");
   m->params_set = true;
-  m->fwd_done = false;
+  m->fwd_done = false;  // a step in progress is dropped
+  m->fwd_next = -1;
+  m->bwd_active = false;
   return MGN_OK;
 }
 
@@ -416,7 +429,9 @@ mgn_status mgn_set_recompute(mgn_model* m, int32_t interval, int64_t chunk_edges
     return fail(m, MGN_E_UNSUPPORTED, "mgn_set_recompute: edge-stream checkpointing needs the bf16 precision");
   m->ckpt = interval;
   m->chunk_edges = chunk_edges;
-  m->fwd_done = false;  // the workspace plan changes
+  m->fwd_done = false;  // the workspace plan changes: a step in progress is dropped
+  m->fwd_next = -1;
+  m->bwd_active = false;
   return MGN_OK;
 }
 
@@ -477,127 +492,6 @@ hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p,
 
 }  // namespace
 
-extern "C" {
-
-mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const float* ef, const float* halo,
-                       float* out, void* workspace, size_t ws_bytes, mgn_stream stream) {
-  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_forward: model is NULL");
-  mgn_status s = check_graph_args(m, g);
-  if (s) return s;
-  if (!m->params_set) return fail(m, MGN_E_STATE, "mgn_forward: parameters were never set");
-  if (!m->graph_ok || !same_graph(*g, m->vg))
-    return fail(m, MGN_E_STATE, "mgn_forward: graph was not validated with mgn_graph_validate");
-  const int64_t no = g->n_owned, nh = g->n_halo, ne = g->n_edges;
-  if ((no > 0 && (!nf || !out)) || (ne > 0 && !ef)) return fail(m, MGN_E_ARG, "mgn_forward: input is NULL");
-  if (nh > 0 && m->K > 0 && !halo) return fail(m, MGN_E_ARG, "mgn_forward: halo is NULL but n_halo > 0");
-  if (!aligned(nf, 4) || !aligned(ef, 4) || !aligned(out, 4) || !aligned(halo, 16))
-    return fail(m, MGN_E_ARG, "mgn_forward: misaligned pointer (features 4 bytes, halo 16 bytes)");
-  if (!workspace || !aligned(workspace, 256)) return fail(m, MGN_E_ARG, "mgn_forward: workspace NULL or not 256-byte aligned");
-  const WsPlan p = make_plan(m, g);
-  if (ws_bytes < p.total)
-    return fail(m, MGN_E_NOMEM, "mgn_forward: workspace too small (need " + std::to_string(p.total) + " bytes)");
-  hipStream_t st = (hipStream_t)stream;
-  char* ws = (char*)workspace;
-  const int L = m->L, K = m->K, D = m->D;
-  const size_t ts = tsize(m);
-  const int te = edge_tile_rows(m->prec, L, D);
-  auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)(p.lean ? (k & 1) : k) * no * L; };
-  auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)(p.lean ? 0 : k) * no * L; };
-  auto ES = [&](int k) -> void* {
-    const int slot = !p.lean ? k : (k % p.s == 0 ? k / p.s : p.nck);
-    return (void*)(ws + p.ES + ts * (size_t)slot * ne * L);
-  };
-  const int64_t v16_stride = (no + nh) * L;  // elements per block of the bf16 node copy
-  auto V16 = [&](int k) -> void* {
-    return m->prec == BF16 ? (void*)((uint16_t*)(ws + p.V16) + (size_t)k * v16_stride) : nullptr;
-  };
-  int32_t* erecv = (int32_t*)(ws + p.erecv);
-  int32_t* unit_r = (int32_t*)(ws + p.unit_r);
-  int32_t* n_units = (int32_t*)(ws + p.nunits);
-  hipError_t e;
-  {
-    Timed t_(m, MGN_T_OTHER, st);
-    e = launch_erecv(g->row_ptr, no, erecv, st);
-    if (e == hipSuccess)
-      e = launch_plan(g->row_ptr, no, 4 * te, 4 * te, (int32_t*)(ws + p.chunk), unit_r, n_units, st);
-  }
-  if (e != hipSuccess) return hip_fail(m, e, "mgn_forward plan");
-  if (m->prec == BF16 && K > 0 && nh > 0) {
-    Timed t_(m, MGN_T_OTHER, st);
-    e = launch_halo_bf16(halo, K, nh, no, L, V16(0), v16_stride, st);
-    if (e != hipSuccess) return hip_fail(m, e, "mgn_forward halo copy");
-  }
-
-  RowsFwdArgs ra{};
-  ra.eps = m->cfg.ln_eps;
-  // EncNode: v^0 for owned nodes
-  ra.mlp = dev_mlp(m, m->enc_node());
-  ra.rows = no;
-  ra.fin = m->cfg.node_in;
-  ra.in0 = nf;
-  ra.out = V(0);
-  ra.out16 = V16(0);
-  {
-    Timed t_(m, MGN_T_ENCODE, st);
-    e = launch_rows_fwd(m->prec, L, D, ENC_NODE, ra, st);
-  }
-  if (e != hipSuccess) return hip_fail(m, e, "mgn_forward EncNode");
-  if (K > 0) {
-    ra.mlp = dev_mlp(m, m->enc_edge());
-    ra.rows = ne;
-    ra.fin = m->cfg.edge_in;
-    ra.in0 = ef;
-    ra.out = ES(0);
-    ra.out16 = nullptr;
-    {
-      Timed t_(m, MGN_T_ENCODE, st);
-      e = launch_rows_fwd(m->prec, L, D, ENC_EDGE, ra, st);
-    }
-    if (e != hipSuccess) return hip_fail(m, e, "mgn_forward EncEdge");
-  }
-  for (int k = 0; k < K; ++k) {
-    e = edge_forward_block(m, *g, p, ws, halo, k, V(k), V16(k), ES(k), k + 1 < K ? ES(k + 1) : nullptr, AGG(k), st);
-    if (e != hipSuccess) return hip_fail(m, e, "mgn_forward edge block");
-    RowsFwdArgs na{};
-    na.mlp = dev_mlp(m, m->node(k));
-    na.rows = no;
-    na.in0 = V(k);
-    na.in1 = AGG(k);
-    na.out = V(k + 1);
-    na.out16 = V16(k + 1);
-    na.in0_16 = V16(k);
-    na.hid_out = (p.HID_NK && !p.lean) ? (void*)((uint16_t*)(ws + p.HID_NK) + (size_t)k * no * L) : nullptr;
-    na.eps = m->cfg.ln_eps;
-    {
-      Timed t_(m, MGN_T_NODE_FWD, st);
-      e = launch_rows_fwd(m->prec, L, D, NODE_BLOCK, na, st);
-    }
-    if (e != hipSuccess) return hip_fail(m, e, "mgn_forward node block");
-  }
-  RowsFwdArgs da{};
-  da.mlp = dev_mlp(m, m->dec());
-  da.rows = no;
-  da.in0 = V(K);
-  da.out = out;
-  da.fout = m->cfg.node_out;
-  da.eps = m->cfg.ln_eps;
-  {
-    Timed t_(m, MGN_T_DECODE, st);
-    e = launch_rows_fwd(m->prec, L, D, DECODER, da, st);
-  }
-  if (e != hipSuccess) return hip_fail(m, e, "mgn_forward DecNode");
-  m->fwd_done = true;
-  m->g = *g;
-  m->nf = nf;
-  m->ef = ef;
-  m->halo = halo;
-  m->ws = ws;
-  m->plan = p;
-  return MGN_OK;
-}
-
-}  // extern "C"
-
 namespace {
 
 // Weight gradient of Linear j of an MLP: split-K GEMM into the partial
@@ -644,42 +538,209 @@ hipError_t run_vec(mgn_model* m, const MlpL& ml, float* d_params, int accumulate
 
 }  // namespace
 
-extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_params, int accumulate, float* d_halo,
-                                   mgn_stream stream) {
-  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_backward: model is NULL");
-  if (!m->fwd_done) return fail(m, MGN_E_STATE, "mgn_backward: no forward pass to differentiate");
-  if (!m->graph_ok || !same_graph(m->g, m->vg))
-    return fail(m, MGN_E_STATE, "mgn_backward: the graph changed since the forward pass");
-  if (!d_params || (m->g.n_owned > 0 && !d_out)) return fail(m, MGN_E_ARG, "mgn_backward: NULL argument");
-  if (!aligned(d_out, 4) || !aligned(d_params, 4) || !aligned(d_halo, 16))
-    return fail(m, MGN_E_ARG, "mgn_backward: misaligned pointer (d_halo 16 bytes)");
-  hipStream_t st = (hipStream_t)stream;
-  const WsPlan& p = m->plan;
-  char* ws = m->ws;
-  const mgn_graph* g = &m->g;
-  const int64_t no = g->n_owned, nh = g->n_halo, ne = g->n_edges;
-  const int L = m->L, K = m->K, D = m->D;
-  const size_t ts = tsize(m);
-  auto V = [&](int k) { return (float*)(ws + p.V) + (size_t)(p.lean ? (k & 1) : k) * no * L; };
-  auto AGG = [&](int k) { return (float*)(ws + p.AGG) + (size_t)(p.lean ? 0 : k) * no * L; };
-  auto ES = [&](int k) -> void* {
+namespace {
+
+// Views of the buffers of the model's current step (the plan, workspace and
+// graph recorded by the forward's first stage).
+struct Views {
+  const WsPlan& p;
+  char* ws;
+  int64_t no, nh, ne;
+  int L;
+  size_t ts;
+  bool bf16;
+  explicit Views(const mgn_model* m)
+      : p(m->plan), ws(m->ws), no(m->g.n_owned), nh(m->g.n_halo), ne(m->g.n_edges), L(m->L), ts(tsize(m)),
+        bf16(m->prec == BF16) {}
+  // fp32 node latents v^k (owned rows): every block's, or a ping-pong pair when checkpointing
+  float* V(int k) const { return (float*)(ws + p.V) + (size_t)(p.lean ? (k & 1) : k) * no * L; }
+  float* AGG(int k) const { return (float*)(ws + p.AGG) + (size_t)(p.lean ? 0 : k) * no * L; }
+  // edge latents e^k: every block's, or the checkpoint slots plus one working slot
+  void* ES(int k) const {
     const int slot = !p.lean ? k : (k % p.s == 0 ? k / p.s : p.nck);
     return (void*)(ws + p.ES + ts * (size_t)slot * ne * L);
-  };
-  auto V16 = [&](int k) -> void* {
-    return m->prec == BF16 ? (void*)((uint16_t*)(ws + p.V16) + (size_t)k * (no + nh) * L) : nullptr;
-  };
-  float* DV[2] = {(float*)(ws + p.DV[0]), (float*)(ws + p.DV[1])};
-  float* DE = (float*)(ws + p.DE);
-  float* DAGG = (float*)(ws + p.DAGG);
-  float* DZS = (float*)(ws + p.DZS);
-  float* VP = (float*)(ws + p.VPART);
-  int32_t* erecv = (int32_t*)(ws + p.erecv);
+  }
+  int64_t v16_stride() const { return (no + nh) * L; }  // elements per block of the bf16 node copy
+  void* V16(int k) const { return bf16 ? (void*)((uint16_t*)(ws + p.V16) + (size_t)k * v16_stride()) : nullptr; }
+};
+
+// ---- forward, in three stages: encoders, one block at a time, decoder
+
+mgn_status fwd_begin(mgn_model* m, const mgn_graph* g, const float* nf, const float* ef, const float* halo,
+                     float* out, void* workspace, size_t ws_bytes, hipStream_t st, const char* fn) {
+  const std::string f(fn);
+  if (!m) return fail(nullptr, MGN_E_ARG, f + ": model is NULL");
+  mgn_status s = check_graph_args(m, g);
+  if (s) return s;
+  if (!m->params_set) return fail(m, MGN_E_STATE, f + ": parameters were never set");
+  if (!m->graph_ok || !same_graph(*g, m->vg))
+    return fail(m, MGN_E_STATE, f + ": graph was not validated with mgn_graph_validate");
+  const int64_t no = g->n_owned, nh = g->n_halo, ne = g->n_edges;
+  if ((no > 0 && (!nf || !out)) || (ne > 0 && !ef)) return fail(m, MGN_E_ARG, f + ": input is NULL");
+  if (nh > 0 && m->K > 0 && !halo) return fail(m, MGN_E_ARG, f + ": halo is NULL but n_halo > 0");
+  if (!aligned(nf, 4) || !aligned(ef, 4) || !aligned(out, 4) || !aligned(halo, 16))
+    return fail(m, MGN_E_ARG, f + ": misaligned pointer (features 4 bytes, halo 16 bytes)");
+  if (!workspace || !aligned(workspace, 256))
+    return fail(m, MGN_E_ARG, f + ": workspace NULL or not 256-byte aligned");
+  const WsPlan p = make_plan(m, g);
+  if (ws_bytes < p.total)
+    return fail(m, MGN_E_NOMEM, f + ": workspace too small (need " + std::to_string(p.total) + " bytes)");
+  // the step's buffers, kept for the later stages and the backward
+  m->fwd_done = false;
+  m->fwd_next = -1;
+  m->bwd_active = false;
+  m->g = *g;
+  m->nf = nf;
+  m->ef = ef;
+  m->halo = halo;
+  m->out = out;
+  m->ws = (char*)workspace;
+  m->plan = p;
+  const Views b(m);
+  const int L = m->L, K = m->K, D = m->D;
+  const int te = edge_tile_rows(m->prec, L, D);
+  hipError_t e;
+  {
+    Timed t_(m, MGN_T_OTHER, st);
+    e = launch_erecv(g->row_ptr, no, (int32_t*)(b.ws + p.erecv), st);
+    if (e == hipSuccess)
+      e = launch_plan(g->row_ptr, no, 4 * te, 4 * te, (int32_t*)(b.ws + p.chunk), (int32_t*)(b.ws + p.unit_r),
+                      (int32_t*)(b.ws + p.nunits), st);
+  }
+  if (e != hipSuccess) return hip_fail(m, e, (f + " plan").c_str());
+  RowsFwdArgs ra{};
+  ra.eps = m->cfg.ln_eps;
+  // EncNode: v^0 for owned nodes
+  ra.mlp = dev_mlp(m, m->enc_node());
+  ra.rows = no;
+  ra.fin = m->cfg.node_in;
+  ra.in0 = nf;
+  ra.out = b.V(0);
+  ra.out16 = b.V16(0);
+  {
+    Timed t_(m, MGN_T_ENCODE, st);
+    e = launch_rows_fwd(m->prec, L, D, ENC_NODE, ra, st);
+  }
+  if (e != hipSuccess) return hip_fail(m, e, (f + " EncNode").c_str());
+  if (K > 0) {
+    ra.mlp = dev_mlp(m, m->enc_edge());
+    ra.rows = ne;
+    ra.fin = m->cfg.edge_in;
+    ra.in0 = ef;
+    ra.out = b.ES(0);
+    ra.out16 = nullptr;
+    {
+      Timed t_(m, MGN_T_ENCODE, st);
+      e = launch_rows_fwd(m->prec, L, D, ENC_EDGE, ra, st);
+    }
+    if (e != hipSuccess) return hip_fail(m, e, (f + " EncEdge").c_str());
+  }
+  m->fwd_next = 0;
+  return MGN_OK;
+}
+
+// Block k = fwd_next: reads halo[k] (when it runs), v^k, e^k; writes v^{k+1}, e^{k+1}.
+mgn_status fwd_block(mgn_model* m, hipStream_t st, const char* fn) {
+  const std::string f(fn);
+  if (!m) return fail(nullptr, MGN_E_ARG, f + ": model is NULL");
+  if (m->fwd_next < 0 || m->fwd_next >= m->K) return fail(m, MGN_E_STATE, f + ": no forward block is pending");
+  const int k = m->fwd_next;
+  m->fwd_next = -1;  // until the block is enqueued
+  const Views b(m);
+  const int L = m->L, K = m->K, D = m->D;
+  const int64_t no = b.no, nh = b.nh;
   hipError_t e = hipSuccess;
+  if (b.bf16 && nh > 0) {  // this block's halo rows of the bf16 node copy
+    Timed t_(m, MGN_T_OTHER, st);
+    e = launch_halo_bf16(m->halo + (size_t)k * nh * L, 1, nh, no, L, b.V16(k), b.v16_stride(), st);
+    if (e != hipSuccess) return hip_fail(m, e, (f + " halo copy").c_str());
+  }
+  e = edge_forward_block(m, m->g, b.p, b.ws, m->halo, k, b.V(k), b.V16(k), b.ES(k), k + 1 < K ? b.ES(k + 1) : nullptr,
+                         b.AGG(k), st);
+  if (e != hipSuccess) return hip_fail(m, e, (f + " edge block").c_str());
+  RowsFwdArgs na{};
+  na.mlp = dev_mlp(m, m->node(k));
+  na.rows = no;
+  na.in0 = b.V(k);
+  na.in1 = b.AGG(k);
+  na.out = b.V(k + 1);
+  na.out16 = b.V16(k + 1);
+  na.in0_16 = b.V16(k);
+  na.hid_out = (b.p.HID_NK && !b.p.lean) ? (void*)((uint16_t*)(b.ws + b.p.HID_NK) + (size_t)k * no * L) : nullptr;
+  na.eps = m->cfg.ln_eps;
+  {
+    Timed t_(m, MGN_T_NODE_FWD, st);
+    e = launch_rows_fwd(m->prec, L, D, NODE_BLOCK, na, st);
+  }
+  if (e != hipSuccess) return hip_fail(m, e, (f + " node block").c_str());
+  m->fwd_next = k + 1;
+  return MGN_OK;
+}
+
+mgn_status fwd_end(mgn_model* m, hipStream_t st, const char* fn) {
+  const std::string f(fn);
+  if (!m) return fail(nullptr, MGN_E_ARG, f + ": model is NULL");
+  if (m->fwd_next != m->K) return fail(m, MGN_E_STATE, f + ": the forward's blocks have not all run");
+  m->fwd_next = -1;
+  const Views b(m);
+  RowsFwdArgs da{};
+  da.mlp = dev_mlp(m, m->dec());
+  da.rows = b.no;
+  da.in0 = b.V(m->K);
+  da.out = m->out;
+  da.fout = m->cfg.node_out;
+  da.eps = m->cfg.ln_eps;
+  hipError_t e;
+  {
+    Timed t_(m, MGN_T_DECODE, st);
+    e = launch_rows_fwd(m->prec, m->L, m->D, DECODER, da, st);
+  }
+  if (e != hipSuccess) return hip_fail(m, e, (f + " DecNode").c_str());
+  m->fwd_done = true;
+  return MGN_OK;
+}
+
+// ---- backward, in three stages: decoder, one block at a time (K-1 .. 0), encoders
+
 #define CHK(what) \
   if (e != hipSuccess) return hip_fail(m, e, "mgn_backward " what);
 
-  auto rows_args = [&](const MlpL& ml, int64_t rows, void* const* del, void* const* hid) {
+struct Bwd {
+  mgn_model* m;
+  hipStream_t st;
+  Views b;
+  const WsPlan& p;
+  char* ws;
+  const mgn_graph* g;
+  int64_t no, nh, ne;
+  int L, K, D;
+  size_t ts;
+  float* DV[2];
+  float *DE, *DAGG, *DZS, *VP;
+  int32_t* erecv;
+  void *DEL_N[3], *HID_N[2], *DEL_E[3], *HID_E[2];
+  float* d_params;
+  int accumulate;
+  size_t nch;  // edge chunks of the backward
+
+  Bwd(mgn_model* m_, hipStream_t s)
+      : m(m_), st(s), b(m_), p(m_->plan), ws(m_->ws), g(&m_->g), no(b.no), nh(b.nh), ne(b.ne), L(m_->L), K(m_->K),
+        D(m_->D), ts(b.ts), d_params(m_->d_params), accumulate(m_->accumulate) {
+    DV[0] = (float*)(ws + p.DV[0]);
+    DV[1] = (float*)(ws + p.DV[1]);
+    DE = (float*)(ws + p.DE);
+    DAGG = (float*)(ws + p.DAGG);
+    DZS = (float*)(ws + p.DZS);
+    VP = (float*)(ws + p.VPART);
+    erecv = (int32_t*)(ws + p.erecv);
+    for (int j = 0; j < 3; ++j) DEL_N[j] = ws + p.DEL_N[j];
+    for (int j = 0; j < 2; ++j) HID_N[j] = ws + p.HID_N[j];
+    for (int j = 0; j < 3; ++j) DEL_E[j] = ws + p.DEL_E[j];
+    for (int j = 0; j < 2; ++j) HID_E[j] = ws + p.HID_E[j];
+    nch = p.cr.size() - 1;
+  }
+
+  RowsBwdArgs rows_args(const MlpL& ml, int64_t rows, void* const* del, void* const* hid) const {
     RowsBwdArgs a{};
     a.mlp = dev_mlp(m, ml);
     a.rows = rows;
@@ -689,15 +750,10 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
     for (int j = 0; j < 3; ++j) a.delta[j] = del[j];
     for (int j = 0; j < 2; ++j) a.hid[j] = hid[j];
     return a;
-  };
-  void* DEL_N[3] = {ws + p.DEL_N[0], ws + p.DEL_N[1], ws + p.DEL_N[2]};
-  void* HID_N[2] = {ws + p.HID_N[0], ws + p.HID_N[1]};
-  void* DEL_E[3] = {ws + p.DEL_E[0], ws + p.DEL_E[1], ws + p.DEL_E[2]};
-  void* HID_E[2] = {ws + p.HID_E[0], ws + p.HID_E[1]};
+  }
 
   // weight gradients of the hidden / last Linears from the stored activations
-  auto dw_hidden = [&](const MlpL& ml, int64_t R, void* const* del, void* const* hid, int ld_last,
-                       int acc) -> hipError_t {
+  hipError_t dw_hidden(const MlpL& ml, int64_t R, void* const* del, void* const* hid, int ld_last, int acc) {
     for (int j = 1; j < D; ++j) {
       DwArgs a{};
       a.delta = del[j];
@@ -710,16 +766,16 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       if (r != hipSuccess) return r;
     }
     return hipSuccess;
-  };
+  }
 
-  // ---- decoder
-  int a_ = 0;  // DV[a_] holds dL/dv^{k+1}
-  {
+  // DecNode: dL/dv^K into DV[0]
+  mgn_status decoder(const float* d_out) {
+    hipError_t e;
     const MlpL& ml = m->dec();
     RowsBwdArgs a = rows_args(ml, no, DEL_N, HID_N);
-    a.in0 = V(K);
+    a.in0 = b.V(K);
     a.dm = d_out;
-    a.dx0 = DV[a_];
+    a.dx0 = DV[0];
     a.fout = m->cfg.node_out;
     {
       Timed t_(m, MGN_T_NODE_BWD, st);
@@ -732,17 +788,20 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
     w.delta = DEL_N[0];
     w.ldd = L;
     w.a_kind = 1;
-    w.a0 = V(K);
+    w.a0 = b.V(K);
     w.lda0 = L;
     w.R = no;
     e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
     CHK("decoder dW");
     e = dw_hidden(ml, no, DEL_N, HID_N, 16, accumulate);
     CHK("decoder dW");
+    return MGN_OK;
   }
-  // ---- processor, last block first
-  const size_t nch = p.cr.size() - 1;  // edge chunks of the backward
-  for (int k = K - 1; k >= 0; --k) {
+
+  // Block k: DV[a_] holds dL/dv^{k+1} (owned rows); writes dL/dv^k into
+  // DV[1 - a_] and dL/dhalo[k] into d_halo_k (when not null).
+  mgn_status block(int k, int a_, float* d_halo_k) {
+    hipError_t e = hipSuccess;
     const int b_ = 1 - a_;
     const float* Hk = nh > 0 ? m->halo + (size_t)k * nh * L : nullptr;
     if (p.lean) {
@@ -750,18 +809,18 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       // then block k's forward once more for agg^k (and its projections)
       const int b0 = k - k % p.s;
       for (int j = b0; j < k; ++j) {
-        e = edge_forward_block(m, *g, p, ws, m->halo, j, V(j), V16(j), ES(j), ES(j + 1), AGG(0), st);
+        e = edge_forward_block(m, *g, p, ws, m->halo, j, b.V(j), b.V16(j), b.ES(j), b.ES(j + 1), b.AGG(0), st);
         CHK("edge-stream recompute");
       }
-      e = edge_forward_block(m, *g, p, ws, m->halo, k, V(k), V16(k), ES(k), nullptr, AGG(0), st);
+      e = edge_forward_block(m, *g, p, ws, m->halo, k, b.V(k), b.V16(k), b.ES(k), nullptr, b.AGG(0), st);
       CHK("aggregate recompute");
     }
     {
       const MlpL& ml = m->node(k);
       RowsBwdArgs a = rows_args(ml, no, DEL_N, HID_N);
-      a.in0 = p.lean ? nullptr : V(k);
-      a.in0_16 = p.lean ? V16(k) : nullptr;  // the bf16 copy is the product operand either way
-      a.in1 = AGG(k);
+      a.in0 = p.lean ? nullptr : b.V(k);
+      a.in0_16 = p.lean ? b.V16(k) : nullptr;  // the bf16 copy is the product operand either way
+      a.in1 = b.AGG(k);
       void* hidk[2] = {HID_N[0], HID_N[1]};
       if (p.HID_NK) {  // the forward's ReLU output of this block
         uint16_t* hk = (uint16_t*)(ws + p.HID_NK) + (p.lean ? 0 : (size_t)k * no * L);
@@ -769,8 +828,8 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
           RowsFwdArgs ra{};
           ra.mlp = a.mlp;
           ra.rows = no;
-          ra.in1 = AGG(k);
-          ra.in0_16 = V16(k);
+          ra.in1 = b.AGG(k);
+          ra.in0_16 = b.V16(k);
           ra.hid_out = hk;
           ra.eps = m->cfg.ln_eps;
           Timed t_(m, MGN_T_NODE_BWD, st);
@@ -795,12 +854,12 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       w.ldd = L;
       if (p.lean) {
         w.a_kind = 5;
-        w.a3 = V16(k);
+        w.a3 = b.V16(k);
       } else {
         w.a_kind = 3;
-        w.a0 = V(k);
+        w.a0 = b.V(k);
       }
-      w.a1 = AGG(k);
+      w.a1 = b.AGG(k);
       w.R = no;
       e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
       CHK("node dW");
@@ -816,11 +875,11 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       a.erecv = erecv;
       a.unit_r = (int32_t*)(ws + p.unit_r);
       a.n_units = (int32_t*)(ws + p.nunits);
-      a.V = V(k);
+      a.V = b.V(k);
       a.H = Hk;
-      a.V16 = V16(k);
+      a.V16 = b.V16(k);
       a.n_owned = no;
-      a.Ein = ES(k);
+      a.Ein = b.ES(k);
       a.de_next = (k == K - 1) ? nullptr : DE;  // dL/de is updated in place
       a.dagg = DAGG;
       a.de_out = DE;
@@ -853,7 +912,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
         w.delta = DEL_E[0];
         w.ldd = L;
         w.a_kind = 0;
-        w.a0 = (const char*)ES(k) + ts * (size_t)e0 * L;
+        w.a0 = (const char*)b.ES(k) + ts * (size_t)e0 * L;
         w.lda0 = L;
         w.R = rows;
         e = run_dw(m, ml.lin[0], w, d_params, acc, st, 0, L);
@@ -872,7 +931,7 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       ig.dz = DEL_E[0];
       ig.dzr = DAGG;
       ig.dv = DV[b_];
-      ig.dh = d_halo ? d_halo + (size_t)k * nh * L : nullptr;
+      ig.dh = d_halo_k;
       ig.dzs = DZS;
       ig.dzs_ready = nch > 1;
       ig.n_local = no + nh;
@@ -894,10 +953,10 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
         wn.R = side == 0 ? no + nh : no;
         if (m->prec == BF16) {
           wn.a_kind = 0;
-          wn.a0 = V16(k);
+          wn.a0 = b.V16(k);
         } else {
           wn.a_kind = 4;
-          wn.a0 = V(k);
+          wn.a0 = b.V(k);
           wn.a2 = Hk;
           wn.n_owned = no;
         }
@@ -905,35 +964,37 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
         CHK("edge dW (node blocks)");
       }
     }
-    a_ = b_;
+    return MGN_OK;
   }
-  // ---- encoders
-  {
-    const MlpL& ml = m->enc_node();
-    RowsBwdArgs a = rows_args(ml, no, DEL_N, HID_N);
-    a.in0 = m->nf;
-    a.fin = m->cfg.node_in;
-    a.dm = DV[a_];
+
+  // EncNode and EncEdge from dL/dv^0 (DV[a_]) and dL/de^0 (DE)
+  mgn_status encoders(int a_) {
+    hipError_t e = hipSuccess;
     {
-      Timed t_(m, MGN_T_NODE_BWD, st);
-      e = launch_rows_bwd(m->prec, L, D, ENC_NODE, a, BWD_GRID, st);
+      const MlpL& ml = m->enc_node();
+      RowsBwdArgs a = rows_args(ml, no, DEL_N, HID_N);
+      a.in0 = m->nf;
+      a.fin = m->cfg.node_in;
+      a.dm = DV[a_];
+      {
+        Timed t_(m, MGN_T_NODE_BWD, st);
+        e = launch_rows_bwd(m->prec, L, D, ENC_NODE, a, BWD_GRID, st);
+      }
+      CHK("EncNode");
+      e = run_vec(m, ml, d_params, accumulate, st);
+      CHK("EncNode vec");
+      DwArgs w{};
+      w.delta = DEL_N[0];
+      w.ldd = L;
+      w.a_kind = 1;
+      w.a0 = m->nf;
+      w.lda0 = m->cfg.node_in;
+      w.R = no;
+      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
+      CHK("EncNode dW");
+      e = dw_hidden(ml, no, DEL_N, HID_N, L, accumulate);
+      CHK("EncNode dW");
     }
-    CHK("EncNode");
-    e = run_vec(m, ml, d_params, accumulate, st);
-    CHK("EncNode vec");
-    DwArgs w{};
-    w.delta = DEL_N[0];
-    w.ldd = L;
-    w.a_kind = 1;
-    w.a0 = m->nf;
-    w.lda0 = m->cfg.node_in;
-    w.R = no;
-    e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
-    CHK("EncNode dW");
-    e = dw_hidden(ml, no, DEL_N, HID_N, L, accumulate);
-    CHK("EncNode dW");
-  }
-  {
     const MlpL& ml = m->enc_edge();
     if (K > 0 && ne > 0) {
       // over the same edge chunks as the blocks (per-edge gradients stored per chunk)
@@ -965,15 +1026,166 @@ extern "C" mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_pa
       }
     } else if (!accumulate) {
       // no edges reach the output: the edge encoder's gradient is zero
-      const int64_t b = ml.lin[0].w;
+      const int64_t b0 = ml.lin[0].w;
       const int64_t end = ml.beta + ml.lin[D - 1].out;
-      e = launch_zero(d_params + b, end - b, st);
+      e = launch_zero(d_params + b0, end - b0, st);
       CHK("EncEdge zero");
     }
+    return MGN_OK;
   }
+};
+
 #undef CHK
+
+mgn_status bwd_begin(mgn_model* m, const float* d_out, float* d_params, int accumulate, float* d_halo,
+                     hipStream_t st, const char* fn) {
+  const std::string f(fn);
+  if (!m) return fail(nullptr, MGN_E_ARG, f + ": model is NULL");
+  if (!m->fwd_done) return fail(m, MGN_E_STATE, f + ": no forward pass to differentiate");
+  if (!m->graph_ok || !same_graph(m->g, m->vg))
+    return fail(m, MGN_E_STATE, f + ": the graph changed since the forward pass");
+  if (!d_params || (m->g.n_owned > 0 && !d_out)) return fail(m, MGN_E_ARG, f + ": NULL argument");
+  if (!aligned(d_out, 4) || !aligned(d_params, 4) || !aligned(d_halo, 16))
+    return fail(m, MGN_E_ARG, f + ": misaligned pointer (d_halo 16 bytes)");
+  m->bwd_active = false;
+  m->d_params = d_params;
+  m->accumulate = accumulate;
+  m->d_halo = d_halo;
+  Bwd w(m, st);
+  mgn_status s = w.decoder(d_out);
+  if (s) return s;
+  m->bwd_active = true;
+  m->bwd_next = m->K - 1;
+  m->bwd_a = 0;
   return MGN_OK;
 }
+
+mgn_status bwd_block(mgn_model* m, hipStream_t st, const char* fn) {
+  const std::string f(fn);
+  if (!m) return fail(nullptr, MGN_E_ARG, f + ": model is NULL");
+  if (!m->bwd_active || !m->fwd_done || m->bwd_next < 0)
+    return fail(m, MGN_E_STATE, f + ": no backward block is pending");
+  const int k = m->bwd_next;
+  m->bwd_active = false;  // until the block is enqueued
+  Bwd w(m, st);
+  const int64_t nh = m->g.n_halo;
+  mgn_status s = w.block(k, m->bwd_a, m->d_halo ? m->d_halo + (size_t)k * nh * m->L : nullptr);
+  if (s) return s;
+  m->bwd_a = 1 - m->bwd_a;
+  m->bwd_next = k - 1;
+  m->bwd_active = true;
+  return MGN_OK;
+}
+
+mgn_status bwd_end(mgn_model* m, hipStream_t st, const char* fn) {
+  const std::string f(fn);
+  if (!m) return fail(nullptr, MGN_E_ARG, f + ": model is NULL");
+  if (!m->bwd_active || !m->fwd_done || m->bwd_next != -1)
+    return fail(m, MGN_E_STATE, f + ": the backward's blocks have not all run");
+  m->bwd_active = false;
+  Bwd w(m, st);
+  return w.encoders(m->bwd_a);
+}
+
+}  // namespace
+
+extern "C" {
+
+mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* nf, const float* ef, const float* halo,
+                       float* out, void* workspace, size_t ws_bytes, mgn_stream stream) {
+  hipStream_t st = (hipStream_t)stream;
+  mgn_status s = fwd_begin(m, g, nf, ef, halo, out, workspace, ws_bytes, st, "mgn_forward");
+  for (int k = 0; s == MGN_OK && k < m->K; ++k) s = fwd_block(m, st, "mgn_forward");
+  if (s == MGN_OK) s = fwd_end(m, st, "mgn_forward");
+  return s;
+}
+
+mgn_status mgn_forward_begin(mgn_model* m, const mgn_graph* g, const float* nf, const float* ef, const float* halo,
+                             float* out, void* workspace, size_t ws_bytes, mgn_stream stream) {
+  return fwd_begin(m, g, nf, ef, halo, out, workspace, ws_bytes, (hipStream_t)stream, "mgn_forward_begin");
+}
+
+mgn_status mgn_forward_block(mgn_model* m, mgn_stream stream) {
+  return fwd_block(m, (hipStream_t)stream, "mgn_forward_block");
+}
+
+mgn_status mgn_forward_end(mgn_model* m, mgn_stream stream) {
+  return fwd_end(m, (hipStream_t)stream, "mgn_forward_end");
+}
+
+mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_params, int accumulate, float* d_halo,
+                        mgn_stream stream) {
+  hipStream_t st = (hipStream_t)stream;
+  mgn_status s = bwd_begin(m, d_out, d_params, accumulate, d_halo, st, "mgn_backward");
+  for (int k = 0; s == MGN_OK && k < m->K; ++k) s = bwd_block(m, st, "mgn_backward");
+  if (s == MGN_OK) s = bwd_end(m, st, "mgn_backward");
+  return s;
+}
+
+mgn_status mgn_backward_begin(mgn_model* m, const float* d_out, float* d_params, int accumulate, float* d_halo,
+                              mgn_stream stream) {
+  return bwd_begin(m, d_out, d_params, accumulate, d_halo, (hipStream_t)stream, "mgn_backward_begin");
+}
+
+mgn_status mgn_backward_block(mgn_model* m, mgn_stream stream) {
+  return bwd_block(m, (hipStream_t)stream, "mgn_backward_block");
+}
+
+mgn_status mgn_backward_end(mgn_model* m, mgn_stream stream) {
+  return bwd_end(m, (hipStream_t)stream, "mgn_backward_end");
+}
+
+mgn_status mgn_halo_masks(const int32_t* l2g_p, int64_t n_owned_p, int64_t n_halo_p, const int32_t* part,
+                          int64_t n_nodes, const int32_t* l2g_q, int64_t n_owned_q, int32_t q, int32_t* recv_idx,
+                          int32_t* send_rows, int64_t* count) {
+  return halo_masks(l2g_p, n_owned_p, n_halo_p, part, n_nodes, l2g_q, n_owned_q, q, recv_idx, send_rows, count,
+                    g_err);
+}
+
+mgn_status mgn_copy_latents(const mgn_model* owner, const int32_t* send_rows, const int32_t* recv_idx, int64_t n,
+                            float* halo_k, int64_t n_halo, mgn_stream stream) {
+  mgn_model* m = const_cast<mgn_model*>(owner);
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_copy_latents: model is NULL");
+  if (n < 0 || n_halo < 0) return fail(m, MGN_E_ARG, "mgn_copy_latents: negative size");
+  if (n == 0) return MGN_OK;
+  if (!send_rows || !recv_idx || !halo_k) return fail(m, MGN_E_ARG, "mgn_copy_latents: NULL argument");
+  if (!aligned(send_rows, 4) || !aligned(recv_idx, 4) || !aligned(halo_k, 16))
+    return fail(m, MGN_E_ARG, "mgn_copy_latents: misaligned pointer (halo_k 16 bytes)");
+  int j;
+  if (m->fwd_next >= 0)
+    j = m->fwd_next;
+  else if (m->fwd_done)
+    j = m->K;
+  else
+    return fail(m, MGN_E_STATE, "mgn_copy_latents: the owner has no forward pass in progress or done");
+  const Views b(m);
+  Timed t_(m, MGN_T_EXCHANGE, (hipStream_t)stream);
+  hipError_t e = launch_rows_copy(b.V(j), b.no, send_rows, recv_idx, n, m->L, halo_k, n_halo, 0, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_copy_latents");
+  return MGN_OK;
+}
+
+mgn_status mgn_add_latent_grads(mgn_model* owner, const float* d_halo_k, int64_t n_halo, const int32_t* recv_idx,
+                                const int32_t* send_rows, int64_t n, mgn_stream stream) {
+  mgn_model* m = owner;
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_add_latent_grads: model is NULL");
+  if (n < 0 || n_halo < 0) return fail(m, MGN_E_ARG, "mgn_add_latent_grads: negative size");
+  if (!m->bwd_active || !m->fwd_done)
+    return fail(m, MGN_E_STATE, "mgn_add_latent_grads: the owner has no backward pass in progress");
+  if (n == 0) return MGN_OK;
+  if (!send_rows || !recv_idx || !d_halo_k) return fail(m, MGN_E_ARG, "mgn_add_latent_grads: NULL argument");
+  if (!aligned(send_rows, 4) || !aligned(recv_idx, 4) || !aligned(d_halo_k, 16))
+    return fail(m, MGN_E_ARG, "mgn_add_latent_grads: misaligned pointer (d_halo_k 16 bytes)");
+  const Views b(m);
+  float* dv = (float*)(b.ws + b.p.DV[m->bwd_a]);
+  Timed t_(m, MGN_T_EXCHANGE, (hipStream_t)stream);
+  hipError_t e =
+      launch_rows_copy(d_halo_k, n_halo, recv_idx, send_rows, n, m->L, dv, b.no, 1, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_add_latent_grads");
+  return MGN_OK;
+}
+
+}  // extern "C"
 
 extern "C" mgn_status mgn_mse_grad(const float* out, const float* target, const uint8_t* mask, int64_t n, int32_t d,
                                    float* loss, float* d_out, mgn_stream stream) {

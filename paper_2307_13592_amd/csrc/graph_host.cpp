@@ -140,6 +140,45 @@ mgn_status graph_build(const int32_t* send, const int32_t* recv, int64_t n_edges
   return MGN_OK;
 }
 
+// The exchange lists between parts p and q (Algorithm 1's create_masks for
+// one neighbour): the halo nodes of p owned by q, by ascending halo index j
+// (p's local id n_owned_p + j), with the local id each has in q (q's owned
+// nodes are its l2g prefix, ascending global ids: a binary search).
+mgn_status halo_masks(const int32_t* l2g_p, int64_t n_owned_p, int64_t n_halo_p, const int32_t* part,
+                      int64_t n_nodes, const int32_t* l2g_q, int64_t n_owned_q, int32_t q, int32_t* recv_idx,
+                      int32_t* send_rows, int64_t* count, std::string& err) {
+  if (n_owned_p < 0 || n_halo_p < 0 || n_owned_q < 0 || n_nodes < 0 || !count ||
+      (n_owned_p + n_halo_p > 0 && !l2g_p) || (n_owned_q > 0 && !l2g_q) || (n_nodes > 0 && !part) ||
+      (n_halo_p > 0 && (!recv_idx || !send_rows))) {
+    err = "mgn_halo_masks: bad arguments";
+    return MGN_E_ARG;
+  }
+  for (int64_t i = 0; i < n_owned_q; ++i)
+    if ((uint32_t)l2g_q[i] >= (uint64_t)n_nodes || (i > 0 && l2g_q[i - 1] >= l2g_q[i]) || part[l2g_q[i]] != q) {
+      err = "mgn_halo_masks: q's owned nodes are not ascending global ids of part q";
+      return MGN_E_GRAPH;
+    }
+  int64_t c = 0;
+  for (int64_t j = 0; j < n_halo_p; ++j) {
+    const int32_t gid = l2g_p[n_owned_p + j];
+    if ((uint32_t)gid >= (uint64_t)n_nodes) {
+      err = "mgn_halo_masks: halo node id out of range";
+      return MGN_E_GRAPH;
+    }
+    if (part[gid] != q) continue;
+    const int32_t* it = std::lower_bound(l2g_q, l2g_q + n_owned_q, gid);
+    if (it == l2g_q + n_owned_q || *it != gid) {
+      err = "mgn_halo_masks: a halo node of part q is not among q's owned nodes";
+      return MGN_E_GRAPH;
+    }
+    recv_idx[c] = (int32_t)j;
+    send_rows[c] = (int32_t)(it - l2g_q);
+    ++c;
+  }
+  *count = c;
+  return MGN_OK;
+}
+
 // Structural checks of a local graph held in host copies of the device arrays.
 mgn_status graph_check(int64_t no, int64_t nh, int64_t ne, const int32_t* row_ptr, const int32_t* send,
                        const int32_t* trow, const int32_t* tedge, std::string& err) {

@@ -132,6 +132,11 @@ struct VecSeg {
 hipError_t launch_zero(float* p, int64_t n, hipStream_t st);
 hipError_t launch_halo_bf16(const float* H, int K, int64_t n_halo, int64_t n_owned, int L, void* V16,
                             int64_t v16_block_stride, hipStream_t st);
+// Halo exchange between partitions on one device: dst[dst_rows[i]] = (or +=,
+// add != 0) src[src_rows[i]], rows of L floats (L a multiple of 4, 16-byte
+// aligned rows); pairs with out-of-range indices are skipped.
+hipError_t launch_rows_copy(const float* src, int64_t n_src, const int32_t* src_rows, const int32_t* dst_rows,
+                            int64_t n, int L, float* dst, int64_t n_dst, int add, hipStream_t st);
 hipError_t launch_pack(int prec, const float* W, int out, int in, int bwd, uint4* dst, int nkg, hipStream_t st);
 hipError_t launch_erecv(const int32_t* row_ptr, int64_t n_owned, int32_t* erecv, hipStream_t st);
 hipError_t launch_plan(const int32_t* row_ptr, int64_t n_owned, int te_target, int r_max, int32_t* chunk_cnt,

@@ -380,6 +380,44 @@ hipError_t launch_halo_bf16(const float* H, int K, int64_t n_halo, int64_t n_own
   return hipGetLastError();
 }
 
+// ------------------------------------------------------- halo exchange ---
+// Row copy between two node-row buffers of width L = 4 * L4 floats, the
+// one-GPU form of Algorithm 1's pack / exchange / unpack:
+// dst[dst_rows[i]] = src[src_rows[i]] (add == 0) or += (add == 1).  A pair
+// with an index outside [0, n_src) or [0, n_dst) is skipped.
+__global__ void rows_copy_kernel(const float* __restrict__ src, int64_t n_src, const int32_t* __restrict__ src_rows,
+                                 const int32_t* __restrict__ dst_rows, int64_t n, int L4, float* __restrict__ dst,
+                                 int64_t n_dst, int add) {
+  const int64_t total = n * L4;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = t / L4;
+    const int c = (int)(t - i * L4);
+    const int32_t s = src_rows[i], d = dst_rows[i];
+    if (s < 0 || s >= n_src || d < 0 || d >= n_dst) continue;
+    const float4 v = reinterpret_cast<const float4*>(src + (int64_t)s * L4 * 4)[c];
+    float4* q = reinterpret_cast<float4*>(dst + (int64_t)d * L4 * 4) + c;
+    if (add) {
+      float4 o = *q;
+      o.x += v.x;
+      o.y += v.y;
+      o.z += v.z;
+      o.w += v.w;
+      *q = o;
+    } else {
+      *q = v;
+    }
+  }
+}
+
+hipError_t launch_rows_copy(const float* src, int64_t n_src, const int32_t* src_rows, const int32_t* dst_rows,
+                            int64_t n, int L, float* dst, int64_t n_dst, int add, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int64_t g = (n * (L / 4) + NT - 1) / NT;
+  hipLaunchKernelGGL(rows_copy_kernel, dim3((unsigned)(g < 8192 ? g : 8192)), dim3(NT), 0, st, src, n_src, src_rows,
+                     dst_rows, n, L / 4, dst, n_dst, add);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------- planning ---
 __global__ void erecv_kernel(const int32_t* __restrict__ row_ptr, int64_t n_owned, int32_t* __restrict__ erecv) {
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;

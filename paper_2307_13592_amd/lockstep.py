@@ -1,0 +1,84 @@
+"""Several partitions of one mesh stepped in lockstep on one device: the
+paper's distributed training step (Algorithm 1) with the partitions side by
+side on one GPU instead of one per GPU.  One Session (model, workspace,
+inputs) per part, all with the same parameters; after every block of the
+forward the halo latents move from their owners into the parts that hold
+them as halo, and after every block of the backward the halo gradients go
+back to the owners (section "Methodology": forward halo exchange and
+backward gradient exchange).  The parts' parameter gradients add up in one
+buffer in part order, which takes the place of the gradient all-reduce.
+
+Call order and argument marshalling only: every step, the exchanges
+included, runs in libmgn's kernels."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import (mgn_add_latent_grads, mgn_backward_begin, mgn_backward_block, mgn_backward_end, mgn_copy_latents,
+               mgn_forward_begin, mgn_forward_block, mgn_forward_end, mgn_halo_masks)
+from .runner import Session
+
+
+class Lockstep:
+    """P parts of one mesh; graphs[p] from mgn_graph_build(..., part, n_nodes, p),
+    node_feats[p] / edge_feats[p] the part's owned-node and local-edge
+    features (local order)."""
+
+    def __init__(self, latent: int, K: int, depth: int, precision: str, part, graphs: list, node_feats: list,
+                 edge_feats: list, params, device: str = "cuda", recompute: int = 0):
+        self.K, self.latent, self.P = K, latent, len(graphs)
+        self.device = torch.device(device)
+        self.sessions = []
+        for g, nf, ef in zip(graphs, node_feats, edge_feats):
+            halo = np.zeros((K, g["n_halo"], latent), np.float32)  # filled by the exchange, block by block
+            self.sessions.append(Session(latent, K, depth, precision, g, nf, ef, halo, params, device,
+                                         recompute=recompute))
+        dev = lambda a: torch.as_tensor(a).to(self.device)
+        # (p, q, recv_idx, send_rows): p's halo nodes owned by q
+        self.links = []
+        for p, gp in enumerate(graphs):
+            for q, gq in enumerate(graphs):
+                if q == p or gp["n_halo"] == 0:
+                    continue
+                recv, send = mgn_halo_masks(gp["l2g"], gp["n_owned"], part, gq["l2g"], gq["n_owned"], q)
+                if recv.size:
+                    self.links.append((p, q, dev(recv), dev(send)))
+        self.d_params = torch.empty(self.sessions[0].n_params, dtype=torch.float32, device=self.device)
+
+    def forward(self, stream=None):
+        S = self.sessions
+        for s in S:
+            mgn_forward_begin(s.model, s.gs, s.node_feat, s.edge_feat, s.halo, s.out, s.workspace, stream)
+        for k in range(self.K):
+            for p, q, recv, send in self.links:
+                mgn_copy_latents(S[q].model, send, recv, S[p].halo[k], stream)
+            for s in S:
+                mgn_forward_block(s.model, stream)
+        for s in S:
+            mgn_forward_end(s.model, stream)
+        return [s.out for s in S]
+
+    def backward(self, d_outs, stream=None):
+        """d_outs[p]: dL/dout of part p's owned nodes.  Returns the summed
+        parameter gradient."""
+        S = self.sessions
+        for i, (s, d) in enumerate(zip(S, d_outs)):
+            if not isinstance(d, torch.Tensor):
+                d = torch.as_tensor(np.ascontiguousarray(d, np.float32)).to(self.device)
+            s._d_out = d.contiguous()  # kept alive until the backward ends
+            mgn_backward_begin(s.model, s._d_out, self.d_params, i > 0, s.d_halo, stream)
+        for k in reversed(range(self.K)):
+            for s in S:
+                mgn_backward_block(s.model, stream)
+            for p, q, recv, send in self.links:
+                mgn_add_latent_grads(S[q].model, S[p].d_halo[k], recv, send, stream)
+        for s in S:
+            mgn_backward_end(s.model, stream)
+        return self.d_params
+
+    def close(self):
+        for s in self.sessions:
+            s.close()
+        self.sessions = []
+        self.links = []

@@ -154,3 +154,72 @@ def test_recompute_setting():
         assert n0.value - n4.value >= 5 * 20000 * 64 * 2
     finally:
         mgn.mgn_destroy(h)
+
+
+@pytest.mark.parametrize("mesh,P,random", [
+    (meshes.sector(6, 16, 10, 4, seed=7), 4, False),
+    (meshes.delaunay_box(9, 8, 7, seed=5), 5, True),
+])
+def test_halo_masks_brute_force(mesh, P, random):
+    """Exchange lists of every (part, owner) pair against their definition
+    (halo nodes of p owned by q, ascending halo index; q's local id of each),
+    written with Python dicts; every halo node is in exactly one owner's list."""
+    if random:
+        part = np.random.default_rng(3).integers(0, P, mesh.n_nodes).astype(np.int32)
+    else:
+        part = mgn.mgn_partition_slabs(mesh.key, P)
+    gs = [mgn.mgn_graph_build(mesh.send, mesh.recv, part, mesh.n_nodes, p) for p in range(P)]
+    for p in range(P):
+        no_p = gs[p]["n_owned"]
+        halo_g = [int(x) for x in gs[p]["l2g"][no_p:]]
+        covered = 0
+        for q in range(P):
+            if q == p:
+                continue
+            recv, send = mgn.mgn_halo_masks(gs[p]["l2g"], no_p, part, gs[q]["l2g"], gs[q]["n_owned"], q)
+            pos = {int(gid): i for i, gid in enumerate(gs[q]["l2g"][:gs[q]["n_owned"]])}
+            want_recv = [j for j, gid in enumerate(halo_g) if part[gid] == q]
+            want_send = [pos[halo_g[j]] for j in want_recv]
+            assert recv.tolist() == want_recv and send.tolist() == want_send
+            covered += len(want_recv)
+        assert covered == len(halo_g)
+
+
+def test_halo_masks_errors():
+    mesh = meshes.sector(4, 12, 5, 4, seed=1)
+    part = mgn.mgn_partition_slabs(mesh.key, 4)
+    g0 = mgn.mgn_graph_build(mesh.send, mesh.recv, part, mesh.n_nodes, 0)
+    g1 = mgn.mgn_graph_build(mesh.send, mesh.recv, part, mesh.n_nodes, 1)
+    bad = g1["l2g"].copy()
+    bad[[0, 1]] = bad[[1, 0]]  # q's owned list no longer ascending
+    with pytest.raises(mgn.MgnError) as e:
+        mgn.mgn_halo_masks(g0["l2g"], g0["n_owned"], part, bad, g1["n_owned"], 1)
+    assert e.value.status == mgn.MGN_E_GRAPH
+    with pytest.raises(mgn.MgnError) as e:  # q = 2 does not own g1's nodes
+        mgn.mgn_halo_masks(g0["l2g"], g0["n_owned"], part, g1["l2g"], g1["n_owned"], 2)
+    assert e.value.status == mgn.MGN_E_GRAPH
+
+
+def test_staged_state_errors_before_any_launch():
+    """The stages of a staged step called out of order, and the exchanges
+    without a step in progress: MGN_E_STATE, nothing launched."""
+    import ctypes as C
+    L = mgn.lib()
+    h = mgn.mgn_create(64, 2, 2)
+    try:
+        fake = C.c_void_p(4096)
+        for call, what in ((lambda: L.mgn_forward_block(h, None), "no forward block"),
+                           (lambda: L.mgn_forward_end(h, None), "not all run"),
+                           (lambda: L.mgn_backward_begin(h, fake, fake, 0, None, None), "no forward"),
+                           (lambda: L.mgn_backward_block(h, None), "no backward block"),
+                           (lambda: L.mgn_backward_end(h, None), "not all run"),
+                           (lambda: L.mgn_copy_latents(h, fake, fake, 3, fake, 5, None), "no forward"),
+                           (lambda: L.mgn_add_latent_grads(h, fake, 5, fake, fake, 3, None), "no backward")):
+            assert call() == mgn.MGN_E_STATE
+            assert what in mgn.mgn_last_error(h)
+        assert L.mgn_copy_latents(h, fake, fake, -1, fake, 5, None) == mgn.MGN_E_ARG
+        assert L.mgn_copy_latents(h, None, fake, 3, fake, 5, None) == mgn.MGN_E_ARG
+        assert L.mgn_copy_latents(h, fake, fake, 0, None, 0, None) == mgn.MGN_OK  # nothing to copy
+        assert L.mgn_forward_block(None, None) == mgn.MGN_E_ARG
+    finally:
+        mgn.mgn_destroy(h)
