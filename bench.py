@@ -69,6 +69,10 @@ def main():
     ap.add_argument("--recompute", type=int, default=None,
                     help="edge-stream checkpoint interval (default: 5 for C5, whose stash-all workspace exceeds "
                          "the GPU's memory; 0 otherwise)")
+    ap.add_argument("--lockstep", type=int, default=0,
+                    help="step P theta slabs of the configuration's whole mesh in lockstep on the one GPU "
+                         "(halo exchange after every block), instead of the configuration's single partition")
+    ap.add_argument("--precision", default=None, help="override the configuration's precision (fp32 / bf16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB once (a plain copy kernel of known size, "
@@ -84,6 +88,10 @@ def main():
     from paper_2307_13592_amd.runner import Session
 
     cfg = synth.CONFIGS[args.config]
+    if args.precision:
+        cfg = synth.Config(**{**cfg.__dict__, "precision": args.precision})
+    if args.lockstep:
+        return bench_lockstep(args, cfg)
     t0 = time.time()
     case = synth.make_case(cfg, region=True)
     mesh = case.mesh
@@ -165,6 +173,85 @@ def main():
         "nodes_per_sec": no * cfg.K / (ms * 1e-3),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_lockstep(args, cfg):
+    """P theta slabs of the configuration's whole mesh stepped in lockstep on
+    one GPU: per block, every part's halo rows are copied from their owners
+    (forward) and the halo gradients added back into the owners (backward).
+    Loss: each part's own masked mean (the global mean would only rescale
+    dOut).  Reports the summed throughput and the exchange's share."""
+    import torch
+    import synth
+    import paper_2307_13592_amd as mgn
+    from paper_2307_13592_amd.lockstep import Lockstep
+
+    P = args.lockstep
+    t0 = time.time()
+    log(f"[bench] lockstep: building the whole {cfg.name} mesh ({cfg.note.split(',')[0]})")
+    case = synth.make_case(cfg, region=False)
+    mesh = case.mesh
+    part = mgn.mgn_partition_slabs(mesh.key, P)
+    graphs = [mgn.mgn_graph_build(mesh.send, mesh.recv, part, mesh.n_nodes, p) for p in range(P)]
+    locs = [case.local_inputs(g["l2g"], g["eperm"], g["n_owned"], g["n_halo"]) for g in graphs]
+    log(f"[bench] {P} parts: " + ", ".join(f"{g['n_owned']}/{g['n_halo']}/{g['n_edges']}" for g in graphs)
+        + f" (owned/halo/edges); inputs {time.time() - t0:.1f}s")
+    recompute = args.recompute if args.recompute is not None else (5 if cfg.precision == "bf16" else 0)
+    ls = Lockstep(cfg.latent, cfg.K, cfg.depth, cfg.precision, part, graphs, [l["node_feat"] for l in locs],
+                  [l["edge_feat"] for l in locs], case.params, recompute=recompute)
+    log(f"[bench] workspace {sum(s.ws_bytes for s in ls.sessions) / 2**30:.1f} GiB over {P} parts, "
+        f"checkpoint interval {recompute}; {len(ls.links)} exchange links")
+    targets = [torch.as_tensor(l["target"]).cuda() for l in locs]
+
+    def step():
+        ls.forward()
+        d_outs = [s.mse(t)[1] for s, t in zip(ls.sessions, targets)]
+        ls.backward(d_outs)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("[bench] warm-up done")
+    for s in ls.sessions:
+        mgn.mgn_timing_enable(s.model, True)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    timers = {}
+    for s in ls.sessions:
+        for k, (t, n) in mgn.mgn_timing_read(s.model).items():
+            a, b = timers.get(k, (0.0, 0))
+            timers[k] = (a + t, b + n)
+        mgn.mgn_timing_enable(s.model, False)
+    ls.close()
+    log(f"[bench] {ms:.2f} ms/step")
+    for k, (t, n) in sorted(timers.items(), key=lambda kv: -kv[1][0]):
+        if n:
+            log(f"[bench]   {k:14s} {t / args.steps:9.3f} ms/step  {n // args.steps:5d} launches/step  "
+                f"{t / n:8.4f} ms/launch")
+    ne = sum(g["n_edges"] for g in graphs)
+    no = sum(g["n_owned"] for g in graphs)
+    nh = sum(g["n_halo"] for g in graphs)
+    ex_ms = timers["exchange"][0] / args.steps
+    line = {
+        "metric": "edges/sec per message-passing step (fwd+bwd)",
+        "value": ne * cfg.K / (ms * 1e-3), "unit": "edge-block updates/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.precision, "data": "synthetic",
+        "config": {"workload": f"{cfg.name} whole mesh, {P} theta slabs in lockstep", "parts": P,
+                   "owned_nodes": no, "halo_nodes": nh, "edges": ne, "latent": cfg.latent, "blocks": cfg.K,
+                   "mlp_depth": cfg.depth, "checkpoint_interval": recompute, "parallelism": "none"},
+        "nodes_per_sec": no * cfg.K / (ms * 1e-3),
+        "exchange_ms_per_step": ex_ms, "exchange_share": ex_ms / ms,
+        "roofline": None, "cpu_baseline": None,
         "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},
     }
     print(json.dumps(line), flush=True)
