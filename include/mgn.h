@@ -111,6 +111,14 @@ int64_t mgn_param_count(const mgn_model* m);
  * the packed copies the kernels use.  Synchronises `stream`.  MGN_E_NOMEM if
  * the first call cannot allocate the model's device memory. */
 mgn_status mgn_set_params(mgn_model* m, const float* src, int src_on_device, mgn_stream stream);
+/* Algorithm 1's update after the (accumulated) gradient: theta <- theta -
+ * lr * grad for every parameter (one fused multiply-add each), then the
+ * packed copies are refreshed.  grad: device fp32 [param_count] (e.g. the
+ * d_params of mgn_backward).  Enqueued on `stream`, no synchronisation; a
+ * step in progress is dropped (its backward would no longer match the
+ * parameters).  MGN_E_ARG for a NULL grad or a non-finite lr, MGN_E_STATE
+ * before mgn_set_params. */
+mgn_status mgn_sgd_step(mgn_model* m, const float* grad, float lr, mgn_stream stream);
 /* Copies the fp32 parameters out (host or device).  Synchronises `stream`. */
 mgn_status mgn_get_params(const mgn_model* m, float* dst, int dst_on_device, mgn_stream stream);
 

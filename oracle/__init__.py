@@ -151,3 +151,12 @@ def mse_grad(out, target, mask=None):
     if lib().orc_mse_grad(_p(out), _p(target), _p(m), C.c_int64(n), C.c_int32(d), _p(loss), _p(dout)):
         raise ValueError("orc_mse_grad rejected its arguments")
     return float(loss[0]), dout
+
+
+def sgd_step(params, grad, lr: float) -> np.ndarray:
+    """Algorithm 1's update: params - lr * grad (float64, new array)."""
+    out = _f64(params).copy()
+    g = _f64(grad)
+    if out.shape != g.shape or lib().orc_sgd_step(_p(out), _p(g), C.c_int64(out.size), C.c_double(lr)):
+        raise ValueError("orc_sgd_step rejected its arguments")
+    return out

@@ -554,4 +554,12 @@ int orc_mse_grad(const double* out, const double* target, const uint8_t* mask, i
   return 0;
 }
 
+// Algorithm 1's parameter update after the accumulated gradient:
+// theta <- theta - eta * grad, element by element.
+int orc_sgd_step(double* params, const double* grad, int64_t n, double lr) {
+  if (n < 0 || (n > 0 && (!params || !grad))) return -1;
+  for (int64_t i = 0; i < n; ++i) params[i] = params[i] - lr * grad[i];
+  return 0;
+}
+
 }  // extern "C"

@@ -90,6 +90,9 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
 int orc_mse_grad(const double* out, const double* target, const uint8_t* mask, int64_t n,
                  int32_t d, double* loss, double* d_out);
 
+/* Algorithm 1's update with learning rate eta: params -= lr * grad (n entries). */
+int orc_sgd_step(double* params, const double* grad, int64_t n, double lr);
+
 #ifdef __cplusplus
 }
 #endif

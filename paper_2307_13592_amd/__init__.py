@@ -20,7 +20,8 @@ MGN_FP32, MGN_BF16 = 0, 1
 STATUS_NAMES = ["MGN_OK", "MGN_E_ARG", "MGN_E_GRAPH", "MGN_E_STATE", "MGN_E_NOMEM", "MGN_E_HIP", "MGN_E_UNSUPPORTED"]
 
 # every symbol include/mgn.h declares
-EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mgn_set_params", "mgn_get_params",
+EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mgn_set_params", "mgn_sgd_step",
+           "mgn_get_params",
            "mgn_partition_slabs", "mgn_graph_sizes", "mgn_graph_build", "mgn_graph_validate", "mgn_set_recompute",
            "mgn_workspace_size",
            "mgn_forward", "mgn_backward", "mgn_forward_begin", "mgn_forward_block", "mgn_forward_end",
@@ -67,6 +68,7 @@ def lib() -> C.CDLL:
             "mgn_param_count": (i64, [vp]),
             "mgn_set_params": (C.c_int, [vp, vp, C.c_int, vp]),
             "mgn_get_params": (C.c_int, [vp, vp, C.c_int, vp]),
+            "mgn_sgd_step": (C.c_int, [vp, vp, C.c_float, vp]),
             "mgn_partition_slabs": (C.c_int, [vp, i64, i32, vp]),
             "mgn_graph_sizes": (C.c_int, [vp, vp, i64, vp, i64, i32, vp]),
             "mgn_graph_build": (C.c_int, [vp, vp, i64, vp, i64, i32, vp, vp, vp, vp, vp, vp]),
@@ -158,6 +160,13 @@ def mgn_set_params(model, params, stream=None) -> None:
         if a.size != mgn_param_count(model):
             raise ValueError("parameter vector has the wrong length")
         _check(lib().mgn_set_params(model, p, 0, _stream(stream)), model)
+
+
+def mgn_sgd_step(model, grad, lr: float, stream=None) -> None:
+    """params -= lr * grad on the device (grad: float32 device tensor)."""
+    if grad.numel() != mgn_param_count(model):
+        raise ValueError("gradient vector has the wrong length")
+    _check(lib().mgn_sgd_step(model, _dev(grad), float(lr), _stream(stream)), model)
 
 
 def mgn_get_params(model, stream=None) -> np.ndarray:

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -109,6 +110,18 @@ mgn_status fail(mgn_model* m, mgn_status s, const std::string& msg) {
 
 mgn_status hip_fail(mgn_model* m, hipError_t e, const char* what) {
   return fail(m, MGN_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Refreshes the packed copies of every Linear's weights from the fp32 master copy.
+hipError_t repack(mgn_model* m, hipStream_t st) {
+  for (const MlpL& ml : m->mlp)
+    for (int j = 0; j < ml.depth; ++j) {
+      const LinL& L = ml.lin[j];
+      hipError_t e = launch_pack(m->prec, m->params + L.w, L.out, L.in, 0, m->packed + L.pf, L.nkgf, st);
+      if (e == hipSuccess) e = launch_pack(m->prec, m->params + L.w, L.out, L.in, 1, m->packed + L.pb, L.nkgb, st);
+      if (e != hipSuccess) return e;
+    }
+  return hipSuccess;
 }
 
 size_t tsize(const mgn_model* m) { return m->prec == BF16 ? 2 : 4; }
@@ -356,19 +369,29 @@ mgn_status mgn_set_params(mgn_model* m, const float* src, int src_on_device, mgn
   hipError_t e = hipMemcpyAsync(m->params, src, sizeof(float) * m->P,
                                 src_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return hip_fail(m, e, "mgn_set_params copy");
-  for (const MlpL& ml : m->mlp)
-    for (int j = 0; j < ml.depth; ++j) {
-      const LinL& L = ml.lin[j];
-      e = launch_pack(m->prec, m->params + L.w, L.out, L.in, 0, m->packed + L.pf, L.nkgf, st);
-      if (e == hipSuccess) e = launch_pack(m->prec, m->params + L.w, L.out, L.in, 1, m->packed + L.pb, L.nkgb, st);
-      if (e != hipSuccess) return hip_fail(m, e, "mgn_set_params pack");
-    }
+  e = repack(m, st);
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_set_params pack");
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_fail(m, e, "mgn_set_params sync");
   m->params_set = true;
   m->fwd_done = false;  // a step in progress is dropped
   m->fwd_next = -1;
   m->bwd_active = false;
+  return MGN_OK;
+}
+
+mgn_status mgn_sgd_step(mgn_model* m, const float* grad, float lr, mgn_stream stream) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_sgd_step: model is NULL");
+  if (!grad || !aligned(grad, 4)) return fail(m, MGN_E_ARG, "mgn_sgd_step: grad NULL or misaligned");
+  if (!std::isfinite(lr)) return fail(m, MGN_E_ARG, "mgn_sgd_step: learning rate is not finite");
+  if (!m->params_set) return fail(m, MGN_E_STATE, "mgn_sgd_step: parameters were never set");
+  hipStream_t st = (hipStream_t)stream;
+  m->fwd_done = false;  // the parameters change: a step in progress is dropped
+  m->fwd_next = -1;
+  m->bwd_active = false;
+  hipError_t e = launch_sgd(m->params, grad, m->P, lr, st);
+  if (e == hipSuccess) e = repack(m, st);
+  if (e != hipSuccess) return hip_fail(m, e, "mgn_sgd_step");
   return MGN_OK;
 }
 

@@ -132,6 +132,8 @@ struct VecSeg {
 hipError_t launch_zero(float* p, int64_t n, hipStream_t st);
 hipError_t launch_halo_bf16(const float* H, int K, int64_t n_halo, int64_t n_owned, int L, void* V16,
                             int64_t v16_block_stride, hipStream_t st);
+// p[i] -= lr * g[i] (fused multiply-add), i < n.
+hipError_t launch_sgd(float* p, const float* g, int64_t n, float lr, hipStream_t st);
 // Halo exchange between partitions on one device: dst[dst_rows[i]] = (or +=,
 // add != 0) src[src_rows[i]], rows of L floats (L a multiple of 4, 16-byte
 // aligned rows); pairs with out-of-range indices are skipped.

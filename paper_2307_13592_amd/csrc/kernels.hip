@@ -380,6 +380,21 @@ hipError_t launch_halo_bf16(const float* H, int K, int64_t n_halo, int64_t n_own
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------ update ---
+// Algorithm 1's parameter update: p <- p - lr * g, one fused multiply-add
+// (one rounding) per entry.
+__global__ void sgd_kernel(float* __restrict__ p, const float* __restrict__ g, int64_t n, float lr) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = __builtin_fmaf(-lr, g[i], p[i]);
+}
+
+hipError_t launch_sgd(float* p, const float* g, int64_t n, float lr, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int64_t b = (n + NT - 1) / NT;
+  hipLaunchKernelGGL(sgd_kernel, dim3((unsigned)(b < 4096 ? b : 4096)), dim3(NT), 0, st, p, g, n, lr);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------- halo exchange ---
 // Row copy between two node-row buffers of width L = 4 * L4 floats, the
 // one-GPU form of Algorithm 1's pack / exchange / unpack:

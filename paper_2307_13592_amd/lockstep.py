@@ -16,7 +16,7 @@ import numpy as np
 import torch
 
 from . import (mgn_add_latent_grads, mgn_backward_begin, mgn_backward_block, mgn_backward_end, mgn_copy_latents,
-               mgn_forward_begin, mgn_forward_block, mgn_forward_end, mgn_halo_masks)
+               mgn_forward_begin, mgn_forward_block, mgn_forward_end, mgn_halo_masks, mgn_sgd_step)
 from .runner import Session
 
 
@@ -76,6 +76,12 @@ class Lockstep:
         for s in S:
             mgn_backward_end(s.model, stream)
         return self.d_params
+
+    def sgd(self, lr: float, stream=None):
+        """Every part's model takes the same update with the summed gradient,
+        so the parts' parameters stay identical."""
+        for s in self.sessions:
+            mgn_sgd_step(s.model, self.d_params, lr, stream)
 
     def close(self):
         for s in self.sessions:

@@ -8,7 +8,7 @@ import torch
 
 from . import (MGN_BF16, MGN_FP32, graph_struct, mgn_backward, mgn_create, mgn_destroy, mgn_forward,
                mgn_graph_validate, mgn_mse_grad, mgn_param_count, mgn_set_params, mgn_set_recompute,
-               mgn_workspace_size)
+               mgn_sgd_step, mgn_workspace_size)
 
 
 class Session:
@@ -56,6 +56,10 @@ class Session:
             d_out = torch.as_tensor(np.ascontiguousarray(d_out, np.float32)).to(self.device)
         mgn_backward(self.model, d_out.contiguous(), self.d_params, accumulate, self.d_halo, stream)
         return self.d_params, self.d_halo
+
+    def sgd(self, lr: float, grad=None, stream=None):
+        """Parameter update with the last backward's gradient (or `grad`)."""
+        mgn_sgd_step(self.model, self.d_params if grad is None else grad, lr, stream)
 
     def mse(self, target, mask=None, stream=None):
         loss = torch.empty(2, dtype=torch.float32, device=self.device)

@@ -21,9 +21,9 @@ from parity import calibrate, compare, local_inputs, run_gpu, run_oracle, say
 pytestmark = pytest.mark.gpu
 
 
-def _lockstep(mesh, P, l, K, D, prec, seed, recompute=0):
-    """Runs P slab parts in lockstep; returns (whole-mesh case, gpu result
-    (out, d_params, empty d_halo) in the whole mesh's node order)."""
+def _lockstep_session(mesh, P, l, K, D, prec, seed, recompute=0):
+    """P slab parts of `mesh` in a Lockstep, with the whole-mesh case whose
+    inputs they share, and each part's owned global ids."""
     whole = local_inputs(mesh, 0, l, K, D, seed, part=np.zeros(mesh.n_nodes, np.int32))
     assert np.array_equal(whole["g"]["l2g"], np.arange(mesh.n_nodes))  # local ids are global ids
     part = mgn.mgn_partition_slabs(mesh.key, P)
@@ -32,6 +32,13 @@ def _lockstep(mesh, P, l, K, D, prec, seed, recompute=0):
     own = [g["l2g"][:g["n_owned"]] for g in graphs]
     ls = Lockstep(l, K, D, prec, part, graphs, [nf_all[o] for o in own], [ef_all[g["eperm"]] for g in graphs],
                   whole["params"], recompute=recompute)
+    return ls, whole, own
+
+
+def _lockstep(mesh, P, l, K, D, prec, seed, recompute=0):
+    """Runs P slab parts in lockstep; returns (whole-mesh case, gpu result
+    (out, d_params, empty d_halo) in the whole mesh's node order)."""
+    ls, whole, own = _lockstep_session(mesh, P, l, K, D, prec, seed, recompute)
     try:
         outs = ls.forward()
         dp = ls.backward([whole["d_out"][o] for o in own]).cpu().numpy().copy()

@@ -230,3 +230,21 @@ def test_mse_grad_matches_autograd():
     assert _rel(d, o.grad.numpy()) < 1e-14
     L0, d0 = oracle.mse_grad(out, tgt, np.zeros(50, np.uint8))
     assert L0 == 0 and np.all(d0 == 0)
+
+
+def test_sgd_step_against_torch_optimizer_and_closed_forms():
+    """Algorithm 1's update: torch.optim.SGD (no momentum) on the same
+    parameters and gradient gives the same values; on L = |theta - t|^2 / 2
+    one step with lr = 1 lands exactly on t; lr = 0 changes nothing."""
+    rng = np.random.default_rng(8)
+    theta, grad = rng.standard_normal(1000), rng.standard_normal(1000)
+    w = torch.nn.Parameter(torch.as_tensor(theta.copy()))
+    opt = torch.optim.SGD([w], lr=0.037)
+    w.grad = torch.as_tensor(grad.copy())
+    opt.step()
+    assert _rel(oracle.sgd_step(theta, grad, 0.037), w.detach().numpy()) < 1e-15
+    t = rng.standard_normal(1000)
+    half = np.round(theta * 64) / 64  # exact in binary: theta - (theta - t) has no rounding
+    t = np.round(t * 64) / 64
+    assert np.array_equal(oracle.sgd_step(half, half - t, 1.0), t)
+    assert np.array_equal(oracle.sgd_step(theta, grad, 0.0), theta)
