@@ -72,6 +72,9 @@ def main():
     ap.add_argument("--lockstep", type=int, default=0,
                     help="step P theta slabs of the configuration's whole mesh in lockstep on the one GPU "
                          "(halo exchange after every block), instead of the configuration's single partition")
+    ap.add_argument("--inference", action="store_true",
+                    help="forward-only rollout steps on the configuration's whole mesh (no halo) instead of the "
+                         "training step on its partition")
     ap.add_argument("--precision", default=None, help="override the configuration's precision (fp32 / bf16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -92,6 +95,8 @@ def main():
         cfg = synth.Config(**{**cfg.__dict__, "precision": args.precision})
     if args.lockstep:
         return bench_lockstep(args, cfg)
+    if args.inference:
+        return bench_inference(args, cfg)
     t0 = time.time()
     case = synth.make_case(cfg, region=True)
     mesh = case.mesh
@@ -173,6 +178,75 @@ def main():
         "nodes_per_sec": no * cfg.K / (ms * 1e-3),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_inference(args, cfg):
+    """Next-step rollout on the configuration's whole mesh in the forward-only
+    plan: one step = forward pass + feeding the prediction back into the
+    node features' flow columns."""
+    import torch
+    import synth
+    import paper_2307_13592_amd as mgn
+    from paper_2307_13592_amd.runner import Session
+
+    t0 = time.time()
+    log(f"[bench] inference: building the whole {cfg.name} mesh ({cfg.note.split(',')[0]})")
+    case = synth.make_case(cfg, region=False)
+    mesh = case.mesh
+    part = np.zeros(mesh.n_nodes, np.int32)
+    g = mgn.mgn_graph_build(mesh.send, mesh.recv, part, mesh.n_nodes, 0)
+    loc = case.local_inputs(g["l2g"], g["eperm"], g["n_owned"], g["n_halo"])
+    no, ne = g["n_owned"], g["n_edges"]
+    log(f"[bench] {no} nodes, {ne} edges; inputs {time.time() - t0:.1f}s")
+    sess = Session(cfg.latent, cfg.K, cfg.depth, cfg.precision, g, loc["node_feat"], loc["edge_feat"], None,
+                   case.params, inference=True)
+    log(f"[bench] workspace {sess.ws_bytes / 2**30:.1f} GiB (forward-only plan)")
+
+    def step():
+        sess.forward()
+        mgn.mgn_rollout_update(sess.out, sess.node_feat)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("[bench] warm-up done")
+    mgn.mgn_timing_enable(sess.model, True)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    timers = mgn.mgn_timing_read(sess.model)
+    sess.close()
+    log(f"[bench] {ms:.2f} ms/step")
+    for k, (t, n) in sorted(timers.items(), key=lambda kv: -kv[1][0]):
+        if n:
+            log(f"[bench]   {k:14s} {t / args.steps:9.3f} ms/step  {n // args.steps:4d} launches/step  "
+                f"{t / n:8.4f} ms/launch")
+    dom = max((k for k in timers if timers[k][1]), key=lambda k: timers[k][0])
+    alg = algorithmic(dom, cfg, ne, no, 0)
+    roof = None
+    if alg is not None:
+        t_launch = timers[dom][0] / timers[dom][1] * 1e-3
+        roof = dict(bound="hbm", achieved=alg[0] / t_launch / 1e9, peak=PEAK["hbm"] / 1e9, unit="GB/s")
+        roof["frac"] = roof["achieved"] / roof["peak"]
+        roof["kernel"] = dom
+        roof["traffic"] = None
+    line = {
+        "metric": "edges/sec per message-passing step (forward only)",
+        "value": ne * cfg.K / (ms * 1e-3), "unit": "edge-block updates/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.precision, "data": "synthetic",
+        "config": {"workload": f"{cfg.name} whole mesh, next-step rollout (forward-only plan)", "owned_nodes": no,
+                   "halo_nodes": 0, "edges": ne, "latent": cfg.latent, "blocks": cfg.K, "mlp_depth": cfg.depth,
+                   "parallelism": "none"},
+        "nodes_per_sec": no * cfg.K / (ms * 1e-3), "roofline": roof, "cpu_baseline": None,
         "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},
     }
     print(json.dumps(line), flush=True)

@@ -161,6 +161,24 @@ mgn_status mgn_graph_validate(mgn_model* m, const mgn_graph* g, mgn_stream strea
  * MGN_E_UNSUPPORTED for fp32 models, MGN_E_ARG for negative arguments. */
 mgn_status mgn_set_recompute(mgn_model* m, int32_t interval, int64_t chunk_edges);
 
+/* Forward-only plan (inference on a whole mesh, the paper's section
+ * "Results": a single GPU holds a complete stator domain for inference).
+ * on != 0: the workspace holds one working copy of each stream (node
+ * latents and their bf16 copy in a ping-pong pair, the edge latents updated
+ * in place) and no backward buffers; mgn_backward then returns MGN_E_STATE.
+ * Same arithmetic as the training plan: outputs are bitwise equal.  Takes
+ * effect for the next mgn_workspace_size / mgn_forward (a pending step is
+ * dropped). */
+mgn_status mgn_set_inference(mgn_model* m, int32_t on);
+
+/* Next-step rollout (section "Model": the network predicts the increment,
+ * q_{t+1} = p + q_t): node_feat[i][col0 + j] += out[i][j] for i < n,
+ * j < node_out (device fp32; row strides node_in and node_out).  With the
+ * default features (3 coordinates, 5 flow quantities, 3 type flags) col0 = 3.
+ * MGN_E_ARG unless col0 + node_out <= node_in. */
+mgn_status mgn_rollout_update(const float* out, int64_t n, int32_t node_out, float* node_feat, int32_t node_in,
+                              int32_t col0, mgn_stream stream);
+
 /* Device workspace mgn_forward/mgn_backward need for graph g (bytes) under
  * the model's checkpointing setting. */
 mgn_status mgn_workspace_size(const mgn_model* m, const mgn_graph* g, size_t* bytes);

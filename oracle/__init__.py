@@ -160,3 +160,15 @@ def sgd_step(params, grad, lr: float) -> np.ndarray:
     if out.shape != g.shape or lib().orc_sgd_step(_p(out), _p(g), C.c_int64(out.size), C.c_double(lr)):
         raise ValueError("orc_sgd_step rejected its arguments")
     return out
+
+
+def rollout_update(node_feat, out, col0: int = 3) -> np.ndarray:
+    """Next-step input: the flow columns of node_feat plus the predicted
+    increment out (float64, new array)."""
+    nf = _f64(node_feat).copy()
+    o = _f64(out)
+    n, fin = nf.shape
+    if o.shape[0] != n or lib().orc_rollout_update(_p(nf), C.c_int64(n), C.c_int32(fin), _p(o),
+                                                   C.c_int32(o.shape[1]), C.c_int32(col0)):
+        raise ValueError("orc_rollout_update rejected its arguments")
+    return nf

@@ -562,4 +562,15 @@ int orc_sgd_step(double* params, const double* grad, int64_t n, double lr) {
   return 0;
 }
 
+// Next-step prediction (section "Model"): the network's output is the
+// increment of the flow quantities, q_{t+1} = p_t + q_t, which sit in node
+// feature columns col0 .. col0 + node_out - 1.
+int orc_rollout_update(double* node_feat, int64_t n, int32_t node_in, const double* out, int32_t node_out,
+                       int32_t col0) {
+  if (n < 0 || col0 < 0 || node_out < 1 || col0 + node_out > node_in || (n > 0 && (!node_feat || !out))) return -1;
+  for (int64_t i = 0; i < n; ++i)
+    for (int32_t j = 0; j < node_out; ++j) node_feat[i * node_in + col0 + j] += out[i * node_out + j];
+  return 0;
+}
+
 }  // extern "C"

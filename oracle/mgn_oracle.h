@@ -93,6 +93,10 @@ int orc_mse_grad(const double* out, const double* target, const uint8_t* mask, i
 /* Algorithm 1's update with learning rate eta: params -= lr * grad (n entries). */
 int orc_sgd_step(double* params, const double* grad, int64_t n, double lr);
 
+/* Next-step rollout: node_feat[i][col0 + j] += out[i][j] (q_{t+1} = p + q_t). */
+int orc_rollout_update(double* node_feat, int64_t n, int32_t node_in, const double* out, int32_t node_out,
+                       int32_t col0);
+
 #ifdef __cplusplus
 }
 #endif

@@ -43,6 +43,8 @@ struct WsPlan {
   // edge-stream checkpointing: interval s (0: every block kept), checkpoints
   bool lean = false;
   int s = 0, nck = 0;
+  // forward-only plan (inference): working copies only, no backward buffers
+  bool infer = false;
   // receiver / edge boundaries of the backward's edge chunks
   std::vector<int64_t> cr, ce;
 };
@@ -66,6 +68,7 @@ struct mgn_model {
   mgn_graph vg{};
   std::vector<int32_t> rp_host;
   int ckpt = 0;                 // edge-stream checkpoint interval (0: keep every block)
+  bool infer = false;           // forward-only plan (mgn_set_inference)
   int64_t chunk_edges = 0;      // edges per backward chunk with checkpointing (0: the default)
   // what the last forward used (kept for the backward)
   bool fwd_done = false;
@@ -209,7 +212,8 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   const size_t ts = tsize(m);
   const int te = edge_tile_rows(m->prec, m->L, m->D);
   p.max_units = plan_max_units(no, ne, 4 * te, 4 * te);
-  p.lean = m->ckpt > 0 && K > 0;
+  p.infer = m->infer;
+  p.lean = m->ckpt > 0 && K > 0 && !p.infer;
   p.s = m->ckpt;
   p.nck = p.lean ? (int)((K + p.s - 1) / p.s) : 0;
   // backward edge chunks: one, or ~LEAN_CHUNK_EDGES edges each on planning-chunk receiver boundaries
@@ -239,16 +243,22 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.chunk = take(4 * (size_t)plan_chunks(no));
   p.unit_r = take(4 * (size_t)(p.max_units + 1));
   p.nunits = take(4);
-  // fp32 node stream: every block's input, or (checkpointing) two working rows
-  p.V = take(4 * (size_t)(p.lean ? 2 : K + 1) * no * L);
-  // bf16 mode: bf16 copy of every block's node input, owned then halo rows
-  p.V16 = m->prec == BF16 ? take(2 * (size_t)(K + 1) * nl * L) : 0;
+  const bool one = p.lean || p.infer;  // one working slot per block-level buffer
+  // fp32 node stream: every block's input, or (checkpointing, inference) two working rows
+  p.V = take(4 * (size_t)(one ? 2 : K + 1) * no * L);
+  // bf16 mode: bf16 copy of every block's node input (inference: two), owned then halo rows
+  p.V16 = m->prec == BF16 ? take(2 * (size_t)(p.infer ? 2 : K + 1) * nl * L) : 0;
   // row-split edge kernels: node projections of every block's input (kept for
-  // the backward), or of the current block only (checkpointing)
-  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(p.lean ? 1 : K) * nl * 2 * L) : 0;
-  p.AGG = take(4 * (size_t)(p.lean ? 1 : K) * no * L);
-  // edge stream: every block's input, or the checkpoints plus one working copy
-  p.ES = take(ts * (size_t)(p.lean ? p.nck + 1 : std::max<int64_t>(K, 1)) * ne * L);
+  // the backward), or of the current block only (checkpointing, inference)
+  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(one ? 1 : K) * nl * 2 * L) : 0;
+  p.AGG = take(4 * (size_t)(one ? 1 : K) * no * L);
+  // edge stream: every block's input, the checkpoints plus one working copy,
+  // or (inference) one copy updated in place
+  p.ES = take(ts * (size_t)(p.infer ? 1 : p.lean ? p.nck + 1 : std::max<int64_t>(K, 1)) * ne * L);
+  if (p.infer) {
+    p.total = o;
+    return p;
+  }
   p.DV[0] = take(4 * (size_t)no * L);
   p.DV[1] = take(4 * (size_t)no * L);
   p.DAGG = take(4 * (size_t)no * L);
@@ -458,6 +468,27 @@ mgn_status mgn_set_recompute(mgn_model* m, int32_t interval, int64_t chunk_edges
   return MGN_OK;
 }
 
+mgn_status mgn_set_inference(mgn_model* m, int32_t on) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_set_inference: model is NULL");
+  m->infer = on != 0;
+  m->fwd_done = false;  // the workspace plan changes: a step in progress is dropped
+  m->fwd_next = -1;
+  m->bwd_active = false;
+  return MGN_OK;
+}
+
+mgn_status mgn_rollout_update(const float* out, int64_t n, int32_t node_out, float* node_feat, int32_t node_in,
+                              int32_t col0, mgn_stream stream) {
+  if (n < 0 || node_out < 1 || node_in < 1 || col0 < 0 || col0 + node_out > node_in)
+    return fail(nullptr, MGN_E_ARG, "mgn_rollout_update: bad sizes (need col0 + node_out <= node_in)");
+  if (n == 0) return MGN_OK;
+  if (!out || !node_feat || !aligned(out, 4) || !aligned(node_feat, 4))
+    return fail(nullptr, MGN_E_ARG, "mgn_rollout_update: NULL or misaligned pointer");
+  hipError_t e = launch_rollout(out, n, node_out, node_feat, node_in, col0, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(nullptr, e, "mgn_rollout_update");
+  return MGN_OK;
+}
+
 mgn_status mgn_workspace_size(const mgn_model* cm, const mgn_graph* g, size_t* bytes) {
   mgn_model* m = const_cast<mgn_model*>(cm);
   if (!m) return fail(nullptr, MGN_E_ARG, "mgn_workspace_size: model is NULL");
@@ -477,7 +508,7 @@ namespace {
 // null), ordered receiver sums into agg.
 // Node projections of block k (one shared slot when checkpointing).
 float* proj_block(const WsPlan& p, char* ws, int k, int64_t nl, int L) {
-  return (float*)(ws + p.PROJ) + (p.lean ? 0 : (size_t)k * nl * 2 * L);
+  return (float*)(ws + p.PROJ) + (p.lean || p.infer ? 0 : (size_t)k * nl * 2 * L);
 }
 
 hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p, char* ws, const float* halo, int k,
@@ -576,15 +607,17 @@ struct Views {
       : p(m->plan), ws(m->ws), no(m->g.n_owned), nh(m->g.n_halo), ne(m->g.n_edges), L(m->L), ts(tsize(m)),
         bf16(m->prec == BF16) {}
   // fp32 node latents v^k (owned rows): every block's, or a ping-pong pair when checkpointing
-  float* V(int k) const { return (float*)(ws + p.V) + (size_t)(p.lean ? (k & 1) : k) * no * L; }
-  float* AGG(int k) const { return (float*)(ws + p.AGG) + (size_t)(p.lean ? 0 : k) * no * L; }
+  float* V(int k) const { return (float*)(ws + p.V) + (size_t)(p.lean || p.infer ? (k & 1) : k) * no * L; }
+  float* AGG(int k) const { return (float*)(ws + p.AGG) + (size_t)(p.lean || p.infer ? 0 : k) * no * L; }
   // edge latents e^k: every block's, or the checkpoint slots plus one working slot
   void* ES(int k) const {
-    const int slot = !p.lean ? k : (k % p.s == 0 ? k / p.s : p.nck);
+    const int slot = p.infer ? 0 : !p.lean ? k : (k % p.s == 0 ? k / p.s : p.nck);
     return (void*)(ws + p.ES + ts * (size_t)slot * ne * L);
   }
   int64_t v16_stride() const { return (no + nh) * L; }  // elements per block of the bf16 node copy
-  void* V16(int k) const { return bf16 ? (void*)((uint16_t*)(ws + p.V16) + (size_t)k * v16_stride()) : nullptr; }
+  void* V16(int k) const {
+    return bf16 ? (void*)((uint16_t*)(ws + p.V16) + (size_t)(p.infer ? (k & 1) : k) * v16_stride()) : nullptr;
+  }
 };
 
 // ---- forward, in three stages: encoders, one block at a time, decoder
@@ -1065,6 +1098,7 @@ mgn_status bwd_begin(mgn_model* m, const float* d_out, float* d_params, int accu
   const std::string f(fn);
   if (!m) return fail(nullptr, MGN_E_ARG, f + ": model is NULL");
   if (!m->fwd_done) return fail(m, MGN_E_STATE, f + ": no forward pass to differentiate");
+  if (m->plan.infer) return fail(m, MGN_E_STATE, f + ": the forward pass ran in inference mode");
   if (!m->graph_ok || !same_graph(m->g, m->vg))
     return fail(m, MGN_E_STATE, f + ": the graph changed since the forward pass");
   if (!d_params || (m->g.n_owned > 0 && !d_out)) return fail(m, MGN_E_ARG, f + ": NULL argument");

@@ -395,6 +395,24 @@ hipError_t launch_sgd(float* p, const float* g, int64_t n, float lr, hipStream_t
   return hipGetLastError();
 }
 
+// Next-step rollout: the flow columns of the node features take the
+// predicted increment, nf[i][col0 + j] += out[i][j].
+__global__ void rollout_kernel(const float* __restrict__ out, int64_t n, int d, float* __restrict__ nf, int fin,
+                               int col0) {
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n * d; t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = t / d;
+    const int j = (int)(t - i * d);
+    nf[i * fin + col0 + j] += out[t];
+  }
+}
+
+hipError_t launch_rollout(const float* out, int64_t n, int d, float* nf, int fin, int col0, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int64_t b = (n * d + NT - 1) / NT;
+  hipLaunchKernelGGL(rollout_kernel, dim3((unsigned)(b < 8192 ? b : 8192)), dim3(NT), 0, st, out, n, d, nf, fin, col0);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------- halo exchange ---
 // Row copy between two node-row buffers of width L = 4 * L4 floats, the
 // one-GPU form of Algorithm 1's pack / exchange / unpack:

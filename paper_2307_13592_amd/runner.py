@@ -8,13 +8,13 @@ import torch
 
 from . import (MGN_BF16, MGN_FP32, graph_struct, mgn_backward, mgn_create, mgn_destroy, mgn_forward,
                mgn_graph_validate, mgn_mse_grad, mgn_param_count, mgn_set_params, mgn_set_recompute,
-               mgn_sgd_step, mgn_workspace_size)
+               mgn_rollout_update, mgn_set_inference, mgn_sgd_step, mgn_workspace_size)
 
 
 class Session:
     def __init__(self, latent: int, K: int, depth: int, precision: str, graph: dict, node_feat, edge_feat, halo,
                  params, device: str = "cuda", node_in: int = 11, edge_in: int = 4, node_out: int = 5,
-                 recompute: int = 0, chunk_edges: int = 0):
+                 recompute: int = 0, chunk_edges: int = 0, inference: bool = False):
         if not torch.cuda.is_available():
             raise RuntimeError("libmgn needs a HIP device")
         self.device = torch.device(device)
@@ -35,11 +35,14 @@ class Session:
         mgn_graph_validate(self.model, self.gs)
         if recompute:
             mgn_set_recompute(self.model, recompute, chunk_edges)
+        if inference:
+            mgn_set_inference(self.model, True)
         self.ws_bytes = mgn_workspace_size(self.model, self.gs)
         self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=self.device)
         self.out = torch.empty((no, node_out), dtype=torch.float32, device=self.device)
-        self.d_params = torch.empty(self.n_params, dtype=torch.float32, device=self.device)
-        self.d_halo = torch.empty((K, nh, latent), dtype=torch.float32, device=self.device) if (nh and K) else None
+        self.d_params = None if inference else torch.empty(self.n_params, dtype=torch.float32, device=self.device)
+        self.d_halo = (torch.empty((K, nh, latent), dtype=torch.float32, device=self.device)
+                       if (nh and K and not inference) else None)
 
     def set_params(self, params):
         if isinstance(params, torch.Tensor):
@@ -60,6 +63,16 @@ class Session:
     def sgd(self, lr: float, grad=None, stream=None):
         """Parameter update with the last backward's gradient (or `grad`)."""
         mgn_sgd_step(self.model, self.d_params if grad is None else grad, lr, stream)
+
+    def rollout(self, steps: int, col0: int = 3, stream=None):
+        """`steps` next-step predictions, each fed back into the flow columns
+        of the node features (q <- q + p); returns the outputs of every step."""
+        outs = []
+        for _ in range(steps):
+            self.forward(stream)
+            outs.append(self.out.clone())
+            mgn_rollout_update(self.out, self.node_feat, col0, stream)
+        return outs
 
     def mse(self, target, mask=None, stream=None):
         loss = torch.empty(2, dtype=torch.float32, device=self.device)

@@ -248,3 +248,20 @@ def test_sgd_step_against_torch_optimizer_and_closed_forms():
     t = np.round(t * 64) / 64
     assert np.array_equal(oracle.sgd_step(half, half - t, 1.0), t)
     assert np.array_equal(oracle.sgd_step(theta, grad, 0.0), theta)
+
+
+def test_rollout_update_special_cases():
+    """q_{t+1} = p + q_t on the flow columns only: p = 0 changes nothing;
+    p = -q zeroes the flow columns and leaves coordinates and type flags;
+    two updates add."""
+    rng = np.random.default_rng(9)
+    nf = rng.standard_normal((40, 11))
+    assert np.array_equal(oracle.rollout_update(nf, np.zeros((40, 5))), nf)
+    z = oracle.rollout_update(nf, -nf[:, 3:8])
+    assert not np.any(z[:, 3:8])
+    assert np.array_equal(z[:, :3], nf[:, :3]) and np.array_equal(z[:, 8:], nf[:, 8:])
+    p = np.round(rng.standard_normal((40, 5)) * 8) / 8
+    q = np.round(nf * 8) / 8
+    assert np.array_equal(oracle.rollout_update(oracle.rollout_update(q, p), p), oracle.rollout_update(q, 2 * p))
+    with pytest.raises(ValueError):
+        oracle.rollout_update(nf, np.zeros((40, 5)), col0=7)
