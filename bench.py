@@ -75,6 +75,8 @@ def main():
     ap.add_argument("--inference", action="store_true",
                     help="forward-only rollout steps on the configuration's whole mesh (no halo) instead of the "
                          "training step on its partition")
+    ap.add_argument("--nocomm", action="store_true",
+                    help="with --lockstep: the paper's NoComm variant (edges across parts dropped, no exchange)")
     ap.add_argument("--precision", default=None, help="override the configuration's precision (fp32 / bf16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -269,7 +271,15 @@ def bench_lockstep(args, cfg):
     case = synth.make_case(cfg, region=False)
     mesh = case.mesh
     part = mgn.mgn_partition_slabs(mesh.key, P)
-    graphs = [mgn.mgn_graph_build(mesh.send, mesh.recv, part, mesh.n_nodes, p) for p in range(P)]
+    send, recv = mesh.send, mesh.recv
+    keep = None
+    if args.nocomm:
+        keep = np.flatnonzero(part[send] == part[recv])
+        send, recv = send[keep], recv[keep]
+    graphs = [mgn.mgn_graph_build(send, recv, part, mesh.n_nodes, p) for p in range(P)]
+    if keep is not None:  # local edge order -> the mesh's global edge ids
+        for g in graphs:
+            g["eperm"] = keep[g["eperm"]].astype(np.int32)
     locs = [case.local_inputs(g["l2g"], g["eperm"], g["n_owned"], g["n_halo"]) for g in graphs]
     log(f"[bench] {P} parts: " + ", ".join(f"{g['n_owned']}/{g['n_halo']}/{g['n_edges']}" for g in graphs)
         + f" (owned/halo/edges); inputs {time.time() - t0:.1f}s")
@@ -320,7 +330,8 @@ def bench_lockstep(args, cfg):
         "value": ne * cfg.K / (ms * 1e-3), "unit": "edge-block updates/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": cfg.precision, "data": "synthetic",
-        "config": {"workload": f"{cfg.name} whole mesh, {P} theta slabs in lockstep", "parts": P,
+        "config": {"workload": f"{cfg.name} whole mesh, {P} theta slabs in lockstep"
+                               + (" without halo (NoComm)" if args.nocomm else ""), "parts": P,
                    "owned_nodes": no, "halo_nodes": nh, "edges": ne, "latent": cfg.latent, "blocks": cfg.K,
                    "mlp_depth": cfg.depth, "checkpoint_interval": recompute, "parallelism": "none"},
         "nodes_per_sec": no * cfg.K / (ms * 1e-3),

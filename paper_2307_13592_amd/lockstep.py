@@ -20,6 +20,15 @@ from . import (mgn_add_latent_grads, mgn_backward_begin, mgn_backward_block, mgn
 from .runner import Session
 
 
+def nocomm_edges(send, recv, part):
+    """The paper's NoComm variant (section "Results": partitions trained
+    without halo exchange): only the edges whose two ends lie in the same
+    part, so every part's local graph has no halo."""
+    send, recv, part = (np.asarray(a, np.int32) for a in (send, recv, part))
+    keep = part[send] == part[recv]
+    return np.ascontiguousarray(send[keep]), np.ascontiguousarray(recv[keep])
+
+
 class Lockstep:
     """P parts of one mesh; graphs[p] from mgn_graph_build(..., part, n_nodes, p),
     node_feats[p] / edge_feats[p] the part's owned-node and local-edge

@@ -96,6 +96,17 @@ def _with_edges(mesh, keep):
 
 
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_nocomm_partition(prec):
+    """The paper's NoComm variant: an interior part's graph without the
+    edges from other parts (no halo)."""
+    from paper_2307_13592_amd.lockstep import nocomm_edges
+    mesh = meshes.sector(6, 16, 10, 4, seed=7)
+    part = mgn.mgn_partition_slabs(mesh.key, 4)
+    _case("sector 6x16x10 p1 NoComm", _with_edges(mesh, part[mesh.send] == part[mesh.recv]), 1, 128, 3, 2, prec,
+          part=part)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
 def test_receivers_without_edges(prec):
     m = meshes.hex_lattice(7)
     keep = (m.recv % 5) != 0          # every 5th node receives nothing

@@ -176,6 +176,42 @@ def test_partition_consistency():
             assert _rel(rp["e_all"][k], ru["e_all"][k][ue]) < 1e-12
 
 
+def test_nocomm_keeps_interior_outputs():
+    """The paper's NoComm variant (each part trained on its own nodes and the
+    edges between them, no halo): an owned node whose receptive field (nodes
+    within K in-edge hops) stays inside its part keeps the whole network's
+    output exactly; the nodes next to the cut lose their cross-part messages
+    and change."""
+    from paper_2307_13592_amd.lockstep import nocomm_edges
+    m = meshes.sector(4, 32, 6, 4, seed=7)
+    K, l, D = 2, 8, 2
+    part = oracle.partition(m.key, 4)
+    full = local_case(m, 0, l, K, D, seed=5, part=np.zeros(m.n_nodes, np.int32))
+    ru = oracle.step(full["cfg"], full["g"], full["params"], full["nf"], full["ef"], None, None)
+    mn = meshes.Mesh(**{**m.__dict__})
+    mn.send, mn.recv = nocomm_edges(m.send, m.recv, part)
+    preds = [[] for _ in range(m.n_nodes)]
+    for s_, r_ in zip(m.send, m.recv):
+        preds[r_].append(s_)
+    for p in (0, 1):
+        c = local_case(mn, p, l, K, D, seed=5, part=part)
+        g = c["g"]
+        assert g["n_halo"] == 0
+        rp = oracle.step(c["cfg"], g, c["params"], c["nf"], c["ef"], None, None)
+        own = g["l2g"][:g["n_owned"]]
+        inside = []
+        for n in own:  # receptive field of n in the whole mesh, by breadth-first search
+            field, front = {int(n)}, {int(n)}
+            for _ in range(K):
+                front = {int(s_) for r_ in front for s_ in preds[r_]} - field
+                field |= front
+            inside.append(all(part[x] == p for x in field))
+        inside = np.asarray(inside)
+        assert inside.any() and (~inside).any()
+        assert _rel(rp["out"][inside], ru["out"][own[inside]]) < 1e-12
+        assert np.abs(rp["out"][~inside] - ru["out"][own[~inside]]).max(axis=1).min() > 1e-6
+
+
 def test_backward_is_linear_in_d_out():
     c = local_case(meshes.sector(3, 8, 4, 4, seed=2), 1, 8, 2, 3, seed=8)
     a = oracle.step(c["cfg"], c["g"], c["params"], c["nf"], c["ef"], c["halo"], c["d_out"])
