@@ -37,9 +37,24 @@ def algorithmic(timer: str, cfg, E: int, No: int, Nh: int):
     gathered node rows once per node; flops are the MLP products (2 per
     multiply-add).  E edges, No owned and Nh halo nodes."""
     l, D = cfg.latent, cfg.depth
-    if cfg.precision != "bf16" or D != 2 or l not in (64, 128):
-        return None
     Nl = No + Nh
+    if cfg.precision != "bf16" or D != 2 or l not in (64, 128):
+        # streaming edge kernels (fp32, or l = 256 / depth 3): the concat
+        # [e | v_s | v_r] times W_1 per edge; ts bytes per stored element,
+        # node rows gathered from the fp32 latents or their bf16 copy
+        ts = 2 if cfg.precision == "bf16" else 4
+        if timer == "edge_fwd":
+            # read e^k, ids, node rows; write e^{k+1} and agg
+            by = E * (2 * ts * l + 8) + Nl * ts * l + No * 4 * l
+            return by, E * 2 * l * l * (D + 2)
+        if timer == "edge_bwd":
+            # recompute the forward, then the data gradients of every layer
+            # and de^k = de^{k+1} + dz_0 W_e: read e^k, de^{k+1} (fp32), ids,
+            # node rows, dagg; write de^k, D output gradients and D-1 hidden
+            # activations, receiver sums of dz_0
+            by = E * (ts * l + 4 * l + 8 + 4 * l + (2 * D - 1) * ts * l) + Nl * ts * l + No * 4 * l * 2
+            return by, E * 4 * l * l * (D + 1)
+        return None
     if timer == "edge_bwd":
         # read e^k (bf16), de^{k+1} (fp32), receiver / sender ids, dagg rows,
         # node projections; write de^k, dy, dz_0, h_1 (bf16) and the
@@ -146,7 +161,10 @@ def main():
     alg = algorithmic(dom, cfg, ne, no, nh)
     roof = None
     if alg is not None:
-        by, fl = alg
+        # a block's edge backward may run as several receiver chunks
+        # (checkpointed plan): one launch then does its share of the block
+        share = cfg.K * args.steps / timers[dom][1] if dom == "edge_bwd" else 1.0
+        by, fl = alg[0] * share, alg[1] * share
         peak_flops = PEAK["bf16"] if cfg.precision == "bf16" else PEAK["fp32"]
         intensity = fl / by if by else 0
         if intensity >= peak_flops / PEAK["hbm"]:
