@@ -93,6 +93,9 @@ def main():
     ap.add_argument("--nocomm", action="store_true",
                     help="with --lockstep: the paper's NoComm variant (edges across parts dropped, no exchange)")
     ap.add_argument("--precision", default=None, help="override the configuration's precision (fp32 / bf16)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the step into a HIP graph once and time its replays (per-kernel timing and "
+                         "the roofline are then omitted: events cannot be read per launch inside a graph)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB once (a plain copy kernel of known size, "
@@ -137,6 +140,8 @@ def main():
         step()
     torch.cuda.synchronize()
     log("[bench] warm-up done")
+    if args.graph:
+        return bench_graph(args, cfg, sess, step, ne, no, nh)
     mgn.mgn_timing_enable(sess.model, True)
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -199,6 +204,44 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_graph(args, cfg, sess, step, ne, no, nh):
+    """Times replays of the training step captured into one HIP graph."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    g.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        g.replay()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    log(f"[bench] {ms:.3f} ms/step (HIP graph replays)")
+    del g
+    sess.close()
+    line = {
+        "metric": "edges/sec per message-passing step (fwd+bwd)",
+        "value": ne * cfg.K / (ms * 1e-3), "unit": "edge-block updates/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.precision, "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.note}, step replayed from a HIP graph", "owned_nodes": no,
+                   "halo_nodes": nh, "edges": ne, "latent": cfg.latent, "blocks": cfg.K, "mlp_depth": cfg.depth,
+                   "parallelism": "none"},
+        "nodes_per_sec": no * cfg.K / (ms * 1e-3), "roofline": None, "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)
 
