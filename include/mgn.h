@@ -278,6 +278,16 @@ mgn_status mgn_add_latent_grads(mgn_model* owner, const float* d_halo_k, int64_t
 mgn_status mgn_mse_grad(const float* out, const float* target, const uint8_t* mask, int64_t n, int32_t d,
                         float* loss, float* d_out, mgn_stream stream);
 
+/* The global mean of Algorithm 1 over several parts (its loss all-reduce):
+ * as mgn_mse_grad for one part's rows, but the mean runs over global_rows
+ * loss-masked rows of all parts together (>= 1; the host knows it from the
+ * masks).  loss[0] = this part's share, sum of its squared errors /
+ * (global_rows * d); the parts' shares add up to the global loss.  d_out =
+ * 2 (out - target) / (global_rows * d) on masked rows, 0 elsewhere: the
+ * gradient of the global loss. */
+mgn_status mgn_mse_grad_global(const float* out, const float* target, const uint8_t* mask, int64_t n, int32_t d,
+                               int64_t global_rows, float* loss, float* d_out, mgn_stream stream);
+
 /* ---- kernel timing (measurement; the paper's section "Performance Study"
  * times its step with host-synchronised streams, this records HIP events on
  * the stream around each launch instead) ---- */

@@ -142,14 +142,17 @@ def step(cfg: ModelCfg, g: dict, params, node_feat, edge_feat, halo=None, d_out=
     return res
 
 
-def mse_grad(out, target, mask=None):
+def mse_grad(out, target, mask=None, global_rows: int = 0):
+    """Masked mean squared error and its gradient; with global_rows > 0 this
+    part's share of the mean over global_rows rows of all parts."""
     out, target = _f64(out), _f64(target)
     n, d = out.shape
     m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
     loss = np.zeros(1, np.float64)
     dout = np.empty_like(out)
-    if lib().orc_mse_grad(_p(out), _p(target), _p(m), C.c_int64(n), C.c_int32(d), _p(loss), _p(dout)):
-        raise ValueError("orc_mse_grad rejected its arguments")
+    if lib().orc_mse_grad_global(_p(out), _p(target), _p(m), C.c_int64(n), C.c_int32(d), C.c_int64(global_rows),
+                                 _p(loss), _p(dout)):
+        raise ValueError("orc_mse_grad_global rejected its arguments")
     return float(loss[0]), dout
 
 

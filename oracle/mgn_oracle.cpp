@@ -537,9 +537,17 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
 
 int orc_mse_grad(const double* out, const double* target, const uint8_t* mask, int64_t n, int32_t d,
                  double* loss, double* d_out) {
-  if (n < 0 || d <= 0 || !loss) return -1;
+  return orc_mse_grad_global(out, target, mask, n, d, 0, loss, d_out);
+}
+
+// One part's share of the global mean over global_rows masked rows of all
+// parts (Algorithm 1's loss all-reduce); global_rows = 0: this part's own rows.
+int orc_mse_grad_global(const double* out, const double* target, const uint8_t* mask, int64_t n, int32_t d,
+                        int64_t global_rows, double* loss, double* d_out) {
+  if (n < 0 || d <= 0 || !loss || global_rows < 0) return -1;
   int64_t cnt = 0;
   for (int64_t i = 0; i < n; ++i) cnt += mask ? (mask[i] != 0) : 1;
+  if (global_rows > 0) cnt = global_rows;
   const double denom = (double)cnt * d;
   double L = 0;
   for (int64_t i = 0; i < n; ++i) {

@@ -90,6 +90,11 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
 int orc_mse_grad(const double* out, const double* target, const uint8_t* mask, int64_t n,
                  int32_t d, double* loss, double* d_out);
 
+/* One part's share of the global masked mean over global_rows rows of all
+ * parts (0: this part's own masked rows); d_out = gradient of the global loss. */
+int orc_mse_grad_global(const double* out, const double* target, const uint8_t* mask, int64_t n,
+                        int32_t d, int64_t global_rows, double* loss, double* d_out);
+
 /* Algorithm 1's update with learning rate eta: params -= lr * grad (n entries). */
 int orc_sgd_step(double* params, const double* grad, int64_t n, double lr);
 

@@ -27,7 +27,8 @@ EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mg
            "mgn_workspace_size",
            "mgn_forward", "mgn_backward", "mgn_forward_begin", "mgn_forward_block", "mgn_forward_end",
            "mgn_backward_begin", "mgn_backward_block", "mgn_backward_end", "mgn_halo_masks", "mgn_copy_latents",
-           "mgn_add_latent_grads", "mgn_mse_grad", "mgn_timing_enable", "mgn_timing_read"]
+           "mgn_add_latent_grads", "mgn_mse_grad", "mgn_mse_grad_global", "mgn_timing_enable",
+           "mgn_timing_read"]
 TIMERS = ["encode", "edge_fwd", "node_fwd", "decode", "edge_bwd", "node_bwd", "input_grad", "weight_grad",
           "other", "node_proj", "exchange"]
 
@@ -90,6 +91,7 @@ def lib() -> C.CDLL:
             "mgn_copy_latents": (C.c_int, [vp, vp, vp, i64, vp, i64, vp]),
             "mgn_add_latent_grads": (C.c_int, [vp, vp, i64, vp, vp, i64, vp]),
             "mgn_mse_grad": (C.c_int, [vp, vp, vp, i64, i32, vp, vp, vp]),
+            "mgn_mse_grad_global": (C.c_int, [vp, vp, vp, i64, i32, i64, vp, vp, vp]),
             "mgn_timing_enable": (C.c_int, [vp, C.c_int]),
             "mgn_timing_read": (C.c_int, [vp, C.c_int, vp, vp]),
         }
@@ -309,6 +311,12 @@ def mgn_mse_grad(out, target, mask, loss, d_out, stream=None) -> None:
     n, d = out.shape
     _check(lib().mgn_mse_grad(_dev(out), _dev(target), _dev(mask), n, d, _dev(loss), _dev(d_out),
                               _stream(stream)))
+
+
+def mgn_mse_grad_global(out, target, mask, global_rows: int, loss, d_out, stream=None) -> None:
+    n, d = out.shape
+    _check(lib().mgn_mse_grad_global(_dev(out), _dev(target), _dev(mask), n, d, int(global_rows), _dev(loss),
+                                     _dev(d_out), _stream(stream)))
 
 
 def mgn_timing_enable(model, enable: bool = True) -> None:

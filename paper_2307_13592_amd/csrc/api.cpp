@@ -1248,8 +1248,19 @@ extern "C" mgn_status mgn_mse_grad(const float* out, const float* target, const 
                                    float* loss, float* d_out, mgn_stream stream) {
   if (n < 0 || d < 1) return fail(nullptr, MGN_E_ARG, "mgn_mse_grad: bad sizes");
   if (!loss || (n > 0 && (!out || !target || !d_out))) return fail(nullptr, MGN_E_ARG, "mgn_mse_grad: NULL argument");
-  hipError_t e = launch_mse(out, target, mask, n, d, loss, d_out, (hipStream_t)stream);
+  hipError_t e = launch_mse(out, target, mask, n, d, 0, loss, d_out, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(nullptr, e, "mgn_mse_grad");
+  return MGN_OK;
+}
+
+extern "C" mgn_status mgn_mse_grad_global(const float* out, const float* target, const uint8_t* mask, int64_t n,
+                                          int32_t d, int64_t global_rows, float* loss, float* d_out,
+                                          mgn_stream stream) {
+  if (n < 0 || d < 1 || global_rows < 1) return fail(nullptr, MGN_E_ARG, "mgn_mse_grad_global: bad sizes");
+  if (!loss || (n > 0 && (!out || !target || !d_out)))
+    return fail(nullptr, MGN_E_ARG, "mgn_mse_grad_global: NULL argument");
+  hipError_t e = launch_mse(out, target, mask, n, d, global_rows, loss, d_out, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(nullptr, e, "mgn_mse_grad_global");
   return MGN_OK;
 }
 

@@ -183,8 +183,10 @@ hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, 
                             hipStream_t st);
 hipError_t launch_vec_reduce(const float* vpart, int nwg, int nvec, const VecSeg* segs, int nseg, float* dparams,
                              int accumulate, hipStream_t st);
-hipError_t launch_mse(const float* out, const float* target, const uint8_t* mask, int64_t n, int d, float* loss,
-                      float* d_out, hipStream_t st);
+// Masked MSE and its gradient; the mean is over global_rows rows when > 0,
+// else over this call's masked rows.
+hipError_t launch_mse(const float* out, const float* target, const uint8_t* mask, int64_t n, int d,
+                      int64_t global_rows, float* loss, float* d_out, hipStream_t st);
 
 // tile sizes the host needs to know (rows per edge sub-tile, per prec/L/D)
 int edge_tile_rows(int prec, int L, int D);

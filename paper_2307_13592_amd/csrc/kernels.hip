@@ -3551,8 +3551,9 @@ __global__ __launch_bounds__(NT) void mse_partial_kernel(const float* __restrict
 }
 
 // Combines the MSE_G partials in workgroup order; writes the loss and the
-// gradient scale 2 / (rows * d).
-__global__ void mse_final_kernel(const uint32_t* __restrict__ scratch, int d, float* __restrict__ loss,
+// gradient scale 2 / (rows * d), rows = the masked row count, or grows when
+// grows > 0 (a global mean over several parts: this part's share).
+__global__ void mse_final_kernel(const uint32_t* __restrict__ scratch, int d, int64_t grows, float* __restrict__ loss,
                                  float* __restrict__ scale) {
   if (threadIdx.x != 0) return;
   double t = 0.0;
@@ -3562,6 +3563,7 @@ __global__ void mse_final_kernel(const uint32_t* __restrict__ scratch, int d, fl
     t += __longlong_as_double((long long)bits);
     c += (int64_t)((uint64_t)scratch[4 * b + 2] | ((uint64_t)scratch[4 * b + 3] << 32));
   }
+  if (grows > 0) c = grows;
   const double den = (double)c * d;
   *loss = c > 0 ? (float)(t / den) : 0.f;
   *scale = c > 0 ? (float)(2.0 / den) : 0.f;
@@ -3569,7 +3571,8 @@ __global__ void mse_final_kernel(const uint32_t* __restrict__ scratch, int d, fl
 
 __global__ __launch_bounds__(NT) void mse_loss_kernel(const float* __restrict__ out, const float* __restrict__ tgt,
                                                       const uint8_t* __restrict__ mask, int64_t n, int d,
-                                                      float* __restrict__ loss, float* __restrict__ scale) {
+                                                      int64_t grows, float* __restrict__ loss,
+                                                      float* __restrict__ scale) {
   __shared__ double ss[NT];
   __shared__ int64_t sc[NT];
   double s = 0.0;
@@ -3592,6 +3595,7 @@ __global__ __launch_bounds__(NT) void mse_loss_kernel(const float* __restrict__ 
       t += ss[i];
       c += sc[i];
     }
+    if (grows > 0) c = grows;
     const double den = (double)c * d;
     *loss = c > 0 ? (float)(t / den) : 0.f;
     *scale = c > 0 ? (float)(2.0 / den) : 0.f;
@@ -3959,17 +3963,18 @@ hipError_t launch_vec_reduce(const float* vpart, int nwg, int nvec, const VecSeg
   return hipGetLastError();
 }
 
-hipError_t launch_mse(const float* out, const float* target, const uint8_t* mask, int64_t n, int d, float* loss,
-                      float* d_out, hipStream_t st) {
+hipError_t launch_mse(const float* out, const float* target, const uint8_t* mask, int64_t n, int d,
+                      int64_t global_rows, float* loss, float* d_out, hipStream_t st) {
   // loss[1] doubles as scratch for the gradient scale: scale is written to loss+1.
   // Large inputs: per-workgroup partials first, parked in d_out (overwritten
   // by the gradient afterwards).
   if (n * d >= 4 * MSE_G) {
     uint32_t* scratch = reinterpret_cast<uint32_t*>(d_out);
     hipLaunchKernelGGL(mse_partial_kernel, dim3(MSE_G), dim3(NT), 0, st, out, target, mask, n, d, scratch);
-    hipLaunchKernelGGL(mse_final_kernel, dim3(1), dim3(64), 0, st, scratch, d, loss, loss + 1);
+    hipLaunchKernelGGL(mse_final_kernel, dim3(1), dim3(64), 0, st, scratch, d, global_rows, loss, loss + 1);
   } else {
-    hipLaunchKernelGGL(mse_loss_kernel, dim3(1), dim3(NT), 0, st, out, target, mask, n, d, loss, loss + 1);
+    hipLaunchKernelGGL(mse_loss_kernel, dim3(1), dim3(NT), 0, st, out, target, mask, n, d, global_rows, loss,
+                       loss + 1);
   }
   if (n > 0)
     hipLaunchKernelGGL(mse_grad_kernel, dim3((unsigned)((n * d + NT - 1) / NT)), dim3(NT), 0, st, out, target, mask,

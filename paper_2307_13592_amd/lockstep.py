@@ -16,7 +16,8 @@ import numpy as np
 import torch
 
 from . import (mgn_add_latent_grads, mgn_backward_begin, mgn_backward_block, mgn_backward_end, mgn_copy_latents,
-               mgn_forward_begin, mgn_forward_block, mgn_forward_end, mgn_halo_masks, mgn_sgd_step)
+               mgn_forward_begin, mgn_forward_block, mgn_forward_end, mgn_halo_masks, mgn_mse_grad_global,
+               mgn_sgd_step)
 from .runner import Session
 
 
@@ -67,6 +68,24 @@ class Lockstep:
         for s in S:
             mgn_forward_end(s.model, stream)
         return [s.out for s in S]
+
+    def mse(self, targets, masks=None, stream=None):
+        """Algorithm 1's global loss: the mean squared error over the
+        loss-masked owned nodes of all parts.  targets[p], masks[p] (uint8 or
+        None) are device tensors of part p.  Returns (the parts' loss shares
+        as device scalars, which add up to the global loss; the parts' dOut)."""
+        S = self.sessions
+        if masks is None:
+            masks = [None] * len(S)
+        rows = sum(s.out.shape[0] if m is None else int(m.count_nonzero().item()) for s, m in zip(S, masks))
+        shares, d_outs = [], []
+        for s, t, m in zip(S, targets, masks):
+            loss = torch.empty(2, dtype=torch.float32, device=self.device)
+            d_out = torch.empty_like(s.out)
+            mgn_mse_grad_global(s.out, t, m, max(rows, 1), loss, d_out, stream)
+            shares.append(loss[0])
+            d_outs.append(d_out)
+        return shares, d_outs
 
     def backward(self, d_outs, stream=None):
         """d_outs[p]: dL/dout of part p's owned nodes.  Returns the summed

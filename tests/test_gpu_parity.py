@@ -187,3 +187,27 @@ def test_mse_grad():
     mgn.mgn_mse_grad(dev(out), dev(tgt), dev(mask), loss, dout)
     assert abs(loss[0].item() - L) / L < 1e-6
     assert rel_err(dout.cpu().numpy(), d) < 1e-6
+
+
+def test_mse_grad_global():
+    """Per-part shares of the global mean (three parts of 1000 rows)."""
+    import torch
+    say("[parity] global mse")
+    rng = np.random.default_rng(7)
+    out = rng.standard_normal((1000, 5)).astype(np.float32)
+    tgt = rng.standard_normal((1000, 5)).astype(np.float32)
+    mask = (rng.random(1000) < 0.6).astype(np.uint8)
+    rows = int(mask.sum())
+    dev = lambda a: torch.as_tensor(np.ascontiguousarray(a)).cuda()
+    total = 0.0
+    for a, b in ((0, 300), (300, 650), (650, 1000)):
+        L, d = oracle.mse_grad(out[a:b].astype(np.float64), tgt[a:b].astype(np.float64), mask[a:b],
+                               global_rows=rows)
+        loss = torch.empty(2, device="cuda")
+        dout = torch.empty((b - a, 5), device="cuda")
+        mgn.mgn_mse_grad_global(dev(out[a:b]), dev(tgt[a:b]), dev(mask[a:b]), rows, loss, dout)
+        assert abs(loss[0].item() - L) / L < 1e-6
+        assert rel_err(dout.cpu().numpy(), d) < 1e-6
+        total += loss[0].item()
+    L_all, _ = oracle.mse_grad(out.astype(np.float64), tgt.astype(np.float64), mask)
+    assert abs(total - L_all) / L_all < 1e-6

@@ -82,12 +82,23 @@ def test_training_steps_match_oracle():
 
 
 def test_lockstep_parts_stay_identical():
+    """A lockstep training step with Algorithm 1's global loss: the parts'
+    loss shares add up to the whole network's loss (oracle, bf16 mode), and
+    after the update every part holds the same parameters."""
     from test_gpu_lockstep import _lockstep_session
     say("[train] lockstep update, bf16")
-    ls, whole, own = _lockstep_session(meshes.sector(5, 12, 9, 4, seed=2), 4, 128, 2, 2, "bf16", 5)
+    mesh = meshes.sector(5, 12, 9, 4, seed=2)
+    ls, whole, own = _lockstep_session(mesh, 4, 128, 2, 2, "bf16", 5)
+    target = np.random.default_rng(31).standard_normal((mesh.n_nodes, 5)).astype(np.float32)
     try:
         ls.forward()
-        ls.backward([whole["d_out"][o] for o in own])
+        shares, d_outs = ls.mse([torch.as_tensor(target[o]).to(ls.device) for o in own])
+        gpu_loss = sum(float(x.item()) for x in shares)
+        ref_out = run_oracle(whole, 128, 2, 2, bf16=True)["out"]
+        ref_loss, _ = oracle.mse_grad(ref_out, target)
+        say(f"  global loss gpu {gpu_loss:.6f} oracle {ref_loss:.6f}")
+        assert abs(gpu_loss - ref_loss) / ref_loss <= TOL["bf16"]
+        ls.backward(d_outs)
         ls.sgd(0.02)
         ps = [mgn.mgn_get_params(s.model) for s in ls.sessions]
         assert not np.array_equal(ps[0], whole["params"])

@@ -301,3 +301,23 @@ def test_rollout_update_special_cases():
     assert np.array_equal(oracle.rollout_update(oracle.rollout_update(q, p), p), oracle.rollout_update(q, 2 * p))
     with pytest.raises(ValueError):
         oracle.rollout_update(nf, np.zeros((40, 5)), col0=7)
+
+
+def test_mse_global_shares_add_up_to_the_whole():
+    """Algorithm 1's loss all-reduce: the parts' shares of the global mean
+    add up to the mean over all rows, and their gradients are the rows of
+    the whole loss's gradient (the single-call form is pinned to autograd
+    above)."""
+    rng = np.random.default_rng(6)
+    out, tgt = rng.standard_normal((90, 5)), rng.standard_normal((90, 5))
+    mask = rng.integers(0, 2, 90).astype(np.uint8)
+    L, d = oracle.mse_grad(out, tgt, mask)
+    cuts = [0, 20, 55, 90]
+    rows = int(mask.sum())
+    shares, grads = [], []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        l_p, d_p = oracle.mse_grad(out[a:b], tgt[a:b], mask[a:b], global_rows=rows)
+        shares.append(l_p)
+        grads.append(d_p)
+    assert abs(sum(shares) - L) < 1e-14
+    assert np.array_equal(np.concatenate(grads), d)
