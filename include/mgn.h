@@ -166,9 +166,10 @@ mgn_status mgn_set_recompute(mgn_model* m, int32_t interval, int64_t chunk_edges
  * on != 0: the workspace holds one working copy of each stream (node
  * latents and their bf16 copy in a ping-pong pair, the edge latents updated
  * in place) and no backward buffers; mgn_backward then returns MGN_E_STATE.
- * Same arithmetic as the training plan: outputs are bitwise equal.  Takes
- * effect for the next mgn_workspace_size / mgn_forward (a pending step is
- * dropped). */
+ * Same arithmetic as the training plan: outputs are bitwise equal.  While on,
+ * the edge-stream checkpointing setting (mgn_set_recompute) is ignored.
+ * Takes effect for the next mgn_workspace_size / mgn_forward (a pending step
+ * is dropped). */
 mgn_status mgn_set_inference(mgn_model* m, int32_t on);
 
 /* Next-step rollout (section "Model": the network predicts the increment,
