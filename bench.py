@@ -30,12 +30,14 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic(timer: str, cfg, E: int, No: int, Nh: int):
+def algorithmic(timer: str, cfg, E: int, No: int, Nh: int, lean: bool = False):
     """Compulsory work of one launch of the kernel class `timer` for one
     block, as (HBM bytes, flops), for the bf16 row-split path the benchmark
     workload takes (latent 64/128, depth 2): each operand row counted once,
     gathered node rows once per node; flops are the MLP products (2 per
-    multiply-add).  E edges, No owned and Nh halo nodes."""
+    multiply-add).  E edges, No owned and Nh halo nodes; lean: the
+    checkpointed plan (the streaming edge backward then recomputes the first
+    Linear instead of reading the forward's ReLU output)."""
     l, D = cfg.latent, cfg.depth
     Nl = No + Nh
     if cfg.precision != "bf16" or D != 2 or l not in (64, 128):
@@ -44,16 +46,24 @@ def algorithmic(timer: str, cfg, E: int, No: int, Nh: int):
         # node rows gathered from the fp32 latents or their bf16 copy
         ts = 2 if cfg.precision == "bf16" else 4
         if timer == "edge_fwd":
-            # read e^k, ids, node rows; write e^{k+1} and agg
-            by = E * (2 * ts * l + 8) + Nl * ts * l + No * 4 * l
+            # read e^k, ids, node rows; write e^{k+1}, h_1 (kept for the
+            # backward unless lean) and agg
+            by = E * ((2 if lean else 3) * ts * l + 8) + Nl * ts * l + No * 4 * l
             return by, E * 2 * l * l * (D + 2)
-        if timer == "edge_bwd":
+        if timer == "edge_bwd" and lean:
             # recompute the forward, then the data gradients of every layer
             # and de^k = de^{k+1} + dz_0 W_e: read e^k, de^{k+1} (fp32), ids,
             # node rows, dagg; write de^k, D output gradients and D-1 hidden
             # activations, receiver sums of dz_0
             by = E * (ts * l + 4 * l + 8 + 4 * l + (2 * D - 1) * ts * l) + Nl * ts * l + No * 4 * l * 2
             return by, E * 4 * l * l * (D + 1)
+        if timer == "edge_bwd":
+            # from the forward's first-Linear ReLU output h_1: recompute the
+            # later layers, then their data gradients and de^k = de^{k+1} +
+            # dz_0 W_e: read h_1, de^{k+1} (fp32), ids, dagg; write de^k, D
+            # output gradients and D-2 hidden activations, receiver sums
+            by = E * (ts * l + 4 * l + 8 + 4 * l + (2 * D - 2) * ts * l) + No * 4 * l * 2
+            return by, E * 2 * l * l * (2 * D - 1)
         return None
     if timer == "edge_bwd":
         # read e^k (bf16), de^{k+1} (fp32), receiver / sender ids, dagg rows,
@@ -163,7 +173,7 @@ def main():
     # dominant kernel and its roofline position
     dom = max((k for k in timers if timers[k][1]), key=lambda k: timers[k][0])
     t_launch = timers[dom][0] / timers[dom][1] * 1e-3
-    alg = algorithmic(dom, cfg, ne, no, nh)
+    alg = algorithmic(dom, cfg, ne, no, nh, lean=recompute > 0)
     roof = None
     if alg is not None:
         # a block's edge backward may run as several receiver chunks

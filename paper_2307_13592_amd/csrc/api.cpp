@@ -38,7 +38,7 @@ struct MlpL {
 
 struct WsPlan {
   size_t erecv, chunk, unit_r, nunits, V, V16, PROJ, AGG, ES, DV[2], DAGG, DZS, DE, DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
-      HID_NK, PART, VPART, total;
+      HID_NK, HID_E1, PART, VPART, total;
   int64_t max_units;
   // edge-stream checkpointing: interval s (0: every block kept), checkpoints
   bool lean = false;
@@ -255,6 +255,10 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   // edge stream: every block's input, the checkpoints plus one working copy,
   // or (inference) one copy updated in place
   p.ES = take(ts * (size_t)(p.infer ? 1 : p.lean ? p.nck + 1 : std::max<int64_t>(K, 1)) * ne * L);
+  // streaming edge kernels, every block kept: each block's first-Linear ReLU
+  // output, written by the forward, so the backward skips recomputing the
+  // first Linear (half its products) and the row gather
+  p.HID_E1 = (!p.infer && !p.lean && K > 0 && !edge_rs(m->prec, m->L, m->D)) ? take(ts * (size_t)K * ne * L) : 0;
   if (p.infer) {
     p.total = o;
     return p;
@@ -531,6 +535,7 @@ hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p,
   ea.Eout = eout;
   ea.agg = agg;
   ea.eps = m->cfg.ln_eps;
+  ea.hid_out = p.HID_E1 ? (void*)(ws + p.HID_E1 + tsize(m) * (size_t)k * g.n_edges * L) : nullptr;
   const bool rs = edge_rs(m->prec, L, D);
   float* proj = rs ? proj_block(p, ws, k, no + nh, L) : nullptr;
   ea.proj = proj;
@@ -942,6 +947,11 @@ struct Bwd {
       const bool rs = edge_rs(m->prec, L, D);
       // the forward's projections of block k (or those of the aggregate recompute)
       a.proj = rs ? proj_block(p, ws, k, no + nh, L) : nullptr;
+      // the forward's first-Linear ReLU output of this block (stash-all
+      // streaming path): not recomputed, and the layer-2 weight gradient
+      // reads it in place
+      void* h1 = p.HID_E1 ? (void*)(ws + p.HID_E1 + ts * (size_t)k * ne * L) : nullptr;
+      a.hid_in = h1;
       for (int j = 0; j < 3; ++j) a.delta[j] = DEL_E[j];
       for (int j = 0; j < 2; ++j) a.hid[j] = HID_E[j];
       a.vpart = VP;
@@ -961,7 +971,8 @@ struct Bwd {
         CHK("edge block");
         e = run_vec(m, ml, d_params, acc, st, edge_bwd_grid(m->prec, L, D, BWD_GRID));
         CHK("edge vec");
-        e = dw_hidden(ml, rows, DEL_E, HID_E, L, acc);
+        void* hid_c[2] = {h1 ? (void*)((char*)h1 + ts * (size_t)e0 * L) : HID_E[0], HID_E[1]};
+        e = dw_hidden(ml, rows, DEL_E, hid_c, L, acc);
         CHK("edge dW");
         // first Linear's weight gradient, e block: e rows of the chunk
         DwArgs w{};

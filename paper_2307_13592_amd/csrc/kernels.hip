@@ -1120,6 +1120,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
         }
       }
       __syncthreads();
+      // kept for the backward (HB is read-only until the next sub-tile)
+      if (a.hid_out) store_rows(reinterpret_cast<T*>(a.hid_out) + sb * L, HB, Lay::LDH, n, L);
       const T* hin = HB;
       if constexpr (D == 3) {
         floatx4 acc[MB][NBW];
@@ -1264,10 +1266,22 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
             da[m][nn][r] = ok ? a.dagg[rv * L + col] : 0.f;
           }
         }
-      gather_rows<P, L, TE, Lay::LDA>(A, mt, Ein, a.V, a.H, a.V16, a.n_owned, sb, n);
-      __syncthreads();
-      // recompute the forward: hidden activations, then the LN input
-      {
+      if (a.hid_in) {
+        // the forward's first-Linear ReLU output (rows past n zero: they
+        // carry dm = 0 and contribute nothing)
+        constexpr int E16 = 16 / sizeof(T);
+        constexpr int CPR = L / E16;
+        const T* hsrc = reinterpret_cast<const T*>(a.hid_in) + sb * L;
+        for (int i = tid; i < TE * CPR; i += NT) {
+          const int r = i / CPR, c = (i % CPR) * E16;
+          uint4 v = make_uint4(0, 0, 0, 0);
+          if (r < n) v = *reinterpret_cast<const uint4*>(hsrc + (int64_t)r * L + c);
+          *reinterpret_cast<uint4*>(HB + r * Lay::LDH + c) = v;
+        }
+      } else {
+        gather_rows<P, L, TE, Lay::LDA>(A, mt, Ein, a.V, a.H, a.V16, a.n_owned, sb, n);
+        __syncthreads();
+        // recompute the forward: hidden activations, then the LN input
         floatx4 acc[MB][NBW];
         wave_gemm_k<P, MB, NBW, NK1>(A, Lay::LDA, a.mlp.lin[0].wf, nb0, acc);
         store_acc<P, MB, NBW, true>(acc, nb0, a.mlp.lin[0].b, L, HB, Lay::LDH);
@@ -1328,7 +1342,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
         }
       __syncthreads();
       store_rows(reinterpret_cast<T*>(a.delta[D - 1]) + (sb - a.e_base) * L, A, Lay::LDA, n, L);
-      store_rows(reinterpret_cast<T*>(a.hid[0]) + (sb - a.e_base) * L, HB, Lay::LDH, n, L);
+      if (!a.hid_in) store_rows(reinterpret_cast<T*>(a.hid[0]) + (sb - a.e_base) * L, HB, Lay::LDH, n, L);
       if constexpr (D == 3) store_rows(reinterpret_cast<T*>(a.hid[1]) + (sb - a.e_base) * L, HC, Lay::LDH, n, L);
       // hidden layers: dz_{j-1} = (dz_j W_j) * [h_{j-1} > 0], into A column block D-j
 #pragma unroll
