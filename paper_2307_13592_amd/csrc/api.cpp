@@ -577,6 +577,7 @@ hipError_t run_dw(mgn_model* m, const LinL& L, DwArgs a, float* d_params, int ac
   }
   Timed t_(m, MGN_T_WEIGHT_GRAD, st);
   if (dw_stream_ok(m->prec, a)) return launch_dw_stream(a, dst, L.in, accumulate, st);
+  if (dw_stream_f32_ok(m->prec, a)) return launch_dw_stream_f32(a, dst, L.in, accumulate, st);
   hipError_t e = launch_dw(m->prec, a, st);
   if (e == hipSuccess) e = launch_dw_reduce(a.part, a.S, a.O, a.I, dst, L.in, accumulate, st);
   return e;

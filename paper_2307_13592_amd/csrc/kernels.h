@@ -182,6 +182,10 @@ hipError_t launch_sender_sums(int prec, int L, const int32_t* trow, const int32_
 int dw_stream_parts();
 bool dw_stream_ok(int prec, const DwArgs& a);
 hipError_t launch_dw_stream(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st);
+// The same for fp32 layers with 128 inputs and 128 outputs (dw_stream_f32_ok):
+// wave partials in plain [o][i] order, then the fixed-order split reduction.
+bool dw_stream_f32_ok(int prec, const DwArgs& a);
+hipError_t launch_dw_stream_f32(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st);
 hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st);
 hipError_t launch_dw_reduce(const float* part, int S, int O, int I, float* dst, int ldw, int accumulate,
                             hipStream_t st);

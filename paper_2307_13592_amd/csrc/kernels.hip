@@ -3448,6 +3448,82 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
       out[(j * 8 + jj) * 64 + lane] = make_float4(acc[j][jj][0], acc[j][jj][1], acc[j][jj][2], acc[j][jj][3]);
 }
 
+// fp32 form: dW = D^T A for fp32 row-major D [R][ldd] and A [R][lda], 128
+// columns each (the per-edge layers at l = 128 in fp32).  The 16x16x4 fp32
+// MFMA takes one value per lane, A[i][k] from lane (k, i) and B[k][j] from
+// lane (k, j), so row-major loads need no transpose: per 4-row k-group, lane
+// (q, m) = (lane >> 4, lane & 15) loads row q's columns 4m .. 4m + 3 and
+// 64 + 4m .. 64 + 4m + 3 of both operands (float4 each), and component c of
+// half h stands for column 64 h + 4 m + c; accumulator block (h, c, h', c')
+// then holds dW[64 h + 4 i + c][64 h' + 4 j + c'] at (i, j) of its 16 x 16
+// tile.  One wave per SIMD, 64 blocks = the 256 accumulator registers; a
+// 16-row step's loads are issued one step ahead.  part[w] = wave w's sum in
+// plain [o][i] order (reduced by dw_reduce_kernel).
+__device__ __forceinline__ void dwf_load(const float* __restrict__ D, int ldd, const float* __restrict__ A, int lda,
+                                         int64_t row, int64_t R, int m, float4 (&v)[4][4]) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int64_t r = row + 4 * g;
+    const bool ok = r < R;
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    v[g][0] = ok ? *reinterpret_cast<const float4*>(D + r * ldd + 4 * m) : z;
+    v[g][1] = ok ? *reinterpret_cast<const float4*>(D + r * ldd + 64 + 4 * m) : z;
+    v[g][2] = ok ? *reinterpret_cast<const float4*>(A + r * lda + 4 * m) : z;
+    v[g][3] = ok ? *reinterpret_cast<const float4*>(A + r * lda + 64 + 4 * m) : z;
+  }
+}
+
+__device__ __forceinline__ float f4c(const float4& v, int c) { return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w; }
+
+__global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void dw_stream_f32_kernel(
+    const float* __restrict__ D, int ldd, const float* __restrict__ A, int lda, int64_t R, float* __restrict__ part) {
+  const int lane = threadIdx.x & 63, q = lane >> 4, m = lane & 15;
+  const int64_t w = (int64_t)blockIdx.x * (DWS_NT / 64) + wave_id();
+  const int64_t nw = (int64_t)gridDim.x * (DWS_NT / 64);
+  const int64_t steps = (R + 15) / 16;
+  const int64_t s0 = steps * w / nw, s1 = steps * (w + 1) / nw;  // this wave's 16-row steps
+  floatx4 acc[8][8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) acc[j][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+  float4 cur[4][4], nxt[4][4];
+  if (s0 < s1) dwf_load(D, ldd, A, lda, s0 * 16 + q, R, m, nxt);
+  for (int64_t st = s0; st < s1; ++st) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) cur[g][t] = nxt[g][t];
+    if (st + 1 < s1) dwf_load(D, ldd, A, lda, (st + 1) * 16 + q, R, m, nxt);
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc)
+              acc[h * 4 + c][hh * 4 + cc] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                  f4c(cur[g][h], c), f4c(cur[g][2 + hh], cc), acc[h * 4 + c][hh * 4 + cc], 0, 0, 0);
+  }
+  float* out = part + w * 16384;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int o = 64 * h + 4 * (4 * q + r) + c, i = 64 * hh + 4 * m + cc;
+            out[o * 128 + i] = acc[h * 4 + c][hh * 4 + cc][r];
+          }
+}
+
 // dst[o * ldw + i] (+)= sum over the S wave partials, in wave order within
 // each of four interleaved sets, combined in set order; entry x of a partial
 // is (j, j', lane, r) -> o = 8 (4 (lane >> 4) + r) + j, i = 8 (lane & 15) + j'.
@@ -3939,6 +4015,20 @@ hipError_t launch_dw(int prec, const DwArgs& a, hipStream_t st) {
 }
 
 int dw_stream_parts() { return DWS_WAVES; }
+
+bool dw_stream_f32_ok(int prec, const DwArgs& a) {
+  return prec == F32 && a.a_kind == 0 && a.d_kind == 0 && a.O == 128 && a.I == 128 && a.ldd % 4 == 0 &&
+         a.lda0 % 4 == 0 && a.R >= 8192 && ((uintptr_t)a.delta % 16) == 0 && ((uintptr_t)a.a0 % 16) == 0;
+}
+
+hipError_t launch_dw_stream_f32(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st) {
+  hipLaunchKernelGGL(dw_stream_f32_kernel, dim3(DWS_GRID), dim3(DWS_NT), 0, st,
+                     reinterpret_cast<const float*>(a.delta), a.ldd, reinterpret_cast<const float*>(a.a0), a.lda0,
+                     a.R, a.part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_dw_reduce(a.part, DWS_WAVES, 128, 128, dst, ldw, accumulate, st);
+}
 
 bool dw_stream_ok(int prec, const DwArgs& a) {
   return prec == BF16 && a.a_kind == 0 && (a.d_kind == 0 || a.d_kind == 1) && a.O == 128 && a.I == 128 &&

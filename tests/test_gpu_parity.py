@@ -70,11 +70,12 @@ def test_sector_partition(prec, l, D):
     _case("sector 6x16x10 p1", meshes.sector(6, 16, 10, 4, seed=7), 1, l, 3, D, prec)
 
 
-def test_sector_medium_bf16():
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_sector_medium(prec):
     """A partition large enough (>= 8192 edge and node rows) for the
     register-resident weight-gradient kernels, which smaller cases do not
     reach; halo on both sides."""
-    _case("sector 40x16x60 p1", meshes.sector(40, 16, 60, 4, seed=9), 1, 128, 2, 2, "bf16")
+    _case("sector 40x16x60 p1", meshes.sector(40, 16, 60, 4, seed=9), 1, 128, 2, 2, prec)
 
 
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
