@@ -911,20 +911,23 @@ struct Bwd {
       CHK("node block");
       e = run_vec(m, ml, d_params, accumulate, st, rows_bwd_grid(m->prec, L, D, NODE_BLOCK, BWD_GRID));
       CHK("node vec");
+      // first Linear, input [v | agg]: one weight gradient per column block
+      // (each a plain row-major operand, so the register-resident kernels
+      // take them at l = 128); fp32 rows enter bf16 products rounded
       DwArgs w{};
       w.delta = DEL_N[0];
       w.ldd = L;
-      if (p.lean) {
-        w.a_kind = 5;
-        w.a3 = b.V16(k);
-      } else {
-        w.a_kind = 3;
-        w.a0 = b.V(k);
-      }
-      w.a1 = b.AGG(k);
+      w.lda0 = L;
       w.R = no;
-      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st);
-      CHK("node dW");
+      const bool st_v = m->prec == F32 || !p.lean;  // v in the storage type (fp32 V) or bf16 copy
+      w.a_kind = (m->prec == BF16 && !p.lean) ? 1 : 0;
+      w.a0 = st_v ? (const void*)b.V(k) : b.V16(k);
+      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st, 0, L);
+      CHK("node dW (v block)");
+      w.a_kind = m->prec == BF16 ? 1 : 0;
+      w.a0 = b.AGG(k);
+      e = run_dw(m, ml.lin[0], w, d_params, accumulate, st, L, L);
+      CHK("node dW (agg block)");
       e = dw_hidden(ml, no, DEL_N, hidk, L, accumulate);
       CHK("node dW");
     }

@@ -3348,6 +3348,23 @@ __device__ __forceinline__ void dws_load(const uint16_t* __restrict__ X, int ldx
   }
 }
 
+// fp32 rows, rounded to bf16 (the products' operand) in the layout of dws_load.
+__device__ __forceinline__ void dws_load_cvt(const float* __restrict__ X, int ldx, int64_t row, int64_t R, int col,
+                                             uint32_t (&v)[8][4]) {
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+    if (row + r < R) {
+      a = *reinterpret_cast<const float4*>(X + (row + r) * ldx + col);
+      b = *reinterpret_cast<const float4*>(X + (row + r) * ldx + col + 4);
+    }
+    v[r][0] = (uint32_t)f2bf(a.x) | ((uint32_t)f2bf(a.y) << 16);
+    v[r][1] = (uint32_t)f2bf(a.z) | ((uint32_t)f2bf(a.w) << 16);
+    v[r][2] = (uint32_t)f2bf(b.x) | ((uint32_t)f2bf(b.y) << 16);
+    v[r][3] = (uint32_t)f2bf(b.z) | ((uint32_t)f2bf(b.w) << 16);
+  }
+}
+
 __device__ __forceinline__ void dws_mma(const uint32_t (&fd)[8][4], const uint32_t (&fa)[8][4], floatx4 (&acc)[8][8]) {
 #pragma unroll
   for (int j = 0; j < 8; ++j)
@@ -3385,10 +3402,17 @@ __device__ __forceinline__ void dws_split(const float4 (&v)[8][2], uint32_t (&hi
 
 // part[w] (16384 floats, accumulator order [j][j'][lane][4]) = wave w's sum.
 // SPLIT: D is fp32 and enters the products as hi + lo (two MFMAs each).
-template <bool SPLIT>
+// AF32: A is fp32, rounded to bf16 as it is loaded.
+template <bool SPLIT, bool AF32 = false>
 __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void dw_stream_kernel(
-    const void* __restrict__ Dv, int ldd, const uint16_t* __restrict__ A, int lda, int64_t R,
+    const void* __restrict__ Dv, int ldd, const void* __restrict__ Av, int lda, int64_t R,
     float* __restrict__ part) {
+  const auto load_a = [&](int64_t row, int col, uint32_t (&v)[8][4]) {
+    if constexpr (AF32)
+      dws_load_cvt(reinterpret_cast<const float*>(Av), lda, row, R, col, v);
+    else
+      dws_load(reinterpret_cast<const uint16_t*>(Av), lda, row, R, col, v);
+  };
   const int lane = threadIdx.x & 63, q = lane >> 4, m = lane & 15;
   const int64_t w = (int64_t)blockIdx.x * (DWS_NT / 64) + wave_id();
   const int64_t nw = (int64_t)gridDim.x * (DWS_NT / 64);
@@ -3408,7 +3432,7 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
     uint32_t av[8][4], fa[8][4];
     if (s0 < s1) {
       dws_load_f32(D, ldd, s0 * 32 + rq, R, 8 * m, dv);
-      dws_load(A, lda, s0 * 32 + rq, R, 8 * m, av);
+      load_a(s0 * 32 + rq, 8 * m, av);
     }
     for (int64_t st = s0; st < s1; ++st) {
       uint32_t hi[8][4], lo[8][4], f[8][4];
@@ -3416,7 +3440,7 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
       dws_transpose(av, fa);
       if (st + 1 < s1) {
         dws_load_f32(D, ldd, (st + 1) * 32 + rq, R, 8 * m, dv);
-        dws_load(A, lda, (st + 1) * 32 + rq, R, 8 * m, av);
+        load_a((st + 1) * 32 + rq, 8 * m, av);
       }
       dws_transpose(hi, f);
       dws_mma(f, fa, acc);
@@ -3428,14 +3452,14 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
     uint32_t dv[8][4], av[8][4], fd[8][4], fa[8][4];
     if (s0 < s1) {
       dws_load(D, ldd, s0 * 32 + rq, R, 8 * m, dv);
-      dws_load(A, lda, s0 * 32 + rq, R, 8 * m, av);
+      load_a(s0 * 32 + rq, 8 * m, av);
     }
     for (int64_t st = s0; st < s1; ++st) {
       dws_transpose(dv, fd);
       dws_transpose(av, fa);
       if (st + 1 < s1) {
         dws_load(D, ldd, (st + 1) * 32 + rq, R, 8 * m, dv);
-        dws_load(A, lda, (st + 1) * 32 + rq, R, 8 * m, av);
+        load_a((st + 1) * 32 + rq, 8 * m, av);
       }
       dws_mma(fd, fa, acc);
     }
@@ -4031,17 +4055,22 @@ hipError_t launch_dw_stream_f32(const DwArgs& a, float* dst, int ldw, int accumu
 }
 
 bool dw_stream_ok(int prec, const DwArgs& a) {
-  return prec == BF16 && a.a_kind == 0 && (a.d_kind == 0 || a.d_kind == 1) && a.O == 128 && a.I == 128 &&
-         a.ldd % 8 == 0 && a.lda0 % 8 == 0 && a.R >= 8192;
+  // A: bf16 rows (a_kind 0) or fp32 rows rounded on load (a_kind 1, bf16 delta)
+  return prec == BF16 && (a.a_kind == 0 || (a.a_kind == 1 && a.d_kind == 0)) &&
+         (a.d_kind == 0 || a.d_kind == 1) && a.O == 128 && a.I == 128 && a.ldd % 8 == 0 && a.lda0 % 8 == 0 &&
+         a.R >= 8192;
 }
 
 hipError_t launch_dw_stream(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st) {
   if (a.d_kind == 1)
-    hipLaunchKernelGGL(dw_stream_kernel<true>, dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd,
-                       reinterpret_cast<const uint16_t*>(a.a0), a.lda0, a.R, a.part);
+    hipLaunchKernelGGL((dw_stream_kernel<true, false>), dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd, a.a0,
+                       a.lda0, a.R, a.part);
+  else if (a.a_kind == 1)
+    hipLaunchKernelGGL((dw_stream_kernel<false, true>), dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd, a.a0,
+                       a.lda0, a.R, a.part);
   else
-    hipLaunchKernelGGL(dw_stream_kernel<false>, dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd,
-                       reinterpret_cast<const uint16_t*>(a.a0), a.lda0, a.R, a.part);
+    hipLaunchKernelGGL((dw_stream_kernel<false, false>), dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd, a.a0,
+                       a.lda0, a.R, a.part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(dw_stream_reduce_kernel, dim3(16384 / 64), dim3(NT), 0, st, a.part, DWS_WAVES, dst, ldw,
