@@ -106,6 +106,9 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="capture the step into a HIP graph once and time its replays (per-kernel timing and "
                          "the roofline are then omitted: events cannot be read per launch inside a graph)")
+    ap.add_argument("--peaks", action="store_true",
+                    help="measure what plain streaming kernels and library GEMMs reach on this GPU (the practical "
+                         "ceilings beside the spec peaks) and exit")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB once (a plain copy kernel of known size, "
@@ -120,6 +123,8 @@ def main():
     import paper_2307_13592_amd as mgn
     from paper_2307_13592_amd.runner import Session
 
+    if args.peaks:
+        return measure_peaks()
     cfg = synth.CONFIGS[args.config]
     if args.precision:
         cfg = synth.Config(**{**cfg.__dict__, "precision": args.precision})
@@ -216,6 +221,47 @@ def main():
         "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},
     }
     print(json.dumps(line), flush=True)
+
+
+def measure_peaks():
+    """Practical ceilings: HBM rates of plain streaming kernels (4 GiB
+    operands) and the matrix rates of library GEMMs (hipBLASLt through
+    torch.matmul, 8192^3), beside the spec peaks."""
+    import torch
+
+    def timed(f, n=10):
+        f()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(n):
+            f()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n * 1e-3
+
+    N = 2 ** 30  # 4 GiB of fp32
+    x = torch.ones(N, device="cuda")
+    y = torch.empty_like(x)
+    res = {"copy_tb_s": 8 * N / timed(lambda: y.copy_(x)) / 1e12,
+           "read_sum_tb_s": 4 * N / timed(lambda: x.sum()) / 1e12,
+           "write_fill_tb_s": 4 * N / timed(lambda: y.fill_(1.0)) / 1e12}
+    h = N // 2
+    z = torch.empty(h, device="cuda")
+    res["add_2r1w_tb_s"] = 12 * h / timed(lambda: torch.add(x[:h], x[h:], out=z)) / 1e12
+    del x, y, z
+    for dt, name in ((torch.bfloat16, "bf16"), (torch.float32, "fp32")):
+        n = 8192
+        a = torch.randn(n, n, device="cuda").to(dt)
+        b = torch.randn(n, n, device="cuda").to(dt)
+        res[f"gemm_{name}_tflop_s"] = 2 * n ** 3 / timed(lambda: torch.matmul(a, b), 20) / 1e12
+        del a, b
+    torch.cuda.empty_cache()
+    res["spec"] = {"hbm_tb_s": PEAK["hbm"] / 1e12, "bf16_tflop_s": PEAK["bf16"] / 1e12,
+                   "fp32_tflop_s": PEAK["fp32"] / 1e12}
+    for k, v in res.items():
+        log(f"[bench] {k}: {v}")
+    print(json.dumps({"peaks": res}), flush=True)
 
 
 def bench_graph(args, cfg, sess, step, ne, no, nh):
