@@ -125,3 +125,35 @@ def test_staged_equals_single_call(prec):
         s.close()
     for x, y in zip(got, ref):
         assert np.array_equal(x, y)
+
+
+def test_exchange_rows_and_range_checks():
+    """mgn_copy_latents copies exactly the listed rows (the owner's current
+    node latents: after mgn_forward_begin these are the encoder outputs,
+    checked against the oracle's v^0) and leaves the rest of the halo block
+    alone; pairs with an index outside the owner's rows or the halo block
+    are skipped by the kernel's own range check."""
+    import torch
+    say("[lockstep] exchange rows and range checks")
+    mesh = meshes.sector(5, 12, 9, 4, seed=2)
+    ls, whole, own = _lockstep_session(mesh, 4, 64, 2, 2, "fp32", 5)
+    try:
+        s1, s2 = ls.sessions[1], ls.sessions[2]
+        mgn.mgn_forward_begin(s2.model, s2.gs, s2.node_feat, s2.edge_feat, s2.halo, s2.out, s2.workspace)
+        nh = s1.halo.shape[1]
+        halo_k = torch.full((nh, 64), 7.0, device=s1.device)
+        send = torch.tensor([0, 3, 10**6, 5], dtype=torch.int32, device=s1.device)  # 10**6: past the owner's rows
+        recv = torch.tensor([2, 4, 6, nh + 9], dtype=torch.int32, device=s1.device)  # nh + 9: past the halo
+        mgn.mgn_copy_latents(s2.model, send, recv, halo_k)
+        got = halo_k.cpu().numpy()
+        # the owner's v^0 rows from the oracle's whole-mesh run (local ids of part 2 -> global ids)
+        import oracle
+        r = oracle.step(oracle.ModelCfg(64, 2, 2), whole["g"], whole["params"].astype(np.float64),
+                        whole["nf"].astype(np.float64), whole["ef"].astype(np.float64), None, None, want_v=True)
+        v0 = r["v_all"][0][own[2]]
+        assert rel_err(got[[2, 4]], v0[[0, 3]]) <= 1e-5
+        untouched = np.ones(nh, bool)
+        untouched[[2, 4]] = False
+        assert np.all(got[untouched] == 7.0)
+    finally:
+        ls.close()
