@@ -45,6 +45,8 @@ struct WsPlan {
   int s = 0, nck = 0;
   // forward-only plan (inference): working copies only, no backward buffers
   bool infer = false;
+  // node projections kept per block (row-split kernels, every block kept)
+  bool proj_all = false;
   // receiver / edge boundaries of the backward's edge chunks
   std::vector<int64_t> cr, ce;
 };
@@ -250,7 +252,10 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.V16 = m->prec == BF16 ? take(2 * (size_t)(p.infer ? 2 : K + 1) * nl * L) : 0;
   // row-split edge kernels: node projections of every block's input (kept for
   // the backward), or of the current block only (checkpointing, inference)
-  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(one ? 1 : K) * nl * 2 * L) : 0;
+  p.proj_all = edge_rs(m->prec, m->L, m->D) && !one;
+  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(one ? 1 : K) * nl * 2 * L)
+           : edge_rsb(m->prec, m->L, m->D) ? take(4 * (size_t)nl * 2 * L)  // l = 256 forward: the current block's
+           : 0;
   p.AGG = take(4 * (size_t)(one ? 1 : K) * no * L);
   // edge stream: every block's input, the checkpoints plus one working copy,
   // or (inference) one copy updated in place
@@ -512,7 +517,7 @@ namespace {
 // null), ordered receiver sums into agg.
 // Node projections of block k (one shared slot when checkpointing).
 float* proj_block(const WsPlan& p, char* ws, int k, int64_t nl, int L) {
-  return (float*)(ws + p.PROJ) + (p.lean || p.infer ? 0 : (size_t)k * nl * 2 * L);
+  return (float*)(ws + p.PROJ) + (p.proj_all ? (size_t)k * nl * 2 * L : 0);
 }
 
 hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p, char* ws, const float* halo, int k,
@@ -536,7 +541,7 @@ hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p,
   ea.agg = agg;
   ea.eps = m->cfg.ln_eps;
   ea.hid_out = p.HID_E1 ? (void*)(ws + p.HID_E1 + tsize(m) * (size_t)k * g.n_edges * L) : nullptr;
-  const bool rs = edge_rs(m->prec, L, D);
+  const bool rs = edge_rs(m->prec, L, D) || edge_rsb(m->prec, L, D);
   float* proj = rs ? proj_block(p, ws, k, no + nh, L) : nullptr;
   ea.proj = proj;
   hipError_t e = hipSuccess;
@@ -949,8 +954,10 @@ struct Bwd {
       a.dagg = DAGG;
       a.de_out = DE;
       const bool rs = edge_rs(m->prec, L, D);
-      // the forward's projections of block k (or those of the aggregate recompute)
-      a.proj = rs ? proj_block(p, ws, k, no + nh, L) : nullptr;
+      // the forward's projections of block k (or those of the aggregate
+      // recompute; with the l = 256 row-split forward the checkpointed plan's
+      // recompute of the first layer uses them too)
+      a.proj = (rs || (p.lean && edge_rsb(m->prec, L, D))) ? proj_block(p, ws, k, no + nh, L) : nullptr;
       // the forward's first-Linear ReLU output of this block (stash-all
       // streaming path): not recomputed, and the layer-2 weight gradient
       // reads it in place

@@ -109,7 +109,9 @@ __device__ __forceinline__ void wave_gemm(const typename P::T* A, int lda, const
 // pipelined: B fragments are fetched PF k-groups ahead (a ring of registers),
 // A fragments one k-group ahead, so neither global nor LDS latency is waited
 // on inside the loop.  ZERO = false accumulates onto acc.
-template <class P, int MB, int NBW, int NKG, bool ZERO = true>
+// STRIDE: k-groups per 16-column block of the packed layer (NKG unless the
+// product uses a k-range of a wider layer, Bp then pointing at its start).
+template <class P, int MB, int NBW, int NKG, bool ZERO = true, int STRIDE = NKG>
 __device__ __forceinline__ void wave_gemm_k(const typename P::T* A, int lda, const uint4* __restrict__ Bp, int nb0,
                                             floatx4 (&acc)[MB][NBW]) {
   constexpr int PFW = NBW >= 4 ? 2 : (NBW == 2 ? 4 : 6);  // at most ~8 fragments in flight
@@ -122,12 +124,12 @@ __device__ __forceinline__ void wave_gemm_k(const typename P::T* A, int lda, con
       for (int n = 0; n < NBW; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
   const typename P::T* Ar = A + (lane & 15) * lda + (lane >> 4) * P::EL;
-  const uint4* Bl = Bp + (size_t)nb0 * NKG * 64 + lane;
+  const uint4* Bl = Bp + (size_t)nb0 * STRIDE * 64 + lane;
   uint4 b[PF][NBW];
 #pragma unroll
   for (int p = 0; p < PF; ++p)
 #pragma unroll
-    for (int n = 0; n < NBW; ++n) b[p][n] = Bl[(n * NKG + p) * 64];
+    for (int n = 0; n < NBW; ++n) b[p][n] = Bl[(n * STRIDE + p) * 64];
   uint4 a[2][MB];
 #pragma unroll
   for (int m = 0; m < MB; ++m) a[0][m] = *reinterpret_cast<const uint4*>(Ar + m * 16 * lda);
@@ -138,7 +140,7 @@ __device__ __forceinline__ void wave_gemm_k(const typename P::T* A, int lda, con
     for (int n = 0; n < NBW; ++n) bc[n] = b[kg % PF][n];
     if (kg + PF < NKG) {
 #pragma unroll
-      for (int n = 0; n < NBW; ++n) b[kg % PF][n] = Bl[(n * NKG + kg + PF) * 64];
+      for (int n = 0; n < NBW; ++n) b[kg % PF][n] = Bl[(n * STRIDE + kg + PF) * 64];
     }
     if (kg + 1 < NKG) {
 #pragma unroll

@@ -171,6 +171,10 @@ int edge_bwd_grid(int prec, int L, int D, int grid);
 // projections of launch_node_proj for each block).
 bool edge_rs(int prec, int L, int D);
 hipError_t launch_node_proj(int L, const void* v16, int64_t n_local, const Lin& w1, float* proj, hipStream_t st);
+// bf16, l = 256: the edge forward in row-split form with 64-edge tiles (needs
+// the node projections of launch_node_proj for the block; the edge backward
+// keeps the concatenated form).
+bool edge_rsb(int prec, int L, int D);
 hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t st);
 // Per-sender sums of dz_0 over the edges [e_lo, e_hi) (dz rows stored from e_lo),
 // assigned (first) or added into dzs.
