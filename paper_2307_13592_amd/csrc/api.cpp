@@ -583,6 +583,28 @@ hipError_t run_dw(mgn_model* m, const LinL& L, DwArgs a, float* d_params, int ac
   Timed t_(m, MGN_T_WEIGHT_GRAD, st);
   if (dw_stream_ok(m->prec, a)) return launch_dw_stream(a, dst, L.in, accumulate, st);
   if (dw_stream_f32_ok(m->prec, a)) return launch_dw_stream_f32(a, dst, L.in, accumulate, st);
+  if ((a.O > 128 || a.I > 128) && a.O % 128 == 0 && a.I % 128 == 0) {
+    // wider layers (l = 256) as 128 x 128 blocks on the register-resident
+    // kernels: each block re-reads its column ranges of both operands
+    DwArgs q = a;
+    q.O = 128;
+    q.I = 128;
+    const bool bf = dw_stream_ok(m->prec, q), f32 = dw_stream_f32_ok(m->prec, q);
+    if (bf || f32) {
+      const size_t st_sz = tsize(m);
+      const size_t ds = a.d_kind == 1 ? 4 : st_sz, as = a.a_kind == 1 ? 4 : st_sz;
+      for (int o0 = 0; o0 < a.O; o0 += 128)
+        for (int i0 = 0; i0 < a.I; i0 += 128) {
+          q.delta = (const char*)a.delta + ds * o0;
+          q.a0 = (const char*)a.a0 + as * i0;
+          float* qd = dst + (size_t)o0 * L.in + i0;
+          hipError_t e = bf ? launch_dw_stream(q, qd, L.in, accumulate, st)
+                            : launch_dw_stream_f32(q, qd, L.in, accumulate, st);
+          if (e != hipSuccess) return e;
+        }
+      return hipSuccess;
+    }
+  }
   hipError_t e = launch_dw(m->prec, a, st);
   if (e == hipSuccess) e = launch_dw_reduce(a.part, a.S, a.O, a.I, dst, L.in, accumulate, st);
   return e;

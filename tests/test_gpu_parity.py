@@ -70,6 +70,13 @@ def test_sector_partition(prec, l, D):
     _case("sector 6x16x10 p1", meshes.sector(6, 16, 10, 4, seed=7), 1, l, 3, D, prec)
 
 
+def test_sector_medium_l256():
+    """l = 256, depth 3, bf16 on a partition large enough (>= 8192 rows) for
+    the weight gradients of the 256 x 256 layers to run as 128 x 128 blocks
+    on the register-resident kernels."""
+    _case("sector 40x16x60 p1 l=256", meshes.sector(40, 16, 60, 4, seed=9), 1, 256, 1, 3, "bf16")
+
+
 @pytest.mark.parametrize("prec", ["fp32", "bf16"])
 def test_sector_medium(prec):
     """A partition large enough (>= 8192 edge and node rows) for the
