@@ -1190,7 +1190,13 @@ struct EdgeBwdLds {
 // LN-backward output and the hidden activations go to HBM for the weight
 // gradients; bias / gamma / beta gradients are per-lane column partials over
 // the workgroup's rows, written once at the end.
-template <int P_, int L, int D>
+// How the edge backward obtains the first Linear's ReLU output h_1: recompute
+// it from the gathered [e | v_s | v_r] rows, read the forward's copy, or
+// recompute it the row-split way from e and the block's node projections
+// (l = 256, bf16).  One instantiation per way keeps the others' registers out.
+enum { BWD_GATHER = 0, BWD_STASH = 1, BWD_RSB = 2 };
+
+template <int P_, int L, int D, int MODE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::value))) void edge_bwd_kernel(EdgeBwdArgs a) {
   using P = typename PrecOf<P_>::type;
   using T = typename P::T;
@@ -1266,7 +1272,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
             da[m][nn][r] = ok ? a.dagg[rv * L + col] : 0.f;
           }
         }
-      if (a.hid_in) {
+      if constexpr (MODE == BWD_STASH) {
         // the forward's first-Linear ReLU output (rows past n zero: they
         // carry dm = 0 and contribute nothing)
         constexpr int E16 = 16 / sizeof(T);
@@ -1278,7 +1284,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
           if (r < n) v = *reinterpret_cast<const uint4*>(hsrc + (int64_t)r * L + c);
           *reinterpret_cast<uint4*>(HB + r * Lay::LDH + c) = v;
         }
-      } else if (sizeof(T) == 2 && L == 256 && a.proj) {
+      } else if constexpr (MODE == BWD_RSB) {
         // recompute the row-split forward's first layer (edge_fwd_rsb_kernel):
         // z_1 = W_e e + P_s[s] + P_r[r] with the block's node projections, the
         // same sums in the same order, so h_1 is bitwise the forward's
@@ -1374,7 +1380,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
         }
       __syncthreads();
       store_rows(reinterpret_cast<T*>(a.delta[D - 1]) + (sb - a.e_base) * L, A, Lay::LDA, n, L);
-      if (!a.hid_in) store_rows(reinterpret_cast<T*>(a.hid[0]) + (sb - a.e_base) * L, HB, Lay::LDH, n, L);
+      if constexpr (MODE != BWD_STASH) store_rows(reinterpret_cast<T*>(a.hid[0]) + (sb - a.e_base) * L, HB, Lay::LDH, n, L);
       if constexpr (D == 3) store_rows(reinterpret_cast<T*>(a.hid[1]) + (sb - a.e_base) * L, HC, Lay::LDH, n, L);
       // hidden layers: dz_{j-1} = (dz_j W_j) * [h_{j-1} > 0], into A column block D-j
 #pragma unroll
@@ -4025,8 +4031,23 @@ template <int P_, int L, int D>
 static hipError_t edge_bwd_t(const EdgeBwdArgs& a, int grid, hipStream_t st) {
   using P = typename PrecOf<P_>::type;
   using Lay = EdgeBwdLds<P, L, D, EdgeTEB<P, L, D>::value>;
-  allow_lds(edge_bwd_kernel<P_, L, D>, Lay::END);
-  hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D>), dim3(grid), dim3(NT), Lay::END, st, a);
+  // the way h_1 is obtained: the forward's copy, the row-split recompute
+  // (l = 256 bf16 with the block's projections), or the gathered rows
+  if (a.hid_in) {
+    allow_lds(edge_bwd_kernel<P_, L, D, BWD_STASH>, Lay::END);
+    hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D, BWD_STASH>), dim3(grid), dim3(NT), Lay::END, st, a);
+  } else if constexpr (P_ == BF16 && L == 256) {
+    if (a.proj) {
+      allow_lds(edge_bwd_kernel<P_, L, D, BWD_RSB>, Lay::END);
+      hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D, BWD_RSB>), dim3(grid), dim3(NT), Lay::END, st, a);
+    } else {
+      allow_lds(edge_bwd_kernel<P_, L, D, BWD_GATHER>, Lay::END);
+      hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D, BWD_GATHER>), dim3(grid), dim3(NT), Lay::END, st, a);
+    }
+  } else {
+    allow_lds(edge_bwd_kernel<P_, L, D, BWD_GATHER>, Lay::END);
+    hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D, BWD_GATHER>), dim3(grid), dim3(NT), Lay::END, st, a);
+  }
   return hipGetLastError();
 }
 
