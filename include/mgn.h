@@ -271,6 +271,38 @@ mgn_status mgn_copy_latents(const mgn_model* owner, const int32_t* send_rows, co
 mgn_status mgn_add_latent_grads(mgn_model* owner, const float* d_halo_k, int64_t n_halo, const int32_t* recv_idx,
                                 const int32_t* send_rows, int64_t n, mgn_stream stream);
 
+/* One exchange list of a lockstep step (device index arrays, n entries, from
+ * mgn_halo_masks): the halo rows recv_idx of part `part` are the node rows
+ * send_rows of part `owner`. */
+typedef struct {
+  int32_t part, owner;
+  const int32_t* recv_idx;
+  const int32_t* send_rows;
+  int64_t n;
+} mgn_halo_link;
+
+/* The staged forward of n_parts parts (one model each, same configuration
+ * and parameters) in Algorithm 1's order: every part's encoders; for each
+ * block, every link's mgn_copy_latents into halo[part] (block k of a
+ * [K][n_halo][latent] buffer), then every part's block; every part's
+ * decoder.  Per part p: graphs[p], node_feat[p], edge_feat[p], halo[p]
+ * (NULL for a part without halo), out[p], workspace[p], ws_bytes[p] as for
+ * mgn_forward.  Links are applied in array order.  Errors as the calls it
+ * makes (on an error the parts' steps are dropped). */
+mgn_status mgn_lockstep_forward(int32_t n_parts, mgn_model* const* models, const mgn_graph* graphs,
+                                const float* const* node_feat, const float* const* edge_feat, float* const* halo,
+                                float* const* out, void* const* workspace, const size_t* ws_bytes,
+                                const mgn_halo_link* links, int32_t n_links, mgn_stream stream);
+/* The staged backward of the same parts: every part's decoder backward;
+ * for k = K-1 .. 0 every part's block backward, then every link's
+ * mgn_add_latent_grads from d_halo[part]; every part's encoder backward.
+ * d_params (device [param_count]) receives the sum of the parts' gradients
+ * in part order (overwritten by the first part unless accumulate != 0);
+ * d_halo[p] [K][n_halo][latent] is part p's halo-gradient buffer. */
+mgn_status mgn_lockstep_backward(int32_t n_parts, mgn_model* const* models, const float* const* d_out,
+                                 float* d_params, int accumulate, float* const* d_halo, const mgn_halo_link* links,
+                                 int32_t n_links, mgn_stream stream);
+
 /* Masked mean squared error (Algorithm 1: local squared error, mean over the
  * loss-masked nodes and outputs) and its gradient, device pointers:
  * out, target [n][d]; mask [n] (NULL = all rows); loss [2]: loss[0] = loss,

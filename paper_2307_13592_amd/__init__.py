@@ -27,8 +27,8 @@ EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mg
            "mgn_workspace_size",
            "mgn_forward", "mgn_backward", "mgn_forward_begin", "mgn_forward_block", "mgn_forward_end",
            "mgn_backward_begin", "mgn_backward_block", "mgn_backward_end", "mgn_halo_masks", "mgn_copy_latents",
-           "mgn_add_latent_grads", "mgn_mse_grad", "mgn_mse_grad_global", "mgn_timing_enable",
-           "mgn_timing_read"]
+           "mgn_add_latent_grads", "mgn_lockstep_forward", "mgn_lockstep_backward", "mgn_mse_grad",
+           "mgn_mse_grad_global", "mgn_timing_enable", "mgn_timing_read"]
 TIMERS = ["encode", "edge_fwd", "node_fwd", "decode", "edge_bwd", "node_bwd", "input_grad", "weight_grad",
           "other", "node_proj", "exchange"]
 
@@ -43,6 +43,11 @@ class MgnError(RuntimeError):
 class mgn_config(C.Structure):
     _fields_ = [("latent", C.c_int32), ("n_blocks", C.c_int32), ("depth", C.c_int32), ("node_in", C.c_int32),
                 ("edge_in", C.c_int32), ("node_out", C.c_int32), ("precision", C.c_int32), ("ln_eps", C.c_float)]
+
+
+class mgn_halo_link(C.Structure):
+    _fields_ = [("part", C.c_int32), ("owner", C.c_int32), ("recv_idx", C.c_void_p), ("send_rows", C.c_void_p),
+                ("n", C.c_int64)]
 
 
 class mgn_graph(C.Structure):
@@ -90,6 +95,8 @@ def lib() -> C.CDLL:
             "mgn_halo_masks": (C.c_int, [vp, i64, i64, vp, i64, vp, i64, i32, vp, vp, vp]),
             "mgn_copy_latents": (C.c_int, [vp, vp, vp, i64, vp, i64, vp]),
             "mgn_add_latent_grads": (C.c_int, [vp, vp, i64, vp, vp, i64, vp]),
+            "mgn_lockstep_forward": (C.c_int, [i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, vp]),
+            "mgn_lockstep_backward": (C.c_int, [i32, vp, vp, vp, C.c_int, vp, vp, i32, vp]),
             "mgn_mse_grad": (C.c_int, [vp, vp, vp, i64, i32, vp, vp, vp]),
             "mgn_mse_grad_global": (C.c_int, [vp, vp, vp, i64, i32, i64, vp, vp, vp]),
             "mgn_timing_enable": (C.c_int, [vp, C.c_int]),
@@ -305,6 +312,36 @@ def mgn_add_latent_grads(owner, d_halo_k, recv_idx, send_rows, stream=None) -> N
     """owner's dL/dv[send_rows[i]] += d_halo_k[recv_idx[i]] (device tensors)."""
     _check(lib().mgn_add_latent_grads(owner, _dev(d_halo_k), int(d_halo_k.shape[0]), _dev(recv_idx),
                                       _dev(send_rows), int(send_rows.numel()), _stream(stream)), owner)
+
+
+def _ptrs(ts):
+    """C array of device pointers (NULL for None)."""
+    return (C.c_void_p * len(ts))(*[None if t is None else t.data_ptr() for t in ts])
+
+
+def mgn_lockstep_forward(models, graphs, node_feats, edge_feats, halos, outs, workspaces, links,
+                         stream=None) -> None:
+    """models, graphs (mgn_graph), device tensors per part; links: list of
+    (part, owner, recv_idx, send_rows) with device int32 index tensors."""
+    P = len(models)
+    ms = (C.c_void_p * P)(*[m.value for m in models])
+    gs = (mgn_graph * P)(*graphs)
+    lk = (mgn_halo_link * max(len(links), 1))(*[mgn_halo_link(p, q, r.data_ptr(), s.data_ptr(), r.numel())
+                                                 for p, q, r, s in links])
+    wb = (C.c_size_t * P)(*[w.numel() * w.element_size() for w in workspaces])
+    st = lib().mgn_lockstep_forward(P, ms, gs, _ptrs(node_feats), _ptrs(edge_feats), _ptrs(halos), _ptrs(outs),
+                                    _ptrs(workspaces), wb, lk, len(links), _stream(stream))
+    _check(st)
+
+
+def mgn_lockstep_backward(models, d_outs, d_params, d_halos, links, accumulate: bool = False, stream=None) -> None:
+    P = len(models)
+    ms = (C.c_void_p * P)(*[m.value for m in models])
+    lk = (mgn_halo_link * max(len(links), 1))(*[mgn_halo_link(p, q, r.data_ptr(), s.data_ptr(), r.numel())
+                                                 for p, q, r, s in links])
+    st = lib().mgn_lockstep_backward(P, ms, _ptrs(d_outs), _dev(d_params), int(bool(accumulate)), _ptrs(d_halos),
+                                     lk, len(links), _stream(stream))
+    _check(st)
 
 
 def mgn_mse_grad(out, target, mask, loss, d_out, stream=None) -> None:

@@ -1288,6 +1288,105 @@ mgn_status mgn_add_latent_grads(mgn_model* owner, const float* d_halo_k, int64_t
 
 }  // extern "C"
 
+// Lockstep step of several parts on one device (one stream): the staged
+// calls in Algorithm 1's order with the halo exchange between the blocks.
+namespace {
+mgn_status check_links(int32_t n_parts, mgn_model* const* models, const mgn_halo_link* links, int32_t n_links,
+                       float* const* bufs, const char* fn) {
+  const std::string f(fn);
+  if (n_parts < 1 || !models || n_links < 0 || (n_links > 0 && !links))
+    return fail(nullptr, MGN_E_ARG, f + ": bad part or link counts");
+  for (int32_t p = 0; p < n_parts; ++p)
+    if (!models[p]) return fail(nullptr, MGN_E_ARG, f + ": model is NULL");
+  for (int32_t i = 0; i < n_links; ++i) {
+    const mgn_halo_link& k = links[i];
+    if (k.part < 0 || k.part >= n_parts || k.owner < 0 || k.owner >= n_parts || k.part == k.owner || k.n < 0)
+      return fail(nullptr, MGN_E_ARG, f + ": link " + std::to_string(i) + " names a bad part");
+    if (models[k.part]->L != models[k.owner]->L || models[k.part]->K != models[k.owner]->K)
+      return fail(nullptr, MGN_E_ARG, f + ": linked parts have different latent sizes or block counts");
+    if (k.n > 0 && (!k.recv_idx || !k.send_rows || !bufs || !bufs[k.part]))
+      return fail(nullptr, MGN_E_ARG, f + ": link " + std::to_string(i) + " without index arrays or buffer");
+  }
+  return MGN_OK;
+}
+}  // namespace
+
+extern "C" {
+
+mgn_status mgn_lockstep_forward(int32_t n_parts, mgn_model* const* models, const mgn_graph* graphs,
+                                const float* const* node_feat, const float* const* edge_feat, float* const* halo,
+                                float* const* out, void* const* workspace, const size_t* ws_bytes,
+                                const mgn_halo_link* links, int32_t n_links, mgn_stream stream) {
+  mgn_status s = check_links(n_parts, models, links, n_links, halo, "mgn_lockstep_forward");
+  if (s) return s;
+  if (!graphs || !node_feat || !edge_feat || !out || !workspace || !ws_bytes)
+    return fail(nullptr, MGN_E_ARG, "mgn_lockstep_forward: NULL array");
+  hipStream_t st = (hipStream_t)stream;
+  for (int32_t p = 0; p < n_parts; ++p) {
+    s = fwd_begin(models[p], &graphs[p], node_feat[p], edge_feat[p], halo ? halo[p] : nullptr, out[p], workspace[p],
+                  ws_bytes[p], st, "mgn_lockstep_forward");
+    if (s) return s;
+  }
+  const int K = models[0]->K;
+  for (int k = 0; k < K; ++k) {
+    for (int32_t i = 0; i < n_links; ++i) {
+      const mgn_halo_link& ln = links[i];
+      if (ln.n == 0) continue;
+      const int64_t nh = graphs[ln.part].n_halo;
+      s = mgn_copy_latents(models[ln.owner], ln.send_rows, ln.recv_idx, ln.n,
+                           halo[ln.part] + (size_t)k * nh * models[ln.part]->L, nh, stream);
+      if (s) return fail(nullptr, s, std::string("mgn_lockstep_forward: ") + mgn_last_error(models[ln.owner]));
+    }
+    for (int32_t p = 0; p < n_parts; ++p) {
+      s = fwd_block(models[p], st, "mgn_lockstep_forward");
+      if (s) return s;
+    }
+  }
+  for (int32_t p = 0; p < n_parts; ++p) {
+    s = fwd_end(models[p], st, "mgn_lockstep_forward");
+    if (s) return s;
+  }
+  return MGN_OK;
+}
+
+mgn_status mgn_lockstep_backward(int32_t n_parts, mgn_model* const* models, const float* const* d_out,
+                                 float* d_params, int accumulate, float* const* d_halo, const mgn_halo_link* links,
+                                 int32_t n_links, mgn_stream stream) {
+  mgn_status s = check_links(n_parts, models, links, n_links, d_halo, "mgn_lockstep_backward");
+  if (s) return s;
+  if (!d_out) return fail(nullptr, MGN_E_ARG, "mgn_lockstep_backward: NULL array");
+  hipStream_t st = (hipStream_t)stream;
+  // one gradient buffer: the first part writes (or adds, accumulate), the others add, in part order
+  for (int32_t p = 0; p < n_parts; ++p) {
+    s = bwd_begin(models[p], d_out[p], d_params, accumulate || p > 0, d_halo ? d_halo[p] : nullptr, st,
+                  "mgn_lockstep_backward");
+    if (s) return s;
+  }
+  const int K = models[0]->K;
+  for (int k = K - 1; k >= 0; --k) {
+    for (int32_t p = 0; p < n_parts; ++p) {
+      s = bwd_block(models[p], st, "mgn_lockstep_backward");
+      if (s) return s;
+    }
+    for (int32_t i = 0; i < n_links; ++i) {
+      const mgn_halo_link& ln = links[i];
+      if (ln.n == 0) continue;
+      mgn_model* mp = models[ln.part];
+      const int64_t nh = mp->g.n_halo;
+      s = mgn_add_latent_grads(models[ln.owner], d_halo[ln.part] + (size_t)k * nh * mp->L, nh, ln.recv_idx,
+                               ln.send_rows, ln.n, stream);
+      if (s) return fail(nullptr, s, std::string("mgn_lockstep_backward: ") + mgn_last_error(models[ln.owner]));
+    }
+  }
+  for (int32_t p = 0; p < n_parts; ++p) {
+    s = bwd_end(models[p], st, "mgn_lockstep_backward");
+    if (s) return s;
+  }
+  return MGN_OK;
+}
+
+}  // extern "C"
+
 extern "C" mgn_status mgn_mse_grad(const float* out, const float* target, const uint8_t* mask, int64_t n, int32_t d,
                                    float* loss, float* d_out, mgn_stream stream) {
   if (n < 0 || d < 1) return fail(nullptr, MGN_E_ARG, "mgn_mse_grad: bad sizes");

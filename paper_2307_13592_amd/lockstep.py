@@ -8,16 +8,15 @@ back to the owners (section "Methodology": forward halo exchange and
 backward gradient exchange).  The parts' parameter gradients add up in one
 buffer in part order, which takes the place of the gradient all-reduce.
 
-Call order and argument marshalling only: every step, the exchanges
-included, runs in libmgn's kernels."""
+Argument marshalling only: the call order lives in libmgn
+(mgn_lockstep_forward / mgn_lockstep_backward), and every step, the
+exchanges included, runs in its kernels."""
 from __future__ import annotations
 
 import numpy as np
 import torch
 
-from . import (mgn_add_latent_grads, mgn_backward_begin, mgn_backward_block, mgn_backward_end, mgn_copy_latents,
-               mgn_forward_begin, mgn_forward_block, mgn_forward_end, mgn_halo_masks, mgn_mse_grad_global,
-               mgn_sgd_step)
+from . import mgn_halo_masks, mgn_lockstep_backward, mgn_lockstep_forward, mgn_mse_grad_global, mgn_sgd_step
 from .runner import Session
 
 
@@ -57,16 +56,12 @@ class Lockstep:
         self.d_params = torch.empty(self.sessions[0].n_params, dtype=torch.float32, device=self.device)
 
     def forward(self, stream=None):
+        """Encoders of every part; per block, the halo copies of every link,
+        then the block on every part; decoders (mgn_lockstep_forward)."""
         S = self.sessions
-        for s in S:
-            mgn_forward_begin(s.model, s.gs, s.node_feat, s.edge_feat, s.halo, s.out, s.workspace, stream)
-        for k in range(self.K):
-            for p, q, recv, send in self.links:
-                mgn_copy_latents(S[q].model, send, recv, S[p].halo[k], stream)
-            for s in S:
-                mgn_forward_block(s.model, stream)
-        for s in S:
-            mgn_forward_end(s.model, stream)
+        mgn_lockstep_forward([s.model for s in S], [s.gs for s in S], [s.node_feat for s in S],
+                             [s.edge_feat for s in S], [s.halo for s in S], [s.out for s in S],
+                             [s.workspace for s in S], self.links, stream)
         return [s.out for s in S]
 
     def mse(self, targets, masks=None, stream=None):
@@ -91,18 +86,13 @@ class Lockstep:
         """d_outs[p]: dL/dout of part p's owned nodes.  Returns the summed
         parameter gradient."""
         S = self.sessions
-        for i, (s, d) in enumerate(zip(S, d_outs)):
+        ds = []
+        for d in d_outs:
             if not isinstance(d, torch.Tensor):
                 d = torch.as_tensor(np.ascontiguousarray(d, np.float32)).to(self.device)
-            s._d_out = d.contiguous()  # kept alive until the backward ends
-            mgn_backward_begin(s.model, s._d_out, self.d_params, i > 0, s.d_halo, stream)
-        for k in reversed(range(self.K)):
-            for s in S:
-                mgn_backward_block(s.model, stream)
-            for p, q, recv, send in self.links:
-                mgn_add_latent_grads(S[q].model, S[p].d_halo[k], recv, send, stream)
-        for s in S:
-            mgn_backward_end(s.model, stream)
+            ds.append(d.contiguous())
+        mgn_lockstep_backward([s.model for s in S], ds, self.d_params, [s.d_halo for s in S], self.links, False,
+                              stream)
         return self.d_params
 
     def sgd(self, lr: float, stream=None):

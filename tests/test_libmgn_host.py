@@ -223,3 +223,30 @@ def test_staged_state_errors_before_any_launch():
         assert L.mgn_forward_block(None, None) == mgn.MGN_E_ARG
     finally:
         mgn.mgn_destroy(h)
+
+
+def test_lockstep_argument_errors():
+    """mgn_lockstep_forward / _backward reject bad part counts and links
+    before anything is launched."""
+    import ctypes as C
+    L = mgn.lib()
+    h0, h1 = mgn.mgn_create(64, 2, 2), mgn.mgn_create(64, 2, 2)
+    h3 = mgn.mgn_create(128, 2, 2)
+    try:
+        ms = (C.c_void_p * 2)(h0.value, h1.value)
+        fake = C.c_void_p(4096)
+        bad = (mgn.mgn_halo_link * 1)(mgn.mgn_halo_link(0, 5, fake, fake, 3))       # owner out of range
+        assert L.mgn_lockstep_backward(2, ms, None, None, 0, None, bad, 1, None) == mgn.MGN_E_ARG
+        self_link = (mgn.mgn_halo_link * 1)(mgn.mgn_halo_link(1, 1, fake, fake, 3))
+        assert L.mgn_lockstep_backward(2, ms, None, None, 0, None, self_link, 1, None) == mgn.MGN_E_ARG
+        assert L.mgn_lockstep_backward(0, ms, None, None, 0, None, None, 0, None) == mgn.MGN_E_ARG
+        mixed = (C.c_void_p * 2)(h0.value, h3.value)                                  # latent 64 vs 128
+        ok = (mgn.mgn_halo_link * 1)(mgn.mgn_halo_link(0, 1, fake, fake, 3))
+        assert L.mgn_lockstep_backward(2, mixed, None, None, 0, None, ok, 1, None) == mgn.MGN_E_ARG
+        assert "latent" in mgn.mgn_last_error(None)
+        # no forward before the backward: each part reports it
+        d = (C.c_void_p * 2)(fake.value, fake.value)
+        assert L.mgn_lockstep_backward(2, ms, d, fake, 0, d, ok, 1, None) == mgn.MGN_E_STATE
+    finally:
+        for h in (h0, h1, h3):
+            mgn.mgn_destroy(h)
