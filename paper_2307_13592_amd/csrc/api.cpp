@@ -1081,7 +1081,7 @@ struct Bwd {
         e = launch_rows_bwd(m->prec, L, D, ENC_NODE, a, BWD_GRID, st);
       }
       CHK("EncNode");
-      e = run_vec(m, ml, d_params, accumulate, st);
+      e = run_vec(m, ml, d_params, accumulate, st, rows_bwd_grid(m->prec, L, D, ENC_NODE, BWD_GRID));
       CHK("EncNode vec");
       DwArgs w{};
       w.delta = DEL_N[0];

@@ -2924,7 +2924,7 @@ __global__ __launch_bounds__((RtRowsLay<L, KIND>::FNTH)) void rows_rt_fwd_kernel
   }
 }
 
-// Backward: ENC_EDGE recomputes its tile's forward from the features;
+// Backward: ENC_NODE / ENC_EDGE recompute their tile's forward from the features;
 // NODE_BLOCK takes the first Linear's ReLU output from the forward
 // (a.hid_in) and ends in the input gradients dv = dm + dz W_1[:, v-block],
 // dagg = dz W_1[:, agg-block].  Outputs as rows_bwd_kernel for these kinds.
@@ -4102,7 +4102,15 @@ static bool rows_rs(int prec, int L, int D, int kind) {
   return prec == BF16 && D == 2 && (L == 64 || L == 128) && (kind == NODE_BLOCK || kind == ENC_EDGE);
 }
 
-int rows_bwd_grid(int prec, int L, int D, int kind, int grid) { return rows_rs(prec, L, D, kind) ? RS_GRID : grid; }
+// Backward kinds on the T-form kernel (NODE_BLOCK only with the forward's
+// ReLU output at hand).
+static bool rows_rt_bwd(int prec, int L, int D, int kind, bool hid_in) {
+  return rows_rt(prec, L, D, kind) && (kind == ENC_EDGE || kind == ENC_NODE || (kind == NODE_BLOCK && hid_in));
+}
+
+int rows_bwd_grid(int prec, int L, int D, int kind, int grid) {
+  return rows_rs(prec, L, D, kind) || rows_rt_bwd(prec, L, D, kind, false) ? RS_GRID : grid;
+}
 
 template <int L, int KIND>
 static hipError_t rows_bwd_rs_t(const RowsBwdArgs& a, hipStream_t st) {
@@ -4113,8 +4121,12 @@ static hipError_t rows_bwd_rs_t(const RowsBwdArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st) {
-  if (rows_rt(prec, L, D, kind) && (kind == ENC_EDGE || (kind == NODE_BLOCK && a.hid_in))) {
-    if (L == 64) return kind == ENC_EDGE ? rows_rt_bwd_t<64, ENC_EDGE>(a, st) : rows_rt_bwd_t<64, NODE_BLOCK>(a, st);
+  if (rows_rt_bwd(prec, L, D, kind, a.hid_in != nullptr)) {
+    if (L == 64) {
+      if (kind == ENC_NODE) return rows_rt_bwd_t<64, ENC_NODE>(a, st);
+      return kind == ENC_EDGE ? rows_rt_bwd_t<64, ENC_EDGE>(a, st) : rows_rt_bwd_t<64, NODE_BLOCK>(a, st);
+    }
+    if (kind == ENC_NODE) return rows_rt_bwd_t<128, ENC_NODE>(a, st);
     return kind == ENC_EDGE ? rows_rt_bwd_t<128, ENC_EDGE>(a, st) : rows_rt_bwd_t<128, NODE_BLOCK>(a, st);
   }
   if (rows_rs(prec, L, D, kind)) {
