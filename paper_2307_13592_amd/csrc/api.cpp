@@ -1105,6 +1105,10 @@ struct Bwd {
         a.in0 = m->ef + (size_t)e0 * m->cfg.edge_in;
         a.fin = m->cfg.edge_in;
         a.dm = DE + (size_t)e0 * L;  // dL/de^0 (block 0 wrote it in plain column order)
+        // narrow features: the kernel forms the first Linear's weight
+        // gradient itself (per-wave partials) instead of storing dz_0
+        const int w1s = rows > 0 ? rows_rt_w1_parts(m->prec, L, D, ENC_EDGE, a.fin) : 0;
+        if (w1s) a.w1_part = (float*)(ws + p.PART);
         {
           Timed t_(m, MGN_T_NODE_BWD, st);
           e = launch_rows_bwd(m->prec, L, D, ENC_EDGE, a, BWD_GRID, st);
@@ -1112,14 +1116,19 @@ struct Bwd {
         CHK("EncEdge");
         e = run_vec(m, ml, d_params, acc, st, rows_bwd_grid(m->prec, L, D, ENC_EDGE, BWD_GRID));
         CHK("EncEdge vec");
-        DwArgs w{};
-        w.delta = DEL_E[0];
-        w.ldd = L;
-        w.a_kind = 1;
-        w.a0 = a.in0;
-        w.lda0 = m->cfg.edge_in;
-        w.R = rows;
-        e = run_dw(m, ml.lin[0], w, d_params, acc, st);
+        if (w1s) {
+          Timed t_(m, MGN_T_WEIGHT_GRAD, st);
+          e = launch_dw_reduce(a.w1_part, w1s, L, a.fin, d_params + ml.lin[0].w, a.fin, acc, st);
+        } else {
+          DwArgs w{};
+          w.delta = DEL_E[0];
+          w.ldd = L;
+          w.a_kind = 1;
+          w.a0 = a.in0;
+          w.lda0 = m->cfg.edge_in;
+          w.R = rows;
+          e = run_dw(m, ml.lin[0], w, d_params, acc, st);
+        }
         CHK("EncEdge dW");
         e = dw_hidden(ml, rows, DEL_E, HID_E, L, acc);
         CHK("EncEdge dW");

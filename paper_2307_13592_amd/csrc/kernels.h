@@ -62,6 +62,8 @@ struct RowsBwdArgs {
   float* vpart;      // [grid][nvec] per-workgroup bias / LayerNorm gradients
   int nvec;
   float eps;
+  float* w1_part;    // ENC_EDGE, T-form kernel: when set, per-wave partials [waves][L][fin] of the
+                     // first Linear's weight gradient instead of storing delta[0] (rows_rt_w1_parts)
 };
 
 struct EdgeBwdArgs {
@@ -164,6 +166,10 @@ hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int gri
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st);
 // Workgroups (= vector-partial slots) launch_rows_bwd uses when asked for `grid`.
 int rows_bwd_grid(int prec, int L, int D, int kind, int grid);
+// Number of per-wave partials (RowsBwdArgs::w1_part) with which the backward
+// of `kind` forms its first Linear's weight gradient itself, or 0 if it
+// stores delta[0] for a separate weight-gradient GEMM instead.
+int rows_rt_w1_parts(int prec, int L, int D, int kind, int fin);
 hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int grid, hipStream_t st);
 // Workgroups (= vector-partial slots) the edge backward uses when asked for `grid`.
 int edge_bwd_grid(int prec, int L, int D, int grid);

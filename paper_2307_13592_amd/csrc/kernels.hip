@@ -2776,7 +2776,13 @@ struct RtRowsLay {
   // waves per workgroup: forward 16 (at most 128 registers), backward 12 (168)
   static constexpr int FNWV = 16, FNTH = 64 * FNWV, NWV = 12, NTH = 64 * NWV;
   static constexpr int NVEC = 4 * L;                     // bias / LayerNorm partials per wave
-  static_assert(F_END <= 160 * 1024 && B_END <= 160 * 1024, "LDS");
+  // ENC_EDGE with the fused first-Linear weight gradient: per-wave scratch
+  // for a tile's dz_0 (16 rows of L bf16, 8 columns of padding) and features
+  // (16 rows of W1_FIN bf16)
+  static constexpr int W1_FIN = 4, DZS = L + 8;
+  static constexpr int B_SCR = B_END, SCR = 16 * DZS * 2 + 16 * W1_FIN * 2;
+  static constexpr int B_END_W1 = KIND == ENC_EDGE ? B_SCR + NWV * SCR : B_END;
+  static_assert(F_END <= 160 * 1024 && B_END <= 160 * 1024 && B_END_W1 <= 160 * 1024, "LDS");
   static_assert(NWV * NVEC * 4 <= B_VEC, "partials reuse the weight area");
 };
 
@@ -2961,6 +2967,17 @@ __global__ __launch_bounds__((RtRowsLay<L, KIND>::NTH)) void rows_rt_bwd_kernel(
 #pragma unroll
     for (int t = 0; t < NR; ++t) qacc[k][t] += f[t];
   };
+  // fused first-Linear weight gradient (ENC_EDGE, fin <= W1_FIN): lane l
+  // accumulates dW_1 rows OPL l .. OPL l + OPL - 1, columns 0 .. W1_FIN - 1
+  constexpr int OPL = L / 64;
+  const bool fuse_w1 = KIND == ENC_EDGE && a.w1_part != nullptr;
+  uint16_t* dz = reinterpret_cast<uint16_t*>(lds + Lay::B_SCR + wave * Lay::SCR);
+  uint16_t* xs = dz + 16 * Lay::DZS;
+  float w1acc[OPL][4];
+#pragma unroll
+  for (int j = 0; j < OPL; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w1acc[j][i] = 0.f;
   const int64_t ntiles = (a.rows + 15) / 16;
   for (int64_t t = (int64_t)blockIdx.x * Lay::NWV + wave; t < ntiles; t += (int64_t)gridDim.x * Lay::NWV) {
     int ln = lane;
@@ -2988,6 +3005,9 @@ __global__ __launch_bounds__((RtRowsLay<L, KIND>::NTH)) void rows_rt_bwd_kernel(
     } else {
       uint4 xf[NK1];
       rt_rows_input<L, KIND>(a.in0, a.in1, nullptr, a.fin, src, q, xf);
+      // the tile's bf16 features (columns >= fin are zero) for the fused
+      // weight gradient; rows past the end get dz_0 = 0 below
+      if (fuse_w1 && q == 0) *reinterpret_cast<uint2*>(xs + e * Lay::W1_FIN) = make_uint2(xf[0].x, xf[0].y);
       floatx4 z[NB];
       rt_gemm<NB, NK1>(W1, xf, z, ln);
       float h[NB][4];
@@ -3076,7 +3096,36 @@ __global__ __launch_bounds__((RtRowsLay<L, KIND>::NTH)) void rows_rt_bwd_kernel(
         for (int r = 0; r < 4; ++r) v[cb][r] = ((mask >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
     }
     rt_frags<NB>(v, gf);
-    rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[0]) + row * L, q, gf, ok);
+    if (fuse_w1) {
+      // dW_1 += dz_0^T x over the tile's 16 rows: dz_0 (bf16, as a stored
+      // delta would hold it) through the wave's scratch, then lane l forms
+      // output rows OPL l .. OPL l + OPL - 1, ascending row order
+      {
+        uint16_t* dr = dz + e * Lay::DZS + q * 8;
+#pragma unroll
+        for (int kg = 0; kg < NKH; ++kg) *reinterpret_cast<uint4*>(dr + kg * 32) = rt_to_plain(gf[kg]);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const uint2 xv = *reinterpret_cast<const uint2*>(xs + r * Lay::W1_FIN);
+        const float x4[4] = {__uint_as_float(xv.x << 16), __uint_as_float(xv.x & 0xffff0000u),
+                             __uint_as_float(xv.y << 16), __uint_as_float(xv.y & 0xffff0000u)};
+        float d[OPL];
+        if constexpr (OPL == 2) {
+          const uint32_t w = *reinterpret_cast<const uint32_t*>(dz + r * Lay::DZS + 2 * lane);
+          d[0] = __uint_as_float(w << 16);
+          d[1] = __uint_as_float(w & 0xffff0000u);
+        } else {
+          d[0] = __uint_as_float((uint32_t)dz[r * Lay::DZS + lane] << 16);
+        }
+#pragma unroll
+        for (int j = 0; j < OPL; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) w1acc[j][i] = fmaf(d[j], x4[i], w1acc[j][i]);
+      }
+    } else {
+      rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[0]) + row * L, q, gf, ok);
+    }
     coltot(v, 0, e);  // hidden bias
     if constexpr (KIND == NODE_BLOCK) {
 #pragma unroll
@@ -3122,6 +3171,14 @@ __global__ __launch_bounds__((RtRowsLay<L, KIND>::NTH)) void rows_rt_bwd_kernel(
     float s = 0.f;
     for (int w = 0; w < Lay::NWV; ++w) s += red[w * Lay::NVEC + i];
     vp[i] = s;
+  }
+  if (fuse_w1) {
+    float* wp = a.w1_part + ((int64_t)blockIdx.x * Lay::NWV + wave) * L * a.fin;
+#pragma unroll
+    for (int j = 0; j < OPL; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (i < a.fin) wp[(OPL * lane + j) * a.fin + i] = w1acc[j][i];
   }
 }
 
@@ -4067,9 +4124,21 @@ static hipError_t rows_rt_fwd_t(const RowsFwdArgs& a, hipStream_t st) {
 template <int L, int KIND>
 static hipError_t rows_rt_bwd_t(const RowsBwdArgs& a, hipStream_t st) {
   using Lay = RtRowsLay<L, KIND>;
-  allow_lds(rows_rt_bwd_kernel<L, KIND>, Lay::B_END);
-  hipLaunchKernelGGL((rows_rt_bwd_kernel<L, KIND>), dim3(RS_GRID), dim3(Lay::NTH), Lay::B_END, st, a);
+  if (a.w1_part && (KIND != ENC_EDGE || a.fin > Lay::W1_FIN || a.fin < 1)) return hipErrorInvalidValue;
+  const int lds = a.w1_part ? Lay::B_END_W1 : Lay::B_END;
+  allow_lds(rows_rt_bwd_kernel<L, KIND>, Lay::B_END_W1);
+  hipLaunchKernelGGL((rows_rt_bwd_kernel<L, KIND>), dim3(RS_GRID), dim3(Lay::NTH), lds, st, a);
   return hipGetLastError();
+}
+
+// the partials fit the weight-gradient partial buffer, which holds at least
+// the register-resident kernel's DWS_WAVES x 16384 floats
+static_assert((int64_t)RS_GRID * RtRowsLay<128, ENC_EDGE>::NWV * 128 * RtRowsLay<128, ENC_EDGE>::W1_FIN <=
+                  (int64_t)DWS_WAVES * 16384,
+              "w1 partials");
+int rows_rt_w1_parts(int prec, int L, int D, int kind, int fin) {
+  if (!rows_rt(prec, L, D, kind) || kind != ENC_EDGE || fin < 1 || fin > RtRowsLay<128, ENC_EDGE>::W1_FIN) return 0;
+  return RS_GRID * RtRowsLay<128, ENC_EDGE>::NWV;
 }
 
 hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st) {
