@@ -30,14 +30,17 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic(timer: str, cfg, E: int, No: int, Nh: int, lean: bool = False):
+def algorithmic(timer: str, cfg, E: int, No: int, Nh: int, lean: bool = False, stash: float = 0.0):
     """Compulsory work of one launch of the kernel class `timer` for one
     block, as (HBM bytes, flops), for the bf16 row-split path the benchmark
     workload takes (latent 64/128, depth 2): each operand row counted once,
     gathered node rows once per node; flops are the MLP products (2 per
     multiply-add).  E edges, No owned and Nh halo nodes; lean: the
     checkpointed plan (the streaming edge backward then recomputes the first
-    Linear instead of reading the forward's ReLU output)."""
+    Linear instead of reading the forward's ReLU output); stash: the share of
+    blocks whose row-split forward keeps h_1 for the backward (which then
+    reads it in place of e^k and skips the projections, W_e e and the h_1
+    write), averaged over the blocks' launches."""
     l, D = cfg.latent, cfg.depth
     Nl = No + Nh
     if cfg.precision != "bf16" or D != 2 or l not in (64, 128):
@@ -68,12 +71,14 @@ def algorithmic(timer: str, cfg, E: int, No: int, Nh: int, lean: bool = False):
     if timer == "edge_bwd":
         # read e^k (bf16), de^{k+1} (fp32), receiver / sender ids, dagg rows,
         # node projections; write de^k, dy, dz_0, h_1 (bf16) and the
-        # receiver sums of dz_0
+        # receiver sums of dz_0; with the stash: read h_1 instead of e^k,
+        # no projections, no h_1 write, no W_e e
         by = E * (2 * l + 4 * l + 8 + 4 * l + 3 * 2 * l) + No * l * 4 * 2 + Nl * 2 * l * 4
-        return by, E * 4 * 2 * l * l
+        by -= stash * (E * 2 * l + Nl * 2 * l * 4)
+        return by, E * (4 - stash) * 2 * l * l
     if timer == "edge_fwd":
-        # read e^k, ids, projections; write e^{k+1} and agg
-        by = E * (2 * l + 8 + 2 * l) + Nl * 2 * l * 4 + No * l * 4
+        # read e^k, ids, projections; write e^{k+1} and agg (and h_1 with the stash)
+        by = E * (2 * l + 8 + 2 * l) + Nl * 2 * l * 4 + No * l * 4 + stash * E * 2 * l
         return by, E * 2 * 2 * l * l
     if timer == "node_proj":
         return Nl * (2 * l + 2 * l * 4), Nl * 2 * l * 2 * l
@@ -109,6 +114,9 @@ def main():
     ap.add_argument("--peaks", action="store_true",
                     help="measure what plain streaming kernels and library GEMMs reach on this GPU (the practical "
                          "ceilings beside the spec peaks) and exit")
+    ap.add_argument("--h1-stash", type=int, default=-1,
+                    help="row-split path: blocks whose first-Linear ReLU output the forward keeps for the "
+                         "backward (-1, the default: as many as the GPU's free memory holds)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB once (a plain copy kernel of known size, "
@@ -141,10 +149,14 @@ def main():
     no, nh, ne = g["n_owned"], g["n_halo"], g["n_edges"]
     log(f"[bench] {cfg.name}: {cfg.note}; owned {no}, halo {nh}, edges {ne}; inputs {time.time() - t0:.1f}s")
     recompute = args.recompute if args.recompute is not None else (5 if cfg.name == "C5" else 0)
+    rs = cfg.precision == "bf16" and (cfg.latent == 64 or (cfg.latent == 128 and cfg.depth == 2))
+    h1 = args.h1_stash if (rs and recompute == 0) else 0
     sess = Session(cfg.latent, cfg.K, cfg.depth, cfg.precision, g, loc["node_feat"], loc["edge_feat"],
-                   loc["halo"], case.params, recompute=recompute)
+                   loc["halo"], case.params, recompute=recompute, h1_stash=h1)
+    stash = min(sess.h1_stash, cfg.K) / cfg.K if (rs and recompute == 0 and cfg.K) else 0.0
     target = torch.as_tensor(loc["target"]).cuda()
-    log(f"[bench] workspace {sess.ws_bytes / 2**30:.1f} GiB")
+    log(f"[bench] workspace {sess.ws_bytes / 2**30:.1f} GiB"
+        + (f" (first-Linear stash for {round(stash * cfg.K)} of {cfg.K} blocks)" if stash else ""))
 
     def step():
         sess.forward()
@@ -178,7 +190,7 @@ def main():
     # dominant kernel and its roofline position
     dom = max((k for k in timers if timers[k][1]), key=lambda k: timers[k][0])
     t_launch = timers[dom][0] / timers[dom][1] * 1e-3
-    alg = algorithmic(dom, cfg, ne, no, nh, lean=recompute > 0)
+    alg = algorithmic(dom, cfg, ne, no, nh, lean=recompute > 0, stash=stash)
     roof = None
     if alg is not None:
         # a block's edge backward may run as several receiver chunks
@@ -216,6 +228,7 @@ def main():
         "config": {"workload": f"{cfg.name}: {cfg.note}", "owned_nodes": no, "halo_nodes": nh, "edges": ne,
                    "latent": cfg.latent, "blocks": cfg.K, "mlp_depth": cfg.depth, "parallelism": "none"},
         "nodes_per_sec": no * cfg.K / (ms * 1e-3),
+        "plan": {"checkpoint_interval": recompute, "h1_stash_blocks": round(stash * cfg.K)},
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},

@@ -161,6 +161,21 @@ mgn_status mgn_graph_validate(mgn_model* m, const mgn_graph* g, mgn_stream strea
  * MGN_E_UNSUPPORTED for fp32 models, MGN_E_ARG for negative arguments. */
 mgn_status mgn_set_recompute(mgn_model* m, int32_t interval, int64_t chunk_edges);
 
+/* First-Linear stash of the row-split edge kernels (bf16, latent 64, or
+ * latent 128 at MLP depth 2; section "Model", the edge MLP of each block).
+ * Without checkpointing, the backward pass recomputes each block's
+ * first-Linear ReLU output h_1 from e^k and the kept node projections, and
+ * writes it for the layer-2 weight gradient.  n_blocks > 0 makes the forward
+ * keep h_1 of the last min(n_blocks, K) blocks (E x latent bf16 each, in the
+ * workspace); their backward reads it instead of e^k and the projections
+ * and writes nothing in its place.  Identical results (h_1 is the same
+ * bf16 value either way); less traffic for more workspace.  Ignored by
+ * other kernels (the streaming kernels keep every block's h_1 anyway),
+ * with checkpointing and in inference.  Takes effect for the next
+ * mgn_workspace_size / mgn_forward (a pending step is dropped).
+ * MGN_E_ARG for a negative count. */
+mgn_status mgn_set_h1_stash(mgn_model* m, int32_t n_blocks);
+
 /* Forward-only plan (inference on a whole mesh, the paper's section
  * "Results": a single GPU holds a complete stator domain for inference).
  * on != 0: the workspace holds one working copy of each stream (node

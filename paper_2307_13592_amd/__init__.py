@@ -23,7 +23,7 @@ STATUS_NAMES = ["MGN_OK", "MGN_E_ARG", "MGN_E_GRAPH", "MGN_E_STATE", "MGN_E_NOME
 EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mgn_set_params", "mgn_sgd_step",
            "mgn_get_params",
            "mgn_partition_slabs", "mgn_graph_sizes", "mgn_graph_build", "mgn_graph_validate", "mgn_set_recompute",
-           "mgn_set_inference", "mgn_rollout_update",
+           "mgn_set_inference", "mgn_set_h1_stash", "mgn_rollout_update",
            "mgn_workspace_size",
            "mgn_forward", "mgn_backward", "mgn_forward_begin", "mgn_forward_block", "mgn_forward_end",
            "mgn_backward_begin", "mgn_backward_block", "mgn_backward_end", "mgn_halo_masks", "mgn_copy_latents",
@@ -82,6 +82,7 @@ def lib() -> C.CDLL:
             "mgn_graph_validate": (C.c_int, [vp, vp, vp]),
             "mgn_set_recompute": (C.c_int, [vp, i32, i64]),
             "mgn_set_inference": (C.c_int, [vp, i32]),
+            "mgn_set_h1_stash": (C.c_int, [vp, i32]),
             "mgn_rollout_update": (C.c_int, [vp, i64, i32, vp, i32, i32, vp]),
             "mgn_workspace_size": (C.c_int, [vp, vp, vp]),
             "mgn_forward": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]),
@@ -234,6 +235,10 @@ def mgn_set_recompute(model, interval: int, chunk_edges: int = 0) -> None:
 
 def mgn_set_inference(model, on: bool = True) -> None:
     _check(lib().mgn_set_inference(model, int(bool(on))), model)
+
+
+def mgn_set_h1_stash(model, n_blocks: int) -> None:
+    _check(lib().mgn_set_h1_stash(model, int(n_blocks)), model)
 
 
 def mgn_rollout_update(out, node_feat, col0: int = 3, stream=None) -> None:

@@ -47,6 +47,8 @@ struct WsPlan {
   bool infer = false;
   // node projections kept per block (row-split kernels, every block kept)
   bool proj_all = false;
+  // blocks k >= h1_first keep their first-Linear ReLU output (HID_E1 slot k - h1_first)
+  int h1_first = 0;
   // receiver / edge boundaries of the backward's edge chunks
   std::vector<int64_t> cr, ce;
 };
@@ -70,6 +72,7 @@ struct mgn_model {
   mgn_graph vg{};
   std::vector<int32_t> rp_host;
   int ckpt = 0;                 // edge-stream checkpoint interval (0: keep every block)
+  int h1_stash = 0;             // row-split kernels: blocks whose first-Linear ReLU output the forward keeps
   bool infer = false;           // forward-only plan (mgn_set_inference)
   int64_t chunk_edges = 0;      // edges per backward chunk with checkpointing (0: the default)
   // what the last forward used (kept for the backward)
@@ -263,7 +266,14 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   // streaming edge kernels, every block kept: each block's first-Linear ReLU
   // output, written by the forward, so the backward skips recomputing the
   // first Linear (half its products) and the row gather
-  p.HID_E1 = (!p.infer && !p.lean && K > 0 && !edge_rs(m->prec, m->L, m->D)) ? take(ts * (size_t)K * ne * L) : 0;
+  // (row-split kernels: for the last h1_stash blocks only, as memory allows;
+  // the others recompute it from e and the kept projections)
+  {
+    int64_t nh1 = 0;
+    if (!p.infer && !p.lean && K > 0) nh1 = edge_rs(m->prec, m->L, m->D) ? std::min<int64_t>(m->h1_stash, K) : K;
+    p.h1_first = (int)(K - nh1);
+    p.HID_E1 = nh1 > 0 ? take(ts * (size_t)nh1 * ne * L) : 0;
+  }
   if (p.infer) {
     p.total = o;
     return p;
@@ -477,6 +487,16 @@ mgn_status mgn_set_recompute(mgn_model* m, int32_t interval, int64_t chunk_edges
   return MGN_OK;
 }
 
+mgn_status mgn_set_h1_stash(mgn_model* m, int32_t n_blocks) {
+  if (!m) return fail(nullptr, MGN_E_ARG, "mgn_set_h1_stash: model is NULL");
+  if (n_blocks < 0) return fail(m, MGN_E_ARG, "mgn_set_h1_stash: negative block count");
+  m->h1_stash = n_blocks;
+  m->fwd_done = false;  // the workspace plan changes: a step in progress is dropped
+  m->fwd_next = -1;
+  m->bwd_active = false;
+  return MGN_OK;
+}
+
 mgn_status mgn_set_inference(mgn_model* m, int32_t on) {
   if (!m) return fail(nullptr, MGN_E_ARG, "mgn_set_inference: model is NULL");
   m->infer = on != 0;
@@ -512,14 +532,20 @@ mgn_status mgn_workspace_size(const mgn_model* cm, const mgn_graph* g, size_t* b
 
 namespace {
 
-// The edge half of block k forward: node projections (row-split path), then
-// the fused edge kernel: e^{k+1} = e^k + m into eout (may equal ein, or be
-// null), ordered receiver sums into agg.
+// Block k's first-Linear ReLU output slot (`bytes` per block), or null when
+// the plan keeps none for it.
+void* h1_slot(const WsPlan& p, char* ws, int k, size_t bytes) {
+  return p.HID_E1 && k >= p.h1_first ? (void*)(ws + p.HID_E1 + bytes * (size_t)(k - p.h1_first)) : nullptr;
+}
+
 // Node projections of block k (one shared slot when checkpointing).
 float* proj_block(const WsPlan& p, char* ws, int k, int64_t nl, int L) {
   return (float*)(ws + p.PROJ) + (p.proj_all ? (size_t)k * nl * 2 * L : 0);
 }
 
+// The edge half of block k forward: node projections (row-split path), then
+// the fused edge kernel: e^{k+1} = e^k + m into eout (may equal ein, or be
+// null), ordered receiver sums into agg.
 hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p, char* ws, const float* halo, int k,
                               float* v, void* v16, const void* ein, void* eout, float* agg, hipStream_t st) {
   const int64_t no = g.n_owned, nh = g.n_halo;
@@ -540,7 +566,7 @@ hipError_t edge_forward_block(mgn_model* m, const mgn_graph& g, const WsPlan& p,
   ea.Eout = eout;
   ea.agg = agg;
   ea.eps = m->cfg.ln_eps;
-  ea.hid_out = p.HID_E1 ? (void*)(ws + p.HID_E1 + tsize(m) * (size_t)k * g.n_edges * L) : nullptr;
+  ea.hid_out = h1_slot(p, ws, k, tsize(m) * (size_t)g.n_edges * L);
   const bool rs = edge_rs(m->prec, L, D) || edge_rsb(m->prec, L, D);
   float* proj = rs ? proj_block(p, ws, k, no + nh, L) : nullptr;
   ea.proj = proj;
@@ -983,7 +1009,7 @@ struct Bwd {
       // the forward's first-Linear ReLU output of this block (stash-all
       // streaming path): not recomputed, and the layer-2 weight gradient
       // reads it in place
-      void* h1 = p.HID_E1 ? (void*)(ws + p.HID_E1 + ts * (size_t)k * ne * L) : nullptr;
+      void* h1 = h1_slot(p, ws, k, ts * (size_t)ne * L);
       a.hid_in = h1;
       for (int j = 0; j < 3; ++j) a.delta[j] = DEL_E[j];
       for (int j = 0; j < 2; ++j) a.hid[j] = HID_E[j];

@@ -41,7 +41,7 @@ struct EdgeFwdArgs {
   void* Eout;       // edge latents out, or null (last block)
   float* agg;       // [n_owned][L]
   const float* proj;  // node projections [n_local][2L] (row-split kernels), else unused
-  void* hid_out;      // streaming kernels: the first Linear's ReLU output [E][L] (storage type) kept for the
+  void* hid_out;      // streaming and row-split kernels: the first Linear's ReLU output [E][L] (storage type) kept for the
                       // backward, or null
   float eps;
 };
@@ -82,7 +82,7 @@ struct EdgeBwdArgs {
   float* dagg;          // [n_owned][L]: dL/dagg in; each receiver's sum of dz_0 out
   float* de_out;        // dL/de^k [E][L]
   const float* proj;    // node projections [n_local][2L] (row-split kernels), else unused
-  const void* hid_in;   // streaming kernels: the forward's first-Linear ReLU output [E][L] (then layer 1 is not
+  const void* hid_in;   // streaming and row-split kernels: the forward's first-Linear ReLU output [E][L] (then layer 1 is not
                         // recomputed and hid[0] is not written), or null
   int64_t r_lo, r_hi;   // receiver range of this launch (a multiple of the planning chunk apart)
   int64_t e_base;       // first edge of the range: delta / hid rows are stored from it

@@ -1823,6 +1823,25 @@ __device__ __forceinline__ uint4 rt_from_plain(const uint4 p) {
 
 // The values of rt_frags -> one plain-order bf16 row, 16 bytes per lane and
 // k-group.  All lanes take part in the swaps; only lanes with ok store.
+// A stored bf16 ReLU output row (plain order; lane (e, q) reads its row's
+// k-slots kg * 32 + 8 q ..) as T-order fragments, and the ReLU mask its
+// signs give: bit cb * 4 + r is set where the value is positive.
+template <int NKH>
+__device__ __forceinline__ void rt_load_relu(const uint16_t* __restrict__ hp, int q, uint4 (&hf)[NKH],
+                                             uint32_t& mask) {
+#pragma unroll
+  for (int kg = 0; kg < NKH; ++kg) {
+    hf[kg] = rt_from_plain(*reinterpret_cast<const uint4*>(hp + kg * 32 + q * 8));
+    const uint32_t w[4] = {hf[kg].x, hf[kg].y, hf[kg].z, hf[kg].w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {  // dword i: block 2 kg + i / 2, rows r = 2 (i % 2) .. + 1
+      const int cb = 2 * kg + i / 2, r = 2 * (i % 2);
+      mask |= ((w[i] & 0x7fffu) != 0u && !(w[i] & 0x8000u) ? 1u : 0u) << (cb * 4 + r);
+      mask |= (((w[i] >> 16) & 0x7fffu) != 0u && !(w[i] & 0x80000000u) ? 1u : 0u) << (cb * 4 + r + 1);
+    }
+  }
+}
+
 template <int NKH>
 __device__ __forceinline__ void rt_store_frags(uint16_t* __restrict__ row, int q, const uint4 (&f)[NKH], bool ok) {
   uint4 p[NKH];
@@ -2040,6 +2059,7 @@ __global__ __launch_bounds__((RsFwdLay<L, D>::NTH)) void edge_fwd_rs_kernel(Edge
       for (int r = 0; r < 4; ++r) h[cb][r] = z[cb][r] > 0.f ? z[cb][r] : 0.f;
     uint4 hf[NKH];
     rt_frags<NB>(h, hf);
+    if (a.hid_out) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid_out) + (sb + e) * L, q, hf, ok);
     if constexpr (D == 3) {
       floatx4 acc[NB];
       rt_gemm<NB, NKH>(WH, hf, acc, ln);
@@ -2153,7 +2173,9 @@ struct RsBwdLay {
 // Backward of one block's edge half (T form) with the tile's forward
 // recomputed: dz_0 receiver sums over the consumed dagg rows, de^k, the
 // stored gradients and activations, per-workgroup bias / LayerNorm partials.
-template <int L, int D>
+// STASH: h_1 comes from the forward (a.hid_in, bf16, the block's edges in
+// order) instead of W_e e + P_s + P_r, and is not stored again.
+template <int L, int D, bool STASH>
 __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
   using Lay = RsBwdLay<L, D>;
   constexpr int NKH = Lay::NKH, NB = Lay::NB, W = Lay::W;
@@ -2208,24 +2230,28 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
     const int64_t srow = (sb - a.e_base + e) * L;  // row of the stored gradients / activations
     // rows past the tile's end repeat row 0 (dm = 0 there, so they add nothing)
     const int64_t er = sb + (ok ? e : 0);
-    uint4 ef[NKH];
-#pragma unroll
-    for (int kg = 0; kg < NKH; ++kg) ef[kg] = *reinterpret_cast<const uint4*>(Ein + er * L + kg * 32 + q * 8);
-    floatx4 z[NB];
-    rt_first_layer<L>(ef, W1f, mt, ok, a.proj, z, ln);
     uint32_t mask[2] = {0u, 0u};  // ReLU derivative of the hidden layers, bit cb * 4 + r
     float h[NB][4];
-#pragma unroll
-    for (int cb = 0; cb < NB; ++cb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool on = z[cb][r] > 0.f;
-        mask[0] |= (on ? 1u : 0u) << (cb * 4 + r);
-        h[cb][r] = on ? z[cb][r] : 0.f;
-      }
     uint4 hf[NKH];
-    rt_frags<NB>(h, hf);
-    rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[0]) + srow, q, hf, ok);
+    if constexpr (STASH) {
+      rt_load_relu<NKH>(reinterpret_cast<const uint16_t*>(a.hid_in) + er * L, q, hf, mask[0]);
+    } else {
+      uint4 ef[NKH];
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) ef[kg] = *reinterpret_cast<const uint4*>(Ein + er * L + kg * 32 + q * 8);
+      floatx4 z[NB];
+      rt_first_layer<L>(ef, W1f, mt, ok, a.proj, z, ln);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool on = z[cb][r] > 0.f;
+          mask[0] |= (on ? 1u : 0u) << (cb * 4 + r);
+          h[cb][r] = on ? z[cb][r] : 0.f;
+        }
+      rt_frags<NB>(h, hf);
+      rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[0]) + srow, q, hf, ok);
+    }
     if constexpr (D == 3) {
       floatx4 acc[NB];
       rt_gemm<NB, NKH>(WHf, hf, acc, ln);
@@ -2990,18 +3016,7 @@ __global__ __launch_bounds__((RtRowsLay<L, KIND>::NTH)) void rows_rt_bwd_kernel(
     uint4 hf[NKH];
     if constexpr (KIND == NODE_BLOCK) {
       // h_1 of the forward (plain order) -> T order; its sign is the ReLU mask
-      const uint16_t* hp = reinterpret_cast<const uint16_t*>(a.hid_in) + src * L;
-#pragma unroll
-      for (int kg = 0; kg < NKH; ++kg) {
-        hf[kg] = rt_from_plain(*reinterpret_cast<const uint4*>(hp + kg * 32 + q * 8));
-        const uint32_t w[4] = {hf[kg].x, hf[kg].y, hf[kg].z, hf[kg].w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {  // dword i: block 2 kg + i / 2, rows r = 2 (i % 2) .. + 1
-          const int cb = 2 * kg + i / 2, r = 2 * (i % 2);
-          mask |= ((w[i] & 0x7fffu) != 0u && !(w[i] & 0x8000u) ? 1u : 0u) << (cb * 4 + r);
-          mask |= (((w[i] >> 16) & 0x7fffu) != 0u && !(w[i] & 0x80000000u) ? 1u : 0u) << (cb * 4 + r + 1);
-        }
-      }
+      rt_load_relu<NKH>(reinterpret_cast<const uint16_t*>(a.hid_in) + src * L, q, hf, mask);
     } else {
       uint4 xf[NK1];
       rt_rows_input<L, KIND>(a.in0, a.in1, nullptr, a.fin, src, q, xf);
@@ -4230,8 +4245,13 @@ static hipError_t edge_fwd_rs_t(const EdgeFwdArgs& a, hipStream_t st) {
 template <int L, int D>
 static hipError_t edge_bwd_rs_t(const EdgeBwdArgs& a, hipStream_t st) {
   using Lay = RsBwdLay<L, D>;
-  allow_lds(edge_bwd_rs_kernel<L, D>, Lay::END);
-  hipLaunchKernelGGL((edge_bwd_rs_kernel<L, D>), dim3(RS_GRID), dim3(RS_NTH), Lay::END, st, a);
+  if (a.hid_in) {
+    allow_lds(edge_bwd_rs_kernel<L, D, true>, Lay::END);
+    hipLaunchKernelGGL((edge_bwd_rs_kernel<L, D, true>), dim3(RS_GRID), dim3(RS_NTH), Lay::END, st, a);
+  } else {
+    allow_lds(edge_bwd_rs_kernel<L, D, false>, Lay::END);
+    hipLaunchKernelGGL((edge_bwd_rs_kernel<L, D, false>), dim3(RS_GRID), dim3(RS_NTH), Lay::END, st, a);
+  }
   return hipGetLastError();
 }
 

@@ -8,13 +8,17 @@ import torch
 
 from . import (MGN_BF16, MGN_FP32, graph_struct, mgn_backward, mgn_create, mgn_destroy, mgn_forward,
                mgn_graph_validate, mgn_mse_grad, mgn_param_count, mgn_set_params, mgn_set_recompute,
-               mgn_rollout_update, mgn_set_inference, mgn_sgd_step, mgn_workspace_size)
+               mgn_rollout_update, mgn_set_h1_stash, mgn_set_inference, mgn_sgd_step, mgn_workspace_size)
 
 
 class Session:
     def __init__(self, latent: int, K: int, depth: int, precision: str, graph: dict, node_feat, edge_feat, halo,
                  params, device: str = "cuda", node_in: int = 11, edge_in: int = 4, node_out: int = 5,
-                 recompute: int = 0, chunk_edges: int = 0, inference: bool = False):
+                 recompute: int = 0, chunk_edges: int = 0, inference: bool = False, h1_stash: int = 0):
+        """h1_stash: blocks whose first-Linear ReLU output the forward keeps
+        for the backward (row-split kernels, mgn_set_h1_stash); -1: as many
+        as the device's free memory holds beside the rest of the workspace
+        (with 8 GiB to spare)."""
         if not torch.cuda.is_available():
             raise RuntimeError("libmgn needs a HIP device")
         self.device = torch.device(device)
@@ -38,6 +42,14 @@ class Session:
         if inference:
             mgn_set_inference(self.model, True)
         self.ws_bytes = mgn_workspace_size(self.model, self.gs)
+        if h1_stash < 0 and not inference and K > 0 and ne > 0:
+            free = torch.cuda.mem_get_info(self.device)[0]
+            per = ne * latent * (2 if precision == "bf16" else 4)
+            h1_stash = int(max(0, min(K, (free - self.ws_bytes - (8 << 30)) // per)))
+        self.h1_stash = max(h1_stash, 0)
+        if self.h1_stash:
+            mgn_set_h1_stash(self.model, self.h1_stash)
+            self.ws_bytes = mgn_workspace_size(self.model, self.gs)
         self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=self.device)
         self.out = torch.empty((no, node_out), dtype=torch.float32, device=self.device)
         self.d_params = None if inference else torch.empty(self.n_params, dtype=torch.float32, device=self.device)

@@ -52,9 +52,9 @@ def local_inputs(mesh, p, latent, K, depth, seed, part=None):
     return dict(g=g, shapes=shapes, params=params, nf=nf, ef=ef, halo=halo, d_out=d_out, part=part)
 
 
-def run_gpu(c, latent, K, depth, prec, d_out=None, recompute=0, chunk_edges=0):
+def run_gpu(c, latent, K, depth, prec, d_out=None, recompute=0, chunk_edges=0, h1_stash=0):
     s = Session(latent, K, depth, prec, c["g"], c["nf"], c["ef"], c["halo"], c["params"], recompute=recompute,
-                chunk_edges=chunk_edges)
+                chunk_edges=chunk_edges, h1_stash=h1_stash)
     try:
         out = s.forward().cpu().numpy().copy()
         dp, dh = s.backward(c["d_out"] if d_out is None else d_out)

@@ -5,7 +5,9 @@ runs the edge backward (and the edge encoder's) in receiver chunks.  Against
 the run that keeps every block's inputs, on the same inputs: outputs bitwise
 equal (the forward is the same computation, only stored elsewhere), every
 gradient tensor equal up to the order in which chunk sums are added; and
-against the oracle with the parity criterion of test_gpu_parity."""
+against the oracle with the parity criterion of test_gpu_parity.  And the
+first-Linear stash of the row-split kernels (mgn_set_h1_stash): bitwise
+the results of the recomputing backward, for every block or only some."""
 import numpy as np
 import pytest
 
@@ -47,4 +49,27 @@ def test_checkpointed_against_oracle():
     gpu = run_gpu(c, l, K, D, "bf16", recompute=3, chunk_edges=300)
     ref = run_oracle(c, l, K, D, bf16=True)
     bad = compare("checkpointed", "bf16", c["shapes"], gpu, ref, calibrate(c, l, K, D, "bf16"))
+    assert not bad, bad
+
+
+@pytest.mark.parametrize("l,D", [(64, 3), (128, 2)])
+@pytest.mark.parametrize("stash", [1, 3, 9])
+def test_h1_stash_equals_recompute(l, D, stash):
+    K = 3
+    say(f"[h1 stash] l={l} D={D} K={K} stash={stash}")
+    c = local_inputs(meshes.sector(6, 16, 10, 4, seed=5), 1, l, K, D, 4)
+    base = run_gpu(c, l, K, D, "bf16")
+    st = run_gpu(c, l, K, D, "bf16", h1_stash=stash)
+    for name, a, b in zip(("outputs", "parameter gradients", "halo gradients"), st, base):
+        assert np.array_equal(a, b), f"{name} differ: {rel_err(a, b):.2e}"
+
+
+def test_h1_stash_against_oracle():
+    # the inputs of test_checkpointed_against_oracle
+    l, K, D = 128, 4, 2
+    say(f"[h1 stash] oracle parity l={l} K={K} D={D}")
+    c = local_inputs(meshes.sector(6, 16, 10, 4, seed=11), 1, l, K, D, 5)
+    gpu = run_gpu(c, l, K, D, "bf16", h1_stash=2)
+    ref = run_oracle(c, l, K, D, bf16=True)
+    bad = compare("h1 stash", "bf16", c["shapes"], gpu, ref, calibrate(c, l, K, D, "bf16"))
     assert not bad, bad

@@ -156,6 +156,45 @@ def test_recompute_setting():
         mgn.mgn_destroy(h)
 
 
+def test_h1_stash_setting():
+    """The first-Linear stash adds one bf16 E x l slot per kept block to the
+    row-split plan (at most K), nothing to the streaming plans (which keep
+    every block's anyway), and nothing with checkpointing."""
+    import ctypes as C
+    L = mgn.lib()
+    g = mgn.mgn_graph(1000, 0, 20000, C.c_void_p(256), C.c_void_p(512), C.c_void_p(768), C.c_void_p(1024))
+
+    def ws(h):
+        n = C.c_size_t()
+        assert L.mgn_workspace_size(h, C.byref(g), C.byref(n)) == mgn.MGN_OK
+        return n.value
+
+    h = mgn.mgn_create(64, 6, 2, mgn.MGN_BF16)
+    try:
+        assert L.mgn_set_h1_stash(h, -1) == mgn.MGN_E_ARG
+        n0 = ws(h)
+        assert L.mgn_set_h1_stash(h, 2) == mgn.MGN_OK
+        n2 = ws(h)
+        assert L.mgn_set_h1_stash(h, 50) == mgn.MGN_OK
+        n6 = ws(h)
+        slot = 20000 * 64 * 2
+        assert 2 * slot <= n2 - n0 <= 2 * slot + 1024 and 6 * slot <= n6 - n0 <= 6 * slot + 1024
+        assert L.mgn_set_recompute(h, 2, 0) == mgn.MGN_OK
+        n_lean = ws(h)
+        assert L.mgn_set_h1_stash(h, 0) == mgn.MGN_OK
+        assert ws(h) == n_lean
+    finally:
+        mgn.mgn_destroy(h)
+    h = mgn.mgn_create(256, 3, 3, mgn.MGN_BF16)  # streaming kernels
+    try:
+        n0 = ws(h)
+        assert L.mgn_set_h1_stash(h, 3) == mgn.MGN_OK
+        assert ws(h) == n0
+    finally:
+        mgn.mgn_destroy(h)
+    assert L.mgn_set_h1_stash(None, 1) == mgn.MGN_E_ARG
+
+
 @pytest.mark.parametrize("mesh,P,random", [
     (meshes.sector(6, 16, 10, 4, seed=7), 4, False),
     (meshes.delaunay_box(9, 8, 7, seed=5), 5, True),
