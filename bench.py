@@ -205,7 +205,7 @@ def main():
             roof = dict(bound="hbm", achieved=by / t_launch / 1e9, peak=PEAK["hbm"] / 1e9, unit="GB/s")
         roof["frac"] = roof["achieved"] / roof["peak"]
         roof["kernel"] = dom
-        roof["traffic"] = measured_traffic(dom, cfg.name)
+        roof["traffic"] = measured_traffic(dom, cfg.name, round(stash * cfg.K))
     else:
         log(f"[bench] no algorithmic model for {dom} on this configuration: roofline omitted")
     if args.copy_calibration:
@@ -472,11 +472,12 @@ def bench_lockstep(args, cfg):
     print(json.dumps(line), flush=True)
 
 
-def measured_traffic(kernel: str, config: str):
+def measured_traffic(kernel: str, config: str, h1_stash: int = 0):
     """HBM bytes per launch of `kernel` from a committed counter summary
     (profiles/<kernel>_<config>_traffic.txt: FETCH_SIZE and WRITE_SIZE per
-    launch, scaled by the counters of a plain copy of known size), used only
-    while the kernels are the ones the counters were taken on."""
+    launch, scaled by the counters of a plain copy of known size, averaged
+    over the step's launches), used only while the kernels and the number of
+    first-Linear stash blocks are the ones the counters were taken with."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"{kernel}_{config}_traffic.txt")
     if not os.path.exists(path):
@@ -488,6 +489,8 @@ def measured_traffic(kernel: str, config: str):
             vals[k.strip()] = v.strip()
     src = open(os.path.join(ROOT, "paper_2307_13592_amd", "csrc", "kernels.hip"), "rb").read()
     if vals.get("kernels_sha256") != hashlib.sha256(src).hexdigest():
+        return None
+    if int(vals.get("h1_stash_blocks", "0")) != h1_stash:
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])
