@@ -175,3 +175,26 @@ def rollout_update(node_feat, out, col0: int = 3) -> np.ndarray:
                                                    C.c_int32(o.shape[1]), C.c_int32(col0)):
         raise ValueError("orc_rollout_update rejected its arguments")
     return nf
+
+
+def norm_accumulate(stats, x) -> np.ndarray:
+    """Normalize's running statistics after adding the rows of x ([rows][cols]):
+    a new float64 array [n, column sums, column sums of squares]."""
+    x = _f64(np.atleast_2d(x))
+    st = _f64(stats).copy()
+    rows, cols = x.shape
+    if st.shape != (1 + 2 * cols,) or lib().orc_norm_accumulate(_p(x), C.c_int64(rows), C.c_int32(cols), _p(st)):
+        raise ValueError("orc_norm_accumulate rejected its arguments")
+    return st
+
+
+def norm_apply(stats, x, eps: float = 1e-8) -> np.ndarray:
+    """x standardised with the statistics: (x - mean) / max(std, eps) per column."""
+    x = _f64(np.atleast_2d(x))
+    st = _f64(stats)
+    rows, cols = x.shape
+    out = np.empty_like(x)
+    if st.shape != (1 + 2 * cols,) or lib().orc_norm_apply(_p(x), C.c_int64(rows), C.c_int32(cols), _p(st),
+                                                            C.c_double(eps), _p(out)):
+        raise ValueError("orc_norm_apply rejected its arguments")
+    return out

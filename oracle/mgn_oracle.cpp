@@ -581,4 +581,37 @@ int orc_rollout_update(double* node_feat, int64_t n, int32_t node_in, const doub
   return 0;
 }
 
+// Normalize of Algorithm 1 (applied to the increments, node features and
+// edge features before the encoders), read as an online standardisation per
+// feature column: running sums over every row seen so far,
+//   stats = [n, sum_i x_ic (c < cols), sum_i x_ic^2 (c < cols)],
+// with mean_c = s1_c / n and std_c = max(sqrt(max(s2_c / n - mean_c^2, 0)), eps)
+// (the population deviation).  No rows seen: mean 0, std 1.
+int orc_norm_accumulate(const double* x, int64_t rows, int32_t cols, double* stats) {
+  if (rows < 0 || cols < 1 || !stats || (rows > 0 && !x)) return -1;
+  for (int64_t i = 0; i < rows; ++i)
+    for (int32_t c = 0; c < cols; ++c) {
+      const double v = x[i * cols + c];
+      stats[1 + c] += v;
+      stats[1 + cols + c] += v * v;
+    }
+  stats[0] += (double)rows;
+  return 0;
+}
+
+int orc_norm_apply(const double* x, int64_t rows, int32_t cols, const double* stats, double eps, double* out) {
+  if (rows < 0 || cols < 1 || !stats || !(eps > 0) || (rows > 0 && (!x || !out))) return -1;
+  for (int32_t c = 0; c < cols; ++c) {
+    double mean = 0.0, sd = 1.0;
+    if (stats[0] > 0) {
+      mean = stats[1 + c] / stats[0];
+      const double var = stats[1 + cols + c] / stats[0] - mean * mean;
+      sd = std::sqrt(var > 0 ? var : 0.0);
+      if (sd < eps) sd = eps;
+    }
+    for (int64_t i = 0; i < rows; ++i) out[i * cols + c] = (x[i * cols + c] - mean) / sd;
+  }
+  return 0;
+}
+
 }  // extern "C"

@@ -102,6 +102,13 @@ int orc_sgd_step(double* params, const double* grad, int64_t n, double lr);
 int orc_rollout_update(double* node_feat, int64_t n, int32_t node_in, const double* out, int32_t node_out,
                        int32_t col0);
 
+/* Normalize (Algorithm 1): online per-column standardisation.  stats holds
+ * 1 + 2 cols doubles [n, column sums, column sums of squares], zero for a
+ * fresh normaliser; accumulate adds rows to it, apply writes
+ * (x - mean) / max(std, eps).  Return -1 on bad arguments. */
+int orc_norm_accumulate(const double* x, int64_t rows, int32_t cols, double* stats);
+int orc_norm_apply(const double* x, int64_t rows, int32_t cols, const double* stats, double eps, double* out);
+
 #ifdef __cplusplus
 }
 #endif

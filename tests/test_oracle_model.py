@@ -321,3 +321,40 @@ def test_mse_global_shares_add_up_to_the_whole():
         grads.append(d_p)
     assert abs(sum(shares) - L) < 1e-14
     assert np.array_equal(np.concatenate(grads), d)
+
+
+def test_norm_hand_case():
+    """Normalize (Algorithm 1) on numbers worked by hand: rows 1 and 3 give
+    mean 2 and population deviation 1, so 5 maps to 3 and 2 to 0; a column
+    that never varies keeps deviation eps; no rows seen is the identity."""
+    st = oracle.norm_accumulate(np.zeros(5), np.array([[1.0, 7.0], [3.0, 7.0]]))
+    assert st.tolist() == [2.0, 4.0, 14.0, 10.0, 98.0]
+    y = oracle.norm_apply(st, np.array([[5.0, 7.0], [2.0, 8.0]]), eps=0.5)
+    assert y.tolist() == [[3.0, 0.0], [0.0, 2.0]]
+    x = np.array([[-1.5, 2.0]])
+    assert np.array_equal(oracle.norm_apply(np.zeros(5), x), x)
+
+
+def test_norm_against_moments():
+    """Statistics accumulated over three calls (one of them empty) equal one
+    call over the concatenated rows, give numpy's mean and population
+    variance of those rows, and standardise them to mean 0 and deviation 1
+    per column; ragged row counts, 11 columns at different scales."""
+    r = np.random.default_rng(12)
+    parts = [r.normal(3.0, 0.5, (97, 11)) * np.arange(1, 12), np.zeros((0, 11)), r.normal(-2.0, 4.0, (1003, 11))]
+    st = np.zeros(23)
+    for x in parts:
+        st = oracle.norm_accumulate(st, x)
+    allx = np.concatenate(parts)
+    one = oracle.norm_accumulate(np.zeros(23), allx)
+    assert np.allclose(st, one, rtol=1e-13, atol=0)
+    assert st[0] == len(allx)
+    mean, var = st[1:12] / st[0], st[12:] / st[0] - (st[1:12] / st[0]) ** 2
+    assert np.allclose(mean, allx.mean(0), rtol=1e-12) and np.allclose(var, allx.var(0), rtol=1e-10)
+    y = oracle.norm_apply(st, allx)
+    assert np.allclose(y.mean(0), 0, atol=1e-12) and np.allclose(y.std(0), 1, rtol=1e-10)
+    with pytest.raises(ValueError):
+        oracle.norm_accumulate(np.zeros(5), np.zeros((3, 4)))
+    with pytest.raises(ValueError):
+        oracle.norm_apply(np.zeros(5), np.zeros((3, 2)), eps=0.0)
+
