@@ -195,6 +195,28 @@ mgn_status mgn_set_inference(mgn_model* m, int32_t on);
 mgn_status mgn_rollout_update(const float* out, int64_t n, int32_t node_out, float* node_feat, int32_t node_in,
                               int32_t col0, mgn_stream stream);
 
+/* Normalize (Algorithm 1: the increments, node features and edge features
+ * are normalised before the encoders), read as an online standardisation
+ * per feature column.  stats is a device array of 1 + 2 cols doubles,
+ * [n, column sums, column sums of squares] over every row accumulated so
+ * far (all zero for a fresh normaliser; the caller owns it, one per kind of
+ * input).  mgn_norm_accumulate adds the rows of x [rows][cols] (device fp32)
+ * to it, summing in fp64 in a fixed order (no atomics: the same inputs give
+ * the same bits); work is a device scratch array of at least
+ * MGN_NORM_WORK_PER_COL * cols doubles, overwritten.  mgn_norm_apply writes
+ * out[i][c] = (x[i][c] - mean_c) / max(std_c, eps) rounded from fp64 once,
+ * with mean_c = sum / n and std_c the population deviation (no rows
+ * accumulated: the identity); out may equal x.  Both are asynchronous on
+ * `stream`.  MGN_E_ARG for rows < 0, cols outside 1 .. MGN_NORM_MAX_COLS,
+ * eps <= 0, or a NULL / misaligned pointer (8-byte stats and work, 4-byte
+ * x and out). */
+#define MGN_NORM_MAX_COLS 64
+#define MGN_NORM_WORK_PER_COL 1024
+mgn_status mgn_norm_accumulate(const float* x, int64_t rows, int32_t cols, double* stats, double* work,
+                               mgn_stream stream);
+mgn_status mgn_norm_apply(const float* x, int64_t rows, int32_t cols, const double* stats, double eps, float* out,
+                          mgn_stream stream);
+
 /* Device workspace mgn_forward/mgn_backward need for graph g (bytes) under
  * the model's checkpointing setting. */
 mgn_status mgn_workspace_size(const mgn_model* m, const mgn_graph* g, size_t* bytes);

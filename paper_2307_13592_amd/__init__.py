@@ -23,7 +23,7 @@ STATUS_NAMES = ["MGN_OK", "MGN_E_ARG", "MGN_E_GRAPH", "MGN_E_STATE", "MGN_E_NOME
 EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mgn_set_params", "mgn_sgd_step",
            "mgn_get_params",
            "mgn_partition_slabs", "mgn_graph_sizes", "mgn_graph_build", "mgn_graph_validate", "mgn_set_recompute",
-           "mgn_set_inference", "mgn_set_h1_stash", "mgn_rollout_update",
+           "mgn_set_inference", "mgn_set_h1_stash", "mgn_rollout_update", "mgn_norm_accumulate", "mgn_norm_apply",
            "mgn_workspace_size",
            "mgn_forward", "mgn_backward", "mgn_forward_begin", "mgn_forward_block", "mgn_forward_end",
            "mgn_backward_begin", "mgn_backward_block", "mgn_backward_end", "mgn_halo_masks", "mgn_copy_latents",
@@ -84,6 +84,8 @@ def lib() -> C.CDLL:
             "mgn_set_inference": (C.c_int, [vp, i32]),
             "mgn_set_h1_stash": (C.c_int, [vp, i32]),
             "mgn_rollout_update": (C.c_int, [vp, i64, i32, vp, i32, i32, vp]),
+            "mgn_norm_accumulate": (C.c_int, [vp, i64, i32, vp, vp, vp]),
+            "mgn_norm_apply": (C.c_int, [vp, i64, i32, vp, C.c_double, vp, vp]),
             "mgn_workspace_size": (C.c_int, [vp, vp, vp]),
             "mgn_forward": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]),
             "mgn_backward": (C.c_int, [vp, vp, vp, C.c_int, vp, vp]),
@@ -239,6 +241,24 @@ def mgn_set_inference(model, on: bool = True) -> None:
 
 def mgn_set_h1_stash(model, n_blocks: int) -> None:
     _check(lib().mgn_set_h1_stash(model, int(n_blocks)), model)
+
+
+MGN_NORM_MAX_COLS = 64
+MGN_NORM_WORK_PER_COL = 1024
+
+
+def mgn_norm_accumulate(x, stats, work, stream=None) -> None:
+    """Adds the rows of x (device float32 [rows][cols]) to the running
+    statistics `stats` (device float64 [1 + 2 cols]); work: device float64
+    scratch of at least MGN_NORM_WORK_PER_COL * cols."""
+    rows, cols = x.shape
+    _check(lib().mgn_norm_accumulate(_dev(x), rows, cols, _dev(stats), _dev(work), _stream(stream)))
+
+
+def mgn_norm_apply(x, stats, out, eps: float = 1e-8, stream=None) -> None:
+    """out = (x - mean) / max(std, eps) per column (device float32; out may be x)."""
+    rows, cols = x.shape
+    _check(lib().mgn_norm_apply(_dev(x), rows, cols, _dev(stats), C.c_double(eps), _dev(out), _stream(stream)))
 
 
 def mgn_rollout_update(out, node_feat, col0: int = 3, stream=None) -> None:

@@ -518,6 +518,30 @@ mgn_status mgn_rollout_update(const float* out, int64_t n, int32_t node_out, flo
   return MGN_OK;
 }
 
+mgn_status mgn_norm_accumulate(const float* x, int64_t rows, int32_t cols, double* stats, double* work,
+                               mgn_stream stream) {
+  if (rows < 0 || cols < 1 || cols > MGN_NORM_MAX_COLS)
+    return fail(nullptr, MGN_E_ARG, "mgn_norm_accumulate: bad sizes (rows >= 0, 1 <= cols <= MGN_NORM_MAX_COLS)");
+  if (!stats || !work || !aligned(stats, 8) || !aligned(work, 8) || (rows > 0 && (!x || !aligned(x, 4))))
+    return fail(nullptr, MGN_E_ARG, "mgn_norm_accumulate: NULL or misaligned pointer");
+  if (rows == 0) return MGN_OK;
+  hipError_t e = launch_norm_accumulate(x, rows, cols, stats, work, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(nullptr, e, "mgn_norm_accumulate");
+  return MGN_OK;
+}
+
+mgn_status mgn_norm_apply(const float* x, int64_t rows, int32_t cols, const double* stats, double eps, float* out,
+                          mgn_stream stream) {
+  if (rows < 0 || cols < 1 || cols > MGN_NORM_MAX_COLS || !(eps > 0))
+    return fail(nullptr, MGN_E_ARG, "mgn_norm_apply: bad sizes or eps (rows >= 0, 1 <= cols <= MGN_NORM_MAX_COLS, eps > 0)");
+  if (!stats || !aligned(stats, 8) || (rows > 0 && (!x || !out || !aligned(x, 4) || !aligned(out, 4))))
+    return fail(nullptr, MGN_E_ARG, "mgn_norm_apply: NULL or misaligned pointer");
+  if (rows == 0) return MGN_OK;
+  hipError_t e = launch_norm_apply(x, rows, cols, stats, eps, out, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(nullptr, e, "mgn_norm_apply");
+  return MGN_OK;
+}
+
 mgn_status mgn_workspace_size(const mgn_model* cm, const mgn_graph* g, size_t* bytes) {
   mgn_model* m = const_cast<mgn_model*>(cm);
   if (!m) return fail(nullptr, MGN_E_ARG, "mgn_workspace_size: model is NULL");

@@ -142,6 +142,13 @@ hipError_t launch_halo_bf16(const float* H, int K, int64_t n_halo, int64_t n_own
 hipError_t launch_sgd(float* p, const float* g, int64_t n, float lr, hipStream_t st);
 // nf[i][col0 + j] += out[i][j], i < n, j < d (row strides fin and d).
 hipError_t launch_rollout(const float* out, int64_t n, int d, float* nf, int fin, int col0, hipStream_t st);
+// Normalize: work holds norm_work_doubles(cols) doubles; cols <= NT (the
+// C ABI allows at most MGN_NORM_MAX_COLS).
+int norm_work_doubles(int cols);
+hipError_t launch_norm_accumulate(const float* x, int64_t rows, int cols, double* stats, double* work,
+                                  hipStream_t st);
+hipError_t launch_norm_apply(const float* x, int64_t rows, int cols, const double* stats, double eps, float* out,
+                             hipStream_t st);
 // Halo exchange between partitions on one device: dst[dst_rows[i]] = (or +=,
 // add != 0) src[src_rows[i]], rows of L floats (L a multiple of 4, 16-byte
 // aligned rows); pairs with out-of-range indices are skipped.

@@ -22,6 +22,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
+#include "../../include/mgn.h"
 
 namespace mgn {
 
@@ -410,6 +411,98 @@ hipError_t launch_rollout(const float* out, int64_t n, int d, float* nf, int fin
   if (n <= 0) return hipSuccess;
   const int64_t b = (n * d + NT - 1) / NT;
   hipLaunchKernelGGL(rollout_kernel, dim3((unsigned)(b < 8192 ? b : 8192)), dim3(NT), 0, st, out, n, d, nf, fin, col0);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ Normalize ---
+// Online standardisation per feature column (Normalize of Algorithm 1):
+// stats = [n, column sums, column sums of squares] in fp64.  Accumulation:
+// up to NORM_BLOCKS workgroups, each over a contiguous row range; thread t
+// takes column t % cols of every (NT / cols)-th row from its group's first
+// (consecutive threads read consecutive floats), with fp64 sums; the groups'
+// sums and then the workgroups' partials are added in a fixed order (no
+// atomics), so the result does not depend on timing.
+constexpr int NORM_BLOCKS = 512;
+
+__global__ __launch_bounds__(NT) void norm_partial_kernel(const float* __restrict__ x, int64_t rows, int cols,
+                                                          double* __restrict__ part) {
+  __shared__ double s1[NT], s2[NT];
+  const int G = NT / cols;  // row groups of the workgroup
+  const int t = threadIdx.x, g = t / cols, c = t - g * cols;
+  const int64_t r0 = rows * blockIdx.x / gridDim.x, r1 = rows * (blockIdx.x + 1) / gridDim.x;
+  double a = 0.0, b = 0.0;
+  if (g < G)
+    for (int64_t r = r0 + g; r < r1; r += G) {
+      const double v = x[r * cols + c];
+      a += v;
+      b += v * v;
+    }
+  s1[t] = a;
+  s2[t] = b;
+  __syncthreads();
+  if (t < cols) {
+    double A = 0.0, B = 0.0;
+    for (int k = 0; k < G; ++k) {
+      A += s1[k * cols + t];
+      B += s2[k * cols + t];
+    }
+    part[(int64_t)blockIdx.x * 2 * cols + t] = A;
+    part[(int64_t)blockIdx.x * 2 * cols + cols + t] = B;
+  }
+}
+
+// stats[1 + j] += sum over the workgroups, in order, of part[b][j] (j < 2 cols:
+// the column sums, then the sums of squares); stats[0] += rows.
+__global__ void norm_final_kernel(const double* __restrict__ part, int nb, int cols, int64_t rows,
+                                  double* __restrict__ stats) {
+  const int t = threadIdx.x;
+  if (t < 2 * cols) {
+    double A = 0.0;
+    for (int b = 0; b < nb; ++b) A += part[(int64_t)b * 2 * cols + t];
+    stats[1 + t] += A;
+  }
+  if (t == 0) stats[0] += (double)rows;
+}
+
+// out = (x - mean) / max(std, eps) per column, in fp64, rounded once; out may be x.
+__global__ void norm_apply_kernel(const float* x, int64_t n, int cols, const double* __restrict__ stats, double eps,
+                                  float* out) {
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = t / cols;
+    const int c = (int)(t - i * cols);
+    double mean = 0.0, sd = 1.0;
+    if (stats[0] > 0) {
+      mean = stats[1 + c] / stats[0];
+      const double var = stats[1 + cols + c] / stats[0] - mean * mean;
+      sd = sqrt(var > 0 ? var : 0.0);
+      if (sd < eps) sd = eps;
+    }
+    out[t] = (float)((x[t] - mean) / sd);
+  }
+}
+
+int norm_work_doubles(int cols) { return NORM_BLOCKS * 2 * cols; }
+static_assert(NORM_BLOCKS * 2 == MGN_NORM_WORK_PER_COL && MGN_NORM_MAX_COLS * 2 <= NT, "Normalize sizes");
+
+hipError_t launch_norm_accumulate(const float* x, int64_t rows, int cols, double* stats, double* work,
+                                  hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  if (cols < 1 || cols > NT) return hipErrorInvalidValue;
+  const int64_t want = (rows + 1023) / 1024;
+  const int nb = (int)(want < NORM_BLOCKS ? want : NORM_BLOCKS);
+  hipLaunchKernelGGL(norm_partial_kernel, dim3(nb), dim3(NT), 0, st, x, rows, cols, work);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(norm_final_kernel, dim3(1), dim3(NT), 0, st, work, nb, cols, rows, stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm_apply(const float* x, int64_t rows, int cols, const double* stats, double eps, float* out,
+                             hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  const int64_t n = rows * cols, b = (n + NT - 1) / NT;
+  hipLaunchKernelGGL(norm_apply_kernel, dim3((unsigned)(b < 8192 ? b : 8192)), dim3(NT), 0, st, x, n, cols, stats,
+                     eps, out);
   return hipGetLastError();
 }
 

@@ -8,7 +8,8 @@ import torch
 
 from . import (MGN_BF16, MGN_FP32, graph_struct, mgn_backward, mgn_create, mgn_destroy, mgn_forward,
                mgn_graph_validate, mgn_mse_grad, mgn_param_count, mgn_set_params, mgn_set_recompute,
-               mgn_rollout_update, mgn_set_h1_stash, mgn_set_inference, mgn_sgd_step, mgn_workspace_size)
+               mgn_norm_accumulate, mgn_norm_apply, MGN_NORM_WORK_PER_COL, mgn_rollout_update, mgn_set_h1_stash,
+               mgn_set_inference, mgn_sgd_step, mgn_workspace_size)
 
 
 class Session:
@@ -106,3 +107,23 @@ class Session:
             self.close()
         except Exception:
             pass
+
+
+class Normalizer:
+    """Running per-column statistics of one kind of input (increments, node
+    features or edge features) on the device, for Normalize of Algorithm 1:
+    accumulate() adds rows while training, apply() standardises."""
+
+    def __init__(self, cols: int, device: str = "cuda", eps: float = 1e-8):
+        self.cols, self.eps = cols, eps
+        self.stats = torch.zeros(1 + 2 * cols, dtype=torch.float64, device=device)
+        self.work = torch.empty(MGN_NORM_WORK_PER_COL * cols, dtype=torch.float64, device=device)
+
+    def accumulate(self, x, stream=None):
+        mgn_norm_accumulate(x, self.stats, self.work, stream)
+
+    def apply(self, x, out=None, stream=None):
+        out = torch.empty_like(x) if out is None else out
+        mgn_norm_apply(x, self.stats, out, self.eps, stream)
+        return out
+

@@ -156,6 +156,32 @@ def test_recompute_setting():
         mgn.mgn_destroy(h)
 
 
+def test_norm_argument_checks():
+    """Normalize's entry points reject bad sizes, eps and pointers on the host
+    (no device work is issued)."""
+    L = mgn.lib()
+    st, wk, x = C_vp(4096), C_vp(8192), C_vp(12288)
+    assert L.mgn_norm_accumulate(x, -1, 4, st, wk, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_accumulate(x, 10, 0, st, wk, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_accumulate(x, 10, mgn.MGN_NORM_MAX_COLS + 1, st, wk, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_accumulate(x, 10, 4, None, wk, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_accumulate(x, 10, 4, st, None, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_accumulate(None, 10, 4, st, wk, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_accumulate(x, 10, 4, C_vp(4100), wk, None) == mgn.MGN_E_ARG  # stats not 8-byte aligned
+    assert L.mgn_norm_accumulate(None, 0, 4, st, wk, None) == mgn.MGN_OK  # no rows: nothing to do
+    assert L.mgn_norm_apply(x, 10, 4, st, 0.0, x, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_apply(x, 10, 4, st, -1.0, x, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_apply(x, 10, 65, st, 1e-8, x, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_apply(x, 10, 4, st, 1e-8, None, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_apply(x, 10, 4, None, 1e-8, x, None) == mgn.MGN_E_ARG
+    assert L.mgn_norm_apply(None, 0, 4, st, 1e-8, None, None) == mgn.MGN_OK
+
+
+def C_vp(v):
+    import ctypes as C
+    return C.c_void_p(v)
+
+
 def test_h1_stash_setting():
     """The first-Linear stash adds one bf16 E x l slot per kept block to the
     row-split plan (at most K), nothing to the streaming plans (which keep
