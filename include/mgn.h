@@ -168,7 +168,8 @@ mgn_status mgn_set_recompute(mgn_model* m, int32_t interval, int64_t chunk_edges
  * writes it for the layer-2 weight gradient.  n_blocks > 0 makes the forward
  * keep h_1 of the last min(n_blocks, K) blocks (E x latent bf16 each, in the
  * workspace); their backward reads it instead of e^k and the projections
- * and writes nothing in its place.  Identical results (h_1 is the same
+ * and writes nothing in its place, so their forwards share one projection
+ * slot (n_nodes x 2 latent fp32) instead of keeping one each.  Identical results (h_1 is the same
  * bf16 value either way); less traffic for more workspace.  Ignored by
  * other kernels (the streaming kernels keep every block's h_1 anyway),
  * with checkpointing and in inference.  Takes effect for the next

@@ -253,10 +253,18 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.V = take(4 * (size_t)(one ? 2 : K + 1) * no * L);
   // bf16 mode: bf16 copy of every block's node input (inference: two), owned then halo rows
   p.V16 = m->prec == BF16 ? take(2 * (size_t)(p.infer ? 2 : K + 1) * nl * L) : 0;
-  // row-split edge kernels: node projections of every block's input (kept for
-  // the backward), or of the current block only (checkpointing, inference)
+  // row-split edge kernels: blocks whose first-Linear ReLU output the forward
+  // keeps (the last h1_stash of them, as memory allows) and whose backward
+  // therefore reads neither e^k's first-layer recompute nor the projections
+  int64_t nh1 = 0;
+  if (!p.infer && !p.lean && K > 0) nh1 = edge_rs(m->prec, m->L, m->D) ? std::min<int64_t>(m->h1_stash, K) : K;
+  p.h1_first = (int)(K - nh1);
+  // row-split edge kernels: node projections of every block's input that the
+  // backward recomputes from (blocks before h1_first) plus one slot shared by
+  // the stashed blocks' forwards, or of the current block only
+  // (checkpointing, inference)
   p.proj_all = edge_rs(m->prec, m->L, m->D) && !one;
-  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(one ? 1 : K) * nl * 2 * L)
+  p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(one ? 1 : p.h1_first + (nh1 > 0)) * nl * 2 * L)
            : edge_rsb(m->prec, m->L, m->D) ? take(4 * (size_t)nl * 2 * L)  // l = 256 forward: the current block's
            : 0;
   p.AGG = take(4 * (size_t)(one ? 1 : K) * no * L);
@@ -268,12 +276,7 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   // first Linear (half its products) and the row gather
   // (row-split kernels: for the last h1_stash blocks only, as memory allows;
   // the others recompute it from e and the kept projections)
-  {
-    int64_t nh1 = 0;
-    if (!p.infer && !p.lean && K > 0) nh1 = edge_rs(m->prec, m->L, m->D) ? std::min<int64_t>(m->h1_stash, K) : K;
-    p.h1_first = (int)(K - nh1);
-    p.HID_E1 = nh1 > 0 ? take(ts * (size_t)nh1 * ne * L) : 0;
-  }
+  p.HID_E1 = nh1 > 0 ? take(ts * (size_t)nh1 * ne * L) : 0;
   if (p.infer) {
     p.total = o;
     return p;
@@ -562,9 +565,10 @@ void* h1_slot(const WsPlan& p, char* ws, int k, size_t bytes) {
   return p.HID_E1 && k >= p.h1_first ? (void*)(ws + p.HID_E1 + bytes * (size_t)(k - p.h1_first)) : nullptr;
 }
 
-// Node projections of block k (one shared slot when checkpointing).
+// Node projections of block k (one shared slot when checkpointing, and one
+// shared by the blocks k >= h1_first, whose backward does not read them).
 float* proj_block(const WsPlan& p, char* ws, int k, int64_t nl, int L) {
-  return (float*)(ws + p.PROJ) + (p.proj_all ? (size_t)k * nl * 2 * L : 0);
+  return (float*)(ws + p.PROJ) + (p.proj_all ? (size_t)std::min(k, p.h1_first) * nl * 2 * L : 0);
 }
 
 // The edge half of block k forward: node projections (row-split path), then
@@ -1029,11 +1033,12 @@ struct Bwd {
       // the forward's projections of block k (or those of the aggregate
       // recompute; with the l = 256 row-split forward the checkpointed plan's
       // recompute of the first layer uses them too)
-      a.proj = (rs || (p.lean && edge_rsb(m->prec, L, D))) ? proj_block(p, ws, k, no + nh, L) : nullptr;
       // the forward's first-Linear ReLU output of this block (stash-all
-      // streaming path): not recomputed, and the layer-2 weight gradient
-      // reads it in place
+      // streaming path, or a stashed row-split block): not recomputed, and
+      // the layer-2 weight gradient reads it in place
       void* h1 = h1_slot(p, ws, k, ts * (size_t)ne * L);
+      // (a stashed row-split block's projection slot is shared and not read)
+      a.proj = ((rs && !h1) || (p.lean && edge_rsb(m->prec, L, D))) ? proj_block(p, ws, k, no + nh, L) : nullptr;
       a.hid_in = h1;
       for (int j = 0; j < 3; ++j) a.delta[j] = DEL_E[j];
       for (int j = 0; j < 2; ++j) a.hid[j] = HID_E[j];

@@ -44,13 +44,18 @@ class Session:
             mgn_set_inference(self.model, True)
         self.ws_bytes = mgn_workspace_size(self.model, self.gs)
         if h1_stash < 0 and not inference and K > 0 and ne > 0:
+            # the most blocks whose workspace (as the library plans it) leaves
+            # 8 GiB of the free memory
             free = torch.cuda.mem_get_info(self.device)[0]
-            per = ne * latent * (2 if precision == "bf16" else 4)
-            h1_stash = int(max(0, min(K, (free - self.ws_bytes - (8 << 30)) // per)))
+            h1_stash = 0
+            for n in range(K, 0, -1):
+                mgn_set_h1_stash(self.model, n)
+                if mgn_workspace_size(self.model, self.gs) + (8 << 30) <= free:
+                    h1_stash = n
+                    break
         self.h1_stash = max(h1_stash, 0)
-        if self.h1_stash:
-            mgn_set_h1_stash(self.model, self.h1_stash)
-            self.ws_bytes = mgn_workspace_size(self.model, self.gs)
+        mgn_set_h1_stash(self.model, self.h1_stash)
+        self.ws_bytes = mgn_workspace_size(self.model, self.gs)
         self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=self.device)
         self.out = torch.empty((no, node_out), dtype=torch.float32, device=self.device)
         self.d_params = None if inference else torch.empty(self.n_params, dtype=torch.float32, device=self.device)

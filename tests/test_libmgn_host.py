@@ -184,8 +184,9 @@ def C_vp(v):
 
 def test_h1_stash_setting():
     """The first-Linear stash adds one bf16 E x l slot per kept block to the
-    row-split plan (at most K), nothing to the streaming plans (which keep
-    every block's anyway), and nothing with checkpointing."""
+    row-split plan (at most K), and the kept blocks share one node-projection
+    slot (fp32, 2l per node) instead of one each; nothing changes for the
+    streaming plans (which keep every block's anyway) or with checkpointing."""
     import ctypes as C
     L = mgn.lib()
     g = mgn.mgn_graph(1000, 0, 20000, C.c_void_p(256), C.c_void_p(512), C.c_void_p(768), C.c_void_p(1024))
@@ -203,8 +204,9 @@ def test_h1_stash_setting():
         n2 = ws(h)
         assert L.mgn_set_h1_stash(h, 50) == mgn.MGN_OK
         n6 = ws(h)
-        slot = 20000 * 64 * 2
-        assert 2 * slot <= n2 - n0 <= 2 * slot + 1024 and 6 * slot <= n6 - n0 <= 6 * slot + 1024
+        slot, proj = 20000 * 64 * 2, 1000 * 2 * 64 * 4
+        d2, d6 = 2 * slot - proj, 6 * slot - 5 * proj
+        assert d2 <= n2 - n0 <= d2 + 1024 and d6 <= n6 - n0 <= d6 + 1024
         assert L.mgn_set_recompute(h, 2, 0) == mgn.MGN_OK
         n_lean = ws(h)
         assert L.mgn_set_h1_stash(h, 0) == mgn.MGN_OK
