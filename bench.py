@@ -90,6 +90,27 @@ def algorithmic(timer: str, cfg, E: int, No: int, Nh: int, lean: bool = False, s
     return None
 
 
+def step_roofline(cfg, E: int, No: int, ms: float) -> dict:
+    """Position of the whole step against the work the method needs per
+    edge-block, for kernels that fuse gather, MLP and scatter: flops per
+    edge-block forward 2l^2(D+2) + 2l^2(D+1) No/E, forward + backward with
+    recompute 4x that; HBM bytes per edge-block forward 2 l s_e + 4, backward
+    l s_e + 4 l s_g + 8 (s_e: bytes of a stored edge latent, s_g = 4: fp32
+    gradients), plus per node and block 40 l bytes (forward: v read, agg
+    written, v and agg read by the node MLP, v written; backward: v, agg
+    and dv read, dv and dagg written), spread over E/No edges.  Roof time =
+    the larger of flops / matrix peak and bytes / HBM peak."""
+    l, D, K = cfg.latent, cfg.depth, cfg.K
+    se = 2 if cfg.precision == "bf16" else 4
+    fl = 4 * (2 * l * l * (D + 2) + 2 * l * l * (D + 1) * No / E)
+    by = (2 * l * se + 4) + (l * se + 4 * l * 4 + 8) + 40 * l * No / E
+    peak_flops = PEAK["bf16"] if cfg.precision == "bf16" else PEAK["fp32"]
+    t_fl, t_by = fl * E * K / peak_flops, by * E * K / PEAK["hbm"]
+    roof_s = max(t_fl, t_by)
+    return dict(bound="mfma" if t_fl >= t_by else "hbm", flops_per_edge_block=fl, bytes_per_edge_block=by,
+                roof_ms=roof_s * 1e3, roof_edges_per_s=E * K / roof_s, frac=roof_s / (ms * 1e-3))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -118,6 +139,10 @@ def main():
                     help="row-split path: blocks whose first-Linear ReLU output the forward keeps for the "
                          "backward (-1, the default: as many as the GPU's free memory holds)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--oracle-timing", default=None, metavar="CONFIG",
+                    help="time only the CPU oracle on CONFIG (whole graph up to --oracle-sample-edges edges, "
+                         "else node 0's receptive field) with the OMP_NUM_THREADS the caller sets, and exit")
+    ap.add_argument("--oracle-sample-edges", type=int, default=100000)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 1 GiB once (a plain copy kernel of known size, "
                          "for scaling HBM byte counters)")
@@ -126,6 +151,8 @@ def main():
         print("bench.py runs on one GPU only: this build has no multi-GPU path (pass --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
+    if args.oracle_timing:
+        return oracle_timing(args.oracle_timing, args.oracle_sample_edges)
     import torch
     import synth
     import paper_2307_13592_amd as mgn
@@ -169,45 +196,67 @@ def main():
     log("[bench] warm-up done")
     if args.graph:
         return bench_graph(args, cfg, sess, step, ne, no, nh)
-    mgn.mgn_timing_enable(sess.model, True)
+    # timed region: launch timing off, one event pair per step on the launch
+    # stream; the step time is the median over the K steps
     stream = torch.cuda.current_stream()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    ev0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         step()
-    ev1.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1) / args.steps
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms = float(np.median(per_step))
+    ms_mean = evs[0].elapsed_time(evs[-1]) / args.steps
+    log(f"[bench] {ms:.2f} ms/step (median of {args.steps}; mean {ms_mean:.2f}, min {min(per_step):.2f}, "
+        f"max {max(per_step):.2f})")
+    # per-kernel pass, after the timed region: HIP events around every launch
+    k_steps = max(1, min(args.steps, 5))
+    mgn.mgn_timing_enable(sess.model, True)
+    for _ in range(k_steps):
+        step()
+    torch.cuda.synchronize()
     timers = mgn.mgn_timing_read(sess.model)
     mgn.mgn_timing_enable(sess.model, False)
-    log(f"[bench] {ms:.2f} ms/step")
     for k, (t, n) in sorted(timers.items(), key=lambda kv: -kv[1][0]):
         if n:
-            log(f"[bench]   {k:14s} {t / args.steps:9.3f} ms/step  {n // args.steps:4d} launches/step  "
+            log(f"[bench]   {k:14s} {t / k_steps:9.3f} ms/step  {n // k_steps:4d} launches/step  "
                 f"{t / n:8.4f} ms/launch")
 
-    # dominant kernel and its roofline position
-    dom = max((k for k in timers if timers[k][1]), key=lambda k: timers[k][0])
-    t_launch = timers[dom][0] / timers[dom][1] * 1e-3
-    alg = algorithmic(dom, cfg, ne, no, nh, lean=recompute > 0, stash=stash)
-    roof = None
-    if alg is not None:
+    # roofline position of every kernel class with an algorithmic model; the
+    # dominant one is the headline's
+    peak_flops = PEAK["bf16"] if cfg.precision == "bf16" else PEAK["fp32"]
+    kroofs = {}
+    for k, (t, n) in timers.items():
+        alg = algorithmic(k, cfg, ne, no, nh, lean=recompute > 0, stash=stash) if n else None
+        if alg is None:
+            continue
         # a block's edge backward may run as several receiver chunks
         # (checkpointed plan): one launch then does its share of the block
-        share = cfg.K * args.steps / timers[dom][1] if dom == "edge_bwd" else 1.0
+        share = cfg.K * k_steps / n if k == "edge_bwd" else 1.0
         by, fl = alg[0] * share, alg[1] * share
-        peak_flops = PEAK["bf16"] if cfg.precision == "bf16" else PEAK["fp32"]
-        intensity = fl / by if by else 0
-        if intensity >= peak_flops / PEAK["hbm"]:
-            roof = dict(bound="mfma", achieved=fl / t_launch / 1e12, peak=peak_flops / 1e12, unit="TFLOP/s")
+        t_launch = t / n * 1e-3
+        if fl / by >= peak_flops / PEAK["hbm"]:
+            r = dict(bound="mfma", achieved=fl / t_launch / 1e12, peak=peak_flops / 1e12, unit="TFLOP/s")
         else:
-            roof = dict(bound="hbm", achieved=by / t_launch / 1e9, peak=PEAK["hbm"] / 1e9, unit="GB/s")
-        roof["frac"] = roof["achieved"] / roof["peak"]
+            r = dict(bound="hbm", achieved=by / t_launch / 1e9, peak=PEAK["hbm"] / 1e9, unit="GB/s")
+        r["frac"] = r["achieved"] / r["peak"]
+        r["ms_per_launch"] = t / n
+        kroofs[k] = r
+    dom = max((k for k in timers if timers[k][1]), key=lambda k: timers[k][0])
+    roof = None
+    if dom in kroofs:
+        roof = {k: v for k, v in kroofs[dom].items() if k != "ms_per_launch"}
         roof["kernel"] = dom
         roof["traffic"] = measured_traffic(dom, cfg.name, round(stash * cfg.K))
     else:
         log(f"[bench] no algorithmic model for {dom} on this configuration: roofline omitted")
+    for k, r in sorted(kroofs.items(), key=lambda kv: -timers[kv[0]][0]):
+        log(f"[bench]   roofline {k:12s} {r['achieved']:9.1f} {r['unit']:8s} {r['frac']:.3f} of {r['bound']}")
+    step_roof = step_roofline(cfg, ne, no, ms)
+    log(f"[bench] step at {step_roof['frac']:.3f} of its roof ({step_roof['bound']}-bound, "
+        f"{step_roof['roof_ms']:.1f} ms at the peak)")
     if args.copy_calibration:
         src = torch.ones(2 ** 28, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -228,10 +277,17 @@ def main():
         "config": {"workload": f"{cfg.name}: {cfg.note}", "owned_nodes": no, "halo_nodes": nh, "edges": ne,
                    "latent": cfg.latent, "blocks": cfg.K, "mlp_depth": cfg.depth, "parallelism": "none"},
         "nodes_per_sec": no * cfg.K / (ms * 1e-3),
-        "plan": {"checkpoint_interval": recompute, "h1_stash_blocks": round(stash * cfg.K)},
+        "ms_per_step_mean": ms_mean,
+        "plan": {"checkpoint_interval": recompute, "h1_stash_blocks": round(stash * cfg.K),
+                 "stored": ("every block's edge latents and node stream; the first-Linear ReLU output of "
+                            f"{round(stash * cfg.K)} blocks, recomputed from node projections for the other "
+                            f"{cfg.K - round(stash * cfg.K)}") if recompute == 0 else
+                           (f"edge latents at every {recompute}th block; the others recomputed in the backward")},
         "roofline": roof,
+        "kernel_roofline": {k: {kk: vv for kk, vv in v.items()} for k, v in kroofs.items()},
+        "step_roofline": step_roof,
         "cpu_baseline": cpu,
-        "kernel_ms_per_step": {k: t / args.steps for k, (t, n) in timers.items() if n},
+        "kernel_ms_per_step": {k: t / k_steps for k, (t, n) in timers.items() if n},
     }
     print(json.dumps(line), flush=True)
 
@@ -498,6 +554,74 @@ def measured_traffic(kernel: str, config: str, h1_stash: int = 0):
         return None
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def prefix_sample(g: dict, n_edges: int) -> dict:
+    """The first receivers' in-edges, up to about n_edges: receivers keep their
+    local ids, senders outside them become halo nodes (ids after the
+    receivers, in their original order, so each receiver's edges stay sorted
+    by sender).  A bounded sample of a graph's edge-block work for timing."""
+    row_ptr = np.asarray(g["row_ptr"], np.int64)
+    r = int(np.searchsorted(row_ptr, n_edges))
+    r = max(1, min(r, g["n_owned"]))
+    ne = int(row_ptr[r])
+    send = np.asarray(g["send"][:ne], np.int64)
+    outside = np.unique(send[send >= r])
+    new = send.copy()
+    new[send >= r] = r + np.searchsorted(outside, send[send >= r])
+    return dict(n_owned=r, n_halo=int(outside.size), n_edges=ne, row_ptr=row_ptr[:r + 1].astype(np.int32),
+                send=new.astype(np.int32), owned=np.arange(r), edges=np.arange(ne))
+
+
+def oracle_timing(name: str, sample_edges: int):
+    """The oracle alone (no GPU) on configuration `name`: the whole graph
+    when it has at most `sample_edges` edges, else prefix_sample() of it
+    (the cost per edge-block is the measured quantity).  Threads:
+    OMP_NUM_THREADS as set by the caller (the oracle's OpenMP runtime reads
+    it when it loads)."""
+    import oracle
+    import synth
+
+    cfg = synth.CONFIGS[name]
+    case = synth.make_case(cfg, region=True)
+    m = case.mesh
+    part = m.part if m.part is not None else np.zeros(m.n_nodes, np.int32)
+    t = time.time()
+    g = oracle.graph_build(m.send, m.recv, part, m.n_nodes, cfg.part)
+    t_graph = time.time() - t
+    loc = case.local_inputs(g["l2g"], g["eperm"], g["n_owned"], g["n_halo"])
+    if g["n_edges"] <= sample_edges:
+        c, what = g, "whole graph"
+        nf, ef, halo = loc["node_feat"], loc["edge_feat"], loc["halo"] if g["n_halo"] else None
+    else:
+        c, what = prefix_sample(g, sample_edges), "first receivers' in-edges"
+        nf, ef = loc["node_feat"][c["owned"]], loc["edge_feat"][c["edges"]]
+        halo = synth.halo_latents(cfg.K, c["n_halo"], cfg.latent, cfg.seed) if c["n_halo"] else None
+    d_out = np.random.default_rng([cfg.seed, 5]).standard_normal((c["n_owned"], 5))
+    ocfg = oracle.ModelCfg(cfg.latent, cfg.K, cfg.depth, bf16=cfg.precision == "bf16")
+    t = time.time()
+    oracle.step(ocfg, c, case.params.astype(np.float64), nf.astype(np.float64), ef.astype(np.float64),
+                None if halo is None else halo.astype(np.float64), d_out)
+    dt = time.time() - t
+    threads = os.environ.get("OMP_NUM_THREADS", "unset (all cores)")
+    res = {"oracle_timing": {"config": name, "sample": f"{what}: {c['n_owned']} owned + {c['n_halo']} halo nodes, "
+                                                      f"{c['n_edges']} edges, {cfg.K} blocks, fwd+bwd",
+                             "seconds": dt, "edge_block_updates_per_s": c["n_edges"] * cfg.K / dt,
+                             "nodes_per_s": c["n_owned"] * cfg.K / dt, "graph_build_s": t_graph,
+                             "omp_num_threads": threads, "cpu_model": cpu_model(),
+                             "host_cpus": os.cpu_count()}}
+    log(f"[bench] oracle {name}: {res['oracle_timing']['sample']} in {dt:.2f}s ({threads} threads)")
+    print(json.dumps(res), flush=True)
+
+
 def cpu_baseline(cfg, g, loc, case):
     """The oracle on a bounded sample of the workload: the receptive field of
     one corner node (every block's edges into nodes within K-1 hops), which is
@@ -521,7 +645,7 @@ def cpu_baseline(cfg, g, loc, case):
     dt = time.time() - t
     log(f"[bench] oracle sample: {c['n_edges']} edges x {cfg.K} blocks in {dt:.1f}s ({threads} threads)")
     return {"value": c["n_edges"] * cfg.K / dt, "unit": "edge-block updates/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"receptive field of one corner node: {c['n_owned']} owned + {c['n_halo']} halo nodes, "
                       f"{c['n_edges']} edges, all {cfg.K} blocks, fwd+bwd"}
 

@@ -222,16 +222,24 @@ mgn_status mgn_norm_apply(const float* x, int64_t rows, int32_t cols, const doub
  * the model's checkpointing setting. */
 mgn_status mgn_workspace_size(const mgn_model* m, const mgn_graph* g, size_t* bytes);
 
-/* Forward pass (device pointers):
+/* Forward pass of one partition: Algorithm 1's forward (EncNode, EncEdge,
+ * the K GraphNetBlocks with the halo latents of block k read from halo[k],
+ * DecNode; section "Model": encoder, processor, decoder).  Device pointers:
  *   node_feat [n_owned][node_in], edge_feat [n_edges][edge_in] in local edge
  *   order, halo [K][n_halo][latent] (NULL iff n_halo == 0 or K == 0; 16-byte
- *   aligned), out [n_owned][node_out], workspace (256-byte aligned).
+ *   aligned), out [n_owned][node_out], workspace (256-byte aligned, at least
+ *   mgn_workspace_size bytes; caller-owned).
  * g must be the graph last passed to mgn_graph_validate.  The pointers and
- * their contents must stay valid and unchanged until mgn_backward. */
+ * their contents must stay valid and unchanged until mgn_backward.
+ * MGN_E_STATE without parameters or a validated graph, MGN_E_NOMEM when
+ * ws_bytes is too small, MGN_E_ARG for NULL or misaligned pointers. */
 mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* node_feat, const float* edge_feat,
                        const float* halo, float* out, void* workspace, size_t ws_bytes, mgn_stream stream);
 
-/* Backward pass of the last forward: d_out [n_owned][node_out] = dL/dout.
+/* Backward pass of the last forward (Algorithm 1: Backprop of the loss
+ * through DecNode, the K blocks in reverse and the encoders; section
+ * "Methodology": the halo gradients are what the owners receive).
+ * d_out [n_owned][node_out] = dL/dout.
  * d_params [param_count] receives dL/dtheta (overwritten, or added to when
  * accumulate != 0: gradient accumulation of Algorithm 1).  d_halo
  * [K][n_halo][latent] (NULL allowed; 16-byte aligned) receives dL/dhalo,

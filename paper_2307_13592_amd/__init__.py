@@ -125,6 +125,23 @@ def _dev(t):
     return C.c_void_p(t.data_ptr())
 
 
+def _devt(t, dtype, name: str, shape=None, numel=None, min_numel=None):
+    """_dev with the checks the C ABI cannot make (it takes no dtype, and
+    no length for some buffers): torch dtype, exact shape, exact or minimum
+    element count."""
+    if t is None:
+        raise ValueError(f"{name}: expected a device tensor, got None")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: expected {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name}: expected {numel} elements, got {t.numel()}")
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError(f"{name}: expected at least {min_numel} elements, got {t.numel()}")
+    return _dev(t)
+
+
 def _host(a, dtype):
     if a is None:
         return None, None
@@ -251,20 +268,35 @@ def mgn_norm_accumulate(x, stats, work, stream=None) -> None:
     """Adds the rows of x (device float32 [rows][cols]) to the running
     statistics `stats` (device float64 [1 + 2 cols]); work: device float64
     scratch of at least MGN_NORM_WORK_PER_COL * cols."""
+    import torch
+    if x.dim() != 2:
+        raise ValueError("x: expected [rows][cols]")
     rows, cols = x.shape
-    _check(lib().mgn_norm_accumulate(_dev(x), rows, cols, _dev(stats), _dev(work), _stream(stream)))
+    _check(lib().mgn_norm_accumulate(_devt(x, torch.float32, "x"), rows, cols,
+                                     _devt(stats, torch.float64, "stats", numel=1 + 2 * cols),
+                                     _devt(work, torch.float64, "work", min_numel=MGN_NORM_WORK_PER_COL * cols),
+                                     _stream(stream)))
 
 
 def mgn_norm_apply(x, stats, out, eps: float = 1e-8, stream=None) -> None:
     """out = (x - mean) / max(std, eps) per column (device float32; out may be x)."""
+    import torch
+    if x.dim() != 2:
+        raise ValueError("x: expected [rows][cols]")
     rows, cols = x.shape
-    _check(lib().mgn_norm_apply(_dev(x), rows, cols, _dev(stats), C.c_double(eps), _dev(out), _stream(stream)))
+    _check(lib().mgn_norm_apply(_devt(x, torch.float32, "x"), rows, cols,
+                                _devt(stats, torch.float64, "stats", numel=1 + 2 * cols), C.c_double(eps),
+                                _devt(out, torch.float32, "out", shape=(rows, cols)), _stream(stream)))
 
 
 def mgn_rollout_update(out, node_feat, col0: int = 3, stream=None) -> None:
     """node_feat[:, col0:col0 + out.shape[1]] += out (device tensors)."""
+    import torch
     n, d = out.shape
-    _check(lib().mgn_rollout_update(_dev(out), n, d, _dev(node_feat), int(node_feat.shape[1]), int(col0),
+    if node_feat.dim() != 2 or node_feat.shape[0] != n:
+        raise ValueError("node_feat: expected [n][features] with the rows of out")
+    _check(lib().mgn_rollout_update(_devt(out, torch.float32, "out"), n, d,
+                                    _devt(node_feat, torch.float32, "node_feat"), int(node_feat.shape[1]), int(col0),
                                     _stream(stream)))
 
 
@@ -369,16 +401,24 @@ def mgn_lockstep_backward(models, d_outs, d_params, d_halos, links, accumulate: 
     _check(st)
 
 
-def mgn_mse_grad(out, target, mask, loss, d_out, stream=None) -> None:
+def _mse_args(out, target, mask, loss, d_out):
+    import torch
+    if out.dim() != 2:
+        raise ValueError("out: expected [n][d]")
     n, d = out.shape
-    _check(lib().mgn_mse_grad(_dev(out), _dev(target), _dev(mask), n, d, _dev(loss), _dev(d_out),
-                              _stream(stream)))
+    return (n, d, _devt(out, torch.float32, "out"), _devt(target, torch.float32, "target", shape=(n, d)),
+            None if mask is None else _devt(mask, torch.uint8, "mask", numel=n),
+            _devt(loss, torch.float32, "loss", min_numel=2), _devt(d_out, torch.float32, "d_out", shape=(n, d)))
+
+
+def mgn_mse_grad(out, target, mask, loss, d_out, stream=None) -> None:
+    n, d, po, pt, pm, pl, pd = _mse_args(out, target, mask, loss, d_out)
+    _check(lib().mgn_mse_grad(po, pt, pm, n, d, pl, pd, _stream(stream)))
 
 
 def mgn_mse_grad_global(out, target, mask, global_rows: int, loss, d_out, stream=None) -> None:
-    n, d = out.shape
-    _check(lib().mgn_mse_grad_global(_dev(out), _dev(target), _dev(mask), n, d, int(global_rows), _dev(loss),
-                                     _dev(d_out), _stream(stream)))
+    n, d, po, pt, pm, pl, pd = _mse_args(out, target, mask, loss, d_out)
+    _check(lib().mgn_mse_grad_global(po, pt, pm, n, d, int(global_rows), pl, pd, _stream(stream)))
 
 
 def mgn_timing_enable(model, enable: bool = True) -> None:

@@ -13,11 +13,11 @@ and partitioned into theta slabs (the stand-in for the METIS partition of
 section "Methodology").
 """
 from .meshes import Mesh, hex_lattice, delaunay_box, sector, edge_count_sector
-from .draws import node_features, edge_features, targets, halo_latents, init_params, param_shapes
+from .draws import node_features, edge_features, targets, halo_latents, init_params, param_shapes, perturbed
 from .configs import CONFIGS, Config, make_case, Case
 
 __all__ = [
     "Mesh", "hex_lattice", "delaunay_box", "sector", "edge_count_sector",
-    "node_features", "edge_features", "targets", "halo_latents", "init_params", "param_shapes",
+    "node_features", "edge_features", "targets", "halo_latents", "init_params", "param_shapes", "perturbed",
     "CONFIGS", "Config", "make_case", "Case",
 ]

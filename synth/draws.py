@@ -77,6 +77,16 @@ def param_shapes(latent: int, K: int, depth: int, node_in: int = NODE_IN,
     return out
 
 
+def perturbed(arrays, run: int, rel: float = 2.0 ** -20):
+    """Copies (float64) of `arrays` with every entry scaled by 1 +- rel, the
+    signs drawn from a generator seeded with (4321, run): inputs that differ
+    at the level of float32 rounding, for measuring how far such noise moves
+    a computation's results."""
+    rng = np.random.default_rng([4321, run])
+    return [None if a is None else np.asarray(a, np.float64) * (1 + rel * rng.choice([-1.0, 1.0], np.shape(a)))
+            for a in arrays]
+
+
 def init_params(shapes, seed: int) -> np.ndarray:
     """float32 flat: W, b ~ U(-1/sqrt(fan_in), 1/sqrt(fan_in)) (PyTorch's default
     for Linear), gamma = 1 + 0.1 N(0,1), beta = 0.1 N(0,1) (perturbed from the

@@ -2,6 +2,8 @@
 and through the oracle on the same seeded fp32 inputs, compare per tensor."""
 from __future__ import annotations
 
+import json
+import os
 import sys
 
 import numpy as np
@@ -12,6 +14,27 @@ import paper_2307_13592_amd as mgn
 from paper_2307_13592_amd.runner import Session
 
 TOL = {"fp32": 1e-4, "bf16": 2e-2}
+# ceiling of a calibrated gradient bound (five times the stated tolerance in
+# float32, two and a half times it in bf16), lifted only for a tensor that the
+# oracle itself moves by more than half of it under float32-level input noise
+CAP = {"fp32": 5e-4, "bf16": 5e-2}
+
+
+def _log_path():
+    return os.environ.get("MGN_PARITY_LOG")
+
+
+def log_bounds(case: str, prec: str, rows):
+    """Appends one JSON line per tensor (case, precision, tensor, error,
+    calibration error of the independent implementation, the oracle's own
+    movement, bound) to the file named by MGN_PARITY_LOG, if set;
+    tests/parity_log.py tabulates them."""
+    path = _log_path()
+    if not path:
+        return
+    with open(path, "a") as f:
+        for nm, e, cal, sens, bound in rows:
+            f.write(json.dumps(dict(case=case, prec=prec, tensor=nm, err=e, calib=cal, sens=sens, bound=bound)) + "\n")
 
 
 def say(*a):
@@ -109,34 +132,88 @@ def calibrate(c, latent, K, depth, prec, g=None, nf=None, ef=None, halo=None, d_
     return res
 
 
-def compare(name, prec, shapes, gpu, ref, calib=None, halo_sel=None, calib_factor=2.0):
+def oracle_sensitivity(c, latent, K, depth, prec, g=None, nf=None, ef=None, halo=None, d_out=None, runs=4,
+                       rel=2.0 ** -20):
+    """The oracle itself (float64, or its bf16 mode) on the inputs perturbed
+    by a relative `rel` (node features, edge features, halo latents; seeded
+    signs), `runs` times: how far float32-level input noise moves each
+    result when nothing but the oracle computes it.  Returns the per-run
+    results in calibrate()'s format."""
+    g = c["g"] if g is None else g
+    nf = c["nf"] if nf is None else nf
+    ef = c["ef"] if ef is None else ef
+    halo = c["halo"] if halo is None else halo
+    res = []
+    for i in range(1, runs + 1):
+        x = synth.perturbed((nf, ef, halo), i, rel)
+        r = run_oracle(c, latent, K, depth, d_out=d_out, g=g, nf=x[0], ef=x[1], halo=x[2], bf16=prec == "bf16")
+        res.append((r["out"], r["d_params"], r["d_halo"]))
+    return res
+
+
+def bound_of(prec, cal_err=None, sens_err=None, calib_factor=2.0):
+    """Gradient bound of one tensor.  cal_err: the largest distance from the
+    oracle of an independent single-precision implementation's runs; sens_err:
+    the largest distance of the oracle's own runs on inputs perturbed at the
+    float32 level.  The bound is the precision's tolerance, widened to
+    calib_factor x the larger of the two when that is larger; it stays under
+    CAP[prec] unless the oracle's own movement alone reaches half the cap
+    (then the tensor is ill-conditioned at that level for any implementation,
+    shown by the oracle alone)."""
+    tol = TOL[prec]
+    errs = [x for x in (cal_err, sens_err) if x is not None]
+    if not errs:
+        return tol
+    b = max(tol, calib_factor * max(errs))
+    if sens_err is None or calib_factor * sens_err <= CAP[prec]:
+        b = min(b, max(tol, CAP[prec]))
+    return b
+
+
+def _max_err(runs, want):
+    return None if runs is None else max(rel_err(x, want) for x in runs)
+
+
+def compare(name, prec, shapes, gpu, ref, calib=None, halo_sel=None, calib_factor=2.0, sens=None):
     """Per-tensor max relative error of the GPU against the oracle.  Outputs
     must meet the tolerance of the precision.  A gradient tensor must meet
-    max(tolerance, calib_factor * the error of the independent float32
-    implementation's runs `calib` on the same tensor): gradients of a ReLU network
-    jump where a pre-activation sits within rounding distance of zero, and
-    in bf16 every rounded operand is such a place.  Returns the failures."""
+    bound_of(): the tolerance, widened to calib_factor x the distance from the
+    oracle of the independent float32 implementation's runs `calib` or of the
+    oracle's own runs on perturbed inputs `sens` (oracle_sensitivity),
+    capped at CAP[prec] unless the oracle's own runs alone need more.
+    Gradients of a ReLU network jump where a pre-activation sits within
+    rounding distance of zero, and in bf16 every rounded operand is such a
+    place.  Every tensor's (error, calibration, oracle movement, bound) goes
+    to the MGN_PARITY_LOG file when set.  Returns the failures."""
     out, dp, dh = gpu
     tol = TOL[prec]
     bad = []
+    rows = []
     e = rel_err(out, ref["out"])
+    rows.append(("out", e, None, None, tol))
     worst = ("out", e, tol)
     if e > tol:
         bad.append(("out", e, tol))
 
-    def check(nm, got, want, cal):
+    def check(nm, got, want, cal, sen):
         nonlocal worst
         e = rel_err(got, want)
-        t = tol if cal is None else max(tol, calib_factor * max(rel_err(x, want) for x in cal))
+        ce, se = _max_err(cal, want), _max_err(sen, want)
+        t = bound_of(prec, ce, se, calib_factor)
+        rows.append((nm, e, ce, se, t))
         if e / t > worst[1] / worst[2]:
             worst = (nm, e, t)
         if e > t:
             bad.append((nm, e, t))
 
     for nm, sl in segments(shapes):
-        check(nm, dp[sl], ref["d_params"][sl], None if calib is None else [cr[1][sl] for cr in calib])
+        check(nm, dp[sl], ref["d_params"][sl], None if calib is None else [cr[1][sl] for cr in calib],
+              None if sens is None else [sr[1][sl] for sr in sens])
     if ref["d_halo"].size:
         check("d_halo", dh if halo_sel is None else dh[:, halo_sel], ref["d_halo"],
-              None if calib is None else [cr[2] for cr in calib])
-    say(f"  {name}: out {rel_err(out, ref['out']):.2e}; tightest {worst[0]} {worst[1]:.2e} (bound {worst[2]:.2e})")
+              None if calib is None else [cr[2] for cr in calib], None if sens is None else [sr[2] for sr in sens])
+    log_bounds(name, prec, rows)
+    wide = [r for r in rows if r[4] > tol]
+    say(f"  {name}: out {rel_err(out, ref['out']):.2e}; tightest {worst[0]} {worst[1]:.2e} (bound {worst[2]:.2e}); "
+        f"{len(wide)} of {len(rows)} tensors above the nominal {tol:.0e}")
     return bad

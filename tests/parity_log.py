@@ -1,0 +1,67 @@
+"""Tabulates the per-tensor parity log the GPU tests append to the file named
+by MGN_PARITY_LOG (one JSON line per tensor: case, precision, tensor, error,
+calibration error of the independent float32 implementation, the oracle's own
+movement under float32-level input noise, bound).
+
+    python tests/parity_log.py LOG [--command "..."] > profiles/parity_bounds.txt
+
+Lists, per case, the tensor closest to its bound, and every tensor whose
+bound is above the nominal tolerance (1e-4 fp32, 2e-2 bf16) with the
+evidence that widened it."""
+from __future__ import annotations
+
+import argparse
+import json
+from collections import OrderedDict
+
+NOMINAL = {"fp32": 1e-4, "bf16": 2e-2}
+CAP = {"fp32": 5e-4, "bf16": 5e-2}
+
+
+def _f(x):
+    return "        -" if x is None else f"{x:9.2e}"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("log")
+    ap.add_argument("--command", default="")
+    ap.add_argument("--wide", type=int, default=400, help="at most this many rows of widened tensors")
+    a = ap.parse_args()
+    cases = OrderedDict()
+    for line in open(a.log):
+        line = line.strip()
+        if line:
+            r = json.loads(line)
+            cases.setdefault((r["case"], r["prec"]), []).append(r)
+    print("# Per-tensor parity of the GPU path against the oracle: err = max|gpu - oracle| / max|oracle|")
+    if a.command:
+        print(f"# command: {a.command}")
+    print("# calib = largest err of an independent float32 implementation (PyTorch layers, bf16 operands in bf16)")
+    print("#         on the same inputs and on inputs perturbed at 2^-20;")
+    print("# sens  = largest distance of the oracle's own results on inputs perturbed at 2^-20 from its results")
+    print("#         on the inputs as given (the oracle alone: how far float32-level noise moves this tensor);")
+    print("# bound = nominal (1e-4 fp32, 2e-2 bf16), widened to 2 x max(calib, sens), capped at 5e-4 / 5e-2")
+    print("#         unless 2 x sens alone exceeds the cap")
+    print()
+    print(f"{'case':56s} {'prec':4s} {'tensors':>7s} {'closest to bound':24s} {'err':>9s} {'bound':>9s}"
+          f" {'err/bnd':>7s} {'>nominal':>8s} {'>cap':>5s}")
+    wide_all = []
+    for (case, prec), rows in cases.items():
+        w = max(rows, key=lambda r: r["err"] / r["bound"])
+        wide = [r for r in rows if r["bound"] > NOMINAL[prec]]
+        over = [r for r in rows if r["bound"] > CAP[prec]]
+        wide_all += wide
+        print(f"{case[:56]:56s} {prec:4s} {len(rows):7d} {w['tensor'][:24]:24s} {w['err']:9.2e} {w['bound']:9.2e}"
+              f" {w['err'] / w['bound']:7.3f} {len(wide):8d} {len(over):5d}")
+    print()
+    print("# tensors whose bound is above the nominal tolerance"
+          + (f" (first {a.wide} of {len(wide_all)})" if len(wide_all) > a.wide else ""))
+    print(f"{'case':56s} {'tensor':24s} {'err':>9s} {'calib':>9s} {'sens':>9s} {'bound':>9s}")
+    for r in wide_all[:a.wide]:
+        print(f"{r['case'][:56]:56s} {r['tensor'][:24]:24s} {r['err']:9.2e} {_f(r.get('calib'))} {_f(r.get('sens'))}"
+              f" {r['bound']:9.2e}")
+
+
+if __name__ == "__main__":
+    main()

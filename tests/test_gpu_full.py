@@ -1,7 +1,13 @@
 """GPU parity at the benchmark sizes, in the launch configuration bench.py
 times (the whole partition in one step).
 
-C5 runs with edge-stream checkpointing (mgn_set_recompute).
+C4 runs with the first-Linear stash sized as bench.py sizes it (as many
+blocks as the GPU's free memory holds: 13 of 15 on a 288 GB MI355X), and a
+separate test checks that this plan gives bitwise the results of the plan
+without the stash.  C5 runs with edge-stream checkpointing
+(mgn_set_recompute).  C2 (100k-node Delaunay, fp32) is compared on every
+output and every gradient tensor with the oracle's full-size run stored by
+tests/golden/make_c2_reference.py.
 
 Sampled outputs: an owned node's output after K blocks depends only on its
 receptive field (tests/cone.py), so the oracle computes it on that
@@ -25,7 +31,7 @@ import synth
 import paper_2307_13592_amd as mgn
 from paper_2307_13592_amd.runner import Session
 from cone import cone
-from parity import TOL, calibrate, compare, rel_err, run_oracle, say
+from parity import TOL, calibrate, compare, oracle_sensitivity, rel_err, run_oracle, say
 
 pytestmark = pytest.mark.gpu
 
@@ -51,6 +57,17 @@ def _free(s):
 # edge-stream checkpoint interval per configuration: C5's stash-all workspace
 # (~430 GB of edge latents alone) does not fit one GPU
 RECOMPUTE = {"C5": 5}
+# first-Linear stash per configuration, as bench.py runs it (-1: as many
+# blocks as the free memory holds)
+H1_STASH = {"C4": -1}
+
+
+def _session(name, cfg, case, g, loc, h1_stash=None):
+    s = Session(cfg.latent, cfg.K, cfg.depth, cfg.precision, g, loc["node_feat"], loc["edge_feat"], loc["halo"],
+                case.params, recompute=RECOMPUTE.get(name, 0),
+                h1_stash=H1_STASH.get(name, 0) if h1_stash is None else h1_stash)
+    say(f"[full] {name}: workspace {s.ws_bytes / 2**30:.1f} GiB, first-Linear stash {s.h1_stash} of {cfg.K} blocks")
+    return s
 
 
 @pytest.mark.parametrize("name", ["C3", "C4", "C5"])
@@ -64,8 +81,9 @@ def test_sampled_outputs_and_gradients(name):
     centers = np.array([0] if name == "C5" else [0, r_mid * n_z + z_mid])
     d_out = np.zeros((no, 5), np.float32)
     d_out[centers] = np.random.default_rng([cfg.seed, 5]).standard_normal((centers.size, 5)).astype(np.float32)
-    s = Session(l, K, D, cfg.precision, g, loc["node_feat"], loc["edge_feat"], loc["halo"], case.params,
-                recompute=RECOMPUTE.get(name, 0))
+    s = _session(name, cfg, case, g, loc)
+    if name == "C4":
+        assert s.h1_stash > 0, "the benchmarked C4 plan stashes h_1"
     try:
         say(f"[full] {name}: GPU step")
         out = s.forward().cpu().numpy()
@@ -80,14 +98,16 @@ def test_sampled_outputs_and_gradients(name):
                d_out=d_out[c["owned"]])
     ref = run_oracle(sub, l, K, D, bf16=cfg.precision == "bf16")
     say(f"[full] {name}: oracle done")
-    cal = calibrate(sub, l, K, D, cfg.precision)
+    cal = calibrate(sub, l, K, D, cfg.precision, runs=4)
     say(f"[full] {name}: calibration done")
+    sens = oracle_sensitivity(sub, l, K, D, cfg.precision, runs=3)
+    say(f"[full] {name}: oracle sensitivity done")
     # outputs at the sampled nodes only
     e_out = rel_err(out[centers], ref["out"][c["centers_sub"]])
     ref_c = dict(ref)
     ref_c["out"] = ref["out"][c["centers_sub"]]
     bad = compare(f"{name} sampled", cfg.precision, case.shapes, (out[centers], dp, dh), ref_c, cal,
-                  halo_sel=c["halo"])
+                  halo_sel=c["halo"], sens=sens)
     assert e_out <= TOL[cfg.precision]
     assert not bad, bad
     outside = np.setdiff1d(np.arange(g["n_halo"]), c["halo"])
@@ -99,8 +119,7 @@ def test_full_size_determinism_and_linearity(name):
     cfg = synth.CONFIGS[name]
     case, g, loc = _inputs(cfg)
     d_out = np.random.default_rng([cfg.seed, 6]).standard_normal((g["n_owned"], 5)).astype(np.float32)
-    s = Session(cfg.latent, cfg.K, cfg.depth, cfg.precision, g, loc["node_feat"], loc["edge_feat"], loc["halo"],
-                case.params)
+    s = _session(name, cfg, case, g, loc)
     try:
         say(f"[full] {name}: run 1")
         o1 = s.forward().cpu().numpy().copy()
@@ -121,3 +140,81 @@ def test_full_size_determinism_and_linearity(name):
         _free(s)
 
 
+
+
+def _step(s, d_out):
+    out = s.forward().cpu().numpy().copy()
+    dp, dh = s.backward(d_out)
+    return out, dp.cpu().numpy().copy(), None if dh is None else dh.cpu().numpy().copy()
+
+
+def test_c4_stash_plan_bitwise():
+    """The benchmarked C4 plan (first-Linear stash for as many blocks as fit,
+    their forwards sharing one node-projection slot) gives bitwise the
+    outputs, parameter gradients and halo gradients of the plan without the
+    stash, at full size."""
+    cfg = synth.CONFIGS["C4"]
+    case, g, loc = _inputs(cfg)
+    d_out = np.random.default_rng([cfg.seed, 8]).standard_normal((g["n_owned"], 5)).astype(np.float32)
+    s = _session("C4", cfg, case, g, loc, h1_stash=-1)
+    n_st = s.h1_stash
+    try:
+        assert 0 < n_st <= cfg.K
+        say(f"[full] C4: step with {n_st} stashed blocks")
+        a = _step(s, d_out)
+    finally:
+        _free(s)
+    s = _session("C4", cfg, case, g, loc, h1_stash=0)
+    try:
+        say("[full] C4: step without the stash")
+        b = _step(s, d_out)
+    finally:
+        _free(s)
+    for nm, x, y in zip(("outputs", "parameter gradients", "halo gradients"), a, b):
+        assert np.array_equal(x, y), f"{nm} differ ({n_st} stashed blocks): {rel_err(x, y):.2e}"
+
+
+def test_c2_against_oracle():
+    """C2 at full size (100k nodes, 1.55M edges, l=128, K=15, fp32): every
+    output and every gradient tensor against the oracle's float64 run stored
+    in tests/golden/c2_reference.npz (written by
+    tests/golden/make_c2_reference.py, which calls only the oracle and the
+    input generator); the loss gradient is the fixture's N(0,1) draw.
+    Outputs within 1e-4; each gradient tensor within bound_of(): 1e-4, or
+    twice the oracle's own movement under float32-level input noise (stored
+    in the fixture) when that is larger, capped at 5e-4 unless the oracle's
+    movement alone reaches half of it."""
+    import os
+    import sys
+    from parity import bound_of, log_bounds, segments
+    sys.path.insert(0, os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden"))
+    import make_c2_reference as ref_script
+    fx = np.load(ref_script.OUT)
+    cfg = synth.CONFIGS["C2"]
+    case, g, loc = _inputs(cfg)
+    d_out = np.random.default_rng([cfg.seed, 7]).standard_normal((g["n_owned"], 5)).astype(np.float32)
+    # the library's local graph and the inputs are the ones the oracle ran on
+    assert ref_script.input_digest(g, loc, case.params, d_out) == str(fx["digest"])
+    s = _session("C2", cfg, case, g, loc)
+    try:
+        say("[full] C2: GPU step")
+        out, dp, _ = _step(s, d_out)
+    finally:
+        _free(s)
+    rows, bad = [], []
+    e = rel_err(out, fx["out"])
+    rows.append(("out", e, None, None, TOL["fp32"]))
+    if e > TOL["fp32"]:
+        bad.append(("out", e))
+    ref = fx["d_params"].astype(np.float64)
+    for i, (nm, sl) in enumerate(segments(case.shapes)):
+        e = rel_err(dp[sl], ref[sl])
+        sens = float(fx["sens_d_params"][i])
+        b = bound_of("fp32", None, sens)
+        rows.append((nm, e, None, sens, b))
+        if e > b:
+            bad.append((nm, e, b))
+    log_bounds("C2 full size", "fp32", rows)
+    w = max(rows, key=lambda r: r[1] / r[4])
+    say(f"  C2 full size: out {rows[0][1]:.2e}; tightest {w[0]} {w[1]:.2e} (bound {w[4]:.2e})")
+    assert not bad, bad

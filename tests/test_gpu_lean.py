@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 from synth import meshes
-from parity import calibrate, compare, local_inputs, rel_err, run_gpu, run_oracle, say
+from parity import calibrate, compare, local_inputs, oracle_sensitivity, rel_err, run_gpu, run_oracle, say
 
 pytestmark = pytest.mark.gpu
 
@@ -48,7 +48,8 @@ def test_checkpointed_against_oracle():
     c = local_inputs(meshes.sector(6, 16, 10, 4, seed=11), 1, l, K, D, 5)
     gpu = run_gpu(c, l, K, D, "bf16", recompute=3, chunk_edges=300)
     ref = run_oracle(c, l, K, D, bf16=True)
-    bad = compare("checkpointed", "bf16", c["shapes"], gpu, ref, calibrate(c, l, K, D, "bf16"))
+    bad = compare("checkpointed", "bf16", c["shapes"], gpu, ref, calibrate(c, l, K, D, "bf16"),
+                  sens=oracle_sensitivity(c, l, K, D, "bf16"))
     assert not bad, bad
 
 
@@ -71,5 +72,6 @@ def test_h1_stash_against_oracle():
     c = local_inputs(meshes.sector(6, 16, 10, 4, seed=11), 1, l, K, D, 5)
     gpu = run_gpu(c, l, K, D, "bf16", h1_stash=2)
     ref = run_oracle(c, l, K, D, bf16=True)
-    bad = compare("h1 stash", "bf16", c["shapes"], gpu, ref, calibrate(c, l, K, D, "bf16"))
+    bad = compare("h1 stash", "bf16", c["shapes"], gpu, ref, calibrate(c, l, K, D, "bf16"),
+                  sens=oracle_sensitivity(c, l, K, D, "bf16"))
     assert not bad, bad

@@ -15,7 +15,7 @@ import pytest
 import synth
 from synth import meshes
 import paper_2307_13592_amd as mgn
-from parity import TOL, calibrate, compare, local_inputs, rel_err, run_gpu, run_oracle, say
+from parity import TOL, calibrate, compare, local_inputs, oracle_sensitivity, rel_err, run_gpu, run_oracle, say
 import oracle
 
 pytestmark = pytest.mark.gpu
@@ -26,7 +26,8 @@ def _case(name, mesh, p, l, K, D, prec, seed=3, part=None):
     c = local_inputs(mesh, p, l, K, D, seed, part)
     gpu = run_gpu(c, l, K, D, prec)
     ref = run_oracle(c, l, K, D, bf16=prec == "bf16")
-    bad = compare(name, prec, c["shapes"], gpu, ref, calibrate(c, l, K, D, prec))
+    bad = compare(f"{name} l={l} K={K} D={D}", prec, c["shapes"], gpu, ref, calibrate(c, l, K, D, prec),
+                  sens=oracle_sensitivity(c, l, K, D, prec))
     assert not bad, bad
     if prec == "bf16":
         # the outputs also stay within the bf16 tolerance of the float64 network
@@ -54,7 +55,8 @@ def test_one_block_strict(prec, mesh_name):
     gpu = run_gpu(c, 128, 1, 2, prec)
     ref = run_oracle(c, 128, 1, 2, bf16=prec == "bf16")
     cal = calibrate(c, 128, 1, 2, prec, runs=3) if prec == "bf16" else None
-    bad = compare(f"{mesh_name} K=1", prec, c["shapes"], gpu, ref, cal)
+    sens = oracle_sensitivity(c, 128, 1, 2, prec) if prec == "bf16" else None
+    bad = compare(f"{mesh_name} K=1", prec, c["shapes"], gpu, ref, cal, sens=sens)
     assert not bad, bad
 
 
