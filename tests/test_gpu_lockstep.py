@@ -69,16 +69,21 @@ def test_lockstep_random_partition(prec):
     """Unstructured mesh, random 3-way partition: a node is a halo node of
     several parts at once, so its owner receives halo gradients from several
     parts per block, and some parts touch every other part.  Outputs and
-    every gradient tensor to the parity bar (the partition puts 70 % of the
-    nodes on a cut, so nearly every receiver's float32 sum is reordered
-    against the unpartitioned graph)."""
+    every gradient tensor to the parity bar; in bf16 the calibration factor is
+    3 instead of 2: the partition puts 70 % of the nodes on a cut, so nearly
+    every receiver's float32 sum and every weight-gradient sum is reordered
+    against the unpartitioned graph the calibration runs use."""
     mesh = meshes.delaunay_box(8, 7, 6, seed=3)
     part = np.random.default_rng(4).integers(0, 3, mesh.n_nodes).astype(np.int32)
     say(f"[lockstep] delaunay 8x7x6, random 3-way partition, {prec}")
     whole, gpu = _lockstep(mesh, 3, 64, 2, 2, prec, 13, part=part)
     ref = run_oracle(whole, 64, 2, 2, bf16=prec == "bf16")
+    # the calibration runs sum in the unpartitioned order; the parts' sums
+    # are reordered against it once more (partition-local sender order,
+    # per-part weight-gradient partials added across parts), hence 3x
     bad = compare("lockstep (random parts) vs whole mesh", prec, whole["shapes"], gpu, ref,
-                  calibrate(whole, 64, 2, 2, prec), sens=oracle_sensitivity(whole, 64, 2, 2, prec))
+                  calibrate(whole, 64, 2, 2, prec), sens=oracle_sensitivity(whole, 64, 2, 2, prec),
+                  calib_factor=3.0 if prec == "bf16" else 2.0)
     assert not bad, bad
 
 
