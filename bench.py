@@ -55,25 +55,25 @@ def algorithmic(timer: str, cfg, E: int, No: int, Nh: int, lean: bool = False, s
             return by, E * 2 * l * l * (D + 2)
         if timer == "edge_bwd" and lean:
             # recompute the forward, then the data gradients of every layer
-            # and de^k = de^{k+1} + dz_0 W_e: read e^k, de^{k+1} (fp32), ids,
-            # node rows, dagg; write de^k, D output gradients and D-1 hidden
-            # activations, receiver sums of dz_0
-            by = E * (ts * l + 4 * l + 8 + 4 * l + (2 * D - 1) * ts * l) + Nl * ts * l + No * 4 * l * 2
+            # and de^k = de^{k+1} + dz_0 W_e: read e^k, de^{k+1} (storage
+            # type), ids, node rows, dagg; write de^k, D output gradients and
+            # D-1 hidden activations, receiver sums of dz_0
+            by = E * (ts * l + ts * l + 8 + ts * l + (2 * D - 1) * ts * l) + Nl * ts * l + No * 4 * l * 2
             return by, E * 4 * l * l * (D + 1)
         if timer == "edge_bwd":
             # from the forward's first-Linear ReLU output h_1: recompute the
             # later layers, then their data gradients and de^k = de^{k+1} +
-            # dz_0 W_e: read h_1, de^{k+1} (fp32), ids, dagg; write de^k, D
-            # output gradients and D-2 hidden activations, receiver sums
-            by = E * (ts * l + 4 * l + 8 + 4 * l + (2 * D - 2) * ts * l) + No * 4 * l * 2
+            # dz_0 W_e: read h_1, de^{k+1} (storage type), ids, dagg; write
+            # de^k, D output gradients and D-2 hidden activations, receiver sums
+            by = E * (ts * l + ts * l + 8 + ts * l + (2 * D - 2) * ts * l) + No * 4 * l * 2
             return by, E * 2 * l * l * (2 * D - 1)
         return None
     if timer == "edge_bwd":
-        # read e^k (bf16), de^{k+1} (fp32), receiver / sender ids, dagg rows,
+        # read e^k, de^{k+1} (bf16), receiver / sender ids, dagg rows (fp32),
         # node projections; write de^k, dy, dz_0, h_1 (bf16) and the
         # receiver sums of dz_0; with the stash: read h_1 instead of e^k,
         # no projections, no h_1 write, no W_e e
-        by = E * (2 * l + 4 * l + 8 + 4 * l + 3 * 2 * l) + No * l * 4 * 2 + Nl * 2 * l * 4
+        by = E * (2 * l + 2 * l + 8 + 2 * l + 3 * 2 * l) + No * l * 4 * 2 + Nl * 2 * l * 4
         by -= stash * (E * 2 * l + Nl * 2 * l * 4)
         return by, E * (4 - stash) * 2 * l * l
     if timer == "edge_fwd":
@@ -95,15 +95,16 @@ def step_roofline(cfg, E: int, No: int, ms: float) -> dict:
     edge-block, for kernels that fuse gather, MLP and scatter: flops per
     edge-block forward 2l^2(D+2) + 2l^2(D+1) No/E, forward + backward with
     recompute 4x that; HBM bytes per edge-block forward 2 l s_e + 4, backward
-    l s_e + 4 l s_g + 8 (s_e: bytes of a stored edge latent, s_g = 4: fp32
-    gradients), plus per node and block 40 l bytes (forward: v read, agg
+    l s_e + 4 l s_g + 8 (s_e: bytes of a stored edge latent, s_g: of a
+    stored edge gradient, both 2 in bf16, 4 in fp32), plus per node and
+    block 40 l bytes (forward: v read, agg
     written, v and agg read by the node MLP, v written; backward: v, agg
     and dv read, dv and dagg written), spread over E/No edges.  Roof time =
     the larger of flops / matrix peak and bytes / HBM peak."""
     l, D, K = cfg.latent, cfg.depth, cfg.K
     se = 2 if cfg.precision == "bf16" else 4
     fl = 4 * (2 * l * l * (D + 2) + 2 * l * l * (D + 1) * No / E)
-    by = (2 * l * se + 4) + (l * se + 4 * l * 4 + 8) + 40 * l * No / E
+    by = (2 * l * se + 4) + (l * se + 4 * l * se + 8) + 40 * l * No / E
     peak_flops = PEAK["bf16"] if cfg.precision == "bf16" else PEAK["fp32"]
     t_fl, t_by = fl * E * K / peak_flops, by * E * K / PEAK["hbm"]
     roof_s = max(t_fl, t_by)

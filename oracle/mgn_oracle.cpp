@@ -502,7 +502,8 @@ int orc_step(const orc_cfg* c, int64_t n_owned, int64_t n_halo, int64_t n_edges,
       mlp_forward(M.edge[k], Q, c->ln_eps, x.data(), y.data(), t);
       mlp_backward(M.edge[k], Q, t, dm.data(), dx.data(), g);
       for (int i = 0; i < l; ++i) {
-        de_next[ed * l + i] = de[ed * l + i] + dx[i];
+        // e^k is stored in bf16 in mixed precision, and so is its gradient
+        de_next[ed * l + i] = Q.r(de[ed * l + i] + dx[i]);
         dxs[ed * l + i] = dx[l + i];
         dxr[ed * l + i] = dx[2 * l + i];
       }

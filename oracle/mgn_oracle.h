@@ -33,9 +33,12 @@ extern "C" {
  * activations and weights, and every backward gradient that feeds a matrix
  * product, are rounded to bfloat16 (as binary32 values, then to nearest
  * with 8 significant bits, ties to even) before the
- * product; the edge-latent stream is stored rounded; biases, LayerNorm, the
- * node-latent stream, every sum and every bias / LayerNorm gradient stay in
- * full precision.  bf16 == 0: float64 throughout. */
+ * product; the edge-latent stream is stored rounded, and so is its gradient
+ * dL/de^k (the sum of the residual's and the MLP input's contributions,
+ * rounded once per block, as the gradient of a bfloat16 tensor is itself
+ * bfloat16); biases, LayerNorm, the node-latent stream and its gradient,
+ * every other sum and every bias / LayerNorm gradient stay in full
+ * precision.  bf16 == 0: float64 throughout. */
 typedef struct {
   int32_t latent, n_blocks, depth, node_in, edge_in, node_out;
   double ln_eps;

@@ -285,7 +285,7 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.DV[1] = take(4 * (size_t)no * L);
   p.DAGG = take(4 * (size_t)no * L);
   p.DZS = take(4 * (size_t)nl * L);
-  p.DE = take(4 * (size_t)ne * L);  // dL/de, updated in place block by block
+  p.DE = take(ts * (size_t)ne * L);  // dL/de in the storage type, updated in place block by block
   for (int j = 0; j < 3; ++j) p.DEL_E[j] = j < m->D ? take(ts * (size_t)emax * L) : 0;
   for (int j = 0; j < 2; ++j) p.HID_E[j] = j < m->D - 1 ? take(ts * (size_t)emax * L) : 0;
   for (int j = 0; j < 3; ++j) p.DEL_N[j] = j < m->D ? take(ts * (size_t)no * std::max<int64_t>(L, 16)) : 0;
@@ -859,7 +859,8 @@ struct Bwd {
   int L, K, D;
   size_t ts;
   float* DV[2];
-  float *DE, *DAGG, *DZS, *VP;
+  void* DE;  // dL/de in the storage type
+  float *DAGG, *DZS, *VP;
   int32_t* erecv;
   void *DEL_N[3], *HID_N[2], *DEL_E[3], *HID_E[2];
   float* d_params;
@@ -871,7 +872,7 @@ struct Bwd {
         D(m_->D), ts(b.ts), d_params(m_->d_params), accumulate(m_->accumulate) {
     DV[0] = (float*)(ws + p.DV[0]);
     DV[1] = (float*)(ws + p.DV[1]);
-    DE = (float*)(ws + p.DE);
+    DE = ws + p.DE;
     DAGG = (float*)(ws + p.DAGG);
     DZS = (float*)(ws + p.DZS);
     VP = (float*)(ws + p.VPART);
@@ -1159,7 +1160,9 @@ struct Bwd {
         RowsBwdArgs a = rows_args(ml, rows, DEL_E, HID_E);
         a.in0 = m->ef + (size_t)e0 * m->cfg.edge_in;
         a.fin = m->cfg.edge_in;
-        a.dm = DE + (size_t)e0 * L;  // dL/de^0 (block 0 wrote it in plain column order)
+        // dL/de^0 (block 0 wrote it in plain column order, in the storage type)
+        if (m->prec == BF16) a.dm16 = (const uint16_t*)DE + (size_t)e0 * L;
+        else a.dm = (const float*)DE + (size_t)e0 * L;
         // narrow features: the kernel forms the first Linear's weight
         // gradient itself (per-wave partials) instead of storing dz_0
         const int w1s = rows > 0 ? rows_rt_w1_parts(m->prec, L, D, ENC_EDGE, a.fin) : 0;

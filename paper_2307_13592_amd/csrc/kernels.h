@@ -55,6 +55,7 @@ struct RowsBwdArgs {
   const void* in0_16;  // NODE / DEC: bf16 rows [rows][L] read instead of in0 when set
   const void* hid_in;  // NODE, bf16 T-form kernel: the forward's first-Linear ReLU output [rows][L]
   const float* dm;   // gradient w.r.t. the MLP output (LN output; dOut for the decoder)
+  const uint16_t* dm16;  // ENC_EDGE in bf16 mode: that gradient as bf16 rows [rows][L] (dL/de^0), read instead of dm
   float* dx0;        // NODE: dv^k owned part (= dm + dX_v); DEC: dv^K
   float* dx1;        // NODE: d agg
   void* delta[3];    // storage type [rows][L]: gradient at each Linear's output
@@ -78,9 +79,9 @@ struct EdgeBwdArgs {
   const void* V16;
   int64_t n_owned;
   const void* Ein;      // e^k (storage type)
-  const float* de_next; // dL/de^{k+1} [E][L] or null (last block)
+  const void* de_next;  // dL/de^{k+1} [E][L] in the storage type (bf16 in bf16 mode), or null (last block)
   float* dagg;          // [n_owned][L]: dL/dagg in; each receiver's sum of dz_0 out
-  float* de_out;        // dL/de^k [E][L]
+  void* de_out;         // dL/de^k [E][L] in the storage type (may alias de_next: each row is read before it is written)
   const float* proj;    // node projections [n_local][2L] (row-split kernels), else unused
   const void* hid_in;   // streaming and row-split kernels: the forward's first-Linear ReLU output [E][L] (then layer 1 is not
                         // recomputed and hid[0] is not written), or null

@@ -848,7 +848,7 @@ __global__ __launch_bounds__(NT) void rows_bwd_kernel(RowsBwdArgs a) {
         if constexpr (KIND == DECODER) {
           if (c < a.fout) v = a.dm[(row0 + r) * a.fout + c];
         } else {
-          v = a.dm[(row0 + r) * L + c];
+          v = a.dm16 ? bf2f(a.dm16[(row0 + r) * L + c]) : a.dm[(row0 + r) * L + c];
         }
       }
       DM[r * Lay::LDM + c] = v;
@@ -1361,7 +1361,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
 #pragma unroll
           for (int nn = 0; nn < NBW; ++nn) {
             const int col = (nb0 + nn) * 16 + acc_col();
-            de[m][nn][r] = (ok && a.de_next) ? a.de_next[(sb + row) * L + col] : 0.f;
+            de[m][nn][r] = (ok && a.de_next) ? P::tof(reinterpret_cast<const T*>(a.de_next)[(sb + row) * L + col]) : 0.f;
             da[m][nn][r] = ok ? a.dagg[rv * L + col] : 0.f;
           }
         }
@@ -1510,7 +1510,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
             if (row < n) {
 #pragma unroll
               for (int nn = 0; nn < NBW; ++nn)
-                a.de_out[(sb + row) * L + (nb0 + nn) * 16 + acc_col()] = acc[m][nn][r] + de[m][nn][r];
+                reinterpret_cast<T*>(a.de_out)[(sb + row) * L + (nb0 + nn) * 16 + acc_col()] =
+                    P::cvt(acc[m][nn][r] + de[m][nn][r]);
             }
           }
       }
@@ -2388,8 +2389,16 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
         d4[cb] = make_float4(0.f, 0.f, 0.f, 0.f);
       }
       if (a.de_next) {
+        // bf16 row, plain order: one 16-byte chunk per k-group -> T order
+        const uint16_t* dp = reinterpret_cast<const uint16_t*>(a.de_next) + er * L;
 #pragma unroll
-        for (int cb = 0; cb < NB; ++cb) d4[cb] = rt_ld4(a.de_next + er * L, cb, q);
+        for (int kg = 0; kg < NKH; ++kg) {
+          const uint4 t = rt_from_plain(*reinterpret_cast<const uint4*>(dp + kg * 32 + q * 8));
+          d4[2 * kg] = make_float4(__uint_as_float(t.x << 16), __uint_as_float(t.x & 0xffff0000u),
+                                   __uint_as_float(t.y << 16), __uint_as_float(t.y & 0xffff0000u));
+          d4[2 * kg + 1] = make_float4(__uint_as_float(t.z << 16), __uint_as_float(t.z & 0xffff0000u),
+                                       __uint_as_float(t.w << 16), __uint_as_float(t.w & 0xffff0000u));
+        }
       }
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
@@ -2485,22 +2494,23 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
       rt_frags<NB>(v, gf);
       rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + srow, q, gf, ok);
     }
-    // edge-stream gradient: de^k = de^{k+1} + dz_0 W_1[:, e-block]
+    // edge-stream gradient: de^k = de^{k+1} + dz_0 W_1[:, e-block], summed
+    // in fp32 and stored as bf16 (the gradient of the bf16 edge stream)
     {
       floatx4 acc[NB];
       rt_gemm<NB, NKH>(W1b, gf, acc, ln);
+      uint4 o[NKH];
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb) {
-        acc[cb][0] += d4[cb].x;
-        acc[cb][1] += d4[cb].y;
-        acc[cb][2] += d4[cb].z;
-        acc[cb][3] += d4[cb].w;
+      for (int kg = 0; kg < NKH; ++kg) {
+        const floatx4 a0 = acc[2 * kg], a1 = acc[2 * kg + 1];
+        const float4 d0 = d4[2 * kg], d1 = d4[2 * kg + 1];
+        o[kg] = rt_to_plain(make_uint4(bf_pack(a0[0] + d0.x, a0[1] + d0.y), bf_pack(a0[2] + d0.z, a0[3] + d0.w),
+                                       bf_pack(a1[0] + d1.x, a1[1] + d1.y), bf_pack(a1[2] + d1.z, a1[3] + d1.w)));
       }
       if (ok) {
-        float* op = a.de_out + (sb + e) * L;
+        uint16_t* op = reinterpret_cast<uint16_t*>(a.de_out) + (sb + e) * L;
 #pragma unroll
-        for (int cb = 0; cb < NB; ++cb)
-          *reinterpret_cast<float4*>(op + cb * 16 + q * 4) = make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
+        for (int kg = 0; kg < NKH; ++kg) *reinterpret_cast<uint4*>(op + kg * 32 + q * 8) = o[kg];
       }
     }
     // receiver sums of dz_0 (bf16, as it fed the products), ascending edge
@@ -2754,7 +2764,10 @@ __global__ __launch_bounds__(RS_NTH) void rows_bwd_rs_kernel(RowsBwdArgs a) {
     for (int r = 0; r < 4; ++r) {
       const int row = (ln >> 4) * 4 + r;
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb) dm[cb][r] = row < n ? a.dm[(row0 + row) * L + cb * 16 + (ln & 15)] : 0.f;
+      for (int cb = 0; cb < NB; ++cb) {
+        const int64_t i = (row0 + row) * L + cb * 16 + (ln & 15);
+        dm[cb][r] = row < n ? (a.dm16 ? bf2f(a.dm16[i]) : a.dm[i]) : 0.f;
+      }
     }
     float mu[4], rs[4], t1[4], t2[4];
     rs_row_totals<NB>(y, mu);
@@ -3137,13 +3150,27 @@ __global__ __launch_bounds__((RtRowsLay<L, KIND>::NTH)) void rows_rt_bwd_kernel(
       }
     }
     float dm[NB][4];
+    if (a.dm16) {
+      // bf16 rows (dL/de^0 of the bf16 edge stream), plain order -> T order
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-      const float4 d4 = rt_ld4(a.dm + src * L, cb, q);
-      dm[cb][0] = ok ? d4.x : 0.f;
-      dm[cb][1] = ok ? d4.y : 0.f;
-      dm[cb][2] = ok ? d4.z : 0.f;
-      dm[cb][3] = ok ? d4.w : 0.f;
+      for (int kg = 0; kg < NKH; ++kg) {
+        const uint4 t = rt_from_plain(*reinterpret_cast<const uint4*>(a.dm16 + src * L + kg * 32 + q * 8));
+        const uint32_t w[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {  // dword i: block 2 kg + i / 2, columns 2 (i % 2) .. + 1
+          dm[2 * kg + i / 2][2 * (i % 2)] = ok ? __uint_as_float(w[i] << 16) : 0.f;
+          dm[2 * kg + i / 2][2 * (i % 2) + 1] = ok ? __uint_as_float(w[i] & 0xffff0000u) : 0.f;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float4 d4 = rt_ld4(a.dm + src * L, cb, q);
+        dm[cb][0] = ok ? d4.x : 0.f;
+        dm[cb][1] = ok ? d4.y : 0.f;
+        dm[cb][2] = ok ? d4.z : 0.f;
+        dm[cb][3] = ok ? d4.w : 0.f;
+      }
     }
     // LayerNorm (recomputed): y becomes xhat
     const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;

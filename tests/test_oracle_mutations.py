@@ -37,6 +37,8 @@ MUTATIONS = {
                           "d[a] = (coords[3 * (int64_t)recv[e] + a] - coords[3 * (int64_t)send[e] + a]) / h;"),
     "halo_grad_dropped": ("for (int i = 0; i < l; ++i) dh[i] += dxs[ed * l + i];", "(void)dh;"),
     "halo_ordered_after_owned_wrongly": ("if (is_halo[g]) g2l[g] = next++;", "if (is_halo[g]) g2l[g] = next++ ^ 1;"),
+    "edge_gradient_not_rounded_in_bf16": ("de_next[ed * l + i] = Q.r(de[ed * l + i] + dx[i]);",
+                                          "de_next[ed * l + i] = de[ed * l + i] + dx[i];"),
 }
 
 
@@ -59,6 +61,14 @@ def _pins_pass():
         out, dp, dh = torch_ref.run(8, 2, 3, c["shapes"], g, c["params"], c["nf"], c["ef"], c["halo"], c["d_out"])
         if not (np.allclose(r["out"], out, atol=1e-10) and np.allclose(r["d_params"], dp, atol=1e-9)
                 and np.allclose(r["d_halo"], dh, atol=1e-9)):
+            return False
+        # the mixed-precision mode against torch's bfloat16 rounding at the same points
+        cb = oracle.ModelCfg(8, 2, 3, bf16=True)
+        rb = oracle.step(cb, g, c["params"], c["nf"], c["ef"], c["halo"], c["d_out"])
+        out, dp, dh = torch_ref.run(8, 2, 3, c["shapes"], g, c["params"], c["nf"], c["ef"], c["halo"], c["d_out"],
+                                    bf16=True)
+        if not (np.allclose(rb["out"], out, atol=1e-10) and np.allclose(rb["d_params"], dp, atol=1e-9)
+                and np.allclose(rb["d_halo"], dh, atol=1e-9)):
             return False
         m = meshes.sector(4, 12, 5, 4, seed=1)
         if not np.allclose(oracle.edge_features(m.coords, m.send, m.recv, m.h),

@@ -36,7 +36,9 @@ class _LinearBf16(torch.autograd.Function):
 
 
 class _RoundBf16(torch.autograd.Function):
-    """Storage rounding of the edge-latent stream (gradient passes through)."""
+    """Storage rounding of the edge-latent stream (gradient passes through;
+    the stream's own gradient is rounded by a hook on each stored tensor,
+    see TorchMGN.forward)."""
 
     @staticmethod
     def forward(ctx, x):
@@ -112,7 +114,16 @@ class TorchMGN(nn.Module):
     def forward(self, g, node_feat, edge_feat, halo, bf16=False):
         """g: partition-local graph (row_ptr, send, n_owned, n_halo).  halo:
         tensor [K, n_halo, l] (requires_grad for d_halo)."""
-        R = (lambda x: _RoundBf16.apply(x)) if bf16 else (lambda x: x)
+        def R(x):
+            if not bf16:
+                return x
+            y = _RoundBf16.apply(x)
+            if y.requires_grad:
+                # a bfloat16 tensor's gradient is bfloat16: the total gradient
+                # of the stored edge latents (residual path plus MLP input)
+                # is rounded once before it flows on
+                y.register_hook(_bf16)
+            return y
         no, nh = g["n_owned"], g["n_halo"]
         row_ptr = np.asarray(g["row_ptr"], np.int64)
         recv = torch.as_tensor(np.repeat(np.arange(no), np.diff(row_ptr)), dtype=torch.long)
