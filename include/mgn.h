@@ -236,6 +236,22 @@ mgn_status mgn_workspace_size(const mgn_model* m, const mgn_graph* g, size_t* by
 mgn_status mgn_forward(mgn_model* m, const mgn_graph* g, const float* node_feat, const float* edge_feat,
                        const float* halo, float* out, void* workspace, size_t ws_bytes, mgn_stream stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): mgn_forward with
+ * its workspace in a library-owned static device array of
+ * MGN_NOALLOC_WS_MAX bytes, one per GPU, held until the process ends.  Same
+ * arguments as mgn_forward without workspace / ws_bytes; same launches and
+ * results.  Allocates nothing (no hipMalloc, no events).  Errors:
+ * MGN_E_NOMEM when mgn_workspace_size for (m, g) exceeds
+ * MGN_NOALLOC_WS_MAX (nothing is enqueued); MGN_E_STATE when launch timing
+ * is on; otherwise as mgn_forward.  Every call on one GPU uses that GPU's one
+ * array, which keeps the last call's contents: calls (from any model) that
+ * overlap on one GPU race, and a later mgn_backward of this forward is valid
+ * only while no other call has used the array since. */
+#define MGN_NOALLOC_WS_MAX (128u << 20)
+mgn_status mgn_forward_noalloc(mgn_model* m, const mgn_graph* g, const float* node_feat, const float* edge_feat,
+                               const float* halo, float* out, mgn_stream stream);
+
 /* Backward pass of the last forward (Algorithm 1: Backprop of the loss
  * through DecNode, the K blocks in reverse and the encoders; section
  * "Methodology": the halo gradients are what the owners receive).

@@ -28,7 +28,7 @@ EXPORTS = ["mgn_create", "mgn_destroy", "mgn_last_error", "mgn_param_count", "mg
            "mgn_forward", "mgn_backward", "mgn_forward_begin", "mgn_forward_block", "mgn_forward_end",
            "mgn_backward_begin", "mgn_backward_block", "mgn_backward_end", "mgn_halo_masks", "mgn_copy_latents",
            "mgn_add_latent_grads", "mgn_lockstep_forward", "mgn_lockstep_backward", "mgn_mse_grad",
-           "mgn_mse_grad_global", "mgn_timing_enable", "mgn_timing_read"]
+           "mgn_mse_grad_global", "mgn_timing_enable", "mgn_timing_read", "mgn_forward_noalloc"]
 TIMERS = ["encode", "edge_fwd", "node_fwd", "decode", "edge_bwd", "node_bwd", "input_grad", "weight_grad",
           "other", "node_proj", "exchange"]
 
@@ -89,6 +89,7 @@ def lib() -> C.CDLL:
             "mgn_workspace_size": (C.c_int, [vp, vp, vp]),
             "mgn_forward": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]),
             "mgn_backward": (C.c_int, [vp, vp, vp, C.c_int, vp, vp]),
+            "mgn_forward_noalloc": (C.c_int, [vp, vp, vp, vp, vp, vp, vp]),
             "mgn_forward_begin": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]),
             "mgn_forward_block": (C.c_int, [vp, vp]),
             "mgn_forward_end": (C.c_int, [vp, vp]),
@@ -310,6 +311,16 @@ def mgn_forward(model, graph: mgn_graph, node_feat, edge_feat, halo, out, worksp
     _check(lib().mgn_forward(model, C.byref(graph), _dev(node_feat), _dev(edge_feat), _dev(halo), _dev(out),
                              _dev(workspace), workspace.numel() * workspace.element_size(), _stream(stream)),
            model)
+
+
+MGN_NOALLOC_WS_MAX = 128 << 20
+
+
+def mgn_forward_noalloc(model, graph: mgn_graph, node_feat, edge_feat, halo, out, stream=None) -> None:
+    """mgn_forward with the library's static per-GPU workspace (no caller
+    workspace, no allocation)."""
+    _check(lib().mgn_forward_noalloc(model, C.byref(graph), _dev(node_feat), _dev(edge_feat), _dev(halo), _dev(out),
+                                     _stream(stream)), model)
 
 
 def mgn_backward(model, d_out, d_params, accumulate: bool = False, d_halo=None, stream=None) -> None:

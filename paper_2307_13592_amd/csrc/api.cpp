@@ -120,6 +120,13 @@ mgn_status hip_fail(mgn_model* m, hipError_t e, const char* what) {
   return fail(m, MGN_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+}  // namespace
+
+mgn_status mgn::set_error(mgn_model* m, mgn_status s, const std::string& msg) { return fail(m, s, msg); }
+bool mgn::timing_enabled(const mgn_model* m) { return m && m->timing; }
+
+namespace {
+
 // Refreshes the packed copies of every Linear's weights from the fp32 master copy.
 hipError_t repack(mgn_model* m, hipStream_t st) {
   for (const MlpL& ml : m->mlp)
