@@ -2637,6 +2637,795 @@ __device__ __forceinline__ void rs_gemm_g(const uint4 (&A)[NKG], const uint4* __
   }
 }
 
+// ------------------------------------ streamed-weight T-form kernels, l = 256 ---
+// bf16, latent 256.  One l x l bf16 layer is 128 KB, so the per-edge layers
+// cannot all sit in LDS as in the row-split kernels above.  Instead each
+// layer's packed fragments are streamed through LDS in chunks of four
+// 16-column blocks x every k-group (32 KB, double-buffered): the
+// workgroup's waves step through the chunks together, one barrier per
+// chunk, and each wave applies every chunk to its own tile of NS x 16 edges
+// (T form as above: the fragments are the MFMA A operand, the tile the B
+// operand, and one layer's accumulators rounded to bf16 are the next
+// layer's B operand as they stand).  A thread loads its share of the chunk
+// after next from L2 into registers before the current chunk's products and
+// writes the next chunk's share to LDS, so the stream overlaps the MFMAs.
+// A chunk of a layer covers column blocks 4c .. 4c + 3 over every k-group,
+// so those output columns are complete after it: bias, projections and
+// ReLU are applied chunk by chunk.  The sequence of chunks is the same for
+// every tile (the block's weights), so the stream runs on across tiles.
+
+constexpr int RW_L = 256;                          // latent width of these kernels
+constexpr int RW_NB = RW_L / 16;                   // 16-column blocks of a layer
+constexpr int RW_NKH = RW_L / 32;                  // k-groups of an l-wide input
+constexpr int RW_CB = 4;                           // column blocks per chunk
+constexpr int RW_NC = RW_NB / RW_CB;               // chunks per layer
+constexpr int RW_CHUNK = RW_CB * RW_NKH * 64;      // uint4 per chunk (32 KB)
+
+// One layer's fragments in the stream: packed [cb][src_nkg][64 lanes],
+// k-groups kg0 .. kg0 + RW_NKH - 1 of each column block.
+struct RwSrc {
+  const uint4* frags;
+  int src_nkg, kg0;
+};
+
+// A thread's share of one chunk, held in registers between its load from
+// L2 and its copy to LDS.  PERM: k-slots permuted for a B operand in
+// accumulator (T) order, as rt_copy_frags does; else plain (B from rows).
+template <int NTH>
+struct RwStage {
+  uint4 v[RW_CHUNK / NTH];
+};
+template <int NTH, bool PERM>
+__device__ __forceinline__ void rw_load(RwStage<NTH>& s, const RwSrc src, int c) {
+  // an opaque copy of the thread index: the addresses are recomputed at
+  // every call instead of being hoisted out of the tile loop (dozens of
+  // 64-bit pointers, one set per chunk position, would stay live); 32-bit
+  // byte offsets from the uniform base
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const char* base = reinterpret_cast<const char*>(src.frags);
+#pragma unroll
+  for (int j = 0; j < RW_CHUNK / NTH; ++j) {
+    const int i = tid + j * NTH;
+    const int cbl = i / (RW_NKH * 64), kg = (i / 64) % RW_NKH, ln = i % 64;
+    const uint32_t f = (uint32_t)(((c * RW_CB + cbl) * src.src_nkg + src.kg0 + kg) * 64) * 16u;
+    if constexpr (PERM) {
+      const int q = ln >> 4, cc = ln & 15;
+      const uint2 lo = *reinterpret_cast<const uint2*>(base + f + (uint32_t)((cc + 16 * (q >> 1)) * 2 + (q & 1)) * 8u);
+      const uint2 hi =
+          *reinterpret_cast<const uint2*>(base + f + (uint32_t)((cc + 16 * (2 + (q >> 1))) * 2 + (q & 1)) * 8u);
+      s.v[j] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+    } else {
+      s.v[j] = *reinterpret_cast<const uint4*>(base + f + (uint32_t)ln * 16u);
+    }
+  }
+}
+template <int NTH>
+__device__ __forceinline__ void rw_store(const RwStage<NTH>& s, uint4* buf) {
+#pragma unroll
+  for (int j = 0; j < RW_CHUNK / NTH; ++j) buf[(int)threadIdx.x + j * NTH] = s.v[j];
+}
+
+// acc[s][4 c + cbl] = sum over k-groups of the chunk's fragments (LDS) times
+// X[s][kg], for the NS 16-edge sub-tiles of the wave.  The fragments of
+// k-group kg + RW_PF are read while the products of k-group kg are issued,
+// so the LDS latency hides behind RW_PF k-groups of products.
+#ifndef RW_PF
+#define RW_PF 2
+#endif
+template <int NS>
+__device__ __forceinline__ void rw_gemm(int C, const uint4* buf, const uint4 (&X)[NS][RW_NKH],
+                                        floatx4 (&acc)[NS][RW_NB], int lane) {
+  constexpr int PF = RW_PF;
+#pragma unroll
+  for (int cbl = 0; cbl < RW_CB; ++cbl)
+#pragma unroll
+    for (int s = 0; s < NS; ++s) acc[s][C * RW_CB + cbl] = floatx4{0.f, 0.f, 0.f, 0.f};
+  uint4 w[PF + 1][RW_CB];
+#pragma unroll
+  for (int kg = 0; kg < PF; ++kg)
+#pragma unroll
+    for (int cbl = 0; cbl < RW_CB; ++cbl) w[kg][cbl] = buf[(cbl * RW_NKH + kg) * 64 + lane];
+#pragma unroll
+  for (int kg = 0; kg < RW_NKH; ++kg) {
+    if (kg + PF < RW_NKH) {
+#pragma unroll
+      for (int cbl = 0; cbl < RW_CB; ++cbl) w[(kg + PF) % (PF + 1)][cbl] = buf[(cbl * RW_NKH + kg + PF) * 64 + lane];
+    }
+#pragma unroll
+    for (int cbl = 0; cbl < RW_CB; ++cbl)
+#pragma unroll
+      for (int s = 0; s < NS; ++s) PBF16::mma(acc[s][C * RW_CB + cbl], w[kg % (PF + 1)][cbl], X[s][kg]);
+  }
+}
+
+// bf16 plain-order 16-byte chunk (8 columns) -> its T-order values: cb 2 kg
+// gets .x/.y, cb 2 kg + 1 gets .z/.w (columns 4 q + r of each block).
+__device__ __forceinline__ void rw_unpack(const uint4 p, float (&lo)[4], float (&hi)[4]) {
+  const uint4 t = rt_from_plain(p);
+  lo[0] = __uint_as_float(t.x << 16);
+  lo[1] = __uint_as_float(t.x & 0xffff0000u);
+  lo[2] = __uint_as_float(t.y << 16);
+  lo[3] = __uint_as_float(t.y & 0xffff0000u);
+  hi[0] = __uint_as_float(t.z << 16);
+  hi[1] = __uint_as_float(t.z & 0xffff0000u);
+  hi[2] = __uint_as_float(t.w << 16);
+  hi[3] = __uint_as_float(t.w & 0xffff0000u);
+}
+
+// Largest tile count over the workgroup's waves (every wave must take part
+// in every chunk step of the stream).
+__device__ __forceinline__ int rw_max_tiles(int mine, int* slot) {
+  const int wave = wave_id(), nwv = blockDim.x >> 6;
+  if ((threadIdx.x & 63) == 0) slot[wave] = mine;
+  __syncthreads();
+  int t = 0;
+  for (int w = 0; w < nwv; ++w) t = slot[w] > t ? slot[w] : t;
+  return t;
+}
+
+template <int D, int NS, int NWV>
+struct RwFwdLay {
+  static constexpr int NTH = 64 * NWV;
+  static constexpr int TE = 16 * NS;                       // edges per wave and tile
+  static constexpr int OFF_BUF = 0;                        // two chunk buffers
+  static constexpr int OFF_VEC = 2 * RW_CHUNK * 16;        // last bias, gamma, beta[, hidden bias]
+  static constexpr int NVEC = (D == 3 ? 4 : 3) * RW_L;
+  static constexpr int OFF_SCR = OFF_VEC + NVEC * 4;
+  static constexpr int SCR = 16 * 64 * 4;                  // per wave: 16 rows x 64 fp32 columns
+  static constexpr int OFF_SLOT = OFF_SCR + NWV * SCR;
+  static constexpr int END = OFF_SLOT + 64;
+  static_assert(END <= 160 * 1024, "LDS");
+  static constexpr int NCH = D * RW_NC;                    // chunks per tile
+  static_assert(NCH % 2 == 0, "the stream's buffer parity repeats every tile");
+};
+
+// Forward of one block's edge half (l = 256, bf16): z_1 = W_e e + P_s[s] +
+// P_r[r] (P = node projections with b_1 in the receiver half), ReLU,
+// [W_h, ReLU,] W_last, LayerNorm; e^{k+1} = e^k + m; agg = ordered receiver
+// sums of m; optionally h_1 kept for the backward.
+template <int D, int NS, int NWV>
+__global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV == 4 ? 1 : 2, NWV == 4 ? 1 : 2)))
+void edge_fwd_rw_kernel(EdgeFwdArgs a) {
+  using Lay = RwFwdLay<D, NS, NWV>;
+  constexpr int NTH = Lay::NTH, NB = RW_NB, NKH = RW_NKH, L = RW_L, TE = Lay::TE;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* buf = reinterpret_cast<uint4*>(lds + Lay::OFF_BUF);
+  float* vbl = reinterpret_cast<float*>(lds + Lay::OFF_VEC);  // last bias
+  float* vg = vbl + L;                                          // gamma
+  float* vbt = vbl + 2 * L;                                     // beta
+  float* vbh = vbl + 3 * L;                                     // hidden bias (D = 3)
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  float* scr32 = reinterpret_cast<float*>(lds + Lay::OFF_SCR + wave * Lay::SCR);
+  const RwSrc src[3] = {{a.mlp.lin[0].wf, 3 * NKH, 0}, {a.mlp.lin[1].wf, NKH, 0}, {a.mlp.lin[D - 1].wf, NKH, 0}};
+  // stream position p (chunk p % NCH of a tile): layer p / RW_NC (0: first,
+  // D - 1: last), chunk p % RW_NC; only the first layer's B operand is plain
+  auto load = [&](RwStage<NTH>& st, int p) {
+    const int pp = p % Lay::NCH, j = pp / RW_NC, c = pp % RW_NC;
+    if (j == 0) rw_load<NTH, false>(st, src[0], c);
+    else rw_load<NTH, true>(st, src[j == D - 1 ? 2 : 1], c);
+  };
+  RwStage<NTH> stg;
+  load(stg, 0);
+  rw_store<NTH>(stg, buf);
+  load(stg, 1);
+  rt_copy_vec(vbl, a.mlp.lin[D - 1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  rt_copy_vec(vbt, a.mlp.beta, L);
+  if constexpr (D == 3) rt_copy_vec(vbh, a.mlp.lin[1].b, L);
+  int64_t r0, r1;
+  rs_range(a.row_ptr, 0, a.n_owned, r0, r1);
+  rs_zero_empty(a.row_ptr, r0, r1, a.agg, L);
+  const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
+  const int ntile = rw_max_tiles((int)((E1 - E0 + TE - 1) / TE), reinterpret_cast<int*>(lds + Lay::OFF_SLOT));
+  const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
+  uint16_t* Eout = reinterpret_cast<uint16_t*>(a.Eout);
+  float run[L / 64] = {};  // running receiver sums, columns lane + 64 j
+  // one step of the stream: the next chunk's share to LDS, the one after
+  // into registers (the barrier ending the previous step freed that buffer)
+  auto advance = [&](int p) {
+    rw_store<NTH>(stg, buf + ((p + 1) & 1) * RW_CHUNK);
+    load(stg, p + 2);
+  };
+  for (int t = 0; t < ntile; ++t) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t sb0 = E0 + (int64_t)t * TE;
+    const bool active = sb0 < E1;  // wave-uniform
+    RsMeta mt[NS];
+    bool ok[NS];
+    uint4 xf[NS][NKH];  // B operand: e^k rows, then h_1 (, h_2)
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const int64_t sb = sb0 + 16 * s;
+      ok[s] = active && sb + e < E1;
+      mt[s] = rt_meta_make(rt_meta_load(a.erecv, a.send, active ? sb : E0, active ? E1 : E0));
+      const uint16_t* erow = Ein + (ok[s] ? sb + e : E0) * L;
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg)
+        xf[s][kg] = active ? *reinterpret_cast<const uint4*>(erow + kg * 32 + q * 8) : make_uint4(0, 0, 0, 0);
+    }
+    floatx4 acc[NS][NB];
+    // first layer: W_e e + P_s[s] + P_r[r], ReLU
+#pragma unroll
+    for (int c = 0; c < RW_NC; ++c) {
+      advance(c);
+      float4 ps[NS][RW_CB], pr[NS][RW_CB];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const float* sp = a.proj + (int64_t)(ok[s] ? mt[s].s : 0) * (2 * L);
+        const float* rp = a.proj + (int64_t)(ok[s] ? mt[s].r : 0) * (2 * L) + L;
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          ps[s][cbl] = active ? rt_ld4(sp, c * RW_CB + cbl, q) : make_float4(0.f, 0.f, 0.f, 0.f);
+          pr[s][cbl] = active ? rt_ld4(rp, c * RW_CB + cbl, q) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+      if (active) rw_gemm<NS>(c, buf + (c & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          floatx4& z = acc[s][c * RW_CB + cbl];
+          const float4 a4 = ps[s][cbl], b4 = pr[s][cbl];
+          z[0] = fmaxf((z[0] + a4.x) + b4.x, 0.f);
+          z[1] = fmaxf((z[1] + a4.y) + b4.y, 0.f);
+          z[2] = fmaxf((z[2] + a4.z) + b4.z, 0.f);
+          z[3] = fmaxf((z[3] + a4.w) + b4.w, 0.f);
+        }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[s][cb][r];
+      rt_frags<NB>(h, xf[s]);
+      if (a.hid_out && active)
+        rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid_out) + (sb0 + 16 * s + e) * L, q, xf[s], ok[s]);
+    }
+    if constexpr (D == 3) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(RW_NC + c);
+        if (active) rw_gemm<NS>(c, buf + ((RW_NC + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+          for (int cbl = 0; cbl < RW_CB; ++cbl) {
+            const float4 bv = rt_ld4(vbh, c * RW_CB + cbl, q);
+            floatx4& z = acc[s][c * RW_CB + cbl];
+            z[0] = fmaxf(z[0] + bv.x, 0.f);
+            z[1] = fmaxf(z[1] + bv.y, 0.f);
+            z[2] = fmaxf(z[2] + bv.z, 0.f);
+            z[3] = fmaxf(z[3] + bv.w, 0.f);
+          }
+        __syncthreads();
+      }
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        float h[NB][4];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) h[cb][r] = acc[s][cb][r];
+        rt_frags<NB>(h, xf[s]);
+      }
+    }
+    // last layer (+ bias)
+#pragma unroll
+    for (int c = 0; c < RW_NC; ++c) {
+      constexpr int P0 = (D - 1) * RW_NC;
+      advance(P0 + c);
+      if (active) rw_gemm<NS>(c, buf + ((P0 + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          const float4 bv = rt_ld4(vbl, c * RW_CB + cbl, q);
+          floatx4& z = acc[s][c * RW_CB + cbl];
+          z[0] += bv.x;
+          z[1] += bv.y;
+          z[2] += bv.z;
+          z[3] += bv.w;
+        }
+      __syncthreads();
+    }
+    if (!active) continue;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const int64_t sb = sb0 + 16 * s;
+      const int n = (int)(E1 - sb < 16 ? (E1 - sb > 0 ? E1 - sb : 0) : 16);
+      float y[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[cb][r] = acc[s][cb][r];
+      // LayerNorm: two-pass statistics of row e, then gamma * xhat + beta
+      const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
+      float dv[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d = y[cb][r] - mu;
+          dv[cb][r] = d * d;
+        }
+      const float rs = 1.0f / sqrtf(rt_sum4(rt_lane_sum<NB>(dv)) / L + a.eps);
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float4 g = rt_ld4(vg, cb, q), bt = rt_ld4(vbt, cb, q);
+        y[cb][0] = g.x * ((y[cb][0] - mu) * rs) + bt.x;
+        y[cb][1] = g.y * ((y[cb][1] - mu) * rs) + bt.y;
+        y[cb][2] = g.z * ((y[cb][2] - mu) * rs) + bt.z;
+        y[cb][3] = g.w * ((y[cb][3] - mu) * rs) + bt.w;
+      }
+      if (Eout) {
+        // e^{k+1} = e^k + m (e^k read again, plain order -> T order)
+        const uint16_t* erow = Ein + (ok[s] ? sb + e : E0) * L;
+        uint4 o[NKH];
+#pragma unroll
+        for (int kg = 0; kg < NKH; ++kg) {
+          float lo[4], hi[4];
+          rw_unpack(*reinterpret_cast<const uint4*>(erow + kg * 32 + q * 8), lo, hi);
+          const float* m0 = y[2 * kg];
+          const float* m1 = y[2 * kg + 1];
+          o[kg] = rt_to_plain(make_uint4(bf_pack(lo[0] + m0[0], lo[1] + m0[1]), bf_pack(lo[2] + m0[2], lo[3] + m0[3]),
+                                         bf_pack(hi[0] + m1[0], hi[1] + m1[1]), bf_pack(hi[2] + m1[2], hi[3] + m1[3])));
+        }
+        if (ok[s]) {
+          uint16_t* orow = Eout + (sb + e) * L;
+#pragma unroll
+          for (int kg = 0; kg < NKH; ++kg) *reinterpret_cast<uint4*>(orow + kg * 32 + q * 8) = o[kg];
+        }
+      }
+      // ordered receiver sums, 64 columns at a time through the wave's
+      // scratch tile; a segment's total goes out at its last row
+#pragma unroll
+      for (int j = 0; j < L / 64; ++j) {
+        const int cc = ln + 64 * j;
+#pragma unroll
+        for (int cb = 4 * j; cb < 4 * j + 4; ++cb)
+          *reinterpret_cast<float4*>(scr32 + rs_sw32<64>(e, (cb - 4 * j) * 16 + q * 4)) =
+              make_float4(y[cb][0], y[cb][1], y[cb][2], y[cb][3]);
+        float x[16];
+#pragma unroll
+        for (int row = 0; row < 16; ++row) x[row] = scr32[rs_sw32<64>(row, ln)];
+#pragma unroll
+        for (int row = 0; row < 16; ++row) {
+          if (row < n) {
+            run[j] += x[row];
+            if ((mt[s].last >> row) & 1ull) {
+              a.agg[(int64_t)__builtin_amdgcn_readlane(mt[s].r, row) * L + cc] = run[j];
+              run[j] = 0.f;
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+
+template <int D, bool STASH, int NWV_>
+struct RwBwdLay {
+  static constexpr int NWV = NWV_, NTH = 64 * NWV;
+  static constexpr int OFF_BUF = 0;                        // two chunk buffers
+  static constexpr int OFF_VEC = 2 * RW_CHUNK * 16;        // last bias, gamma[, hidden bias]
+  static constexpr int OFF_SCR = OFF_VEC + (D == 3 ? 3 : 2) * RW_L * 4;
+  static constexpr int SCR = 16 * 64 * 2;                  // per wave: 16 rows x 64 bf16 columns
+  static constexpr int OFF_SLOT = OFF_SCR + NWV * SCR;
+  static constexpr int END = OFF_SLOT + 64;
+  static_assert(END <= 160 * 1024, "LDS");
+  static constexpr int NVEC = (D + 2) * RW_L;              // hidden biases, last bias, gamma, beta
+  static_assert(NWV * NVEC * 4 <= OFF_VEC, "the partials reuse the chunk buffers");
+  // forward layers streamed (the first only when it is recomputed), then
+  // the backward products of layers D-1 .. 0
+  static constexpr int NFL = STASH ? D - 1 : D;
+  static constexpr int NCH = (NFL + D) * RW_NC;
+  static_assert(NCH % 2 == 0, "the stream's buffer parity repeats every tile");
+};
+
+// A stored bf16 ReLU output row (plain order) as T-order B fragments, and
+// its ReLU mask (bit 4 cb + r set where the value is positive).
+__device__ __forceinline__ void rw_load_relu(const uint16_t* __restrict__ hp, int q, uint4 (&hf)[RW_NKH],
+                                             uint64_t& mask) {
+#pragma unroll
+  for (int kg = 0; kg < RW_NKH; ++kg) {
+    hf[kg] = rt_from_plain(*reinterpret_cast<const uint4*>(hp + kg * 32 + q * 8));
+    const uint32_t w[4] = {hf[kg].x, hf[kg].y, hf[kg].z, hf[kg].w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {  // dword i: block 2 kg + i / 2, rows r = 2 (i % 2) .. + 1
+      const int cb = 2 * kg + i / 2, r = 2 * (i % 2);
+      mask |= (uint64_t)((w[i] & 0x7fffu) != 0u && !(w[i] & 0x8000u)) << (cb * 4 + r);
+      mask |= (uint64_t)(((w[i] >> 16) & 0x7fffu) != 0u && !(w[i] & 0x80000000u)) << (cb * 4 + r + 1);
+    }
+  }
+}
+
+// Backward of one block's edge half, l = 256, bf16, weights streamed as in
+// edge_fwd_rw_kernel.  Per 16-edge tile of a wave's receiver-aligned range
+// (within the launch's receiver chunk [r_lo, r_hi)): the forward's first
+// layer (recomputed from e^k and the block's node projections, or read from
+// the forward's h_1 when STASH), the later layers, LayerNorm; dm = dagg[r]
+// + de^{k+1}; LayerNorm backward; each layer's output gradient (stored for
+// the weight gradients, with the hidden activations) down to dz_0; de^k =
+// de^{k+1} + dz_0 W_e (bf16, in place); the ordered receiver sums of dz_0
+// overwrite the consumed dagg rows; bias / LayerNorm column partials per
+// workgroup.
+template <int D, bool STASH, int NWV>
+__global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV == 4 ? 1 : 2, NWV == 4 ? 1 : 2)))
+void edge_bwd_rw_kernel(EdgeBwdArgs a) {
+  using Lay = RwBwdLay<D, STASH, NWV>;
+  constexpr int NTH = Lay::NTH, NB = RW_NB, NKH = RW_NKH, L = RW_L;
+  constexpr int NV = 4 * NB, NR = NV / 16;  // accumulator values per lane; column totals kept per lane
+  constexpr int NFL = Lay::NFL, NCH = Lay::NCH;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* buf = reinterpret_cast<uint4*>(lds + Lay::OFF_BUF);
+  float* vbl = reinterpret_cast<float*>(lds + Lay::OFF_VEC);  // last bias
+  float* vg = vbl + L;                                          // gamma
+  float* vbh = vbl + 2 * L;                                     // hidden bias (D = 3)
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  uint16_t* scr = reinterpret_cast<uint16_t*>(lds + Lay::OFF_SCR + wave * Lay::SCR);
+  // the stream: forward layers (first layer: e block of W_1, rows from memory;
+  // the others from accumulators), then backward layers D-1 .. 0 (packed
+  // for dY W; the first Linear's e block is its first 16 column blocks)
+  const RwSrc fsrc[3] = {{a.mlp.lin[0].wf, 3 * NKH, 0}, {a.mlp.lin[1].wf, NKH, 0}, {a.mlp.lin[D - 1].wf, NKH, 0}};
+  const RwSrc bsrc[3] = {{a.mlp.lin[0].wb, NKH, 0}, {a.mlp.lin[1].wb, NKH, 0}, {a.mlp.lin[D - 1].wb, NKH, 0}};
+  auto load = [&](RwStage<NTH>& st, int p) {
+    const int pp = p % NCH, j = pp / RW_NC, c = pp % RW_NC;
+    if (j < NFL) {
+      const int layer = STASH ? j + 1 : j;  // forward layer
+      if (layer == 0) rw_load<NTH, false>(st, fsrc[0], c);
+      else rw_load<NTH, true>(st, fsrc[layer == D - 1 ? 2 : 1], c);
+    } else {
+      const int layer = D - 1 - (j - NFL);  // backward product of this layer
+      rw_load<NTH, true>(st, bsrc[layer == 0 ? 0 : (layer == D - 1 ? 2 : 1)], c);
+    }
+  };
+  RwStage<NTH> stg;
+  load(stg, 0);
+  rw_store<NTH>(stg, buf);
+  load(stg, 1);
+  rt_copy_vec(vbl, a.mlp.lin[D - 1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  if constexpr (D == 3) rt_copy_vec(vbh, a.mlp.lin[1].b, L);
+  int64_t r0, r1;
+  rs_range(a.row_ptr, a.r_lo, a.r_hi, r0, r1);
+  rs_zero_empty(a.row_ptr, r0, r1, a.dagg, L);
+  const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
+  const int ntile = rw_max_tiles((int)((E1 - E0 + 15) / 16), reinterpret_cast<int*>(lds + Lay::OFF_SLOT));
+  const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
+  // column totals of the bias / LayerNorm gradients (rt_col_totals' share of
+  // each lane): gamma, beta, last bias, hidden biases
+  constexpr int NQ = 2 + D;
+  float qacc[NQ][NR];
+#pragma unroll
+  for (int k = 0; k < NQ; ++k)
+#pragma unroll
+    for (int t = 0; t < NR; ++t) qacc[k][t] = 0.f;
+  float run[L / 64] = {};
+  auto advance = [&](int p) {
+    rw_store<NTH>(stg, buf + ((p + 1) & 1) * RW_CHUNK);
+    load(stg, p + 2);
+  };
+  for (int t = 0; t < ntile; ++t) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t sb = E0 + (int64_t)t * 16;
+    const bool active = sb < E1;  // wave-uniform
+    const int n = active ? (int)(E1 - sb < 16 ? E1 - sb : 16) : 0;
+    const bool ok = e < n;
+    const RsMeta mt = rt_meta_make(rt_meta_load(a.erecv, a.send, active ? sb : E0, active ? E1 : E0));
+    const int64_t srow = (sb - a.e_base + e) * L;  // row of the stored gradients / activations
+    // rows past the tile's end repeat the tile's first row (dm = 0 there)
+    const int64_t er = active ? sb + (ok ? e : 0) : E0;
+    uint64_t mask[2] = {0ull, 0ull};  // ReLU derivative of the hidden layers, bit 4 cb + r
+    uint4 xf[1][NKH];                  // B operand (one 16-edge sub-tile)
+    floatx4 acc[1][NB];
+    int p = 0;                         // stream position within the tile
+    if constexpr (STASH) {
+      if (active) rw_load_relu(reinterpret_cast<const uint16_t*>(a.hid_in) + er * L, q, xf[0], mask[0]);
+    } else {
+      const RsMeta* mp = &mt;
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg)
+        xf[0][kg] = active ? *reinterpret_cast<const uint4*>(Ein + er * L + kg * 32 + q * 8) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        const float* sp = a.proj + (int64_t)(ok ? mp->s : 0) * (2 * L);
+        const float* rp = a.proj + (int64_t)(ok ? mp->r : 0) * (2 * L) + L;
+        float4 ps[RW_CB], pr[RW_CB];
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          ps[cbl] = active ? rt_ld4(sp, c * RW_CB + cbl, q) : make_float4(0.f, 0.f, 0.f, 0.f);
+          pr[cbl] = active ? rt_ld4(rp, c * RW_CB + cbl, q) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          const int cb = c * RW_CB + cbl;
+          floatx4& z = acc[0][cb];
+          const float4 a4 = ps[cbl], b4 = pr[cbl];
+          const float zz[4] = {(z[0] + a4.x) + b4.x, (z[1] + a4.y) + b4.y, (z[2] + a4.z) + b4.z,
+                               (z[3] + a4.w) + b4.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const bool on = zz[r] > 0.f;
+            mask[0] |= (uint64_t)on << (cb * 4 + r);
+            z[r] = on ? zz[r] : 0.f;
+          }
+        }
+        __syncthreads();
+      }
+      p += RW_NC;
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[0][cb][r];
+      rt_frags<NB>(h, xf[0]);
+      if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[0]) + srow, q, xf[0], ok);
+    }
+    if constexpr (D == 3) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          const int cb = c * RW_CB + cbl;
+          const float4 bv = rt_ld4(vbh, cb, q);
+          const float b4[4] = {bv.x, bv.y, bv.z, bv.w};
+          floatx4& z = acc[0][cb];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float v = z[r] + b4[r];
+            const bool on = v > 0.f;
+            mask[1] |= (uint64_t)on << (cb * 4 + r);
+            z[r] = on ? v : 0.f;
+          }
+        }
+        __syncthreads();
+      }
+      p += RW_NC;
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[0][cb][r];
+      rt_frags<NB>(h, xf[0]);
+      if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[1]) + srow, q, xf[0], ok);
+    }
+    // dm = dagg[receiver] + de^{k+1}, loaded before the last layer's
+    // products so that the loads overlap them
+    float dm[NB][4];
+    {
+      const float* gp = a.dagg + (int64_t)(ok ? mt.r : 0) * L;
+      const uint16_t* dp = reinterpret_cast<const uint16_t*>(a.de_next) + er * L;
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) {
+        float lo[4] = {0.f, 0.f, 0.f, 0.f}, hi[4] = {0.f, 0.f, 0.f, 0.f};
+        float4 g0 = make_float4(0.f, 0.f, 0.f, 0.f), g1 = g0;
+        if (active) {
+          if (a.de_next) rw_unpack(*reinterpret_cast<const uint4*>(dp + kg * 32 + q * 8), lo, hi);
+          g0 = rt_ld4(gp, 2 * kg, q);
+          g1 = rt_ld4(gp, 2 * kg + 1, q);
+        }
+        dm[2 * kg][0] = ok ? g0.x + lo[0] : 0.f;
+        dm[2 * kg][1] = ok ? g0.y + lo[1] : 0.f;
+        dm[2 * kg][2] = ok ? g0.z + lo[2] : 0.f;
+        dm[2 * kg][3] = ok ? g0.w + lo[3] : 0.f;
+        dm[2 * kg + 1][0] = ok ? g1.x + hi[0] : 0.f;
+        dm[2 * kg + 1][1] = ok ? g1.y + hi[1] : 0.f;
+        dm[2 * kg + 1][2] = ok ? g1.z + hi[2] : 0.f;
+        dm[2 * kg + 1][3] = ok ? g1.w + hi[3] : 0.f;
+      }
+    }
+    // last layer + bias: y
+    {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          const float4 bv = rt_ld4(vbl, c * RW_CB + cbl, q);
+          floatx4& z = acc[0][c * RW_CB + cbl];
+          z[0] += bv.x;
+          z[1] += bv.y;
+          z[2] += bv.z;
+          z[3] += bv.w;
+        }
+        __syncthreads();
+      }
+      p += RW_NC;
+    }
+    // LayerNorm recomputed (y becomes xhat), then its backward
+    float gv[NB][4];  // the gradient being propagated (fp32, accumulator order)
+    if (active) {
+      float y[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[cb][r] = acc[0][cb][r];
+      const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
+      float s2 = 0.f;
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d = y[cb][r] - mu;
+          s2 += d * d;
+        }
+      const float rs = 1.0f / sqrtf(rt_sum4(s2) / L + a.eps);
+      float t1 = 0.f, t2 = 0.f;
+      {
+        float tg[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          const float4 g4 = rt_ld4(vg, cb, q);
+          const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            y[cb][r] = (y[cb][r] - mu) * rs;
+            const float d = dm[cb][r] * g[r];
+            t1 += d;
+            t2 += d * y[cb][r];
+            tg[cb * 4 + r] = dm[cb][r] * y[cb][r];
+          }
+        }
+        t1 = rt_sum4(t1);
+        t2 = rt_sum4(t2);
+        rt_col_totals<NV>(tg, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[0][tt] += tg[tt];
+      }
+      {
+        float tb[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) tb[cb * 4 + r] = dm[cb][r];
+        rt_col_totals<NV>(tb, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[1][tt] += tb[tt];
+      }
+      {
+        float tl[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          const float4 g4 = rt_ld4(vg, cb, q);
+          const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            gv[cb][r] = rs * (dm[cb][r] * g[r] - t1 / L - y[cb][r] * (t2 / L));
+            tl[cb * 4 + r] = gv[cb][r];
+          }
+        }
+        rt_col_totals<NV>(tl, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[2][tt] += tl[tt];
+      }
+    } else {
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gv[cb][r] = 0.f;
+    }
+    rt_frags<NB>(gv, xf[0]);
+    if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + srow, q, xf[0], ok);
+    // hidden layers: dz_{j-1} = (dz_j W_j) * [z_{j-1} > 0]
+#pragma unroll
+    for (int j = D - 1; j >= 1; --j) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+        __syncthreads();
+      }
+      p += RW_NC;
+      if (active) {
+        float th[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            gv[cb][r] = ((mask[j - 1] >> (cb * 4 + r)) & 1ull) ? acc[0][cb][r] : 0.f;
+            th[cb * 4 + r] = gv[cb][r];
+          }
+        rt_col_totals<NV>(th, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[3 + (j - 1)][tt] += th[tt];
+      }
+      rt_frags<NB>(gv, xf[0]);
+      if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + srow, q, xf[0], ok);
+    }
+    // edge-stream gradient: de^k = de^{k+1} + dz_0 W_1[:, e-block], bf16
+    {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+        __syncthreads();
+      }
+    }
+    if (!active) continue;
+    {
+      const uint16_t* dp = reinterpret_cast<const uint16_t*>(a.de_next) + er * L;
+      uint4 o[NKH];
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) {
+        float lo[4] = {0.f, 0.f, 0.f, 0.f}, hi[4] = {0.f, 0.f, 0.f, 0.f};
+        if (a.de_next) rw_unpack(*reinterpret_cast<const uint4*>(dp + kg * 32 + q * 8), lo, hi);
+        const floatx4 a0 = acc[0][2 * kg], a1 = acc[0][2 * kg + 1];
+        o[kg] = rt_to_plain(make_uint4(bf_pack(a0[0] + lo[0], a0[1] + lo[1]), bf_pack(a0[2] + lo[2], a0[3] + lo[3]),
+                                       bf_pack(a1[0] + hi[0], a1[1] + hi[1]), bf_pack(a1[2] + hi[2], a1[3] + hi[3])));
+      }
+      if (ok) {
+        uint16_t* op = reinterpret_cast<uint16_t*>(a.de_out) + (sb + e) * L;
+#pragma unroll
+        for (int kg = 0; kg < NKH; ++kg) *reinterpret_cast<uint4*>(op + kg * 32 + q * 8) = o[kg];
+      }
+    }
+    // receiver sums of dz_0 (bf16, as it fed the products), ascending edge
+    // order, 64 columns at a time through the wave's scratch tile
+#pragma unroll
+    for (int j = 0; j < L / 64; ++j) {
+      const int cc = ln + 64 * j;
+#pragma unroll
+      for (int kg = 2 * j; kg < 2 * j + 2; ++kg) {
+        const int c0 = (kg - 2 * j) * 32 + q * 4;
+        *reinterpret_cast<uint2*>(scr + rs_sw16<64>(e, c0)) = make_uint2(xf[0][kg].x, xf[0][kg].y);
+        *reinterpret_cast<uint2*>(scr + rs_sw16<64>(e, c0 + 16)) = make_uint2(xf[0][kg].z, xf[0][kg].w);
+      }
+      float x[16];
+#pragma unroll
+      for (int row = 0; row < 16; ++row) x[row] = bf2f(scr[rs_sw16<64>(row, ln)]);
+#pragma unroll
+      for (int row = 0; row < 16; ++row) {
+        if (row < n) {
+          run[j] += x[row];
+          if ((mt.last >> row) & 1ull) {
+            a.dagg[(int64_t)__builtin_amdgcn_readlane(mt.r, row) * L + cc] = run[j];
+            run[j] = 0.f;
+          }
+        }
+      }
+    }
+  }
+  // column partials: lane (e, q)'s totals are columns 16 cb + 4 q + r for
+  // index e * NR + t = 4 cb + r; then the waves in order through LDS (the
+  // chunk buffers are free now)
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(lds);
+  {
+    float* rw = red + wave * Lay::NVEC;
+#pragma unroll
+    for (int tt = 0; tt < NR; ++tt) {
+      const int i = (lane & 15) * NR + tt;
+      const int col = (i >> 2) * 16 + (lane >> 4) * 4 + (i & 3);
+#pragma unroll
+      for (int h = 0; h < D - 1; ++h) rw[h * L + col] = qacc[3 + h][tt];
+      rw[(D - 1) * L + col] = qacc[2][tt];
+      rw[D * L + col] = qacc[0][tt];
+      rw[(D + 1) * L + col] = qacc[1][tt];
+    }
+  }
+  __syncthreads();
+  float* vp = a.vpart + (int64_t)blockIdx.x * a.nvec;
+  for (int i = threadIdx.x; i < Lay::NVEC; i += NTH) {
+    float tsum = 0.f;
+    for (int w = 0; w < Lay::NWV; ++w) tsum += red[w * Lay::NVEC + i];
+    vp[i] = tsum;
+  }
+}
+
 template <int L, int KIND>
 struct RsRowsLay {
   static constexpr int NKH = L / 32, NB = L / 16;
@@ -4407,10 +5196,27 @@ static hipError_t edge_fwd_rsb_t(const EdgeFwdArgs& a, int grid, hipStream_t st)
   return hipGetLastError();
 }
 
+template <int D, int NS, int NWV>
+static hipError_t edge_fwd_rw_t(const EdgeFwdArgs& a, hipStream_t st) {
+  using Lay = RwFwdLay<D, NS, NWV>;
+  allow_lds(edge_fwd_rw_kernel<D, NS, NWV>, Lay::END);
+  hipLaunchKernelGGL((edge_fwd_rw_kernel<D, NS, NWV>), dim3(RS_GRID), dim3(Lay::NTH), Lay::END, st, a);
+  return hipGetLastError();
+}
+
+// the l = 256 forward's tile shape: edges per wave (16 x RW_FWD_NS) and waves
+// per workgroup
+#ifndef RW_FWD_NS
+#define RW_FWD_NS 1
+#endif
+#ifndef RW_FWD_NWV
+#define RW_FWD_NWV 8
+#endif
+
 hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int grid, hipStream_t st) {
   if (edge_rsb(prec, L, D)) {
     if (!a.proj) return hipErrorInvalidValue;
-    return D == 2 ? edge_fwd_rsb_t<256, 2>(a, grid, st) : edge_fwd_rsb_t<256, 3>(a, grid, st);
+    return D == 2 ? edge_fwd_rw_t<2, RW_FWD_NS, RW_FWD_NWV>(a, st) : edge_fwd_rw_t<3, RW_FWD_NS, RW_FWD_NWV>(a, st);
   }
   if (edge_rs(prec, L, D)) {
     if (L == 64) return D == 2 ? edge_fwd_rs_t<64, 2>(a, st) : edge_fwd_rs_t<64, 3>(a, st);
@@ -4424,9 +5230,29 @@ hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int gri
   return hipErrorInvalidValue;
 }
 
-int edge_bwd_grid(int prec, int L, int D, int grid) { return edge_rs(prec, L, D) ? RS_GRID : grid; }
+int edge_bwd_grid(int prec, int L, int D, int grid) {
+  return edge_rs(prec, L, D) || edge_rsb(prec, L, D) ? RS_GRID : grid;
+}
+
+#ifndef RW_BWD_NWV
+#define RW_BWD_NWV 4
+#endif
+
+template <int D, bool STASH>
+static hipError_t edge_bwd_rw_t(const EdgeBwdArgs& a, hipStream_t st) {
+  using Lay = RwBwdLay<D, STASH, RW_BWD_NWV>;
+  allow_lds(edge_bwd_rw_kernel<D, STASH, RW_BWD_NWV>, Lay::END);
+  hipLaunchKernelGGL((edge_bwd_rw_kernel<D, STASH, RW_BWD_NWV>), dim3(RS_GRID), dim3(Lay::NTH), Lay::END, st, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_edge_bwd(int prec, int L, int D, const EdgeBwdArgs& a, int grid, hipStream_t st) {
+  if (edge_rsb(prec, L, D)) {
+    // h_1 from the forward's copy, or recomputed from e and the projections
+    if (a.hid_in) return D == 2 ? edge_bwd_rw_t<2, true>(a, st) : edge_bwd_rw_t<3, true>(a, st);
+    if (!a.proj) return hipErrorInvalidValue;
+    return D == 2 ? edge_bwd_rw_t<2, false>(a, st) : edge_bwd_rw_t<3, false>(a, st);
+  }
   if (edge_rs(prec, L, D)) {
     if (L == 64) return D == 2 ? edge_bwd_rs_t<64, 2>(a, st) : edge_bwd_rs_t<64, 3>(a, st);
     return edge_bwd_rs_t<128, 2>(a, st);

@@ -14,7 +14,9 @@ numpy generator seeded with (config seed, 7).  Run from the repository root:
     python tests/golden/make_c2_reference.py
 
 (about 5 minutes per oracle run on 16 host cores, 1 + SENS_RUNS runs; the
-oracle uses every OpenMP thread)."""
+oracle uses every OpenMP thread).  With --extend, an existing fixture of the
+same inputs keeps its reference run and only the missing perturbed runs are
+made (their movement is merged by taking the larger)."""
 from __future__ import annotations
 
 import os
@@ -30,7 +32,7 @@ import oracle  # noqa: E402
 import synth  # noqa: E402
 
 OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "c2_reference.npz")
-SENS_RUNS = 3
+SENS_RUNS = 6
 
 
 def c2_inputs():
@@ -72,6 +74,7 @@ def main():
     print(f"C2: {g['n_owned']} nodes, {g['n_edges']} edges; inputs {time.time() - t:.1f}s", flush=True)
     ocfg = oracle.ModelCfg(cfg.latent, cfg.K, cfg.depth)
     params = case.params.astype(np.float64)
+    digest = input_digest(g, loc, case.params, d_out)
 
     def run(nf, ef):
         t = time.time()
@@ -79,17 +82,25 @@ def main():
         print(f"oracle step {time.time() - t:.1f}s", flush=True)
         return r
 
-    r = run(loc["node_feat"].astype(np.float64), loc["edge_feat"].astype(np.float64))
-    sens = np.zeros(len(case.shapes))
-    sens_out = 0.0
-    for i in range(1, SENS_RUNS + 1):
+    first = 1
+    if "--extend" in sys.argv and os.path.exists(OUT):
+        old = np.load(OUT)
+        assert str(old["digest"]) == digest, "the stored fixture belongs to other inputs"
+        # the stored float32 copy of the reference, as the GPU test reads it
+        r = {"out": old["out"].astype(np.float64), "d_params": old["d_params"].astype(np.float64)}
+        sens, sens_out, first = old["sens_d_params"].copy(), float(old["sens_out"]), int(old["sens_runs"]) + 1
+    else:
+        r = run(loc["node_feat"].astype(np.float64), loc["edge_feat"].astype(np.float64))
+        sens = np.zeros(len(case.shapes))
+        sens_out = 0.0
+    for i in range(first, SENS_RUNS + 1):
         nf, ef = synth.perturbed((loc["node_feat"], loc["edge_feat"]), i)
         rp = run(nf, ef)
         sens = np.maximum(sens, tensor_rel_err(rp["d_params"], r["d_params"], case.shapes))
         sens_out = max(sens_out, float(np.abs(rp["out"] - r["out"]).max() / np.abs(r["out"]).max()))
     np.savez(OUT, out=r["out"].astype(np.float32), d_params=r["d_params"].astype(np.float32),
              sens_d_params=sens, sens_out=sens_out, sens_runs=SENS_RUNS, n_owned=g["n_owned"],
-             n_edges=g["n_edges"], digest=input_digest(g, loc, case.params, d_out))
+             n_edges=g["n_edges"], digest=digest)
     print(f"wrote {OUT}", flush=True)
 
 
