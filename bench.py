@@ -119,8 +119,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="C4")
     ap.add_argument("--recompute", type=int, default=None,
-                    help="edge-stream checkpoint interval (default: 5 for C5, whose stash-all workspace exceeds "
-                         "the GPU's memory; 0 otherwise)")
+                    help="edge-stream checkpoint interval (default for C5, whose stash-all workspace exceeds the "
+                         "GPU's memory: -1, the smallest interval that fits; 0 otherwise)")
     ap.add_argument("--lockstep", type=int, default=0,
                     help="step P theta slabs of the configuration's whole mesh in lockstep on the one GPU "
                          "(halo exchange after every block), instead of the configuration's single partition")
@@ -176,15 +176,17 @@ def main():
     loc = case.local_inputs(g["l2g"], g["eperm"], g["n_owned"], g["n_halo"])
     no, nh, ne = g["n_owned"], g["n_halo"], g["n_edges"]
     log(f"[bench] {cfg.name}: {cfg.note}; owned {no}, halo {nh}, edges {ne}; inputs {time.time() - t0:.1f}s")
-    recompute = args.recompute if args.recompute is not None else (5 if cfg.name == "C5" else 0)
+    recompute = args.recompute if args.recompute is not None else (-1 if cfg.name == "C5" else 0)
     rs = cfg.precision == "bf16" and (cfg.latent == 64 or (cfg.latent == 128 and cfg.depth == 2))
     h1 = args.h1_stash if (rs and recompute == 0) else 0
     sess = Session(cfg.latent, cfg.K, cfg.depth, cfg.precision, g, loc["node_feat"], loc["edge_feat"],
                    loc["halo"], case.params, recompute=recompute, h1_stash=h1)
+    recompute = sess.recompute
     stash = min(sess.h1_stash, cfg.K) / cfg.K if (rs and recompute == 0 and cfg.K) else 0.0
     target = torch.as_tensor(loc["target"]).cuda()
     log(f"[bench] workspace {sess.ws_bytes / 2**30:.1f} GiB"
-        + (f" (first-Linear stash for {round(stash * cfg.K)} of {cfg.K} blocks)" if stash else ""))
+        + (f" (first-Linear stash for {round(stash * cfg.K)} of {cfg.K} blocks)" if stash else "")
+        + (f" (checkpoint interval {recompute})" if recompute else ""))
 
     def step():
         sess.forward()

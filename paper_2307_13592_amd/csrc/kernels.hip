@@ -1284,10 +1284,9 @@ struct EdgeBwdLds {
 // gradients; bias / gamma / beta gradients are per-lane column partials over
 // the workgroup's rows, written once at the end.
 // How the edge backward obtains the first Linear's ReLU output h_1: recompute
-// it from the gathered [e | v_s | v_r] rows, read the forward's copy, or
-// recompute it the row-split way from e and the block's node projections
-// (l = 256, bf16).  One instantiation per way keeps the others' registers out.
-enum { BWD_GATHER = 0, BWD_STASH = 1, BWD_RSB = 2 };
+// it from the gathered [e | v_s | v_r] rows, or read the forward's copy.  One
+// instantiation per way keeps the other's registers out.
+enum { BWD_GATHER = 0, BWD_STASH = 1 };
 
 template <int P_, int L, int D, int MODE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::value))) void edge_bwd_kernel(EdgeBwdArgs a) {
@@ -1376,38 +1375,6 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
           uint4 v = make_uint4(0, 0, 0, 0);
           if (r < n) v = *reinterpret_cast<const uint4*>(hsrc + (int64_t)r * L + c);
           *reinterpret_cast<uint4*>(HB + r * Lay::LDH + c) = v;
-        }
-      } else if constexpr (MODE == BWD_RSB) {
-        // recompute the row-split forward's first layer (edge_fwd_rsb_kernel):
-        // z_1 = W_e e + P_s[s] + P_r[r] with the block's node projections, the
-        // same sums in the same order, so h_1 is bitwise the forward's
-        constexpr int E16 = 16 / sizeof(T);
-        constexpr int CPR = L / E16;
-        for (int i = tid; i < TE * CPR; i += NT) {
-          const int r = i / CPR, c = (i % CPR) * E16;
-          uint4 v = make_uint4(0, 0, 0, 0);
-          if (r < n) v = *reinterpret_cast<const uint4*>(Ein + (sb + r) * L + c);
-          *reinterpret_cast<uint4*>(A + r * Lay::LDA + c) = v;
-        }
-        __syncthreads();
-        floatx4 acc[MB][NBW];
-        wave_gemm_k<P, MB, NBW, NKH, true, NK1>(A, Lay::LDA, a.mlp.lin[0].wf, nb0, acc);
-#pragma unroll
-        for (int nn = 0; nn < NBW; ++nn) {
-          const int col = (nb0 + nn) * 16 + acc_col();
-#pragma unroll
-          for (int m = 0; m < MB; ++m)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int row = m * 16 + acc_row(r);
-              float v = 0.f;
-              if (row < n) {
-                v = (acc[m][nn][r] + a.proj[(int64_t)mt.ss[row] * (2 * L) + col]) +
-                    a.proj[(int64_t)mt.rr[row] * (2 * L) + L + col];
-                v = v > 0.f ? v : 0.f;
-              }
-              HB[row * Lay::LDH + col] = P::cvt(v);
-            }
         }
       } else {
         gather_rows<P, L, TE, Lay::LDA>(A, mt, Ein, a.V, a.H, a.V16, a.n_owned, sb, n);
@@ -1545,131 +1512,6 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
       vp[off_last + col] = pl[nn];
       vp[off_last + L + col] = pg[nn];
       vp[off_last + 2 * L + col] = pb[nn];
-    }
-  }
-}
-
-// ---------------------------------------- row-split forward, l = 256 ---
-// bf16, l = 256, depth 2 or 3.  The first Linear's sender and receiver
-// blocks are applied per node (node_proj_big_kernel: P[n] = [W_s v_n |
-// W_r v_n + b_1], bf16 operands, fp32 sums), so a tile stages only its e
-// rows (l wide instead of 3l) and 64-edge tiles fit the LDS: every weight
-// fragment streamed from L2 serves 64 edges (the concatenated form fits 32).
-// Per edge z_1 = W_e e + P_s[s] + P_r[r]; the rest as edge_fwd_kernel.
-// LDS: e rows | first hidden rows | second hidden rows, or (first) the fp32
-// first-layer product; the last product (fp32) over the hidden rows once the
-// last product has read them.
-template <int L, int D>
-struct EdgeRsbLds {
-  static constexpr int TE = 64;
-  static constexpr int LDA = L + PBF16::PAD;  // e rows (bf16)
-  static constexpr int LDH = L + PBF16::PAD;  // hidden rows (bf16)
-  static constexpr int LDY = L + 4;           // fp32 rows
-  static constexpr int OFF_B = rup(TE * LDA * 2, 16);
-  static constexpr int OFF_C = OFF_B + TE * LDH * 2;  // HC (D = 3); before it, Z = W_e e (fp32)
-  static constexpr int CEND = OFF_C + (TE * LDY * 4 > TE * LDH * 2 ? TE * LDY * 4 : TE * LDH * 2);
-  static constexpr int OFF_Y = OFF_B;
-  static constexpr int YEND = OFF_Y + TE * LDY * 4;
-  static constexpr int OFF_META = rup(CEND > YEND ? CEND : YEND, 16);
-  static constexpr int END = OFF_META + TE * 8 + 16;
-  static_assert(END <= LDS_MAX, "LDS");
-};
-
-template <int L, int D>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void edge_fwd_rsb_kernel(EdgeFwdArgs a) {
-  using P = PBF16;
-  using T = uint16_t;
-  using Lay = EdgeRsbLds<L, D>;
-  constexpr int TE = Lay::TE, MB = TE / 16, NBW = L / 16 / NW, NKH = L / P::KG, NK1 = 3 * L / P::KG;
-  constexpr int CPR = L / 8;  // 16-byte chunks per bf16 row
-  extern __shared__ __align__(16) unsigned char lds[];
-  T* A = reinterpret_cast<T*>(lds);
-  T* HB = reinterpret_cast<T*>(lds + Lay::OFF_B);
-  T* HC = reinterpret_cast<T*>(lds + Lay::OFF_C);
-  float* Z = reinterpret_cast<float*>(lds + Lay::OFF_C);
-  float* Y = reinterpret_cast<float*>(lds + Lay::OFF_Y);
-  EdgeMeta mt;
-  mt.rr = reinterpret_cast<int32_t*>(lds + Lay::OFF_META);
-  mt.ss = mt.rr + TE;
-  mt.last = reinterpret_cast<unsigned long long*>(mt.ss + TE);
-  const int wave = threadIdx.x >> 6, tid = threadIdx.x, nb0 = wave * NBW;
-  const T* Ein = reinterpret_cast<const T*>(a.Ein);
-  T* Eout = reinterpret_cast<T*>(a.Eout);
-  constexpr int C4 = L / 4;  // float4 chunks per fp32 row
-  for (TileIter it(*a.n_units); it.valid(); it.next()) {
-    const int64_t r0 = a.unit_r[it.t], r1 = a.unit_r[it.t + 1];
-    const int64_t e0 = a.row_ptr[r0], e1 = a.row_ptr[r1];
-    zero_empty_receivers(a.row_ptr, r0, r1, a.agg, L);
-    float run = 0.f;  // running receiver sum of column tid
-    for (int64_t sb = e0; sb < e1; sb += TE) {
-      const int n = (int)(e1 - sb < TE ? e1 - sb : TE);
-      stage_meta<TE>(mt, a.erecv, a.send, sb, n, e1);
-      for (int i = tid; i < TE * CPR; i += NT) {
-        const int r = i / CPR, c = (i % CPR) * 8;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (r < n) v = *reinterpret_cast<const uint4*>(Ein + (sb + r) * L + c);
-        *reinterpret_cast<uint4*>(A + r * Lay::LDA + c) = v;
-      }
-      __syncthreads();
-      {
-        // Z = W_e e (the e columns of W_1), fp32 in LDS
-        floatx4 acc[MB][NBW];
-        wave_gemm_k<P, MB, NBW, NKH, true, NK1>(A, Lay::LDA, a.mlp.lin[0].wf, nb0, acc);
-        store_acc<P, MB, NBW, false>(acc, nb0, nullptr, L, Z, Lay::LDY);
-      }
-      __syncthreads();
-      // z_1 = (Z + P_s[s]) + P_r[r], ReLU, by rows: 16-byte projection loads
-      for (int i = tid; i < TE * C4; i += NT) {
-        const int r = i / C4, c = (i % C4) * 4;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (r < n) {
-          const float4 z = *reinterpret_cast<const float4*>(Z + r * Lay::LDY + c);
-          const float4 ps = *reinterpret_cast<const float4*>(a.proj + (int64_t)mt.ss[r] * (2 * L) + c);
-          const float4 pr = *reinterpret_cast<const float4*>(a.proj + (int64_t)mt.rr[r] * (2 * L) + L + c);
-          const float4 t = make_float4((z.x + ps.x) + pr.x, (z.y + ps.y) + pr.y, (z.z + ps.z) + pr.z,
-                                       (z.w + ps.w) + pr.w);
-          v = make_float4(t.x > 0.f ? t.x : 0.f, t.y > 0.f ? t.y : 0.f, t.z > 0.f ? t.z : 0.f,
-                          t.w > 0.f ? t.w : 0.f);
-        }
-        uint2 h;
-        h.x = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
-        h.y = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
-        *reinterpret_cast<uint2*>(HB + r * Lay::LDH + c) = h;
-      }
-      __syncthreads();
-      // kept for the backward (HB is read-only until the last product is done)
-      if (a.hid_out) store_rows(reinterpret_cast<T*>(a.hid_out) + sb * L, HB, Lay::LDH, n, L);
-      const T* hin = HB;
-      if constexpr (D == 3) {
-        floatx4 acc[MB][NBW];
-        wave_gemm_k<P, MB, NBW, NKH>(HB, Lay::LDH, a.mlp.lin[1].wf, nb0, acc);
-        store_acc<P, MB, NBW, true>(acc, nb0, a.mlp.lin[1].b, L, HC, Lay::LDH);
-        __syncthreads();
-        hin = HC;
-      }
-      {
-        floatx4 acc[MB][NBW];
-        wave_gemm_k<P, MB, NBW, NKH>(hin, Lay::LDH, a.mlp.lin[D - 1].wf, nb0, acc);
-        __syncthreads();  // Y overlays the hidden rows
-        store_acc<P, MB, NBW, false>(acc, nb0, a.mlp.lin[D - 1].b, L, Y, Lay::LDY);
-      }
-      __syncthreads();
-      ln_rows<TE, L>(Y, Lay::LDY, a.eps, a.mlp.gamma, a.mlp.beta);
-      __syncthreads();
-      if (Eout) {
-        // e^{k+1} = e^k + m
-        for (int i = tid; i < n * CPR; i += NT) {
-          const int r = i / CPR, c = (i % CPR) * 8;
-          T o[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) o[j] = f2bf(bf2f(A[r * Lay::LDA + c + j]) + Y[r * Lay::LDY + c + j]);
-          *reinterpret_cast<uint4*>(Eout + (sb + r) * L + c) = *reinterpret_cast<const uint4*>(o);
-        }
-      }
-      if (tid < L)
-        segment_sums<TE>(Y, Lay::LDY, n, tid, mt, run,
-                         [&](int32_t r, float v) { a.agg[(int64_t)r * L + tid] = v; });
-      __syncthreads();
     }
   }
 }
@@ -5012,19 +4854,10 @@ template <int P_, int L, int D>
 static hipError_t edge_bwd_t(const EdgeBwdArgs& a, int grid, hipStream_t st) {
   using P = typename PrecOf<P_>::type;
   using Lay = EdgeBwdLds<P, L, D, EdgeTEB<P, L, D>::value>;
-  // the way h_1 is obtained: the forward's copy, the row-split recompute
-  // (l = 256 bf16 with the block's projections), or the gathered rows
+  // the way h_1 is obtained: the forward's copy or the gathered rows
   if (a.hid_in) {
     allow_lds(edge_bwd_kernel<P_, L, D, BWD_STASH>, Lay::END);
     hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D, BWD_STASH>), dim3(grid), dim3(NT), Lay::END, st, a);
-  } else if constexpr (P_ == BF16 && L == 256) {
-    if (a.proj) {
-      allow_lds(edge_bwd_kernel<P_, L, D, BWD_RSB>, Lay::END);
-      hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D, BWD_RSB>), dim3(grid), dim3(NT), Lay::END, st, a);
-    } else {
-      allow_lds(edge_bwd_kernel<P_, L, D, BWD_GATHER>, Lay::END);
-      hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D, BWD_GATHER>), dim3(grid), dim3(NT), Lay::END, st, a);
-    }
   } else {
     allow_lds(edge_bwd_kernel<P_, L, D, BWD_GATHER>, Lay::END);
     hipLaunchKernelGGL((edge_bwd_kernel<P_, L, D, BWD_GATHER>), dim3(grid), dim3(NT), Lay::END, st, a);
@@ -5188,13 +5021,6 @@ hipError_t launch_node_proj(int L, const void* v16, int64_t n_local, const Lin& 
 
 bool edge_rsb(int prec, int L, int D) { return prec == BF16 && L == 256 && (D == 2 || D == 3); }
 
-template <int L, int D>
-static hipError_t edge_fwd_rsb_t(const EdgeFwdArgs& a, int grid, hipStream_t st) {
-  using Lay = EdgeRsbLds<L, D>;
-  allow_lds(edge_fwd_rsb_kernel<L, D>, Lay::END);
-  hipLaunchKernelGGL((edge_fwd_rsb_kernel<L, D>), dim3(grid), dim3(NT), Lay::END, st, a);
-  return hipGetLastError();
-}
 
 template <int D, int NS, int NWV>
 static hipError_t edge_fwd_rw_t(const EdgeFwdArgs& a, hipStream_t st) {

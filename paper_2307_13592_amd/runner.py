@@ -16,10 +16,13 @@ class Session:
     def __init__(self, latent: int, K: int, depth: int, precision: str, graph: dict, node_feat, edge_feat, halo,
                  params, device: str = "cuda", node_in: int = 11, edge_in: int = 4, node_out: int = 5,
                  recompute: int = 0, chunk_edges: int = 0, inference: bool = False, h1_stash: int = 0):
-        """h1_stash: blocks whose first-Linear ReLU output the forward keeps
-        for the backward (row-split kernels, mgn_set_h1_stash); -1: as many
-        as the device's free memory holds beside the rest of the workspace
-        (with 8 GiB to spare)."""
+        """recompute: edge-stream checkpoint interval (mgn_set_recompute, bf16;
+        0: keep every block); -1: the smallest interval whose workspace fits
+        the device's free memory with 8 GiB to spare.  h1_stash: blocks whose
+        first-Linear ReLU output the forward keeps for the backward
+        (row-split kernels, mgn_set_h1_stash); -1: as many as the device's
+        free memory holds beside the rest of the workspace (with 8 GiB to
+        spare)."""
         if not torch.cuda.is_available():
             raise RuntimeError("libmgn needs a HIP device")
         self.device = torch.device(device)
@@ -38,8 +41,21 @@ class Session:
         self.n_params = mgn_param_count(self.model)
         self.set_params(params)
         mgn_graph_validate(self.model, self.gs)
-        if recompute:
-            mgn_set_recompute(self.model, recompute, chunk_edges)
+        if recompute < 0 and not inference and K > 0 and ne > 0:
+            # the smallest checkpoint interval whose workspace (as the library
+            # plans it) leaves 8 GiB of the free memory: fewer blocks'
+            # edge forwards repeated in the backward
+            free = torch.cuda.mem_get_info(self.device)[0]
+            for s in range(1, K + 1):
+                mgn_set_recompute(self.model, s, chunk_edges)
+                if mgn_workspace_size(self.model, self.gs) + (8 << 30) <= free:
+                    recompute = s
+                    break
+            else:
+                recompute = K
+        self.recompute = max(recompute, 0)
+        if self.recompute:
+            mgn_set_recompute(self.model, self.recompute, chunk_edges)
         if inference:
             mgn_set_inference(self.model, True)
         self.ws_bytes = mgn_workspace_size(self.model, self.gs)

@@ -56,7 +56,7 @@ def _free(s):
 
 # edge-stream checkpoint interval per configuration: C5's stash-all workspace
 # (~430 GB of edge latents alone) does not fit one GPU
-RECOMPUTE = {"C5": 5}
+RECOMPUTE = {"C5": -1}
 # first-Linear stash per configuration, as bench.py runs it (-1: as many
 # blocks as the free memory holds)
 H1_STASH = {"C4": -1}
