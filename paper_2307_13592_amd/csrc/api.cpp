@@ -38,7 +38,7 @@ struct MlpL {
 
 struct WsPlan {
   size_t erecv, chunk, unit_r, nunits, V, V16, PROJ, AGG, ES, DV[2], DAGG, DZS, DE, DEL_E[3], HID_E[2], DEL_N[3], HID_N[2],
-      HID_NK, HID_E1, PART, VPART, total;
+      HID_NK, HID_E1, PART, VPART, SRANGE, total;
   int64_t max_units;
   // edge-stream checkpointing: interval s (0: every block kept), checkpoints
   bool lean = false;
@@ -318,6 +318,7 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   int nvec = 0;
   for (const MlpL& ml : m->mlp) nvec = std::max(nvec, ml.nvec);
   p.VPART = take(4 * (size_t)BWD_GRID * nvec);
+  p.SRANGE = take(8);  // sender-id range of a backward edge chunk
   p.total = o;
   return p;
 }
@@ -1081,9 +1082,15 @@ struct Bwd {
         e = run_dw(m, ml.lin[0], w, d_params, acc, st, 0, L);
         CHK("edge dW (e block)");
         if (nch > 1) {
+          // per-sender sums of dz_0, chunk by chunk in ascending edge order:
+          // zero once, then each chunk adds to the senders of its edges only
           Timed t_(m, MGN_T_INPUT_GRAD, st);
-          e = launch_sender_sums(m->prec, L, g->trow_ptr, g->tedge, DEL_E[0], e0, e0 + rows, no + nh, DZS, c == 0,
-                                 st);
+          int32_t* sr = (int32_t*)(ws + p.SRANGE);
+          if (c == 0) e = launch_zero(DZS, (no + nh) * (int64_t)L, st);
+          if (e == hipSuccess) e = launch_sender_range(g->send, e0, e0 + rows, sr, st);
+          if (e == hipSuccess)
+            e = launch_sender_sums(m->prec, L, g->trow_ptr, g->tedge, DEL_E[0], e0, e0 + rows, no + nh, DZS, 0, sr,
+                                   st);
           CHK("sender sums");
         }
       }

@@ -193,7 +193,10 @@ hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t s
 // Per-sender sums of dz_0 over the edges [e_lo, e_hi) (dz rows stored from e_lo),
 // assigned (first) or added into dzs.
 hipError_t launch_sender_sums(int prec, int L, const int32_t* trow, const int32_t* tedge, const void* dz, int64_t e_lo,
-                              int64_t e_hi, int64_t n_local, float* dzs, int first, hipStream_t st);
+                              int64_t e_hi, int64_t n_local, float* dzs, int first, const int32_t* range,
+                              hipStream_t st);
+// range[0 .. 1] = min and max sender id of the edges [e_lo, e_hi) (empty: INT32_MAX, -1)
+hipError_t launch_sender_range(const int32_t* send, int64_t e_lo, int64_t e_hi, int32_t* range, hipStream_t st);
 // Register-resident weight gradient for bf16 layers with 128 inputs and 128
 // outputs over many rows (dw_stream_ok); part needs dw_stream_parts() * 16384
 // floats; writes (or adds to) dst[o * ldw + i].

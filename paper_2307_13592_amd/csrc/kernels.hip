@@ -4090,49 +4090,76 @@ template <int P_, int L>
 __global__ __launch_bounds__(NT) void sender_sums_kernel(const int32_t* __restrict__ trow,
                                                          const int32_t* __restrict__ tedge, const void* dzv,
                                                          int64_t e_lo, int64_t e_hi, int64_t n_local,
-                                                         float* __restrict__ dzs, int first) {
+                                                         float* __restrict__ dzs, int first,
+                                                         const int32_t* __restrict__ range) {
   using P = typename PrecOf<P_>::type;
   using T = typename P::T;
   constexpr int E16 = 16 / sizeof(T);
   constexpr int CPR = L / E16;
   const T* dz = reinterpret_cast<const T*>(dzv);
-  const int64_t it = (int64_t)blockIdx.x * NT + threadIdx.x;
-  if (it >= n_local * CPR) return;
-  const int64_t node = it / CPR;
-  const int c = (int)(it % CPR) * E16;
-  int32_t lo = trow[node], hi = trow[node + 1];
-  while (lo < hi) {  // first of the node's edges at or after e_lo
-    const int32_t mid = (lo + hi) >> 1;
-    if (tedge[mid] < e_lo) lo = mid + 1;
-    else hi = mid;
-  }
-  float s[E16];
-#pragma unroll
-  for (int j = 0; j < E16; ++j) s[j] = 0.f;
-  // up to 16 rows in flight, summed in ascending edge order
-  const int32_t nend = trow[node + 1];
-  for (int32_t i = lo; i < nend; i += 16) {
-    int32_t ed[16];
-#pragma unroll
-    for (int u = 0; u < 16; ++u) ed[u] = i + u < nend ? tedge[i + u] : INT32_MAX;
-    uint4 v[16];
-#pragma unroll
-    for (int u = 0; u < 16; ++u)
-      v[u] = ed[u] < e_hi ? *reinterpret_cast<const uint4*>(dz + (int64_t)(ed[u] - e_lo) * L + c)
-                          : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      if (ed[u] < e_hi) {
-        const T* t = reinterpret_cast<const T*>(&v[u]);
-#pragma unroll
-        for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
-      }
+  // every local node, or (range) only the senders [range[0], range[1]] of
+  // the edges in [e_lo, e_hi): the other nodes' sums do not change
+  const int64_t n0 = range ? (int64_t)range[0] : 0;
+  const int64_t n1 = range ? (int64_t)range[1] + 1 : n_local;
+  for (int64_t it = (int64_t)blockIdx.x * NT + threadIdx.x; it < (n1 - n0) * CPR; it += (int64_t)gridDim.x * NT) {
+    const int64_t node = n0 + it / CPR;
+    const int c = (int)(it % CPR) * E16;
+    int32_t lo = trow[node], hi = trow[node + 1];
+    while (lo < hi) {  // first of the node's edges at or after e_lo
+      const int32_t mid = (lo + hi) >> 1;
+      if (tedge[mid] < e_lo) lo = mid + 1;
+      else hi = mid;
     }
-    if (ed[15] >= e_hi) break;
-  }
-  float* d = dzs + node * L + c;
+    float s[E16];
 #pragma unroll
-  for (int j = 0; j < E16; ++j) d[j] = (first ? 0.f : d[j]) + s[j];
+    for (int j = 0; j < E16; ++j) s[j] = 0.f;
+    // up to 16 rows in flight, summed in ascending edge order
+    const int32_t nend = trow[node + 1];
+    for (int32_t i = lo; i < nend; i += 16) {
+      int32_t ed[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) ed[u] = i + u < nend ? tedge[i + u] : INT32_MAX;
+      uint4 v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        v[u] = ed[u] < e_hi ? *reinterpret_cast<const uint4*>(dz + (int64_t)(ed[u] - e_lo) * L + c)
+                            : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        if (ed[u] < e_hi) {
+          const T* t = reinterpret_cast<const T*>(&v[u]);
+#pragma unroll
+          for (int j = 0; j < E16; ++j) s[j] += to_f(t[j]);
+        }
+      }
+      if (ed[15] >= e_hi) break;
+    }
+    float* d = dzs + node * L + c;
+#pragma unroll
+    for (int j = 0; j < E16; ++j) d[j] = (first ? 0.f : d[j]) + s[j];
+  }
+}
+
+// range[0] = min, range[1] = max of send[e_lo .. e_hi) (range pre-filled
+// with INT32_MAX, -1); integer minimum and maximum, so the result does not
+// depend on the order of the updates.
+__global__ __launch_bounds__(NT) void sender_range_kernel(const int32_t* __restrict__ send, int64_t e_lo, int64_t e_hi,
+                                                          int32_t* __restrict__ range) {
+  int32_t lo = INT32_MAX, hi = -1;
+  for (int64_t e = e_lo + (int64_t)blockIdx.x * NT + threadIdx.x; e < e_hi; e += (int64_t)gridDim.x * NT) {
+    const int32_t v = send[e];
+    lo = v < lo ? v : lo;
+    hi = v > hi ? v : hi;
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const int32_t a = __shfl_xor(lo, off, 64), b = __shfl_xor(hi, off, 64);
+    lo = a < lo ? a : lo;
+    hi = b > hi ? b : hi;
+  }
+  if ((threadIdx.x & 63) == 0 && hi >= 0) {
+    atomicMin(range, lo);
+    atomicMax(range + 1, hi);
+  }
 }
 
 // -------------------------------------------------- weight gradients ---
@@ -5103,22 +5130,36 @@ static hipError_t input_grad_t(const InGradArgs& a, hipStream_t st) {
 
 template <int P_, int L>
 static hipError_t sender_sums_t(const int32_t* trow, const int32_t* tedge, const void* dz, int64_t e_lo, int64_t e_hi,
-                                int64_t n_local, float* dzs, int first, hipStream_t st) {
+                                int64_t n_local, float* dzs, int first, const int32_t* range, hipStream_t st) {
   constexpr int CPR = L / (16 / (P_ == BF16 ? 2 : 4));
-  const unsigned grid = (unsigned)((n_local * CPR + NT - 1) / NT);
-  hipLaunchKernelGGL((sender_sums_kernel<P_, L>), dim3(grid), dim3(NT), 0, st, trow, tedge, dz, e_lo, e_hi, n_local,
-                     dzs, first);
+  int64_t grid = (n_local * CPR + NT - 1) / NT;
+  if (range && grid > 4096) grid = 4096;  // a grid-stride loop over the range read on the device
+  hipLaunchKernelGGL((sender_sums_kernel<P_, L>), dim3((unsigned)grid), dim3(NT), 0, st, trow, tedge, dz, e_lo, e_hi,
+                     n_local, dzs, first, range);
   return hipGetLastError();
 }
 
 hipError_t launch_sender_sums(int prec, int L, const int32_t* trow, const int32_t* tedge, const void* dz, int64_t e_lo,
-                              int64_t e_hi, int64_t n_local, float* dzs, int first, hipStream_t st) {
+                              int64_t e_hi, int64_t n_local, float* dzs, int first, const int32_t* range,
+                              hipStream_t st) {
   if (n_local == 0) return hipSuccess;
 #define SS(PP, LL) \
-  if (prec == PP && L == LL) return sender_sums_t<PP, LL>(trow, tedge, dz, e_lo, e_hi, n_local, dzs, first, st);
+  if (prec == PP && L == LL) return sender_sums_t<PP, LL>(trow, tedge, dz, e_lo, e_hi, n_local, dzs, first, range, st);
   SS(F32, 64) SS(F32, 128) SS(F32, 256) SS(BF16, 64) SS(BF16, 128) SS(BF16, 256)
 #undef SS
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_sender_range(const int32_t* send, int64_t e_lo, int64_t e_hi, int32_t* range, hipStream_t st) {
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, st, range, (int64_t)1, (int32_t)INT32_MAX);
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, st, range + 1, (int64_t)1, (int32_t)-1);
+  const int64_t n = e_hi - e_lo;
+  if (n > 0) {
+    int64_t grid = (n + NT - 1) / NT;
+    if (grid > 1024) grid = 1024;
+    hipLaunchKernelGGL(sender_range_kernel, dim3((unsigned)grid), dim3(NT), 0, st, send, e_lo, e_hi, range);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t st) {
