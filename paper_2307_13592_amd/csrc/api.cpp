@@ -644,6 +644,7 @@ hipError_t run_dw(mgn_model* m, const LinL& L, DwArgs a, float* d_params, int ac
   }
   Timed t_(m, MGN_T_WEIGHT_GRAD, st);
   if (dw_stream_ok(m->prec, a)) return launch_dw_stream(a, dst, L.in, accumulate, st);
+  if (dw_stream_quad_ok(m->prec, a)) return launch_dw_stream_quad(a, dst, L.in, accumulate, st);
   if (dw_stream_f32_ok(m->prec, a)) return launch_dw_stream_f32(a, dst, L.in, accumulate, st);
   if ((a.O > 128 || a.I > 128) && a.O % 128 == 0 && a.I % 128 == 0) {
     // wider layers (l = 256) as 128 x 128 blocks on the register-resident

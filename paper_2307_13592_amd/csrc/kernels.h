@@ -185,9 +185,9 @@ int edge_bwd_grid(int prec, int L, int D, int grid);
 // projections of launch_node_proj for each block).
 bool edge_rs(int prec, int L, int D);
 hipError_t launch_node_proj(int L, const void* v16, int64_t n_local, const Lin& w1, float* proj, hipStream_t st);
-// bf16, l = 256: the edge forward in row-split form with 64-edge tiles (needs
-// the node projections of launch_node_proj for the block; the edge backward
-// keeps the concatenated form).
+// bf16, l = 256: the edge forward and backward in row-split form with the
+// weights streamed through LDS (the forward, and a backward that recomputes
+// h_1, need the node projections of launch_node_proj for the block).
 bool edge_rsb(int prec, int L, int D);
 hipError_t launch_input_grad(int prec, int L, const InGradArgs& a, hipStream_t st);
 // Per-sender sums of dz_0 over the edges [e_lo, e_hi) (dz rows stored from e_lo),
@@ -203,6 +203,10 @@ hipError_t launch_sender_range(const int32_t* send, int64_t e_lo, int64_t e_hi, 
 int dw_stream_parts();
 bool dw_stream_ok(int prec, const DwArgs& a);
 hipError_t launch_dw_stream(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st);
+// The same for bf16 layers with 256 inputs and 256 outputs in one launch (each
+// operand row read once; same partial buffer).
+bool dw_stream_quad_ok(int prec, const DwArgs& a);
+hipError_t launch_dw_stream_quad(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st);
 // The same for fp32 layers with 128 inputs and 128 outputs (dw_stream_f32_ok):
 // wave partials in plain [o][i] order, then the fixed-order split reduction.
 bool dw_stream_f32_ok(int prec, const DwArgs& a);

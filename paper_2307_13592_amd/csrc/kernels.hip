@@ -4458,7 +4458,12 @@ __device__ __forceinline__ void dws_split(const float4 (&v)[8][2], uint32_t (&hi
 // part[w] (16384 floats, accumulator order [j][j'][lane][4]) = wave w's sum.
 // SPLIT: D is fp32 and enters the products as hi + lo (two MFMAs each).
 // AF32: A is fp32, rounded to bf16 as it is loaded.
-template <bool SPLIT, bool AF32 = false>
+// QUAD: a 256 x 256 product.  The four waves of a workgroup take the same rows
+// and one 128 x 128 quadrant each (wave v: D columns 128 (v >> 1) on, A
+// columns 128 (v & 1) on), so each operand row is fetched from HBM once and
+// its second reader finds it in the cache; part[v * gridDim.x + block] is
+// quadrant v's partial of the workgroup's rows.
+template <bool SPLIT, bool AF32 = false, bool QUAD = false>
 __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void dw_stream_kernel(
     const void* __restrict__ Dv, int ldd, const void* __restrict__ Av, int lda, int64_t R,
     float* __restrict__ part) {
@@ -4469,8 +4474,9 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
       dws_load(reinterpret_cast<const uint16_t*>(Av), lda, row, R, col, v);
   };
   const int lane = threadIdx.x & 63, q = lane >> 4, m = lane & 15;
-  const int64_t w = (int64_t)blockIdx.x * (DWS_NT / 64) + wave_id();
-  const int64_t nw = (int64_t)gridDim.x * (DWS_NT / 64);
+  const int wv = wave_id();
+  const int64_t w = QUAD ? (int64_t)blockIdx.x : (int64_t)blockIdx.x * (DWS_NT / 64) + wv;
+  const int64_t nw = QUAD ? (int64_t)gridDim.x : (int64_t)gridDim.x * (DWS_NT / 64);
   const int64_t steps = (R + 31) / 32;
   const int64_t s0 = steps * w / nw, s1 = steps * (w + 1) / nw;  // this wave's 32-row steps
   floatx4 acc[8][8];
@@ -4479,6 +4485,7 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) acc[j][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int64_t rq = 8 * q;
+  const int dc = (QUAD ? 128 * (wv >> 1) : 0) + 8 * m, ac = (QUAD ? 128 * (wv & 1) : 0) + 8 * m;
   // the next step's loads reuse the source registers once they are
   // transposed, so they are in flight during the current step's products
   if constexpr (SPLIT) {
@@ -4486,16 +4493,16 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
     float4 dv[8][2];
     uint32_t av[8][4], fa[8][4];
     if (s0 < s1) {
-      dws_load_f32(D, ldd, s0 * 32 + rq, R, 8 * m, dv);
-      load_a(s0 * 32 + rq, 8 * m, av);
+      dws_load_f32(D, ldd, s0 * 32 + rq, R, dc, dv);
+      load_a(s0 * 32 + rq, ac, av);
     }
     for (int64_t st = s0; st < s1; ++st) {
       uint32_t hi[8][4], lo[8][4], f[8][4];
       dws_split(dv, hi, lo);
       dws_transpose(av, fa);
       if (st + 1 < s1) {
-        dws_load_f32(D, ldd, (st + 1) * 32 + rq, R, 8 * m, dv);
-        load_a((st + 1) * 32 + rq, 8 * m, av);
+        dws_load_f32(D, ldd, (st + 1) * 32 + rq, R, dc, dv);
+        load_a((st + 1) * 32 + rq, ac, av);
       }
       dws_transpose(hi, f);
       dws_mma(f, fa, acc);
@@ -4506,20 +4513,21 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
     const uint16_t* D = reinterpret_cast<const uint16_t*>(Dv);
     uint32_t dv[8][4], av[8][4], fd[8][4], fa[8][4];
     if (s0 < s1) {
-      dws_load(D, ldd, s0 * 32 + rq, R, 8 * m, dv);
-      load_a(s0 * 32 + rq, 8 * m, av);
+      dws_load(D, ldd, s0 * 32 + rq, R, dc, dv);
+      load_a(s0 * 32 + rq, ac, av);
     }
     for (int64_t st = s0; st < s1; ++st) {
       dws_transpose(dv, fd);
       dws_transpose(av, fa);
       if (st + 1 < s1) {
-        dws_load(D, ldd, (st + 1) * 32 + rq, R, 8 * m, dv);
-        load_a((st + 1) * 32 + rq, 8 * m, av);
+        dws_load(D, ldd, (st + 1) * 32 + rq, R, dc, dv);
+        load_a((st + 1) * 32 + rq, ac, av);
       }
       dws_mma(fd, fa, acc);
     }
   }
-  float4* out = reinterpret_cast<float4*>(part + w * 16384);
+  float4* out =
+      reinterpret_cast<float4*>(part + (QUAD ? (int64_t)wv * gridDim.x + blockIdx.x : w) * 16384);
 #pragma unroll
   for (int j = 0; j < 8; ++j)
 #pragma unroll
@@ -4606,11 +4614,16 @@ __global__ __launch_bounds__(DWS_NT) __attribute__((amdgpu_waves_per_eu(1, 1))) 
 // dst[o * ldw + i] (+)= sum over the S wave partials, in wave order within
 // each of four interleaved sets, combined in set order; entry x of a partial
 // is (j, j', lane, r) -> o = 8 (4 (lane >> 4) + r) + j, i = 8 (lane & 15) + j'.
+// gridDim.y > 1: quadrant y = blockIdx.y of a 256 x 256 gradient, its S
+// partials from part + y S 16384, its outputs at rows 128 (y >> 1) and
+// columns 128 (y & 1) on.
 __global__ __launch_bounds__(NT) void dw_stream_reduce_kernel(const float* __restrict__ part, int S,
                                                               float* __restrict__ dst, int ldw, int accumulate) {
   __shared__ float sh[NT];
   const int jx = threadIdx.x & 63, qq = threadIdx.x >> 6;
   const int x = blockIdx.x * 64 + jx;
+  part += (int64_t)blockIdx.y * S * 16384;
+  dst += (int64_t)(blockIdx.y >> 1) * 128 * ldw + (blockIdx.y & 1) * 128;
   float t = 0.f;
 #pragma unroll 8
   for (int k = qq; k < S; k += 4) t += part[(int64_t)k * 16384 + x];
@@ -5228,6 +5241,30 @@ hipError_t launch_dw_stream(const DwArgs& a, float* dst, int ldw, int accumulate
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(dw_stream_reduce_kernel, dim3(16384 / 64), dim3(NT), 0, st, a.part, DWS_WAVES, dst, ldw,
+                     accumulate);
+  return hipGetLastError();
+}
+
+bool dw_stream_quad_ok(int prec, const DwArgs& a) {
+  return prec == BF16 && (a.a_kind == 0 || (a.a_kind == 1 && a.d_kind == 0)) &&
+         (a.d_kind == 0 || a.d_kind == 1) && a.O == 256 && a.I == 256 && a.ldd % 8 == 0 && a.lda0 % 8 == 0 &&
+         a.R >= 8192;
+}
+
+hipError_t launch_dw_stream_quad(const DwArgs& a, float* dst, int ldw, int accumulate, hipStream_t st) {
+  // DWS_GRID workgroups x 4 quadrants = the DWS_WAVES partials of the plain form
+  if (a.d_kind == 1)
+    hipLaunchKernelGGL((dw_stream_kernel<true, false, true>), dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd,
+                       a.a0, a.lda0, a.R, a.part);
+  else if (a.a_kind == 1)
+    hipLaunchKernelGGL((dw_stream_kernel<false, true, true>), dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd,
+                       a.a0, a.lda0, a.R, a.part);
+  else
+    hipLaunchKernelGGL((dw_stream_kernel<false, false, true>), dim3(DWS_GRID), dim3(DWS_NT), 0, st, a.delta, a.ldd,
+                       a.a0, a.lda0, a.R, a.part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(dw_stream_reduce_kernel, dim3(16384 / 64, 4), dim3(NT), 0, st, a.part, DWS_GRID, dst, ldw,
                      accumulate);
   return hipGetLastError();
 }

@@ -74,8 +74,8 @@ def test_sector_partition(prec, l, D):
 
 def test_sector_medium_l256():
     """l = 256, depth 3, bf16 on a partition large enough (>= 8192 rows) for
-    the weight gradients of the 256 x 256 layers to run as 128 x 128 blocks
-    on the register-resident kernels."""
+    the weight gradients of the 256 x 256 layers to run on the one-launch
+    register-resident kernel (four 128 x 128 quadrants per workgroup)."""
     _case("sector 40x16x60 p1 l=256", meshes.sector(40, 16, 60, 4, seed=9), 1, 256, 1, 3, "bf16")
 
 
