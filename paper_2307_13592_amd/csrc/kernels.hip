@@ -2517,28 +2517,39 @@ template <int NTH>
 struct RwStage {
   uint4 v[RW_CHUNK / NTH];
 };
+// Thread tid's byte offset within a chunk's k-group run: element i = tid +
+// j NTH of the share is column block i / 512 and k-group (i / 64) % 8 of the
+// chunk, so with 512 % NTH == 0 the k-group is (j NTH % 512) / 64 + tid / 64
+// and the column block j NTH / 512: the thread-dependent part is tid / 64
+// k-groups plus the lane's place in a fragment (PERM: the 8-byte half at
+// k-slot order, as rt_copy_frags permutes them).
+template <bool PERM>
+__device__ __forceinline__ uint32_t rw_thread_off() {
+  const int tid = threadIdx.x, ln = tid & 63, q = ln >> 4, cc = ln & 15;
+  const uint32_t lane = PERM ? (uint32_t)((cc + 16 * (q >> 1)) * 2 + (q & 1)) * 8u : (uint32_t)ln * 16u;
+  return (uint32_t)(tid >> 6) * 1024u + lane;
+}
+
 template <int NTH, bool PERM>
-__device__ __forceinline__ void rw_load(RwStage<NTH>& s, const RwSrc src, int c) {
-  // an opaque copy of the thread index: the addresses are recomputed at
-  // every call instead of being hoisted out of the tile loop (dozens of
-  // 64-bit pointers, one set per chunk position, would stay live); 32-bit
-  // byte offsets from the uniform base
-  int tid = threadIdx.x;
-  asm volatile("" : "+v"(tid));
-  const char* base = reinterpret_cast<const char*>(src.frags);
+__device__ __forceinline__ void rw_load(RwStage<NTH>& s, const RwSrc src, int c, uint32_t vo) {
+  static_assert(NTH % 64 == 0 && (RW_NKH * 64) % NTH == 0, "a share's k-groups stay within one column block");
+  // the uniform part of the addresses, kept opaque so that it is formed at
+  // every call (scalar arithmetic) instead of being hoisted out of the tile
+  // loop as dozens of live pointers, one set per chunk position; vo is the
+  // thread's part (rw_thread_off)
+  uint32_t u = (uint32_t)(c * RW_CB * src.src_nkg + src.kg0) * 1024u;
+  asm volatile("" : "+s"(u));
+  const char* base = reinterpret_cast<const char*>(src.frags) + u;
 #pragma unroll
   for (int j = 0; j < RW_CHUNK / NTH; ++j) {
-    const int i = tid + j * NTH;
-    const int cbl = i / (RW_NKH * 64), kg = (i / 64) % RW_NKH, ln = i % 64;
-    const uint32_t f = (uint32_t)(((c * RW_CB + cbl) * src.src_nkg + src.kg0 + kg) * 64) * 16u;
+    constexpr int SPAN = RW_NKH * 64;  // elements per column block
+    const uint32_t f = (uint32_t)((j * NTH) / SPAN * src.src_nkg + ((j * NTH) % SPAN) / 64) * 1024u + vo;
     if constexpr (PERM) {
-      const int q = ln >> 4, cc = ln & 15;
-      const uint2 lo = *reinterpret_cast<const uint2*>(base + f + (uint32_t)((cc + 16 * (q >> 1)) * 2 + (q & 1)) * 8u);
-      const uint2 hi =
-          *reinterpret_cast<const uint2*>(base + f + (uint32_t)((cc + 16 * (2 + (q >> 1))) * 2 + (q & 1)) * 8u);
+      const uint2 lo = *reinterpret_cast<const uint2*>(base + f);
+      const uint2 hi = *reinterpret_cast<const uint2*>(base + f + 512u);
       s.v[j] = make_uint4(lo.x, lo.y, hi.x, hi.y);
     } else {
-      s.v[j] = *reinterpret_cast<const uint4*>(base + f + (uint32_t)ln * 16u);
+      s.v[j] = *reinterpret_cast<const uint4*>(base + f);
     }
   }
 }
@@ -2642,10 +2653,11 @@ void edge_fwd_rw_kernel(EdgeFwdArgs a) {
   const RwSrc src[3] = {{a.mlp.lin[0].wf, 3 * NKH, 0}, {a.mlp.lin[1].wf, NKH, 0}, {a.mlp.lin[D - 1].wf, NKH, 0}};
   // stream position p (chunk p % NCH of a tile): layer p / RW_NC (0: first,
   // D - 1: last), chunk p % RW_NC; only the first layer's B operand is plain
+  const uint32_t vo_plain = rw_thread_off<false>(), vo_perm = rw_thread_off<true>();
   auto load = [&](RwStage<NTH>& st, int p) {
     const int pp = p % Lay::NCH, j = pp / RW_NC, c = pp % RW_NC;
-    if (j == 0) rw_load<NTH, false>(st, src[0], c);
-    else rw_load<NTH, true>(st, src[j == D - 1 ? 2 : 1], c);
+    if (j == 0) rw_load<NTH, false>(st, src[0], c, vo_plain);
+    else rw_load<NTH, true>(st, src[j == D - 1 ? 2 : 1], c, vo_perm);
   };
   RwStage<NTH> stg;
   load(stg, 0);
@@ -2917,15 +2929,16 @@ void edge_bwd_rw_kernel(EdgeBwdArgs a) {
   // for dY W; the first Linear's e block is its first 16 column blocks)
   const RwSrc fsrc[3] = {{a.mlp.lin[0].wf, 3 * NKH, 0}, {a.mlp.lin[1].wf, NKH, 0}, {a.mlp.lin[D - 1].wf, NKH, 0}};
   const RwSrc bsrc[3] = {{a.mlp.lin[0].wb, NKH, 0}, {a.mlp.lin[1].wb, NKH, 0}, {a.mlp.lin[D - 1].wb, NKH, 0}};
+  const uint32_t vo_plain = rw_thread_off<false>(), vo_perm = rw_thread_off<true>();
   auto load = [&](RwStage<NTH>& st, int p) {
     const int pp = p % NCH, j = pp / RW_NC, c = pp % RW_NC;
     if (j < NFL) {
       const int layer = STASH ? j + 1 : j;  // forward layer
-      if (layer == 0) rw_load<NTH, false>(st, fsrc[0], c);
-      else rw_load<NTH, true>(st, fsrc[layer == D - 1 ? 2 : 1], c);
+      if (layer == 0) rw_load<NTH, false>(st, fsrc[0], c, vo_plain);
+      else rw_load<NTH, true>(st, fsrc[layer == D - 1 ? 2 : 1], c, vo_perm);
     } else {
       const int layer = D - 1 - (j - NFL);  // backward product of this layer
-      rw_load<NTH, true>(st, bsrc[layer == 0 ? 0 : (layer == D - 1 ? 2 : 1)], c);
+      rw_load<NTH, true>(st, bsrc[layer == 0 ? 0 : (layer == D - 1 ? 2 : 1)], c, vo_perm);
     }
   };
   RwStage<NTH> stg;
