@@ -2941,10 +2941,11 @@ void edge_bwd_rw_kernel(EdgeBwdArgs a) {
       rw_load<NTH, true>(st, bsrc[layer == 0 ? 0 : (layer == D - 1 ? 2 : 1)], c, vo_perm);
     }
   };
-  RwStage<NTH> stg;
-  load(stg, 0);
-  rw_store<NTH>(stg, buf);
-  load(stg, 1);
+  RwStage<NTH> stg[2];  // chunks p + 1 and p + 2 in flight at step p
+  load(stg[0], 0);
+  rw_store<NTH>(stg[0], buf);
+  load(stg[1], 1);
+  load(stg[0], 2);
   rt_copy_vec(vbl, a.mlp.lin[D - 1].b, L);
   rt_copy_vec(vg, a.mlp.gamma, L);
   if constexpr (D == 3) rt_copy_vec(vbh, a.mlp.lin[1].b, L);
@@ -2964,8 +2965,8 @@ void edge_bwd_rw_kernel(EdgeBwdArgs a) {
     for (int t = 0; t < NR; ++t) qacc[k][t] = 0.f;
   float run[L / 64] = {};
   auto advance = [&](int p) {
-    rw_store<NTH>(stg, buf + ((p + 1) & 1) * RW_CHUNK);
-    load(stg, p + 2);
+    rw_store<NTH>(stg[(p + 1) & 1], buf + ((p + 1) & 1) * RW_CHUNK);
+    load(stg[(p + 1) & 1], p + 3);
   };
   for (int t = 0; t < ntile; ++t) {
     int ln = lane;
