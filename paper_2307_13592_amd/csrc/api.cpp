@@ -299,7 +299,7 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   for (int j = 0; j < 2; ++j) p.HID_N[j] = j < m->D - 1 ? take(ts * (size_t)no * L) : 0;
   // T-form node kernels: every block's first-Linear ReLU output, written by
   // the forward for the backward; checkpointing: one block's, recomputed
-  p.HID_NK = rows_rt(m->prec, L, m->D, NODE_BLOCK) ? take(2 * (size_t)(p.lean ? 1 : K) * no * L) : 0;
+  p.HID_NK = rows_keep_h1(m->prec, L, m->D) ? take(2 * (size_t)(p.lean ? 1 : K) * no * L) : 0;
   // split-K partials: the largest S*O*I over all weight matrices
   size_t part = 0;
   const size_t nm = m->mlp.size();

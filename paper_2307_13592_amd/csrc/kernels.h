@@ -169,6 +169,12 @@ int plan_chunk_receivers();
 // (RowsFwdArgs::hid_out -> RowsBwdArgs::hid_in); without it the older
 // row-split kernel recomputes it.
 bool rows_rt(int prec, int L, int D, int kind);
+// bf16, l = 256 node half: the streamed-weight row kernels (the backward
+// starts from the forward's first-Linear ReLU output, RowsBwdArgs::hid_in).
+bool rows_rw(int prec, int L, int D, int kind);
+// Whether the node half's forward keeps its first-Linear ReLU output for the
+// backward (T-form or streamed-weight row kernels).
+bool rows_keep_h1(int prec, int L, int D);
 hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st);
 hipError_t launch_edge_fwd(int prec, int L, int D, const EdgeFwdArgs& a, int grid, hipStream_t st);
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st);

@@ -2566,14 +2566,16 @@ __device__ __forceinline__ void rw_store(const RwStage<NTH>& s, uint4* buf) {
 #ifndef RW_PF
 #define RW_PF 2
 #endif
-template <int NS>
+template <int NS, bool ZERO = true>
 __device__ __forceinline__ void rw_gemm(int C, const uint4* buf, const uint4 (&X)[NS][RW_NKH],
                                         floatx4 (&acc)[NS][RW_NB], int lane) {
   constexpr int PF = RW_PF;
+  if constexpr (ZERO) {
 #pragma unroll
-  for (int cbl = 0; cbl < RW_CB; ++cbl)
+    for (int cbl = 0; cbl < RW_CB; ++cbl)
 #pragma unroll
-    for (int s = 0; s < NS; ++s) acc[s][C * RW_CB + cbl] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < NS; ++s) acc[s][C * RW_CB + cbl] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
   uint4 w[PF + 1][RW_CB];
 #pragma unroll
   for (int kg = 0; kg < PF; ++kg)
@@ -3251,6 +3253,509 @@ void edge_bwd_rw_kernel(EdgeBwdArgs a) {
             a.dagg[(int64_t)__builtin_amdgcn_readlane(mt.r, row) * L + cc] = run[j];
             run[j] = 0.f;
           }
+        }
+      }
+    }
+  }
+  // column partials: lane (e, q)'s totals are columns 16 cb + 4 q + r for
+  // index e * NR + t = 4 cb + r; then the waves in order through LDS (the
+  // chunk buffers are free now)
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(lds);
+  {
+    float* rw = red + wave * Lay::NVEC;
+#pragma unroll
+    for (int tt = 0; tt < NR; ++tt) {
+      const int i = (lane & 15) * NR + tt;
+      const int col = (i >> 2) * 16 + (lane >> 4) * 4 + (i & 3);
+#pragma unroll
+      for (int h = 0; h < D - 1; ++h) rw[h * L + col] = qacc[3 + h][tt];
+      rw[(D - 1) * L + col] = qacc[2][tt];
+      rw[D * L + col] = qacc[0][tt];
+      rw[(D + 1) * L + col] = qacc[1][tt];
+    }
+  }
+  __syncthreads();
+  float* vp = a.vpart + (int64_t)blockIdx.x * a.nvec;
+  for (int i = threadIdx.x; i < Lay::NVEC; i += NTH) {
+    float tsum = 0.f;
+    for (int w = 0; w < Lay::NWV; ++w) tsum += red[w * Lay::NVEC + i];
+    vp[i] = tsum;
+  }
+}
+
+// ------------------------------------------ l = 256 node half (bf16) ---
+// The node MLP of a block at l = 256 in the streamed-weight form of the edge
+// kernels (weights in 32 KB chunks through LDS, T-form products, one 16-row
+// tile per wave and step, contiguous row ranges per wave).  Forward: z_1 =
+// W_1 [v | agg] + b_1, the v and agg k-ranges of each column chunk streamed
+// one after the other, then ReLU, [W_h, ReLU,] W_last + b, LayerNorm, v + m
+// (fp32 and its bf16 copy); the first Linear's ReLU output h_1 is kept for the
+// backward when hid_out is set (only that when out is null: the backward's
+// recompute).  Backward (from that h_1): the later layers recomputed,
+// LayerNorm backward, each layer's output gradient (stored for the weight
+// gradients, with h_2) down to dz_0, then dv = dm + dz_0 W_1[:, v] and dagg =
+// dz_0 W_1[:, agg] (fp32); bias / LayerNorm column partials per workgroup.
+
+// Rows [r0, r1) of unit q of W (contiguous 16-row tiles).
+__device__ __forceinline__ void rw_row_tiles(int64_t rows, int64_t q, int64_t W, int64_t& t0, int64_t& t1) {
+  const int64_t T = (rows + 15) / 16;
+  t0 = T * q / W;
+  t1 = T * (q + 1) / W;
+}
+
+template <int D>
+struct RwNodeFwdLay {
+  static constexpr int NWV = 8, NTH = 64 * NWV;
+  static constexpr int OFF_BUF = 0;                        // two chunk buffers
+  static constexpr int OFF_VEC = 2 * RW_CHUNK * 16;        // b_1, last bias, gamma, beta[, hidden bias]
+  static constexpr int NVEC = (D == 3 ? 5 : 4) * RW_L;
+  static constexpr int END = OFF_VEC + NVEC * 4;
+  static_assert(END <= 160 * 1024, "LDS");
+  static constexpr int NCH0 = 2 * RW_NC;                   // first layer: v and agg halves per column chunk
+  static constexpr int NCH = NCH0 + (D - 1) * RW_NC;
+  static_assert(NCH % 2 == 0 && NCH0 % 2 == 0, "the stream's buffer parity repeats every tile");
+};
+
+template <int D>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void rows_rw_fwd_kernel(RowsFwdArgs a) {
+  using Lay = RwNodeFwdLay<D>;
+  constexpr int NTH = Lay::NTH, NB = RW_NB, NKH = RW_NKH, L = RW_L;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* buf = reinterpret_cast<uint4*>(lds + Lay::OFF_BUF);
+  float* vb1 = reinterpret_cast<float*>(lds + Lay::OFF_VEC);  // first bias
+  float* vbl = vb1 + L;                                         // last bias
+  float* vg = vb1 + 2 * L;                                      // gamma
+  float* vbt = vb1 + 3 * L;                                     // beta
+  float* vbh = vb1 + 4 * L;                                     // hidden bias (D = 3)
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  // forward packing of W_1: 2 NKH k-groups per column block, v then agg
+  const RwSrc src0[2] = {{a.mlp.lin[0].wf, 2 * NKH, 0}, {a.mlp.lin[0].wf, 2 * NKH, NKH}};
+  const RwSrc src[2] = {{a.mlp.lin[1].wf, NKH, 0}, {a.mlp.lin[D - 1].wf, NKH, 0}};
+  // the whole MLP, or only the first layer (out null)
+  const int nch = a.out ? Lay::NCH : Lay::NCH0;
+  const uint32_t vo_plain = rw_thread_off<false>(), vo_perm = rw_thread_off<true>();
+  auto load = [&](RwStage<NTH>& st, int p) {
+    const int pp = p % nch;
+    if (pp < Lay::NCH0) rw_load<NTH, false>(st, src0[pp & 1], pp >> 1, vo_plain);
+    else {
+      const int j = (pp - Lay::NCH0) / RW_NC + 1, c = (pp - Lay::NCH0) % RW_NC;  // layer 1 .. D-1
+      rw_load<NTH, true>(st, src[j == D - 1 ? 1 : 0], c, vo_perm);
+    }
+  };
+  RwStage<NTH> stg;
+  load(stg, 0);
+  rw_store<NTH>(stg, buf);
+  load(stg, 1);
+  rt_copy_vec(vb1, a.mlp.lin[0].b, L);
+  rt_copy_vec(vbl, a.mlp.lin[D - 1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  rt_copy_vec(vbt, a.mlp.beta, L);
+  if constexpr (D == 3) rt_copy_vec(vbh, a.mlp.lin[1].b, L);
+  int64_t t0, t1;
+  rw_row_tiles(a.rows, (int64_t)blockIdx.x * Lay::NWV + wave, (int64_t)gridDim.x * Lay::NWV, t0, t1);
+  // every wave takes part in every chunk step: the largest range's count
+  const int64_t T = (a.rows + 15) / 16, Wt = (int64_t)gridDim.x * Lay::NWV;
+  const int ntile = (int)((T + Wt - 1) / Wt);
+  __syncthreads();
+  const uint16_t* V16 = reinterpret_cast<const uint16_t*>(a.in0_16);
+  auto advance = [&](int p) {
+    rw_store<NTH>(stg, buf + ((p + 1) & 1) * RW_CHUNK);
+    load(stg, p + 2);
+  };
+  for (int t = 0; t < ntile; ++t) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t tile = t0 + t;
+    const bool active = tile < t1;  // wave-uniform
+    const int64_t row = tile * 16 + e;
+    const bool ok = active && row < a.rows;
+    const int64_t src_row = ok ? row : (active ? tile * 16 : 0);  // rows past the end repeat the tile's first
+    // first-layer B operands: v (bf16 copy), agg (fp32 rounded to bf16)
+    uint4 xv[1][NKH], xa[1][NKH];
+#pragma unroll
+    for (int kg = 0; kg < NKH; ++kg) {
+      xv[0][kg] = active ? *reinterpret_cast<const uint4*>(V16 + src_row * L + kg * 32 + q * 8) : make_uint4(0, 0, 0, 0);
+      float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+      if (active) {
+        const float* ap = a.in1 + src_row * L + kg * 32 + q * 8;
+        x0 = reinterpret_cast<const float4*>(ap)[0];
+        x1 = reinterpret_cast<const float4*>(ap)[1];
+      }
+      xa[0][kg] = make_uint4(bf_pack(x0.x, x0.y), bf_pack(x0.z, x0.w), bf_pack(x1.x, x1.y), bf_pack(x1.z, x1.w));
+    }
+    floatx4 acc[1][NB];
+#pragma unroll
+    for (int c = 0; c < RW_NC; ++c) {
+      advance(2 * c);
+      if (active) rw_gemm<1>(c, buf, xv, acc, ln);
+      __syncthreads();
+      advance(2 * c + 1);
+      if (active) rw_gemm<1, false>(c, buf + RW_CHUNK, xa, acc, ln);
+#pragma unroll
+      for (int cbl = 0; cbl < RW_CB; ++cbl) {
+        const float4 bv = rt_ld4(vb1, c * RW_CB + cbl, q);
+        floatx4& z = acc[0][c * RW_CB + cbl];
+        z[0] = fmaxf(z[0] + bv.x, 0.f);
+        z[1] = fmaxf(z[1] + bv.y, 0.f);
+        z[2] = fmaxf(z[2] + bv.z, 0.f);
+        z[3] = fmaxf(z[3] + bv.w, 0.f);
+      }
+      __syncthreads();
+    }
+    uint4 xf[1][NKH];
+    {
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[0][cb][r];
+      rt_frags<NB>(h, xf[0]);
+      if (a.hid_out && active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid_out) + row * L, q, xf[0], ok);
+    }
+    if (!a.out) continue;  // only h_1 wanted (launch-uniform)
+    int p = Lay::NCH0;
+    if constexpr (D == 3) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          const float4 bv = rt_ld4(vbh, c * RW_CB + cbl, q);
+          floatx4& z = acc[0][c * RW_CB + cbl];
+          z[0] = fmaxf(z[0] + bv.x, 0.f);
+          z[1] = fmaxf(z[1] + bv.y, 0.f);
+          z[2] = fmaxf(z[2] + bv.z, 0.f);
+          z[3] = fmaxf(z[3] + bv.w, 0.f);
+        }
+        __syncthreads();
+      }
+      p += RW_NC;
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[0][cb][r];
+      rt_frags<NB>(h, xf[0]);
+    }
+#pragma unroll
+    for (int c = 0; c < RW_NC; ++c) {
+      advance(p + c);
+      if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+      for (int cbl = 0; cbl < RW_CB; ++cbl) {
+        const float4 bv = rt_ld4(vbl, c * RW_CB + cbl, q);
+        floatx4& z = acc[0][c * RW_CB + cbl];
+        z[0] += bv.x;
+        z[1] += bv.y;
+        z[2] += bv.z;
+        z[3] += bv.w;
+      }
+      __syncthreads();
+    }
+    if (!active) continue;
+    float y[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[cb][r] = acc[0][cb][r];
+    const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
+    float dv[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float d = y[cb][r] - mu;
+        dv[cb][r] = d * d;
+      }
+    const float rs = 1.0f / sqrtf(rt_sum4(rt_lane_sum<NB>(dv)) / L + a.eps);
+    // v + gamma * xhat + beta
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float4 g = rt_ld4(vg, cb, q), bt = rt_ld4(vbt, cb, q), v = rt_ld4(a.in0 + src_row * L, cb, q);
+      y[cb][0] = (g.x * ((y[cb][0] - mu) * rs) + bt.x) + v.x;
+      y[cb][1] = (g.y * ((y[cb][1] - mu) * rs) + bt.y) + v.y;
+      y[cb][2] = (g.z * ((y[cb][2] - mu) * rs) + bt.z) + v.z;
+      y[cb][3] = (g.w * ((y[cb][3] - mu) * rs) + bt.w) + v.w;
+    }
+    if (ok) {
+      float* op = reinterpret_cast<float*>(a.out) + row * L;
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+        *reinterpret_cast<float4*>(op + cb * 16 + q * 4) = make_float4(y[cb][0], y[cb][1], y[cb][2], y[cb][3]);
+    }
+    if (a.out16) {
+      uint4 o[NKH];
+      rt_frags<NB>(y, o);
+      rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.out16) + row * L, q, o, ok);
+    }
+  }
+}
+
+template <int D>
+struct RwNodeBwdLay {
+  static constexpr int NWV = 4, NTH = 64 * NWV;
+  static constexpr int OFF_BUF = 0;                        // two chunk buffers
+  static constexpr int OFF_VEC = 2 * RW_CHUNK * 16;        // last bias, gamma[, hidden bias]
+  static constexpr int END = OFF_VEC + (D == 3 ? 3 : 2) * RW_L * 4;
+  static_assert(END <= 160 * 1024, "LDS");
+  static constexpr int NVEC = (D + 2) * RW_L;              // biases, gamma, beta
+  static_assert(NWV * NVEC * 4 <= OFF_VEC, "the partials reuse the chunk buffers");
+  // forward layers 1 .. D-1, backward products of layers D-1 .. 1, then the
+  // first Linear's v and agg column halves
+  static constexpr int NCH = 2 * (D - 1) * RW_NC + 2 * RW_NC;
+  static_assert(NCH % 2 == 0, "the stream's buffer parity repeats every tile");
+};
+
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void rows_rw_bwd_kernel(RowsBwdArgs a) {
+  using Lay = RwNodeBwdLay<D>;
+  constexpr int NTH = Lay::NTH, NB = RW_NB, NKH = RW_NKH, L = RW_L, NCH = Lay::NCH;
+  constexpr int NV = 4 * NB, NR = NV / 16;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* buf = reinterpret_cast<uint4*>(lds + Lay::OFF_BUF);
+  float* vbl = reinterpret_cast<float*>(lds + Lay::OFF_VEC);  // last bias
+  float* vg = vbl + L;                                          // gamma
+  float* vbh = vbl + 2 * L;                                     // hidden bias (D = 3)
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  // backward packing of W_1: 2 x NB column blocks (v, then agg inputs) of NKH k-groups
+  const RwSrc fsrc[2] = {{a.mlp.lin[1].wf, NKH, 0}, {a.mlp.lin[D - 1].wf, NKH, 0}};
+  const RwSrc bsrc[2] = {{a.mlp.lin[1].wb, NKH, 0}, {a.mlp.lin[D - 1].wb, NKH, 0}};
+  const RwSrc isrc[2] = {{a.mlp.lin[0].wb, NKH, 0}, {a.mlp.lin[0].wb + (size_t)NB * NKH * 64, NKH, 0}};
+  const uint32_t vo_perm = rw_thread_off<true>();
+  auto load = [&](RwStage<NTH>& st, int p) {
+    const int pp = p % NCH, j = pp / RW_NC, c = pp % RW_NC;
+    if (j < D - 1) rw_load<NTH, true>(st, fsrc[j == D - 2 ? 1 : 0], c, vo_perm);  // forward layer j + 1
+    else if (j < 2 * (D - 1)) {
+      const int layer = D - 1 - (j - (D - 1));                                 // backward product, D-1 .. 1
+      rw_load<NTH, true>(st, bsrc[layer == D - 1 ? 1 : 0], c, vo_perm);
+    } else {
+      rw_load<NTH, true>(st, isrc[j - 2 * (D - 1)], c, vo_perm);               // dv, then dagg
+    }
+  };
+  RwStage<NTH> stg[2];  // chunks p + 1 and p + 2 in flight at step p
+  load(stg[0], 0);
+  rw_store<NTH>(stg[0], buf);
+  load(stg[1], 1);
+  load(stg[0], 2);
+  rt_copy_vec(vbl, a.mlp.lin[D - 1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  if constexpr (D == 3) rt_copy_vec(vbh, a.mlp.lin[1].b, L);
+  int64_t t0, t1;
+  rw_row_tiles(a.rows, (int64_t)blockIdx.x * Lay::NWV + wave, (int64_t)gridDim.x * Lay::NWV, t0, t1);
+  const int64_t T = (a.rows + 15) / 16, Wt = (int64_t)gridDim.x * Lay::NWV;
+  const int ntile = (int)((T + Wt - 1) / Wt);
+  __syncthreads();
+  // column totals (rt_col_totals' share of each lane): gamma, beta, last
+  // bias, hidden biases
+  constexpr int NQ = 2 + D;
+  float qacc[NQ][NR];
+#pragma unroll
+  for (int k = 0; k < NQ; ++k)
+#pragma unroll
+    for (int t = 0; t < NR; ++t) qacc[k][t] = 0.f;
+  auto advance = [&](int p) {
+    rw_store<NTH>(stg[(p + 1) & 1], buf + ((p + 1) & 1) * RW_CHUNK);
+    load(stg[(p + 1) & 1], p + 3);
+  };
+  for (int t = 0; t < ntile; ++t) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t tile = t0 + t;
+    const bool active = tile < t1;  // wave-uniform
+    const int64_t row = tile * 16 + e;
+    const bool ok = active && row < a.rows;
+    const int64_t src_row = ok ? row : (active ? tile * 16 : 0);
+    uint64_t mask[2] = {0ull, 0ull};  // ReLU derivative of the hidden layers, bit 4 cb + r
+    uint4 xf[1][NKH];
+    floatx4 acc[1][NB];
+    int p = 0;
+    if (active) rw_load_relu(reinterpret_cast<const uint16_t*>(a.hid_in) + src_row * L, q, xf[0], mask[0]);
+    if constexpr (D == 3) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          const int cb = c * RW_CB + cbl;
+          const float4 bv = rt_ld4(vbh, cb, q);
+          const float b4[4] = {bv.x, bv.y, bv.z, bv.w};
+          floatx4& z = acc[0][cb];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float v = z[r] + b4[r];
+            const bool on = v > 0.f;
+            mask[1] |= (uint64_t)on << (cb * 4 + r);
+            z[r] = on ? v : 0.f;
+          }
+        }
+        __syncthreads();
+      }
+      p += RW_NC;
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[0][cb][r];
+      rt_frags<NB>(h, xf[0]);
+      if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[1]) + row * L, q, xf[0], ok);
+    }
+    // dm (fp32), loaded before the last layer's products
+    float dm[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      float4 d4 = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (active) d4 = rt_ld4(a.dm + src_row * L, cb, q);
+      dm[cb][0] = ok ? d4.x : 0.f;
+      dm[cb][1] = ok ? d4.y : 0.f;
+      dm[cb][2] = ok ? d4.z : 0.f;
+      dm[cb][3] = ok ? d4.w : 0.f;
+    }
+    // last layer + bias: y
+#pragma unroll
+    for (int c = 0; c < RW_NC; ++c) {
+      advance(p + c);
+      if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+      for (int cbl = 0; cbl < RW_CB; ++cbl) {
+        const float4 bv = rt_ld4(vbl, c * RW_CB + cbl, q);
+        floatx4& z = acc[0][c * RW_CB + cbl];
+        z[0] += bv.x;
+        z[1] += bv.y;
+        z[2] += bv.z;
+        z[3] += bv.w;
+      }
+      __syncthreads();
+    }
+    p += RW_NC;
+    // LayerNorm recomputed (y becomes xhat), then its backward
+    float gv[NB][4];
+    if (active) {
+      float y[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[cb][r] = acc[0][cb][r];
+      const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
+      float s2 = 0.f;
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d = y[cb][r] - mu;
+          s2 += d * d;
+        }
+      const float rs = 1.0f / sqrtf(rt_sum4(s2) / L + a.eps);
+      float t1s = 0.f, t2s = 0.f;
+      {
+        float tg[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          const float4 g4 = rt_ld4(vg, cb, q);
+          const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            y[cb][r] = (y[cb][r] - mu) * rs;
+            const float d = dm[cb][r] * g[r];
+            t1s += d;
+            t2s += d * y[cb][r];
+            tg[cb * 4 + r] = dm[cb][r] * y[cb][r];
+          }
+        }
+        t1s = rt_sum4(t1s);
+        t2s = rt_sum4(t2s);
+        rt_col_totals<NV>(tg, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[0][tt] += tg[tt];
+      }
+      {
+        float tb[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) tb[cb * 4 + r] = dm[cb][r];
+        rt_col_totals<NV>(tb, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[1][tt] += tb[tt];
+      }
+      {
+        float tl[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          const float4 g4 = rt_ld4(vg, cb, q);
+          const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            gv[cb][r] = rs * (dm[cb][r] * g[r] - t1s / L - y[cb][r] * (t2s / L));
+            tl[cb * 4 + r] = gv[cb][r];
+          }
+        }
+        rt_col_totals<NV>(tl, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[2][tt] += tl[tt];
+      }
+    } else {
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gv[cb][r] = 0.f;
+    }
+    rt_frags<NB>(gv, xf[0]);
+    if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + row * L, q, xf[0], ok);
+    // hidden layers: dz_{j-1} = (dz_j W_j) * [z_{j-1} > 0]
+#pragma unroll
+    for (int j = D - 1; j >= 1; --j) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+        __syncthreads();
+      }
+      p += RW_NC;
+      if (active) {
+        float th[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            gv[cb][r] = ((mask[j - 1] >> (cb * 4 + r)) & 1ull) ? acc[0][cb][r] : 0.f;
+            th[cb * 4 + r] = gv[cb][r];
+          }
+        rt_col_totals<NV>(th, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[3 + (j - 1)][tt] += th[tt];
+      }
+      rt_frags<NB>(gv, xf[0]);
+      if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + row * L, q, xf[0], ok);
+    }
+    // input gradients: dv = dm + dz_0 W_1[:, v-block], dagg = dz_0 W_1[:, agg-block]
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+        __syncthreads();
+      }
+      p += RW_NC;
+      if (ok) {
+        float* op = (pass == 0 ? a.dx0 : a.dx1) + row * L;
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          floatx4 v = acc[0][cb];
+          if (pass == 0) {
+            v[0] += dm[cb][0];
+            v[1] += dm[cb][1];
+            v[2] += dm[cb][2];
+            v[3] += dm[cb][3];
+          }
+          *reinterpret_cast<float4*>(op + cb * 16 + q * 4) = make_float4(v[0], v[1], v[2], v[3]);
         }
       }
     }
@@ -4923,6 +5428,31 @@ bool rows_rt(int prec, int L, int D, int kind) {
   return prec == BF16 && D == 2 && (L == 64 || L == 128) && kind != DECODER;
 }
 
+bool rows_rw(int prec, int L, int D, int kind) {
+  return prec == BF16 && L == 256 && (D == 2 || D == 3) && kind == NODE_BLOCK;
+}
+
+bool rows_keep_h1(int prec, int L, int D) { return rows_rt(prec, L, D, NODE_BLOCK) || rows_rw(prec, L, D, NODE_BLOCK); }
+
+template <int D>
+static hipError_t rows_rw_fwd_t(const RowsFwdArgs& a, hipStream_t st) {
+  using Lay = RwNodeFwdLay<D>;
+  if (a.rows == 0) return hipSuccess;
+  if (!a.in0_16 || !a.in1 || (a.out && !a.in0)) return hipErrorInvalidValue;
+  allow_lds(rows_rw_fwd_kernel<D>, Lay::END);
+  hipLaunchKernelGGL((rows_rw_fwd_kernel<D>), dim3(RS_GRID), dim3(Lay::NTH), Lay::END, st, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t rows_rw_bwd_t(const RowsBwdArgs& a, hipStream_t st) {
+  using Lay = RwNodeBwdLay<D>;
+  if (!a.hid_in || a.nvec != Lay::NVEC) return hipErrorInvalidValue;
+  allow_lds(rows_rw_bwd_kernel<D>, Lay::END);
+  hipLaunchKernelGGL((rows_rw_bwd_kernel<D>), dim3(RS_GRID), dim3(Lay::NTH), Lay::END, st, a);
+  return hipGetLastError();
+}
+
 template <int L, int KIND>
 static hipError_t rows_rt_fwd_t(const RowsFwdArgs& a, hipStream_t st) {
   using Lay = RtRowsLay<L, KIND>;
@@ -4953,6 +5483,7 @@ int rows_rt_w1_parts(int prec, int L, int D, int kind, int fin) {
 }
 
 hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st) {
+  if (rows_rw(prec, L, D, kind)) return D == 2 ? rows_rw_fwd_t<2>(a, st) : rows_rw_fwd_t<3>(a, st);
   if (rows_rt(prec, L, D, kind)) {
     if (L == 64) {
       if (kind == ENC_NODE) return rows_rt_fwd_t<64, ENC_NODE>(a, st);
@@ -4989,7 +5520,8 @@ static bool rows_rt_bwd(int prec, int L, int D, int kind, bool hid_in) {
 }
 
 int rows_bwd_grid(int prec, int L, int D, int kind, int grid) {
-  return rows_rs(prec, L, D, kind) || rows_rt_bwd(prec, L, D, kind, false) ? RS_GRID : grid;
+  return rows_rs(prec, L, D, kind) || rows_rt_bwd(prec, L, D, kind, false) || rows_rw(prec, L, D, kind) ? RS_GRID
+                                                                                                       : grid;
 }
 
 template <int L, int KIND>
@@ -5001,6 +5533,7 @@ static hipError_t rows_bwd_rs_t(const RowsBwdArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st) {
+  if (rows_rw(prec, L, D, kind)) return D == 2 ? rows_rw_bwd_t<2>(a, st) : rows_rw_bwd_t<3>(a, st);
   if (rows_rt_bwd(prec, L, D, kind, a.hid_in != nullptr)) {
     if (L == 64) {
       if (kind == ENC_NODE) return rows_rt_bwd_t<64, ENC_NODE>(a, st);
