@@ -274,7 +274,10 @@ WsPlan make_plan(const mgn_model* m, const mgn_graph* g) {
   p.PROJ = edge_rs(m->prec, m->L, m->D) ? take(4 * (size_t)(one ? 1 : p.h1_first + (nh1 > 0)) * nl * 2 * L)
            : edge_rsb(m->prec, m->L, m->D) ? take(4 * (size_t)nl * 2 * L)  // l = 256 forward: the current block's
            : 0;
-  p.AGG = take(4 * (size_t)(one ? 1 : K) * no * L);
+  // aggregated messages: every block's; (checkpointing) two slots, block k's
+  // in slot k % 2, so that the backward's recompute of e^k leaves agg^{k-1}
+  // in place for the next block; (inference) one
+  p.AGG = take(4 * (size_t)(p.infer ? 1 : p.lean ? 2 : K) * no * L);
   // edge stream: every block's input, the checkpoints plus one working copy,
   // or (inference) one copy updated in place
   p.ES = take(ts * (size_t)(p.infer ? 1 : p.lean ? p.nck + 1 : std::max<int64_t>(K, 1)) * ne * L);
@@ -704,7 +707,7 @@ struct Views {
         bf16(m->prec == BF16) {}
   // fp32 node latents v^k (owned rows): every block's, or a ping-pong pair when checkpointing
   float* V(int k) const { return (float*)(ws + p.V) + (size_t)(p.lean || p.infer ? (k & 1) : k) * no * L; }
-  float* AGG(int k) const { return (float*)(ws + p.AGG) + (size_t)(p.lean || p.infer ? 0 : k) * no * L; }
+  float* AGG(int k) const { return (float*)(ws + p.AGG) + (size_t)(p.infer ? 0 : p.lean ? (k & 1) : k) * no * L; }
   // edge latents e^k: every block's, or the checkpoint slots plus one working slot
   void* ES(int k) const {
     const int slot = p.infer ? 0 : !p.lean ? k : (k % p.s == 0 ? k / p.s : p.nck);
@@ -958,15 +961,26 @@ struct Bwd {
     const int b_ = 1 - a_;
     const float* Hk = nh > 0 ? m->halo + (size_t)k * nh * L : nullptr;
     if (p.lean) {
-      // e^k: the edge forwards of blocks b0 .. k-1 from the checkpoint e^{b0};
-      // then block k's forward once more for agg^k (and its projections)
+      // e^k: the edge forwards of blocks b0 .. k-1 from the checkpoint e^{b0}
+      // (their aggregates into block k-1's slot: the last one is agg^{k-1},
+      // which block k-1's backward then reads).  agg^k is in block k's slot
+      // when block k+1's recompute ended with block k; otherwise block k's
+      // forward runs once more for it.
       const int b0 = k - k % p.s;
       for (int j = b0; j < k; ++j) {
-        e = edge_forward_block(m, *g, p, ws, m->halo, j, b.V(j), b.V16(j), b.ES(j), b.ES(j + 1), b.AGG(0), st);
+        e = edge_forward_block(m, *g, p, ws, m->halo, j, b.V(j), b.V16(j), b.ES(j), b.ES(j + 1), b.AGG(k - 1), st);
         CHK("edge-stream recompute");
       }
-      e = edge_forward_block(m, *g, p, ws, m->halo, k, b.V(k), b.V16(k), b.ES(k), nullptr, b.AGG(0), st);
-      CHK("aggregate recompute");
+      const bool have_agg = k + 1 < K && (k + 1) % p.s != 0;
+      if (!have_agg) {
+        e = edge_forward_block(m, *g, p, ws, m->halo, k, b.V(k), b.V16(k), b.ES(k), nullptr, b.AGG(k), st);
+        CHK("aggregate recompute");
+      } else if ((edge_rs(m->prec, L, D) || edge_rsb(m->prec, L, D)) && no > 0) {
+        // block k's node projections for its edge backward (the slot holds block k-1's)
+        Timed t_(m, MGN_T_NODE_PROJ, st);
+        e = launch_node_proj(L, b.V16(k), no + nh, dev_mlp(m, m->edge(k)).lin[0], proj_block(p, ws, k, no + nh, L), st);
+        CHK("projections");
+      }
     }
     {
       const MlpL& ml = m->node(k);
