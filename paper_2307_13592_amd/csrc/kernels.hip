@@ -1516,48 +1516,6 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(EdgeWpe<L>::
   }
 }
 
-// Node projections for the l = 256 row-split forward: P[n] = [W_s v_n |
-// W_r v_n + b_1] (fp32) for 64 node rows per tile, v_n the bf16 copy; the
-// sender and receiver k-ranges of the packed W_1.
-template <int L>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void node_proj_big_kernel(
-    const uint16_t* __restrict__ V16, int64_t n_local, Lin w1, float* __restrict__ proj) {
-  using P = PBF16;
-  constexpr int TE = 64, LDA = L + P::PAD, MB = TE / 16, NBW = L / 16 / NW, NKH = L / P::KG, NK1 = 3 * L / P::KG;
-  constexpr int CPR = L / 8;
-  __shared__ __align__(16) uint16_t A[TE * LDA];
-  const int wave = threadIdx.x >> 6, tid = threadIdx.x, nb0 = wave * NBW;
-  for (int64_t t = blockIdx.x; t * TE < n_local; t += gridDim.x) {
-    const int64_t n0 = t * TE;
-    const int n = (int)(n_local - n0 < TE ? n_local - n0 : TE);
-    for (int i = tid; i < TE * CPR; i += NT) {
-      const int r = i / CPR, c = (i % CPR) * 8;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (r < n) v = *reinterpret_cast<const uint4*>(V16 + (n0 + r) * L + c);
-      *reinterpret_cast<uint4*>(A + r * LDA + c) = v;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int side = 0; side < 2; ++side) {
-      floatx4 acc[MB][NBW];
-      wave_gemm_k<P, MB, NBW, NKH, true, NK1>(A, LDA, w1.wf + (size_t)(1 + side) * NKH * 64, nb0, acc);
-#pragma unroll
-      for (int nn = 0; nn < NBW; ++nn) {
-        const int col = (nb0 + nn) * 16 + acc_col();
-        const float bv = side ? w1.b[col] : 0.f;  // the first Linear's bias rides with the receiver half
-#pragma unroll
-        for (int m = 0; m < MB; ++m)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = m * 16 + acc_row(r);
-            if (row < n) proj[(n0 + row) * (2 * L) + side * L + col] = acc[m][nn][r] + bv;
-          }
-      }
-    }
-    __syncthreads();
-  }
-}
-
 // ------------------------------------------------ row-split edge kernels ---
 // bf16, latent 64 or 128.  The first Linear of the edge MLP acts on
 // [e | v_s | v_r]; its sender and receiver blocks are applied per node once
@@ -2515,7 +2473,9 @@ struct RwSrc {
 // accumulator (T) order, as rt_copy_frags does; else plain (B from rows).
 template <int NTH>
 struct RwStage {
-  uint4 v[RW_CHUNK / NTH];
+  // native vectors (a uint4 struct copy can leave the stage in scratch memory)
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 v[RW_CHUNK / NTH];
 };
 // Thread tid's byte offset within a chunk's k-group run: element i = tid +
 // j NTH of the share is column block i / 512 and k-group (i / 64) % 8 of the
@@ -2547,16 +2507,17 @@ __device__ __forceinline__ void rw_load(RwStage<NTH>& s, const RwSrc src, int c,
     if constexpr (PERM) {
       const uint2 lo = *reinterpret_cast<const uint2*>(base + f);
       const uint2 hi = *reinterpret_cast<const uint2*>(base + f + 512u);
-      s.v[j] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      s.v[j] = typename RwStage<NTH>::u32x4{lo.x, lo.y, hi.x, hi.y};
     } else {
-      s.v[j] = *reinterpret_cast<const uint4*>(base + f);
+      s.v[j] = *reinterpret_cast<const typename RwStage<NTH>::u32x4*>(base + f);
     }
   }
 }
 template <int NTH>
 __device__ __forceinline__ void rw_store(const RwStage<NTH>& s, uint4* buf) {
 #pragma unroll
-  for (int j = 0; j < RW_CHUNK / NTH; ++j) buf[(int)threadIdx.x + j * NTH] = s.v[j];
+  for (int j = 0; j < RW_CHUNK / NTH; ++j)
+    *reinterpret_cast<typename RwStage<NTH>::u32x4*>(buf + (int)threadIdx.x + j * NTH) = s.v[j];
 }
 
 // acc[s][4 c + cbl] = sum over k-groups of the chunk's fragments (LDS) times
@@ -3784,6 +3745,89 @@ void rows_rw_bwd_kernel(RowsBwdArgs a) {
     float tsum = 0.f;
     for (int w = 0; w < Lay::NWV; ++w) tsum += red[w * Lay::NVEC + i];
     vp[i] = tsum;
+  }
+}
+
+// Node projections at l = 256 in the streamed-weight form: P[n] = [W_s v_n |
+// W_r v_n + b_1] (fp32), v_n the bf16 copy; per 16-row tile of a wave the
+// sender then the receiver k-range of the packed W_1 stream through LDS in
+// column chunks, and each chunk's accumulators go out as 16-byte row pieces.
+struct RwProjLay {
+  static constexpr int NWV = 8, NTH = 64 * NWV;
+  static constexpr int OFF_BUF = 0;                        // two chunk buffers
+  static constexpr int OFF_VEC = 2 * RW_CHUNK * 16;        // b_1
+  static constexpr int END = OFF_VEC + RW_L * 4;
+  static constexpr int NCH = 2 * RW_NC;
+  static_assert(END <= 160 * 1024 && NCH % 2 == 0, "");
+};
+
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void node_proj_rw_kernel(const uint16_t* __restrict__ V16, int64_t n_local, Lin w1, float* __restrict__ proj) {
+  using Lay = RwProjLay;
+  constexpr int NTH = Lay::NTH, NKH = RW_NKH, L = RW_L;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* buf = reinterpret_cast<uint4*>(lds + Lay::OFF_BUF);
+  float* vb1 = reinterpret_cast<float*>(lds + Lay::OFF_VEC);
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const uint32_t vo_plain = rw_thread_off<false>();
+  auto load = [&](RwStage<NTH>& st, int p) {
+    // the sender k-range of the packed W_1, then the receiver one
+    const int pp = p % Lay::NCH;
+    rw_load<NTH, false>(st, RwSrc{w1.wf, 3 * NKH, (1 + pp / RW_NC) * NKH}, pp % RW_NC, vo_plain);
+  };
+  RwStage<NTH> stg;
+  load(stg, 0);
+  rw_store<NTH>(stg, buf);
+  load(stg, 1);
+  rt_copy_vec(vb1, w1.b, L);
+  int64_t t0, t1;
+  rw_row_tiles(n_local, (int64_t)blockIdx.x * Lay::NWV + wave, (int64_t)gridDim.x * Lay::NWV, t0, t1);
+  const int64_t T = (n_local + 15) / 16, Wt = (int64_t)gridDim.x * Lay::NWV;
+  const int ntile = (int)((T + Wt - 1) / Wt);
+  __syncthreads();
+  auto advance = [&](int p) {
+    rw_store<NTH>(stg, buf + ((p + 1) & 1) * RW_CHUNK);
+    load(stg, p + 2);
+  };
+  for (int t = 0; t < ntile; ++t) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t tile = t0 + t;
+    const bool active = tile < t1;  // wave-uniform
+    const int64_t row = tile * 16 + e;
+    const bool ok = active && row < n_local;
+    const int64_t src_row = ok ? row : (active ? tile * 16 : 0);
+    uint4 xv[1][NKH];
+#pragma unroll
+    for (int kg = 0; kg < NKH; ++kg)
+      xv[0][kg] = active ? *reinterpret_cast<const uint4*>(V16 + src_row * L + kg * 32 + q * 8) : make_uint4(0, 0, 0, 0);
+    floatx4 acc[1][RW_NB];
+#pragma unroll
+    for (int side = 0; side < 2; ++side)
+#pragma unroll
+    for (int c = 0; c < RW_NC; ++c) {
+      const int p = side * RW_NC + c;
+      advance(p);
+      if (active) rw_gemm<1>(c, buf + (p & 1) * RW_CHUNK, xv, acc, ln);
+      if (ok) {
+        float* op = proj + row * (2 * L) + side * L;
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          const int cb = c * RW_CB + cbl;
+          floatx4 z = acc[0][cb];
+          if (side) {  // the first Linear's bias rides with the receiver half
+            const float4 bv = rt_ld4(vb1, cb, q);
+            z[0] += bv.x;
+            z[1] += bv.y;
+            z[2] += bv.z;
+            z[3] += bv.w;
+          }
+          *reinterpret_cast<float4*>(op + cb * 16 + q * 4) = make_float4(z[0], z[1], z[2], z[3]);
+        }
+      }
+      __syncthreads();
+    }
   }
 }
 
@@ -5598,8 +5642,8 @@ hipError_t launch_node_proj(int L, const void* v16, int64_t n_local, const Lin& 
   if (L == 64) return node_proj_t<64>(v16, n_local, w1, proj, st);
   if (L == 128) return node_proj_t<128>(v16, n_local, w1, proj, st);
   if (L == 256) {
-    const int64_t tiles = (n_local + 63) / 64;
-    hipLaunchKernelGGL(node_proj_big_kernel<256>, dim3((unsigned)(tiles < 4096 ? tiles : 4096)), dim3(NT), 0, st,
+    allow_lds(node_proj_rw_kernel, RwProjLay::END);
+    hipLaunchKernelGGL(node_proj_rw_kernel, dim3(RS_GRID), dim3(RwProjLay::NTH), RwProjLay::END, st,
                        reinterpret_cast<const uint16_t*>(v16), n_local, w1, proj);
     return hipGetLastError();
   }
