@@ -154,6 +154,7 @@ def oracle_sensitivity(c, latent, K, depth, prec, g=None, nf=None, ef=None, halo
         x = synth.perturbed((nf, ef, halo), i, rel)
         r = run_oracle(c, latent, K, depth, d_out=d_out, g=g, nf=x[0], ef=x[1], halo=x[2], bf16=prec == "bf16")
         res.append((r["out"], r["d_params"], r["d_halo"]))
+        say(f"  oracle sensitivity run {i} of {runs}")
     return res
 
 

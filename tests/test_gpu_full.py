@@ -70,6 +70,7 @@ def _session(name, cfg, case, g, loc, h1_stash=None):
     return s
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["C3", "C4", "C5"])
 def test_sampled_outputs_and_gradients(name):
     cfg = synth.CONFIGS[name]
@@ -100,7 +101,11 @@ def test_sampled_outputs_and_gradients(name):
     say(f"[full] {name}: oracle done")
     cal = calibrate(sub, l, K, D, cfg.precision, runs=4)
     say(f"[full] {name}: calibration done")
-    sens = oracle_sensitivity(sub, l, K, D, cfg.precision, runs=3)
+    # K = 15 blocks amplify float32-level input noise into movements of
+    # 0.1-0.7 in some bf16 gradient tensors (ReLU flips); eight runs sample
+    # that spread (three missed the largest movement of block 10's node
+    # Linear at C5, 0.22, which the oracle alone reaches in one of eight)
+    sens = oracle_sensitivity(sub, l, K, D, cfg.precision, runs=8)
     say(f"[full] {name}: oracle sensitivity done")
     # outputs at the sampled nodes only
     e_out = rel_err(out[centers], ref["out"][c["centers_sub"]])
