@@ -1574,6 +1574,14 @@ __device__ __forceinline__ void rs_copy_frags(uint4* dst, const uint4* __restric
 // The wave's index in its workgroup, as a wave-uniform (scalar) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
+// A wave-uniform value held in scalar registers.
+__device__ __forceinline__ int64_t rs_uniform(int64_t x) {
+  const uint64_t u = (uint64_t)x;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 // Receiver range of wave w (of W waves in total) within [lo_r, hi_r):
 // receiver-aligned, about E / W edges each; the waves of one XCD
 // (blockIdx % 8) get neighbouring ranges.
@@ -1923,7 +1931,7 @@ __global__ __launch_bounds__((RsFwdLay<L, D>::NTH)) void edge_fwd_rs_kernel(Edge
   int64_t r0, r1;
   rs_range(a.row_ptr, 0, a.n_owned, r0, r1);
   rs_zero_empty(a.row_ptr, r0, r1, a.agg, L);
-  const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
+  const int64_t E0 = rs_uniform(a.row_ptr[r0]), E1 = rs_uniform(a.row_ptr[r1]);  // wave-uniform
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
   uint16_t* Eout = reinterpret_cast<uint16_t*>(a.Eout);
   float run[(L + 63) / 64] = {};  // running receiver sums, columns lane + 64 j
@@ -2099,7 +2107,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
   int64_t r0, r1;
   rs_range(a.row_ptr, a.r_lo, a.r_hi, r0, r1);
   rs_zero_empty(a.row_ptr, r0, r1, a.dagg, L);
-  const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
+  const int64_t E0 = rs_uniform(a.row_ptr[r0]), E1 = rs_uniform(a.row_ptr[r1]);  // wave-uniform
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
   // column totals of the bias / LayerNorm gradients (rt_col_totals' share of
   // each lane): gamma, beta, last bias, hidden biases
@@ -2633,7 +2641,8 @@ void edge_fwd_rw_kernel(EdgeFwdArgs a) {
   int64_t r0, r1;
   rs_range(a.row_ptr, 0, a.n_owned, r0, r1);
   rs_zero_empty(a.row_ptr, r0, r1, a.agg, L);
-  const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
+  // wave-uniform bounds, kept in scalar registers
+  const int64_t E0 = rs_uniform(a.row_ptr[r0]), E1 = rs_uniform(a.row_ptr[r1]);
   const int ntile = rw_max_tiles((int)((E1 - E0 + TE - 1) / TE), reinterpret_cast<int*>(lds + Lay::OFF_SLOT));
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
   uint16_t* Eout = reinterpret_cast<uint16_t*>(a.Eout);
@@ -2915,7 +2924,7 @@ void edge_bwd_rw_kernel(EdgeBwdArgs a) {
   int64_t r0, r1;
   rs_range(a.row_ptr, a.r_lo, a.r_hi, r0, r1);
   rs_zero_empty(a.row_ptr, r0, r1, a.dagg, L);
-  const int64_t E0 = a.row_ptr[r0], E1 = a.row_ptr[r1];
+  const int64_t E0 = rs_uniform(a.row_ptr[r0]), E1 = rs_uniform(a.row_ptr[r1]);  // wave-uniform
   const int ntile = rw_max_tiles((int)((E1 - E0 + 15) / 16), reinterpret_cast<int*>(lds + Lay::OFF_SLOT));
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
   // column totals of the bias / LayerNorm gradients (rt_col_totals' share of
