@@ -169,8 +169,9 @@ int plan_chunk_receivers();
 // (RowsFwdArgs::hid_out -> RowsBwdArgs::hid_in); without it the older
 // row-split kernel recomputes it.
 bool rows_rt(int prec, int L, int D, int kind);
-// bf16, l = 256 node half: the streamed-weight row kernels (the backward
-// starts from the forward's first-Linear ReLU output, RowsBwdArgs::hid_in).
+// bf16, l = 256 node half and edge encoder: the streamed-weight row kernels
+// (the node half's backward starts from the forward's first-Linear ReLU
+// output, RowsBwdArgs::hid_in).
 bool rows_rw(int prec, int L, int D, int kind);
 // Whether the node half's forward keeps its first-Linear ReLU output for the
 // backward (T-form or streamed-weight row kernels).

@@ -3757,6 +3757,528 @@ void rows_rw_bwd_kernel(RowsBwdArgs a) {
   }
 }
 
+// The edge encoder at l = 256 (bf16) in the same streamed-weight form: its
+// first Linear (input fin <= 4 features, one k-group) stays in LDS for the
+// whole launch, the later layers stream.  Forward: e^0 = LN(MLP(x)) (bf16
+// rows).  Backward: the tile's forward recomputed from x, LayerNorm
+// backward, each layer's output gradient (stored for the weight gradients,
+// with h_1 and h_2) down to dz_0, whose product with x (the first Linear's
+// weight gradient, 256 x fin) each wave accumulates itself: per tile dz_0 and
+// x pass through a per-wave LDS scratch and lane l sums output rows 4 l ..
+// 4 l + 3; bias / LayerNorm column partials per workgroup.
+constexpr int RW_ENC_FIN = 4;
+
+// The tile's first-Linear B operand from fin <= 4 fp32 features (lane group
+// 0 holds k-slots 0 .. 7, the others zero), rounded to bf16.
+__device__ __forceinline__ uint4 rw_enc_input(const float* __restrict__ x, int fin, int64_t row, int q, bool active) {
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (active && q == 0) {
+#pragma unroll
+    for (int j = 0; j < RW_ENC_FIN; ++j)
+      if (j < fin) v[j] = x[row * fin + j];
+  }
+  return make_uint4(bf_pack(v[0], v[1]), bf_pack(v[2], v[3]), bf_pack(v[4], v[5]), bf_pack(v[6], v[7]));
+}
+
+// z_1 = W_1 x + b_1 over every column block, ReLU (mask bits when asked), as
+// accumulators; W_1's NB fragments (one k-group) in LDS.
+__device__ __forceinline__ void rw_enc_first(const uint4* W0, const float* vb1, const uint4 x, int lane,
+                                             floatx4 (&acc)[1][RW_NB], uint64_t* mask) {
+  const int q = lane >> 4;
+#pragma unroll
+  for (int cb = 0; cb < RW_NB; ++cb) {
+    acc[0][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    PBF16::mma(acc[0][cb], W0[cb * 64 + lane], x);
+    const float4 bv = rt_ld4(vb1, cb, q);
+    const float b4[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float v = acc[0][cb][r] + b4[r];
+      const bool on = v > 0.f;
+      if (mask) *mask |= (uint64_t)on << (cb * 4 + r);
+      acc[0][cb][r] = on ? v : 0.f;
+    }
+  }
+}
+
+template <int D>
+struct RwEncFwdLay {
+  static constexpr int NWV = 8, NTH = 64 * NWV;
+  static constexpr int OFF_BUF = 0;                        // two chunk buffers
+  static constexpr int OFF_W0 = 2 * RW_CHUNK * 16;         // first Linear, NB fragments
+  static constexpr int OFF_VEC = OFF_W0 + RW_NB * 64 * 16;  // b_1, last bias, gamma, beta[, hidden bias]
+  static constexpr int END = OFF_VEC + (D == 3 ? 5 : 4) * RW_L * 4;
+  static_assert(END <= 160 * 1024, "LDS");
+  static constexpr int NCH = (D - 1) * RW_NC;
+  static_assert(NCH % 2 == 0, "the stream's buffer parity repeats every tile");
+};
+
+template <int D>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void rows_rw_enc_fwd_kernel(RowsFwdArgs a) {
+  using Lay = RwEncFwdLay<D>;
+  constexpr int NTH = Lay::NTH, NB = RW_NB, NKH = RW_NKH, L = RW_L, NCH = Lay::NCH;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* buf = reinterpret_cast<uint4*>(lds + Lay::OFF_BUF);
+  uint4* W0 = reinterpret_cast<uint4*>(lds + Lay::OFF_W0);
+  float* vb1 = reinterpret_cast<float*>(lds + Lay::OFF_VEC);  // first bias
+  float* vbl = vb1 + L;                                         // last bias
+  float* vg = vb1 + 2 * L;                                      // gamma
+  float* vbt = vb1 + 3 * L;                                     // beta
+  float* vbh = vb1 + 4 * L;                                     // hidden bias (D = 3)
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const RwSrc src[2] = {{a.mlp.lin[1].wf, NKH, 0}, {a.mlp.lin[D - 1].wf, NKH, 0}};
+  const uint32_t vo_perm = rw_thread_off<true>();
+  auto load = [&](RwStage<NTH>& st, int p) {
+    const int pp = p % NCH, j = pp / RW_NC + 1, c = pp % RW_NC;  // layer 1 .. D-1
+    rw_load<NTH, true>(st, src[j == D - 1 ? 1 : 0], c, vo_perm);
+  };
+  RwStage<NTH> stg;
+  load(stg, 0);
+  rw_store<NTH>(stg, buf);
+  load(stg, 1);
+  rs_copy_frags(W0, a.mlp.lin[0].wf, NB, 1, a.mlp.lin[0].nkgf, 0);
+  rt_copy_vec(vb1, a.mlp.lin[0].b, L);
+  rt_copy_vec(vbl, a.mlp.lin[D - 1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  rt_copy_vec(vbt, a.mlp.beta, L);
+  if constexpr (D == 3) rt_copy_vec(vbh, a.mlp.lin[1].b, L);
+  int64_t t0, t1;
+  rw_row_tiles(a.rows, (int64_t)blockIdx.x * Lay::NWV + wave, (int64_t)gridDim.x * Lay::NWV, t0, t1);
+  const int64_t T = (a.rows + 15) / 16, Wt = (int64_t)gridDim.x * Lay::NWV;
+  const int ntile = (int)((T + Wt - 1) / Wt);
+  __syncthreads();
+  auto advance = [&](int p) {
+    rw_store<NTH>(stg, buf + ((p + 1) & 1) * RW_CHUNK);
+    load(stg, p + 2);
+  };
+  uint16_t* out = reinterpret_cast<uint16_t*>(a.out);
+  for (int t = 0; t < ntile; ++t) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t tile = t0 + t;
+    const bool active = tile < t1;  // wave-uniform
+    const int64_t row = tile * 16 + e;
+    const bool ok = active && row < a.rows;
+    const int64_t src_row = ok ? row : (active ? tile * 16 : 0);
+    floatx4 acc[1][NB];
+    rw_enc_first(W0, vb1, rw_enc_input(a.in0, a.fin, src_row, q, active), ln, acc, nullptr);
+    uint4 xf[1][NKH];
+    {
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[0][cb][r];
+      rt_frags<NB>(h, xf[0]);
+    }
+    int p = 0;
+    if constexpr (D == 3) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          const float4 bv = rt_ld4(vbh, c * RW_CB + cbl, q);
+          floatx4& z = acc[0][c * RW_CB + cbl];
+          z[0] = fmaxf(z[0] + bv.x, 0.f);
+          z[1] = fmaxf(z[1] + bv.y, 0.f);
+          z[2] = fmaxf(z[2] + bv.z, 0.f);
+          z[3] = fmaxf(z[3] + bv.w, 0.f);
+        }
+        __syncthreads();
+      }
+      p += RW_NC;
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[0][cb][r];
+      rt_frags<NB>(h, xf[0]);
+    }
+#pragma unroll
+    for (int c = 0; c < RW_NC; ++c) {
+      advance(p + c);
+      if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+      for (int cbl = 0; cbl < RW_CB; ++cbl) {
+        const float4 bv = rt_ld4(vbl, c * RW_CB + cbl, q);
+        floatx4& z = acc[0][c * RW_CB + cbl];
+        z[0] += bv.x;
+        z[1] += bv.y;
+        z[2] += bv.z;
+        z[3] += bv.w;
+      }
+      __syncthreads();
+    }
+    if (!active) continue;
+    float y[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[cb][r] = acc[0][cb][r];
+    const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
+    float dv[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float d = y[cb][r] - mu;
+        dv[cb][r] = d * d;
+      }
+    const float rs = 1.0f / sqrtf(rt_sum4(rt_lane_sum<NB>(dv)) / L + a.eps);
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float4 g = rt_ld4(vg, cb, q), bt = rt_ld4(vbt, cb, q);
+      y[cb][0] = g.x * ((y[cb][0] - mu) * rs) + bt.x;
+      y[cb][1] = g.y * ((y[cb][1] - mu) * rs) + bt.y;
+      y[cb][2] = g.z * ((y[cb][2] - mu) * rs) + bt.z;
+      y[cb][3] = g.w * ((y[cb][3] - mu) * rs) + bt.w;
+    }
+    uint4 o[NKH];
+    rt_frags<NB>(y, o);
+    rt_store_frags<NKH>(out + row * L, q, o, ok);
+  }
+}
+
+template <int D>
+struct RwEncBwdLay {
+  static constexpr int NWV = 4, NTH = 64 * NWV;
+  static constexpr int OFF_BUF = 0;                        // two chunk buffers
+  static constexpr int OFF_W0 = 2 * RW_CHUNK * 16;         // first Linear, NB fragments
+  static constexpr int OFF_VEC = OFF_W0 + RW_NB * 64 * 16;  // b_1, last bias, gamma[, hidden bias]
+  static constexpr int OFF_SCR = OFF_VEC + (D == 3 ? 4 : 3) * RW_L * 4;
+  // per wave: a tile's dz_0 (16 rows of l bf16, 8 columns of padding) and features
+  static constexpr int DZS = RW_L + 8;
+  static constexpr int SCR = 16 * DZS * 2 + 16 * RW_ENC_FIN * 2;
+  static constexpr int END = OFF_SCR + NWV * SCR;
+  static_assert(END <= 160 * 1024, "LDS");
+  static constexpr int NVEC = (D + 2) * RW_L;              // biases, gamma, beta
+  static_assert(NWV * NVEC * 4 <= OFF_W0, "the partials reuse the chunk buffers");
+  // forward layers 1 .. D-1, then the backward products of layers D-1 .. 1
+  static constexpr int NCH = 2 * (D - 1) * RW_NC;
+  static_assert(NCH % 2 == 0, "the stream's buffer parity repeats every tile");
+};
+
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void rows_rw_enc_bwd_kernel(RowsBwdArgs a) {
+  using Lay = RwEncBwdLay<D>;
+  constexpr int NTH = Lay::NTH, NB = RW_NB, NKH = RW_NKH, L = RW_L, NCH = Lay::NCH;
+  constexpr int NV = 4 * NB, NR = NV / 16, OPL = L / 64;
+  extern __shared__ __align__(16) unsigned char lds[];
+  uint4* buf = reinterpret_cast<uint4*>(lds + Lay::OFF_BUF);
+  uint4* W0 = reinterpret_cast<uint4*>(lds + Lay::OFF_W0);
+  float* vb1 = reinterpret_cast<float*>(lds + Lay::OFF_VEC);  // first bias
+  float* vbl = vb1 + L;                                         // last bias
+  float* vg = vb1 + 2 * L;                                      // gamma
+  float* vbh = vb1 + 3 * L;                                     // hidden bias (D = 3)
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  uint16_t* dzs = reinterpret_cast<uint16_t*>(lds + Lay::OFF_SCR + wave * Lay::SCR);
+  uint16_t* xs = dzs + 16 * Lay::DZS;
+  const RwSrc fsrc[2] = {{a.mlp.lin[1].wf, NKH, 0}, {a.mlp.lin[D - 1].wf, NKH, 0}};
+  const RwSrc bsrc[2] = {{a.mlp.lin[1].wb, NKH, 0}, {a.mlp.lin[D - 1].wb, NKH, 0}};
+  const uint32_t vo_perm = rw_thread_off<true>();
+  auto load = [&](RwStage<NTH>& st, int p) {
+    const int pp = p % NCH, j = pp / RW_NC, c = pp % RW_NC;
+    if (j < D - 1) rw_load<NTH, true>(st, fsrc[j == D - 2 ? 1 : 0], c, vo_perm);  // forward layer j + 1
+    else {
+      const int layer = D - 1 - (j - (D - 1));                                 // backward product, D-1 .. 1
+      rw_load<NTH, true>(st, bsrc[layer == D - 1 ? 1 : 0], c, vo_perm);
+    }
+  };
+  RwStage<NTH> stg[2];  // chunks p + 1 and p + 2 in flight at step p
+  load(stg[0], 0);
+  rw_store<NTH>(stg[0], buf);
+  load(stg[1], 1);
+  load(stg[0], 2);
+  rs_copy_frags(W0, a.mlp.lin[0].wf, NB, 1, a.mlp.lin[0].nkgf, 0);
+  rt_copy_vec(vb1, a.mlp.lin[0].b, L);
+  rt_copy_vec(vbl, a.mlp.lin[D - 1].b, L);
+  rt_copy_vec(vg, a.mlp.gamma, L);
+  if constexpr (D == 3) rt_copy_vec(vbh, a.mlp.lin[1].b, L);
+  int64_t t0, t1;
+  rw_row_tiles(a.rows, (int64_t)blockIdx.x * Lay::NWV + wave, (int64_t)gridDim.x * Lay::NWV, t0, t1);
+  const int64_t T = (a.rows + 15) / 16, Wt = (int64_t)gridDim.x * Lay::NWV;
+  const int ntile = (int)((T + Wt - 1) / Wt);
+  __syncthreads();
+  constexpr int NQ = 2 + D;  // gamma, beta, last bias, hidden biases
+  float qacc[NQ][NR];
+#pragma unroll
+  for (int k = 0; k < NQ; ++k)
+#pragma unroll
+    for (int t = 0; t < NR; ++t) qacc[k][t] = 0.f;
+  const bool fuse_w1 = a.w1_part != nullptr;
+  float w1acc[OPL][RW_ENC_FIN];
+#pragma unroll
+  for (int j = 0; j < OPL; ++j)
+#pragma unroll
+    for (int i = 0; i < RW_ENC_FIN; ++i) w1acc[j][i] = 0.f;
+  auto advance = [&](int p) {
+    rw_store<NTH>(stg[(p + 1) & 1], buf + ((p + 1) & 1) * RW_CHUNK);
+    load(stg[(p + 1) & 1], p + 3);
+  };
+  for (int t = 0; t < ntile; ++t) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int e = ln & 15, q = ln >> 4;
+    const int64_t tile = t0 + t;
+    const bool active = tile < t1;  // wave-uniform
+    const int64_t row = tile * 16 + e;
+    const bool ok = active && row < a.rows;
+    const int64_t src_row = ok ? row : (active ? tile * 16 : 0);
+    uint64_t mask[2] = {0ull, 0ull};  // ReLU derivative of the hidden layers, bit 4 cb + r
+    floatx4 acc[1][NB];
+    uint4 xf[1][NKH];
+    const uint4 x0 = rw_enc_input(a.in0, a.fin, src_row, q, active);
+    // the tile's bf16 features (columns >= fin are zero; rows past the end
+    // get dz_0 = 0 below) for the fused weight gradient
+    if (fuse_w1 && q == 0) *reinterpret_cast<uint2*>(xs + e * RW_ENC_FIN) = make_uint2(x0.x, x0.y);
+    rw_enc_first(W0, vb1, x0, ln, acc, &mask[0]);
+    {
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[0][cb][r];
+      rt_frags<NB>(h, xf[0]);
+      if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[0]) + row * L, q, xf[0], ok);
+    }
+    int p = 0;
+    if constexpr (D == 3) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+        for (int cbl = 0; cbl < RW_CB; ++cbl) {
+          const int cb = c * RW_CB + cbl;
+          const float4 bv = rt_ld4(vbh, cb, q);
+          const float b4[4] = {bv.x, bv.y, bv.z, bv.w};
+          floatx4& z = acc[0][cb];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float v = z[r] + b4[r];
+            const bool on = v > 0.f;
+            mask[1] |= (uint64_t)on << (cb * 4 + r);
+            z[r] = on ? v : 0.f;
+          }
+        }
+        __syncthreads();
+      }
+      p += RW_NC;
+      float h[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[cb][r] = acc[0][cb][r];
+      rt_frags<NB>(h, xf[0]);
+      if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid[1]) + row * L, q, xf[0], ok);
+    }
+    // dm: bf16 rows (dL/de^0 of the bf16 edge stream) or fp32 rows
+    float dm[NB][4];
+    if (a.dm16) {
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) {
+        float lo[4] = {0.f, 0.f, 0.f, 0.f}, hi[4] = {0.f, 0.f, 0.f, 0.f};
+        if (active) rw_unpack(*reinterpret_cast<const uint4*>(a.dm16 + src_row * L + kg * 32 + q * 8), lo, hi);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          dm[2 * kg][r] = ok ? lo[r] : 0.f;
+          dm[2 * kg + 1][r] = ok ? hi[r] : 0.f;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        float4 d4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (active) d4 = rt_ld4(a.dm + src_row * L, cb, q);
+        dm[cb][0] = ok ? d4.x : 0.f;
+        dm[cb][1] = ok ? d4.y : 0.f;
+        dm[cb][2] = ok ? d4.z : 0.f;
+        dm[cb][3] = ok ? d4.w : 0.f;
+      }
+    }
+    // last layer + bias: y
+#pragma unroll
+    for (int c = 0; c < RW_NC; ++c) {
+      advance(p + c);
+      if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+#pragma unroll
+      for (int cbl = 0; cbl < RW_CB; ++cbl) {
+        const float4 bv = rt_ld4(vbl, c * RW_CB + cbl, q);
+        floatx4& z = acc[0][c * RW_CB + cbl];
+        z[0] += bv.x;
+        z[1] += bv.y;
+        z[2] += bv.z;
+        z[3] += bv.w;
+      }
+      __syncthreads();
+    }
+    p += RW_NC;
+    // LayerNorm recomputed (y becomes xhat), then its backward
+    float gv[NB][4];
+    if (active) {
+      float y[NB][4];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[cb][r] = acc[0][cb][r];
+      const float mu = rt_sum4(rt_lane_sum<NB>(y)) / L;
+      float s2 = 0.f;
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float d = y[cb][r] - mu;
+          s2 += d * d;
+        }
+      const float rs = 1.0f / sqrtf(rt_sum4(s2) / L + a.eps);
+      float t1s = 0.f, t2s = 0.f;
+      {
+        float tg[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          const float4 g4 = rt_ld4(vg, cb, q);
+          const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            y[cb][r] = (y[cb][r] - mu) * rs;
+            const float d = dm[cb][r] * g[r];
+            t1s += d;
+            t2s += d * y[cb][r];
+            tg[cb * 4 + r] = dm[cb][r] * y[cb][r];
+          }
+        }
+        t1s = rt_sum4(t1s);
+        t2s = rt_sum4(t2s);
+        rt_col_totals<NV>(tg, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[0][tt] += tg[tt];
+      }
+      {
+        float tb[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) tb[cb * 4 + r] = dm[cb][r];
+        rt_col_totals<NV>(tb, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[1][tt] += tb[tt];
+      }
+      {
+        float tl[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          const float4 g4 = rt_ld4(vg, cb, q);
+          const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            gv[cb][r] = rs * (dm[cb][r] * g[r] - t1s / L - y[cb][r] * (t2s / L));
+            tl[cb * 4 + r] = gv[cb][r];
+          }
+        }
+        rt_col_totals<NV>(tl, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[2][tt] += tl[tt];
+      }
+    } else {
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gv[cb][r] = 0.f;
+    }
+    rt_frags<NB>(gv, xf[0]);
+    if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + row * L, q, xf[0], ok);
+    // hidden layers: dz_{j-1} = (dz_j W_j) * [z_{j-1} > 0]
+#pragma unroll
+    for (int j = D - 1; j >= 1; --j) {
+#pragma unroll
+      for (int c = 0; c < RW_NC; ++c) {
+        advance(p + c);
+        if (active) rw_gemm<1>(c, buf + ((p + c) & 1) * RW_CHUNK, xf, acc, ln);
+        __syncthreads();
+      }
+      p += RW_NC;
+      if (active) {
+        float th[NV];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            gv[cb][r] = ((mask[j - 1] >> (cb * 4 + r)) & 1ull) ? acc[0][cb][r] : 0.f;
+            th[cb * 4 + r] = gv[cb][r];
+          }
+        rt_col_totals<NV>(th, e);
+#pragma unroll
+        for (int tt = 0; tt < NR; ++tt) qacc[3 + (j - 1)][tt] += th[tt];
+      }
+      rt_frags<NB>(gv, xf[0]);
+      if (j > 1 || !fuse_w1) {
+        if (active) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[j - 1]) + row * L, q, xf[0], ok);
+      }
+    }
+    if (fuse_w1 && active) {
+      // dW_1 += dz_0^T x over the tile's 16 rows: dz_0 (bf16, as a stored
+      // delta would hold it) through the wave's scratch; lane l forms output
+      // rows OPL l .. OPL l + OPL - 1, ascending row order
+      {
+        uint16_t* dr = dzs + e * Lay::DZS + q * 8;
+#pragma unroll
+        for (int kg = 0; kg < NKH; ++kg) *reinterpret_cast<uint4*>(dr + kg * 32) = rt_to_plain(xf[0][kg]);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const uint2 xv = *reinterpret_cast<const uint2*>(xs + r * RW_ENC_FIN);
+        const float x4[4] = {__uint_as_float(xv.x << 16), __uint_as_float(xv.x & 0xffff0000u),
+                             __uint_as_float(xv.y << 16), __uint_as_float(xv.y & 0xffff0000u)};
+        const uint2 w = *reinterpret_cast<const uint2*>(dzs + r * Lay::DZS + OPL * lane);
+        const float d[OPL] = {__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                              __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u)};
+#pragma unroll
+        for (int j = 0; j < OPL; ++j)
+#pragma unroll
+          for (int i = 0; i < RW_ENC_FIN; ++i) w1acc[j][i] = fmaf(d[j], x4[i], w1acc[j][i]);
+      }
+    }
+  }
+  // column partials: lane (e, q)'s totals are columns 16 cb + 4 q + r for
+  // index e * NR + t = 4 cb + r; then the waves in order through LDS (the
+  // chunk buffers are free now)
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(lds);
+  {
+    float* rw = red + wave * Lay::NVEC;
+#pragma unroll
+    for (int tt = 0; tt < NR; ++tt) {
+      const int i = (lane & 15) * NR + tt;
+      const int col = (i >> 2) * 16 + (lane >> 4) * 4 + (i & 3);
+#pragma unroll
+      for (int h = 0; h < D - 1; ++h) rw[h * L + col] = qacc[3 + h][tt];
+      rw[(D - 1) * L + col] = qacc[2][tt];
+      rw[D * L + col] = qacc[0][tt];
+      rw[(D + 1) * L + col] = qacc[1][tt];
+    }
+  }
+  __syncthreads();
+  float* vp = a.vpart + (int64_t)blockIdx.x * a.nvec;
+  for (int i = threadIdx.x; i < Lay::NVEC; i += NTH) {
+    float tsum = 0.f;
+    for (int w = 0; w < Lay::NWV; ++w) tsum += red[w * Lay::NVEC + i];
+    vp[i] = tsum;
+  }
+  if (fuse_w1) {
+    float* wp = a.w1_part + ((int64_t)blockIdx.x * Lay::NWV + wave) * L * a.fin;
+#pragma unroll
+    for (int j = 0; j < OPL; ++j)
+#pragma unroll
+      for (int i = 0; i < RW_ENC_FIN; ++i)
+        if (i < a.fin) wp[(OPL * lane + j) * a.fin + i] = w1acc[j][i];
+  }
+}
+
 // Node projections at l = 256 in the streamed-weight form: P[n] = [W_s v_n |
 // W_r v_n + b_1] (fp32), v_n the bf16 copy; per 16-row tile of a wave the
 // sender then the receiver k-range of the packed W_1 stream through LDS in
@@ -5482,7 +6004,7 @@ bool rows_rt(int prec, int L, int D, int kind) {
 }
 
 bool rows_rw(int prec, int L, int D, int kind) {
-  return prec == BF16 && L == 256 && (D == 2 || D == 3) && kind == NODE_BLOCK;
+  return prec == BF16 && L == 256 && (D == 2 || D == 3) && (kind == NODE_BLOCK || kind == ENC_EDGE);
 }
 
 bool rows_keep_h1(int prec, int L, int D) { return rows_rt(prec, L, D, NODE_BLOCK) || rows_rw(prec, L, D, NODE_BLOCK); }
@@ -5494,6 +6016,25 @@ static hipError_t rows_rw_fwd_t(const RowsFwdArgs& a, hipStream_t st) {
   if (!a.in0_16 || !a.in1 || (a.out && !a.in0)) return hipErrorInvalidValue;
   allow_lds(rows_rw_fwd_kernel<D>, Lay::END);
   hipLaunchKernelGGL((rows_rw_fwd_kernel<D>), dim3(RS_GRID), dim3(Lay::NTH), Lay::END, st, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t rows_rw_enc_fwd_t(const RowsFwdArgs& a, hipStream_t st) {
+  using Lay = RwEncFwdLay<D>;
+  if (a.rows == 0) return hipSuccess;
+  if (!a.in0 || !a.out || a.fin < 1 || a.fin > RW_ENC_FIN) return hipErrorInvalidValue;
+  allow_lds(rows_rw_enc_fwd_kernel<D>, Lay::END);
+  hipLaunchKernelGGL((rows_rw_enc_fwd_kernel<D>), dim3(RS_GRID), dim3(Lay::NTH), Lay::END, st, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t rows_rw_enc_bwd_t(const RowsBwdArgs& a, hipStream_t st) {
+  using Lay = RwEncBwdLay<D>;
+  if (!a.in0 || a.fin < 1 || a.fin > RW_ENC_FIN || a.nvec != Lay::NVEC) return hipErrorInvalidValue;
+  allow_lds(rows_rw_enc_bwd_kernel<D>, Lay::END);
+  hipLaunchKernelGGL((rows_rw_enc_bwd_kernel<D>), dim3(RS_GRID), dim3(Lay::NTH), Lay::END, st, a);
   return hipGetLastError();
 }
 
@@ -5531,12 +6072,17 @@ static_assert((int64_t)RS_GRID * RtRowsLay<128, ENC_EDGE>::NWV * 128 * RtRowsLay
                   (int64_t)DWS_WAVES * 16384,
               "w1 partials");
 int rows_rt_w1_parts(int prec, int L, int D, int kind, int fin) {
-  if (!rows_rt(prec, L, D, kind) || kind != ENC_EDGE || fin < 1 || fin > RtRowsLay<128, ENC_EDGE>::W1_FIN) return 0;
+  if (kind != ENC_EDGE || fin < 1) return 0;
+  if (rows_rw(prec, L, D, kind)) return fin <= RW_ENC_FIN ? RS_GRID * RwEncBwdLay<3>::NWV : 0;
+  if (!rows_rt(prec, L, D, kind) || fin > RtRowsLay<128, ENC_EDGE>::W1_FIN) return 0;
   return RS_GRID * RtRowsLay<128, ENC_EDGE>::NWV;
 }
 
 hipError_t launch_rows_fwd(int prec, int L, int D, int kind, const RowsFwdArgs& a, hipStream_t st) {
-  if (rows_rw(prec, L, D, kind)) return D == 2 ? rows_rw_fwd_t<2>(a, st) : rows_rw_fwd_t<3>(a, st);
+  if (rows_rw(prec, L, D, kind)) {
+    if (kind == ENC_EDGE) return D == 2 ? rows_rw_enc_fwd_t<2>(a, st) : rows_rw_enc_fwd_t<3>(a, st);
+    return D == 2 ? rows_rw_fwd_t<2>(a, st) : rows_rw_fwd_t<3>(a, st);
+  }
   if (rows_rt(prec, L, D, kind)) {
     if (L == 64) {
       if (kind == ENC_NODE) return rows_rt_fwd_t<64, ENC_NODE>(a, st);
@@ -5586,7 +6132,10 @@ static hipError_t rows_bwd_rs_t(const RowsBwdArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_rows_bwd(int prec, int L, int D, int kind, const RowsBwdArgs& a, int grid, hipStream_t st) {
-  if (rows_rw(prec, L, D, kind)) return D == 2 ? rows_rw_bwd_t<2>(a, st) : rows_rw_bwd_t<3>(a, st);
+  if (rows_rw(prec, L, D, kind)) {
+    if (kind == ENC_EDGE) return D == 2 ? rows_rw_enc_bwd_t<2>(a, st) : rows_rw_enc_bwd_t<3>(a, st);
+    return D == 2 ? rows_rw_bwd_t<2>(a, st) : rows_rw_bwd_t<3>(a, st);
+  }
   if (rows_rt_bwd(prec, L, D, kind, a.hid_in != nullptr)) {
     if (L == 64) {
       if (kind == ENC_NODE) return rows_rt_bwd_t<64, ENC_NODE>(a, st);
