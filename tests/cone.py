@@ -51,3 +51,15 @@ def cone(g: dict, centers, K: int) -> dict:
     return dict(n_owned=int(owned.size), n_halo=int(halo.size), n_edges=int(idx.size),
                 row_ptr=rp.astype(np.int32), send=s_sub.astype(np.int32),
                 owned=owned, halo=halo - no, edges=idx, centers_sub=sub_id[centers])
+
+
+def cone_digest(c: dict, sub: dict, params) -> str:
+    """sha256 over a cone's graph and its inputs (node and edge features, halo
+    latents, loss gradient, parameters), in that order: ties a stored result
+    to the inputs that regenerate it."""
+    import hashlib
+    h = hashlib.sha256()
+    for a in (c["row_ptr"], c["send"], sub["nf"], sub["ef"], sub["halo"], sub["d_out"], params):
+        h.update(np.ascontiguousarray(a).tobytes())
+    return h.hexdigest()
+

@@ -184,7 +184,9 @@ def compare(name, prec, shapes, gpu, ref, calib=None, halo_sel=None, calib_facto
     must meet the tolerance of the precision.  A gradient tensor must meet
     bound_of(): the tolerance, widened to calib_factor x the distance from the
     oracle of the independent float32 implementation's runs `calib` or of the
-    oracle's own runs on perturbed inputs `sens` (oracle_sensitivity); in
+    oracle's own runs on perturbed inputs `sens` (oracle_sensitivity's runs,
+    or their per-tensor movements as a dict: "d_params" in tensor order and
+    "d_halo", e.g. from a stored fixture); in
     float32 capped at CAP_FP32 unless the oracle's own runs need more.
     Gradients of a ReLU network jump where a pre-activation sits within
     rounding distance of zero, and in bf16 every rounded operand is such a
@@ -203,7 +205,8 @@ def compare(name, prec, shapes, gpu, ref, calib=None, halo_sel=None, calib_facto
     def check(nm, got, want, cal, sen):
         nonlocal worst
         e = rel_err(got, want)
-        ce, se = _max_err(cal, want), _max_err(sen, want)
+        ce = _max_err(cal, want)
+        se = float(sen) if isinstance(sen, (float, np.floating)) else _max_err(sen, want)
         t = bound_of(prec, ce, se, calib_factor)
         rows.append((nm, e, ce, se, t))
         if e / t > worst[1] / worst[2]:
@@ -211,12 +214,14 @@ def compare(name, prec, shapes, gpu, ref, calib=None, halo_sel=None, calib_facto
         if e > t:
             bad.append((nm, e, t))
 
-    for nm, sl in segments(shapes):
+    stored = isinstance(sens, dict)
+    for i, (nm, sl) in enumerate(segments(shapes)):
         check(nm, dp[sl], ref["d_params"][sl], None if calib is None else [cr[1][sl] for cr in calib],
-              None if sens is None else [sr[1][sl] for sr in sens])
+              None if sens is None else (float(sens["d_params"][i]) if stored else [sr[1][sl] for sr in sens]))
     if ref["d_halo"].size:
         check("d_halo", dh if halo_sel is None else dh[:, halo_sel], ref["d_halo"],
-              None if calib is None else [cr[2] for cr in calib], None if sens is None else [sr[2] for sr in sens])
+              None if calib is None else [cr[2] for cr in calib],
+              None if sens is None else (float(sens["d_halo"]) if stored else [sr[2] for sr in sens]))
     log_bounds(name, prec, rows)
     wide = [r for r in rows if r[4] > tol]
     say(f"  {name}: out {rel_err(out, ref['out']):.2e}; tightest {worst[0]} {worst[1]:.2e} (bound {worst[2]:.2e}); "

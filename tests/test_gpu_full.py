@@ -23,6 +23,7 @@ linear in the loss gradient; halo gradients outside the receptive field are
 exactly zero.
 """
 import gc
+import os
 
 import numpy as np
 import pytest
@@ -30,8 +31,8 @@ import pytest
 import synth
 import paper_2307_13592_amd as mgn
 from paper_2307_13592_amd.runner import Session
-from cone import cone
-from parity import TOL, calibrate, compare, oracle_sensitivity, rel_err, run_oracle, say
+from cone import cone, cone_digest
+from parity import TOL, calibrate, compare, rel_err, run_oracle, say
 
 pytestmark = pytest.mark.gpu
 
@@ -101,12 +102,17 @@ def test_sampled_outputs_and_gradients(name):
     say(f"[full] {name}: oracle done")
     cal = calibrate(sub, l, K, D, cfg.precision, runs=4)
     say(f"[full] {name}: calibration done")
-    # K = 15 blocks amplify float32-level input noise into movements of
-    # 0.1-0.7 in some bf16 gradient tensors (ReLU flips); eight runs sample
-    # that spread (three missed the largest movement of block 10's node
-    # Linear at C5, 0.22, which the oracle alone reaches in one of eight)
-    sens = oracle_sensitivity(sub, l, K, D, cfg.precision, runs=8)
-    say(f"[full] {name}: oracle sensitivity done")
+    # the oracle's own movement under float32-level input noise, eight runs
+    # on this cone, written by tests/golden/make_cone_sensitivity.py (oracle
+    # only): K = 15 blocks amplify such noise into movements of 0.1-0.7 in
+    # some bf16 gradient tensors (ReLU flips), and eight runs sample that
+    # spread (three missed the largest movement of block 10's node Linear at
+    # C5, 0.22, which the oracle alone reaches in one of eight)
+    fx = np.load(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                              f"cone_sensitivity_{name}.npz"))
+    assert str(fx["digest"]) == cone_digest(c, sub, case.params), "the stored sensitivity belongs to other inputs"
+    assert list(fx["names"]) == [s[0] for s in case.shapes]
+    sens = {"d_params": fx["sens_d_params"], "d_halo": float(fx["sens_d_halo"])}
     # outputs at the sampled nodes only
     e_out = rel_err(out[centers], ref["out"][c["centers_sub"]])
     ref_c = dict(ref)
