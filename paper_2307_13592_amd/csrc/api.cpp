@@ -77,6 +77,10 @@ struct mgn_model {
   int64_t chunk_edges = 0;      // edges per backward chunk with checkpointing (0: the default)
   // what the last forward used (kept for the backward)
   bool fwd_done = false;
+  // checkpointing: the forward's last block left its aggregate in its slot,
+  // and no backward block has run since (the backward's last block reads it
+  // instead of running that block's edge forward once more)
+  bool agg_last = false;
   mgn_graph g{};
   const float *nf = nullptr, *ef = nullptr, *halo = nullptr;
   float* out = nullptr;
@@ -852,6 +856,7 @@ mgn_status fwd_end(mgn_model* m, hipStream_t st, const char* fn) {
   }
   if (e != hipSuccess) return hip_fail(m, e, (f + " DecNode").c_str());
   m->fwd_done = true;
+  m->agg_last = m->plan.lean;
   return MGN_OK;
 }
 
@@ -971,7 +976,10 @@ struct Bwd {
         e = edge_forward_block(m, *g, p, ws, m->halo, j, b.V(j), b.V16(j), b.ES(j), b.ES(j + 1), b.AGG(k - 1), st);
         CHK("edge-stream recompute");
       }
-      const bool have_agg = k + 1 < K && (k + 1) % p.s != 0;
+      // the last block's aggregate is still where the forward left it
+      // unless an earlier backward has run since
+      const bool have_agg = k + 1 < K ? (k + 1) % p.s != 0 : m->agg_last;
+      m->agg_last = false;
       if (!have_agg) {
         e = edge_forward_block(m, *g, p, ws, m->halo, k, b.V(k), b.V16(k), b.ES(k), nullptr, b.AGG(k), st);
         CHK("aggregate recompute");

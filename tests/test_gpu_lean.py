@@ -1,6 +1,8 @@
 """Edge-stream checkpointing (mgn_set_recompute): the backward pass that
 recomputes each block's edge latents from the checkpoint below it, its
-aggregate by one more edge forward, reads the node stream's bf16 copy and
+aggregate by one more edge forward (the last block's is still where the
+forward left it, unless a backward has run since), reads the node stream's
+bf16 copy and
 runs the edge backward (and the edge encoder's) in receiver chunks.  Against
 the run that keeps every block's inputs, on the same inputs: outputs bitwise
 equal (the forward is the same computation, only stored elsewhere), every
@@ -40,6 +42,34 @@ def test_checkpointed_equals_stash_all(l, D, interval, chunk):
     eh = rel_err(lean[2], base[2])
     say(f"  parameter gradients: worst {e:.2e} ({name}); halo gradient {eh:.2e}")
     assert e <= 1e-4 and eh <= 1e-4
+
+
+@pytest.mark.parametrize("K,interval", [(5, 2), (4, 4), (1, 1)])
+def test_checkpointed_backward_twice(K, interval):
+    # the first backward reads the last block's aggregate the forward left;
+    # its recompute chains overwrite that slot, so a second backward after
+    # the same forward must run that block's edge forward again: both give
+    # the same bits, and those of the plan that keeps every block
+    from paper_2307_13592_amd.runner import Session
+    l, D = 128, 2
+    say(f"[lean] backward twice l={l} D={D} K={K} interval={interval}")
+    c = local_inputs(meshes.sector(6, 16, 10, 4, seed=13), 1, l, K, D, 6)
+    base = run_gpu(c, l, K, D, "bf16")
+    s = Session(l, K, D, "bf16", c["g"], c["nf"], c["ef"], c["halo"], c["params"], recompute=interval,
+                chunk_edges=300)
+    try:
+        out = s.forward().cpu().numpy().copy()
+        runs = []
+        for _ in range(2):
+            dp, dh = s.backward(c["d_out"])
+            runs.append((dp.cpu().numpy().copy(), dh.cpu().numpy().copy()))
+    finally:
+        s.close()
+    assert np.array_equal(out, base[0]), "outputs differ"
+    for name, i in (("parameter gradients", 0), ("halo gradients", 1)):
+        assert np.array_equal(runs[0][i], runs[1][i]), f"second backward: {name} differ"
+    e, name = _segments_err(c["shapes"], runs[0][0], base[1])
+    assert e <= 1e-4 and rel_err(runs[0][1], base[2]) <= 1e-4, (e, name)
 
 
 def test_checkpointed_against_oracle():
