@@ -1725,15 +1725,15 @@ __device__ __forceinline__ uint4 rt_from_plain(const uint4 p) {
 
 // The values of rt_frags -> one plain-order bf16 row, 16 bytes per lane and
 // k-group.  All lanes take part in the swaps; only lanes with ok store.
-// A stored bf16 ReLU output row (plain order; lane (e, q) reads its row's
-// k-slots kg * 32 + 8 q ..) as T-order fragments, and the ReLU mask its
-// signs give: bit cb * 4 + r is set where the value is positive.
+// A stored bf16 ReLU output row as read (plain order: lane (e, q) holds its
+// row's k-slots kg * 32 + 8 q ..) -> T-order fragments, and the ReLU mask
+// their signs give: bit cb * 4 + r is set where the value is positive.
+// rt_load_relu reads the row as well.
 template <int NKH>
-__device__ __forceinline__ void rt_load_relu(const uint16_t* __restrict__ hp, int q, uint4 (&hf)[NKH],
-                                             uint32_t& mask) {
+__device__ __forceinline__ void rt_relu_frags(const uint4 (&raw)[NKH], uint4 (&hf)[NKH], uint32_t& mask) {
 #pragma unroll
   for (int kg = 0; kg < NKH; ++kg) {
-    hf[kg] = rt_from_plain(*reinterpret_cast<const uint4*>(hp + kg * 32 + q * 8));
+    hf[kg] = rt_from_plain(raw[kg]);
     const uint32_t w[4] = {hf[kg].x, hf[kg].y, hf[kg].z, hf[kg].w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {  // dword i: block 2 kg + i / 2, rows r = 2 (i % 2) .. + 1
@@ -1742,6 +1742,14 @@ __device__ __forceinline__ void rt_load_relu(const uint16_t* __restrict__ hp, in
       mask |= (((w[i] >> 16) & 0x7fffu) != 0u && !(w[i] & 0x80000000u) ? 1u : 0u) << (cb * 4 + r + 1);
     }
   }
+}
+template <int NKH>
+__device__ __forceinline__ void rt_load_relu(const uint16_t* __restrict__ hp, int q, uint4 (&hf)[NKH],
+                                             uint32_t& mask) {
+  uint4 raw[NKH];
+#pragma unroll
+  for (int kg = 0; kg < NKH; ++kg) raw[kg] = *reinterpret_cast<const uint4*>(hp + kg * 32 + q * 8);
+  rt_relu_frags<NKH>(raw, hf, mask);
 }
 
 template <int NKH>
@@ -1935,7 +1943,10 @@ __global__ __launch_bounds__((RsFwdLay<L, D>::NTH)) void edge_fwd_rs_kernel(Edge
   const uint16_t* Ein = reinterpret_cast<const uint16_t*>(a.Ein);
   uint16_t* Eout = reinterpret_cast<uint16_t*>(a.Eout);
   float run[(L + 63) / 64] = {};  // running receiver sums, columns lane + 64 j
-  RsMetaRaw nxt = rt_meta_load(a.erecv, a.send, E0, E1);
+  // the next tile's metadata is loaded when a tile starts and turned into
+  // its mask before the tile's first store, so that the loop's head waits on
+  // no store of the tile before
+  RsMeta mt_next = rt_meta_make(rt_meta_load(a.erecv, a.send, E0, E1));
   for (int64_t sb = E0; sb < E1; sb += 16) {
     // an opaque copy of the lane index, so that the lane-dependent addresses
     // are recomputed per tile instead of being hoisted into registers
@@ -1944,8 +1955,8 @@ __global__ __launch_bounds__((RsFwdLay<L, D>::NTH)) void edge_fwd_rs_kernel(Edge
     const int e = ln & 15, q = ln >> 4;
     const int n = (int)(E1 - sb < 16 ? E1 - sb : 16);
     const bool ok = e < n;
-    const RsMeta mt = rt_meta_make(nxt);
-    nxt = rt_meta_load(a.erecv, a.send, sb + 16, E1);
+    const RsMeta mt = mt_next;
+    const RsMetaRaw nxt = rt_meta_load(a.erecv, a.send, sb + 16, E1);
     // rows past the tile's end repeat row 0 (their results are never stored)
     const int64_t er = sb + (ok ? e : 0);
     const uint16_t* erow = Ein + er * L;
@@ -1961,6 +1972,7 @@ __global__ __launch_bounds__((RsFwdLay<L, D>::NTH)) void edge_fwd_rs_kernel(Edge
       for (int r = 0; r < 4; ++r) h[cb][r] = z[cb][r] > 0.f ? z[cb][r] : 0.f;
     uint4 hf[NKH];
     rt_frags<NB>(h, hf);
+    mt_next = rt_meta_make(nxt);
     if (a.hid_out) rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.hid_out) + (sb + e) * L, q, hf, ok);
     if constexpr (D == 3) {
       floatx4 acc[NB];
@@ -2118,7 +2130,10 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
 #pragma unroll
     for (int t = 0; t < NR; ++t) qacc[k][t] = 0.f;
   float run[(L + 63) / 64] = {};
-  RsMetaRaw nxt = rt_meta_load(a.erecv, a.send, E0, E1);
+  // the next tile's metadata is loaded when a tile starts and turned into
+  // its mask before the tile's first store, so that the loop's head waits on
+  // no store of the tile before
+  RsMeta mt_next = rt_meta_make(rt_meta_load(a.erecv, a.send, E0, E1));
   for (int64_t sb = E0; sb < E1; sb += 16) {
     // an opaque copy of the lane index, so that the lane-dependent addresses
     // are recomputed per tile instead of being hoisted into registers
@@ -2127,20 +2142,37 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
     const int e = ln & 15, q = ln >> 4;
     const int n = (int)(E1 - sb < 16 ? E1 - sb : 16);
     const bool ok = e < n;
-    const RsMeta mt = rt_meta_make(nxt);
-    nxt = rt_meta_load(a.erecv, a.send, sb + 16, E1);
+    const RsMeta mt = mt_next;
+    const RsMetaRaw nxt = rt_meta_load(a.erecv, a.send, sb + 16, E1);
     const int64_t srow = (sb - a.e_base + e) * L;  // row of the stored gradients / activations
     // rows past the tile's end repeat row 0 (dm = 0 there, so they add nothing)
     const int64_t er = sb + (ok ? e : 0);
+    // the tile's streamed rows, issued together before any is used, so that
+    // their latencies overlap: the stashed h_1 (or e^k), the receivers' dagg
+    // rows and de^{k+1} (bf16, plain order).  The last block has no de^{k+1}:
+    // its loads then re-read the first row (a cache hit) and are replaced by
+    // zeros where they are used, so no load waits on a branch.
+    uint4 xr[NKH], dnr[NKH];
+    float4 g4[NB];
+    {
+      const uint16_t* xp = (STASH ? reinterpret_cast<const uint16_t*>(a.hid_in) : Ein) + er * L;
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) xr[kg] = *reinterpret_cast<const uint4*>(xp + kg * 32 + q * 8);
+      const float* gp = a.dagg + (int64_t)(ok ? mt.r : 0) * L;
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) g4[cb] = rt_ld4(gp, cb, q);
+      const uint16_t* dp = a.de_next ? reinterpret_cast<const uint16_t*>(a.de_next) + er * L : xp;
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) dnr[kg] = *reinterpret_cast<const uint4*>(dp + kg * 32 + q * 8);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     uint32_t mask[2] = {0u, 0u};  // ReLU derivative of the hidden layers, bit cb * 4 + r
     float h[NB][4];
     uint4 hf[NKH];
     if constexpr (STASH) {
-      rt_load_relu<NKH>(reinterpret_cast<const uint16_t*>(a.hid_in) + er * L, q, hf, mask[0]);
+      rt_relu_frags<NKH>(xr, hf, mask[0]);
     } else {
-      uint4 ef[NKH];
-#pragma unroll
-      for (int kg = 0; kg < NKH; ++kg) ef[kg] = *reinterpret_cast<const uint4*>(Ein + er * L + kg * 32 + q * 8);
+      const uint4(&ef)[NKH] = xr;
       floatx4 z[NB];
       rt_first_layer<L>(ef, W1f, mt, ok, a.proj, z, ln);
 #pragma unroll
@@ -2189,24 +2221,14 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
     float dm[NB][4];
     float4 d4[NB];  // de^{k+1}, kept for de^k
     {
-      const float* gp = a.dagg + (int64_t)(ok ? mt.r : 0) * L;
-      float4 g4[NB];
+      const bool has_de = a.de_next != nullptr;
 #pragma unroll
-      for (int cb = 0; cb < NB; ++cb) {
-        g4[cb] = rt_ld4(gp, cb, q);
-        d4[cb] = make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-      if (a.de_next) {
-        // bf16 row, plain order: one 16-byte chunk per k-group -> T order
-        const uint16_t* dp = reinterpret_cast<const uint16_t*>(a.de_next) + er * L;
-#pragma unroll
-        for (int kg = 0; kg < NKH; ++kg) {
-          const uint4 t = rt_from_plain(*reinterpret_cast<const uint4*>(dp + kg * 32 + q * 8));
-          d4[2 * kg] = make_float4(__uint_as_float(t.x << 16), __uint_as_float(t.x & 0xffff0000u),
-                                   __uint_as_float(t.y << 16), __uint_as_float(t.y & 0xffff0000u));
-          d4[2 * kg + 1] = make_float4(__uint_as_float(t.z << 16), __uint_as_float(t.z & 0xffff0000u),
-                                       __uint_as_float(t.w << 16), __uint_as_float(t.w & 0xffff0000u));
-        }
+      for (int kg = 0; kg < NKH; ++kg) {  // plain order -> T order
+        const uint4 t = rt_from_plain(has_de ? dnr[kg] : make_uint4(0u, 0u, 0u, 0u));
+        d4[2 * kg] = make_float4(__uint_as_float(t.x << 16), __uint_as_float(t.x & 0xffff0000u),
+                                 __uint_as_float(t.y << 16), __uint_as_float(t.y & 0xffff0000u));
+        d4[2 * kg + 1] = make_float4(__uint_as_float(t.z << 16), __uint_as_float(t.z & 0xffff0000u),
+                                     __uint_as_float(t.w << 16), __uint_as_float(t.w & 0xffff0000u));
       }
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
@@ -2278,6 +2300,7 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
     }
     uint4 gf[NKH];
     rt_frags<NB>(v, gf);
+    mt_next = rt_meta_make(nxt);
     rt_store_frags<NKH>(reinterpret_cast<uint16_t*>(a.delta[D - 1]) + srow, q, gf, ok);
     // hidden layers: dz_{j-1} = (dz_j W_j) * [z_{j-1} > 0]
 #pragma unroll
