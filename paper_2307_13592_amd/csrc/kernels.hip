@@ -1743,6 +1743,16 @@ __device__ __forceinline__ void rt_relu_frags(const uint4 (&raw)[NKH], uint4 (&h
     }
   }
 }
+// Whether the value of T-order fragments hf at accumulator position
+// (cb, r) is positive: bf16 bits with the sign clear and a nonzero
+// magnitude, the test rt_relu_frags makes for its mask bit cb * 4 + r.
+template <int NKH>
+__device__ __forceinline__ bool rt_relu_on(const uint4 (&hf)[NKH], int cb, int r) {
+  const uint4 f = hf[cb / 2];
+  const int i = 2 * (cb % 2) + r / 2;
+  const uint32_t w = i == 0 ? f.x : i == 1 ? f.y : i == 2 ? f.z : f.w;
+  return (int32_t)(r % 2 ? (w & 0xffff0000u) : (w << 16)) > 0;
+}
 template <int NKH>
 __device__ __forceinline__ void rt_load_relu(const uint16_t* __restrict__ hp, int q, uint4 (&hf)[NKH],
                                              uint32_t& mask) {
@@ -1785,14 +1795,22 @@ __device__ __forceinline__ float rt_lane_sum(const float (&v)[NB][4]) {
 }
 
 // One reduce-scatter step within a 16-lane group: v[0, N) -> v[0, N / 2);
-// the lane keeps the half that `hi` selects and adds the DPP partner's copy
-// of it (the partner keeps the other half).
+// the lane keeps the half that `hi` selects, summed with the DPP partner's
+// copy of it (the partner keeps the other half).  Both halves' sums are
+// formed, each one add with the partner's value read through DPP (every
+// lane of these patterns has a partner in its row), and one is selected:
+// three instructions per pair instead of two selects, a move and an add.
 template <int N, int CTRL>
 __device__ __forceinline__ void rt_halve(float* v, bool hi) {
+  // no contraction with a product that formed v: both partners must add the
+  // same two rounded values
+#pragma clang fp contract(off)
 #pragma unroll
   for (int k = 0; k < N / 2; ++k) {
-    const float keep = hi ? v[k + N / 2] : v[k], send = hi ? v[k] : v[k + N / 2];
-    v[k] = keep + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(send), CTRL, 0xf, 0xf, false));
+    const float lo = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v[k]), CTRL, 0xf, 0xf, true)) + v[k];
+    const float up =
+        __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v[k + N / 2]), CTRL, 0xf, 0xf, true)) + v[k + N / 2];
+    v[k] = hi ? up : lo;
   }
 }
 
@@ -2169,8 +2187,15 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
     uint32_t mask[2] = {0u, 0u};  // ReLU derivative of the hidden layers, bit cb * 4 + r
     float h[NB][4];
     uint4 hf[NKH];
+    // STASH: h_1's fragments; the ReLU derivative of the first layer is read
+    // off their signs where it is applied (rt_relu_on), so no mask is built
+    uint4 h1f[NKH];
     if constexpr (STASH) {
-      rt_relu_frags<NKH>(xr, hf, mask[0]);
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) {
+        h1f[kg] = rt_from_plain(xr[kg]);
+        hf[kg] = h1f[kg];
+      }
     } else {
       const uint4(&ef)[NKH] = xr;
       floatx4 z[NB];
@@ -2316,7 +2341,8 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
       for (int cb = 0; cb < NB; ++cb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          v[cb][r] = ((mask[j - 1] >> (cb * 4 + r)) & 1u) ? acc[cb][r] : 0.f;
+          const bool on = (STASH && j == 1) ? rt_relu_on<NKH>(h1f, cb, r) : ((mask[j - 1] >> (cb * 4 + r)) & 1u);
+          v[cb][r] = on ? acc[cb][r] : 0.f;
           th[cb * 4 + r] = v[cb][r];
         }
       rt_col_totals<NV>(th, e);
