@@ -5154,6 +5154,20 @@ __global__ __launch_bounds__(NT) void input_grad_kernel(InGradArgs a) {
       put_operand<P>(Sh + row * LDT + c + 3, Sl + row * LDT + c + 3, v.w);
     }
   }
+  // receiver sums (owned rows; zero for halo rows and past the end): this
+  // thread's rows are loaded before the sender gather, so that their latency
+  // overlaps it, and go to LDS after it
+  constexpr int RPT = TM * (L / 4) / NT;  // 16-byte receiver chunks per thread
+  static_assert(TM * (L / 4) % NT == 0, "receiver chunks");
+  float4 rv[RPT];
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int it = tid + k * NT, row = it / (L / 4), c = (it % (L / 4)) * 4;
+    const int64_t node = n0 + row;
+    // rows past the owned ones read row 0 (then replaced by zeros)
+    rv[k] = a.n_owned > 0 ? *reinterpret_cast<const float4*>(a.dzr + (node < a.n_owned ? node : 0) * L + c)
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   for (int it = tid; !a.dzs_ready && it < TM * CPR; it += NT) {
     const int row = it / CPR, c = (it % CPR) * E16;
     const int64_t node = n0 + row;
@@ -5161,15 +5175,19 @@ __global__ __launch_bounds__(NT) void input_grad_kernel(InGradArgs a) {
 #pragma unroll
     for (int j = 0; j < E16; ++j) s[j] = 0.f;
     if (node < a.n_local) {
-      // up to IG_FLIGHT rows in flight per thread, summed in ascending edge order
+      // up to IG_FLIGHT rows in flight per thread, summed in ascending edge
+      // order: the group's edge ids are loaded first, then its rows, each
+      // all at once (positions past the end repeat the last edge, a cache
+      // hit, and are not summed)
       constexpr int IG_FLIGHT = 16;
       const int32_t end = a.trow[node + 1];
       for (int32_t i = a.trow[node]; i < end; i += IG_FLIGHT) {
+        int32_t id[IG_FLIGHT];
+#pragma unroll
+        for (int u = 0; u < IG_FLIGHT; ++u) id[u] = a.tedge[i + u < end ? i + u : end - 1];
         uint4 v[IG_FLIGHT];
 #pragma unroll
-        for (int u = 0; u < IG_FLIGHT; ++u)
-          v[u] = i + u < end ? *reinterpret_cast<const uint4*>(dz + (int64_t)a.tedge[i + u] * L + c)
-                             : make_uint4(0, 0, 0, 0);
+        for (int u = 0; u < IG_FLIGHT; ++u) v[u] = *reinterpret_cast<const uint4*>(dz + (int64_t)id[u] * L + c);
 #pragma unroll
         for (int u = 0; u < IG_FLIGHT; ++u) {
           if (i + u < end) {
@@ -5188,12 +5206,10 @@ __global__ __launch_bounds__(NT) void input_grad_kernel(InGradArgs a) {
         *reinterpret_cast<float4*>(a.dzs + node * L + c + j) = make_float4(s[j], s[j + 1], s[j + 2], s[j + 3]);
     }
   }
-  // receiver sums (owned rows; zero for halo rows and past the end)
-  for (int it = tid; it < TM * (L / 4); it += NT) {
-    const int row = it / (L / 4), c = (it % (L / 4)) * 4;
-    const int64_t node = n0 + row;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (node < a.n_owned) v = *reinterpret_cast<const float4*>(a.dzr + node * L + c);
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int it = tid + k * NT, row = it / (L / 4), c = (it % (L / 4)) * 4;
+    const float4 v = n0 + row < a.n_owned ? rv[k] : make_float4(0.f, 0.f, 0.f, 0.f);
     put_operand<P>(Rh + row * LDT + c, Rl + row * LDT + c, v.x);
     put_operand<P>(Rh + row * LDT + c + 1, Rl + row * LDT + c + 1, v.y);
     put_operand<P>(Rh + row * LDT + c + 2, Rl + row * LDT + c + 2, v.z);
@@ -5206,6 +5222,18 @@ __global__ __launch_bounds__(NT) void input_grad_kernel(InGradArgs a) {
   if constexpr (SPLIT) wave_gemm_k<P, MB, NBW, NKH, false>(Rl, LDT, a.w1.wb, 2 * (L / 16) + nb, acc);
   wave_gemm_k<P, MB, NBW, NKH, false>(Sh, LDT, a.w1.wb, (L / 16) + nb, acc);
   if constexpr (SPLIT) wave_gemm_k<P, MB, NBW, NKH, false>(Sl, LDT, a.w1.wb, (L / 16) + nb, acc);
+  // the dv values this lane adds to, all loaded before any is written (rows
+  // past the owned ones read row 0 and are not written)
+  float old[MB][4][NBW];
+#pragma unroll
+  for (int m = 0; m < MB; ++m)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t node = n0 + m * 16 + acc_row(r);
+#pragma unroll
+      for (int nn = 0; nn < NBW; ++nn)
+        old[m][r][nn] = a.n_owned > 0 ? a.dv[(node < a.n_owned ? node : 0) * L + (nb + nn) * 16 + acc_col()] : 0.f;
+    }
 #pragma unroll
   for (int m = 0; m < MB; ++m)
 #pragma unroll
@@ -5215,8 +5243,7 @@ __global__ __launch_bounds__(NT) void input_grad_kernel(InGradArgs a) {
       for (int nn = 0; nn < NBW; ++nn) {
         const int col = (nb + nn) * 16 + acc_col();
         if (node < a.n_owned) {
-          float* d = a.dv + node * L + col;
-          *d = *d + acc[m][nn][r];
+          a.dv[node * L + col] = old[m][r][nn] + acc[m][nn][r];
         } else if (node < a.n_local && a.dh) {
           a.dh[(node - a.n_owned) * L + col] = acc[m][nn][r];
         }
