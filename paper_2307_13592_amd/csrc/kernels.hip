@@ -2989,6 +2989,20 @@ void edge_bwd_rw_kernel(EdgeBwdArgs a) {
     rw_store<NTH>(stg[(p + 1) & 1], buf + ((p + 1) & 1) * RW_CHUNK);
     load(stg[(p + 1) & 1], p + 3);
   };
+  // the next tile's metadata is loaded when a tile starts and made into its
+  // mask before the tile's last stores, so that no tile's start waits on
+  // the stores of the tile before (the memory counter is in order)
+  RsMeta mt_next = rt_meta_make(rt_meta_load(a.erecv, a.send, E0, E1));
+  // rows of the tile's own input, read in place of de^{k+1} by the last
+  // block (which has none; the values are then replaced by zeros)
+  const uint16_t* xin = STASH ? reinterpret_cast<const uint16_t*>(a.hid_in) : Ein;
+  const bool has_de = a.de_next != nullptr;
+  // all ones with de^{k+1}, zero without: the loaded bits are masked rather
+  // than selected, so that the loads are not moved into a branch
+  const uint32_t de_mask = has_de ? 0xffffffffu : 0u;
+  auto de_bits = [&](const uint4 r) {
+    return make_uint4(r.x & de_mask, r.y & de_mask, r.z & de_mask, r.w & de_mask);
+  };
   for (int t = 0; t < ntile; ++t) {
     int ln = lane;
     asm volatile("" : "+v"(ln));
@@ -2997,7 +3011,9 @@ void edge_bwd_rw_kernel(EdgeBwdArgs a) {
     const bool active = sb < E1;  // wave-uniform
     const int n = active ? (int)(E1 - sb < 16 ? E1 - sb : 16) : 0;
     const bool ok = e < n;
-    const RsMeta mt = rt_meta_make(rt_meta_load(a.erecv, a.send, active ? sb : E0, active ? E1 : E0));
+    const RsMeta mt = mt_next;
+    const bool active_next = sb + 16 < E1;
+    const RsMetaRaw nxt = rt_meta_load(a.erecv, a.send, active_next ? sb + 16 : E0, active_next ? E1 : E0);
     const int64_t srow = (sb - a.e_base + e) * L;  // row of the stored gradients / activations
     // rows past the tile's end repeat the tile's first row (dm = 0 there)
     const int64_t er = active ? sb + (ok ? e : 0) : E0;
@@ -3084,13 +3100,14 @@ void edge_bwd_rw_kernel(EdgeBwdArgs a) {
     float dm[NB][4];
     {
       const float* gp = a.dagg + (int64_t)(ok ? mt.r : 0) * L;
-      const uint16_t* dp = reinterpret_cast<const uint16_t*>(a.de_next) + er * L;
+      const uint16_t* dp = (has_de ? reinterpret_cast<const uint16_t*>(a.de_next) : xin) + er * L;
 #pragma unroll
       for (int kg = 0; kg < NKH; ++kg) {
         float lo[4] = {0.f, 0.f, 0.f, 0.f}, hi[4] = {0.f, 0.f, 0.f, 0.f};
         float4 g0 = make_float4(0.f, 0.f, 0.f, 0.f), g1 = g0;
         if (active) {
-          if (a.de_next) rw_unpack(*reinterpret_cast<const uint4*>(dp + kg * 32 + q * 8), lo, hi);
+          const uint4 raw = *reinterpret_cast<const uint4*>(dp + kg * 32 + q * 8);
+          rw_unpack(de_bits(raw), lo, hi);
           g0 = rt_ld4(gp, 2 * kg, q);
           g1 = rt_ld4(gp, 2 * kg + 1, q);
         }
@@ -3233,13 +3250,17 @@ void edge_bwd_rw_kernel(EdgeBwdArgs a) {
       }
     }
     if (!active) continue;
+    mt_next = rt_meta_make(nxt);
     {
-      const uint16_t* dp = reinterpret_cast<const uint16_t*>(a.de_next) + er * L;
+      const uint16_t* dp = (has_de ? reinterpret_cast<const uint16_t*>(a.de_next) : xin) + er * L;
+      uint4 raw[NKH];
+#pragma unroll
+      for (int kg = 0; kg < NKH; ++kg) raw[kg] = *reinterpret_cast<const uint4*>(dp + kg * 32 + q * 8);
       uint4 o[NKH];
 #pragma unroll
       for (int kg = 0; kg < NKH; ++kg) {
         float lo[4] = {0.f, 0.f, 0.f, 0.f}, hi[4] = {0.f, 0.f, 0.f, 0.f};
-        if (a.de_next) rw_unpack(*reinterpret_cast<const uint4*>(dp + kg * 32 + q * 8), lo, hi);
+        rw_unpack(de_bits(raw[kg]), lo, hi);
         const floatx4 a0 = acc[0][2 * kg], a1 = acc[0][2 * kg + 1];
         o[kg] = rt_to_plain(make_uint4(bf_pack(a0[0] + lo[0], a0[1] + lo[1]), bf_pack(a0[2] + lo[2], a0[3] + lo[3]),
                                        bf_pack(a1[0] + hi[0], a1[1] + hi[1]), bf_pack(a1[2] + hi[2], a1[3] + hi[3])));
@@ -5283,12 +5304,16 @@ __global__ __launch_bounds__(NT) void sender_sums_kernel(const int32_t* __restri
     float s[E16];
 #pragma unroll
     for (int j = 0; j < E16; ++j) s[j] = 0.f;
-    // up to 16 rows in flight, summed in ascending edge order
+    // up to 16 rows in flight, summed in ascending edge order; the group's
+    // edge ids load at once (positions past the node's end re-read its last
+    // id and are then marked past every chunk)
     const int32_t nend = trow[node + 1];
     for (int32_t i = lo; i < nend; i += 16) {
       int32_t ed[16];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) ed[u] = i + u < nend ? tedge[i + u] : INT32_MAX;
+      for (int u = 0; u < 16; ++u) ed[u] = tedge[i + u < nend ? i + u : nend - 1];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) ed[u] = i + u < nend ? ed[u] : INT32_MAX;
       uint4 v[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u)
