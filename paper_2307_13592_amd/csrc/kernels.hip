@@ -1849,6 +1849,8 @@ __device__ __forceinline__ void rt_first_layer(const uint4 (&ef)[L / 32], const 
     ps[cb] = rt_ld4(sp, cb, q);
     pr[cb] = rt_ld4(rp, cb, q);
   }
+  // the gathers issue before the products, which then hide their latency
+  __builtin_amdgcn_sched_barrier(0);
   rt_gemm<NB, L / 32>(W1e, ef, z, lane);
 #pragma unroll
   for (int cb = 0; cb < NB; ++cb) {
@@ -1923,8 +1925,9 @@ struct RsFwdLay {
   static constexpr int OFF_W1 = 0, OFF_WH = W, OFF_WL = (D - 1) * W, OFF_VEC = D * W;
   static constexpr int NVEC = (D == 3 ? 4 : 3) * L;
   static constexpr int OFF_SCR = OFF_VEC + NVEC * 4;
-  // 16 waves per workgroup (at most 128 registers each)
-  static constexpr int NWV = 16;
+  // 12 waves per workgroup (at most 168 registers each: a tile's gathers are
+  // all in flight before its first product)
+  static constexpr int NWV = 12;
   static constexpr int NTH = 64 * NWV;
   static constexpr int END = OFF_SCR + NWV * SCR;
   static_assert(END <= 160 * 1024, "LDS");
