@@ -2171,8 +2171,9 @@ __global__ __launch_bounds__(RS_NTH) void edge_bwd_rs_kernel(EdgeBwdArgs a) {
     // the tile's streamed rows, issued together before any is used, so that
     // their latencies overlap: the stashed h_1 (or e^k), the receivers' dagg
     // rows and de^{k+1} (bf16, plain order).  The last block has no de^{k+1}:
-    // its loads then re-read the first row (a cache hit) and are replaced by
-    // zeros where they are used, so no load waits on a branch.
+    // its loads then re-read the tile's own h_1 (or e^k) rows (cache hits)
+    // and are replaced by zeros where they are used, so no load waits on a
+    // branch.
     uint4 xr[NKH], dnr[NKH];
     float4 g4[NB];
     {
