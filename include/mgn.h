@@ -260,7 +260,12 @@ mgn_status mgn_forward_noalloc(mgn_model* m, const mgn_graph* g, const float* no
  * accumulate != 0: gradient accumulation of Algorithm 1).  d_halo
  * [K][n_halo][latent] (NULL allowed; 16-byte aligned) receives dL/dhalo,
  * overwritten: the gradients the halo owners would receive (section
- * "Methodology": backward gradient exchange). */
+ * "Methodology": backward gradient exchange).
+ * Several backward calls may follow one forward.  With edge-stream
+ * checkpointing (mgn_set_recompute) the first of them reads the last
+ * block's aggregate where the forward left it and later ones recompute it;
+ * a backward captured into a HIP graph records the choice made at capture,
+ * so each replay of such a graph must follow a replay of the forward. */
 mgn_status mgn_backward(mgn_model* m, const float* d_out, float* d_params, int accumulate, float* d_halo,
                         mgn_stream stream);
 
